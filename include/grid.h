@@ -1,0 +1,229 @@
+/*
+ * grid.h -- C ABI of the MI355X grammar-mask library (libgrid.so).
+ *
+ * The library computes the exact next-token mask of grammar-constrained
+ * decoding (Definition 4, section 4.1): for a batch of parser configurations
+ * (Definition 1, section 3.2: an LALR(1) stack plus the scan state of the
+ * pending lexeme) it walks every vocabulary token's bytes through the lexer
+ * DFA, checks each completed terminal against the incrementally advanced
+ * LALR(1) parser (Proposition 3), and writes a [B, ceil(V/32)] u32 bitmask;
+ * a second call fills disallowed logits with -inf (section 2, masked decoding).
+ *
+ * Conventions for every call:
+ *  - return value: GRID_OK (0) or a negative GRID_E_* code; a message for the
+ *    last failure on the calling thread is available from grid_last_error();
+ *    no C++ exception crosses this boundary;
+ *  - "host" pointers are CPU memory owned by the caller and only read during
+ *    the call; "device" pointers are GPU memory owned by the caller (the
+ *    library never allocates device memory);
+ *  - asynchronous calls enqueue work on the given HIP stream (a hipStream_t
+ *    passed as void*, NULL = the default stream) and return before it runs;
+ *    argument errors are reported immediately and nothing is enqueued.
+ *
+ * Mask layout (used by grid_mask and grid_apply): token t of row b is bit
+ * (t & 31) of word mask[b * W + (t >> 5)], W = ceil(V / 32); bits for t >= V
+ * are 0; special tokens are 0 except the end-of-sequence id, whose bit is
+ * eos_ok.
+ */
+#ifndef GRID_H
+#define GRID_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------ status codes */
+#define GRID_OK 0
+#define GRID_E_ARG (-1)             /* bad argument (null pointer, size, range) */
+#define GRID_E_GRAMMAR_SYNTAX (-2)  /* grammar text or regex does not parse */
+#define GRID_E_LALR_CONFLICT (-3)   /* projected grammar is not LALR(1) */
+#define GRID_E_EMPTY_LANGUAGE (-4)  /* projection left L(G) empty (section 2, L2) */
+#define GRID_E_LEXICON (-5)         /* a word is not in its category's regex (W_c in R_c) */
+#define GRID_E_LEXER_GAP (-6)       /* a live non-accepting DFA state follows an accepting one */
+#define GRID_E_VOCAB (-7)           /* malformed vocabulary */
+#define GRID_E_NOT_VIABLE (-8)      /* prefix is not in Prefix(L) */
+#define GRID_E_UNBOUND (-9)         /* a device artifact was not bound */
+#define GRID_E_HIP (-10)            /* a HIP launch or runtime call failed */
+#define GRID_E_CAPACITY (-11)       /* a fixed capacity is exceeded (see grid_info) */
+
+/* Row status written by grid_mask (status_dev[b]). */
+#define GRID_ROW_OK 0
+#define GRID_ROW_EMPTY 1            /* no token and no EOS allowed: Proposition 8 says a
+                                       viable configuration never has an empty mask */
+#define GRID_ROW_BAD_CONFIG 2       /* state, slot or stack out of range */
+#define GRID_ROW_OVERFLOW 4         /* a per-lane parser overlay capacity was exceeded;
+                                       the row's mask is not exact */
+
+typedef struct grid_compiled grid_compiled;
+
+/* ------------------------------------------------------------------ compile */
+typedef struct {
+  const char* grammar;            /* host: grammar text (format in the design notes) */
+  size_t grammar_len;
+  const char* drop_labels;        /* host: comma-separated production labels the role
+                                     projection removes (section 2, L2); NULL = none */
+  const uint8_t* vocab_bytes;     /* host: concatenated token spellings */
+  const uint64_t* vocab_offsets;  /* host: [vocab_size + 1]; token t = bytes[off[t], off[t+1]) */
+  int32_t vocab_size;             /* V >= 1 */
+  const int32_t* special_ids;     /* host: ids that are never allowed (except eos_id) */
+  int32_t n_special;
+  int32_t eos_id;                 /* -1: none; else its bit mirrors eos_ok */
+} grid_compile_args;
+
+/* Builds the host artifacts (section 6.1, offline layer): parses the grammar,
+ * applies the role projection then removes useless symbols and checks that
+ * the language is not empty; builds the LALR(1) ACTION/GOTO tables (reports
+ * the first conflict); builds a dense 256-wide union lexer DFA over every
+ * declared terminal (minimized, with byte classes, accept lists in priority
+ * order and live-terminal sets) and checks it is gap-free; builds the
+ * vocabulary artifacts: spellings sorted in byte order (trie DFS order), a
+ * levelized CSR byte trie, and the alias table mapping each spelling to every
+ * id that shares it (Definition 3).  Empty spellings count as special.
+ * Copies all inputs.  *out receives a handle owned by the caller
+ * (grid_free).  A vocabulary that does not contain every single byte is not
+ * an error; grid_info reports it (completeness precondition (a),
+ * Proposition 8). */
+int grid_compile(const grid_compile_args* args, grid_compiled** out);
+void grid_free(grid_compiled* g);
+/* Message of the last failing call on this thread ("" if none). */
+const char* grid_last_error(void);
+
+typedef struct {
+  int32_t n_terminals;      /* T (declared terminals, never renumbered by projection) */
+  int32_t n_nonterminals;   /* after projection and reduction */
+  int32_t n_productions;
+  int32_t n_lr_states;
+  int32_t n_dfa_states;     /* including the dead state 0; state 1 is the start */
+  int32_t n_byte_classes;
+  int32_t vocab_size;       /* V */
+  int32_t mask_words;       /* W = ceil(V / 32) */
+  int32_t n_spellings;      /* distinct non-special spellings */
+  int32_t max_spelling_len;
+  int32_t n_trie_nodes;     /* levelized trie nodes (without the root) */
+  int32_t n_lexicon_slots;
+  int32_t byte_complete;    /* 1 if every byte 0..255 is a token spelling */
+  int32_t overlay_capacity; /* per-lane parser overlay entries in grid_mask */
+} grid_info_t;
+int grid_info(const grid_compiled* g, grid_info_t* out);
+
+/* Adds a schema lexicon (section 2, L3): n_categories category terminals,
+ * names[i] a terminal declared with the "category" option and words[i] its
+ * allow-list W_c as '\n'-separated words.  Categories not named are
+ * unrestricted for rows using this slot.  Every word must be accepted by its
+ * category's regex (W_c subset of R_c, checked, Proposition 8 (d)).
+ * *slot receives the new slot index (slot 0 is created by grid_compile and is
+ * the empty lexicon).  Adding a slot changes the lexicon artifacts: query and
+ * re-bind them afterwards. */
+typedef struct {
+  int32_t n_categories;
+  const char* const* names;
+  const char* const* words;
+} grid_lexicon_args;
+int grid_add_lexicon(grid_compiled* g, const grid_lexicon_args* lex, int32_t* slot);
+
+/* ---------------------------------------------------------------- artifacts */
+/* Device artifacts.  The caller allocates device memory of the reported size,
+ * copies the host bytes there and binds the device pointer; grid_mask reads
+ * only bound artifacts (GRID_E_UNBOUND otherwise). */
+enum {
+  GRID_ART_DFA_DENSE = 0,   /* u16 [S][256] next state, 0 = dead */
+  GRID_ART_DFA_CLASS,       /* u16 [S][C] next state by byte class */
+  GRID_ART_BYTE_CLASS,      /* u8  [256] byte -> class */
+  GRID_ART_DFA_ACCEPT_OFF,  /* u32 [S+1] offsets into ACCEPT_LIST */
+  GRID_ART_DFA_ACCEPT_LIST, /* u8  accepted terminals per state, priority order */
+  GRID_ART_DFA_LIVE,        /* u32 [S][8] terminals with an accept reachable */
+  GRID_ART_ACTION,          /* u16 [n_lr][T+1]: 0 error, 0x4000|s shift, 0x8000|p reduce,
+                               0xC000 accept; column T is end of input */
+  GRID_ART_GOTO,            /* u16 [n_lr][N] */
+  GRID_ART_PROD,            /* u32 [P]: lhs | len << 16 */
+  GRID_ART_TERM_INFO,       /* u32 [T]: bit0 ignored, bits 8..15 category index or 0xFF */
+  GRID_ART_SPELL_OFF,       /* u32 [U+1] offsets of the sorted distinct spellings */
+  GRID_ART_SPELL_BYTES,     /* u8  spelling bytes (+32 bytes of zero padding) */
+  GRID_ART_ALIAS_OFF,       /* u32 [U+1] */
+  GRID_ART_ALIAS_IDS,       /* i32 token ids per spelling */
+  GRID_ART_TRIE_LEVEL_OFF,  /* u32 [Lmax+2] first node of each level (level 1 first) */
+  GRID_ART_TRIE_NODES,      /* u32 [n][2]: byte | parent << 8 (parent: node index + 1, 0 =
+                               root), spelling index + 1 (0 = none) */
+  GRID_ART_LEX_FLAGS,       /* u16 per lexicon-trie node: bit c prefix-of-category-c,
+                               bit 8+c word-of-category-c */
+  GRID_ART_LEX_HASH,        /* u32 [2] per entry: key = node * 256 + byte + 1 (0 empty), child */
+  GRID_ART_LEX_SLOTS,       /* u32 [4] per slot: flags base, hash base, hash mask,
+                               restricted-category mask */
+  GRID_ART_COUNT
+};
+int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);
+int grid_bind_device(grid_compiled* g, int32_t which, void* device_ptr);
+
+/* ----------------------------------------------------------- configurations */
+/* Device form of a configuration (Definition 1), 32 bytes.  The LALR stack
+ * states of the row are stack_pool[stk_off .. stk_off + stk_depth), bottom
+ * first (bottom = the initial state 0); the stack is the one right after the
+ * last shift.  q is the lexer DFA state after the pending lexeme r and lexnode
+ * the lexicon-trie node of r in slot `slot` (0xFFFFFFFF when r is not a
+ * prefix of any lexicon word).  flags bit 0: r is empty. */
+typedef struct {
+  uint32_t stk_off;
+  uint32_t stk_depth;
+  uint32_t lexnode;
+  uint16_t q;
+  uint16_t slot;
+  uint32_t flags;
+  uint32_t rem_len;
+  uint32_t reserved[2];
+} grid_config;
+
+/* Host advance (section 6.1, per-token step 7): lexes and parses the prefix
+ * w[0..n) with the same rules as the mask and fills *cfg (stk_off = 0) and
+ * stack_out[0 .. *depth).  GRID_E_NOT_VIABLE if w is not a viable prefix;
+ * GRID_E_CAPACITY if the stack needs more than stack_cap entries. */
+int grid_config_from_prefix(const grid_compiled* g, int32_t slot, const uint8_t* w, size_t n,
+                            grid_config* cfg, uint16_t* stack_out, uint32_t stack_cap,
+                            uint32_t* depth);
+
+/* --------------------------------------------------------------------- mask */
+/* Device workspace bytes grid_mask needs for B rows. */
+size_t grid_mask_workspace_bytes(const grid_compiled* g, int32_t B);
+
+/* The cold exact mask of B rows (Definition 4; per-token hot path steps 1, 2,
+ * 4 on a miss, and 5, section 6.1).  cfg_dev: device grid_config[B];
+ * stack_pool_dev: device u16 states the configs point into; mask_dev: device
+ * u32 [B][W] (fully overwritten); eos_dev: device u8 [B] (nullable);
+ * status_dev: device i32 [B] GRID_ROW_* bits (nullable); workspace_dev:
+ * device scratch of at least grid_mask_workspace_bytes(g, B).  All device
+ * buffers are caller-owned; asynchronous on stream. */
+int grid_mask(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+              const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
+              int32_t* status_dev, void* workspace_dev, size_t workspace_bytes, void* stream);
+
+/* The same work split into its launches, for callers that time or overlap
+ * them: phases is a bit set of GRID_PHASE_* run in order on the stream.  A
+ * walk needs the prologue of the same rows and workspace to have run before
+ * it (earlier on the stream); finalize needs the walk.  grid_mask equals
+ * grid_mask_phases with GRID_PHASE_ALL. */
+#define GRID_PHASE_PROLOGUE 1u      /* allowed sets, EOS gate, row clear */
+#define GRID_PHASE_WALK 2u          /* full-vocabulary walk and bit packing */
+#define GRID_PHASE_FINALIZE 4u      /* row status (needs status_dev) */
+#define GRID_PHASE_ALL 7u
+int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                     const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
+                     int32_t* status_dev, void* workspace_dev, size_t workspace_bytes,
+                     uint32_t phases, void* stream);
+
+/* -------------------------------------------------------------------- apply */
+#define GRID_DTYPE_F32 0
+#define GRID_DTYPE_BF16 1
+/* In place: logits[b * row_stride + t] = -inf for every t < V whose mask bit
+ * is 0 (fp32 0xFF800000, bf16 0xFF80); other entries are not written
+ * (section 2: hard -inf masking, a soundness precondition of Proposition 7).
+ * mask_dev: device u32 [B][ceil(V/32)]; logits_dev: device fp32 or bf16 with
+ * row_stride >= V elements.  Asynchronous on stream. */
+int grid_apply(const uint32_t* mask_dev, void* logits_dev, int32_t dtype, int32_t B, int32_t V,
+               int64_t row_stride, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

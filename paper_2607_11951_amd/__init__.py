@@ -1,0 +1,8 @@
+"""MI355X-native exact grammar-constrained next-token masks (GRID's cold path).
+
+The compute path lives in libgrid.so (HIP kernels for gfx950 plus the host
+compiler behind a C ABI, include/grid.h); this package is the Python binding.
+"""
+
+from .grid import (Grid, GridError, apply, from_workload, lib, CONFIG_DTYPE, ROW_OK,  # noqa: F401
+                   ROW_EMPTY, ROW_BAD_CONFIG, ROW_OVERFLOW, EXPORTS)

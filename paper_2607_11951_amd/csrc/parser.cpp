@@ -1,0 +1,313 @@
+// parser.cpp -- role projection, useless-symbol removal and LALR(1) tables.
+//
+// Section 2 (L2): a role keeps a subset of the productions; useless symbols
+// are then removed (reducedness is what makes "the parser accepts the next
+// terminal" equal "the prefix stays viable", Proposition 3) and the language
+// must stay nonempty.  The LALR(1) automaton is built from the LR(0) item sets
+// with lookaheads found by spontaneous generation and propagation (the
+// classic kernel-item method); any shift/reduce or reduce/reduce conflict is
+// an error.  Tables keep full reduce rows (no default reductions); the mask
+// path computes allowed terminals by simulating reduce chains anyway
+// (section 3.2), so it is exact with or without table compression.
+#include <algorithm>
+#include <map>
+#include <set>
+
+#include "host.h"
+
+namespace grid {
+namespace {
+
+struct Bits {  // terminal set over T+2 symbols (T = end of input, T+1 = probe)
+  uint64_t w[5] = {0, 0, 0, 0, 0};
+  void set(int i) { w[i >> 6] |= 1ull << (i & 63); }
+  bool test(int i) const { return (w[i >> 6] >> (i & 63)) & 1; }
+  bool merge(const Bits& o) {
+    bool ch = false;
+    for (int k = 0; k < 5; ++k) {
+      uint64_t n = w[k] | o.w[k];
+      ch |= n != w[k];
+      w[k] = n;
+    }
+    return ch;
+  }
+};
+
+struct G2 {  // reduced grammar with augmented production 0: S' -> S
+  int T = 0, N = 0;  // N includes S' as the last nonterminal
+  std::vector<int> lhs;
+  std::vector<std::vector<int>> rhs;  // symbols: t < T terminal, T + n nonterminal
+  std::vector<std::vector<int>> prods_of;
+  std::vector<char> nullable;
+  std::vector<Bits> first;
+  bool is_nt(int x) const { return x >= T; }
+};
+
+using Item = uint32_t;  // prod << 8 | dot
+inline Item mk(int p, int d) { return (Item)p << 8 | (Item)d; }
+inline int ip(Item x) { return (int)(x >> 8); }
+inline int id(Item x) { return (int)(x & 255); }
+
+}  // namespace
+
+Parser build_parser(const GrammarText& g, const std::vector<std::string>& drop) {
+  const int T = (int)g.terminals.size();
+  const int N0 = (int)g.nonterminals.size();
+  // projection
+  std::set<std::string> dropset(drop.begin(), drop.end());
+  for (const auto& lab : dropset) {
+    bool found = false;
+    for (const auto& p : g.productions) found |= p.label == lab;
+    if (!found) throw Error(GRID_E_ARG, "role projection names unknown label '" + lab + "'");
+  }
+  std::vector<const Production*> kept;
+  for (const auto& p : g.productions)
+    if (p.label.empty() || !dropset.count(p.label)) kept.push_back(&p);
+  // generating nonterminals
+  std::vector<char> gen(N0, 0);
+  for (bool ch = true; ch;) {
+    ch = false;
+    for (const Production* p : kept) {
+      if (gen[p->lhs]) continue;
+      bool all = true;
+      for (int s : p->rhs)
+        if (s < 0 && !gen[~s]) { all = false; break; }
+      if (all) gen[p->lhs] = ch = true;
+    }
+  }
+  if (!gen[g.start]) throw Error(GRID_E_EMPTY_LANGUAGE, "the role projection leaves an empty language");
+  std::vector<const Production*> genp;
+  for (const Production* p : kept) {
+    bool ok = gen[p->lhs];
+    for (int s : p->rhs) ok = ok && (s >= 0 || gen[~s]);
+    if (ok) genp.push_back(p);
+  }
+  // reachable from the start symbol
+  std::vector<char> reach(N0, 0);
+  reach[g.start] = 1;
+  for (bool ch = true; ch;) {
+    ch = false;
+    for (const Production* p : genp)
+      if (reach[p->lhs])
+        for (int s : p->rhs)
+          if (s < 0 && !reach[~s]) reach[~s] = ch = true;
+  }
+  std::vector<int> nt_new(N0, -1);
+  int N = 0;
+  for (int a = 0; a < N0; ++a)
+    if (reach[a] && gen[a]) nt_new[a] = N++;
+
+  G2 G;
+  G.T = T;
+  G.N = N + 1;  // + S'
+  const int SP = N;
+  G.lhs.push_back(SP);
+  G.rhs.push_back({T + nt_new[g.start]});
+  Parser out;
+  out.term_used.assign(T, 0);
+  for (const Production* p : genp) {
+    if (!reach[p->lhs]) continue;
+    G.lhs.push_back(nt_new[p->lhs]);
+    std::vector<int> r;
+    for (int s : p->rhs) {
+      if (s >= 0) {
+        r.push_back(s);
+        out.term_used[s] = 1;
+      } else {
+        r.push_back(T + nt_new[~s]);
+      }
+    }
+    if (r.size() > 200) throw Error(GRID_E_CAPACITY, "production longer than 200 symbols");
+    G.rhs.push_back(r);
+  }
+  const int P = (int)G.lhs.size();
+  G.prods_of.assign(G.N, {});
+  for (int p = 0; p < P; ++p) G.prods_of[G.lhs[p]].push_back(p);
+  // nullable and FIRST
+  G.nullable.assign(G.N, 0);
+  G.first.assign(G.N, Bits());
+  for (bool ch = true; ch;) {
+    ch = false;
+    for (int p = 0; p < P; ++p) {
+      int A = G.lhs[p];
+      bool all_null = true;
+      for (int x : G.rhs[p]) {
+        if (!G.is_nt(x)) {
+          Bits b;
+          b.set(x);
+          ch |= G.first[A].merge(b);
+          all_null = false;
+          break;
+        }
+        ch |= G.first[A].merge(G.first[x - T]);
+        if (!G.nullable[x - T]) { all_null = false; break; }
+      }
+      if (all_null && !G.nullable[A]) G.nullable[A] = ch = true;
+    }
+  }
+  auto first_of_seq = [&](int p, int from, const Bits& tail, Bits& out_bits) {
+    for (size_t k = (size_t)from; k < G.rhs[p].size(); ++k) {
+      int x = G.rhs[p][k];
+      if (!G.is_nt(x)) { out_bits.set(x); return; }
+      out_bits.merge(G.first[x - T]);
+      if (!G.nullable[x - T]) return;
+    }
+    out_bits.merge(tail);
+  };
+
+  // LR(0) item sets
+  auto closure0 = [&](std::vector<Item> items) {
+    std::set<Item> seen(items.begin(), items.end());
+    for (size_t k = 0; k < items.size(); ++k) {
+      int p = ip(items[k]), d = id(items[k]);
+      if (d < (int)G.rhs[p].size() && G.is_nt(G.rhs[p][d]))
+        for (int q : G.prods_of[G.rhs[p][d] - T])
+          if (seen.insert(mk(q, 0)).second) items.push_back(mk(q, 0));
+    }
+    std::sort(items.begin(), items.end());
+    return items;
+  };
+  std::vector<std::vector<Item>> kernels;
+  std::map<std::vector<Item>, int> kid;
+  std::vector<std::map<int, int>> edges;  // state -> symbol -> state
+  kernels.push_back({mk(0, 0)});
+  kid[kernels[0]] = 0;
+  for (size_t s = 0; s < kernels.size(); ++s) {
+    std::vector<Item> cl = closure0(kernels[s]);
+    std::map<int, std::vector<Item>> moves;
+    for (Item it : cl) {
+      int p = ip(it), d = id(it);
+      if (d < (int)G.rhs[p].size()) moves[G.rhs[p][d]].push_back(mk(p, d + 1));
+    }
+    std::map<int, int> e;
+    for (auto& mv : moves) {
+      std::vector<Item> k = mv.second;
+      std::sort(k.begin(), k.end());
+      k.erase(std::unique(k.begin(), k.end()), k.end());
+      auto it = kid.find(k);
+      int t;
+      if (it == kid.end()) {
+        t = (int)kernels.size();
+        kid.emplace(k, t);
+        kernels.push_back(k);
+      } else {
+        t = it->second;
+      }
+      e[mv.first] = t;
+    }
+    edges.push_back(e);
+  }
+  const int NS = (int)kernels.size();
+  if (NS >= 0x4000) throw Error(GRID_E_CAPACITY, "more than 16383 LR states");
+  if (P >= 0x4000) throw Error(GRID_E_CAPACITY, "more than 16383 productions");
+
+  // LR(1) closure of one item set with lookahead sets (worklist)
+  const int PROBE = T + 1;
+  auto closure1 = [&](const std::vector<std::pair<Item, Bits>>& seed) {
+    std::map<Item, Bits> la;
+    std::vector<Item> work;
+    for (auto& pr : seed) {
+      if (la[pr.first].merge(pr.second) || true) work.push_back(pr.first);
+    }
+    while (!work.empty()) {
+      Item it = work.back();
+      work.pop_back();
+      int p = ip(it), d = id(it);
+      if (d >= (int)G.rhs[p].size() || !G.is_nt(G.rhs[p][d])) continue;
+      Bits look;
+      first_of_seq(p, d + 1, la[it], look);
+      for (int q : G.prods_of[G.rhs[p][d] - T]) {
+        Item ni = mk(q, 0);
+        bool fresh = !la.count(ni);
+        if (la[ni].merge(look) || fresh) work.push_back(ni);
+      }
+    }
+    return la;
+  };
+
+  // lookahead determination for kernel items
+  std::vector<std::map<Item, Bits>> kla(NS);
+  std::vector<std::map<Item, std::vector<std::pair<int, Item>>>> prop(NS);
+  for (int s = 0; s < NS; ++s)
+    for (Item k : kernels[s]) kla[s][k];
+  {
+    Bits e;
+    e.set(T);
+    kla[0][mk(0, 0)].merge(e);
+  }
+  for (int s = 0; s < NS; ++s) {
+    for (Item k : kernels[s]) {
+      Bits probe;
+      probe.set(PROBE);
+      auto J = closure1({{k, probe}});
+      for (auto& jt : J) {
+        int p = ip(jt.first), d = id(jt.first);
+        if (d >= (int)G.rhs[p].size()) continue;
+        int X = G.rhs[p][d];
+        int tgt = edges[s].at(X);
+        Item moved = mk(p, d + 1);
+        Bits spont = jt.second;
+        if (spont.test(PROBE)) {
+          prop[s][k].push_back({tgt, moved});
+          spont.w[PROBE >> 6] &= ~(1ull << (PROBE & 63));
+        }
+        kla[tgt][moved].merge(spont);
+      }
+    }
+  }
+  for (bool ch = true; ch;) {
+    ch = false;
+    for (int s = 0; s < NS; ++s)
+      for (auto& pk : prop[s]) {
+        const Bits src = kla[s][pk.first];
+        for (auto& dst : pk.second) ch |= kla[dst.first][dst.second].merge(src);
+      }
+  }
+
+  // tables
+  out.T = T;
+  out.N = G.N - 1;  // S' has no GOTO column
+  out.n_states = NS;
+  out.action.assign((size_t)NS * (T + 1), 0);
+  out.go.assign((size_t)NS * std::max(out.N, 1), kNoGoto);
+  out.prod.resize(P);
+  for (int p = 0; p < P; ++p) out.prod[p] = (uint32_t)G.lhs[p] | (uint32_t)G.rhs[p].size() << 16;
+  auto sym_name = [&](int x) -> std::string {
+    if (x == T) return "$end";
+    return x < T ? g.terminals[x].name : "<nonterminal>";
+  };
+  auto conflict = [&](int s, int t, uint16_t a, uint16_t b) {
+    auto describe = [&](uint16_t v) -> std::string {
+      if ((v & 0xC000) == kActShift) return "shift";
+      if ((v & 0xC000) == kActAccept) return "accept";
+      int p = v & 0x3FFF;
+      std::string r = "reduce rule " + std::to_string(p) + " (";
+      for (int x : G.rhs[p]) r += (G.is_nt(x) ? std::string("nt") : sym_name(x)) + " ";
+      return r + ")";
+    };
+    throw Error(GRID_E_LALR_CONFLICT, "LALR(1) conflict in state " + std::to_string(s) + " on " +
+                                          sym_name(t) + ": " + describe(a) + " vs " + describe(b));
+  };
+  for (int s = 0; s < NS; ++s) {
+    for (auto& e : edges[s]) {
+      if (e.first < T) out.action[(size_t)s * (T + 1) + e.first] = (uint16_t)(kActShift | e.second);
+      else if (e.first - T < out.N) out.go[(size_t)s * out.N + (e.first - T)] = (uint16_t)e.second;
+    }
+    std::vector<std::pair<Item, Bits>> seed(kla[s].begin(), kla[s].end());
+    auto J = closure1(seed);
+    for (auto& jt : J) {
+      int p = ip(jt.first), d = id(jt.first);
+      if (d != (int)G.rhs[p].size()) continue;
+      for (int t = 0; t <= T; ++t) {
+        if (!jt.second.test(t)) continue;
+        uint16_t a = (p == 0) ? kActAccept : (uint16_t)(kActReduce | p);
+        uint16_t& cell = out.action[(size_t)s * (T + 1) + t];
+        if (cell != 0 && cell != a) conflict(s, t, cell, a);
+        cell = a;
+      }
+    }
+  }
+  return out;
+}
+
+}  // namespace grid

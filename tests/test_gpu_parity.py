@@ -1,0 +1,236 @@
+"""GPU path (libgrid.so HIP kernels, called through the C ABI) against the CPU
+oracle, element by element, bit-exact.
+
+Masks are compared word for word with the oracle's full mask for every row
+(checkpoint mode of the oracle, itself checked equal to from-scratch mode on
+CPU tests) at every workload's real size and in the launch configuration the
+benchmark times; end-of-sequence flags and row status are checked too.  The
+apply kernel is compared with torch's CPU masked_fill on fp32 and bf16.
+"""
+
+import os
+import sys
+import time
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from workloads import make_workload  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def G():
+    import paper_2607_11951_amd as pkg
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    pkg.lib()  # raises when libgrid.so is missing: no fallback
+    return pkg
+
+
+def _gpu_masks(G, wl, rows, grid=None, slot_map=None):
+    """Runs the GPU path over rows in batches of wl.batch; returns host arrays."""
+    if grid is None:
+        grid, slot_map = G.from_workload(wl)
+        grid.to_device("cuda")
+    masks, eos, status = [], [], []
+    for i in range(0, len(rows), wl.batch):
+        idx = rows[i:i + wl.batch]
+        cfgs, pool = grid.configs([wl.prefixes[j] for j in idx], [slot_map[wl.slots[j]] for j in idx])
+        c, p = grid.configs_to_device(cfgs, pool)
+        m, e, s = grid.mask(c, p, len(idx))
+        torch.cuda.synchronize()
+        masks.append(m.cpu().numpy().view(np.uint32))
+        eos.append(e.cpu().numpy())
+        status.append(s.cpu().numpy())
+    return grid, np.concatenate(masks), np.concatenate(eos), np.concatenate(status)
+
+
+def _oracle_rows(oracle_mod, wl, rows):
+    o = oracle_mod.from_workload(wl)
+    out, eos = [], []
+    lex_cache = {}
+    for j in rows:
+        lexicon = None
+        if len(wl.lexicons) > 1:
+            s = wl.slots[j]
+            if s not in lex_cache:
+                lex_cache[s] = oracle_mod.Lexicon(o.grammar, wl.lexicons[s])
+            lexicon = lex_cache[s]
+        w, e = o.mask(wl.prefixes[j], mode=1, lexicon=lexicon)
+        out.append(w)
+        eos.append(e)
+    return np.stack(out), np.array(eos, dtype=np.uint8)
+
+
+def _compare(wl, rows, gm, ge, gs, om, oe, label):
+    bad_rows = [r for r in range(len(rows)) if not np.array_equal(gm[r], om[r]) or ge[r] != oe[r]]
+    for r in bad_rows[:3]:
+        diff = np.nonzero(gm[r] != om[r])[0]
+        toks = []
+        for w in diff[:4]:
+            x = int(gm[r][w]) ^ int(om[r][w])
+            toks += [int(w) * 32 + b for b in range(32) if (x >> b) & 1][:3]
+        log(f"[{label}] row {rows[r]} prefix={wl.prefixes[rows[r]][-60:]!r} eos gpu={ge[r]} "
+            f"oracle={oe[r]} differing tokens {[(t, wl.vocab[t]) for t in toks[:6]]}")
+    assert not bad_rows, f"{label}: {len(bad_rows)} rows differ"
+    assert (gs == 0).all(), f"{label}: row status {gs}"
+    # nothing viable is empty (Proposition 8 with a byte-complete vocabulary)
+    assert all(int(om[r].any()) or oe[r] for r in range(len(rows)))
+
+
+def test_expr_all_configs_one_per_call(G, oracle_mod):
+    wl = make_workload(1)
+    rows = list(range(len(wl.prefixes)))
+    log(f"workload 1: {len(rows)} rows, V={wl.V}, one row per call")
+    _, gm, ge, gs = _gpu_masks(G, wl, rows)
+    om, oe = _oracle_rows(oracle_mod, wl, rows)
+    _compare(wl, rows, gm, ge, gs, om, oe, "expr")
+
+
+def test_select_subset_batch(G, oracle_mod):
+    wl = make_workload(2, n_batches=2)
+    rows = list(range(len(wl.prefixes)))
+    log(f"workload 2: {len(rows)} rows, V={wl.V}, batch {wl.batch}")
+    _, gm, ge, gs = _gpu_masks(G, wl, rows)
+    om, oe = _oracle_rows(oracle_mod, wl, rows)
+    _compare(wl, rows, gm, ge, gs, om, oe, "select")
+
+
+def test_dml_full_size_batch(G, oracle_mod):
+    """The benchmark's workload and launch shape: B = 32, V = 151,936."""
+    wl = make_workload(3, n_batches=2)
+    rows = list(range(len(wl.prefixes)))
+    log(f"workload 3: {len(rows)} rows, V={wl.V}, batch {wl.batch}")
+    t = time.time()
+    _, gm, ge, gs = _gpu_masks(G, wl, rows)
+    om, oe = _oracle_rows(oracle_mod, wl, rows)
+    log(f"  compared in {time.time() - t:.1f}s")
+    _compare(wl, rows, gm, ge, gs, om, oe, "dml")
+
+
+def test_long_sentences_positions_and_depths(G, oracle_mod):
+    """16,000-token sentences: configurations at 1k / 4k / 16k tokens, nesting
+    depth 1 / 8 / 32 / 128 (stack up to several hundred states)."""
+    wl = make_workload(4, rows=8)
+    rows = list(range(len(wl.prefixes)))
+    log(f"workload 4: {len(rows)} rows (8 per cell), V={wl.V}")
+    grid, gm, ge, gs = _gpu_masks(G, wl, rows)
+    om, oe = _oracle_rows(oracle_mod, wl, rows)
+    _compare(wl, rows, gm, ge, gs, om, oe, "long")
+    cfgs, _ = grid.configs([wl.prefixes[j] for j in rows[-8:]])
+    log(f"  stack depths at depth-128 cells: {sorted(cfgs['stk_depth'].tolist())}")
+    assert cfgs["stk_depth"].max() > 300
+
+
+def test_cold_schema_batch_and_bf16_apply(G, oracle_mod):
+    """256 rows, each with its own freshly generated schema lexicon, then the
+    fused -inf fill of bf16 logits [256, 151,936] ~ N(0, 4)."""
+    wl = make_workload(5)
+    rows = list(range(len(wl.prefixes)))
+    log(f"workload 5: {len(rows)} rows / schemas, V={wl.V}")
+    t = time.time()
+    grid, slot_map = G.from_workload(wl)
+    grid.to_device("cuda")
+    log(f"  compile + {len(slot_map)} lexicons + upload: {time.time() - t:.1f}s")
+    _, gm, ge, gs = _gpu_masks(G, wl, rows, grid, slot_map)
+    om, oe = _oracle_rows(oracle_mod, wl, rows)
+    _compare(wl, rows, gm, ge, gs, om, oe, "cold-schema")
+    gen = torch.Generator(device="cpu").manual_seed(wl.meta["logits_seed"])
+    logits = (torch.randn(len(rows), wl.V, generator=gen) * wl.meta["logits_std"]).to(torch.bfloat16)
+    ref = _apply_reference(logits, om, wl.V)
+    dev = logits.cuda()
+    mask_dev = torch.from_numpy(om.view(np.int32).copy()).cuda()
+    G.apply(mask_dev, dev)
+    torch.cuda.synchronize()
+    assert torch.equal(dev.cpu().view(torch.int16), ref.view(torch.int16))
+
+
+def _apply_reference(logits, words, V):
+    bits = np.unpackbits(words.view(np.uint8), axis=1, bitorder="little")[:, :V].astype(bool)
+    out = logits.clone()
+    out.masked_fill_(~torch.from_numpy(bits), float("-inf"))
+    return out
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("B,V,pad", [(1, 1, 0), (3, 37, 5), (5, 1024, 0), (2, 151936, 8), (7, 1001, 3)])
+def test_apply_bit_exact(G, dtype, B, V, pad):
+    g = torch.Generator(device="cpu").manual_seed(B * 1000 + V)
+    W = (V + 31) // 32
+    words = torch.randint(0, 2 ** 31, (B, W), generator=g, dtype=torch.int64)
+    words[0, :] = 0                                   # a fully masked row
+    if B > 1:
+        words[1, :] = -1                              # a fully allowed row
+    words = words.to(torch.int32).numpy().view(np.uint32)
+    words = words.copy()
+    if V % 32:
+        words[:, -1] &= (1 << (V % 32)) - 1
+    store = (torch.randn(B, V + pad, generator=g) * 2).to(dtype)
+    ref = store.clone()
+    ref[:, :V] = _apply_reference(store[:, :V].contiguous(), words, V)
+    dev = store.cuda()
+    view = dev[:, :V]
+    G.apply(torch.from_numpy(words.view(np.int32).copy()).cuda(), view)
+    torch.cuda.synchronize()
+    itype = torch.int16 if dtype == torch.bfloat16 else torch.int32
+    assert torch.equal(dev.cpu().view(itype), ref.view(itype))
+
+
+def test_edge_cases(G, oracle_mod):
+    wl = make_workload(3, rows=4)
+    grid, slot_map = G.from_workload(wl)
+    grid.to_device("cuda")
+    prefixes = [b"", b"select", b"select 1;", b"select 1; \n ", b"  ", b"with t1 as (select *"]
+    cfgs, pool = grid.configs(prefixes, [slot_map[0]] * len(prefixes))
+    c, p = grid.configs_to_device(cfgs, pool)
+    m, e, s = grid.mask(c, p, len(prefixes))
+    torch.cuda.synchronize()
+    o = oracle_mod.from_workload(wl)
+    for i, w in enumerate(prefixes):
+        ow, oe = o.mask(w, mode=1)
+        assert np.array_equal(m[i].cpu().numpy().view(np.uint32), ow), w
+        assert int(e[i]) == oe, w
+    assert e.cpu().tolist() == [0, 0, 1, 1, 0, 0]
+    # a configuration with an out-of-range DFA state is flagged, not walked
+    bad = cfgs.copy()
+    bad["q"][1] = 60000
+    c2, p2 = grid.configs_to_device(bad, pool)
+    m2, e2, s2 = grid.mask(c2, p2, len(prefixes))
+    torch.cuda.synchronize()
+    assert s2.cpu().tolist()[1] == G.ROW_BAD_CONFIG
+    assert int(m2[1].abs().sum()) == 0 and s2.cpu().tolist()[0] == 0
+
+
+def test_gpu_invariants_full_vocab(G):
+    """Properties that hold at any size: alias ids carry equal bits; a blocked
+    spelling blocks every extension (monotone rejection); specials and padding
+    bits are 0."""
+    wl = make_workload(3, rows=32)
+    rows = list(range(32))
+    _, gm, ge, gs = _gpu_masks(G, wl, rows)
+    bits = np.unpackbits(gm.view(np.uint8), axis=1, bitorder="little")
+    V = wl.V
+    assert not bits[:, V:].any()
+    specials = [t for t in wl.specials if t != wl.eos_id]
+    assert not bits[:, specials].any()
+    assert (bits[:, wl.eos_id] == ge).all()
+    first = {}
+    for t, sp in enumerate(wl.vocab):
+        if sp and t not in wl.specials:
+            first.setdefault(sp, t)
+    for t, sp in enumerate(wl.vocab):
+        if sp in first and first[sp] != t:
+            assert (bits[:, t] == bits[:, first[sp]]).all()
+    by_spelling = {sp: t for sp, t in first.items()}
+    for sp, t in list(by_spelling.items())[:20000]:
+        if len(sp) > 1 and sp[:-1] in by_spelling:
+            parent = by_spelling[sp[:-1]]
+            assert not (bits[:, t] & ~bits[:, parent]).any(), sp
