@@ -50,6 +50,7 @@ def _gpu_masks(G, wl, rows, grid=None, slot_map=None):
         masks.append(m.cpu().numpy().view(np.uint32))
         eos.append(e.cpu().numpy())
         status.append(s.cpu().numpy())
+    _gpu_masks.slot_map = slot_map
     return grid, np.concatenate(masks), np.concatenate(eos), np.concatenate(status)
 
 
@@ -125,7 +126,8 @@ def test_long_sentences_positions_and_depths(G, oracle_mod):
     grid, gm, ge, gs = _gpu_masks(G, wl, rows)
     om, oe = _oracle_rows(oracle_mod, wl, rows)
     _compare(wl, rows, gm, ge, gs, om, oe, "long")
-    cfgs, _ = grid.configs([wl.prefixes[j] for j in rows[-8:]])
+    sm = _gpu_masks.slot_map
+    cfgs, _ = grid.configs([wl.prefixes[j] for j in rows[-8:]], [sm[wl.slots[j]] for j in rows[-8:]])
     log(f"  stack depths at depth-128 cells: {sorted(cfgs['stk_depth'].tolist())}")
     assert cfgs["stk_depth"].max() > 300
 
@@ -165,12 +167,10 @@ def _apply_reference(logits, words, V):
 def test_apply_bit_exact(G, dtype, B, V, pad):
     g = torch.Generator(device="cpu").manual_seed(B * 1000 + V)
     W = (V + 31) // 32
-    words = torch.randint(0, 2 ** 31, (B, W), generator=g, dtype=torch.int64)
+    words = torch.randint(0, 2 ** 32, (B, W), generator=g, dtype=torch.int64).numpy().astype(np.uint32)
     words[0, :] = 0                                   # a fully masked row
     if B > 1:
-        words[1, :] = -1                              # a fully allowed row
-    words = words.to(torch.int32).numpy().view(np.uint32)
-    words = words.copy()
+        words[1, :] = 0xFFFFFFFF                      # a fully allowed row
     if V % 32:
         words[:, -1] &= (1 << (V % 32)) - 1
     store = (torch.randn(B, V + pad, generator=g) * 2).to(dtype)
