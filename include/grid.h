@@ -150,8 +150,18 @@ enum {
   GRID_ART_LEX_FLAGS,       /* u16 per lexicon-trie node: bit c prefix-of-category-c,
                                bit 8+c word-of-category-c */
   GRID_ART_LEX_HASH,        /* u32 [2] per entry: key = node * 256 + byte + 1 (0 empty), child */
-  GRID_ART_LEX_SLOTS,       /* u32 [4] per slot: flags base, hash base, hash mask,
-                               restricted-category mask */
+  GRID_ART_LEX_SLOTS,       /* u32 [8] per slot: flags base, hash base, hash mask,
+                               restricted-category mask, node count, 3 reserved */
+  GRID_ART_SPELL_REC,       /* u32 [U][4] per sorted spelling: its first 8 bytes (little-
+                               endian, zero padded), first alias id | 1 << 31 when more ids
+                               share the spelling, length */
+  GRID_ART_PARSE_STATE,     /* u32 [n_lr][2*TW+2], TW = ceil((T+1)/32): terminals that shift
+                               (or accept), terminals reduced by the state's main
+                               production, main production | extra groups << 16, offset of
+                               the extra groups in PARSE_REDX */
+  GRID_ART_PARSE_REDX,      /* u32 per extra reduce group: production, TW words of terminals */
+  GRID_ART_GOTO_OFF,        /* u32 [n_lr+1] offsets into GOTO_ENT */
+  GRID_ART_GOTO_ENT,        /* u32 nonterminal | target << 16 */
   GRID_ART_COUNT
 };
 int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);
@@ -201,11 +211,13 @@ int grid_mask(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
 /* The same work split into its launches, for callers that time or overlap
  * them: phases is a bit set of GRID_PHASE_* run in order on the stream.  A
  * walk needs the prologue of the same rows and workspace to have run before
- * it (earlier on the stream); finalize needs the walk.  grid_mask equals
- * grid_mask_phases with GRID_PHASE_ALL. */
+ * it (earlier on the stream); finalize needs the walk; the mask is exact once
+ * all three have run.  grid_mask equals grid_mask_phases with GRID_PHASE_ALL. */
 #define GRID_PHASE_PROLOGUE 1u      /* allowed sets, EOS gate, row clear */
 #define GRID_PHASE_WALK 2u          /* full-vocabulary walk and bit packing */
-#define GRID_PHASE_FINALIZE 4u      /* row status (needs status_dev) */
+#define GRID_PHASE_FINALIZE 4u      /* finishes the spellings the walk handed to the slow
+                                       path (needed for an exact mask) and writes the row
+                                       status when status_dev is not null */
 #define GRID_PHASE_ALL 7u
 int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
                      const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,

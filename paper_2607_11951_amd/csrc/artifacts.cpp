@@ -63,6 +63,14 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
       va.spell_bytes.insert(va.spell_bytes.end(), s.begin(), s.end());
       va.spell_off.push_back((uint32_t)va.spell_bytes.size());
       va.max_len = std::max(va.max_len, (int)s.size());
+      uint64_t head = 0;
+      for (size_t k = 0; k < s.size() && k < 8; ++k) head |= (uint64_t)(uint8_t)s[k] << (8 * k);
+      va.spell_rec.push_back((uint32_t)head);
+      va.spell_rec.push_back((uint32_t)(head >> 32));
+      va.spell_rec.push_back((uint32_t)ids[k]);
+      va.spell_rec.push_back((uint32_t)s.size());
+    } else {
+      va.spell_rec[va.spell_rec.size() - 2] |= 1u << 31;  // more than one id
     }
     va.alias_ids.push_back(ids[k]);
   }

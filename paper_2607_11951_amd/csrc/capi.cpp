@@ -163,6 +163,11 @@ extern "C" int grid_artifact(const grid_compiled* g, int32_t which, const void**
     case GRID_ART_LEX_FLAGS: put(g->lex.flags, p, n); break;
     case GRID_ART_LEX_HASH: put(g->lex.hash, p, n); break;
     case GRID_ART_LEX_SLOTS: put(g->lex.slots, p, n); break;
+    case GRID_ART_SPELL_REC: put(g->vocab.spell_rec, p, n); break;
+    case GRID_ART_PARSE_STATE: put(g->parser.pstate, p, n); break;
+    case GRID_ART_PARSE_REDX: put(g->parser.predx, p, n); break;
+    case GRID_ART_GOTO_OFF: put(g->parser.goto_off, p, n); break;
+    case GRID_ART_GOTO_ENT: put(g->parser.goto_ent, p, n); break;
     default: return fail(GRID_E_ARG, "unknown artifact " + std::to_string(which));
   }
   return GRID_OK;

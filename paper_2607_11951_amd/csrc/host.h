@@ -77,6 +77,13 @@ struct Parser {
   std::vector<uint16_t> go;       // [n_states*N]
   std::vector<uint32_t> prod;     // lhs | len << 16
   std::vector<uint8_t> term_used; // terminal appears in the reduced grammar
+  // compact form for set simulation (TW = words per terminal set incl. end of input):
+  // per state [shift bits TW][main reduce bits TW][main prod | extra groups << 16][extra off]
+  int tw = 0;
+  std::vector<uint32_t> pstate;
+  std::vector<uint32_t> predx;     // extra reduce groups: [prod][bits TW]
+  std::vector<uint32_t> goto_off;  // [n_states+1]
+  std::vector<uint32_t> goto_ent;  // nonterminal | target << 16
   uint16_t act(int s, int t) const { return action[(size_t)s * (T + 1) + t]; }
   uint16_t gto(int s, int a) const { return go[(size_t)s * N + a]; }
 };
@@ -88,6 +95,7 @@ struct VocabArtifacts {
   int V = 0;
   std::vector<uint32_t> spell_off;   // [U+1]
   std::vector<uint8_t> spell_bytes;  // + padding
+  std::vector<uint32_t> spell_rec;   // [U][4]: head lo, head hi, id | multi << 31, length
   std::vector<uint32_t> alias_off;   // [U+1]
   std::vector<int32_t> alias_ids;
   std::vector<uint32_t> level_off;   // [Lmax+2]

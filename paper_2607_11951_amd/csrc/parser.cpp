@@ -50,6 +50,8 @@ inline int id(Item x) { return (int)(x & 255); }
 
 }  // namespace
 
+void compact_tables(Parser& P);
+
 Parser build_parser(const GrammarText& g, const std::vector<std::string>& drop) {
   const int T = (int)g.terminals.size();
   const int N0 = (int)g.nonterminals.size();
@@ -307,7 +309,63 @@ Parser build_parser(const GrammarText& g, const std::vector<std::string>& drop) 
       }
     }
   }
+  compact_tables(out);
   return out;
+}
+
+// Compact tables for simulating a whole set of lookahead terminals at once:
+// per state the terminals that shift (or accept, end-of-input column), the
+// terminals reduced by the state's main production, and any further reduce
+// productions with their own terminal sets; GOTO as per-state lists.
+void compact_tables(Parser& P) {
+  const int T1 = P.T + 1;
+  const int TW = (T1 + 31) / 32;
+  P.tw = TW;
+  const int stride = 2 * TW + 2;
+  P.pstate.assign((size_t)P.n_states * stride, 0);
+  P.predx.clear();
+  P.goto_off.assign(P.n_states + 1, 0);
+  P.goto_ent.clear();
+  for (int s = 0; s < P.n_states; ++s) {
+    uint32_t* rec = &P.pstate[(size_t)s * stride];
+    std::map<int, std::vector<uint32_t>> groups;  // prod -> bits
+    for (int t = 0; t < T1; ++t) {
+      const uint16_t a = P.act(s, t);
+      const uint16_t kind = a & 0xC000;
+      if (a == 0) continue;
+      if (kind == kActShift || kind == kActAccept) {
+        rec[t >> 5] |= 1u << (t & 31);
+      } else {
+        auto& g = groups[a & 0x3FFF];
+        g.resize(TW, 0);
+        g[t >> 5] |= 1u << (t & 31);
+      }
+    }
+    int main_prod = 0xFFFF;
+    size_t best = 0;
+    for (auto& g : groups) {
+      size_t n = 0;
+      for (uint32_t w : g.second) n += (size_t)__builtin_popcount(w);
+      if (n > best) { best = n; main_prod = g.first; }
+    }
+    uint32_t n_extra = 0;
+    rec[2 * TW + 1] = (uint32_t)P.predx.size();
+    for (auto& g : groups) {
+      if (g.first == main_prod) {
+        for (int w = 0; w < TW; ++w) rec[TW + w] = g.second[w];
+      } else {
+        P.predx.push_back((uint32_t)g.first);
+        P.predx.insert(P.predx.end(), g.second.begin(), g.second.end());
+        ++n_extra;
+      }
+    }
+    rec[2 * TW] = (uint32_t)main_prod | n_extra << 16;
+    for (int a = 0; a < P.N; ++a) {
+      const uint16_t g = P.gto(s, a);
+      if (g != kNoGoto) P.goto_ent.push_back((uint32_t)a | (uint32_t)g << 16);
+    }
+    P.goto_off[s + 1] = (uint32_t)P.goto_ent.size();
+  }
 }
 
 }  // namespace grid

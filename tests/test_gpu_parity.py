@@ -234,3 +234,39 @@ def test_gpu_invariants_full_vocab(G):
         if len(sp) > 1 and sp[:-1] in by_spelling:
             parent = by_spelling[sp[:-1]]
             assert not (bits[:, t] & ~bits[:, parent]).any(), sp
+
+
+def test_overlay_handoff_to_slow_path(G, oracle_mod):
+    """Tokens that shift many terminals (runs of '(' at a boolean position,
+    '(' and ')' mixes) outgrow a walk lane's LDS stack area and are finished by
+    the slow path; the mask must still equal the oracle's and no row may report
+    an overflow."""
+    from workloads import grammar_text
+    base = make_workload(3, rows=1)
+    vocab = [bytes([b]) for b in range(256)]
+    vocab += [b"(" * k for k in range(2, 61)] + [b"( " * k for k in range(2, 30)]
+    vocab += [b"((a=1)" * k for k in range(1, 9)] + [b")" * k for k in range(2, 20)]
+    vocab += [b" (((((((((( 1", b"((((((((((((((((((((((((((((((((((((((((1", b""]
+    eos = len(vocab) - 1
+    lex = base.lexicons[0]
+    g = G.Grid(grammar_text("sql_dml"), base.drop, vocab, [eos], eos)
+    slot = g.add_lexicon(lex)
+    g.to_device("cuda")
+    t, c = base.meta["schema"].tables[0], base.meta["schema"].columns[0][0]
+    prefixes = [f"select {c} from {t} where ".encode(), f"select {c} from {t} where ((".encode(),
+                f"select {c} from {t} where {c} in (select {c} from {t} where ((((".encode(),
+                b"select 1 + ", b"select ("]
+    cfgs, pool = g.configs(prefixes, [slot] * len(prefixes))
+    cd, pd = g.configs_to_device(cfgs, pool)
+    m, e, s = g.mask(cd, pd, len(prefixes))
+    torch.cuda.synchronize()
+    o = oracle_mod.Oracle(grammar_text("sql_dml"), base.drop, lex, vocab, [eos], eos)
+    for i, w in enumerate(prefixes):
+        want, want_eos = o.mask(w, mode=1)
+        got = m[i].cpu().numpy().view(np.uint32)
+        assert np.array_equal(got, want), (w, [vocab[t] for t in range(len(vocab))
+                                               if ((int(got[t >> 5]) ^ int(want[t >> 5])) >> (t & 31)) & 1])
+        assert int(e[i]) == want_eos
+    assert (s.cpu().numpy() == 0).all(), s.cpu().tolist()
+    bits = np.unpackbits(m[0].cpu().numpy().view(np.uint8), bitorder="little")
+    assert bits[vocab.index(b"(" * 60)] == 1    # a 60-deep run is viable and came back exact
