@@ -126,8 +126,10 @@ int grid_add_lexicon(grid_compiled* g, const grid_lexicon_args* lex, int32_t* sl
 
 /* ---------------------------------------------------------------- artifacts */
 /* Device artifacts.  The caller allocates device memory of the reported size,
- * copies the host bytes there and binds the device pointer; grid_mask reads
- * only bound artifacts (GRID_E_UNBOUND otherwise). */
+ * copies the host bytes there and binds the device pointer, which must be
+ * 16-byte aligned (the kernels read artifacts with 16-byte loads; GRID_E_ARG
+ * otherwise); grid_mask reads only bound artifacts (GRID_E_UNBOUND otherwise).
+ * The device copy stays owned by the caller and must outlive its use. */
 enum {
   GRID_ART_DFA_DENSE = 0,   /* u16 [S][256] next state, 0 = dead */
   GRID_ART_DFA_CLASS,       /* u16 [S][C] next state by byte class */
@@ -154,14 +156,19 @@ enum {
                                restricted-category mask, node count, 3 reserved */
   GRID_ART_SPELL_REC,       /* u32 [U][4] per sorted spelling: its first 8 bytes (little-
                                endian, zero padded), first alias id | 1 << 31 when more ids
-                               share the spelling, length */
+                               share the spelling, length | tail chunk << 8 (bytes 8.. of a
+                               longer spelling start at SPELL_TAIL + 16 * tail chunk) */
   GRID_ART_PARSE_STATE,     /* u32 [n_lr][2*TW+2], TW = ceil((T+1)/32): terminals that shift
                                (or accept), terminals reduced by the state's main
                                production, main production | extra groups << 16, offset of
                                the extra groups in PARSE_REDX */
   GRID_ART_PARSE_REDX,      /* u32 per extra reduce group: production, TW words of terminals */
-  GRID_ART_GOTO_OFF,        /* u32 [n_lr+1] offsets into GOTO_ENT */
-  GRID_ART_GOTO_ENT,        /* u32 nonterminal | target << 16 */
+  GRID_ART_GOTO_HASH,       /* GOTO as an open-addressing table of H = 2^k slots (k >= 6,
+                               load <= 2/3): u32 [H] keys (state << 16 | nonterminal) + 1
+                               (0 empty), then u16 [H] targets; slot of a key =
+                               (key * 0x9E3779B1 mod 2^32) >> (32 - k), linear probing */
+  GRID_ART_SPELL_TAIL,      /* u8 [16 * chunks]: bytes 8.. of each spelling longer than 8
+                               bytes, each starting on a 16-byte boundary, zero padded */
   GRID_ART_COUNT
 };
 int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);

@@ -1,7 +1,9 @@
 // artifacts.cpp -- vocabulary and schema-lexicon artifacts.
 //
 // Vocabulary (Definition 3, section 4.1): the distinct non-special spellings,
-// sorted in byte order, which is the depth-first order of the token byte trie;
+// sorted in byte order, which is the depth-first order of the token byte trie,
+// each with a 16-byte record (first 8 bytes, first id, length) and, past 8
+// bytes, a tail on 16-byte boundaries so a walk fetches 16 bytes per load;
 // an alias table lists every token id sharing a spelling (section 2: masks are
 // over ids, so alias expansion is needed for completeness); and a levelized
 // CSR form of the same trie (level by level, children in byte order, each
@@ -68,7 +70,14 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
       va.spell_rec.push_back((uint32_t)head);
       va.spell_rec.push_back((uint32_t)(head >> 32));
       va.spell_rec.push_back((uint32_t)ids[k]);
-      va.spell_rec.push_back((uint32_t)s.size());
+      uint32_t chunk = 0;
+      if (s.size() > 8) {  // bytes 8.. on a 16-byte boundary of their own
+        chunk = (uint32_t)(va.spell_tail.size() / 16);
+        if (chunk >= (1u << 24)) throw Error(GRID_E_CAPACITY, "spelling tails larger than 256 MiB");
+        va.spell_tail.insert(va.spell_tail.end(), s.begin() + 8, s.end());
+        va.spell_tail.resize((va.spell_tail.size() + 15) & ~(size_t)15, 0);
+      }
+      va.spell_rec.push_back((uint32_t)s.size() | chunk << 8);
     } else {
       va.spell_rec[va.spell_rec.size() - 2] |= 1u << 31;  // more than one id
     }
@@ -76,6 +85,7 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
   }
   if (!uniq.empty()) va.alias_off.push_back((uint32_t)va.alias_ids.size());
   va.spell_bytes.resize(va.spell_bytes.size() + 32, 0);  // safe over-read padding
+  va.spell_tail.resize(va.spell_tail.size() + 32, 0);    // one chunk of read-ahead
   std::vector<char> single(256, 0);
   for (auto& s : uniq)
     if (s.size() == 1) single[(uint8_t)s[0]] = 1;

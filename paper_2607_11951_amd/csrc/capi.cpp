@@ -164,10 +164,10 @@ extern "C" int grid_artifact(const grid_compiled* g, int32_t which, const void**
     case GRID_ART_LEX_HASH: put(g->lex.hash, p, n); break;
     case GRID_ART_LEX_SLOTS: put(g->lex.slots, p, n); break;
     case GRID_ART_SPELL_REC: put(g->vocab.spell_rec, p, n); break;
+    case GRID_ART_SPELL_TAIL: put(g->vocab.spell_tail, p, n); break;
     case GRID_ART_PARSE_STATE: put(g->parser.pstate, p, n); break;
     case GRID_ART_PARSE_REDX: put(g->parser.predx, p, n); break;
-    case GRID_ART_GOTO_OFF: put(g->parser.goto_off, p, n); break;
-    case GRID_ART_GOTO_ENT: put(g->parser.goto_ent, p, n); break;
+    case GRID_ART_GOTO_HASH: put(g->parser.goto_hash, p, n); break;
     default: return fail(GRID_E_ARG, "unknown artifact " + std::to_string(which));
   }
   return GRID_OK;
@@ -181,6 +181,7 @@ extern "C" int grid_bind_device(grid_compiled* g, int32_t which, void* dev) {
   int rc = grid_artifact(g, which, &hp, &n);
   if (rc) return rc;
   if (!dev && n > 0) return fail(GRID_E_ARG, "null device pointer");
+  if (((uintptr_t)dev & 15) != 0) return fail(GRID_E_ARG, "device pointer not 16-byte aligned");
   g->dev[which] = dev;
   g->dev_bytes[which] = n;
   return GRID_OK;

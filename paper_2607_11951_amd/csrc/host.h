@@ -82,8 +82,10 @@ struct Parser {
   int tw = 0;
   std::vector<uint32_t> pstate;
   std::vector<uint32_t> predx;     // extra reduce groups: [prod][bits TW]
-  std::vector<uint32_t> goto_off;  // [n_states+1]
-  std::vector<uint32_t> goto_ent;  // nonterminal | target << 16
+  // GOTO as an open-addressing hash: H (power of two) u32 keys
+  // (state << 16 | nonterminal) + 1, 0 empty, then H u16 targets
+  std::vector<uint8_t> goto_hash;
+  int goto_hbits = 0;
   uint16_t act(int s, int t) const { return action[(size_t)s * (T + 1) + t]; }
   uint16_t gto(int s, int a) const { return go[(size_t)s * N + a]; }
 };
@@ -95,7 +97,8 @@ struct VocabArtifacts {
   int V = 0;
   std::vector<uint32_t> spell_off;   // [U+1]
   std::vector<uint8_t> spell_bytes;  // + padding
-  std::vector<uint32_t> spell_rec;   // [U][4]: head lo, head hi, id | multi << 31, length
+  std::vector<uint32_t> spell_rec;   // [U][4]: head lo, head hi, id | multi << 31, length | chunk << 8
+  std::vector<uint8_t> spell_tail;   // bytes 8.. per spelling, 16-byte aligned chunks
   std::vector<uint32_t> alias_off;   // [U+1]
   std::vector<int32_t> alias_ids;
   std::vector<uint32_t> level_off;   // [Lmax+2]

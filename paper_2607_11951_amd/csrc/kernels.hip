@@ -6,32 +6,32 @@
 //     terminals A(sigma) (section 3.2, allowed terminals under table
 //     compression) by simulating the reduce chain for the whole set of
 //     terminals at once: at each state the terminals that shift are allowed,
-//     those reduced by the state's production travel on together, the rest
-//     are errors.  Each workgroup then records, for its share of the allowed
-//     terminals, the stack after that terminal's shift (on a private overlay
-//     above the shared read-only stack), that stack's own allowed set, and the
-//     trailing-lexeme codes of every lexer state under it.  Workgroup 0 also
+//     those reduced by one production travel on together, the rest are
+//     errors.  Each workgroup then records, for its share of the allowed
+//     terminals t, the stack after shifting t (an overlay above the shared
+//     read-only stack) and that stack's own allowed set.  Workgroup 0 also
 //     resolves the pending lexeme (its winner at an emission), the end-of-
-//     sequence gate (section 3.2, EOS gating, mid-lexeme aware), the trailing
-//     codes under A(sigma) (Definition 2), and a 256-entry first-byte table:
-//     the scan state after any first byte of a token (continuing the pending
-//     lexeme, or emitting it and starting a new one), or "rejected"; it clears
-//     the row's mask words.
-//  2. walk (persistent; work items = row x spelling tile): one lane per
+//     sequence gate (section 3.2, EOS gating, mid-lexeme aware) and a
+//     256-entry first-byte table: the scan state after any first byte of a
+//     token (continuing the pending lexeme, or emitting it and starting a new
+//     one), or "rejected"; it clears the row's mask words.
+//  2. walk (persistent; work items = spelling chunk x row): one lane per
 //     distinct spelling in byte order, so neighbouring lanes share prefixes
-//     and die together.  The lexer DFA, compact LR tables, byte classes,
-//     accept lists, first-byte table and trailing codes sit in LDS; each
-//     spelling's first 8 bytes and first alias id arrive in one 16-byte load.
-//     A byte that kills the DFA emits the pending lexeme as the highest-
-//     priority candidate that is allowed (or ignored) and passes the schema
-//     lexicon, then the byte is scanned again (section 4.1, trie walk).
-//     Tokens that stay in one lexeme are decided by the trailing codes
-//     (context-independent part, section 4.2); after one shift the recorded
-//     stack, allowed set and codes are used; later shifts run reduce chains on
-//     the lane's own LDS overlay (context-dependent part, Proposition 4).
-//     Rejection is monotone, so a lane stops at its first failing byte.
-//     Allowed spellings set the bits of every alias id; a lane whose LDS stack
-//     area is too small hands its spelling to the slow path.
+//     and die together; inside an item every wave takes 64-spelling sub-tiles
+//     on its own.  The lexer DFA, compact LR tables, live-terminal sets,
+//     accept lists and the row's first-byte table sit in LDS; each spelling's
+//     first 8 bytes and first alias id arrive in one 16-byte load, longer
+//     spellings' tails 16 bytes per load.  Every lane carries the allowed set
+//     of its current stack: that of sigma, that recorded after the first
+//     shift, or one computed by a set simulation after each later shift
+//     (context-dependent part, Proposition 4).  A byte that kills the DFA
+//     emits the pending lexeme as the highest-priority candidate that is
+//     allowed (or ignored) and passes the schema lexicon, then is scanned again
+//     (section 4.1, trie walk); after every byte the pending lexeme must still
+//     complete to an allowed or ignored terminal (Definition 2).  Rejection is
+//     monotone, so a lane stops at its first failing byte.  Allowed spellings
+//     set the bits of every alias id; a lane whose LDS stack area is too small
+//     hands its spelling to the slow path.
 //  3. finalize (one workgroup per row): re-walks handed-over spellings with a
 //     large stack area in the workspace, writes the row status and flags an
 //     empty mask (Proposition 8: a viable configuration has a nonempty mask).
@@ -60,20 +60,20 @@ constexpr int kStackWin = 256;       // top of the row's stack kept in LDS (prol
 constexpr int kPostCap = 14;         // overlay states recorded per first shift
 constexpr int kTmpCap = 32;          // prologue: virtual pushes of one simulation
 constexpr int kGuard = 4096;         // reduce-chain step bound
-constexpr int kAccCap = 4096;        // accept-list bytes staged in LDS by the walk
 constexpr int kSlowCap = 4096;       // spellings handed to the slow path per row
 constexpr int kSlowThreads = 64;
 constexpr int kSlowLane = 512;       // slow path per-thread stack area (workspace)
 constexpr uint32_t kRowValid = 0x600D;
-constexpr size_t kWsHead = 256;      // workspace head: the walk's work counter
+constexpr size_t kWsHead = 256;      // workspace head (reserved)
 constexpr int kMaxRounds = 257;      // set-simulation reruns (each peels one reduce group)
 
-// walk launch shape
-constexpr int kWalkThreads = 512;
-constexpr int kWalkSpt = 2;          // spellings per thread
-constexpr int kWalkTile = kWalkThreads * kWalkSpt;
+// walk launch shape: one 1024-thread workgroup per compute unit
+constexpr int kWalkThreads = 1024;
+constexpr int kSub = 64;             // spellings per wave item (one per lane)
 constexpr int kFastLane = 16;        // per-lane stack area in LDS (overlay at the bottom,
                                      // virtual pushes above it)
+constexpr int kRowGroup = 32;        // rows resident in LDS at once (at most)
+constexpr uint32_t kWalkLdsMax = 160 * 1024;
 
 struct Tables {
   const uint16_t* dfa;        // [S*C]
@@ -86,32 +86,34 @@ struct Tables {
   const uint32_t* term_info;  // [T]
   const uint32_t* pstate;     // [NS][2*tw+2]
   const uint32_t* predx;
-  const uint32_t* goff;       // [NS+1]
-  const uint32_t* gent;
+  const uint8_t* ghash;       // u32 keys [H], u16 targets [H]
   const uint32_t* spell_off;  // [U+1]
   const uint8_t* spell_bytes;
-  const uint4* spell_rec;     // [U]: head lo, head hi, first id | multi << 31, length
+  const uint4* spell_rec;     // [U]: head lo, head hi, first id | multi << 31, length | chunk << 8
+  const uint4* spell_tail;    // bytes 8.. of long spellings, 16-byte chunks
   const uint32_t* alias_off;  // [U+1]
   const int32_t* alias_ids;
   const uint16_t* lex_flags;
   const uint32_t* lex_hash;
   const uint32_t* lex_slots;
   int S, C, T, N, NS, P, U, V, W, n_slots, eos_id;
-  int tw, n_pstate, n_predx, n_gent, n_acc;
+  int tw, n_pstate, n_predx, n_acc, hbits;
 };
 
 // ---------------------------------------------------------------- workspace
 struct RowHeader {
-  uint32_t A[8];
+  uint32_t A[8];              // allowed terminals of sigma
+  uint32_t Aw[8];             // allowed terminals after shifting the winner
+  uint32_t R[8];              // terminals whose category the row's lexicon restricts
   uint32_t eos_ok;
   uint32_t valid;
   int32_t winner;             // pending lexeme's winner at an emission, -1 none
   uint32_t slow_count;
   int32_t pstat[kProGroups];  // status bits from each prologue workgroup
   int32_t wstat;              // status bits from the walk
-  uint32_t pad[11];
+  uint32_t pad[27];
 };
-static_assert(sizeof(RowHeader) == 128, "row header is 128 bytes");
+static_assert(sizeof(RowHeader) == 256, "row header is 256 bytes");
 
 struct Post {                 // stack after shifting one allowed terminal
   uint16_t k;                 // shared base entries kept
@@ -122,28 +124,22 @@ struct Post {                 // stack after shifting one allowed terminal
 static_assert(sizeof(Post) == 32, "post entry is 32 bytes");
 
 struct RowLayout {
-  size_t post, a2, vend, fb, slow, slow_ov, vend1, total;
-  size_t s_pad;  // trailing-code row stride (entries)
+  size_t post, a2, fb, slow, slow_ov, total;
 };
 
-__host__ __device__ inline RowLayout row_layout(int T, int S) {
+__host__ __device__ inline RowLayout row_layout(int T) {
   RowLayout L;
   size_t o = sizeof(RowHeader);
   L.post = o;
   o += (size_t)T * sizeof(Post);
   L.a2 = o;
   o += (size_t)T * 32;
-  L.vend = o;
-  o += ((size_t)S * 2 + 15) & ~(size_t)15;
   L.fb = o;
   o += 256 * 8;
   L.slow = o;
   o += kSlowCap * 4;
   L.slow_ov = o;
   o += (size_t)kSlowThreads * kSlowLane * 2;
-  L.s_pad = ((size_t)S + 7) & ~(size_t)7;
-  L.vend1 = o;
-  o += (size_t)T * L.s_pad * 2;
   L.total = (o + 255) & ~(size_t)255;
   return L;
 }
@@ -162,19 +158,27 @@ __device__ inline void stage16(uint8_t* dst, const uint8_t* src, uint32_t bytes,
   for (uint32_t i = (n16 << 4) + tid; i < bytes; i += nt) dst[i] = src[i];
 }
 
+// Terminal set of every terminal (not the end of input), word w.
+__device__ inline uint32_t all_word(int T, int w) {
+  const int lo = w * 32;
+  if (T >= lo + 32) return 0xFFFFFFFFu;
+  if (T <= lo) return 0u;
+  return (1u << (T - lo)) - 1u;
+}
+
 // ------------------------------------------------------- compact LR tables
 struct ParseTabs {  // pointers into LDS (or global memory)
   const uint32_t* st;
   const uint32_t* redx;
-  const uint32_t* goff;
-  const uint32_t* gent;
   const uint32_t* prod;
+  const uint32_t* gkey;
+  const uint16_t* gval;
   const uint16_t* action;  // global, dense: shift targets
-  int tw, stride, T;
+  int tw, stride, T, hbits;
 };
 
 struct ParseLds {  // byte offsets of the staged tables
-  uint32_t st, redx, goff, gent, prod, total;
+  uint32_t st, redx, prod, ghash, total;
 };
 
 __host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base) {
@@ -184,29 +188,31 @@ __host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base) {
   o += pad16((uint32_t)tb.n_pstate * 4);
   L.redx = o;
   o += pad16((uint32_t)tb.n_predx * 4);
-  L.goff = o;
-  o += pad16((uint32_t)(tb.NS + 1) * 4);
-  L.gent = o;
-  o += pad16((uint32_t)tb.n_gent * 4);
   L.prod = o;
   o += pad16((uint32_t)tb.P * 4);
+  L.ghash = o;
+  o += pad16((6u << tb.hbits));
   L.total = o - base;
   return L;
+}
+
+__device__ inline ParseTabs make_parse(const Tables& tb, const uint32_t* st, const uint32_t* redx,
+                                       const uint32_t* prod, const uint8_t* gh) {
+  return {st, redx, prod, (const uint32_t*)gh, (const uint16_t*)(gh + (4u << tb.hbits)), tb.action,
+          tb.tw, 2 * tb.tw + 2, tb.T, tb.hbits};
 }
 
 __device__ inline ParseTabs stage_parse(const Tables& tb, uint8_t* lds, const ParseLds& L, int tid, int nt) {
   stage16(lds + L.st, (const uint8_t*)tb.pstate, (uint32_t)tb.n_pstate * 4, tid, nt);
   stage16(lds + L.redx, (const uint8_t*)tb.predx, (uint32_t)tb.n_predx * 4, tid, nt);
-  stage16(lds + L.goff, (const uint8_t*)tb.goff, (uint32_t)(tb.NS + 1) * 4, tid, nt);
-  stage16(lds + L.gent, (const uint8_t*)tb.gent, (uint32_t)tb.n_gent * 4, tid, nt);
   stage16(lds + L.prod, (const uint8_t*)tb.prod, (uint32_t)tb.P * 4, tid, nt);
-  return {(const uint32_t*)(lds + L.st),   (const uint32_t*)(lds + L.redx), (const uint32_t*)(lds + L.goff),
-          (const uint32_t*)(lds + L.gent), (const uint32_t*)(lds + L.prod), tb.action,
-          tb.tw,                           2 * tb.tw + 2,                    tb.T};
+  stage16(lds + L.ghash, tb.ghash, 6u << tb.hbits, tid, nt);
+  return make_parse(tb, (const uint32_t*)(lds + L.st), (const uint32_t*)(lds + L.redx),
+                    (const uint32_t*)(lds + L.prod), lds + L.ghash);
 }
 
 __device__ inline ParseTabs global_parse(const Tables& tb) {
-  return {tb.pstate, tb.predx, tb.goff, tb.gent, tb.prod, tb.action, tb.tw, 2 * tb.tw + 2, tb.T};
+  return make_parse(tb, tb.pstate, tb.predx, tb.prod, tb.ghash);
 }
 
 struct BaseStack {  // the shared read-only stack of one row
@@ -217,9 +223,13 @@ struct BaseStack {  // the shared read-only stack of one row
 };
 
 __device__ inline uint16_t goto_of(const ParseTabs& pt, uint32_t s, uint32_t a) {
-  for (uint32_t j = pt.goff[s]; j < pt.goff[s + 1]; ++j) {
-    const uint32_t e = pt.gent[j];
-    if ((e & 0xFFFFu) == a) return (uint16_t)(e >> 16);
+  const uint32_t key = goto_key(s, a);
+  const uint32_t mask = (1u << pt.hbits) - 1u;
+  uint32_t h = goto_slot(key, pt.hbits);
+  for (uint32_t i = 0; i <= mask; ++i, h = (h + 1) & mask) {
+    const uint32_t k = pt.gkey[h];
+    if (k == key) return pt.gval[h];
+    if (k == 0) break;
   }
   return kNoGoto;
 }
@@ -270,11 +280,10 @@ __device__ int sim1_test(const ParseTabs& pt, const BaseStack& bs, uint32_t k, i
   return -1;
 }
 
-// Reduce chain of terminal x applied to (k, m, ov), then its shift.
-__device__ int sim1_shift(const ParseTabs& pt, const BaseStack& bs, uint32_t& k, int& m, uint16_t* ov, int cap,
+// Reduce chain of terminal x applied to (k, m, ov), then its shift.  1 shifted,
+// 2 accept, 0 error, -1 capacity.
+__device__ __forceinline__ int sim1_shift(const ParseTabs& pt, const BaseStack& bs, uint32_t& k, int& m, uint16_t* ov, int cap,
                           int x) {
-  const uint16_t* tmp = nullptr;  // unused by GRID_TOP with t = 0
-  (void)tmp;
   for (int guard = 0; guard < kGuard; ++guard) {
     const uint16_t s = m > 0 ? ov[m - 1] : bs.at(k - 1);
     const int a = action_of(pt, s, x);
@@ -305,10 +314,11 @@ __device__ int sim1_shift(const ParseTabs& pt, const BaseStack& bs, uint32_t& k,
 // base[0,k0) ++ ov[0,m0).  All of X runs one reduce chain; at each state the
 // shifting terminals are accepted, those reduced by one production continue
 // together, terminals of another reduce production of the same state rerun
-// from the start, the rest fail.  MW = words per set (>= tw).  0 ok, -1
-// capacity (acc is then incomplete).
+// from the start (they follow the same chain up to that state, so every rerun
+// peels off at least one group), the rest fail.  MW = words per set (>= tw).
+// 0 ok, -1 capacity (acc is then incomplete).
 template <int MW>
-__device__ int sim_set(const ParseTabs& pt, const BaseStack& bs, uint32_t k0, int m0, const uint16_t* ov,
+__device__ __forceinline__ int sim_set(const ParseTabs& pt, const BaseStack& bs, uint32_t k0, int m0, const uint16_t* ov,
                        uint16_t* tmp, int tmpcap, const uint32_t (&X)[MW], uint32_t (&acc)[MW]) {
   uint32_t todo[MW];
 #pragma unroll
@@ -384,6 +394,20 @@ __device__ int sim_set(const ParseTabs& pt, const BaseStack& bs, uint32_t k0, in
   return any ? -1 : 0;
 }
 
+// Allowed set of base[0,k) ++ ov[0,m): every terminal (not the end of input)
+// that can be shifted next.
+template <int MW>
+__device__ __forceinline__ int allowed_set(const ParseTabs& pt, const BaseStack& bs, uint32_t k, int m, const uint16_t* ov,
+                                  uint16_t* tmp, int tmpcap, uint32_t (&acc)[MW]) {
+  uint32_t X[MW];
+#pragma unroll
+  for (int w = 0; w < MW; ++w) {
+    X[w] = all_word(pt.T, w);
+    acc[w] = 0;
+  }
+  return sim_set<MW>(pt, bs, k, m, ov, tmp, tmpcap, X, acc);
+}
+
 // ---------------------------------------------------------- lexicon helpers
 struct Slot {
   uint32_t fbase, hbase, hmask, restricted, nodes;
@@ -410,32 +434,73 @@ __device__ inline uint32_t lex_flags_of(const Tables& tb, const Slot& sl, uint32
   return node == kNoLex ? 0u : tb.lex_flags[sl.fbase + node];
 }
 
-// Category c of terminal info ti restricts the lexeme in this slot.
-__device__ inline bool restricted_cat(const Slot& sl, uint32_t ti, uint32_t& c) {
-  c = (ti >> 8) & 0xFF;
-  return c != 0xFF && ((sl.restricted >> c) & 1u);
-}
+__device__ inline bool bit_of(const uint32_t* s, int t) { return (s[t >> 5] >> (t & 31)) & 1u; }
 
-// Trailing-lexeme code of DFA state q under allowed set bits8 plus the
-// ignored set I8: bit 15 = viable through an unrestricted terminal, bits
-// 0..7 = categories whose lexicon prefix test decides (Definition 2).
-__device__ inline uint16_t state_code(const Tables& tb, const Slot& sl, int q, const uint32_t* bits8,
-                                      const uint32_t* I8) {
-  uint32_t code = 0;
-  for (int wd = 0; wd < 8; ++wd) {
-    uint32_t bits = tb.live[(size_t)q * 8 + wd] & (bits8[wd] | I8[wd]);
-    while (bits) {
-      const int t = wd * 32 + __ffs(bits) - 1;
-      bits &= bits - 1;
-      uint32_t c;
-      if (restricted_cat(sl, tb.term_info[t], c)) code |= 1u << c;
-      else code |= 0x8000u;
+// What a lane needs to judge terminals: term info, ignored set I, the row's
+// restricted set R and the live-terminal sets of the lexer DFA (MW words per
+// state, stride lstride).
+struct TermView {
+  const uint32_t* tinfo;
+  const uint32_t* I;
+  const uint32_t* R;
+  const uint32_t* live;
+  int lstride;
+};
+
+// Definition 2 for a pending lexeme in DFA state q, lexicon node lex: some
+// terminal it can still complete to is allowed (acur) or ignored and, if its
+// category is restricted, the lexeme is a prefix of one of its words.
+template <int MW>
+__device__ inline bool trail_ok(const Tables& tb, const Slot& sl, const TermView& tv, const uint32_t (&acur)[MW],
+                                int q, uint32_t lex) {
+  uint32_t bits[MW], unres = 0, res = 0;
+  const uint32_t* lv = tv.live + (size_t)q * tv.lstride;
+#pragma unroll
+  for (int w = 0; w < MW; ++w) {
+    bits[w] = lv[w] & (acur[w] | tv.I[w]);
+    unres |= bits[w] & ~tv.R[w];
+    res |= bits[w] & tv.R[w];
+  }
+  if (unres) return true;
+  if (!res) return false;
+  const uint32_t lf = lex_flags_of(tb, sl, lex);
+#pragma unroll
+  for (int w = 0; w < MW; ++w) {
+    uint32_t r = bits[w] & tv.R[w];
+    while (r) {
+      const int t = w * 32 + __ffs(r) - 1;
+      r &= r - 1;
+      if ((lf >> ((tv.tinfo[t] >> 8) & 0xFFu)) & 1u) return true;
     }
   }
-  return (uint16_t)code;
+  return false;
 }
 
-__device__ inline bool code_ok(uint32_t code, uint32_t lf) { return (code & 0x8000u) || (lf & code & 0xFFu); }
+// Pending lexeme's winner at an emission: the first accept-list entry (highest
+// priority, ties to the lower id) that passes the lexicon word test and is
+// ignored or allowed.  -1 if none.
+template <int MW>
+__device__ inline int winner_of(const Tables& tb, const Slot& sl, const TermView& tv, const uint32_t* acc_off,
+                                const uint8_t* acc_list, const uint32_t (&acur)[MW], int q, uint32_t lex) {
+  uint32_t lf = 0;
+  bool have_lf = false;
+  for (uint32_t j = acc_off[q]; j < acc_off[q + 1]; ++j) {
+    const int t = acc_list[j];
+    if (bit_of(tv.R, t)) {
+      if (!have_lf) {
+        lf = lex_flags_of(tb, sl, lex);
+        have_lf = true;
+      }
+      if (!((lf >> (8 + ((tv.tinfo[t] >> 8) & 0xFFu))) & 1u)) continue;
+    }
+    bool ok = bit_of(tv.I, t);
+#pragma unroll
+    for (int w = 0; w < MW; ++w)
+      if (w == (t >> 5)) ok = ok || ((acur[w] >> (t & 31)) & 1u);
+    if (ok) return t;
+  }
+  return -1;
+}
 
 // ---------------------------------------------------------------- prologue
 template <int MW>
@@ -449,16 +514,15 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   const int grp = blockIdx.y;
   const int tid = threadIdx.x;
   __shared__ uint16_t win[kStackWin];
-  __shared__ uint32_t A[8], I[8], Aw[8], ALL[8];
+  __shared__ uint32_t A[8], I[8], R[8], Aw[8];
   __shared__ uint32_t A2s[256 * 8];
   __shared__ Post posts[256];
   __shared__ uint16_t scratch[kBlock][kPostCap + kTmpCap];
   __shared__ uint8_t glist[256];  // allowed terminals this workgroup expands
   __shared__ int nG, bad, overflow, winner;
-  if (row == 0 && grp == 0 && tid == 0) *(uint32_t*)ws = 0u;  // walk work counter
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
-  const RowLayout L = row_layout(tb.T, tb.S);
+  const RowLayout L = row_layout(tb.T);
   Post* post = (Post*)(rw + L.post);
   uint32_t* a2 = (uint32_t*)(rw + L.a2);
   const grid_config cfg = cfgs[row];
@@ -476,20 +540,6 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     overflow = 0;
     nG = 0;
     winner = -1;
-  }
-  if (tid < 8) {
-    A[tid] = 0;
-    Aw[tid] = 0;
-    uint32_t iw = 0, all = 0;
-    for (int j = 0; j < 32; ++j) {
-      const int t = tid * 32 + j;
-      if (t < tb.T) {
-        all |= 1u << j;
-        if (tb.term_info[t] & 1u) iw |= 1u << j;
-      }
-    }
-    I[tid] = iw;
-    ALL[tid] = all;
   }
   if (grp == 0)
     for (int w = tid; w < tb.W; w += kBlock) mrow[w] = 0u;
@@ -517,47 +567,45 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     }
     return;
   }
-  const BaseStack bs{pool + cfg.stk_off, win, depth, lo};
-  uint16_t* my = scratch[tid];
-
-  // A(sigma): one set simulation over every terminal
-  if (tid == 0) {
-    uint32_t X[MW], acc[MW];
-#pragma unroll
-    for (int w = 0; w < MW; ++w) {
-      X[w] = ALL[w];
-      acc[w] = 0;
-    }
-    if (sim_set<MW>(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, X, acc) < 0) overflow = 1;
-#pragma unroll
-    for (int w = 0; w < MW; ++w) A[w] = acc[w] & ALL[w];
-    // the pending lexeme's winner if a byte ends it: the highest-priority
-    // candidate that is allowed (or ignored) and passes the schema lexicon
-    if (!(cfg.flags & 1u)) {
-      const Slot sl = load_slot(tb, cfg.slot);
-      const uint32_t lf = lex_flags_of(tb, sl, cfg.lexnode);
-      for (uint32_t j = tb.acc_off[cfg.q]; j < tb.acc_off[cfg.q + 1]; ++j) {
-        const int t = tb.acc_list[j];
+  const Slot sl = load_slot(tb, cfg.slot);
+  if (tid < 8) {
+    uint32_t iw = 0, rw8 = 0;
+    for (int j = 0; j < 32; ++j) {
+      const int t = tid * 32 + j;
+      if (t < tb.T) {
         const uint32_t ti = tb.term_info[t];
-        uint32_t c;
-        const bool allowed = (ti & 1u) || ((A[t >> 5] >> (t & 31)) & 1u);
-        const bool lexok = !restricted_cat(sl, ti, c) || ((lf >> (8 + c)) & 1u);
-        if (allowed && lexok) {
-          winner = t;
-          break;
-        }
+        const uint32_t c = (ti >> 8) & 0xFFu;
+        if (ti & 1u) iw |= 1u << j;
+        if (c != 0xFFu && ((sl.restricted >> c) & 1u)) rw8 |= 1u << j;
       }
     }
-    // terminals t of A with t mod kProGroups == grp; workgroup 0 also needs
-    // the winner's stack and allowed set
-    int n = 0;
-    for (int t = grp; t < tb.T; t += kProGroups)
-      if ((A[t >> 5] >> (t & 31)) & 1u) glist[n++] = (uint8_t)t;
-    const int wt = winner;
-    if (grp == 0 && wt >= 0 && wt % kProGroups != 0 && ((A[wt >> 5] >> (wt & 31)) & 1u)) glist[n++] = (uint8_t)wt;
-    nG = n;
+    I[tid] = iw;
+    R[tid] = rw8;
+    Aw[tid] = 0;
   }
   for (int i = tid; i < 256 * 8; i += kBlock) A2s[i] = 0;
+  const BaseStack bs{pool + cfg.stk_off, win, depth, lo};
+  uint16_t* my = scratch[tid];
+  const TermView tv{tb.term_info, I, R, tb.live, 8};
+  __syncthreads();
+
+  // A(sigma): one set simulation over every terminal; then the pending
+  // lexeme's winner and this workgroup's share of A
+  if (tid == 0) {
+    uint32_t acc[MW];
+    if (allowed_set<MW>(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, acc) < 0) overflow = 1;
+#pragma unroll
+    for (int w = 0; w < MW; ++w) A[w] = acc[w];
+    for (int w = MW; w < 8; ++w) A[w] = 0;
+    int wt = -1;
+    if (!(cfg.flags & 1u)) wt = winner_of<MW>(tb, sl, tv, tb.acc_off, tb.acc_list, acc, cfg.q, cfg.lexnode);
+    winner = wt;
+    int n = 0;
+    for (int t = grp; t < tb.T; t += kProGroups)
+      if (bit_of(A, t)) glist[n++] = (uint8_t)t;
+    if (grp == 0 && wt >= 0 && wt % kProGroups != 0 && bit_of(A, wt)) glist[n++] = (uint8_t)wt;
+    nG = n;
+  }
   __syncthreads();
   // the stack after each allowed terminal's shift, then its allowed set
   for (int i = tid; i < nG; i += kBlock) {
@@ -574,30 +622,16 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     posts[t] = p;
     if (t % kProGroups == grp) post[t] = p;
     if (r == 1) {
-      uint32_t X[MW], acc[MW];
+      uint32_t acc[MW];
+      if (allowed_set<MW>(pt, bs, k, m, my, my + m, kPostCap + kTmpCap - m, acc) < 0) overflow = 1;
 #pragma unroll
-      for (int w = 0; w < MW; ++w) {
-        X[w] = ALL[w];
-        acc[w] = 0;
-      }
-      if (sim_set<MW>(pt, bs, k, m, my, my + m, kPostCap + kTmpCap - m, X, acc) < 0) overflow = 1;
-#pragma unroll
-      for (int w = 0; w < MW; ++w) A2s[t * 8 + w] = acc[w] & ALL[w];
+      for (int w = 0; w < MW; ++w) A2s[t * 8 + w] = acc[w];
     }
   }
   __syncthreads();
-  {  // allowed sets and trailing codes after this workgroup's first shifts
-    const Slot sl0 = load_slot(tb, cfg.slot);
-    uint16_t* vend1 = (uint16_t*)(rw + L.vend1);
-    for (int i = tid; i < nG * 8; i += kBlock) {
-      const int t = glist[i >> 3];
-      if (t % kProGroups == grp) a2[t * 8 + (i & 7)] = A2s[t * 8 + (i & 7)];
-    }
-    const int n = nG * tb.S;
-    for (int idx = tid; idx < n; idx += kBlock) {
-      const int t = glist[idx / tb.S], q = idx % tb.S;
-      if (t % kProGroups == grp) vend1[(size_t)t * L.s_pad + q] = state_code(tb, sl0, q, &A2s[t * 8], I);
-    }
+  for (int i = tid; i < nG * 8; i += kBlock) {
+    const int t = glist[i >> 3];
+    if (t % kProGroups == grp) a2[t * 8 + (i & 7)] = A2s[t * 8 + (i & 7)];
   }
   if (grp != 0) {
     __syncthreads();
@@ -605,25 +639,27 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     return;
   }
 
-  // ---- workgroup 0: pending lexeme, EOS gate, state codes, first-byte table
-  const Slot sl = load_slot(tb, cfg.slot);
+  // ---- workgroup 0: first-byte table, EOS gate, row header
   const bool rem_empty = (cfg.flags & 1u) != 0;
   const int w = winner;
-  const bool w_shifts = w >= 0 && !(tb.term_info[w] & 1u);
+  const bool w_shifts = w >= 0 && !bit_of(I, w);
   if (w_shifts && tid < 8) Aw[tid] = A2s[w * 8 + tid];
   __syncthreads();
-  uint16_t* vend = (uint16_t*)(rw + L.vend);
-  for (int q = tid; q < tb.S; q += kBlock) vend[q] = state_code(tb, sl, q, A, I);
-  // first-byte table
   uint2* fb = (uint2*)(rw + L.fb);
   {
     const int b = tid;  // kBlock == 256: one byte value per thread
     const uint32_t c = tb.bclass[b];
     uint32_t kind = kFbDead, q1 = 0, t1 = 0, lex1 = kNoLex;
+    uint32_t a0[MW], aw[MW];
+#pragma unroll
+    for (int k = 0; k < MW; ++k) {
+      a0[k] = A[k];
+      aw[k] = Aw[k];
+    }
     const int nq = tb.dfa[(size_t)cfg.q * tb.C + c];
     if (nq != kDead) {
       lex1 = lex_child(tb, sl, cfg.lexnode, b);
-      if (code_ok(state_code(tb, sl, nq, A, I), lex_flags_of(tb, sl, lex1))) {
+      if (trail_ok<MW>(tb, sl, tv, a0, nq, lex1)) {
         kind = kFbMode0;
         q1 = nq;
       }
@@ -631,17 +667,16 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
       const int sq = tb.dfa[(size_t)kStart * tb.C + c];
       if (sq != kDead) {
         lex1 = lex_child(tb, sl, 0u, b);
-        const uint32_t lf1 = lex_flags_of(tb, sl, lex1);
         if (!w_shifts) {
-          if (code_ok(state_code(tb, sl, sq, A, I), lf1)) kind = kFbMode0;
-        } else if (code_ok(state_code(tb, sl, sq, Aw, I), lf1)) {
+          if (trail_ok<MW>(tb, sl, tv, a0, sq, lex1)) kind = kFbMode0;
+        } else if (trail_ok<MW>(tb, sl, tv, aw, sq, lex1)) {
           kind = kFbMode1;
           t1 = (uint32_t)w;
         }
         q1 = sq;
       }
     }
-    if (kind == kFbDead) lex1 = kNoLex;
+    if (kind == kFbDead || sl.restricted == 0) lex1 = kNoLex;
     fb[b] = make_uint2(q1 | kind << 16 | t1 << 24, lex1);
   }
   // end-of-sequence gate (mid-lexeme aware)
@@ -651,14 +686,18 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
       ok = sim1_test(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, tb.T) == 2;
     } else if (w >= 0) {
       const Post& p = posts[w];
-      ok = sim1_test(pt, bs, p.k, p.m, p.ov, my, kPostCap + kTmpCap, tb.T) == 2;
+      ok = p.ok && sim1_test(pt, bs, p.k, p.m, p.ov, my, kPostCap + kTmpCap, tb.T) == 2;
     }
     hdr->eos_ok = (uint32_t)ok;
     if (eos_out) eos_out[row] = (uint8_t)ok;
     if (ok && tb.eos_id >= 0) mrow[tb.eos_id >> 5] |= 1u << (tb.eos_id & 31);
   }
   __syncthreads();
-  if (tid < 8) hdr->A[tid] = A[tid];
+  if (tid < 8) {
+    hdr->A[tid] = A[tid];
+    hdr->Aw[tid] = Aw[tid];
+    hdr->R[tid] = R[tid];
+  }
   if (tid == 0) {
     hdr->winner = w;
     hdr->slow_count = 0;
@@ -669,13 +708,15 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
 }
 
 // ------------------------------------------------------- lane machinery
-// Lane state after at least one byte: the stack is sigma (mode 0), the stack
-// after the first shift t1 (mode 1), or base[0,k) ++ ov[0,m) (mode 2).
-struct LaneState {
+// A lane's stack is sigma (mode 0), the stack after the first shift t1
+// (mode 1), or base[0,k) ++ ov[0,m) (mode 2); acur is its allowed set.
+template <int MW>
+struct Lane {
   int mode;
   int t1;
   uint32_t k;
   int m;
+  uint32_t acur[MW];
 };
 
 struct RowCtx {
@@ -683,130 +724,39 @@ struct RowCtx {
   ParseTabs pt;
   BaseStack bs;
   Slot sl;
-  const uint32_t* A;        // allowed set of sigma (8 words)
-  const uint32_t* I;        // ignored terminals (8 words)
-  const uint32_t* a2;       // row's A2 table (global)
-  const Post* post;         // row's post table (global)
-  const uint32_t* tinfo;    // terminal info (LDS or global)
+  TermView tv;
   const uint32_t* acc_off;  // accept-list offsets (LDS or global)
   const uint8_t* acc_list;  // accept lists (LDS or global)
-  const uint16_t* vend0;    // trailing codes under A(sigma)
-  const uint16_t* vendw;    // trailing codes after the row winner's shift
-  const uint16_t* vend1;    // trailing codes after each first shift, [T][s_pad] (global)
-  size_t s_pad;
-  int winner;
+  const uint32_t* a2;       // row's allowed sets after each first shift (global)
+  const Post* post;         // row's stacks after each first shift (global)
 };
 
-// Trailing-code row for a lane in mode 0 or 1.
-__device__ inline const uint16_t* code_row(const RowCtx& rc, const LaneState& st) {
-  if (st.mode == 0) return rc.vend0;
-  if (st.t1 == rc.winner) return rc.vendw;
-  return rc.vend1 + (size_t)st.t1 * rc.s_pad;
-}
-
-// Emits the pending lexeme in DFA state q (lexicon flags lf).  ov is the
+// Emits the pending lexeme in DFA state q (lexicon node lex).  ov is the
 // lane's stack area of cap entries: the overlay occupies [0, m), virtual
 // pushes use [m, cap).  1 ok, 0 reject, -1 capacity.
 template <int MW>
-__device__ int emit_general(const RowCtx& rc, LaneState& st, uint16_t* ov, int cap, int q, uint32_t lf) {
-  const uint32_t a0 = rc.acc_off[q], a1 = rc.acc_off[q + 1];
-  if (a0 == a1) return 0;
-  uint32_t acc[MW];
+__device__ __forceinline__ int emit(const RowCtx& rc, Lane<MW>& ln, uint16_t* ov, int cap, int q, uint32_t lex) {
+  const int t = winner_of<MW>(*rc.tb, rc.sl, rc.tv, rc.acc_off, rc.acc_list, ln.acur, q, lex);
+  if (t < 0) return 0;
+  if (bit_of(rc.tv.I, t)) return 1;  // ignored: the stack is unchanged
+  if (ln.mode == 0) {
+    ln.mode = 1;
+    ln.t1 = t;
 #pragma unroll
-  for (int w = 0; w < MW; ++w) acc[w] = 0;
-  if (st.mode == 2) {  // one set simulation over the non-ignored candidates
-    uint32_t X[MW];
-#pragma unroll
-    for (int w = 0; w < MW; ++w) X[w] = 0;
-    for (uint32_t j = a0; j < a1; ++j) {
-      const int t = rc.acc_list[j];
-      const uint32_t ti = rc.tinfo[t];
-      uint32_t c;
-      if ((ti & 1u) || (restricted_cat(rc.sl, ti, c) && !((lf >> (8 + c)) & 1u))) continue;
-#pragma unroll
-      for (int w = 0; w < MW; ++w)
-        if (w == (t >> 5)) X[w] |= 1u << (t & 31);
-    }
-    if (sim_set<MW>(rc.pt, rc.bs, st.k, st.m, ov, ov + st.m, cap - st.m, X, acc) < 0) return -1;
-  }
-  int winner = -1;
-  for (uint32_t j = a0; j < a1; ++j) {
-    const int t = rc.acc_list[j];
-    const uint32_t ti = rc.tinfo[t];
-    uint32_t c;
-    if (restricted_cat(rc.sl, ti, c) && !((lf >> (8 + c)) & 1u)) continue;
-    bool ok;
-    if (ti & 1u) ok = true;
-    else if (st.mode == 0) ok = (rc.A[t >> 5] >> (t & 31)) & 1u;
-    else if (st.mode == 1) ok = (rc.a2[st.t1 * 8 + (t >> 5)] >> (t & 31)) & 1u;
-    else {
-      ok = false;
-#pragma unroll
-      for (int w = 0; w < MW; ++w)
-        if (w == (t >> 5)) ok = (acc[w] >> (t & 31)) & 1u;
-    }
-    if (ok) {
-      winner = t;
-      break;
-    }
-  }
-  if (winner < 0) return 0;
-  if (rc.tinfo[winner] & 1u) return 1;  // ignored: the stack is unchanged
-  if (st.mode == 0) {
-    st.mode = 1;
-    st.t1 = winner;
+    for (int w = 0; w < MW; ++w) ln.acur[w] = rc.a2[t * 8 + w];
     return 1;
   }
-  if (st.mode == 1) {
-    const Post& p = rc.post[st.t1];
-    if (p.k == 0 || p.k > rc.bs.depth || p.m > kPostCap || p.m > cap) return -1;
-    st.k = p.k;
-    st.m = p.m;
-    for (int j = 0; j < st.m; ++j) ov[j] = p.ov[j];
-    st.mode = 2;
+  if (ln.mode == 1) {
+    const Post& p = rc.post[ln.t1];
+    if (!p.ok || p.k == 0 || p.k > rc.bs.depth || p.m > kPostCap || p.m > cap) return -1;
+    ln.k = p.k;
+    ln.m = p.m;
+    for (int j = 0; j < ln.m; ++j) ov[j] = p.ov[j];
+    ln.mode = 2;
   }
-  const int r = sim1_shift(rc.pt, rc.bs, st.k, st.m, ov, cap, winner);
-  return r < 0 ? -1 : (r == 1);
-}
-
-// Trailing test of Definition 2 in any lane state.  -1: capacity.
-template <int MW>
-__device__ int trailing_any(const RowCtx& rc, const LaneState& st, uint16_t* ov, int cap, int q, uint32_t lex) {
-  const Tables& tb = *rc.tb;
-  if (st.mode <= 1) {
-    const uint32_t code = code_row(rc, st)[q];
-    if (code & 0x8000u) return 1;
-    if (!(code & 0xFFu)) return 0;
-    return (lex_flags_of(tb, rc.sl, lex) & code & 0xFFu) != 0;
-  }
-  const uint32_t lf = lex_flags_of(tb, rc.sl, lex);
-  uint32_t X[MW], any = 0;
-#pragma unroll
-  for (int w = 0; w < MW; ++w) {
-    uint32_t bits = tb.live[(size_t)q * 8 + w];
-    uint32_t keep = 0;
-    while (bits) {
-      const int b = __ffs(bits) - 1;
-      bits &= bits - 1;
-      const int t = w * 32 + b;
-      const uint32_t ti = rc.tinfo[t];
-      uint32_t c;
-      if (restricted_cat(rc.sl, ti, c) && !((lf >> c) & 1u)) continue;
-      if (ti & 1u) return 1;
-      keep |= 1u << b;
-    }
-    X[w] = keep;
-    any |= keep;
-  }
-  if (!any) return 0;
-  uint32_t acc[MW];
-#pragma unroll
-  for (int w = 0; w < MW; ++w) acc[w] = 0;
-  if (sim_set<MW>(rc.pt, rc.bs, st.k, st.m, ov, ov + st.m, cap - st.m, X, acc) < 0) return -1;
-  uint32_t hit = 0;
-#pragma unroll
-  for (int w = 0; w < MW; ++w) hit |= acc[w] & X[w];
-  return hit != 0;
+  const int r = sim1_shift(rc.pt, rc.bs, ln.k, ln.m, ov, cap, t);
+  if (r != 1) return r < 0 ? -1 : 0;
+  return allowed_set<MW>(rc.pt, rc.bs, ln.k, ln.m, ov, ov + ln.m, cap - ln.m, ln.acur) < 0 ? -1 : 1;
 }
 
 __device__ inline void set_alias_bits(const Tables& tb, uint32_t* mrow, int u) {
@@ -824,39 +774,51 @@ struct DfaView {  // lexer DFA by byte class (LDS copy or global)
   __device__ int next(int q, uint32_t c) const { return next_[q * C + c]; }
 };
 
-// Walks the bytes [i, n) of one spelling from lane state (st, q, lex).
-// byte_at(i) yields byte i.  1 allowed, 0 rejected, -1 capacity.
+// Walks the bytes [i, n) of one spelling from lane state (ln, q, lex); lex
+// is kNoLex throughout when the row's lexicon restricts nothing.  byte_at(i)
+// yields byte i.  1 allowed, 0 rejected, -1 capacity.
 template <int MW, class ByteAt>
-__device__ inline int walk_bytes(const RowCtx& rc, LaneState& st, int q, uint32_t lex, uint32_t i, uint32_t n,
-                                 ByteAt byte_at, const DfaView& step, uint16_t* ov, int cap) {
+__device__ __forceinline__ int walk_bytes(const RowCtx& rc, Lane<MW>& ln, int q, uint32_t lex, uint32_t i,
+                                          uint32_t n, ByteAt byte_at, const DfaView& step, uint16_t* ov, int cap) {
   const Tables& tb = *rc.tb;
+  const bool track = rc.sl.restricted != 0;
   for (; i < n; ++i) {
     const uint32_t b = byte_at(i);
     const uint32_t c = step.cls(b);
     const int nq = step.next(q, c);
     if (nq != kDead) {
       q = nq;
-      if (lex != kNoLex) lex = lex_child(tb, rc.sl, lex, b);
+      lex = lex_child(tb, rc.sl, lex, b);
     } else {
-      const int r = emit_general<MW>(rc, st, ov, cap, q, lex_flags_of(tb, rc.sl, lex));
+      const int r = emit<MW>(rc, ln, ov, cap, q, lex);
       if (r <= 0) return r;
       q = step.next(kStart, c);
       if (q == kDead) return 0;
-      lex = lex_child(tb, rc.sl, 0u, b);
+      lex = track ? lex_child(tb, rc.sl, 0u, b) : kNoLex;
     }
-    const int r = trailing_any<MW>(rc, st, ov, cap, q, lex);
-    if (r <= 0) return r;
+    if (!trail_ok<MW>(tb, rc.sl, rc.tv, ln.acur, q, lex)) return 0;
   }
   return 1;
 }
 
 // -------------------------------------------------------------------- walk
+// Per-row data a walk workgroup keeps in LDS for every row of its group.
+struct RowLds {
+  uint32_t A[8], Aw[8], R[8];
+  uint32_t valid;
+  uint32_t stk_off, stk_depth;
+  uint32_t slot;
+  uint32_t pad[4];
+};
+static_assert(sizeof(RowLds) == 128, "row record is 128 bytes");
+
 struct WalkLds {  // byte offsets into dynamic LDS
-  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, fb, vend0, vendw, lanes, total, vstride;
+  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, live, lanes, rows, fb, total;
+  int group;  // rows per group
   ParseLds pl;
 };
 
-__host__ __device__ inline WalkLds walk_lds(const Tables& tb) {
+__host__ __device__ inline WalkLds walk_lds(const Tables& tb, int mw, int B) {
   WalkLds w;
   uint32_t o = 0;
   w.dfa = o;
@@ -874,40 +836,80 @@ __host__ __device__ inline WalkLds walk_lds(const Tables& tb) {
   w.parse = o;
   w.pl = parse_lds(tb, o);
   o += w.pl.total;
-  w.fb = o;
-  o += 256 * 8;
-  w.vstride = pad16((uint32_t)((tb.S + 7) & ~7) * 2);
-  w.vend0 = o;
-  o += w.vstride;
-  w.vendw = o;
-  o += w.vstride;
+  w.live = o;
+  o += pad16((uint32_t)(tb.S * mw * 4));
   w.lanes = o;
   o += kWalkThreads * kFastLane * 2;
+  // as many rows as fit, at most kRowGroup and B
+  const uint32_t per_row = sizeof(RowLds) + 256 * 8;
+  int g = kRowGroup < B ? kRowGroup : B;
+  while (g > 1 && o + per_row * (uint32_t)g > kWalkLdsMax) --g;
+  w.group = g;
+  w.rows = o;
+  o += sizeof(RowLds) * (uint32_t)g;
+  w.fb = o;
+  o += 256 * 8 * (uint32_t)g;
   w.total = o;
   return w;
 }
 
-// Persistent: each workgroup stages the grammar tables once, then takes work
-// items (row x spelling tile) from a counter in the workspace head.
+// Bytes 1, 2, ... of one spelling, called in that order: a 64-bit window
+// holds the next bytes, taken from the record (bytes 0..7), the first tail
+// chunk fetched with the record (bytes 8..23), then one 16-byte load per
+// further tail chunk.
+struct SpellBytes {
+  uint64_t win;       // next bytes, lowest first
+  uint64_t lo0, hi;   // bytes 8..15, and the second half of the current tail chunk
+  const uint4* tail;  // chunk c holds bytes 8 + 16c .. 23 + 16c
+  __device__ uint32_t operator()(uint32_t i) {
+    if (i >= 8 && (i & 7) == 0) {
+      if (i == 8) {
+        win = lo0;
+      } else if ((i & 15) == 0) {
+        win = hi;
+      } else {
+        const uint4 c = tail[(i - 8) >> 4];
+        win = (uint64_t)c.x | (uint64_t)c.y << 32;
+        hi = (uint64_t)c.z | (uint64_t)c.w << 32;
+      }
+    }
+    const uint32_t b = (uint32_t)win & 0xFFu;
+    win >>= 8;
+    return b;
+  }
+};
+
+__device__ inline int wave_grab(int* ctr) {
+  int v = 0;
+  if ((threadIdx.x & 63) == 0) v = atomicAdd(ctr, 1);
+  return __builtin_amdgcn_readfirstlane(v);
+}
+
+// Persistent, one workgroup per compute unit.  The grammar tables are staged
+// once; then, for each group of up to kRowGroup rows, the rows' first-byte
+// tables and scalars are staged and the workgroup's share of the (row,
+// 64-spelling sub-tile) items -- every gridDim.x-th item in row-major order,
+// so each workgroup sees every row and all of the vocabulary -- is taken by
+// its waves one item at a time from an LDS counter, with no barrier between
+// items.
 template <int MW>
 __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const grid_config* __restrict__ cfgs,
                                                             const uint16_t* __restrict__ pool,
                                                             uint32_t* __restrict__ mask,
-                                                            uint8_t* __restrict__ ws, size_t rbytes, int B,
-                                                            int n_tiles, int n_items) {
+                                                            uint8_t* __restrict__ ws, size_t rbytes, int B) {
   extern __shared__ __align__(16) uint8_t lds[];
-  __shared__ int item_s;
-  __shared__ uint32_t A_s[8];
-  __shared__ int winner_s;
+  __shared__ int item_ctr;
   const int tid = threadIdx.x;
-  const WalkLds WL = walk_lds(tb);
-  const RowLayout RL = row_layout(tb.T, tb.S);
+  const int lane = tid & 63;
+  const WalkLds WL = walk_lds(tb, MW, B);
+  const RowLayout RL = row_layout(tb.T);
   uint8_t* bcls = lds + WL.bcls;
   uint32_t* tinfo_s = (uint32_t*)(lds + WL.tinfo);
   uint32_t* I_s = (uint32_t*)(lds + WL.I);
-  uint2* fb_s = (uint2*)(lds + WL.fb);
-  uint16_t* lane = (uint16_t*)(lds + WL.lanes) + tid * kFastLane;
-  uint32_t* counter = (uint32_t*)ws;
+  uint32_t* live_s = (uint32_t*)(lds + WL.live);
+  RowLds* rows_s = (RowLds*)(lds + WL.rows);
+  const uint2* fb_all = (const uint2*)(lds + WL.fb);
+  uint16_t* lane_area = (uint16_t*)(lds + WL.lanes) + tid * kFastLane;
   uint8_t* rows = ws + kWsHead;
 
   // grammar tables, once per workgroup
@@ -916,6 +918,7 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
   stage16(lds + WL.acc_off, (const uint8_t*)tb.acc_off, (uint32_t)(tb.S + 1) * 4, tid, kWalkThreads);
   stage16(lds + WL.acc_list, tb.acc_list, (uint32_t)tb.n_acc, tid, kWalkThreads);
   const ParseTabs pt = stage_parse(tb, lds, WL.pl, tid, kWalkThreads);
+  for (int i = tid; i < tb.S * MW; i += kWalkThreads) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
   for (int t = tid; t < 256; t += kWalkThreads) tinfo_s[t] = t < tb.T ? tb.term_info[t] : 0u;
   __syncthreads();
   if (tid < 8) {
@@ -927,82 +930,102 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
 
   const DfaView step{(const uint16_t*)(lds + WL.dfa), bcls, tb.C};
   const uint4* recs = tb.spell_rec;
-  for (;;) {
-    __syncthreads();  // the previous item is done with the row tables
-    if (tid == 0) item_s = (int)atomicAdd(counter, 1u);
-    __syncthreads();
-    const int item = item_s;
-    if (item >= n_items) break;
-    const int row = item / n_tiles;
-    const int tile = item % n_tiles;
-    uint8_t* rw = rows + (size_t)row * rbytes;
-    RowHeader* hdr = (RowHeader*)rw;
-    if (hdr->valid != kRowValid) continue;  // uniform across the workgroup
-    const int w = hdr->winner;
-    const bool w_shifts = w >= 0 && !(tinfo_s[w] & 1u);
-    stage16((uint8_t*)fb_s, rw + RL.fb, 256 * 8, tid, kWalkThreads);
-    stage16(lds + WL.vend0, rw + RL.vend, WL.vstride, tid, kWalkThreads);
-    if (w_shifts)
-      stage16(lds + WL.vendw, rw + RL.vend1 + (size_t)w * RL.s_pad * 2, WL.vstride, tid, kWalkThreads);
-    if (tid < 8) A_s[tid] = hdr->A[tid];
-    if (tid == 0) winner_s = w_shifts ? w : -1;
-    __syncthreads();
-
-    // this thread's spellings in the tile
-    static_assert(kWalkSpt == 2, "two spelling records per thread");
-    const int ubase = tile * kWalkTile + tid;
-    const uint4 rec0 = ubase < tb.U ? recs[ubase] : make_uint4(0, 0, 0, 0);
-    const uint4 rec1 = ubase + kWalkThreads < tb.U ? recs[ubase + kWalkThreads] : make_uint4(0, 0, 0, 0);
-    const grid_config cfg = cfgs[row];
-    RowCtx rc;
-    rc.tb = &tb;
-    rc.pt = pt;
-    rc.bs = BaseStack{pool + cfg.stk_off, nullptr, cfg.stk_depth, cfg.stk_depth};
-    rc.sl = load_slot(tb, cfg.slot);
-    rc.A = A_s;
-    rc.I = I_s;
-    rc.a2 = (const uint32_t*)(rw + RL.a2);
-    rc.post = (const Post*)(rw + RL.post);
-    rc.tinfo = tinfo_s;
-    rc.acc_off = (const uint32_t*)(lds + WL.acc_off);
-    rc.acc_list = lds + WL.acc_list;
-    rc.vend0 = (const uint16_t*)(lds + WL.vend0);
-    rc.vendw = (const uint16_t*)(lds + WL.vendw);
-    rc.vend1 = (const uint16_t*)(rw + RL.vend1);
-    rc.s_pad = RL.s_pad;
-    rc.winner = winner_s;
-    uint32_t* mrow = mask + (size_t)row * tb.W;
-    int handoff = 0;
-
-#pragma unroll 1
-    for (int k = 0; k < kWalkSpt; ++k) {
-      const uint4 rk = k == 0 ? rec0 : rec1;
-      const uint32_t n = rk.w;
-      if (n == 0) continue;
-      const uint64_t h = (uint64_t)rk.x | (uint64_t)rk.y << 32;
-      const uint2 e = fb_s[h & 0xFF];
-      const uint32_t kind = (e.x >> 16) & 3u;
-      if (kind == kFbDead) continue;
-      const int u = ubase + k * kWalkThreads;
-      LaneState st{(int)kind - 1, (int)(e.x >> 24), 0, 0};
-      uint32_t off = 0;
-      auto byte_at = [&](uint32_t i) -> uint32_t {
-        if (i < 8) return (uint32_t)(h >> (8 * i)) & 0xFFu;
-        if (i == 8) off = tb.spell_off[u];
-        return tb.spell_bytes[off + i];
-      };
-      const int ok = walk_bytes<MW>(rc, st, (int)(e.x & 0xFFFF), e.y, 1u, n, byte_at, step, lane, kFastLane);
-      if (ok > 0) {
-        const uint32_t id = rk.z;
-        if (!(id >> 31)) atomicOr(&mrow[id >> 5], 1u << (id & 31));
-        else set_alias_bits(tb, mrow, u);
-      } else if (ok < 0) {  // the lane's stack area is too small: hand over
-        const uint32_t slot = atomicAdd(&hdr->slow_count, 1u);
-        if (slot < (uint32_t)kSlowCap) ((uint32_t*)(rw + RL.slow))[slot] = (uint32_t)u;
-        else handoff = 1;
-      }
+  const int nsub = (tb.U + kSub - 1) / kSub;
+  for (int g0 = 0; g0 < B; g0 += WL.group) {
+    const int gr = min(WL.group, B - g0);
+    __syncthreads();  // the previous group is done with the row tables
+    for (int r = 0; r < gr; ++r) {
+      const uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
+      stage16((uint8_t*)(fb_all + r * 256), rw + RL.fb, 256 * 8, tid, kWalkThreads);
     }
-    if (handoff) atomicOr(&hdr->wstat, GRID_ROW_OVERFLOW);
+    for (int r = tid; r < gr; r += kWalkThreads) {
+      const RowHeader* hdr = (const RowHeader*)(rows + (size_t)(g0 + r) * rbytes);
+      const grid_config cfg = cfgs[g0 + r];
+      RowLds& rl = rows_s[r];
+      for (int w = 0; w < 8; ++w) {
+        rl.A[w] = hdr->A[w];
+        rl.Aw[w] = hdr->Aw[w];
+        rl.R[w] = hdr->R[w];
+      }
+      rl.valid = hdr->valid;
+      rl.stk_off = cfg.stk_off;
+      rl.stk_depth = cfg.stk_depth;
+      rl.slot = cfg.slot;
+    }
+    if (tid == 0) item_ctr = 0;
+    __syncthreads();
+
+    // this workgroup's items: j = blockIdx.x + k * gridDim.x, row j / nsub,
+    // sub-tile j % nsub.  Two deep: while item k0 is walked, the record of
+    // k2 and the first tail chunk of k1 (whose record has arrived) are in
+    // flight.
+    const int total = gr * nsub;
+    auto rec_of = [&](int k) -> uint4 {
+      const int j = blockIdx.x + k * gridDim.x;
+      const int uu = (j % nsub) * kSub + lane;
+      return recs[(j < total && uu < tb.U) ? uu : 0];
+    };
+    int k0 = wave_grab(&item_ctr);
+    int k1 = wave_grab(&item_ctr);
+    uint4 rk0 = rec_of(k0);
+    uint4 rk1 = rec_of(k1);
+    uint4 tl0 = tb.spell_tail[rk0.w >> 8];
+    for (;;) {
+      const int j0 = blockIdx.x + k0 * gridDim.x;
+      if (j0 >= total) break;
+      const int k2 = wave_grab(&item_ctr);
+      const uint4 rk2 = rec_of(k2);
+      const uint4 tl1 = tb.spell_tail[rk1.w >> 8];
+      const int r = j0 / nsub;
+      const int u = (j0 - r * nsub) * kSub + lane;
+      const RowLds& rl = rows_s[r];
+      const uint32_t n = (u < tb.U) ? (rk0.w & 0xFFu) : 0u;
+      const uint64_t h = (uint64_t)rk0.x | (uint64_t)rk0.y << 32;
+      const uint2 e = fb_all[r * 256 + (h & 0xFF)];
+      const uint32_t kind = (e.x >> 16) & 3u;
+      if (rl.valid == kRowValid && n != 0 && kind != kFbDead) {
+        uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
+        RowCtx rc;
+        rc.tb = &tb;
+        rc.pt = pt;
+        rc.bs = BaseStack{pool + rl.stk_off, nullptr, rl.stk_depth, rl.stk_depth};
+        rc.sl = load_slot(tb, rl.slot);
+        rc.tv = TermView{tinfo_s, I_s, rl.R, live_s, MW};
+        rc.acc_off = (const uint32_t*)(lds + WL.acc_off);
+        rc.acc_list = lds + WL.acc_list;
+        rc.a2 = (const uint32_t*)(rw + RL.a2);
+        rc.post = (const Post*)(rw + RL.post);
+        Lane<MW> ln;
+        ln.mode = (int)kind - 1;
+        ln.t1 = (int)(e.x >> 24);
+        ln.k = 0;
+        ln.m = 0;
+#pragma unroll
+        for (int w = 0; w < MW; ++w) ln.acur[w] = kind == kFbMode0 ? rl.A[w] : rl.Aw[w];
+        SpellBytes byte_at;
+        byte_at.win = h >> 8;
+        byte_at.lo0 = (uint64_t)tl0.x | (uint64_t)tl0.y << 32;
+        byte_at.hi = (uint64_t)tl0.z | (uint64_t)tl0.w << 32;
+        byte_at.tail = tb.spell_tail + (rk0.w >> 8);
+        const int ok = walk_bytes<MW>(rc, ln, (int)(e.x & 0xFFFF), e.y, 1u, n, byte_at, step, lane_area, kFastLane);
+        uint32_t* mrow = mask + (size_t)(g0 + r) * tb.W;
+        if (ok > 0) {
+          const uint32_t id = rk0.z;
+          if (!(id >> 31)) atomicOr(&mrow[id >> 5], 1u << (id & 31));
+          else set_alias_bits(tb, mrow, u);
+        } else if (ok < 0) {  // the lane's stack area is too small: hand over
+          RowHeader* hdr = (RowHeader*)rw;
+          const uint32_t slot = atomicAdd(&hdr->slow_count, 1u);
+          if (slot < (uint32_t)kSlowCap) ((uint32_t*)(rw + RL.slow))[slot] = (uint32_t)u;
+          else atomicOr(&hdr->wstat, GRID_ROW_OVERFLOW);
+        }
+      }
+      k0 = k1;
+      rk0 = rk1;
+      tl0 = tl1;
+      k1 = k2;
+      rk1 = rk2;
+    }
   }
 }
 
@@ -1020,7 +1043,7 @@ __global__ __launch_bounds__(kSlowThreads) void finalize_kernel(Tables tb, const
   const int tid = threadIdx.x;
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
-  const RowLayout RL = row_layout(tb.T, tb.S);
+  const RowLayout RL = row_layout(tb.T);
   uint32_t* mrow = mask + (size_t)row * tb.W;
   __shared__ uint32_t any;
   __shared__ int slow_err;
@@ -1049,26 +1072,26 @@ __global__ __launch_bounds__(kSlowThreads) void finalize_kernel(Tables tb, const
     rc.pt = pt;
     rc.bs = BaseStack{pool + cfg.stk_off, nullptr, cfg.stk_depth, cfg.stk_depth};
     rc.sl = load_slot(tb, cfg.slot);
-    rc.A = hdr->A;
-    rc.I = I_s;
-    rc.a2 = (const uint32_t*)(rw + RL.a2);
-    rc.post = (const Post*)(rw + RL.post);
-    rc.tinfo = tb.term_info;
+    rc.tv = TermView{tb.term_info, I_s, hdr->R, tb.live, 8};
     rc.acc_off = tb.acc_off;
     rc.acc_list = tb.acc_list;
-    rc.vend0 = (const uint16_t*)(rw + RL.vend);
-    rc.vend1 = (const uint16_t*)(rw + RL.vend1);
-    rc.s_pad = RL.s_pad;
-    rc.winner = -1;  // every mode-1 lane reads its own trailing-code row
-    rc.vendw = rc.vend1;
+    rc.a2 = (const uint32_t*)(rw + RL.a2);
+    rc.post = (const Post*)(rw + RL.post);
     uint16_t* ov = (uint16_t*)(rw + RL.slow_ov) + tid * kSlowLane;
     const DfaView step{tb.dfa, tb.bclass, tb.C};
+    const uint32_t lex0 = rc.sl.restricted != 0 ? cfg.lexnode : kNoLex;
     for (uint32_t k = tid; k < count; k += kSlowThreads) {
       const int u = (int)((const uint32_t*)(rw + RL.slow))[k];
-      LaneState st{0, -1, 0, 0};
+      Lane<MW> ln;
+      ln.mode = 0;
+      ln.t1 = -1;
+      ln.k = 0;
+      ln.m = 0;
+#pragma unroll
+      for (int w = 0; w < MW; ++w) ln.acur[w] = hdr->A[w];
       const uint32_t base = tb.spell_off[u];
       auto byte_at = [&](uint32_t i) -> uint32_t { return tb.spell_bytes[base + i]; };
-      const int ok = walk_bytes<MW>(rc, st, cfg.q, cfg.lexnode, 0u, tb.spell_off[u + 1] - base, byte_at, step, ov,
+      const int ok = walk_bytes<MW>(rc, ln, cfg.q, lex0, 0u, tb.spell_off[u + 1] - base, byte_at, step, ov,
                                     kSlowLane);
       if (ok > 0) set_alias_bits(tb, mrow, u);
       if (ok < 0) slow_err = 1;
@@ -1132,40 +1155,62 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(const uint32_t* __restric
 
 bool bound(const grid_compiled* g, int which) { return g->dev[which] != nullptr || g->dev_bytes[which] == 0; }
 
-// Resident walk workgroups per device (compute units x occupancy), cached.
-template <int MW>
-int walk_grid_size(size_t lds) {
-  static int cached[64] = {0};
+// Raises a kernel's dynamic-LDS limit (needed above 64 KB of LDS in total)
+// once per kernel, device and size.
+bool raise_lds(const void* fn, uint32_t bytes) {
+  struct Entry {
+    const void* fn;
+    int dev;
+    uint32_t bytes;
+  };
+  static Entry done[64];
+  static int n_done = 0;
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
-  if (cached[dev] > 0) return cached[dev];
-  int cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  for (int i = 0; i < n_done; ++i)
+    if (done[i].fn == fn && done[i].dev == dev && done[i].bytes >= bytes) return true;
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) != hipSuccess) return false;
+  if (n_done < 64) done[n_done++] = {fn, dev, bytes};
+  return true;
+}
+
+// Resident walk workgroups on the current device (compute units x
+// occupancy) for an LDS size; raises the kernel's LDS limit first.
+template <int MW>
+int walk_grid_size(uint32_t lds) {
+  if (!raise_lds((const void*)walk_kernel<MW>, lds)) return -1;
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -1;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, walk_kernel<MW>, kWalkThreads, lds) != hipSuccess ||
       per_cu <= 0)
     per_cu = 1;
-  cached[dev] = cus * per_cu;
-  return cached[dev];
+  return cus * per_cu;
 }
 
 template <int MW>
-void launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint16_t* pool, uint32_t* mask,
-                 uint8_t* eos, int32_t* status, uint8_t* ws, size_t rb, uint32_t phases, hipStream_t s) {
+int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint16_t* pool, uint32_t* mask,
+                uint8_t* eos, int32_t* status, uint8_t* ws, size_t rb, uint32_t phases, hipStream_t s) {
   const uint32_t parse_bytes = parse_lds(tb, 0).total;
+  if (!raise_lds((const void*)prologue_kernel<MW>, parse_bytes) ||
+      !raise_lds((const void*)finalize_kernel<MW>, parse_bytes))
+    return fail(GRID_E_HIP, "grid_mask: cannot raise the LDS limit");
   if (phases & GRID_PHASE_PROLOGUE)
     hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B, kProGroups), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool,
                        mask, eos, ws, rb);
   if ((phases & GRID_PHASE_WALK) && tb.U > 0) {
-    const WalkLds WL = walk_lds(tb);
-    const int n_tiles = (tb.U + kWalkTile - 1) / kWalkTile;
-    const int n_items = n_tiles * B;
-    const int blocks = std::min(n_items, walk_grid_size<MW>(WL.total));
+    const WalkLds WL = walk_lds(tb, MW, B);
+    const int n_items = ((tb.U + kSub - 1) / kSub) * std::min(B, WL.group);
+    const int resident = walk_grid_size<MW>(WL.total);
+    if (resident <= 0) return fail(GRID_E_HIP, "grid_mask: cannot raise the walk's LDS limit");
+    const int blocks = std::min((n_items + kWalkThreads / 64 - 1) / (kWalkThreads / 64), resident);
     hipLaunchKernelGGL(walk_kernel<MW>, dim3(blocks), dim3(kWalkThreads), WL.total, s, tb, cfg_dev, pool, mask, ws,
-                       rb, B, n_tiles, n_items);
+                       rb, B);
   }
   if (phases & GRID_PHASE_FINALIZE)
     hipLaunchKernelGGL(finalize_kernel<MW>, dim3(B), dim3(kSlowThreads), parse_bytes, s, tb, cfg_dev, pool, mask,
                        ws, rb, status);
+  return GRID_OK;
 }
 
 }  // namespace
@@ -1174,7 +1219,7 @@ int grid::overlay_capacity() { return kFastLane; }
 
 extern "C" size_t grid_mask_workspace_bytes(const grid_compiled* g, int32_t B) {
   if (!g || B <= 0) return 0;
-  return kWsHead + row_layout(g->parser.T, g->dfa.S).total * (size_t)B;
+  return kWsHead + row_layout(g->parser.T).total * (size_t)B;
 }
 
 extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
@@ -1185,16 +1230,16 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   if (phases & ~GRID_PHASE_ALL) return fail(GRID_E_ARG, "grid_mask: unknown phase bits");
   if (!g || B <= 0 || B > 65535 || !cfg_dev || !stack_pool_dev || !mask_dev || !workspace_dev)
     return fail(GRID_E_ARG, "grid_mask: null pointer or batch size out of range");
-  const size_t rb = row_layout(g->parser.T, g->dfa.S).total;
+  const size_t rb = row_layout(g->parser.T).total;
   if (workspace_bytes < kWsHead + rb * (size_t)B) return fail(GRID_E_ARG, "grid_mask: workspace too small");
   if (((uintptr_t)workspace_dev & 255) != 0) return fail(GRID_E_ARG, "grid_mask: workspace not 256-byte aligned");
-  static const int needed[] = {GRID_ART_DFA_CLASS,  GRID_ART_BYTE_CLASS, GRID_ART_DFA_ACCEPT_OFF,
+  static const int needed[] = {GRID_ART_DFA_CLASS,   GRID_ART_BYTE_CLASS,  GRID_ART_DFA_ACCEPT_OFF,
                                GRID_ART_DFA_ACCEPT_LIST, GRID_ART_DFA_LIVE, GRID_ART_ACTION,
-                               GRID_ART_PROD,       GRID_ART_TERM_INFO,  GRID_ART_SPELL_OFF,
-                               GRID_ART_SPELL_BYTES, GRID_ART_SPELL_REC, GRID_ART_ALIAS_OFF,
-                               GRID_ART_ALIAS_IDS,  GRID_ART_LEX_FLAGS,  GRID_ART_LEX_HASH,
-                               GRID_ART_LEX_SLOTS,  GRID_ART_PARSE_STATE, GRID_ART_PARSE_REDX,
-                               GRID_ART_GOTO_OFF,   GRID_ART_GOTO_ENT};
+                               GRID_ART_PROD,        GRID_ART_TERM_INFO,   GRID_ART_SPELL_OFF,
+                               GRID_ART_SPELL_BYTES, GRID_ART_SPELL_REC,   GRID_ART_SPELL_TAIL,
+                               GRID_ART_ALIAS_OFF,   GRID_ART_ALIAS_IDS,   GRID_ART_LEX_FLAGS,
+                               GRID_ART_LEX_HASH,    GRID_ART_LEX_SLOTS,   GRID_ART_PARSE_STATE,
+                               GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH};
   for (int w : needed)
     if (!bound(g, w)) return fail(GRID_E_UNBOUND, "grid_mask: artifact " + std::to_string(w) + " is not bound");
   Tables tb;
@@ -1208,11 +1253,11 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   tb.term_info = (const uint32_t*)g->dev[GRID_ART_TERM_INFO];
   tb.pstate = (const uint32_t*)g->dev[GRID_ART_PARSE_STATE];
   tb.predx = (const uint32_t*)g->dev[GRID_ART_PARSE_REDX];
-  tb.goff = (const uint32_t*)g->dev[GRID_ART_GOTO_OFF];
-  tb.gent = (const uint32_t*)g->dev[GRID_ART_GOTO_ENT];
+  tb.ghash = (const uint8_t*)g->dev[GRID_ART_GOTO_HASH];
   tb.spell_off = (const uint32_t*)g->dev[GRID_ART_SPELL_OFF];
   tb.spell_bytes = (const uint8_t*)g->dev[GRID_ART_SPELL_BYTES];
   tb.spell_rec = (const uint4*)g->dev[GRID_ART_SPELL_REC];
+  tb.spell_tail = (const uint4*)g->dev[GRID_ART_SPELL_TAIL];
   tb.alias_off = (const uint32_t*)g->dev[GRID_ART_ALIAS_OFF];
   tb.alias_ids = (const int32_t*)g->dev[GRID_ART_ALIAS_IDS];
   tb.lex_flags = (const uint16_t*)g->dev[GRID_ART_LEX_FLAGS];
@@ -1232,17 +1277,19 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   tb.tw = g->parser.tw;
   tb.n_pstate = (int)g->parser.pstate.size();
   tb.n_predx = (int)g->parser.predx.size();
-  tb.n_gent = (int)g->parser.goto_ent.size();
   tb.n_acc = (int)g->dfa.accept_list.size();
-  const WalkLds WL = walk_lds(tb);
-  if (WL.total > 64 * 1024 || tb.n_acc > kAccCap || parse_lds(tb, 0).total > 32 * 1024 || tb.tw > 8)
+  tb.hbits = g->parser.goto_hbits;
+  const int mw = tb.tw <= 4 ? 4 : 8;
+  const WalkLds WL = walk_lds(tb, mw, B);
+  if (tb.T > 255 || tb.tw > 8 || WL.total > kWalkLdsMax || parse_lds(tb, 0).total > 24 * 1024)
     return fail(GRID_E_CAPACITY, "grid_mask: lexer DFA or LR tables too large for the LDS staging");
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace_dev;
-  if (tb.tw <= 4)
-    launch_mask<4>(tb, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, ws, rb, phases, s);
-  else
-    launch_mask<8>(tb, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, ws, rb, phases, s);
+  const int rc = mw == 4 ? launch_mask<4>(tb, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, ws, rb,
+                                          phases, s)
+                         : launch_mask<8>(tb, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, ws, rb,
+                                          phases, s);
+  if (rc != GRID_OK) return rc;
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_mask launch: ") + hipGetErrorString(e));
   return GRID_OK;

@@ -10,10 +10,12 @@
 // path computes allowed terminals by simulating reduce chains anyway
 // (section 3.2), so it is exact with or without table compression.
 #include <algorithm>
+#include <cstring>
 #include <map>
 #include <set>
 
 #include "host.h"
+#include "lexhash.h"
 
 namespace grid {
 namespace {
@@ -324,8 +326,7 @@ void compact_tables(Parser& P) {
   const int stride = 2 * TW + 2;
   P.pstate.assign((size_t)P.n_states * stride, 0);
   P.predx.clear();
-  P.goto_off.assign(P.n_states + 1, 0);
-  P.goto_ent.clear();
+  std::vector<std::pair<uint32_t, uint16_t>> gotos;
   for (int s = 0; s < P.n_states; ++s) {
     uint32_t* rec = &P.pstate[(size_t)s * stride];
     std::map<int, std::vector<uint32_t>> groups;  // prod -> bits
@@ -362,10 +363,27 @@ void compact_tables(Parser& P) {
     rec[2 * TW] = (uint32_t)main_prod | n_extra << 16;
     for (int a = 0; a < P.N; ++a) {
       const uint16_t g = P.gto(s, a);
-      if (g != kNoGoto) P.goto_ent.push_back((uint32_t)a | (uint32_t)g << 16);
+      if (g != kNoGoto) gotos.push_back({goto_key(s, a), g});
     }
-    P.goto_off[s + 1] = (uint32_t)P.goto_ent.size();
   }
+  // load factor at most 2/3, so a lookup probes few slots
+  int hb = 6;
+  while ((size_t)1 << hb < gotos.size() + gotos.size() / 2) ++hb;
+  if (P.n_states >= 0xFFFF || P.N > 0xFFFF) throw Error(GRID_E_CAPACITY, "more than 65534 LR states");
+  const uint32_t H = 1u << hb;
+  std::vector<uint32_t> keys(H, 0);
+  std::vector<uint16_t> vals(H, kNoGoto);
+  for (auto& e : gotos)
+    for (uint32_t h = goto_slot(e.first, hb);; h = (h + 1) & (H - 1))
+      if (keys[h] == 0) {
+        keys[h] = e.first;
+        vals[h] = e.second;
+        break;
+      }
+  P.goto_hbits = hb;
+  P.goto_hash.resize((size_t)H * 6);
+  memcpy(P.goto_hash.data(), keys.data(), (size_t)H * 4);
+  memcpy(P.goto_hash.data() + (size_t)H * 4, vals.data(), (size_t)H * 2);
 }
 
 }  // namespace grid

@@ -165,6 +165,35 @@ def test_vocab_artifacts(G):
             assert strs[-1] == spells[int(nodes[n, 1]) - 1]
 
 
+def test_spelling_records_and_tails(G):
+    # record = first 8 bytes, first alias id (| 1 << 31 when shared), length |
+    # tail chunk << 8; bytes 8.. of a longer spelling start on a 16-byte chunk
+    rng = np.random.default_rng(7)
+    vocab = [bytes(rng.integers(40, 41, n, dtype=np.uint8)) for n in range(1, 60)]
+    vocab += [bytes(rng.integers(33, 127, int(n), dtype=np.uint8)) for n in rng.integers(1, 120, 300)]
+    vocab += [vocab[5], vocab[70], bytes(range(256))[:255]]
+    g = G.Grid(grammar_text("expr"), (), vocab)
+    off = np.frombuffer(g.artifact("SPELL_OFF"), np.uint32)
+    data = np.frombuffer(g.artifact("SPELL_BYTES"), np.uint8)
+    rec = np.frombuffer(g.artifact("SPELL_REC"), np.uint32).reshape(-1, 4)
+    tail = np.frombuffer(g.artifact("SPELL_TAIL"), np.uint8)
+    aoff = np.frombuffer(g.artifact("ALIAS_OFF"), np.uint32)
+    ids = np.frombuffer(g.artifact("ALIAS_IDS"), np.int32)
+    assert len(rec) == len(off) - 1
+    for u in range(len(rec)):
+        sp = data[off[u]:off[u + 1]].tobytes()
+        head = int(rec[u, 0]) | int(rec[u, 1]) << 32
+        assert head.to_bytes(8, "little") == sp[:8].ljust(8, b"\0")
+        assert rec[u, 3] & 0xFF == len(sp)
+        first = ids[aoff[u]]
+        assert rec[u, 2] & 0x7FFFFFFF == first
+        assert bool(rec[u, 2] >> 31) == (aoff[u + 1] - aoff[u] > 1)
+        if len(sp) > 8:
+            c = int(rec[u, 3]) >> 8
+            assert tail[16 * c:16 * c + len(sp) - 8].tobytes() == sp[8:]
+            assert len(tail) >= 16 * c + ((len(sp) - 8 + 15) // 16) * 16 + 16
+
+
 def test_specials_are_excluded_and_incomplete_vocab_flagged(G):
     vocab = [b"1", b"+", b"", b"(", b"1"]
     g = G.Grid(grammar_text("expr"), (), vocab, specials=[3], eos_id=2)
