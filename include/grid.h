@@ -153,7 +153,8 @@ enum {
                                bit 8+c word-of-category-c */
   GRID_ART_LEX_HASH,        /* u32 [2] per entry: key = node * 256 + byte + 1 (0 empty), child */
   GRID_ART_LEX_SLOTS,       /* u32 [8] per slot: flags base, hash base, hash mask,
-                               restricted-category mask, node count, 3 reserved */
+                               restricted-category mask, node count, prefix-table base,
+                               prefix-table mask, 1 reserved */
   GRID_ART_SPELL_REC,       /* u32 [U][4] per sorted spelling: its first 8 bytes (little-
                                endian, zero padded), first alias id | 1 << 31 when more ids
                                share the spelling, length | tail chunk << 8 (bytes 8.. of a
@@ -169,6 +170,10 @@ enum {
                                (key * 0x9E3779B1 mod 2^32) >> (32 - k), linear probing */
   GRID_ART_SPELL_TAIL,      /* u8 [16 * chunks]: bytes 8.. of each spelling longer than 8
                                bytes, each starting on a 16-byte boundary, zero padded */
+  GRID_ART_LEX_PREFIX,      /* u32 [4] per entry, per slot an open-addressing table of every
+                               lexicon-trie node of depth 1..8 keyed exactly by its bytes:
+                               bytes 0..3, bytes 4..7 (little-endian, zero padded),
+                               length | flags << 16 (length 0 = empty), node */
   GRID_ART_COUNT
 };
 int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);
@@ -180,7 +185,8 @@ int grid_bind_device(grid_compiled* g, int32_t which, void* device_ptr);
  * first (bottom = the initial state 0); the stack is the one right after the
  * last shift.  q is the lexer DFA state after the pending lexeme r and lexnode
  * the lexicon-trie node of r in slot `slot` (0xFFFFFFFF when r is not a
- * prefix of any lexicon word).  flags bit 0: r is empty. */
+ * prefix of any lexicon word).  flags bit 0: r is empty.  rem_len = |r| and
+ * rem_head holds the first min(|r|, 8) bytes of r, zero padded. */
 typedef struct {
   uint32_t stk_off;
   uint32_t stk_depth;
@@ -189,7 +195,7 @@ typedef struct {
   uint16_t slot;
   uint32_t flags;
   uint32_t rem_len;
-  uint32_t reserved[2];
+  uint8_t rem_head[8];
 } grid_config;
 
 /* Host advance (section 6.1, per-token step 7): lexes and parses the prefix

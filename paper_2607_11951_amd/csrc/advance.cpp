@@ -9,6 +9,8 @@
 // DFA state of the pending lexeme and its lexicon-trie node.  The prefix must
 // be viable (Definition 2), i.e. the pending lexeme is live for an allowed or
 // ignored terminal.
+#include <cstring>
+
 #include "host.h"
 #include "lexhash.h"
 
@@ -110,6 +112,7 @@ int host_config_from_prefix(const grid_compiled* g, int slot, const uint8_t* w, 
   cfg->slot = (uint16_t)slot;
   cfg->flags = rem == 0 ? 1u : 0u;
   cfg->rem_len = rem;
-  cfg->reserved[0] = cfg->reserved[1] = 0;
+  memset(cfg->rem_head, 0, sizeof cfg->rem_head);
+  for (uint32_t k = 0; k < rem && k < 8; ++k) cfg->rem_head[k] = w[n - rem + k];
   return GRID_OK;
 }

@@ -11,7 +11,8 @@
 //
 // Schema lexicon (section 2, L3): per slot, one byte trie over the words of
 // every category with per-node flags "prefix of a category-c word" and
-// "category-c word", edges in a hash table (lexhash.h).  Each word must be a
+// "category-c word", edges in a hash table and the nodes of depth 1..8 in a
+// prefix table keyed by their bytes (lexhash.h).  Each word must be a
 // lexeme of its category's terminal (W_c subset of R_c, Proposition 8 (d)).
 #include <algorithm>
 #include <cstring>
@@ -205,7 +206,41 @@ void add_lexicon(LexiconStore& st, const LexerDfa& dfa, const GrammarText& g,
         }
       }
     }
-  uint32_t rec[kSlotWords] = {flags_base, hash_base, size - 1, restricted, (uint32_t)nodes.size(), 0, 0, 0};
+  // prefix table: every node of depth 1..8 keyed by its bytes
+  std::vector<std::pair<uint64_t, uint32_t>> pref;  // (bytes, len << 24 | node)
+  {
+    std::vector<std::pair<uint32_t, std::pair<uint64_t, uint32_t>>> todo{{0u, {0ull, 0u}}};
+    while (!todo.empty()) {
+      auto [n, kb] = todo.back();
+      todo.pop_back();
+      if (kb.second >= 8) continue;
+      for (auto& e : nodes[n].kids) {
+        const uint64_t b2 = kb.first | (uint64_t)e.first << (8 * kb.second);
+        pref.push_back({b2, (kb.second + 1) << 24 | e.second});
+        todo.push_back({e.second, {b2, kb.second + 1}});
+      }
+    }
+  }
+  uint32_t psize = 16;
+  while (psize < 2 * pref.size()) psize <<= 1;
+  const uint32_t pref_base = (uint32_t)(st.prefix.size() / 4);
+  st.prefix.resize(st.prefix.size() + (size_t)psize * 4, 0);
+  for (auto& e : pref) {
+    const uint32_t lo = (uint32_t)e.first, hi = (uint32_t)(e.first >> 32), len = e.second >> 24;
+    const uint32_t node = e.second & 0xFFFFFF;
+    for (uint32_t h = lexp_hash(lo, hi, len) & (psize - 1);; h = (h + 1) & (psize - 1)) {
+      uint32_t* slot = &st.prefix[(size_t)(pref_base + h) * 4];
+      if ((slot[2] & 0xFFFF) == 0) {
+        slot[0] = lo;
+        slot[1] = hi;
+        slot[2] = len | (uint32_t)nodes[node].flags << 16;
+        slot[3] = node;
+        break;
+      }
+    }
+  }
+  uint32_t rec[kSlotWords] = {flags_base, hash_base, size - 1, restricted, (uint32_t)nodes.size(),
+                              pref_base,  psize - 1, 0};
   st.slots.insert(st.slots.end(), rec, rec + kSlotWords);
   st.n_slots += 1;
 }

@@ -115,6 +115,7 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
 struct LexiconStore {
   std::vector<uint16_t> flags;     // all slots' nodes
   std::vector<uint32_t> hash;      // all slots' entries (2 u32 each)
+  std::vector<uint32_t> prefix;    // all slots' prefix-table entries (4 u32 each)
   std::vector<uint32_t> slots;     // kSlotWords u32 per slot
   int n_slots = 0;
   // host-side lookup helpers

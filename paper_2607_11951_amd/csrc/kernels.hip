@@ -55,7 +55,6 @@ using namespace grid;
 namespace {
 
 constexpr int kBlock = 256;          // prologue / apply workgroup size
-constexpr int kProGroups = 8;        // prologue workgroups per row
 constexpr int kStackWin = 256;       // top of the row's stack kept in LDS (prologue)
 constexpr int kPostCap = 14;         // overlay states recorded per first shift
 constexpr int kTmpCap = 32;          // prologue: virtual pushes of one simulation
@@ -96,6 +95,7 @@ struct Tables {
   const uint16_t* lex_flags;
   const uint32_t* lex_hash;
   const uint32_t* lex_slots;
+  const uint4* lex_prefix;
   int S, C, T, N, NS, P, U, V, W, n_slots, eos_id;
   int tw, n_pstate, n_predx, n_acc, hbits;
 };
@@ -109,9 +109,10 @@ struct RowHeader {
   uint32_t valid;
   int32_t winner;             // pending lexeme's winner at an emission, -1 none
   uint32_t slow_count;
-  int32_t pstat[kProGroups];  // status bits from each prologue workgroup
+  int32_t pstat;              // status bits from the prologue
   int32_t wstat;              // status bits from the walk
-  uint32_t pad[27];
+  uint32_t nonempty;          // the walk allowed some token
+  uint32_t pad[33];
 };
 static_assert(sizeof(RowHeader) == 256, "row header is 256 bytes");
 
@@ -144,8 +145,9 @@ __host__ __device__ inline RowLayout row_layout(int T) {
   return L;
 }
 
-// first-byte table entry: x = q | kind << 16 | t1 << 24 (kind 0 rejected,
-// 1 alive on sigma, 2 alive after shifting t1); y = lexicon node
+// first-byte table entry: x = q | kind << 16 | fresh << 18 | t1 << 24 (kind 0
+// rejected, 1 alive on sigma, 2 alive after shifting t1; fresh: the byte
+// starts a new lexeme); y = lexicon node after the byte
 constexpr uint32_t kFbDead = 0, kFbMode0 = 1, kFbMode1 = 2;
 
 __host__ __device__ inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u; }
@@ -410,12 +412,12 @@ __device__ __forceinline__ int allowed_set(const ParseTabs& pt, const BaseStack&
 
 // ---------------------------------------------------------- lexicon helpers
 struct Slot {
-  uint32_t fbase, hbase, hmask, restricted, nodes;
+  uint32_t fbase, hbase, hmask, restricted, nodes, pbase, pmask;
 };
 
 __device__ inline Slot load_slot(const Tables& tb, int s) {
   const uint32_t* r = tb.lex_slots + (size_t)s * kSlotWords;
-  return {r[0], r[1], r[2], r[3], r[4]};
+  return {r[0], r[1], r[2], r[3], r[4], r[5], r[6]};
 }
 
 __device__ inline uint32_t lex_child(const Tables& tb, const Slot& sl, uint32_t node, uint32_t b) {
@@ -434,6 +436,47 @@ __device__ inline uint32_t lex_flags_of(const Tables& tb, const Slot& sl, uint32
   return node == kNoLex ? 0u : tb.lex_flags[sl.fbase + node];
 }
 
+// Lexicon node and flags of the prefix given by its bytes (length 1..8): one
+// probe in the slot's prefix table.  (0, kNoLex) if it is no word's prefix.
+__device__ inline uint2 lexp_find(const Tables& tb, const Slot& sl, uint64_t bytes, uint32_t len) {
+  const uint32_t lo = (uint32_t)bytes, hi = (uint32_t)(bytes >> 32);
+  uint32_t h = lexp_hash(lo, hi, len) & sl.pmask;
+  for (uint32_t probe = 0; probe <= sl.pmask; ++probe, h = (h + 1) & sl.pmask) {
+    const uint4 e = tb.lex_prefix[sl.pbase + h];
+    const uint32_t el = e.z & 0xFFFFu;
+    if (el == 0) break;
+    if (e.x == lo && e.y == hi && el == len) return make_uint2(e.z >> 16, e.w);
+  }
+  return make_uint2(0u, kNoLex);
+}
+
+// The pending lexeme as the lexicon sees it: its bytes while it has at most 8
+// (bytes mode), else its lexicon-trie node (kNoLex once no word has it as a
+// prefix).  Kept only when the row's lexicon restricts some category.
+struct LexState {
+  uint64_t w;
+  uint32_t len;
+  uint32_t node;
+};
+
+// Appends byte b to the pending lexeme.
+__device__ inline void lex_push(const Tables& tb, const Slot& sl, LexState& lx, uint32_t b) {
+  if (lx.len < 8) {
+    lx.w |= (uint64_t)b << (8 * lx.len);
+  } else if (lx.len == 8) {
+    lx.node = lex_child(tb, sl, lexp_find(tb, sl, lx.w, 8).y, b);
+  } else {
+    lx.node = lex_child(tb, sl, lx.node, b);
+  }
+  ++lx.len;
+}
+
+__device__ inline uint32_t lex_flags_now(const Tables& tb, const Slot& sl, const LexState& lx) {
+  if (lx.len == 0) return 0u;
+  if (lx.len <= 8) return lexp_find(tb, sl, lx.w, lx.len).x;
+  return lex_flags_of(tb, sl, lx.node);
+}
+
 __device__ inline bool bit_of(const uint32_t* s, int t) { return (s[t >> 5] >> (t & 31)) & 1u; }
 
 // What a lane needs to judge terminals: term info, ignored set I, the row's
@@ -447,26 +490,33 @@ struct TermView {
   int lstride;
 };
 
-// Definition 2 for a pending lexeme in DFA state q, lexicon node lex: some
-// terminal it can still complete to is allowed (acur) or ignored and, if its
-// category is restricted, the lexeme is a prefix of one of its words.
+// Terminals a pending lexeme in DFA state q can still complete to that are
+// allowed (acur) or ignored; returns 1 if one of them has an unrestricted
+// category, 2 if all of them are restricted (the lexicon decides), 0 if there
+// are none.  Live sets only shrink as a lexeme grows, so the class of a later
+// byte of the same lexeme is never better than that of an earlier one.
 template <int MW>
-__device__ inline bool trail_ok(const Tables& tb, const Slot& sl, const TermView& tv, const uint32_t (&acur)[MW],
-                                int q, uint32_t lex) {
-  uint32_t bits[MW], unres = 0, res = 0;
+__device__ inline int trail_class(const TermView& tv, const uint32_t (&acur)[MW], int q) {
+  uint32_t unres = 0, res = 0;
   const uint32_t* lv = tv.live + (size_t)q * tv.lstride;
 #pragma unroll
   for (int w = 0; w < MW; ++w) {
-    bits[w] = lv[w] & (acur[w] | tv.I[w]);
-    unres |= bits[w] & ~tv.R[w];
-    res |= bits[w] & tv.R[w];
+    const uint32_t bits = lv[w] & (acur[w] | tv.I[w]);
+    unres |= bits & ~tv.R[w];
+    res |= bits & tv.R[w];
   }
-  if (unres) return true;
-  if (!res) return false;
-  const uint32_t lf = lex_flags_of(tb, sl, lex);
+  return unres ? 1 : (res ? 2 : 0);
+}
+
+// Lexicon half of Definition 2 for a lexeme whose trailing class is 2: some
+// restricted terminal it can complete to has a category whose words it
+// prefixes (lf = the lexeme's lexicon flags).
+template <int MW>
+__device__ inline bool trail_lex(const TermView& tv, const uint32_t (&acur)[MW], int q, uint32_t lf) {
+  const uint32_t* lv = tv.live + (size_t)q * tv.lstride;
 #pragma unroll
   for (int w = 0; w < MW; ++w) {
-    uint32_t r = bits[w] & tv.R[w];
+    uint32_t r = lv[w] & (acur[w] | tv.I[w]) & tv.R[w];
     while (r) {
       const int t = w * 32 + __ffs(r) - 1;
       r &= r - 1;
@@ -476,19 +526,27 @@ __device__ inline bool trail_ok(const Tables& tb, const Slot& sl, const TermView
   return false;
 }
 
+// Definition 2 for a pending lexeme in DFA state q with lexicon flags lf.
+template <int MW>
+__device__ inline bool trail_ok(const TermView& tv, const uint32_t (&acur)[MW], int q, uint32_t lf) {
+  const int c = trail_class<MW>(tv, acur, q);
+  return c == 1 || (c == 2 && trail_lex<MW>(tv, acur, q, lf));
+}
+
 // Pending lexeme's winner at an emission: the first accept-list entry (highest
 // priority, ties to the lower id) that passes the lexicon word test and is
-// ignored or allowed.  -1 if none.
-template <int MW>
-__device__ inline int winner_of(const Tables& tb, const Slot& sl, const TermView& tv, const uint32_t* acc_off,
-                                const uint8_t* acc_list, const uint32_t (&acur)[MW], int q, uint32_t lex) {
+// ignored or allowed.  -1 if none.  lf_of() yields the lexeme's lexicon flags
+// and is called at most once, only if a candidate's category is restricted.
+template <int MW, class LexFlags>
+__device__ inline int winner_of(const TermView& tv, const uint32_t* acc_off, const uint8_t* acc_list,
+                                const uint32_t (&acur)[MW], int q, LexFlags lf_of) {
   uint32_t lf = 0;
   bool have_lf = false;
   for (uint32_t j = acc_off[q]; j < acc_off[q + 1]; ++j) {
     const int t = acc_list[j];
     if (bit_of(tv.R, t)) {
       if (!have_lf) {
-        lf = lex_flags_of(tb, sl, lex);
+        lf = lf_of();
         have_lf = true;
       }
       if (!((lf >> (8 + ((tv.tinfo[t] >> 8) & 0xFFu))) & 1u)) continue;
@@ -503,6 +561,11 @@ __device__ inline int winner_of(const Tables& tb, const Slot& sl, const TermView
 }
 
 // ---------------------------------------------------------------- prologue
+// One workgroup per row, three parallel phases: every terminal's reduce chain
+// and shift from sigma (thread t; A(sigma) is the set that shifted), then the
+// pending lexeme's winner and, for every allowed terminal, the allowed set of
+// the stack after its shift; then the first-byte table (thread b) while one
+// thread runs the end-of-sequence gate.
 template <int MW>
 __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_config* __restrict__ cfgs,
                                                           const uint16_t* __restrict__ pool,
@@ -511,15 +574,12 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
                                                           uint8_t* __restrict__ ws, size_t rbytes) {
   extern __shared__ __align__(16) uint8_t plds[];
   const int row = blockIdx.x;
-  const int grp = blockIdx.y;
   const int tid = threadIdx.x;
   __shared__ uint16_t win[kStackWin];
   __shared__ uint32_t A[8], I[8], R[8], Aw[8];
-  __shared__ uint32_t A2s[256 * 8];
   __shared__ Post posts[256];
   __shared__ uint16_t scratch[kBlock][kPostCap + kTmpCap];
-  __shared__ uint8_t glist[256];  // allowed terminals this workgroup expands
-  __shared__ int nG, bad, overflow, winner;
+  __shared__ int bad, overflow, winner, eos_ok;
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
   const RowLayout L = row_layout(tb.T);
@@ -538,11 +598,10 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     }
     bad = b;
     overflow = 0;
-    nG = 0;
     winner = -1;
+    eos_ok = 0;
   }
-  if (grp == 0)
-    for (int w = tid; w < tb.W; w += kBlock) mrow[w] = 0u;
+  for (int w = tid; w < tb.W; w += kBlock) mrow[w] = 0u;
   __syncthreads();
   const uint32_t depth = cfg.stk_depth;
   const uint32_t lo = depth > (uint32_t)kStackWin ? depth - kStackWin : 0;
@@ -556,14 +615,13 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   __syncthreads();
   if (bad) {
     if (tid == 0) {
-      hdr->pstat[grp] = grp == 0 ? GRID_ROW_BAD_CONFIG : 0;
-      if (grp == 0) {
-        hdr->valid = 0;
-        hdr->eos_ok = 0;
-        hdr->slow_count = 0;
-        hdr->wstat = 0;
-        if (eos_out) eos_out[row] = 0;
-      }
+      hdr->pstat = GRID_ROW_BAD_CONFIG;
+      hdr->valid = 0;
+      hdr->eos_ok = 0;
+      hdr->slow_count = 0;
+      hdr->wstat = 0;
+      hdr->nonempty = 0;
+      if (eos_out) eos_out[row] = 0;
     }
     return;
   }
@@ -581,70 +639,69 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     }
     I[tid] = iw;
     R[tid] = rw8;
+    A[tid] = 0;
     Aw[tid] = 0;
   }
-  for (int i = tid; i < 256 * 8; i += kBlock) A2s[i] = 0;
   const BaseStack bs{pool + cfg.stk_off, win, depth, lo};
   uint16_t* my = scratch[tid];
   const TermView tv{tb.term_info, I, R, tb.live, 8};
   __syncthreads();
 
-  // A(sigma): one set simulation over every terminal; then the pending
-  // lexeme's winner and this workgroup's share of A
-  if (tid == 0) {
-    uint32_t acc[MW];
-    if (allowed_set<MW>(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, acc) < 0) overflow = 1;
-#pragma unroll
-    for (int w = 0; w < MW; ++w) A[w] = acc[w];
-    for (int w = MW; w < 8; ++w) A[w] = 0;
-    int wt = -1;
-    if (!(cfg.flags & 1u)) wt = winner_of<MW>(tb, sl, tv, tb.acc_off, tb.acc_list, acc, cfg.q, cfg.lexnode);
-    winner = wt;
-    int n = 0;
-    for (int t = grp; t < tb.T; t += kProGroups)
-      if (bit_of(A, t)) glist[n++] = (uint8_t)t;
-    if (grp == 0 && wt >= 0 && wt % kProGroups != 0 && bit_of(A, wt)) glist[n++] = (uint8_t)wt;
-    nG = n;
-  }
-  __syncthreads();
-  // the stack after each allowed terminal's shift, then its allowed set
-  for (int i = tid; i < nG; i += kBlock) {
-    const int t = glist[i];
+  // phase 1: terminal tid's reduce chain and shift from sigma
+  if (tid < tb.T) {
+    const int t = tid;
     uint32_t k = depth;
     int m = 0;
     const int r = sim1_shift(pt, bs, k, m, my, kPostCap, t);
-    Post p;
-    p.k = (uint16_t)k;
-    p.m = (uint8_t)m;
-    p.ok = r == 1;
-    for (int j = 0; j < kPostCap; ++j) p.ov[j] = j < m ? my[j] : 0;
-    if (r != 1 || k > 0xFFFF) overflow = 1;
-    posts[t] = p;
-    if (t % kProGroups == grp) post[t] = p;
+    if (r < 0 || (r == 1 && k > 0xFFFF)) overflow = 1;
     if (r == 1) {
-      uint32_t acc[MW];
-      if (allowed_set<MW>(pt, bs, k, m, my, my + m, kPostCap + kTmpCap - m, acc) < 0) overflow = 1;
-#pragma unroll
-      for (int w = 0; w < MW; ++w) A2s[t * 8 + w] = acc[w];
+      atomicOr(&A[t >> 5], 1u << (t & 31));
+      Post p;
+      p.k = (uint16_t)k;
+      p.m = (uint8_t)m;
+      p.ok = 1;
+      for (int j = 0; j < kPostCap; ++j) p.ov[j] = j < m ? my[j] : 0;
+      posts[t] = p;
+      post[t] = p;
     }
   }
   __syncthreads();
-  for (int i = tid; i < nG * 8; i += kBlock) {
-    const int t = glist[i >> 3];
-    if (t % kProGroups == grp) a2[t * 8 + (i & 7)] = A2s[t * 8 + (i & 7)];
+  // the pending lexeme's winner if a byte ends it
+  if (tid == 0 && !(cfg.flags & 1u)) {
+    uint32_t a0[MW];
+#pragma unroll
+    for (int w = 0; w < MW; ++w) a0[w] = A[w];
+    winner = winner_of<MW>(tv, tb.acc_off, tb.acc_list, a0, cfg.q,
+                           [&]() { return lex_flags_of(tb, sl, cfg.lexnode); });
   }
-  if (grp != 0) {
-    __syncthreads();
-    if (tid == 0) hdr->pstat[grp] = overflow ? GRID_ROW_OVERFLOW : 0;
-    return;
-  }
-
-  // ---- workgroup 0: first-byte table, EOS gate, row header
+  __syncthreads();
   const bool rem_empty = (cfg.flags & 1u) != 0;
   const int w = winner;
   const bool w_shifts = w >= 0 && !bit_of(I, w);
-  if (w_shifts && tid < 8) Aw[tid] = A2s[w * 8 + tid];
+  // phase 2: allowed set after each allowed terminal's shift; the last thread
+  // runs the end-of-sequence gate (mid-lexeme aware)
+  if (tid < tb.T && bit_of(A, tid)) {
+    const Post& p = posts[tid];
+    uint32_t acc[MW];
+    if (allowed_set<MW>(pt, bs, p.k, p.m, p.ov, my, kPostCap + kTmpCap, acc) < 0) overflow = 1;
+#pragma unroll
+    for (int k = 0; k < MW; ++k) a2[tid * 8 + k] = acc[k];
+    if (tid == w) {
+#pragma unroll
+      for (int k = 0; k < MW; ++k) Aw[k] = acc[k];
+    }
+  } else if (tid == kBlock - 1) {
+    int ok = 0;
+    if (rem_empty || (w >= 0 && !w_shifts)) {
+      ok = sim1_test(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, tb.T) == 2;
+    } else if (w >= 0) {
+      const Post& p = posts[w];
+      ok = sim1_test(pt, bs, p.k, p.m, p.ov, my, kPostCap + kTmpCap, tb.T) == 2;
+    }
+    eos_ok = ok;
+  }
   __syncthreads();
+  // phase 3: first-byte table
   uint2* fb = (uint2*)(rw + L.fb);
   {
     const int b = tid;  // kBlock == 256: one byte value per thread
@@ -656,10 +713,11 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
       a0[k] = A[k];
       aw[k] = Aw[k];
     }
+    uint32_t fresh = 0;
     const int nq = tb.dfa[(size_t)cfg.q * tb.C + c];
     if (nq != kDead) {
       lex1 = lex_child(tb, sl, cfg.lexnode, b);
-      if (trail_ok<MW>(tb, sl, tv, a0, nq, lex1)) {
+      if (trail_ok<MW>(tv, a0, nq, lex_flags_of(tb, sl, lex1))) {
         kind = kFbMode0;
         q1 = nq;
       }
@@ -667,42 +725,34 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
       const int sq = tb.dfa[(size_t)kStart * tb.C + c];
       if (sq != kDead) {
         lex1 = lex_child(tb, sl, 0u, b);
+        const uint32_t lf1 = lex_flags_of(tb, sl, lex1);
         if (!w_shifts) {
-          if (trail_ok<MW>(tb, sl, tv, a0, sq, lex1)) kind = kFbMode0;
-        } else if (trail_ok<MW>(tb, sl, tv, aw, sq, lex1)) {
+          if (trail_ok<MW>(tv, a0, sq, lf1)) kind = kFbMode0;
+        } else if (trail_ok<MW>(tv, aw, sq, lf1)) {
           kind = kFbMode1;
           t1 = (uint32_t)w;
         }
         q1 = sq;
+        fresh = 1;
       }
     }
     if (kind == kFbDead || sl.restricted == 0) lex1 = kNoLex;
-    fb[b] = make_uint2(q1 | kind << 16 | t1 << 24, lex1);
+    fb[b] = make_uint2(q1 | kind << 16 | fresh << 18 | t1 << 24, lex1);
   }
-  // end-of-sequence gate (mid-lexeme aware)
-  if (tid == 0) {
-    int ok = 0;
-    if (rem_empty || (w >= 0 && !w_shifts)) {
-      ok = sim1_test(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, tb.T) == 2;
-    } else if (w >= 0) {
-      const Post& p = posts[w];
-      ok = p.ok && sim1_test(pt, bs, p.k, p.m, p.ov, my, kPostCap + kTmpCap, tb.T) == 2;
-    }
-    hdr->eos_ok = (uint32_t)ok;
-    if (eos_out) eos_out[row] = (uint8_t)ok;
-    if (ok && tb.eos_id >= 0) mrow[tb.eos_id >> 5] |= 1u << (tb.eos_id & 31);
-  }
-  __syncthreads();
   if (tid < 8) {
     hdr->A[tid] = A[tid];
     hdr->Aw[tid] = Aw[tid];
     hdr->R[tid] = R[tid];
   }
   if (tid == 0) {
+    hdr->eos_ok = (uint32_t)eos_ok;
+    if (eos_out) eos_out[row] = (uint8_t)eos_ok;
+    if (eos_ok && tb.eos_id >= 0) atomicOr(&mrow[tb.eos_id >> 5], 1u << (tb.eos_id & 31));
     hdr->winner = w;
     hdr->slow_count = 0;
     hdr->wstat = 0;
-    hdr->pstat[0] = overflow ? GRID_ROW_OVERFLOW : GRID_ROW_OK;
+    hdr->nonempty = 0;
+    hdr->pstat = overflow ? GRID_ROW_OVERFLOW : GRID_ROW_OK;
     hdr->valid = kRowValid;
   }
 }
@@ -731,12 +781,14 @@ struct RowCtx {
   const Post* post;         // row's stacks after each first shift (global)
 };
 
-// Emits the pending lexeme in DFA state q (lexicon node lex).  ov is the
+// Emits the pending lexeme in DFA state q (lexicon state lx).  ov is the
 // lane's stack area of cap entries: the overlay occupies [0, m), virtual
 // pushes use [m, cap).  1 ok, 0 reject, -1 capacity.
 template <int MW>
-__device__ __forceinline__ int emit(const RowCtx& rc, Lane<MW>& ln, uint16_t* ov, int cap, int q, uint32_t lex) {
-  const int t = winner_of<MW>(*rc.tb, rc.sl, rc.tv, rc.acc_off, rc.acc_list, ln.acur, q, lex);
+__device__ __forceinline__ int emit(const RowCtx& rc, Lane<MW>& ln, uint16_t* ov, int cap, int q,
+                                    const LexState& lx) {
+  const int t = winner_of<MW>(rc.tv, rc.acc_off, rc.acc_list, ln.acur, q,
+                              [&]() { return lex_flags_now(*rc.tb, rc.sl, lx); });
   if (t < 0) return 0;
   if (bit_of(rc.tv.I, t)) return 1;  // ignored: the stack is unchanged
   if (ln.mode == 0) {
@@ -774,31 +826,66 @@ struct DfaView {  // lexer DFA by byte class (LDS copy or global)
   __device__ int next(int q, uint32_t c) const { return next_[q * C + c]; }
 };
 
-// Walks the bytes [i, n) of one spelling from lane state (ln, q, lex); lex
-// is kNoLex throughout when the row's lexicon restricts nothing.  byte_at(i)
-// yields byte i.  1 allowed, 0 rejected, -1 capacity.
+// Walks the bytes [i, n) of one spelling from lane state (ln, q, lx).
+// byte_at(i) yields byte i, called once per i in increasing order.  The lanes
+// of a wave alternate between a scan phase (every lane that can takes its
+// next byte: a DFA step and the trailing class, all in LDS) and an emission
+// phase (lanes whose byte killed the DFA emit together), so a wave pays for
+// emissions once per emission depth rather than once per byte.  Lexicon
+// lookups happen only where a lexeme ends: at an emission, and at the end of
+// the spelling when only restricted terminals remain (by the shrinking of live
+// sets this one check covers every byte of the lexeme).  1 allowed,
+// 0 rejected, -1 capacity.
 template <int MW, class ByteAt>
-__device__ __forceinline__ int walk_bytes(const RowCtx& rc, Lane<MW>& ln, int q, uint32_t lex, uint32_t i,
-                                          uint32_t n, ByteAt byte_at, const DfaView& step, uint16_t* ov, int cap) {
+__device__ __forceinline__ int walk_bytes(const RowCtx& rc, Lane<MW>& ln, int q, LexState lx, uint32_t i,
+                                          uint32_t n, ByteAt byte_at, const DfaView& step, uint16_t* ov,
+                                          int cap) {
   const Tables& tb = *rc.tb;
   const bool track = rc.sl.restricted != 0;
-  for (; i < n; ++i) {
-    const uint32_t b = byte_at(i);
-    const uint32_t c = step.cls(b);
-    const int nq = step.next(q, c);
-    if (nq != kDead) {
-      q = nq;
-      lex = lex_child(tb, rc.sl, lex, b);
-    } else {
-      const int r = emit<MW>(rc, ln, ov, cap, q, lex);
-      if (r <= 0) return r;
-      q = step.next(kStart, c);
-      if (q == kDead) return 0;
-      lex = track ? lex_child(tb, rc.sl, 0u, b) : kNoLex;
+  int status = 2;         // 2 running, else the result
+  int pend = -1;          // byte class waiting for an emission
+  uint32_t pend_b = 0;    // that byte
+  int cls = 1;            // trailing class after the last byte taken
+  for (;;) {
+    for (;;) {  // scan phase
+      const bool run = status == 2 && pend < 0 && i < n;
+      if (!__any(run)) break;
+      if (run) {
+        const uint32_t b = byte_at(i);
+        const uint32_t c = step.cls(b);
+        const int nq = step.next(q, c);
+        if (nq != kDead) {
+          q = nq;
+          if (track) lex_push(tb, rc.sl, lx, b);
+          cls = trail_class<MW>(rc.tv, ln.acur, q);
+          if (cls == 0) status = 0;
+          else ++i;
+        } else {
+          pend = (int)c;
+          pend_b = b;
+        }
+      }
     }
-    if (!trail_ok<MW>(tb, rc.sl, rc.tv, ln.acur, q, lex)) return 0;
+    if (status == 2 && pend < 0)  // the spelling ended inside a lexeme
+      status = (cls == 1 || trail_lex<MW>(rc.tv, ln.acur, q, lex_flags_now(tb, rc.sl, lx))) ? 1 : 0;
+    const bool em = status == 2 && pend >= 0;
+    if (!__any(em)) break;
+    if (em) {  // emission phase
+      const int r = emit<MW>(rc, ln, ov, cap, q, lx);
+      if (r <= 0) {
+        status = r;
+      } else {
+        q = step.next(kStart, (uint32_t)pend);
+        lx.w = pend_b;
+        lx.len = 1;
+        cls = q == kDead ? 0 : trail_class<MW>(rc.tv, ln.acur, q);
+        if (cls == 0) status = 0;
+        else ++i;
+        pend = -1;
+      }
+    }
   }
-  return 1;
+  return status;
 }
 
 // -------------------------------------------------------------------- walk
@@ -808,7 +895,9 @@ struct RowLds {
   uint32_t valid;
   uint32_t stk_off, stk_depth;
   uint32_t slot;
-  uint32_t pad[4];
+  uint32_t rem_lo, rem_hi;  // first 8 bytes of the pending lexeme
+  uint32_t rem_len;
+  uint32_t pad;
 };
 static_assert(sizeof(RowLds) == 128, "row record is 128 bytes");
 
@@ -951,6 +1040,11 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
       rl.stk_off = cfg.stk_off;
       rl.stk_depth = cfg.stk_depth;
       rl.slot = cfg.slot;
+      rl.rem_lo = (uint32_t)cfg.rem_head[0] | (uint32_t)cfg.rem_head[1] << 8 | (uint32_t)cfg.rem_head[2] << 16 |
+                  (uint32_t)cfg.rem_head[3] << 24;
+      rl.rem_hi = (uint32_t)cfg.rem_head[4] | (uint32_t)cfg.rem_head[5] << 8 | (uint32_t)cfg.rem_head[6] << 16 |
+                  (uint32_t)cfg.rem_head[7] << 24;
+      rl.rem_len = cfg.flags & 1u ? 0u : cfg.rem_len;
     }
     if (tid == 0) item_ctr = 0;
     __syncthreads();
@@ -1007,13 +1101,26 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
         byte_at.lo0 = (uint64_t)tl0.x | (uint64_t)tl0.y << 32;
         byte_at.hi = (uint64_t)tl0.z | (uint64_t)tl0.w << 32;
         byte_at.tail = tb.spell_tail + (rk0.w >> 8);
-        const int ok = walk_bytes<MW>(rc, ln, (int)(e.x & 0xFFFF), e.y, 1u, n, byte_at, step, lane_area, kFastLane);
+        // the lexeme after byte 0: a new one, or the pending lexeme plus the byte
+        LexState lx;
+        const uint32_t b0 = (uint32_t)(h & 0xFF);
+        if ((e.x >> 18) & 1u) {
+          lx = LexState{b0, 1u, kNoLex};
+        } else {
+          lx.len = rl.rem_len + 1;
+          lx.node = e.y;
+          lx.w = lx.len <= 8 ? (((uint64_t)rl.rem_lo | (uint64_t)rl.rem_hi << 32) | (uint64_t)b0 << (8 * rl.rem_len))
+                             : 0ull;
+        }
+        const int ok = walk_bytes<MW>(rc, ln, (int)(e.x & 0xFFFF), lx, 1u, n, byte_at, step, lane_area, kFastLane);
         uint32_t* mrow = mask + (size_t)(g0 + r) * tb.W;
         if (ok > 0) {
           const uint32_t id = rk0.z;
           if (!(id >> 31)) atomicOr(&mrow[id >> 5], 1u << (id & 31));
           else set_alias_bits(tb, mrow, u);
-        } else if (ok < 0) {  // the lane's stack area is too small: hand over
+        }
+        const uint64_t allowed = __ballot(ok > 0);
+        if (allowed && lane == __ffsll((unsigned long long)allowed) - 1) ((RowHeader*)rw)->nonempty = 1u; else if (ok < 0) {  // the lane's stack area is too small: hand over
           RowHeader* hdr = (RowHeader*)rw;
           const uint32_t slot = atomicAdd(&hdr->slow_count, 1u);
           if (slot < (uint32_t)kSlowCap) ((uint32_t*)(rw + RL.slow))[slot] = (uint32_t)u;
@@ -1079,7 +1186,11 @@ __global__ __launch_bounds__(kSlowThreads) void finalize_kernel(Tables tb, const
     rc.post = (const Post*)(rw + RL.post);
     uint16_t* ov = (uint16_t*)(rw + RL.slow_ov) + tid * kSlowLane;
     const DfaView step{tb.dfa, tb.bclass, tb.C};
-    const uint32_t lex0 = rc.sl.restricted != 0 ? cfg.lexnode : kNoLex;
+    LexState lex0;
+    lex0.len = cfg.flags & 1u ? 0u : cfg.rem_len;
+    lex0.node = cfg.lexnode;
+    lex0.w = 0;
+    for (int k = 0; k < 8; ++k) lex0.w |= (uint64_t)cfg.rem_head[k] << (8 * k);
     for (uint32_t k = tid; k < count; k += kSlowThreads) {
       const int u = (int)((const uint32_t*)(rw + RL.slow))[k];
       Lane<MW> ln;
@@ -1093,25 +1204,22 @@ __global__ __launch_bounds__(kSlowThreads) void finalize_kernel(Tables tb, const
       auto byte_at = [&](uint32_t i) -> uint32_t { return tb.spell_bytes[base + i]; };
       const int ok = walk_bytes<MW>(rc, ln, cfg.q, lex0, 0u, tb.spell_off[u + 1] - base, byte_at, step, ov,
                                     kSlowLane);
-      if (ok > 0) set_alias_bits(tb, mrow, u);
+      if (ok > 0) {
+        set_alias_bits(tb, mrow, u);
+        any = 1;
+      }
       if (ok < 0) slow_err = 1;
     }
   }
   __syncthreads();
-  __threadfence();
-  uint32_t acc = 0;
-  for (int w = tid; w < tb.W; w += kSlowThreads) acc |= __atomic_load_n(&mrow[w], __ATOMIC_RELAXED);
-  if (acc) atomicOr(&any, 1u);
-  __syncthreads();
   if (tid == 0) {
     int32_t st = 0;
     if (valid) {
-      for (int g = 0; g < kProGroups; ++g) st |= hdr->pstat[g];
-      st |= hdr->wstat;
+      st = hdr->pstat | hdr->wstat;
       if (slow_err || hdr->slow_count > (uint32_t)kSlowCap) st |= GRID_ROW_OVERFLOW;
-      if (!any && !hdr->eos_ok) st |= GRID_ROW_EMPTY;
+      if (!any && !hdr->nonempty && !hdr->eos_ok) st |= GRID_ROW_EMPTY;
     } else {
-      st = hdr->pstat[0] | GRID_ROW_BAD_CONFIG;
+      st = hdr->pstat | GRID_ROW_BAD_CONFIG;
     }
     if (status) status[row] = st;
   }
@@ -1196,7 +1304,7 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
       !raise_lds((const void*)finalize_kernel<MW>, parse_bytes))
     return fail(GRID_E_HIP, "grid_mask: cannot raise the LDS limit");
   if (phases & GRID_PHASE_PROLOGUE)
-    hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B, kProGroups), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool,
+    hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool,
                        mask, eos, ws, rb);
   if ((phases & GRID_PHASE_WALK) && tb.U > 0) {
     const WalkLds WL = walk_lds(tb, MW, B);
@@ -1239,7 +1347,7 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
                                GRID_ART_SPELL_BYTES, GRID_ART_SPELL_REC,   GRID_ART_SPELL_TAIL,
                                GRID_ART_ALIAS_OFF,   GRID_ART_ALIAS_IDS,   GRID_ART_LEX_FLAGS,
                                GRID_ART_LEX_HASH,    GRID_ART_LEX_SLOTS,   GRID_ART_PARSE_STATE,
-                               GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH};
+                               GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH,   GRID_ART_LEX_PREFIX};
   for (int w : needed)
     if (!bound(g, w)) return fail(GRID_E_UNBOUND, "grid_mask: artifact " + std::to_string(w) + " is not bound");
   Tables tb;
@@ -1263,6 +1371,7 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   tb.lex_flags = (const uint16_t*)g->dev[GRID_ART_LEX_FLAGS];
   tb.lex_hash = (const uint32_t*)g->dev[GRID_ART_LEX_HASH];
   tb.lex_slots = (const uint32_t*)g->dev[GRID_ART_LEX_SLOTS];
+  tb.lex_prefix = (const uint4*)g->dev[GRID_ART_LEX_PREFIX];
   tb.S = g->dfa.S;
   tb.C = g->dfa.C;
   tb.T = g->parser.T;

@@ -26,12 +26,12 @@ DTYPE_F32, DTYPE_BF16 = 0, 1
 ART_NAMES = ["DFA_DENSE", "DFA_CLASS", "BYTE_CLASS", "DFA_ACCEPT_OFF", "DFA_ACCEPT_LIST", "DFA_LIVE",
              "ACTION", "GOTO", "PROD", "TERM_INFO", "SPELL_OFF", "SPELL_BYTES", "ALIAS_OFF",
              "ALIAS_IDS", "TRIE_LEVEL_OFF", "TRIE_NODES", "LEX_FLAGS", "LEX_HASH", "LEX_SLOTS",
-             "SPELL_REC", "PARSE_STATE", "PARSE_REDX", "GOTO_HASH", "SPELL_TAIL"]
+             "SPELL_REC", "PARSE_STATE", "PARSE_REDX", "GOTO_HASH", "SPELL_TAIL", "LEX_PREFIX"]
 ART = {n: i for i, n in enumerate(ART_NAMES)}
 
 CONFIG_DTYPE = np.dtype([("stk_off", "<u4"), ("stk_depth", "<u4"), ("lexnode", "<u4"), ("q", "<u2"),
                          ("slot", "<u2"), ("flags", "<u4"), ("rem_len", "<u4"),
-                         ("reserved", "<u4", (2,))])
+                         ("rem_head", "u1", (8,))])
 assert CONFIG_DTYPE.itemsize == 32
 
 # every symbol include/grid.h declares
@@ -148,7 +148,7 @@ class Grid:
         slot = ctypes.c_int32()
         _check(lib().grid_add_lexicon(self.h, ctypes.byref(la), ctypes.byref(slot)))
         if self.device is not None:
-            self._upload(self.device, ["LEX_FLAGS", "LEX_HASH", "LEX_SLOTS"])
+            self._upload(self.device, ["LEX_FLAGS", "LEX_HASH", "LEX_SLOTS", "LEX_PREFIX"])
         return slot.value
 
     def artifact(self, name):

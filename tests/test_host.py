@@ -75,6 +75,74 @@ def test_lexicon_validation(G):
     assert g.info()["n_lexicon_slots"] == 2
 
 
+def _lexp_hash(lo, hi, ln):
+    # prefix-table slot hash of the LEX_PREFIX artifact (mod 2^32 arithmetic)
+    m = 0xFFFFFFFF
+    h = ((lo * 0x9E3779B1) & m) ^ ((hi * 0x85EBCA77) & m) ^ ((ln * 0xC2B2AE3D) & m)
+    h ^= h >> 15
+    h = (h * 0x2C1B3C6D) & m
+    return h ^ (h >> 12)
+
+
+def test_lexicon_prefix_table(G):
+    # every trie node of depth 1..8 is found by its bytes with the node id and
+    # flags the edge hash gives; strings that prefix no word are not found
+    words_t = ["employees", "emp", "e", "dept_history_2020", "orders"]
+    words_c = ["id", "emp_no", "employee_name_full", "e_x", "order_id"]
+    g = G.Grid(grammar_text("crud"), ["insert", "update", "delete"], [b"a"])
+    slot = g.add_lexicon({"TABLE_NAME": words_t, "COLUMN_NAME": words_c})
+    rec = np.frombuffer(g.artifact("LEX_SLOTS"), np.uint32).reshape(-1, 8)[slot]
+    flags = np.frombuffer(g.artifact("LEX_FLAGS"), np.uint16)
+    edges = np.frombuffer(g.artifact("LEX_HASH"), np.uint32).reshape(-1, 2)
+    pref = np.frombuffer(g.artifact("LEX_PREFIX"), np.uint32).reshape(-1, 4)
+    fbase, hbase, hmask, _, nodes, pbase, pmask = (int(x) for x in rec[:7])
+
+    def child(node, b):
+        key = node * 256 + b + 1
+        h = ((key * 0x9E3779B1) & 0xFFFFFFFF)
+        h = (h ^ (h >> 15)) & hmask
+        while True:
+            k, c = edges[hbase + h]
+            if k == key:
+                return int(c)
+            if k == 0:
+                return None
+            h = (h + 1) & hmask
+
+    def lookup(bs):
+        lo = int.from_bytes(bs[:4].ljust(4, b"\0"), "little")
+        hi = int.from_bytes(bs[4:8].ljust(4, b"\0"), "little")
+        h = _lexp_hash(lo, hi, len(bs)) & pmask
+        while True:
+            e = pref[pbase + h]
+            if e[2] & 0xFFFF == 0:
+                return None
+            if e[0] == lo and e[1] == hi and e[2] & 0xFFFF == len(bs):
+                return int(e[2] >> 16), int(e[3])
+            h = (h + 1) & pmask
+
+    prefixes = {w[:k].encode() for w in words_t + words_c for k in range(1, min(len(w), 8) + 1)}
+    for p in prefixes:
+        node = 0
+        for b in p:
+            node = child(node, b)
+        assert node is not None
+        assert lookup(p) == (int(flags[fbase + node]), node), p
+    for p in [b"x", b"emq", b"employeez", b"id_", b"ordersXY", b"e_y"]:
+        if p[:8] not in prefixes:
+            assert lookup(p[:8]) is None, p
+    assert int((pref[pbase:pbase + pmask + 1, 2] & 0xFFFF > 0).sum()) == len(prefixes)
+
+
+def test_config_pending_head_bytes(G):
+    g = G.Grid(grammar_text("crud"), ["insert", "update", "delete"], [b"a"])
+    for w in [b"select ", b"select emp", b"select employees_history_x", b"select a from t where x = 'abc"]:
+        cfg, _ = g.config(w)
+        r = int(cfg["rem_len"])
+        head = bytes(cfg["rem_head"])
+        assert head == w[len(w) - r:][:8].ljust(8, b"\0"), (w, r, head)
+
+
 def _viable_agree(G, oracle_mod, grammar, drop, lexicon, strings):
     g = G.Grid(grammar_text(grammar), drop, [b"x"])
     slot = g.add_lexicon(lexicon) if lexicon else 0
