@@ -157,8 +157,8 @@ enum {
                                prefix-table mask, 1 reserved */
   GRID_ART_SPELL_REC,       /* u32 [U][4] per sorted spelling: its first 8 bytes (little-
                                endian, zero padded), first alias id | 1 << 31 when more ids
-                               share the spelling, length | tail chunk << 8 (bytes 8.. of a
-                               longer spelling start at SPELL_TAIL + 16 * tail chunk) */
+                               share the spelling, length | overflow chunk << 8 (bytes 24..
+                               of a longer spelling start at SPELL_TAIL + 16 * chunk) */
   GRID_ART_PARSE_STATE,     /* u32 [n_lr][2*TW+2], TW = ceil((T+1)/32): terminals that shift
                                (or accept), terminals reduced by the state's main
                                production, main production | extra groups << 16, offset of
@@ -168,12 +168,17 @@ enum {
                                load <= 2/3): u32 [H] keys (state << 16 | nonterminal) + 1
                                (0 empty), then u16 [H] targets; slot of a key =
                                (key * 0x9E3779B1 mod 2^32) >> (32 - k), linear probing */
-  GRID_ART_SPELL_TAIL,      /* u8 [16 * chunks]: bytes 8.. of each spelling longer than 8
-                               bytes, each starting on a 16-byte boundary, zero padded */
+  GRID_ART_SPELL_TAIL,      /* u8 [16 * chunks]: chunk u = bytes 8..23 of spelling u (zero
+                               padded), then overflow chunks with bytes 24.. of spellings
+                               longer than 24 bytes, each on a 16-byte boundary */
   GRID_ART_LEX_PREFIX,      /* u32 [4] per entry, per slot an open-addressing table of every
                                lexicon-trie node of depth 1..8 keyed exactly by its bytes:
                                bytes 0..3, bytes 4..7 (little-endian, zero padded),
                                length | flags << 16 (length 0 = empty), node */
+  GRID_ART_SPELL_RANGE,     /* u16 per 64-spelling sub-tile (sorted order): lowest first
+                               byte | highest first byte << 8 of its spellings */
+  GRID_ART_SPELL_OF_ID,     /* u32 [V]: sorted-spelling index of each token id, 0xFFFFFFFF
+                               for specials and empty tokens */
   GRID_ART_COUNT
 };
 int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);
@@ -226,11 +231,13 @@ int grid_mask(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
  * walk needs the prologue of the same rows and workspace to have run before
  * it (earlier on the stream); finalize needs the walk; the mask is exact once
  * all three have run.  grid_mask equals grid_mask_phases with GRID_PHASE_ALL. */
-#define GRID_PHASE_PROLOGUE 1u      /* allowed sets, EOS gate, row clear */
-#define GRID_PHASE_WALK 2u          /* full-vocabulary walk and bit packing */
-#define GRID_PHASE_FINALIZE 4u      /* finishes the spellings the walk handed to the slow
-                                       path (needed for an exact mask) and writes the row
-                                       status when status_dev is not null */
+#define GRID_PHASE_PROLOGUE 1u      /* allowed sets, EOS gate, first-byte table */
+#define GRID_PHASE_WALK 2u          /* full-vocabulary walk into a mask over sorted
+                                       spellings (workspace), then the spellings the
+                                       fast walk handed to the slow path */
+#define GRID_PHASE_FINALIZE 4u      /* writes mask_dev (each id takes its spelling's bit;
+                                       the EOS bit) and the row status when status_dev
+                                       is not null */
 #define GRID_PHASE_ALL 7u
 int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
                      const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,

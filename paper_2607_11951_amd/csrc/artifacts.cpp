@@ -2,8 +2,9 @@
 //
 // Vocabulary (Definition 3, section 4.1): the distinct non-special spellings,
 // sorted in byte order, which is the depth-first order of the token byte trie,
-// each with a 16-byte record (first 8 bytes, first id, length) and, past 8
-// bytes, a tail on 16-byte boundaries so a walk fetches 16 bytes per load;
+// each with a 16-byte record (first 8 bytes, first id, length) and a 16-byte
+// tail chunk (bytes 8..23) at the same index, longer spellings continuing in
+// overflow chunks, so a walk fetches 16 bytes per load;
 // an alias table lists every token id sharing a spelling (section 2: masks are
 // over ids, so alias expansion is needed for completeness); and a levelized
 // CSR form of the same trie (level by level, children in byte order, each
@@ -71,14 +72,7 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
       va.spell_rec.push_back((uint32_t)head);
       va.spell_rec.push_back((uint32_t)(head >> 32));
       va.spell_rec.push_back((uint32_t)ids[k]);
-      uint32_t chunk = 0;
-      if (s.size() > 8) {  // bytes 8.. on a 16-byte boundary of their own
-        chunk = (uint32_t)(va.spell_tail.size() / 16);
-        if (chunk >= (1u << 24)) throw Error(GRID_E_CAPACITY, "spelling tails larger than 256 MiB");
-        va.spell_tail.insert(va.spell_tail.end(), s.begin() + 8, s.end());
-        va.spell_tail.resize((va.spell_tail.size() + 15) & ~(size_t)15, 0);
-      }
-      va.spell_rec.push_back((uint32_t)s.size() | chunk << 8);
+      va.spell_rec.push_back((uint32_t)s.size());  // | overflow chunk << 8, below
     } else {
       va.spell_rec[va.spell_rec.size() - 2] |= 1u << 31;  // more than one id
     }
@@ -86,11 +80,35 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
   }
   if (!uniq.empty()) va.alias_off.push_back((uint32_t)va.alias_ids.size());
   va.spell_bytes.resize(va.spell_bytes.size() + 32, 0);  // safe over-read padding
-  va.spell_tail.resize(va.spell_tail.size() + 32, 0);    // one chunk of read-ahead
+  // tails: chunk u holds bytes 8..23 of spelling u, so it can be fetched with
+  // the record; bytes 24.. of longer spellings follow in overflow chunks
+  const size_t U = uniq.size();
+  va.spell_tail.assign(U * 16, 0);
+  for (size_t u = 0; u < U; ++u) {
+    const std::string& sp = uniq[u];
+    for (size_t k = 8; k < sp.size() && k < 24; ++k) va.spell_tail[u * 16 + k - 8] = (uint8_t)sp[k];
+    if (sp.size() > 24) {
+      const size_t chunk = va.spell_tail.size() / 16;
+      if (chunk >= (1u << 24)) throw Error(GRID_E_CAPACITY, "spelling tails larger than 256 MiB");
+      va.spell_tail.insert(va.spell_tail.end(), sp.begin() + 24, sp.end());
+      va.spell_tail.resize((va.spell_tail.size() + 15) & ~(size_t)15, 0);
+      va.spell_rec[u * 4 + 3] |= (uint32_t)chunk << 8;
+    }
+  }
+  va.spell_tail.resize(va.spell_tail.size() + 32, 0);  // read-ahead padding
   std::vector<char> single(256, 0);
   for (auto& s : uniq)
     if (s.size() == 1) single[(uint8_t)s[0]] = 1;
   va.byte_complete = std::all_of(single.begin(), single.end(), [](char c) { return c != 0; });
+  va.spell_of_id.assign(V, 0xFFFFFFFFu);
+  for (size_t u = 0; u < U; ++u)
+    for (uint32_t k = va.alias_off[u]; k < va.alias_off[u + 1]; ++k) va.spell_of_id[va.alias_ids[k]] = (uint32_t)u;
+  // first-byte range of every 64 consecutive spellings (sorted, so the first
+  // and the last spelling of the group bound it)
+  for (size_t u0 = 0; u0 < uniq.size(); u0 += 64) {
+    const size_t u1 = std::min(uniq.size(), u0 + 64) - 1;
+    va.sub_range.push_back((uint16_t)((uint8_t)uniq[u0][0] | (uint8_t)uniq[u1][0] << 8));
+  }
 
   // levelized trie: nodes of level L are the distinct length-L prefixes,
   // ordered by (parent, byte) -- the byte order of the prefixes themselves

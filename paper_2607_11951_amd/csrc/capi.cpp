@@ -166,6 +166,8 @@ extern "C" int grid_artifact(const grid_compiled* g, int32_t which, const void**
     case GRID_ART_SPELL_REC: put(g->vocab.spell_rec, p, n); break;
     case GRID_ART_SPELL_TAIL: put(g->vocab.spell_tail, p, n); break;
     case GRID_ART_LEX_PREFIX: put(g->lex.prefix, p, n); break;
+    case GRID_ART_SPELL_RANGE: put(g->vocab.sub_range, p, n); break;
+    case GRID_ART_SPELL_OF_ID: put(g->vocab.spell_of_id, p, n); break;
     case GRID_ART_PARSE_STATE: put(g->parser.pstate, p, n); break;
     case GRID_ART_PARSE_REDX: put(g->parser.predx, p, n); break;
     case GRID_ART_GOTO_HASH: put(g->parser.goto_hash, p, n); break;

@@ -99,6 +99,8 @@ struct VocabArtifacts {
   std::vector<uint8_t> spell_bytes;  // + padding
   std::vector<uint32_t> spell_rec;   // [U][4]: head lo, head hi, id | multi << 31, length | chunk << 8
   std::vector<uint8_t> spell_tail;   // bytes 8.. per spelling, 16-byte aligned chunks
+  std::vector<uint16_t> sub_range;   // per 64 spellings: lowest | highest first byte << 8
+  std::vector<uint32_t> spell_of_id; // [V]: spelling index, 0xFFFFFFFF none
   std::vector<uint32_t> alias_off;   // [U+1]
   std::vector<int32_t> alias_ids;
   std::vector<uint32_t> level_off;   // [Lmax+2]

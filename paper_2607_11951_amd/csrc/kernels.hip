@@ -62,6 +62,7 @@ constexpr int kGuard = 4096;         // reduce-chain step bound
 constexpr int kSlowCap = 4096;       // spellings handed to the slow path per row
 constexpr int kSlowThreads = 64;
 constexpr int kSlowLane = 512;       // slow path per-thread stack area (workspace)
+constexpr int kGatherGroups = 32;    // finalize workgroups per row
 constexpr uint32_t kRowValid = 0x600D;
 constexpr size_t kWsHead = 256;      // workspace head (reserved)
 constexpr int kMaxRounds = 257;      // set-simulation reruns (each peels one reduce group)
@@ -89,13 +90,15 @@ struct Tables {
   const uint32_t* spell_off;  // [U+1]
   const uint8_t* spell_bytes;
   const uint4* spell_rec;     // [U]: head lo, head hi, first id | multi << 31, length | chunk << 8
-  const uint4* spell_tail;    // bytes 8.. of long spellings, 16-byte chunks
+  const uint4* spell_tail;    // chunk u: bytes 8..23 of spelling u; overflow chunks after
   const uint32_t* alias_off;  // [U+1]
   const int32_t* alias_ids;
+  const uint32_t* spell_of_id;  // [V]
   const uint16_t* lex_flags;
   const uint32_t* lex_hash;
   const uint32_t* lex_slots;
   const uint4* lex_prefix;
+  const uint16_t* sub_range;  // per 64 spellings: lowest | highest first byte << 8
   int S, C, T, N, NS, P, U, V, W, n_slots, eos_id;
   int tw, n_pstate, n_predx, n_acc, hbits;
 };
@@ -112,7 +115,8 @@ struct RowHeader {
   int32_t pstat;              // status bits from the prologue
   int32_t wstat;              // status bits from the walk
   uint32_t nonempty;          // the walk allowed some token
-  uint32_t pad[33];
+  uint32_t alive[8];          // first bytes whose first-byte entry is not rejected
+  uint32_t pad[25];
 };
 static_assert(sizeof(RowHeader) == 256, "row header is 256 bytes");
 
@@ -125,10 +129,12 @@ struct Post {                 // stack after shifting one allowed terminal
 static_assert(sizeof(Post) == 32, "post entry is 32 bytes");
 
 struct RowLayout {
-  size_t post, a2, fb, slow, slow_ov, total;
+  size_t post, a2, fb, smask, slow, slow_ov, total;
 };
 
-__host__ __device__ inline RowLayout row_layout(int T) {
+// One row's workspace.  smask is the row's mask in sorted-spelling order, one
+// 64-bit word per 64-spelling sub-tile.
+__host__ __device__ inline RowLayout row_layout(int T, int U) {
   RowLayout L;
   size_t o = sizeof(RowHeader);
   L.post = o;
@@ -136,7 +142,9 @@ __host__ __device__ inline RowLayout row_layout(int T) {
   L.a2 = o;
   o += (size_t)T * 32;
   L.fb = o;
-  o += 256 * 8;
+  o += 256 * 4;
+  L.smask = o;
+  o += (size_t)((U + 63) / 64) * 8;
   L.slow = o;
   o += kSlowCap * 4;
   L.slow_ov = o;
@@ -145,9 +153,9 @@ __host__ __device__ inline RowLayout row_layout(int T) {
   return L;
 }
 
-// first-byte table entry: x = q | kind << 16 | fresh << 18 | t1 << 24 (kind 0
+// first-byte table entry: q | kind << 16 | fresh << 18 | t1 << 24 (kind 0
 // rejected, 1 alive on sigma, 2 alive after shifting t1; fresh: the byte
-// starts a new lexeme); y = lexicon node after the byte
+// starts a new lexeme)
 constexpr uint32_t kFbDead = 0, kFbMode0 = 1, kFbMode1 = 2;
 
 __host__ __device__ inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u; }
@@ -457,6 +465,7 @@ struct LexState {
   uint64_t w;
   uint32_t len;
   uint32_t node;
+  uint32_t need;  // some restricted terminal was viable where the lexeme began
 };
 
 // Appends byte b to the pending lexeme.
@@ -491,12 +500,12 @@ struct TermView {
 };
 
 // Terminals a pending lexeme in DFA state q can still complete to that are
-// allowed (acur) or ignored; returns 1 if one of them has an unrestricted
-// category, 2 if all of them are restricted (the lexicon decides), 0 if there
-// are none.  Live sets only shrink as a lexeme grows, so the class of a later
-// byte of the same lexeme is never better than that of an earlier one.
+// allowed (acur) or ignored: bit 0 set if one of them has an unrestricted
+// category, bit 1 if one has a restricted category (the lexicon decides for
+// it).  Live sets only shrink as a lexeme grows, so a later byte of the same
+// lexeme never gains a bit.
 template <int MW>
-__device__ inline int trail_class(const TermView& tv, const uint32_t (&acur)[MW], int q) {
+__device__ inline uint32_t trail_flags(const TermView& tv, const uint32_t (&acur)[MW], int q) {
   uint32_t unres = 0, res = 0;
   const uint32_t* lv = tv.live + (size_t)q * tv.lstride;
 #pragma unroll
@@ -505,7 +514,7 @@ __device__ inline int trail_class(const TermView& tv, const uint32_t (&acur)[MW]
     unres |= bits & ~tv.R[w];
     res |= bits & tv.R[w];
   }
-  return unres ? 1 : (res ? 2 : 0);
+  return (unres ? 1u : 0u) | (res ? 2u : 0u);
 }
 
 // Lexicon half of Definition 2 for a lexeme whose trailing class is 2: some
@@ -529,14 +538,15 @@ __device__ inline bool trail_lex(const TermView& tv, const uint32_t (&acur)[MW],
 // Definition 2 for a pending lexeme in DFA state q with lexicon flags lf.
 template <int MW>
 __device__ inline bool trail_ok(const TermView& tv, const uint32_t (&acur)[MW], int q, uint32_t lf) {
-  const int c = trail_class<MW>(tv, acur, q);
-  return c == 1 || (c == 2 && trail_lex<MW>(tv, acur, q, lf));
+  const uint32_t f = trail_flags<MW>(tv, acur, q);
+  return (f & 1u) || ((f & 2u) && trail_lex<MW>(tv, acur, q, lf));
 }
 
 // Pending lexeme's winner at an emission: the first accept-list entry (highest
-// priority, ties to the lower id) that passes the lexicon word test and is
-// ignored or allowed.  -1 if none.  lf_of() yields the lexeme's lexicon flags
-// and is called at most once, only if a candidate's category is restricted.
+// priority, ties to the lower id) that is ignored or allowed and passes the
+// lexicon word test.  -1 if none.  lf_of() yields the lexeme's lexicon flags
+// and is called at most once, only for an allowed candidate whose category is
+// restricted.
 template <int MW, class LexFlags>
 __device__ inline int winner_of(const TermView& tv, const uint32_t* acc_off, const uint8_t* acc_list,
                                 const uint32_t (&acur)[MW], int q, LexFlags lf_of) {
@@ -544,6 +554,11 @@ __device__ inline int winner_of(const TermView& tv, const uint32_t* acc_off, con
   bool have_lf = false;
   for (uint32_t j = acc_off[q]; j < acc_off[q + 1]; ++j) {
     const int t = acc_list[j];
+    bool ok = bit_of(tv.I, t);
+#pragma unroll
+    for (int w = 0; w < MW; ++w)
+      if (w == (t >> 5)) ok = ok || ((acur[w] >> (t & 31)) & 1u);
+    if (!ok) continue;
     if (bit_of(tv.R, t)) {
       if (!have_lf) {
         lf = lf_of();
@@ -551,11 +566,7 @@ __device__ inline int winner_of(const TermView& tv, const uint32_t* acc_off, con
       }
       if (!((lf >> (8 + ((tv.tinfo[t] >> 8) & 0xFFu))) & 1u)) continue;
     }
-    bool ok = bit_of(tv.I, t);
-#pragma unroll
-    for (int w = 0; w < MW; ++w)
-      if (w == (t >> 5)) ok = ok || ((acur[w] >> (t & 31)) & 1u);
-    if (ok) return t;
+    return t;
   }
   return -1;
 }
@@ -569,24 +580,22 @@ __device__ inline int winner_of(const TermView& tv, const uint32_t* acc_off, con
 template <int MW>
 __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_config* __restrict__ cfgs,
                                                           const uint16_t* __restrict__ pool,
-                                                          uint32_t* __restrict__ mask,
                                                           uint8_t* __restrict__ eos_out,
                                                           uint8_t* __restrict__ ws, size_t rbytes) {
   extern __shared__ __align__(16) uint8_t plds[];
   const int row = blockIdx.x;
   const int tid = threadIdx.x;
   __shared__ uint16_t win[kStackWin];
-  __shared__ uint32_t A[8], I[8], R[8], Aw[8];
+  __shared__ uint32_t A[8], I[8], R[8], Aw[8], alive[8];
   __shared__ Post posts[256];
   __shared__ uint16_t scratch[kBlock][kPostCap + kTmpCap];
   __shared__ int bad, overflow, winner, eos_ok;
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
-  const RowLayout L = row_layout(tb.T);
+  const RowLayout L = row_layout(tb.T, tb.U);
   Post* post = (Post*)(rw + L.post);
   uint32_t* a2 = (uint32_t*)(rw + L.a2);
   const grid_config cfg = cfgs[row];
-  uint32_t* mrow = mask + (size_t)row * tb.W;
   const ParseTabs pt = stage_parse(tb, plds, parse_lds(tb, 0), tid, kBlock);
 
   if (tid == 0) {
@@ -601,7 +610,10 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     winner = -1;
     eos_ok = 0;
   }
-  for (int w = tid; w < tb.W; w += kBlock) mrow[w] = 0u;
+  {
+    uint64_t* sm = (uint64_t*)(rw + L.smask);
+    for (int i = tid; i < (tb.U + 63) / 64; i += kBlock) sm[i] = 0ull;
+  }
   __syncthreads();
   const uint32_t depth = cfg.stk_depth;
   const uint32_t lo = depth > (uint32_t)kStackWin ? depth - kStackWin : 0;
@@ -641,6 +653,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     R[tid] = rw8;
     A[tid] = 0;
     Aw[tid] = 0;
+    alive[tid] = 0;
   }
   const BaseStack bs{pool + cfg.stk_off, win, depth, lo};
   uint16_t* my = scratch[tid];
@@ -702,7 +715,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   }
   __syncthreads();
   // phase 3: first-byte table
-  uint2* fb = (uint2*)(rw + L.fb);
+  uint32_t* fb = (uint32_t*)(rw + L.fb);
   {
     const int b = tid;  // kBlock == 256: one byte value per thread
     const uint32_t c = tb.bclass[b];
@@ -736,10 +749,12 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
         fresh = 1;
       }
     }
-    if (kind == kFbDead || sl.restricted == 0) lex1 = kNoLex;
-    fb[b] = make_uint2(q1 | kind << 16 | fresh << 18 | t1 << 24, lex1);
+    fb[b] = q1 | kind << 16 | fresh << 18 | t1 << 24;
+    if (kind != kFbDead) atomicOr(&alive[b >> 5], 1u << (b & 31));
   }
+  __syncthreads();
   if (tid < 8) {
+    hdr->alive[tid] = alive[tid];
     hdr->A[tid] = A[tid];
     hdr->Aw[tid] = Aw[tid];
     hdr->R[tid] = R[tid];
@@ -747,7 +762,6 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   if (tid == 0) {
     hdr->eos_ok = (uint32_t)eos_ok;
     if (eos_out) eos_out[row] = (uint8_t)eos_ok;
-    if (eos_ok && tb.eos_id >= 0) atomicOr(&mrow[tb.eos_id >> 5], 1u << (tb.eos_id & 31));
     hdr->winner = w;
     hdr->slow_count = 0;
     hdr->wstat = 0;
@@ -777,7 +791,11 @@ struct RowCtx {
   TermView tv;
   const uint32_t* acc_off;  // accept-list offsets (LDS or global)
   const uint8_t* acc_list;  // accept lists (LDS or global)
-  const uint32_t* a2;       // row's allowed sets after each first shift (global)
+  const uint32_t* a2;       // row's allowed sets after each first shift
+  int a2_stride;            // words per terminal in a2
+  const uint8_t* clsA;      // trailing flags per DFA state under A(sigma), or null
+  const uint8_t* clsW;      // the same after shifting the winner, or null
+  int winner;               // the pending lexeme's winner (-1 none)
   const Post* post;         // row's stacks after each first shift (global)
 };
 
@@ -795,7 +813,7 @@ __device__ __forceinline__ int emit(const RowCtx& rc, Lane<MW>& ln, uint16_t* ov
     ln.mode = 1;
     ln.t1 = t;
 #pragma unroll
-    for (int w = 0; w < MW; ++w) ln.acur[w] = rc.a2[t * 8 + w];
+    for (int w = 0; w < MW; ++w) ln.acur[w] = rc.a2[t * rc.a2_stride + w];
     return 1;
   }
   if (ln.mode == 1) {
@@ -809,13 +827,6 @@ __device__ __forceinline__ int emit(const RowCtx& rc, Lane<MW>& ln, uint16_t* ov
   const int r = sim1_shift(rc.pt, rc.bs, ln.k, ln.m, ov, cap, t);
   if (r != 1) return r < 0 ? -1 : 0;
   return allowed_set<MW>(rc.pt, rc.bs, ln.k, ln.m, ov, ov + ln.m, cap - ln.m, ln.acur) < 0 ? -1 : 1;
-}
-
-__device__ inline void set_alias_bits(const Tables& tb, uint32_t* mrow, int u) {
-  for (uint32_t j = tb.alias_off[u]; j < tb.alias_off[u + 1]; ++j) {
-    const int id = tb.alias_ids[j];
-    atomicOr(&mrow[id >> 5], 1u << (id & 31));
-  }
 }
 
 struct DfaView {  // lexer DFA by byte class (LDS copy or global)
@@ -842,10 +853,13 @@ __device__ __forceinline__ int walk_bytes(const RowCtx& rc, Lane<MW>& ln, int q,
                                           int cap) {
   const Tables& tb = *rc.tb;
   const bool track = rc.sl.restricted != 0;
+  // trailing flags of a state: from the row's table while the lane's allowed
+  // set is that of sigma or of the winner's shift, else computed
+  const uint8_t* ctab = ln.mode == 0 ? rc.clsA : (ln.mode == 1 && ln.t1 == rc.winner ? rc.clsW : nullptr);
   int status = 2;         // 2 running, else the result
   int pend = -1;          // byte class waiting for an emission
   uint32_t pend_b = 0;    // that byte
-  int cls = 1;            // trailing class after the last byte taken
+  uint32_t f = 1;         // trailing flags after the last byte taken
   for (;;) {
     for (;;) {  // scan phase
       const bool run = status == 2 && pend < 0 && i < n;
@@ -856,9 +870,9 @@ __device__ __forceinline__ int walk_bytes(const RowCtx& rc, Lane<MW>& ln, int q,
         const int nq = step.next(q, c);
         if (nq != kDead) {
           q = nq;
-          if (track) lex_push(tb, rc.sl, lx, b);
-          cls = trail_class<MW>(rc.tv, ln.acur, q);
-          if (cls == 0) status = 0;
+          if (lx.need) lex_push(tb, rc.sl, lx, b);
+          f = ctab ? (uint32_t)ctab[q] : trail_flags<MW>(rc.tv, ln.acur, q);
+          if (f == 0) status = 0;
           else ++i;
         } else {
           pend = (int)c;
@@ -867,7 +881,7 @@ __device__ __forceinline__ int walk_bytes(const RowCtx& rc, Lane<MW>& ln, int q,
       }
     }
     if (status == 2 && pend < 0)  // the spelling ended inside a lexeme
-      status = (cls == 1 || trail_lex<MW>(rc.tv, ln.acur, q, lex_flags_now(tb, rc.sl, lx))) ? 1 : 0;
+      status = ((f & 1u) || trail_lex<MW>(rc.tv, ln.acur, q, lex_flags_now(tb, rc.sl, lx))) ? 1 : 0;
     const bool em = status == 2 && pend >= 0;
     if (!__any(em)) break;
     if (em) {  // emission phase
@@ -875,11 +889,11 @@ __device__ __forceinline__ int walk_bytes(const RowCtx& rc, Lane<MW>& ln, int q,
       if (r <= 0) {
         status = r;
       } else {
+        ctab = ln.mode == 0 ? rc.clsA : (ln.mode == 1 && ln.t1 == rc.winner ? rc.clsW : nullptr);
         q = step.next(kStart, (uint32_t)pend);
-        lx.w = pend_b;
-        lx.len = 1;
-        cls = q == kDead ? 0 : trail_class<MW>(rc.tv, ln.acur, q);
-        if (cls == 0) status = 0;
+        f = q == kDead ? 0u : (ctab ? (uint32_t)ctab[q] : trail_flags<MW>(rc.tv, ln.acur, q));
+        lx = LexState{pend_b, 1u, kNoLex, track && (f & 2u) ? 1u : 0u};
+        if (f == 0) status = 0;
         else ++i;
         pend = -1;
       }
@@ -892,18 +906,21 @@ __device__ __forceinline__ int walk_bytes(const RowCtx& rc, Lane<MW>& ln, int q,
 // Per-row data a walk workgroup keeps in LDS for every row of its group.
 struct RowLds {
   uint32_t A[8], Aw[8], R[8];
-  uint32_t valid;
-  uint32_t stk_off, stk_depth;
-  uint32_t slot;
+  uint32_t alive[8];  // first bytes whose first-byte entry is not rejected
+  Slot sl;
+  uint32_t valid, stk_off, stk_depth;
   uint32_t rem_lo, rem_hi;  // first 8 bytes of the pending lexeme
   uint32_t rem_len;
-  uint32_t pad;
+  uint32_t lexnode;         // lexicon node of the pending lexeme
+  int32_t winner;           // its winner when a byte ends it (-1 none)
+  uint32_t pad[17];
 };
-static_assert(sizeof(RowLds) == 128, "row record is 128 bytes");
+static_assert(sizeof(RowLds) == 256, "row record is 256 bytes");
 
 struct WalkLds {  // byte offsets into dynamic LDS
-  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, live, lanes, rows, fb, total;
-  int group;  // rows per group
+  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, live, range, lanes, rows, fb, cls, total;
+  uint32_t cls_row;  // bytes per row of trailing-flag tables (two of S entries)
+  int group;         // rows per group
   ParseLds pl;
 };
 
@@ -927,29 +944,35 @@ __host__ __device__ inline WalkLds walk_lds(const Tables& tb, int mw, int B) {
   o += w.pl.total;
   w.live = o;
   o += pad16((uint32_t)(tb.S * mw * 4));
+  w.range = o;
+  o += pad16((uint32_t)((tb.U + 63) / 64) * 2);
   w.lanes = o;
   o += kWalkThreads * kFastLane * 2;
-  // as many rows as fit, at most kRowGroup and B
-  const uint32_t per_row = sizeof(RowLds) + 256 * 8;
+  // as many rows as fit beside the static LDS (counters), at most kRowGroup
+  // and B
+  const uint32_t fixed = o + 64;
+  w.cls_row = 2 * pad16((uint32_t)tb.S);
+  const uint32_t per_row = sizeof(RowLds) + 256 * 4 + w.cls_row;
   int g = kRowGroup < B ? kRowGroup : B;
-  while (g > 1 && o + per_row * (uint32_t)g > kWalkLdsMax) --g;
+  while (g > 1 && fixed + per_row * (uint32_t)g > kWalkLdsMax) --g;
   w.group = g;
   w.rows = o;
   o += sizeof(RowLds) * (uint32_t)g;
   w.fb = o;
-  o += 256 * 8 * (uint32_t)g;
+  o += 256 * 4 * (uint32_t)g;
+  w.cls = o;
+  o += w.cls_row * (uint32_t)g;
   w.total = o;
   return w;
 }
 
 // Bytes 1, 2, ... of one spelling, called in that order: a 64-bit window
-// holds the next bytes, taken from the record (bytes 0..7), the first tail
-// chunk fetched with the record (bytes 8..23), then one 16-byte load per
-// further tail chunk.
+// holds the next bytes, taken from the record (bytes 0..7), the tail chunk
+// fetched with it (bytes 8..23), then one 16-byte load per overflow chunk.
 struct SpellBytes {
-  uint64_t win;       // next bytes, lowest first
-  uint64_t lo0, hi;   // bytes 8..15, and the second half of the current tail chunk
-  const uint4* tail;  // chunk c holds bytes 8 + 16c .. 23 + 16c
+  uint64_t win;      // next bytes, lowest first
+  uint64_t lo0, hi;  // bytes 8..15; the second half of the current chunk
+  const uint4* ovf;  // overflow chunk c holds bytes 24 + 16c .. 39 + 16c
   __device__ uint32_t operator()(uint32_t i) {
     if (i >= 8 && (i & 7) == 0) {
       if (i == 8) {
@@ -957,7 +980,7 @@ struct SpellBytes {
       } else if ((i & 15) == 0) {
         win = hi;
       } else {
-        const uint4 c = tail[(i - 8) >> 4];
+        const uint4 c = ovf[(i - 24) >> 4];
         win = (uint64_t)c.x | (uint64_t)c.y << 32;
         hi = (uint64_t)c.z | (uint64_t)c.w << 32;
       }
@@ -968,6 +991,17 @@ struct SpellBytes {
   }
 };
 
+// Some first byte in [lo, hi] opens a token (bit set in the 256-bit mask).
+__device__ inline bool any_in_range(const uint32_t* m, uint32_t lo, uint32_t hi) {
+  for (uint32_t w = lo >> 5; w <= (hi >> 5); ++w) {
+    uint32_t bits = m[w];
+    if (w == (lo >> 5)) bits &= 0xFFFFFFFFu << (lo & 31);
+    if (w == (hi >> 5)) bits &= 0xFFFFFFFFu >> (31 - (hi & 31));
+    if (bits) return true;
+  }
+  return false;
+}
+
 __device__ inline int wave_grab(int* ctr) {
   int v = 0;
   if ((threadIdx.x & 63) == 0) v = atomicAdd(ctr, 1);
@@ -975,37 +1009,43 @@ __device__ inline int wave_grab(int* ctr) {
 }
 
 // Persistent, one workgroup per compute unit.  The grammar tables are staged
-// once; then, for each group of up to kRowGroup rows, the rows' first-byte
-// tables and scalars are staged and the workgroup's share of the (row,
-// 64-spelling sub-tile) items -- every gridDim.x-th item in row-major order,
-// so each workgroup sees every row and all of the vocabulary -- is taken by
-// its waves one item at a time from an LDS counter, with no barrier between
-// items.
+// once; then, for each group of rows that fits, the rows' first-byte tables
+// and scalars are staged.  A work item is one row against one 64-spelling
+// sub-tile.  The workgroup's share of the items -- every gridDim.x-th in
+// row-major order, so each workgroup sees every row and all of the
+// vocabulary -- is taken by its waves one item at a time from an LDS counter;
+// items whose spellings cannot start a token (the sub-tile's first-byte range
+// misses the row's table) are passed over without loading anything, and the
+// next live item's records and tail chunks are in flight while one is walked.
+// There is no barrier between items.
 template <int MW>
 __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const grid_config* __restrict__ cfgs,
                                                             const uint16_t* __restrict__ pool,
-                                                            uint32_t* __restrict__ mask,
                                                             uint8_t* __restrict__ ws, size_t rbytes, int B) {
   extern __shared__ __align__(16) uint8_t lds[];
   __shared__ int item_ctr;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const WalkLds WL = walk_lds(tb, MW, B);
-  const RowLayout RL = row_layout(tb.T);
+  const RowLayout RL = row_layout(tb.T, tb.U);
   uint8_t* bcls = lds + WL.bcls;
   uint32_t* tinfo_s = (uint32_t*)(lds + WL.tinfo);
   uint32_t* I_s = (uint32_t*)(lds + WL.I);
   uint32_t* live_s = (uint32_t*)(lds + WL.live);
   RowLds* rows_s = (RowLds*)(lds + WL.rows);
-  const uint2* fb_all = (const uint2*)(lds + WL.fb);
+  const uint32_t* fb_all = (const uint32_t*)(lds + WL.fb);
+  uint8_t* cls_all = lds + WL.cls;
+  const uint16_t* range_s = (const uint16_t*)(lds + WL.range);
   uint16_t* lane_area = (uint16_t*)(lds + WL.lanes) + tid * kFastLane;
   uint8_t* rows = ws + kWsHead;
+  const int nsub = (tb.U + kSub - 1) / kSub;
 
   // grammar tables, once per workgroup
   stage16(lds + WL.dfa, (const uint8_t*)tb.dfa, (uint32_t)(tb.S * tb.C * 2), tid, kWalkThreads);
   stage16(bcls, tb.bclass, 256, tid, kWalkThreads);
   stage16(lds + WL.acc_off, (const uint8_t*)tb.acc_off, (uint32_t)(tb.S + 1) * 4, tid, kWalkThreads);
   stage16(lds + WL.acc_list, tb.acc_list, (uint32_t)tb.n_acc, tid, kWalkThreads);
+  stage16(lds + WL.range, (const uint8_t*)tb.sub_range, (uint32_t)nsub * 2, tid, kWalkThreads);
   const ParseTabs pt = stage_parse(tb, lds, WL.pl, tid, kWalkThreads);
   for (int i = tid; i < tb.S * MW; i += kWalkThreads) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
   for (int t = tid; t < 256; t += kWalkThreads) tinfo_s[t] = t < tb.T ? tb.term_info[t] : 0u;
@@ -1019,13 +1059,13 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
 
   const DfaView step{(const uint16_t*)(lds + WL.dfa), bcls, tb.C};
   const uint4* recs = tb.spell_rec;
-  const int nsub = (tb.U + kSub - 1) / kSub;
+  const uint4* tails = tb.spell_tail;
   for (int g0 = 0; g0 < B; g0 += WL.group) {
     const int gr = min(WL.group, B - g0);
     __syncthreads();  // the previous group is done with the row tables
     for (int r = 0; r < gr; ++r) {
       const uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
-      stage16((uint8_t*)(fb_all + r * 256), rw + RL.fb, 256 * 8, tid, kWalkThreads);
+      stage16((uint8_t*)(fb_all + r * 256), rw + RL.fb, 256 * 4, tid, kWalkThreads);
     }
     for (int r = tid; r < gr; r += kWalkThreads) {
       const RowHeader* hdr = (const RowHeader*)(rows + (size_t)(g0 + r) * rbytes);
@@ -1035,130 +1075,160 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
         rl.A[w] = hdr->A[w];
         rl.Aw[w] = hdr->Aw[w];
         rl.R[w] = hdr->R[w];
+        rl.alive[w] = hdr->alive[w];
       }
       rl.valid = hdr->valid;
       rl.stk_off = cfg.stk_off;
       rl.stk_depth = cfg.stk_depth;
-      rl.slot = cfg.slot;
+      rl.sl = load_slot(tb, rl.valid == kRowValid ? cfg.slot : 0);
       rl.rem_lo = (uint32_t)cfg.rem_head[0] | (uint32_t)cfg.rem_head[1] << 8 | (uint32_t)cfg.rem_head[2] << 16 |
                   (uint32_t)cfg.rem_head[3] << 24;
       rl.rem_hi = (uint32_t)cfg.rem_head[4] | (uint32_t)cfg.rem_head[5] << 8 | (uint32_t)cfg.rem_head[6] << 16 |
                   (uint32_t)cfg.rem_head[7] << 24;
       rl.rem_len = cfg.flags & 1u ? 0u : cfg.rem_len;
+      rl.lexnode = cfg.lexnode;
+      rl.winner = hdr->winner >= 0 && !((I_s[hdr->winner >> 5] >> (hdr->winner & 31)) & 1u) ? hdr->winner : -1;
     }
     if (tid == 0) item_ctr = 0;
     __syncthreads();
-
-    // this workgroup's items: j = blockIdx.x + k * gridDim.x, row j / nsub,
-    // sub-tile j % nsub.  Two deep: while item k0 is walked, the record of
-    // k2 and the first tail chunk of k1 (whose record has arrived) are in
-    // flight.
-    const int total = gr * nsub;
-    auto rec_of = [&](int k) -> uint4 {
-      const int j = blockIdx.x + k * gridDim.x;
-      const int uu = (j % nsub) * kSub + lane;
-      return recs[(j < total && uu < tb.U) ? uu : 0];
-    };
-    int k0 = wave_grab(&item_ctr);
-    int k1 = wave_grab(&item_ctr);
-    uint4 rk0 = rec_of(k0);
-    uint4 rk1 = rec_of(k1);
-    uint4 tl0 = tb.spell_tail[rk0.w >> 8];
-    for (;;) {
-      const int j0 = blockIdx.x + k0 * gridDim.x;
-      if (j0 >= total) break;
-      const int k2 = wave_grab(&item_ctr);
-      const uint4 rk2 = rec_of(k2);
-      const uint4 tl1 = tb.spell_tail[rk1.w >> 8];
-      const int r = j0 / nsub;
-      const int u = (j0 - r * nsub) * kSub + lane;
+    // trailing flags of every DFA state under A(sigma) and after the winner's shift
+    for (int i = tid; i < gr * tb.S; i += kWalkThreads) {
+      const int r = i / tb.S, q = i - r * tb.S;
       const RowLds& rl = rows_s[r];
-      const uint32_t n = (u < tb.U) ? (rk0.w & 0xFFu) : 0u;
-      const uint64_t h = (uint64_t)rk0.x | (uint64_t)rk0.y << 32;
-      const uint2 e = fb_all[r * 256 + (h & 0xFF)];
-      const uint32_t kind = (e.x >> 16) & 3u;
-      if (rl.valid == kRowValid && n != 0 && kind != kFbDead) {
-        uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
+      const TermView tv{tinfo_s, I_s, rl.R, live_s, MW};
+      uint32_t a[MW], aw[MW];
+#pragma unroll
+      for (int w = 0; w < MW; ++w) {
+        a[w] = rl.A[w];
+        aw[w] = rl.Aw[w];
+      }
+      uint8_t* ct = cls_all + r * WL.cls_row;
+      ct[q] = (uint8_t)trail_flags<MW>(tv, a, q);
+      ct[WL.cls_row / 2 + q] = (uint8_t)trail_flags<MW>(tv, aw, q);
+    }
+    __syncthreads();
+
+    // item k: j = blockIdx.x + k * gridDim.x, row j / nsub, sub-tile j % nsub
+    const int total = gr * nsub;
+    const int mine = total > (int)blockIdx.x ? (total - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x : 0;
+    auto spelling = [&](int k, int& r) -> int {
+      const int j = (int)blockIdx.x + (k < mine ? k : 0) * (int)gridDim.x;
+      r = j / nsub;
+      return (j - r * nsub) * kSub + lane;
+    };
+    auto next_live = [&]() -> int {
+      for (;;) {
+        const int k = wave_grab(&item_ctr);
+        if (k >= mine) return k;
+        const int j = (int)blockIdx.x + k * (int)gridDim.x;
+        const int r = j / nsub;
+        const uint32_t rg = range_s[j - r * nsub];
+        if (rows_s[r].valid == kRowValid && any_in_range(rows_s[r].alive, rg & 0xFFu, rg >> 8)) return k;
+      }
+    };
+    int k0 = next_live();
+    int r0;
+    int u = spelling(k0, r0);
+    uint4 rk = recs[u < tb.U ? u : 0];
+    uint4 tl = tails[u < tb.U ? u : 0];
+    while (k0 < mine) {
+      const int k1 = next_live();
+      int r1;
+      const int u1 = spelling(k1, r1);
+      const uint4 rk1 = recs[u1 < tb.U ? u1 : 0];
+      const uint4 tl1 = tails[u1 < tb.U ? u1 : 0];
+
+      const RowLds& rl = rows_s[r0];
+      const uint32_t n = u < tb.U ? (rk.w & 0xFFu) : 0u;
+      const uint64_t h = (uint64_t)rk.x | (uint64_t)rk.y << 32;
+      const uint32_t b0 = (uint32_t)(h & 0xFF);
+      const uint32_t e = fb_all[r0 * 256 + b0];
+      const uint32_t kind = (e >> 16) & 3u;
+      if (n != 0 && kind != kFbDead) {
+        uint8_t* rw = rows + (size_t)(g0 + r0) * rbytes;
         RowCtx rc;
         rc.tb = &tb;
         rc.pt = pt;
         rc.bs = BaseStack{pool + rl.stk_off, nullptr, rl.stk_depth, rl.stk_depth};
-        rc.sl = load_slot(tb, rl.slot);
+        rc.sl = rl.sl;
         rc.tv = TermView{tinfo_s, I_s, rl.R, live_s, MW};
         rc.acc_off = (const uint32_t*)(lds + WL.acc_off);
         rc.acc_list = lds + WL.acc_list;
         rc.a2 = (const uint32_t*)(rw + RL.a2);
+        rc.a2_stride = 8;
         rc.post = (const Post*)(rw + RL.post);
+        rc.clsA = cls_all + r0 * WL.cls_row;
+        rc.clsW = rc.clsA + WL.cls_row / 2;
+        rc.winner = rl.winner;
         Lane<MW> ln;
         ln.mode = (int)kind - 1;
-        ln.t1 = (int)(e.x >> 24);
+        ln.t1 = (int)(e >> 24);
         ln.k = 0;
         ln.m = 0;
 #pragma unroll
         for (int w = 0; w < MW; ++w) ln.acur[w] = kind == kFbMode0 ? rl.A[w] : rl.Aw[w];
         SpellBytes byte_at;
         byte_at.win = h >> 8;
-        byte_at.lo0 = (uint64_t)tl0.x | (uint64_t)tl0.y << 32;
-        byte_at.hi = (uint64_t)tl0.z | (uint64_t)tl0.w << 32;
-        byte_at.tail = tb.spell_tail + (rk0.w >> 8);
-        // the lexeme after byte 0: a new one, or the pending lexeme plus the byte
+        byte_at.lo0 = (uint64_t)tl.x | (uint64_t)tl.y << 32;
+        byte_at.hi = (uint64_t)tl.z | (uint64_t)tl.w << 32;
+        byte_at.ovf = tails + (rk.w >> 8);
+        // the lexeme after byte 0: a new one, or the pending lexeme plus the
+        // byte; the lexicon follows it only if a restricted terminal is viable
+        const int q1 = (int)(e & 0xFFFF);
+        const uint8_t* ct = kind == kFbMode0 ? rc.clsA : rc.clsW;
         LexState lx;
-        const uint32_t b0 = (uint32_t)(h & 0xFF);
-        if ((e.x >> 18) & 1u) {
-          lx = LexState{b0, 1u, kNoLex};
+        lx.need = rl.sl.restricted != 0 && (ct[q1] & 2u) ? 1u : 0u;
+        if ((e >> 18) & 1u) {
+          lx.w = b0;
+          lx.len = 1;
+          lx.node = kNoLex;
         } else {
           lx.len = rl.rem_len + 1;
-          lx.node = e.y;
           lx.w = lx.len <= 8 ? (((uint64_t)rl.rem_lo | (uint64_t)rl.rem_hi << 32) | (uint64_t)b0 << (8 * rl.rem_len))
                              : 0ull;
+          lx.node = lx.need && lx.len > 8 ? lex_child(tb, rl.sl, rl.lexnode, b0) : kNoLex;
         }
-        const int ok = walk_bytes<MW>(rc, ln, (int)(e.x & 0xFFFF), lx, 1u, n, byte_at, step, lane_area, kFastLane);
-        uint32_t* mrow = mask + (size_t)(g0 + r) * tb.W;
-        if (ok > 0) {
-          const uint32_t id = rk0.z;
-          if (!(id >> 31)) atomicOr(&mrow[id >> 5], 1u << (id & 31));
-          else set_alias_bits(tb, mrow, u);
-        }
-        const uint64_t allowed = __ballot(ok > 0);
-        if (allowed && lane == __ffsll((unsigned long long)allowed) - 1) ((RowHeader*)rw)->nonempty = 1u; else if (ok < 0) {  // the lane's stack area is too small: hand over
+        const int ok = walk_bytes<MW>(rc, ln, q1, lx, 1u, n, byte_at, step, lane_area, kFastLane);
+        if (ok < 0) {  // the lane's stack area is too small: hand over
           RowHeader* hdr = (RowHeader*)rw;
           const uint32_t slot = atomicAdd(&hdr->slow_count, 1u);
           if (slot < (uint32_t)kSlowCap) ((uint32_t*)(rw + RL.slow))[slot] = (uint32_t)u;
           else atomicOr(&hdr->wstat, GRID_ROW_OVERFLOW);
         }
+        // the sub-tile's word of the sorted-spelling mask: one wave owns it
+        const uint64_t allowed = __ballot(ok > 0);
+        if (allowed && lane == __ffsll((unsigned long long)__ballot(1)) - 1) {
+          ((uint64_t*)(rw + RL.smask))[u / kSub] = allowed;
+          ((RowHeader*)rw)->nonempty = 1u;
+        }
       }
       k0 = k1;
-      rk0 = rk1;
-      tl0 = tl1;
-      k1 = k2;
-      rk1 = rk2;
+      r0 = r1;
+      u = u1;
+      rk = rk1;
+      tl = tl1;
     }
   }
+
 }
 
-// ---------------------------------------------------------------- finalize
-// Re-walks handed-over spellings from the row's configuration with a large
-// stack area in the workspace, then combines the status bits.
+// -------------------------------------------------------------- slow path
+// Re-walks the spellings the walk handed over (its LDS stack area was too
+// small) from the row's configuration, with a large stack area per thread in
+// the workspace, and sets their bits in the sorted-spelling mask.
 template <int MW>
-__global__ __launch_bounds__(kSlowThreads) void finalize_kernel(Tables tb, const grid_config* __restrict__ cfgs,
-                                                                const uint16_t* __restrict__ pool,
-                                                                uint32_t* __restrict__ mask,
-                                                                uint8_t* __restrict__ ws, size_t rbytes,
-                                                                int32_t* __restrict__ status) {
-  extern __shared__ __align__(16) uint8_t flds[];
+__global__ __launch_bounds__(kSlowThreads) void slow_kernel(Tables tb, const grid_config* __restrict__ cfgs,
+                                                            const uint16_t* __restrict__ pool,
+                                                            uint8_t* __restrict__ ws, size_t rbytes) {
+  extern __shared__ __align__(16) uint8_t slds[];
   const int row = blockIdx.x;
   const int tid = threadIdx.x;
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
-  const RowLayout RL = row_layout(tb.T);
-  uint32_t* mrow = mask + (size_t)row * tb.W;
-  __shared__ uint32_t any;
-  __shared__ int slow_err;
+  const RowLayout RL = row_layout(tb.T, tb.U);
+  const uint32_t count = hdr->valid == kRowValid ? min(hdr->slow_count, (uint32_t)kSlowCap) : 0u;
+  if (count == 0) return;  // uniform
   __shared__ uint32_t I_s[8];
-  if (tid == 0) {
-    any = 0;
-    slow_err = 0;
-  }
   if (tid < 8) {
     uint32_t iw = 0;
     for (int j = 0; j < 32; ++j) {
@@ -1167,57 +1237,93 @@ __global__ __launch_bounds__(kSlowThreads) void finalize_kernel(Tables tb, const
     }
     I_s[tid] = iw;
   }
-  const bool valid = hdr->valid == kRowValid;
-  const uint32_t count = valid ? min(hdr->slow_count, (uint32_t)kSlowCap) : 0u;
-  ParseTabs pt = global_parse(tb);
-  if (count > 0) pt = stage_parse(tb, flds, parse_lds(tb, 0), tid, kSlowThreads);
+  const ParseTabs pt = stage_parse(tb, slds, parse_lds(tb, 0), tid, kSlowThreads);
   __syncthreads();
-  if (count > 0) {
-    const grid_config cfg = cfgs[row];
-    RowCtx rc;
-    rc.tb = &tb;
-    rc.pt = pt;
-    rc.bs = BaseStack{pool + cfg.stk_off, nullptr, cfg.stk_depth, cfg.stk_depth};
-    rc.sl = load_slot(tb, cfg.slot);
-    rc.tv = TermView{tb.term_info, I_s, hdr->R, tb.live, 8};
-    rc.acc_off = tb.acc_off;
-    rc.acc_list = tb.acc_list;
-    rc.a2 = (const uint32_t*)(rw + RL.a2);
-    rc.post = (const Post*)(rw + RL.post);
-    uint16_t* ov = (uint16_t*)(rw + RL.slow_ov) + tid * kSlowLane;
-    const DfaView step{tb.dfa, tb.bclass, tb.C};
-    LexState lex0;
-    lex0.len = cfg.flags & 1u ? 0u : cfg.rem_len;
-    lex0.node = cfg.lexnode;
-    lex0.w = 0;
-    for (int k = 0; k < 8; ++k) lex0.w |= (uint64_t)cfg.rem_head[k] << (8 * k);
-    for (uint32_t k = tid; k < count; k += kSlowThreads) {
-      const int u = (int)((const uint32_t*)(rw + RL.slow))[k];
-      Lane<MW> ln;
-      ln.mode = 0;
-      ln.t1 = -1;
-      ln.k = 0;
-      ln.m = 0;
+  const grid_config cfg = cfgs[row];
+  RowCtx rc;
+  rc.tb = &tb;
+  rc.pt = pt;
+  rc.bs = BaseStack{pool + cfg.stk_off, nullptr, cfg.stk_depth, cfg.stk_depth};
+  rc.sl = load_slot(tb, cfg.slot);
+  rc.tv = TermView{tb.term_info, I_s, hdr->R, tb.live, 8};
+  rc.acc_off = tb.acc_off;
+  rc.acc_list = tb.acc_list;
+  rc.a2 = (const uint32_t*)(rw + RL.a2);
+  rc.a2_stride = 8;
+  rc.post = (const Post*)(rw + RL.post);
+  rc.clsA = nullptr;
+  rc.clsW = nullptr;
+  rc.winner = -1;
+  uint16_t* ov = (uint16_t*)(rw + RL.slow_ov) + tid * kSlowLane;
+  const DfaView step{tb.dfa, tb.bclass, tb.C};
+  LexState lex0;
+  lex0.len = cfg.flags & 1u ? 0u : cfg.rem_len;
+  lex0.node = cfg.lexnode;
+  lex0.need = rc.sl.restricted != 0 ? 1u : 0u;
+  lex0.w = 0;
+  for (int k = 0; k < 8; ++k) lex0.w |= (uint64_t)cfg.rem_head[k] << (8 * k);
+  for (uint32_t k = tid; k < count; k += kSlowThreads) {
+    const int su = (int)((const uint32_t*)(rw + RL.slow))[k];
+    Lane<MW> ln;
+    ln.mode = 0;
+    ln.t1 = -1;
+    ln.k = 0;
+    ln.m = 0;
 #pragma unroll
-      for (int w = 0; w < MW; ++w) ln.acur[w] = hdr->A[w];
-      const uint32_t base = tb.spell_off[u];
-      auto byte_at = [&](uint32_t i) -> uint32_t { return tb.spell_bytes[base + i]; };
-      const int ok = walk_bytes<MW>(rc, ln, cfg.q, lex0, 0u, tb.spell_off[u + 1] - base, byte_at, step, ov,
-                                    kSlowLane);
-      if (ok > 0) {
-        set_alias_bits(tb, mrow, u);
-        any = 1;
-      }
-      if (ok < 0) slow_err = 1;
+    for (int w = 0; w < MW; ++w) ln.acur[w] = hdr->A[w];
+    const uint32_t base = tb.spell_off[su];
+    auto byte_at = [&](uint32_t i) -> uint32_t { return tb.spell_bytes[base + i]; };
+    const int ok = walk_bytes<MW>(rc, ln, cfg.q, lex0, 0u, tb.spell_off[su + 1] - base, byte_at, step, ov,
+                                  kSlowLane);
+    if (ok > 0) {
+      atomicOr((uint32_t*)(rw + RL.smask) + (su >> 5), 1u << (su & 31));
+      hdr->nonempty = 1u;
+    } else if (ok < 0) {
+      atomicOr(&hdr->wstat, GRID_ROW_OVERFLOW);
     }
   }
-  __syncthreads();
-  if (tid == 0) {
-    int32_t st = 0;
+}
+
+// ---------------------------------------------------------------- finalize
+// The row's mask over token ids, gathered from the sorted-spelling mask (each
+// id looks up its spelling, so every alias of an allowed spelling is set), the
+// end-of-sequence bit, and the row status.  kGatherGroups workgroups per row;
+// each wave builds 64 consecutive ids, i.e. two mask words, per step.
+__global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, uint32_t* __restrict__ mask,
+                                                          const uint8_t* __restrict__ ws, size_t rbytes,
+                                                          int32_t* __restrict__ status) {
+  const int row = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
+  const RowHeader* hdr = (const RowHeader*)rw;
+  const RowLayout RL = row_layout(tb.T, tb.U);
+  const uint64_t* sm = (const uint64_t*)(rw + RL.smask);
+  uint32_t* mrow = mask + (size_t)row * tb.W;
+  const bool valid = hdr->valid == kRowValid;
+  const int eos = valid && hdr->eos_ok ? tb.eos_id : -1;
+  // ids [64 c, 64 c + 64) for chunks c of this workgroup
+  const int n_chunks = (tb.V + 63) / 64;
+  const int per = (n_chunks + kGatherGroups - 1) / kGatherGroups;
+  const int c_end = min(n_chunks, ((int)blockIdx.y + 1) * per);
+  for (int c = (int)blockIdx.y * per + (tid >> 6); c < c_end; c += kBlock / 64) {
+    const int id = c * 64 + lane;
+    bool bit = false;
+    if (id < tb.V && valid) {
+      const uint32_t su = tb.spell_of_id[id];
+      bit = su != 0xFFFFFFFFu && ((sm[su >> 6] >> (su & 63)) & 1ull);
+    }
+    bit = bit || id == eos;
+    const uint64_t word = __ballot(bit);
+    if (lane == 0) mrow[2 * c] = (uint32_t)word;
+    if (lane == 1 && 2 * c + 1 < tb.W) mrow[2 * c + 1] = (uint32_t)(word >> 32);
+  }
+  if (blockIdx.y == 0 && tid == 0) {
+    int32_t st;
     if (valid) {
       st = hdr->pstat | hdr->wstat;
-      if (slow_err || hdr->slow_count > (uint32_t)kSlowCap) st |= GRID_ROW_OVERFLOW;
-      if (!any && !hdr->nonempty && !hdr->eos_ok) st |= GRID_ROW_EMPTY;
+      if (hdr->slow_count > (uint32_t)kSlowCap) st |= GRID_ROW_OVERFLOW;
+      if (!hdr->nonempty && !hdr->eos_ok) st |= GRID_ROW_EMPTY;
     } else {
       st = hdr->pstat | GRID_ROW_BAD_CONFIG;
     }
@@ -1301,23 +1407,24 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
                 uint8_t* eos, int32_t* status, uint8_t* ws, size_t rb, uint32_t phases, hipStream_t s) {
   const uint32_t parse_bytes = parse_lds(tb, 0).total;
   if (!raise_lds((const void*)prologue_kernel<MW>, parse_bytes) ||
-      !raise_lds((const void*)finalize_kernel<MW>, parse_bytes))
+      !raise_lds((const void*)slow_kernel<MW>, parse_bytes))
     return fail(GRID_E_HIP, "grid_mask: cannot raise the LDS limit");
   if (phases & GRID_PHASE_PROLOGUE)
-    hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool,
-                       mask, eos, ws, rb);
+    hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool, eos, ws,
+                       rb);
   if ((phases & GRID_PHASE_WALK) && tb.U > 0) {
     const WalkLds WL = walk_lds(tb, MW, B);
     const int n_items = ((tb.U + kSub - 1) / kSub) * std::min(B, WL.group);
     const int resident = walk_grid_size<MW>(WL.total);
     if (resident <= 0) return fail(GRID_E_HIP, "grid_mask: cannot raise the walk's LDS limit");
     const int blocks = std::min((n_items + kWalkThreads / 64 - 1) / (kWalkThreads / 64), resident);
-    hipLaunchKernelGGL(walk_kernel<MW>, dim3(blocks), dim3(kWalkThreads), WL.total, s, tb, cfg_dev, pool, mask, ws,
-                       rb, B);
+    hipLaunchKernelGGL(walk_kernel<MW>, dim3(blocks), dim3(kWalkThreads), WL.total, s, tb, cfg_dev, pool, ws, rb,
+                       B);
   }
+  if (phases & GRID_PHASE_WALK)
+    hipLaunchKernelGGL(slow_kernel<MW>, dim3(B), dim3(kSlowThreads), parse_bytes, s, tb, cfg_dev, pool, ws, rb);
   if (phases & GRID_PHASE_FINALIZE)
-    hipLaunchKernelGGL(finalize_kernel<MW>, dim3(B), dim3(kSlowThreads), parse_bytes, s, tb, cfg_dev, pool, mask,
-                       ws, rb, status);
+    hipLaunchKernelGGL(finalize_kernel, dim3(B, kGatherGroups), dim3(kBlock), 0, s, tb, mask, ws, rb, status);
   return GRID_OK;
 }
 
@@ -1325,9 +1432,16 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
 
 int grid::overlay_capacity() { return kFastLane; }
 
+static int n_spellings(const grid_compiled* g) { return (int)g->vocab.spell_off.size() - 1; }
+
+// head, then B rows
+static size_t workspace_size(const grid_compiled* g, int B) {
+  return kWsHead + row_layout(g->parser.T, n_spellings(g)).total * (size_t)B;
+}
+
 extern "C" size_t grid_mask_workspace_bytes(const grid_compiled* g, int32_t B) {
   if (!g || B <= 0) return 0;
-  return kWsHead + row_layout(g->parser.T).total * (size_t)B;
+  return workspace_size(g, B);
 }
 
 extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
@@ -1338,8 +1452,8 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   if (phases & ~GRID_PHASE_ALL) return fail(GRID_E_ARG, "grid_mask: unknown phase bits");
   if (!g || B <= 0 || B > 65535 || !cfg_dev || !stack_pool_dev || !mask_dev || !workspace_dev)
     return fail(GRID_E_ARG, "grid_mask: null pointer or batch size out of range");
-  const size_t rb = row_layout(g->parser.T).total;
-  if (workspace_bytes < kWsHead + rb * (size_t)B) return fail(GRID_E_ARG, "grid_mask: workspace too small");
+  const size_t rb = row_layout(g->parser.T, n_spellings(g)).total;
+  if (workspace_bytes < workspace_size(g, B)) return fail(GRID_E_ARG, "grid_mask: workspace too small");
   if (((uintptr_t)workspace_dev & 255) != 0) return fail(GRID_E_ARG, "grid_mask: workspace not 256-byte aligned");
   static const int needed[] = {GRID_ART_DFA_CLASS,   GRID_ART_BYTE_CLASS,  GRID_ART_DFA_ACCEPT_OFF,
                                GRID_ART_DFA_ACCEPT_LIST, GRID_ART_DFA_LIVE, GRID_ART_ACTION,
@@ -1347,7 +1461,8 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
                                GRID_ART_SPELL_BYTES, GRID_ART_SPELL_REC,   GRID_ART_SPELL_TAIL,
                                GRID_ART_ALIAS_OFF,   GRID_ART_ALIAS_IDS,   GRID_ART_LEX_FLAGS,
                                GRID_ART_LEX_HASH,    GRID_ART_LEX_SLOTS,   GRID_ART_PARSE_STATE,
-                               GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH,   GRID_ART_LEX_PREFIX};
+                               GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH,   GRID_ART_LEX_PREFIX,
+                               GRID_ART_SPELL_RANGE, GRID_ART_SPELL_OF_ID};
   for (int w : needed)
     if (!bound(g, w)) return fail(GRID_E_UNBOUND, "grid_mask: artifact " + std::to_string(w) + " is not bound");
   Tables tb;
@@ -1372,6 +1487,8 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   tb.lex_hash = (const uint32_t*)g->dev[GRID_ART_LEX_HASH];
   tb.lex_slots = (const uint32_t*)g->dev[GRID_ART_LEX_SLOTS];
   tb.lex_prefix = (const uint4*)g->dev[GRID_ART_LEX_PREFIX];
+  tb.sub_range = (const uint16_t*)g->dev[GRID_ART_SPELL_RANGE];
+  tb.spell_of_id = (const uint32_t*)g->dev[GRID_ART_SPELL_OF_ID];
   tb.S = g->dfa.S;
   tb.C = g->dfa.C;
   tb.T = g->parser.T;
@@ -1390,7 +1507,7 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   tb.hbits = g->parser.goto_hbits;
   const int mw = tb.tw <= 4 ? 4 : 8;
   const WalkLds WL = walk_lds(tb, mw, B);
-  if (tb.T > 255 || tb.tw > 8 || WL.total > kWalkLdsMax || parse_lds(tb, 0).total > 24 * 1024)
+  if (tb.T > 255 || tb.tw > 8 || WL.total + 64 > kWalkLdsMax || parse_lds(tb, 0).total > 24 * 1024)
     return fail(GRID_E_CAPACITY, "grid_mask: lexer DFA or LR tables too large for the LDS staging");
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace_dev;

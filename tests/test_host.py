@@ -218,6 +218,10 @@ def test_vocab_artifacts(G):
             assert wl.vocab[t] == spells[u]
             seen[int(t)] = u
     assert sorted(seen) == list(range(wl.V))
+    of_id = np.frombuffer(g.artifact("SPELL_OF_ID"), np.uint32)
+    assert len(of_id) == wl.V
+    for t in range(wl.V):
+        assert of_id[t] == seen[t]
     # levelized trie: every spelling ends at exactly one node
     lvl = np.frombuffer(g.artifact("TRIE_LEVEL_OFF"), np.uint32)
     nodes = np.frombuffer(g.artifact("TRIE_NODES"), np.uint32).reshape(-1, 2)
@@ -235,7 +239,7 @@ def test_vocab_artifacts(G):
 
 def test_spelling_records_and_tails(G):
     # record = first 8 bytes, first alias id (| 1 << 31 when shared), length |
-    # tail chunk << 8; bytes 8.. of a longer spelling start on a 16-byte chunk
+    # overflow chunk << 8; tail chunk u = bytes 8..23, bytes 24.. in overflow
     rng = np.random.default_rng(7)
     vocab = [bytes(rng.integers(40, 41, n, dtype=np.uint8)) for n in range(1, 60)]
     vocab += [bytes(rng.integers(33, 127, int(n), dtype=np.uint8)) for n in rng.integers(1, 120, 300)]
@@ -256,10 +260,14 @@ def test_spelling_records_and_tails(G):
         first = ids[aoff[u]]
         assert rec[u, 2] & 0x7FFFFFFF == first
         assert bool(rec[u, 2] >> 31) == (aoff[u + 1] - aoff[u] > 1)
-        if len(sp) > 8:
+        assert tail[16 * u:16 * u + 16].tobytes() == sp[8:24].ljust(16, b"\0")
+        if len(sp) > 24:
             c = int(rec[u, 3]) >> 8
-            assert tail[16 * c:16 * c + len(sp) - 8].tobytes() == sp[8:]
-            assert len(tail) >= 16 * c + ((len(sp) - 8 + 15) // 16) * 16 + 16
+            assert c >= len(rec)
+            assert tail[16 * c:16 * c + len(sp) - 24].tobytes() == sp[24:]
+            assert len(tail) >= 16 * c + ((len(sp) - 24 + 15) // 16) * 16 + 16
+        else:
+            assert rec[u, 3] >> 8 == 0
 
 
 def test_specials_are_excluded_and_incomplete_vocab_flagged(G):
