@@ -233,9 +233,9 @@ int grid_mask(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
  * all three have run.  grid_mask equals grid_mask_phases with GRID_PHASE_ALL. */
 #define GRID_PHASE_PROLOGUE 1u      /* allowed sets, EOS gate, first-byte table */
 #define GRID_PHASE_WALK 2u          /* full-vocabulary walk into a mask over sorted
-                                       spellings (workspace), then the spellings the
-                                       fast walk handed to the slow path */
-#define GRID_PHASE_FINALIZE 4u      /* writes mask_dev (each id takes its spelling's bit;
+                                       spellings (workspace) */
+#define GRID_PHASE_FINALIZE 4u      /* the spellings the walk handed to the slow path,
+                                       then mask_dev (each id takes its spelling's bit;
                                        the EOS bit) and the row status when status_dev
                                        is not null */
 #define GRID_PHASE_ALL 7u

@@ -1421,10 +1421,10 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
     hipLaunchKernelGGL(walk_kernel<MW>, dim3(blocks), dim3(kWalkThreads), WL.total, s, tb, cfg_dev, pool, ws, rb,
                        B);
   }
-  if (phases & GRID_PHASE_WALK)
+  if (phases & GRID_PHASE_FINALIZE) {
     hipLaunchKernelGGL(slow_kernel<MW>, dim3(B), dim3(kSlowThreads), parse_bytes, s, tb, cfg_dev, pool, ws, rb);
-  if (phases & GRID_PHASE_FINALIZE)
     hipLaunchKernelGGL(finalize_kernel, dim3(B, kGatherGroups), dim3(kBlock), 0, s, tb, mask, ws, rb, status);
+  }
   return GRID_OK;
 }
 
