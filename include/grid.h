@@ -79,9 +79,9 @@ typedef struct {
  * the first conflict); builds a dense 256-wide union lexer DFA over every
  * declared terminal (minimized, with byte classes, accept lists in priority
  * order and live-terminal sets) and checks it is gap-free; builds the
- * vocabulary artifacts: spellings sorted in byte order (trie DFS order), a
- * levelized CSR byte trie, and the alias table mapping each spelling to every
- * id that shares it (Definition 3).  Empty spellings count as special.
+ * vocabulary artifacts: the distinct spellings sorted in byte order (trie DFS
+ * order; "spelling order"), a levelized CSR byte trie, and the alias table
+ * mapping each spelling to every id that shares it (Definition 3).  Empty spellings count as special.
  * Copies all inputs.  *out receives a handle owned by the caller
  * (grid_free).  A vocabulary that does not contain every single byte is not
  * an error; grid_info reports it (completeness precondition (a),
@@ -142,7 +142,7 @@ enum {
   GRID_ART_GOTO,            /* u16 [n_lr][N] */
   GRID_ART_PROD,            /* u32 [P]: lhs | len << 16 */
   GRID_ART_TERM_INFO,       /* u32 [T]: bit0 ignored, bits 8..15 category index or 0xFF */
-  GRID_ART_SPELL_OFF,       /* u32 [U+1] offsets of the sorted distinct spellings */
+  GRID_ART_SPELL_OFF,       /* u32 [U+1] offsets of the distinct spellings, spelling order */
   GRID_ART_SPELL_BYTES,     /* u8  spelling bytes (+32 bytes of zero padding) */
   GRID_ART_ALIAS_OFF,       /* u32 [U+1] */
   GRID_ART_ALIAS_IDS,       /* i32 token ids per spelling */
@@ -155,7 +155,7 @@ enum {
   GRID_ART_LEX_SLOTS,       /* u32 [8] per slot: flags base, hash base, hash mask,
                                restricted-category mask, node count, prefix-table base,
                                prefix-table mask, 1 reserved */
-  GRID_ART_SPELL_REC,       /* u32 [U][4] per sorted spelling: its first 8 bytes (little-
+  GRID_ART_SPELL_REC,       /* u32 [U][4] per spelling: its first 8 bytes (little-
                                endian, zero padded), first alias id | 1 << 31 when more ids
                                share the spelling, length | overflow chunk << 8 (bytes 24..
                                of a longer spelling start at SPELL_TAIL + 16 * chunk) */
@@ -175,9 +175,9 @@ enum {
                                lexicon-trie node of depth 1..8 keyed exactly by its bytes:
                                bytes 0..3, bytes 4..7 (little-endian, zero padded),
                                length | flags << 16 (length 0 = empty), node */
-  GRID_ART_SPELL_RANGE,     /* u16 per 64-spelling sub-tile (sorted order): lowest first
+  GRID_ART_SPELL_RANGE,     /* u16 per 64 consecutive spellings (a sub-tile): lowest first
                                byte | highest first byte << 8 of its spellings */
-  GRID_ART_SPELL_OF_ID,     /* u32 [V]: sorted-spelling index of each token id, 0xFFFFFFFF
+  GRID_ART_SPELL_OF_ID,     /* u32 [V]: spelling index of each token id, 0xFFFFFFFF
                                for specials and empty tokens */
   GRID_ART_COUNT
 };
@@ -232,8 +232,8 @@ int grid_mask(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
  * it (earlier on the stream); finalize needs the walk; the mask is exact once
  * all three have run.  grid_mask equals grid_mask_phases with GRID_PHASE_ALL. */
 #define GRID_PHASE_PROLOGUE 1u      /* allowed sets, EOS gate, first-byte table */
-#define GRID_PHASE_WALK 2u          /* full-vocabulary walk into a mask over sorted
-                                       spellings (workspace) */
+#define GRID_PHASE_WALK 2u          /* full-vocabulary walk into a mask in spelling
+                                       order (workspace) */
 #define GRID_PHASE_FINALIZE 4u      /* the spellings the walk handed to the slow path,
                                        then mask_dev (each id takes its spelling's bit;
                                        the EOS bit) and the row status when status_dev

@@ -1,8 +1,8 @@
 // artifacts.cpp -- vocabulary and schema-lexicon artifacts.
 //
 // Vocabulary (Definition 3, section 4.1): the distinct non-special spellings,
-// sorted in byte order, which is the depth-first order of the token byte trie,
-// each with a 16-byte record (first 8 bytes, first id, length) and a 16-byte
+// sorted in byte order (the depth-first order of the token byte trie), each
+// with a 16-byte record (first 8 bytes, first id, length) and a 16-byte
 // tail chunk (bytes 8..23) at the same index, longer spellings continuing in
 // overflow chunks, so a walk fetches 16 bytes per load;
 // an alias table lists every token id sharing a spelling (section 2: masks are
@@ -51,6 +51,8 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
   auto spell = [&](int t) {
     return std::string((const char*)bytes + off[t], (size_t)(off[t + 1] - off[t]));
   };
+  // byte order (the depth-first order of the token trie): the 64 spellings a
+  // wave walks together share prefixes, so their lanes tend to stop together
   std::stable_sort(ids.begin(), ids.end(), [&](int a, int b) {
     size_t la = off[a + 1] - off[a], lb = off[b + 1] - off[b];
     int c = memcmp(bytes + off[a], bytes + off[b], std::min(la, lb));
@@ -103,8 +105,8 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
   va.spell_of_id.assign(V, 0xFFFFFFFFu);
   for (size_t u = 0; u < U; ++u)
     for (uint32_t k = va.alias_off[u]; k < va.alias_off[u + 1]; ++k) va.spell_of_id[va.alias_ids[k]] = (uint32_t)u;
-  // first-byte range of every 64 consecutive spellings (sorted, so the first
-  // and the last spelling of the group bound it)
+  // first-byte range of every 64 consecutive spellings (first bytes are
+  // non-decreasing, so the first and the last spelling of the group bound it)
   for (size_t u0 = 0; u0 < uniq.size(); u0 += 64) {
     const size_t u1 = std::min(uniq.size(), u0 + 64) - 1;
     va.sub_range.push_back((uint16_t)((uint8_t)uniq[u0][0] | (uint8_t)uniq[u1][0] << 8));

@@ -1,40 +1,36 @@
 // kernels.hip -- device side of the cold exact mask and the -inf apply (gfx950).
 //
 // grid_mask launches, on the caller's stream:
-//  1. prologue (8 workgroups per row): every workgroup stages the compact LR
-//     tables and the top of the row's stack in LDS and computes the allowed
-//     terminals A(sigma) (section 3.2, allowed terminals under table
-//     compression) by simulating the reduce chain for the whole set of
-//     terminals at once: at each state the terminals that shift are allowed,
-//     those reduced by one production travel on together, the rest are
-//     errors.  Each workgroup then records, for its share of the allowed
-//     terminals t, the stack after shifting t (an overlay above the shared
-//     read-only stack) and that stack's own allowed set.  Workgroup 0 also
-//     resolves the pending lexeme (its winner at an emission), the end-of-
-//     sequence gate (section 3.2, EOS gating, mid-lexeme aware) and a
-//     256-entry first-byte table: the scan state after any first byte of a
-//     token (continuing the pending lexeme, or emitting it and starting a new
-//     one), or "rejected"; it clears the row's mask words.
-//  2. walk (persistent; work items = spelling chunk x row): one lane per
-//     distinct spelling in byte order, so neighbouring lanes share prefixes
-//     and die together; inside an item every wave takes 64-spelling sub-tiles
-//     on its own.  The lexer DFA, compact LR tables, live-terminal sets,
-//     accept lists and the row's first-byte table sit in LDS; each spelling's
-//     first 8 bytes and first alias id arrive in one 16-byte load, longer
-//     spellings' tails 16 bytes per load.  Every lane carries the allowed set
-//     of its current stack: that of sigma, that recorded after the first
-//     shift, or one computed by a set simulation after each later shift
-//     (context-dependent part, Proposition 4).  A byte that kills the DFA
-//     emits the pending lexeme as the highest-priority candidate that is
-//     allowed (or ignored) and passes the schema lexicon, then is scanned again
-//     (section 4.1, trie walk); after every byte the pending lexeme must still
-//     complete to an allowed or ignored terminal (Definition 2).  Rejection is
-//     monotone, so a lane stops at its first failing byte.  Allowed spellings
-//     set the bits of every alias id; a lane whose LDS stack area is too small
-//     hands its spelling to the slow path.
-//  3. finalize (one workgroup per row): re-walks handed-over spellings with a
-//     large stack area in the workspace, writes the row status and flags an
-//     empty mask (Proposition 8: a viable configuration has a nonempty mask).
+//  1. prologue (one workgroup per row; compact LR tables and the top of the
+//     row's stack in LDS): thread t runs terminal t's reduce chain and shift
+//     from sigma, so A(sigma) (section 3.2, allowed terminals under table
+//     compression) is the set that shifted and each one's post-shift stack (an
+//     overlay above the shared read-only stack) is recorded; thread t in A then
+//     computes the allowed set of its post-shift stack by set simulation (one
+//     reduce chain for a whole terminal set), while one thread runs the
+//     end-of-sequence gate (section 3.2, EOS gating, mid-lexeme aware); finally
+//     thread b fills entry b of a 256-entry first-byte table: the scan state
+//     after byte b starts a token (continuing the pending lexeme, or emitting
+//     it as its winner and starting a new one), or "rejected".
+//  2. walk (one 1024-thread workgroup per compute unit): items are (row, 64
+//     consecutive spellings); spellings are in byte order, so a wave's lanes
+//     share prefixes and tend to stop at the same byte.  The lexer DFA,
+//     compact LR tables, live-terminal sets, accept lists and, per row, the
+//     first-byte table and trailing-flag tables sit in LDS.  Every lane carries
+//     the allowed set of its current stack: that of sigma, that recorded after
+//     the first shift, or one set-simulated on the lane's LDS overlay after
+//     each later shift (context-dependent part, Proposition 4).  A byte that
+//     kills the DFA emits the pending lexeme as the highest-priority candidate
+//     that is allowed (or ignored) and passes the schema lexicon, then is
+//     scanned again (section 4.1, trie walk); after every byte the pending
+//     lexeme must still complete to an allowed or ignored terminal (Definition
+//     2).  Rejection is monotone, so a lane stops at its first failing byte.
+//     A wave writes one 64-bit word of the row's mask in spelling order; a lane
+//     whose LDS stack area is too small hands its spelling to the slow path.
+//  3. finalize: the slow path re-walks handed-over spellings with a large stack
+//     area; then every id takes its spelling's bit (alias expansion), the EOS
+//     bit is set, and the row status is written (Proposition 8: a viable
+//     configuration has a nonempty mask).
 // grid_apply is a streaming in-place -inf fill of the masked logits.
 #include <hip/hip_runtime.h>
 
@@ -62,7 +58,7 @@ constexpr int kGuard = 4096;         // reduce-chain step bound
 constexpr int kSlowCap = 4096;       // spellings handed to the slow path per row
 constexpr int kSlowThreads = 64;
 constexpr int kSlowLane = 512;       // slow path per-thread stack area (workspace)
-constexpr int kGatherGroups = 32;    // finalize workgroups per row
+constexpr int kGatherGroups = 128;   // finalize workgroups per row
 constexpr uint32_t kRowValid = 0x600D;
 constexpr size_t kWsHead = 256;      // workspace head (reserved)
 constexpr int kMaxRounds = 257;      // set-simulation reruns (each peels one reduce group)
@@ -639,21 +635,18 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   }
   const Slot sl = load_slot(tb, cfg.slot);
   if (tid < 8) {
-    uint32_t iw = 0, rw8 = 0;
-    for (int j = 0; j < 32; ++j) {
-      const int t = tid * 32 + j;
-      if (t < tb.T) {
-        const uint32_t ti = tb.term_info[t];
-        const uint32_t c = (ti >> 8) & 0xFFu;
-        if (ti & 1u) iw |= 1u << j;
-        if (c != 0xFFu && ((sl.restricted >> c) & 1u)) rw8 |= 1u << j;
-      }
-    }
-    I[tid] = iw;
-    R[tid] = rw8;
+    I[tid] = 0;
+    R[tid] = 0;
     A[tid] = 0;
     Aw[tid] = 0;
     alive[tid] = 0;
+  }
+  __syncthreads();
+  if (tid < tb.T) {  // ignored and restricted terminals, one per thread
+    const uint32_t ti = tb.term_info[tid];
+    const uint32_t c = (ti >> 8) & 0xFFu;
+    if (ti & 1u) atomicOr(&I[tid >> 5], 1u << (tid & 31));
+    if (c != 0xFFu && ((sl.restricted >> c) & 1u)) atomicOr(&R[tid >> 5], 1u << (tid & 31));
   }
   const BaseStack bs{pool + cfg.stk_off, win, depth, lo};
   uint16_t* my = scratch[tid];
@@ -1212,118 +1205,131 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
 
 }
 
-// -------------------------------------------------------------- slow path
-// Re-walks the spellings the walk handed over (its LDS stack area was too
-// small) from the row's configuration, with a large stack area per thread in
-// the workspace, and sets their bits in the sorted-spelling mask.
-template <int MW>
-__global__ __launch_bounds__(kSlowThreads) void slow_kernel(Tables tb, const grid_config* __restrict__ cfgs,
-                                                            const uint16_t* __restrict__ pool,
-                                                            uint8_t* __restrict__ ws, size_t rbytes) {
-  extern __shared__ __align__(16) uint8_t slds[];
-  const int row = blockIdx.x;
-  const int tid = threadIdx.x;
-  uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
-  RowHeader* hdr = (RowHeader*)rw;
-  const RowLayout RL = row_layout(tb.T, tb.U);
-  const uint32_t count = hdr->valid == kRowValid ? min(hdr->slow_count, (uint32_t)kSlowCap) : 0u;
-  if (count == 0) return;  // uniform
-  __shared__ uint32_t I_s[8];
-  if (tid < 8) {
-    uint32_t iw = 0;
-    for (int j = 0; j < 32; ++j) {
-      const int t = tid * 32 + j;
-      if (t < tb.T && (tb.term_info[t] & 1u)) iw |= 1u << j;
-    }
-    I_s[tid] = iw;
-  }
-  const ParseTabs pt = stage_parse(tb, slds, parse_lds(tb, 0), tid, kSlowThreads);
-  __syncthreads();
-  const grid_config cfg = cfgs[row];
-  RowCtx rc;
-  rc.tb = &tb;
-  rc.pt = pt;
-  rc.bs = BaseStack{pool + cfg.stk_off, nullptr, cfg.stk_depth, cfg.stk_depth};
-  rc.sl = load_slot(tb, cfg.slot);
-  rc.tv = TermView{tb.term_info, I_s, hdr->R, tb.live, 8};
-  rc.acc_off = tb.acc_off;
-  rc.acc_list = tb.acc_list;
-  rc.a2 = (const uint32_t*)(rw + RL.a2);
-  rc.a2_stride = 8;
-  rc.post = (const Post*)(rw + RL.post);
-  rc.clsA = nullptr;
-  rc.clsW = nullptr;
-  rc.winner = -1;
-  uint16_t* ov = (uint16_t*)(rw + RL.slow_ov) + tid * kSlowLane;
-  const DfaView step{tb.dfa, tb.bclass, tb.C};
-  LexState lex0;
-  lex0.len = cfg.flags & 1u ? 0u : cfg.rem_len;
-  lex0.node = cfg.lexnode;
-  lex0.need = rc.sl.restricted != 0 ? 1u : 0u;
-  lex0.w = 0;
-  for (int k = 0; k < 8; ++k) lex0.w |= (uint64_t)cfg.rem_head[k] << (8 * k);
-  for (uint32_t k = tid; k < count; k += kSlowThreads) {
-    const int su = (int)((const uint32_t*)(rw + RL.slow))[k];
-    Lane<MW> ln;
-    ln.mode = 0;
-    ln.t1 = -1;
-    ln.k = 0;
-    ln.m = 0;
-#pragma unroll
-    for (int w = 0; w < MW; ++w) ln.acur[w] = hdr->A[w];
-    const uint32_t base = tb.spell_off[su];
-    auto byte_at = [&](uint32_t i) -> uint32_t { return tb.spell_bytes[base + i]; };
-    const int ok = walk_bytes<MW>(rc, ln, cfg.q, lex0, 0u, tb.spell_off[su + 1] - base, byte_at, step, ov,
-                                  kSlowLane);
-    if (ok > 0) {
-      atomicOr((uint32_t*)(rw + RL.smask) + (su >> 5), 1u << (su & 31));
-      hdr->nonempty = 1u;
-    } else if (ok < 0) {
-      atomicOr(&hdr->wstat, GRID_ROW_OVERFLOW);
-    }
-  }
-}
-
 // ---------------------------------------------------------------- finalize
-// The row's mask over token ids, gathered from the sorted-spelling mask (each
-// id looks up its spelling, so every alias of an allowed spelling is set), the
-// end-of-sequence bit, and the row status.  kGatherGroups workgroups per row;
-// each wave builds 64 consecutive ids, i.e. two mask words, per step.
-__global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, uint32_t* __restrict__ mask,
-                                                          const uint8_t* __restrict__ ws, size_t rbytes,
-                                                          int32_t* __restrict__ status) {
+// Workgroups (row, y), y < kGatherGroups.  The row's mask over token ids is
+// gathered from the mask in spelling order: each wave turns 64 consecutive ids
+// into two mask words by a ballot (every alias takes its spelling's bit;
+// specials and padding are 0; the EOS bit mirrors eos_ok).  When the walk
+// handed spellings to the slow path, workgroup (row, 0) alone first re-walks
+// them from the row's configuration with a large stack area per thread in
+// the workspace, then gathers the whole row; the other workgroups of that row
+// exit.  Workgroup (row, 0) also writes the row status.
+template <int MW>
+__global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_config* __restrict__ cfgs,
+                                                          const uint16_t* __restrict__ pool,
+                                                          uint32_t* __restrict__ mask, uint8_t* __restrict__ ws,
+                                                          size_t rbytes, int32_t* __restrict__ status) {
   const int row = blockIdx.x;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
-  const RowHeader* hdr = (const RowHeader*)rw;
+  uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
+  RowHeader* hdr = (RowHeader*)rw;
   const RowLayout RL = row_layout(tb.T, tb.U);
+  const bool valid = hdr->valid == kRowValid;
+  const uint32_t count = valid ? min(hdr->slow_count, (uint32_t)kSlowCap) : 0u;
+  if (count > 0 && blockIdx.y != 0) return;  // uniform
+  __shared__ uint32_t I_s[8];
+  __shared__ int slow_ok;
+  if (tid == 0) slow_ok = 0;
+  if (count > 0) {
+    if (tid < 8) {
+      uint32_t iw = 0;
+      for (int j = 0; j < 32; ++j) {
+        const int t = tid * 32 + j;
+        if (t < tb.T && (tb.term_info[t] & 1u)) iw |= 1u << j;
+      }
+      I_s[tid] = iw;
+    }
+    const ParseTabs pt = global_parse(tb);  // rare: tables stay in global memory
+    __syncthreads();
+    if (tid < kSlowThreads) {
+      const grid_config cfg = cfgs[row];
+      RowCtx rc;
+      rc.tb = &tb;
+      rc.pt = pt;
+      rc.bs = BaseStack{pool + cfg.stk_off, nullptr, cfg.stk_depth, cfg.stk_depth};
+      rc.sl = load_slot(tb, cfg.slot);
+      rc.tv = TermView{tb.term_info, I_s, hdr->R, tb.live, 8};
+      rc.acc_off = tb.acc_off;
+      rc.acc_list = tb.acc_list;
+      rc.a2 = (const uint32_t*)(rw + RL.a2);
+      rc.a2_stride = 8;
+      rc.post = (const Post*)(rw + RL.post);
+      rc.clsA = nullptr;
+      rc.clsW = nullptr;
+      rc.winner = -1;
+      uint16_t* ov = (uint16_t*)(rw + RL.slow_ov) + tid * kSlowLane;
+      const DfaView step{tb.dfa, tb.bclass, tb.C};
+      LexState lex0;
+      lex0.len = cfg.flags & 1u ? 0u : cfg.rem_len;
+      lex0.node = cfg.lexnode;
+      lex0.need = rc.sl.restricted != 0 ? 1u : 0u;
+      lex0.w = 0;
+      for (int k = 0; k < 8; ++k) lex0.w |= (uint64_t)cfg.rem_head[k] << (8 * k);
+      for (uint32_t k = tid; k < count; k += kSlowThreads) {
+        const int su = (int)((const uint32_t*)(rw + RL.slow))[k];
+        Lane<MW> ln;
+        ln.mode = 0;
+        ln.t1 = -1;
+        ln.k = 0;
+        ln.m = 0;
+#pragma unroll
+        for (int w = 0; w < MW; ++w) ln.acur[w] = hdr->A[w];
+        const uint32_t base = tb.spell_off[su];
+        auto byte_at = [&](uint32_t i) -> uint32_t { return tb.spell_bytes[base + i]; };
+        const int ok = walk_bytes<MW>(rc, ln, cfg.q, lex0, 0u, tb.spell_off[su + 1] - base, byte_at, step, ov,
+                                      kSlowLane);
+        if (ok > 0) {
+          atomicOr((uint32_t*)(rw + RL.smask) + (su >> 5), 1u << (su & 31));
+          slow_ok = 1;
+        } else if (ok < 0) {
+          atomicOr(&hdr->wstat, GRID_ROW_OVERFLOW);
+        }
+      }
+    }
+    __syncthreads();
+    __threadfence();  // the gather below reads the bits set above
+  }
+
   const uint64_t* sm = (const uint64_t*)(rw + RL.smask);
   uint32_t* mrow = mask + (size_t)row * tb.W;
-  const bool valid = hdr->valid == kRowValid;
   const int eos = valid && hdr->eos_ok ? tb.eos_id : -1;
-  // ids [64 c, 64 c + 64) for chunks c of this workgroup
+  // ids [64 c, 64 c + 64) for the chunks c of this workgroup, four per wave at
+  // a time so their loads overlap
   const int n_chunks = (tb.V + 63) / 64;
-  const int per = (n_chunks + kGatherGroups - 1) / kGatherGroups;
-  const int c_end = min(n_chunks, ((int)blockIdx.y + 1) * per);
-  for (int c = (int)blockIdx.y * per + (tid >> 6); c < c_end; c += kBlock / 64) {
-    const int id = c * 64 + lane;
-    bool bit = false;
-    if (id < tb.V && valid) {
-      const uint32_t su = tb.spell_of_id[id];
-      bit = su != 0xFFFFFFFFu && ((sm[su >> 6] >> (su & 63)) & 1ull);
+  const int groups = count > 0 ? 1 : kGatherGroups;
+  const int per = (n_chunks + groups - 1) / groups;
+  const int c_begin = (count > 0 ? 0 : (int)blockIdx.y) * per;
+  const int c_end = min(n_chunks, c_begin + per);
+  constexpr int kWaves = kBlock / 64, kUnroll = 8;
+  for (int c0 = c_begin + (tid >> 6); c0 < c_end; c0 += kWaves * kUnroll) {
+    uint32_t su[kUnroll];
+    uint64_t word[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const int c = c0 + k * kWaves;
+      const int id = c * 64 + lane;
+      su[k] = (c < c_end && id < tb.V && valid) ? tb.spell_of_id[id] : 0xFFFFFFFFu;
     }
-    bit = bit || id == eos;
-    const uint64_t word = __ballot(bit);
-    if (lane == 0) mrow[2 * c] = (uint32_t)word;
-    if (lane == 1 && 2 * c + 1 < tb.W) mrow[2 * c + 1] = (uint32_t)(word >> 32);
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) word[k] = su[k] != 0xFFFFFFFFu ? sm[su[k] >> 6] : 0ull;
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const int c = c0 + k * kWaves;
+      if (c >= c_end) break;  // uniform across the wave
+      const int id = c * 64 + lane;
+      const bool bit = (su[k] != 0xFFFFFFFFu && ((word[k] >> (su[k] & 63)) & 1ull)) || id == eos;
+      const uint64_t bits = __ballot(bit);
+      if (lane == 0) mrow[2 * c] = (uint32_t)bits;
+      if (lane == 1 && 2 * c + 1 < tb.W) mrow[2 * c + 1] = (uint32_t)(bits >> 32);
+    }
   }
   if (blockIdx.y == 0 && tid == 0) {
     int32_t st;
     if (valid) {
       st = hdr->pstat | hdr->wstat;
       if (hdr->slow_count > (uint32_t)kSlowCap) st |= GRID_ROW_OVERFLOW;
-      if (!hdr->nonempty && !hdr->eos_ok) st |= GRID_ROW_EMPTY;
+      if (!hdr->nonempty && !slow_ok && !hdr->eos_ok) st |= GRID_ROW_EMPTY;
     } else {
       st = hdr->pstat | GRID_ROW_BAD_CONFIG;
     }
@@ -1406,8 +1412,7 @@ template <int MW>
 int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint16_t* pool, uint32_t* mask,
                 uint8_t* eos, int32_t* status, uint8_t* ws, size_t rb, uint32_t phases, hipStream_t s) {
   const uint32_t parse_bytes = parse_lds(tb, 0).total;
-  if (!raise_lds((const void*)prologue_kernel<MW>, parse_bytes) ||
-      !raise_lds((const void*)slow_kernel<MW>, parse_bytes))
+  if (!raise_lds((const void*)prologue_kernel<MW>, parse_bytes))
     return fail(GRID_E_HIP, "grid_mask: cannot raise the LDS limit");
   if (phases & GRID_PHASE_PROLOGUE)
     hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool, eos, ws,
@@ -1421,10 +1426,9 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
     hipLaunchKernelGGL(walk_kernel<MW>, dim3(blocks), dim3(kWalkThreads), WL.total, s, tb, cfg_dev, pool, ws, rb,
                        B);
   }
-  if (phases & GRID_PHASE_FINALIZE) {
-    hipLaunchKernelGGL(slow_kernel<MW>, dim3(B), dim3(kSlowThreads), parse_bytes, s, tb, cfg_dev, pool, ws, rb);
-    hipLaunchKernelGGL(finalize_kernel, dim3(B, kGatherGroups), dim3(kBlock), 0, s, tb, mask, ws, rb, status);
-  }
+  if (phases & GRID_PHASE_FINALIZE)
+    hipLaunchKernelGGL(finalize_kernel<MW>, dim3(B, kGatherGroups), dim3(kBlock), 0, s, tb, cfg_dev, pool, mask,
+                       ws, rb, status);
   return GRID_OK;
 }
 
