@@ -159,14 +159,17 @@ enum {
                                endian, zero padded), first alias id | 1 << 31 when more ids
                                share the spelling, length | overflow chunk << 8 (bytes 24..
                                of a longer spelling start at SPELL_TAIL + 16 * chunk) */
-  GRID_ART_PARSE_STATE,     /* u32 [n_lr][2*TW+2], TW = ceil((T+1)/32): terminals that shift
-                               (or accept), terminals reduced by the state's main
-                               production, main production | extra groups << 16, offset of
-                               the extra groups in PARSE_REDX */
-  GRID_ART_PARSE_REDX,      /* u32 per extra reduce group: production, TW words of terminals */
+  GRID_ART_PARSE_STATE,     /* u32 [n_lr][R] with TW = the smallest power of two >= (T+1)/32
+                               and R = 2*TW+2 rounded up to a multiple of 4: terminals
+                               that shift (or accept), terminals reduced by the state's
+                               main production, that production as lhs | length << 16
+                               (0xFFFFFFFF none), extra groups | their offset in
+                               PARSE_REDX << 8, padding */
+  GRID_ART_PARSE_REDX,      /* u32 per extra reduce group: production (lhs | length << 16),
+                               TW words of terminals */
   GRID_ART_GOTO_HASH,       /* GOTO as an open-addressing table of H = 2^k slots (k >= 6,
-                               load <= 2/3): u32 [H] keys (state << 16 | nonterminal) + 1
-                               (0 empty), then u16 [H] targets; slot of a key =
+                               load <= 2/3), u32 [H][2]: key (state << 16 | nonterminal) + 1
+                               (0 empty), target; slot of a key =
                                (key * 0x9E3779B1 mod 2^32) >> (32 - k), linear probing */
   GRID_ART_SPELL_TAIL,      /* u8 [16 * chunks]: chunk u = bytes 8..23 of spelling u (zero
                                padded), then overflow chunks with bytes 24.. of spellings
@@ -179,6 +182,15 @@ enum {
                                byte | highest first byte << 8 of its spellings */
   GRID_ART_SPELL_OF_ID,     /* u32 [V]: spelling index of each token id, 0xFFFFFFFF
                                for specials and empty tokens */
+  GRID_ART_SCAN_SUMMARY,    /* u32 [S][U]: for lexer DFA state q and spelling u, how
+                               maximal munch segments u when the scan resumes in q (the
+                               walk's scan state, section 4.1; lexeme-internal versus
+                               boundary-crossing tokens, section 4.2).  Bits 0-8 state
+                               after the last byte, 9-17 state in which the first lexeme
+                               ended, 18-25 index of the byte that ended it, 26-27 lexeme
+                               ends inside u (2 = two or more), bit 28 rejected by the
+                               lexer alone.  Empty (0 bytes) when S > 512; the kernels
+                               then scan every byte */
   GRID_ART_COUNT
 };
 int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);

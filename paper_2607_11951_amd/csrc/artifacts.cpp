@@ -10,6 +10,12 @@
 // CSR form of the same trie (level by level, children in byte order, each
 // node pointing at its parent and at the spelling that ends there).
 //
+// Scan summary (section 4.1: the walk carries the scan state; section 4.2: a
+// token either stays inside the current lexeme or crosses boundaries): for
+// every DFA state q and spelling u, where maximal munch ends lexemes in u when
+// the scan resumes in q, packed as in lexhash.h.  It depends on the lexer and
+// the vocabulary only, so it is built once per compile.
+//
 // Schema lexicon (section 2, L3): per slot, one byte trie over the words of
 // every category with per-node flags "prefix of a category-c word" and
 // "category-c word", edges in a hash table and the nodes of depth 1..8 in a
@@ -19,6 +25,7 @@
 #include <cstring>
 #include <map>
 #include <numeric>
+#include <thread>
 
 #include "host.h"
 #include "lexhash.h"
@@ -139,6 +146,44 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
   va.level_off[va.max_len] = next;
   va.level_off[va.max_len + 1] = next;
   return va;
+}
+
+std::vector<uint32_t> build_scan_summary(const LexerDfa& dfa, const VocabArtifacts& va) {
+  const size_t U = va.spell_off.size() - 1;
+  if ((uint32_t)dfa.S > kScanMaxStates || U == 0) return {};
+  std::vector<uint32_t> out((size_t)dfa.S * U);
+  auto one = [&](int q, size_t u) -> uint32_t {
+    const uint8_t* b = va.spell_bytes.data() + va.spell_off[u];
+    const uint32_t n = va.spell_off[u + 1] - va.spell_off[u];
+    uint32_t cur = (uint32_t)q, q_first = 0, p_first = 0, ends = 0;
+    for (uint32_t i = 0; i < n; ++i) {
+      const uint32_t nq = dfa.step((int)cur, b[i]);
+      if (nq != (uint32_t)kDead) {
+        cur = nq;
+        continue;
+      }
+      // byte i ends the lexeme in state cur; it must accept something, and
+      // byte i must start the next lexeme
+      if (!dfa.accepting[cur]) return kScanReject;
+      if (ends == 0) {
+        q_first = cur;
+        p_first = i;
+      }
+      if (++ends == 2) return scan_word(0, q_first, p_first, 2);
+      cur = dfa.step(kStart, b[i]);
+      if (cur == (uint32_t)kDead) return kScanReject;
+    }
+    return scan_word(cur, q_first, p_first, ends);
+  };
+  const int nt = (int)std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+  std::vector<std::thread> pool;
+  for (int w = 0; w < nt; ++w)
+    pool.emplace_back([&, w]() {
+      for (int q = w; q < dfa.S; q += nt)
+        for (size_t u = 0; u < U; ++u) out[(size_t)q * U + u] = one(q, u);
+    });
+  for (auto& th : pool) th.join();
+  return out;
 }
 
 uint32_t LexiconStore::child(int slot, uint32_t node, uint8_t b) const {

@@ -64,6 +64,7 @@ extern "C" int grid_compile(const grid_compile_args* a, grid_compiled** out) {
     }
     g->vocab = build_vocab(a->vocab_bytes, a->vocab_offsets, a->vocab_size, a->special_ids,
                            a->n_special, a->eos_id);
+    g->scan = build_scan_summary(g->dfa, g->vocab);
     add_lexicon(g->lex, g->dfa, g->gram, g->term_cat, {});  // slot 0: no restrictions
     *out = g.release();
     return GRID_OK;
@@ -168,6 +169,7 @@ extern "C" int grid_artifact(const grid_compiled* g, int32_t which, const void**
     case GRID_ART_LEX_PREFIX: put(g->lex.prefix, p, n); break;
     case GRID_ART_SPELL_RANGE: put(g->vocab.sub_range, p, n); break;
     case GRID_ART_SPELL_OF_ID: put(g->vocab.spell_of_id, p, n); break;
+    case GRID_ART_SCAN_SUMMARY: put(g->scan, p, n); break;
     case GRID_ART_PARSE_STATE: put(g->parser.pstate, p, n); break;
     case GRID_ART_PARSE_REDX: put(g->parser.predx, p, n); break;
     case GRID_ART_GOTO_HASH: put(g->parser.goto_hash, p, n); break;

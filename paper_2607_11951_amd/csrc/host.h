@@ -77,14 +77,16 @@ struct Parser {
   std::vector<uint16_t> go;       // [n_states*N]
   std::vector<uint32_t> prod;     // lhs | len << 16
   std::vector<uint8_t> term_used; // terminal appears in the reduced grammar
-  // compact form for set simulation (TW = words per terminal set incl. end of input):
-  // per state [shift bits TW][main reduce bits TW][main prod | extra groups << 16][extra off]
+  // compact form for set simulation (TW = words per terminal set incl. end of
+  // input, a power of two): per state, parse_record_words(TW) words
+  // [shift bits TW][main reduce bits TW][main production][extra groups | offset << 8]
+  // (productions as lhs | length << 16, 0xFFFFFFFF none)
   int tw = 0;
   std::vector<uint32_t> pstate;
-  std::vector<uint32_t> predx;     // extra reduce groups: [prod][bits TW]
-  // GOTO as an open-addressing hash: H (power of two) u32 keys
-  // (state << 16 | nonterminal) + 1, 0 empty, then H u16 targets
-  std::vector<uint8_t> goto_hash;
+  std::vector<uint32_t> predx;     // extra reduce groups: [production][bits TW]
+  // GOTO as an open-addressing hash of H (power of two) u32 pairs: key
+  // (state << 16 | nonterminal) + 1 (0 empty), target
+  std::vector<uint32_t> goto_hash;
   int goto_hbits = 0;
   uint16_t act(int s, int t) const { return action[(size_t)s * (T + 1) + t]; }
   uint16_t gto(int s, int a) const { return go[(size_t)s * N + a]; }
@@ -113,6 +115,9 @@ struct VocabArtifacts {
 VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, const int32_t* specials,
                            int n_special, int eos_id);
 
+// scan summary [S][U] (lexhash.h); empty when the DFA has more than 512 states
+std::vector<uint32_t> build_scan_summary(const LexerDfa& dfa, const VocabArtifacts& va);
+
 // ---- lexicon slots
 struct LexiconStore {
   std::vector<uint16_t> flags;     // all slots' nodes
@@ -138,6 +143,7 @@ struct grid_compiled {
   grid::Parser parser;
   grid::VocabArtifacts vocab;
   grid::LexiconStore lex;
+  std::vector<uint32_t> scan;         // scan summary [S][U]
   std::vector<int> term_cat;          // category index per terminal or -1
   std::vector<uint32_t> term_info;    // device word per terminal
   std::vector<int> cat_term;          // terminal id per category index

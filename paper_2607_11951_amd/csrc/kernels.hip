@@ -25,6 +25,11 @@
 //     scanned again (section 4.1, trie walk); after every byte the pending
 //     lexeme must still complete to an allowed or ignored terminal (Definition
 //     2).  Rejection is monotone, so a lane stops at its first failing byte.
+//     The DFA side of this depends only on (DFA state, spelling), so the scan
+//     summary built at compile time gives each lane where its lexemes end: a
+//     spelling that ends at most one lexeme needs no DFA step at all (the
+//     winner, its shift and the trailing check of the last lexeme remain),
+//     and a longer one starts scanning at its first lexeme end.
 //     A wave writes one 64-bit word of the row's mask in spelling order; a lane
 //     whose LDS stack area is too small hands its spelling to the slow path.
 //  3. finalize: the slow path re-walks handed-over spellings with a large stack
@@ -69,6 +74,7 @@ constexpr int kSub = 64;             // spellings per wave item (one per lane)
 constexpr int kFastLane = 16;        // per-lane stack area in LDS (overlay at the bottom,
                                      // virtual pushes above it)
 constexpr int kRowGroup = 32;        // rows resident in LDS at once (at most)
+constexpr int kWalkWin = 64;         // top stack entries of each resident row in LDS
 constexpr uint32_t kWalkLdsMax = 160 * 1024;
 
 struct Tables {
@@ -78,11 +84,10 @@ struct Tables {
   const uint8_t* acc_list;
   const uint32_t* live;       // [S*8]
   const uint16_t* action;     // [NS*(T+1)] (shift targets)
-  const uint32_t* prod;       // [P]
   const uint32_t* term_info;  // [T]
-  const uint32_t* pstate;     // [NS][2*tw+2]
+  const uint32_t* pstate;     // [NS][parse_record_words(tw)]
   const uint32_t* predx;
-  const uint8_t* ghash;       // u32 keys [H], u16 targets [H]
+  const uint2* ghash;         // [H]: key, target
   const uint32_t* spell_off;  // [U+1]
   const uint8_t* spell_bytes;
   const uint4* spell_rec;     // [U]: head lo, head hi, first id | multi << 31, length | chunk << 8
@@ -95,6 +100,7 @@ struct Tables {
   const uint32_t* lex_slots;
   const uint4* lex_prefix;
   const uint16_t* sub_range;  // per 64 spellings: lowest | highest first byte << 8
+  const uint32_t* scan;       // scan summary [S][U], or null (scan every byte)
   int S, C, T, N, NS, P, U, V, W, n_slots, eos_id;
   int tw, n_pstate, n_predx, n_acc, hbits;
 };
@@ -173,18 +179,41 @@ __device__ inline uint32_t all_word(int T, int w) {
 }
 
 // ------------------------------------------------------- compact LR tables
-struct ParseTabs {  // pointers into LDS (or global memory)
-  const uint32_t* st;
-  const uint32_t* redx;
-  const uint32_t* prod;
-  const uint32_t* gkey;
-  const uint16_t* gval;
-  const uint16_t* action;  // global, dense: shift targets
-  int tw, stride, T, hbits;
+// The tables and the lanes' stack areas sit in LDS in the prologue and the
+// walk (L = true), where LDS-typed pointers make every access an LDS load;
+// the rare slow path (L = false) reads them from global memory.
+#define GRID_LDS __attribute__((address_space(3)))
+template <bool L, class T>
+struct MemSpace;
+template <class T>
+struct MemSpace<true, T> {
+  typedef GRID_LDS T* ptr;
+};
+template <class T>
+struct MemSpace<false, T> {
+  typedef T* ptr;
+};
+template <bool L, class T>
+using mptr = typename MemSpace<L, T>::ptr;
+// plain vector types for 8- and 16-byte loads through typed pointers
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+template <bool L, class T>
+__device__ inline mptr<L, T> in_mem(T* p) {
+  return (mptr<L, T>)p;
+}
+
+template <bool L>
+struct ParseTabs {
+  mptr<L, const uint32_t> st;    // state records, parse_record_words(MW) words each
+  mptr<L, const uint32_t> redx;  // extra reduce groups
+  mptr<L, const u32x2> gh;       // GOTO (key, target) slots
+  const uint16_t* action;        // global, dense: shift targets
+  int T, hbits;
 };
 
 struct ParseLds {  // byte offsets of the staged tables
-  uint32_t st, redx, prod, ghash, total;
+  uint32_t st, redx, ghash, total;
 };
 
 __host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base) {
@@ -194,124 +223,168 @@ __host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base) {
   o += pad16((uint32_t)tb.n_pstate * 4);
   L.redx = o;
   o += pad16((uint32_t)tb.n_predx * 4);
-  L.prod = o;
-  o += pad16((uint32_t)tb.P * 4);
   L.ghash = o;
-  o += pad16((6u << tb.hbits));
+  o += 8u << tb.hbits;
   L.total = o - base;
   return L;
 }
 
-__device__ inline ParseTabs make_parse(const Tables& tb, const uint32_t* st, const uint32_t* redx,
-                                       const uint32_t* prod, const uint8_t* gh) {
-  return {st, redx, prod, (const uint32_t*)gh, (const uint16_t*)(gh + (4u << tb.hbits)), tb.action,
-          tb.tw, 2 * tb.tw + 2, tb.T, tb.hbits};
-}
-
-__device__ inline ParseTabs stage_parse(const Tables& tb, uint8_t* lds, const ParseLds& L, int tid, int nt) {
+__device__ inline ParseTabs<true> stage_parse(const Tables& tb, uint8_t* lds, const ParseLds& L, int tid, int nt) {
   stage16(lds + L.st, (const uint8_t*)tb.pstate, (uint32_t)tb.n_pstate * 4, tid, nt);
   stage16(lds + L.redx, (const uint8_t*)tb.predx, (uint32_t)tb.n_predx * 4, tid, nt);
-  stage16(lds + L.prod, (const uint8_t*)tb.prod, (uint32_t)tb.P * 4, tid, nt);
-  stage16(lds + L.ghash, tb.ghash, 6u << tb.hbits, tid, nt);
-  return make_parse(tb, (const uint32_t*)(lds + L.st), (const uint32_t*)(lds + L.redx),
-                    (const uint32_t*)(lds + L.prod), lds + L.ghash);
+  stage16(lds + L.ghash, (const uint8_t*)tb.ghash, 8u << tb.hbits, tid, nt);
+  return {in_mem<true>((const uint32_t*)(lds + L.st)), in_mem<true>((const uint32_t*)(lds + L.redx)),
+          in_mem<true>((const u32x2*)(lds + L.ghash)), tb.action, tb.T, tb.hbits};
 }
 
-__device__ inline ParseTabs global_parse(const Tables& tb) {
-  return make_parse(tb, tb.pstate, tb.predx, tb.prod, tb.ghash);
+__device__ inline ParseTabs<false> global_parse(const Tables& tb) {
+  return {in_mem<false>(tb.pstate), in_mem<false>(tb.predx), in_mem<false>((const u32x2*)tb.ghash), tb.action,
+          tb.T, tb.hbits};
 }
 
+template <bool L>
 struct BaseStack {  // the shared read-only stack of one row
-  const uint16_t* pool;  // states [0, depth)
-  const uint16_t* win;   // copy of states [lo, depth) (LDS), or null with lo = depth
+  const uint16_t* pool;           // states [0, depth), global
+  mptr<L, const uint16_t> win;    // copy of states [lo, depth), or unused with lo = depth
   uint32_t depth, lo;
   __device__ uint16_t at(uint32_t i) const { return i >= lo ? win[i - lo] : pool[i]; }
 };
 
-__device__ inline uint16_t goto_of(const ParseTabs& pt, uint32_t s, uint32_t a) {
+template <bool L>
+__device__ inline uint16_t goto_of(const ParseTabs<L>& pt, uint32_t s, uint32_t a) {
   const uint32_t key = goto_key(s, a);
   const uint32_t mask = (1u << pt.hbits) - 1u;
   uint32_t h = goto_slot(key, pt.hbits);
   for (uint32_t i = 0; i <= mask; ++i, h = (h + 1) & mask) {
-    const uint32_t k = pt.gkey[h];
-    if (k == key) return pt.gval[h];
-    if (k == 0) break;
+    const u32x2 e = pt.gh[h];
+    if (e.x == key) return (uint16_t)e.y;
+    if (e.x == 0) break;
   }
   return kNoGoto;
 }
 
-// Action of terminal x in state s: -2 shift (or accept for the end-of-input
-// column), -1 error, else the production to reduce.
-__device__ inline int action_of(const ParseTabs& pt, uint32_t s, int x) {
-  const uint32_t* rec = pt.st + (size_t)s * pt.stride;
-  const uint32_t w = (uint32_t)x >> 5, bit = 1u << (x & 31);
-  if (rec[w] & bit) return -2;
-  const uint32_t info = rec[2 * pt.tw];
-  if (rec[pt.tw + w] & bit) return (int)(info & 0xFFFFu);
-  const uint32_t nx = info >> 16;
-  const uint32_t* g = pt.redx + rec[2 * pt.tw + 1];
-  for (uint32_t e = 0; e < nx; ++e, g += pt.tw + 1)
-    if (g[1 + w] & bit) return (int)g[0];
-  return -1;
+// One state record: shift bits, main-reduce bits, main production (lhs |
+// length << 16, kNoProd none), extra groups | offset << 8.
+constexpr uint32_t kNoProd = 0xFFFFFFFFu;
+template <int MW>
+struct PRec {
+  uint32_t sh[MW], rd[MW], main, extra;
+};
+
+template <bool L, int MW>
+__device__ __forceinline__ PRec<MW> rec_of(const ParseTabs<L>& pt, uint32_t s) {
+  constexpr int R = parse_record_words(MW);
+  const mptr<L, const u32x4> p = (mptr<L, const u32x4>)(pt.st + (size_t)s * R);
+  uint32_t w[R];
+#pragma unroll
+  for (int i = 0; i < R / 4; ++i) {
+    const u32x4 v = p[i];
+    w[4 * i] = v.x;
+    w[4 * i + 1] = v.y;
+    w[4 * i + 2] = v.z;
+    w[4 * i + 3] = v.w;
+  }
+  PRec<MW> r;
+#pragma unroll
+  for (int k = 0; k < MW; ++k) {
+    r.sh[k] = w[k];
+    r.rd[k] = w[MW + k];
+  }
+  r.main = w[2 * MW];
+  r.extra = w[2 * MW + 1];
+  return r;
 }
 
-// Virtual stack base[0,k) ++ ov[0,m) ++ tmp[0,t).
-#define GRID_TOP(k, m, t) ((t) > 0 ? tmp[(t)-1] : ((m) > 0 ? ov[(m)-1] : bs.at((k)-1)))
+// Action of terminal x in state s: kActShiftP (shift, or accept for the
+// end-of-input column), kNoProd (error), else the production to reduce.
+constexpr uint32_t kActShiftP = 0xFFFFFFFEu;
+template <bool L, int MW>
+__device__ __forceinline__ uint32_t action_of(const ParseTabs<L>& pt, uint32_t s, int x) {
+  constexpr int R = parse_record_words(MW);
+  const mptr<L, const uint32_t> rec = pt.st + (size_t)s * R;
+  const uint32_t w = (uint32_t)x >> 5, bit = 1u << (x & 31);
+  const uint32_t sh = rec[w], rd = rec[MW + w];
+  const u32x2 me = *(mptr<L, const u32x2>)(rec + 2 * MW);
+  if (sh & bit) return kActShiftP;
+  if (rd & bit) return me.x;
+  const uint32_t nx = me.y & 0xFFu;
+  mptr<L, const uint32_t> g = pt.redx + (me.y >> 8);
+  for (uint32_t e = 0; e < nx; ++e, g += MW + 1)
+    if (g[1 + w] & bit) return g[0];
+  return kNoProd;
+}
 
-// Reduce chain of terminal x, not changing the stack.  1 shift, 2 accept (x
-// is the end of input), 0 error, -1 capacity.
-__device__ int sim1_test(const ParseTabs& pt, const BaseStack& bs, uint32_t k, int m, const uint16_t* ov,
-                         uint16_t* tmp, int tmpcap, int x) {
+// Virtual stack base[0,k) ++ ov[0,m) ++ tmp[0,t); the state below a pop.
+template <bool L>
+__device__ __forceinline__ uint16_t stack_at_top(const BaseStack<L>& bs, uint32_t k, int m,
+                                                 mptr<L, const uint16_t> ov, int t,
+                                                 mptr<L, const uint16_t> tmp) {
+  if (t > 0) return tmp[t - 1];
+  if (m > 0) return ov[m - 1];
+  return bs.at(k - 1);
+}
+
+// Reduce chain of terminal x, not changing the stack (pushes go to tmp).  1
+// shift, 2 accept (x is the end of input), 0 error, -1 capacity.
+template <bool L, int MW>
+__device__ __forceinline__ int sim1_test(const ParseTabs<L>& pt, const BaseStack<L>& bs, uint32_t k, int m,
+                                         mptr<L, const uint16_t> ov, mptr<L, uint16_t> tmp, int tmpcap, int x) {
   int t = 0;
+  uint32_t s = stack_at_top<L>(bs, k, m, ov, 0, tmp);
   for (int guard = 0; guard < kGuard; ++guard) {
-    const uint16_t s = GRID_TOP(k, m, t);
-    const int a = action_of(pt, s, x);
-    if (a == -2) return x == pt.T ? 2 : 1;
-    if (a < 0) return 0;
-    const uint32_t pr = pt.prod[a];
-    uint32_t len = pr >> 16;
-    uint32_t d = min((uint32_t)t, len);
-    t -= (int)d;
-    len -= d;
-    d = min((uint32_t)m, len);
-    m -= (int)d;
-    len -= d;
-    if (len >= k) return 0;
-    k -= len;
-    const uint16_t g = goto_of(pt, GRID_TOP(k, m, t), pr & 0xFFFFu);
+    const uint32_t a = action_of<L, MW>(pt, s, x);
+    if (a == kActShiftP) return x == pt.T ? 2 : 1;
+    if (a == kNoProd) return 0;
+    uint32_t len = a >> 16;
+    if (len > 0) {
+      uint32_t d = min((uint32_t)t, len);
+      t -= (int)d;
+      len -= d;
+      d = min((uint32_t)m, len);
+      m -= (int)d;
+      len -= d;
+      if (len >= k) return 0;
+      k -= len;
+      s = stack_at_top<L>(bs, k, m, ov, t, tmp);
+    }
+    const uint16_t g = goto_of<L>(pt, s, a & 0xFFFFu);
     if (g == kNoGoto) return 0;
     if (t >= tmpcap) return -1;
     tmp[t++] = g;
+    s = g;
   }
   return -1;
 }
 
 // Reduce chain of terminal x applied to (k, m, ov), then its shift.  1 shifted,
 // 2 accept, 0 error, -1 capacity.
-__device__ __forceinline__ int sim1_shift(const ParseTabs& pt, const BaseStack& bs, uint32_t& k, int& m, uint16_t* ov, int cap,
-                          int x) {
+template <bool L, int MW>
+__device__ __forceinline__ int sim1_shift(const ParseTabs<L>& pt, const BaseStack<L>& bs, uint32_t& k, int& m,
+                                          mptr<L, uint16_t> ov, int cap, int x) {
+  uint32_t s = stack_at_top<L>(bs, k, m, ov, 0, ov);
   for (int guard = 0; guard < kGuard; ++guard) {
-    const uint16_t s = m > 0 ? ov[m - 1] : bs.at(k - 1);
-    const int a = action_of(pt, s, x);
-    if (a == -2) {
+    const uint32_t a = action_of<L, MW>(pt, s, x);
+    if (a == kActShiftP) {
       if (x == pt.T) return 2;
       if (m >= cap) return -1;
       ov[m++] = (uint16_t)(pt.action[(size_t)s * (pt.T + 1) + x] & 0x3FFF);
       return 1;
     }
-    if (a < 0) return 0;
-    const uint32_t pr = pt.prod[a];
-    uint32_t len = pr >> 16;
-    const uint32_t d = min((uint32_t)m, len);
-    m -= (int)d;
-    len -= d;
-    if (len >= k) return 0;
-    k -= len;
-    const uint16_t under = m > 0 ? ov[m - 1] : bs.at(k - 1);
-    const uint16_t g = goto_of(pt, under, pr & 0xFFFFu);
+    if (a == kNoProd) return 0;
+    uint32_t len = a >> 16;
+    if (len > 0) {
+      const uint32_t d = min((uint32_t)m, len);
+      m -= (int)d;
+      len -= d;
+      if (len >= k) return 0;
+      k -= len;
+      s = stack_at_top<L>(bs, k, m, ov, 0, ov);
+    }
+    const uint16_t g = goto_of<L>(pt, s, a & 0xFFFFu);
     if (g == kNoGoto) return 0;
     if (m >= cap) return -1;
     ov[m++] = g;
+    s = g;
   }
   return -1;
 }
@@ -321,14 +394,16 @@ __device__ __forceinline__ int sim1_shift(const ParseTabs& pt, const BaseStack& 
 // shifting terminals are accepted, those reduced by one production continue
 // together, terminals of another reduce production of the same state rerun
 // from the start (they follow the same chain up to that state, so every rerun
-// peels off at least one group), the rest fail.  MW = words per set (>= tw).
-// 0 ok, -1 capacity (acc is then incomplete).
-template <int MW>
-__device__ __forceinline__ int sim_set(const ParseTabs& pt, const BaseStack& bs, uint32_t k0, int m0, const uint16_t* ov,
-                       uint16_t* tmp, int tmpcap, const uint32_t (&X)[MW], uint32_t (&acc)[MW]) {
+// peels off at least one group), the rest fail.  MW = words per set (the
+// tables' TW).  0 ok, -1 capacity (acc is then incomplete).
+template <bool L, int MW>
+__device__ __forceinline__ int sim_set(const ParseTabs<L>& pt, const BaseStack<L>& bs, uint32_t k0, int m0,
+                                       mptr<L, const uint16_t> ov, mptr<L, uint16_t> tmp, int tmpcap,
+                                       const uint32_t (&X)[MW], uint32_t (&acc)[MW]) {
   uint32_t todo[MW];
 #pragma unroll
   for (int w = 0; w < MW; ++w) todo[w] = X[w];
+  const uint32_t s0 = stack_at_top<L>(bs, k0, m0, ov, 0, tmp);
   for (int round = 0; round < kMaxRounds; ++round) {
     uint32_t any = 0;
 #pragma unroll
@@ -340,34 +415,30 @@ __device__ __forceinline__ int sim_set(const ParseTabs& pt, const BaseStack& bs,
       cur[w] = todo[w];
       todo[w] = 0;
     }
-    uint32_t k = k0;
+    uint32_t k = k0, s = s0;
     int m = m0, t = 0;
     for (int guard = 0; guard < kGuard; ++guard) {
-      const uint16_t s = GRID_TOP(k, m, t);
-      const uint32_t* rec = pt.st + (size_t)s * pt.stride;
+      const PRec<MW> r = rec_of<L, MW>(pt, s);
       uint32_t nxt[MW], live = 0;
 #pragma unroll
       for (int w = 0; w < MW; ++w) {
-        const uint32_t sh = w < pt.tw ? rec[w] : 0u;
-        const uint32_t rd = w < pt.tw ? rec[pt.tw + w] : 0u;
-        acc[w] |= cur[w] & sh;
-        nxt[w] = cur[w] & rd;
+        acc[w] |= cur[w] & r.sh[w];
+        nxt[w] = cur[w] & r.rd[w];
         live |= nxt[w];
       }
-      const uint32_t info = rec[2 * pt.tw];
-      int chosen = live ? (int)(info & 0xFFFFu) : -1;
-      const uint32_t nx = info >> 16;
-      const uint32_t* g = pt.redx + rec[2 * pt.tw + 1];
-      for (uint32_t e = 0; e < nx; ++e, g += pt.tw + 1) {
+      uint32_t chosen = live ? r.main : kNoProd;
+      const uint32_t nx = r.extra & 0xFFu;
+      mptr<L, const uint32_t> g = pt.redx + (r.extra >> 8);
+      for (uint32_t e = 0; e < nx; ++e, g += MW + 1) {
         uint32_t gl = 0, part[MW];
 #pragma unroll
         for (int w = 0; w < MW; ++w) {
-          part[w] = cur[w] & (w < pt.tw ? g[1 + w] : 0u);
+          part[w] = cur[w] & g[1 + w];
           gl |= part[w];
         }
         if (!gl) continue;
-        if (chosen < 0) {
-          chosen = (int)g[0];
+        if (chosen == kNoProd) {
+          chosen = g[0];
 #pragma unroll
           for (int w = 0; w < MW; ++w) nxt[w] = part[w];
         } else {
@@ -375,23 +446,26 @@ __device__ __forceinline__ int sim_set(const ParseTabs& pt, const BaseStack& bs,
           for (int w = 0; w < MW; ++w) todo[w] |= part[w];
         }
       }
-      if (chosen < 0) break;
+      if (chosen == kNoProd) break;
 #pragma unroll
       for (int w = 0; w < MW; ++w) cur[w] = nxt[w];
-      const uint32_t pr = pt.prod[chosen];
-      uint32_t len = pr >> 16;
-      uint32_t d = min((uint32_t)t, len);
-      t -= (int)d;
-      len -= d;
-      d = min((uint32_t)m, len);
-      m -= (int)d;
-      len -= d;
-      if (len >= k) break;
-      k -= len;
-      const uint16_t gs = goto_of(pt, GRID_TOP(k, m, t), pr & 0xFFFFu);
+      uint32_t len = chosen >> 16;
+      if (len > 0) {
+        uint32_t d = min((uint32_t)t, len);
+        t -= (int)d;
+        len -= d;
+        d = min((uint32_t)m, len);
+        m -= (int)d;
+        len -= d;
+        if (len >= k) break;
+        k -= len;
+        s = stack_at_top<L>(bs, k, m, ov, t, tmp);
+      }
+      const uint16_t gs = goto_of<L>(pt, s, chosen & 0xFFFFu);
       if (gs == kNoGoto) break;
       if (t >= tmpcap) return -1;
       tmp[t++] = gs;
+      s = gs;
     }
   }
   uint32_t any = 0;
@@ -402,16 +476,17 @@ __device__ __forceinline__ int sim_set(const ParseTabs& pt, const BaseStack& bs,
 
 // Allowed set of base[0,k) ++ ov[0,m): every terminal (not the end of input)
 // that can be shifted next.
-template <int MW>
-__device__ __forceinline__ int allowed_set(const ParseTabs& pt, const BaseStack& bs, uint32_t k, int m, const uint16_t* ov,
-                                  uint16_t* tmp, int tmpcap, uint32_t (&acc)[MW]) {
+template <bool L, int MW>
+__device__ __forceinline__ int allowed_set(const ParseTabs<L>& pt, const BaseStack<L>& bs, uint32_t k, int m,
+                                           mptr<L, const uint16_t> ov, mptr<L, uint16_t> tmp, int tmpcap,
+                                           uint32_t (&acc)[MW]) {
   uint32_t X[MW];
 #pragma unroll
   for (int w = 0; w < MW; ++w) {
     X[w] = all_word(pt.T, w);
     acc[w] = 0;
   }
-  return sim_set<MW>(pt, bs, k, m, ov, tmp, tmpcap, X, acc);
+  return sim_set<L, MW>(pt, bs, k, m, ov, tmp, tmpcap, X, acc);
 }
 
 // ---------------------------------------------------------- lexicon helpers
@@ -592,7 +667,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   Post* post = (Post*)(rw + L.post);
   uint32_t* a2 = (uint32_t*)(rw + L.a2);
   const grid_config cfg = cfgs[row];
-  const ParseTabs pt = stage_parse(tb, plds, parse_lds(tb, 0), tid, kBlock);
+  const ParseTabs<true> pt = stage_parse(tb, plds, parse_lds(tb, 0), tid, kBlock);
 
   if (tid == 0) {
     int b = 0;
@@ -648,8 +723,8 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     if (ti & 1u) atomicOr(&I[tid >> 5], 1u << (tid & 31));
     if (c != 0xFFu && ((sl.restricted >> c) & 1u)) atomicOr(&R[tid >> 5], 1u << (tid & 31));
   }
-  const BaseStack bs{pool + cfg.stk_off, win, depth, lo};
-  uint16_t* my = scratch[tid];
+  const BaseStack<true> bs{pool + cfg.stk_off, in_mem<true>((const uint16_t*)win), depth, lo};
+  const mptr<true, uint16_t> my = in_mem<true>(&scratch[tid][0]);
   const TermView tv{tb.term_info, I, R, tb.live, 8};
   __syncthreads();
 
@@ -658,7 +733,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     const int t = tid;
     uint32_t k = depth;
     int m = 0;
-    const int r = sim1_shift(pt, bs, k, m, my, kPostCap, t);
+    const int r = sim1_shift<true, MW>(pt, bs, k, m, my, kPostCap, t);
     if (r < 0 || (r == 1 && k > 0xFFFF)) overflow = 1;
     if (r == 1) {
       atomicOr(&A[t >> 5], 1u << (t & 31));
@@ -666,7 +741,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
       p.k = (uint16_t)k;
       p.m = (uint8_t)m;
       p.ok = 1;
-      for (int j = 0; j < kPostCap; ++j) p.ov[j] = j < m ? my[j] : 0;
+      for (int j = 0; j < kPostCap; ++j) p.ov[j] = j < m ? (uint16_t)my[j] : (uint16_t)0;
       posts[t] = p;
       post[t] = p;
     }
@@ -689,7 +764,9 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   if (tid < tb.T && bit_of(A, tid)) {
     const Post& p = posts[tid];
     uint32_t acc[MW];
-    if (allowed_set<MW>(pt, bs, p.k, p.m, p.ov, my, kPostCap + kTmpCap, acc) < 0) overflow = 1;
+    if (allowed_set<true, MW>(pt, bs, p.k, p.m, in_mem<true>((const uint16_t*)p.ov), my, kPostCap + kTmpCap, acc) <
+        0)
+      overflow = 1;
 #pragma unroll
     for (int k = 0; k < MW; ++k) a2[tid * 8 + k] = acc[k];
     if (tid == w) {
@@ -699,10 +776,11 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   } else if (tid == kBlock - 1) {
     int ok = 0;
     if (rem_empty || (w >= 0 && !w_shifts)) {
-      ok = sim1_test(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, tb.T) == 2;
+      ok = sim1_test<true, MW>(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, tb.T) == 2;
     } else if (w >= 0) {
       const Post& p = posts[w];
-      ok = sim1_test(pt, bs, p.k, p.m, p.ov, my, kPostCap + kTmpCap, tb.T) == 2;
+      ok = sim1_test<true, MW>(pt, bs, p.k, p.m, in_mem<true>((const uint16_t*)p.ov), my, kPostCap + kTmpCap,
+                               tb.T) == 2;
     }
     eos_ok = ok;
   }
@@ -765,8 +843,10 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
 }
 
 // ------------------------------------------------------- lane machinery
-// A lane's stack is sigma (mode 0), the stack after the first shift t1
-// (mode 1), or base[0,k) ++ ov[0,m) (mode 2); acur is its allowed set.
+// A lane's parser side.  Mode 0: the stack is sigma and acur = A(sigma).
+// Mode 1: sigma plus the shift of t1, acur = that stack's allowed set (from
+// the prologue).  Mode 2: a stack of its own (base[0,k) ++ overlay[0,m)) and
+// its allowed set, set-simulated after every shift.
 template <int MW>
 struct Lane {
   int mode;
@@ -776,10 +856,11 @@ struct Lane {
   uint32_t acur[MW];
 };
 
+template <bool L>
 struct RowCtx {
   const Tables* tb;
-  ParseTabs pt;
-  BaseStack bs;
+  ParseTabs<L> pt;
+  BaseStack<L> bs;
   Slot sl;
   TermView tv;
   const uint32_t* acc_off;  // accept-list offsets (LDS or global)
@@ -795,8 +876,8 @@ struct RowCtx {
 // Emits the pending lexeme in DFA state q (lexicon state lx).  ov is the
 // lane's stack area of cap entries: the overlay occupies [0, m), virtual
 // pushes use [m, cap).  1 ok, 0 reject, -1 capacity.
-template <int MW>
-__device__ __forceinline__ int emit(const RowCtx& rc, Lane<MW>& ln, uint16_t* ov, int cap, int q,
+template <bool L, int MW>
+__device__ __forceinline__ int emit(const RowCtx<L>& rc, Lane<MW>& ln, mptr<L, uint16_t> ov, int cap, int q,
                                     const LexState& lx) {
   const int t = winner_of<MW>(rc.tv, rc.acc_off, rc.acc_list, ln.acur, q,
                               [&]() { return lex_flags_now(*rc.tb, rc.sl, lx); });
@@ -817,9 +898,9 @@ __device__ __forceinline__ int emit(const RowCtx& rc, Lane<MW>& ln, uint16_t* ov
     for (int j = 0; j < ln.m; ++j) ov[j] = p.ov[j];
     ln.mode = 2;
   }
-  const int r = sim1_shift(rc.pt, rc.bs, ln.k, ln.m, ov, cap, t);
+  const int r = sim1_shift<L, MW>(rc.pt, rc.bs, ln.k, ln.m, ov, cap, t);
   if (r != 1) return r < 0 ? -1 : 0;
-  return allowed_set<MW>(rc.pt, rc.bs, ln.k, ln.m, ov, ov + ln.m, cap - ln.m, ln.acur) < 0 ? -1 : 1;
+  return allowed_set<L, MW>(rc.pt, rc.bs, ln.k, ln.m, ov, ov + ln.m, cap - ln.m, ln.acur) < 0 ? -1 : 1;
 }
 
 struct DfaView {  // lexer DFA by byte class (LDS copy or global)
@@ -840,9 +921,9 @@ struct DfaView {  // lexer DFA by byte class (LDS copy or global)
 // the spelling when only restricted terminals remain (by the shrinking of live
 // sets this one check covers every byte of the lexeme).  1 allowed,
 // 0 rejected, -1 capacity.
-template <int MW, class ByteAt>
-__device__ __forceinline__ int walk_bytes(const RowCtx& rc, Lane<MW>& ln, int q, LexState lx, uint32_t i,
-                                          uint32_t n, ByteAt byte_at, const DfaView& step, uint16_t* ov,
+template <bool L, int MW, class ByteAt>
+__device__ __forceinline__ int walk_bytes(const RowCtx<L>& rc, Lane<MW>& ln, int q, LexState lx, uint32_t i,
+                                          uint32_t n, ByteAt byte_at, const DfaView& step, mptr<L, uint16_t> ov,
                                           int cap) {
   const Tables& tb = *rc.tb;
   const bool track = rc.sl.restricted != 0;
@@ -878,7 +959,7 @@ __device__ __forceinline__ int walk_bytes(const RowCtx& rc, Lane<MW>& ln, int q,
     const bool em = status == 2 && pend >= 0;
     if (!__any(em)) break;
     if (em) {  // emission phase
-      const int r = emit<MW>(rc, ln, ov, cap, q, lx);
+      const int r = emit<L, MW>(rc, ln, ov, cap, q, lx);
       if (r <= 0) {
         status = r;
       } else {
@@ -895,6 +976,42 @@ __device__ __forceinline__ int walk_bytes(const RowCtx& rc, Lane<MW>& ln, int q,
   return status;
 }
 
+// Verdict of a lane whose spelling ends at most one lexeme, from the scan
+// summary word sc of (row's DFA state, spelling): the DFA steps were taken at
+// compile time, what is left is the parser side -- the ended lexeme's winner
+// and its shift, from the prologue's tables -- and the trailing check of the
+// last lexeme, which reads the lexicon only where a restricted terminal alone
+// keeps the lexeme viable.  ln and lx describe the lane after byte 0;
+// byte_at yields bytes 1, 2, ... in order.  1 allowed, 0 rejected.
+template <bool L, int MW, class ByteAt>
+__device__ __forceinline__ int summary_verdict(const RowCtx<L>& rc, Lane<MW>& ln, uint32_t sc, LexState lx,
+                                               uint32_t n, ByteAt& byte_at, mptr<L, uint16_t> ov, int cap) {
+  const Tables& tb = *rc.tb;
+  uint32_t i = 1;
+  const uint32_t p = scan_p_first(sc);
+  if (scan_ends(sc) == 1 && p > 0) {
+    // bytes 1 .. p-1 extend the pending lexeme; byte p ends it and starts the
+    // last lexeme
+    for (; i < p; ++i) {
+      const uint32_t b = byte_at(i);
+      if (lx.need) lex_push(tb, rc.sl, lx, b);
+    }
+    const int r = emit<L, MW>(rc, ln, ov, cap, (int)scan_q_first(sc), lx);
+    if (r <= 0) return 0;
+    lx = LexState{byte_at(p), 1u, kNoLex, 1u};
+    i = p + 1;
+  }
+  const int qf = (int)scan_q_end(sc);
+  const uint8_t* ctab = ln.mode == 0 ? rc.clsA : (ln.mode == 1 && ln.t1 == rc.winner ? rc.clsW : nullptr);
+  const uint32_t f = ctab ? (uint32_t)ctab[qf] : trail_flags<MW>(rc.tv, ln.acur, qf);
+  if (f & 1u) return 1;
+  if (!(f & 2u)) return 0;
+  // only restricted terminals remain (live sets shrink along a lexeme, so the
+  // lexicon state was tracked from the lexeme's first byte): ask the lexicon
+  for (; i < n; ++i) lex_push(tb, rc.sl, lx, byte_at(i));
+  return trail_lex<MW>(rc.tv, ln.acur, qf, lex_flags_now(tb, rc.sl, lx)) ? 1 : 0;
+}
+
 // -------------------------------------------------------------------- walk
 // Per-row data a walk workgroup keeps in LDS for every row of its group.
 struct RowLds {
@@ -906,12 +1023,13 @@ struct RowLds {
   uint32_t rem_len;
   uint32_t lexnode;         // lexicon node of the pending lexeme
   int32_t winner;           // its winner when a byte ends it (-1 none)
-  uint32_t pad[17];
+  uint32_t q;               // DFA state of the pending lexeme (clamped below S)
+  uint32_t pad[16];
 };
 static_assert(sizeof(RowLds) == 256, "row record is 256 bytes");
 
 struct WalkLds {  // byte offsets into dynamic LDS
-  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, live, range, lanes, rows, fb, cls, total;
+  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, live, range, lanes, rows, fb, cls, win, total;
   uint32_t cls_row;  // bytes per row of trailing-flag tables (two of S entries)
   int group;         // rows per group
   ParseLds pl;
@@ -945,7 +1063,7 @@ __host__ __device__ inline WalkLds walk_lds(const Tables& tb, int mw, int B) {
   // and B
   const uint32_t fixed = o + 64;
   w.cls_row = 2 * pad16((uint32_t)tb.S);
-  const uint32_t per_row = sizeof(RowLds) + 256 * 4 + w.cls_row;
+  const uint32_t per_row = sizeof(RowLds) + 256 * 4 + w.cls_row + kWalkWin * 2;
   int g = kRowGroup < B ? kRowGroup : B;
   while (g > 1 && fixed + per_row * (uint32_t)g > kWalkLdsMax) --g;
   w.group = g;
@@ -955,6 +1073,8 @@ __host__ __device__ inline WalkLds walk_lds(const Tables& tb, int mw, int B) {
   o += 256 * 4 * (uint32_t)g;
   w.cls = o;
   o += w.cls_row * (uint32_t)g;
+  w.win = o;
+  o += kWalkWin * 2 * (uint32_t)g;
   w.total = o;
   return w;
 }
@@ -1028,8 +1148,9 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
   RowLds* rows_s = (RowLds*)(lds + WL.rows);
   const uint32_t* fb_all = (const uint32_t*)(lds + WL.fb);
   uint8_t* cls_all = lds + WL.cls;
+  uint16_t* win_all = (uint16_t*)(lds + WL.win);
   const uint16_t* range_s = (const uint16_t*)(lds + WL.range);
-  uint16_t* lane_area = (uint16_t*)(lds + WL.lanes) + tid * kFastLane;
+  const mptr<true, uint16_t> lane_area = in_mem<true>((uint16_t*)(lds + WL.lanes) + tid * kFastLane);
   uint8_t* rows = ws + kWsHead;
   const int nsub = (tb.U + kSub - 1) / kSub;
 
@@ -1039,7 +1160,7 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
   stage16(lds + WL.acc_off, (const uint8_t*)tb.acc_off, (uint32_t)(tb.S + 1) * 4, tid, kWalkThreads);
   stage16(lds + WL.acc_list, tb.acc_list, (uint32_t)tb.n_acc, tid, kWalkThreads);
   stage16(lds + WL.range, (const uint8_t*)tb.sub_range, (uint32_t)nsub * 2, tid, kWalkThreads);
-  const ParseTabs pt = stage_parse(tb, lds, WL.pl, tid, kWalkThreads);
+  const ParseTabs<true> pt = stage_parse(tb, lds, WL.pl, tid, kWalkThreads);
   for (int i = tid; i < tb.S * MW; i += kWalkThreads) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
   for (int t = tid; t < 256; t += kWalkThreads) tinfo_s[t] = t < tb.T ? tb.term_info[t] : 0u;
   __syncthreads();
@@ -1060,6 +1181,7 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
       const uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
       stage16((uint8_t*)(fb_all + r * 256), rw + RL.fb, 256 * 4, tid, kWalkThreads);
     }
+
     for (int r = tid; r < gr; r += kWalkThreads) {
       const RowHeader* hdr = (const RowHeader*)(rows + (size_t)(g0 + r) * rbytes);
       const grid_config cfg = cfgs[g0 + r];
@@ -1080,10 +1202,18 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
                   (uint32_t)cfg.rem_head[7] << 24;
       rl.rem_len = cfg.flags & 1u ? 0u : cfg.rem_len;
       rl.lexnode = cfg.lexnode;
+      rl.q = cfg.q < tb.S ? cfg.q : 0u;
       rl.winner = hdr->winner >= 0 && !((I_s[hdr->winner >> 5] >> (hdr->winner & 31)) & 1u) ? hdr->winner : -1;
     }
     if (tid == 0) item_ctr = 0;
     __syncthreads();
+    // the top of every valid row's stack (the prologue checked its entries)
+    for (int i = tid; i < gr * kWalkWin; i += kWalkThreads) {
+      const int r = i / kWalkWin, j = i - r * kWalkWin;
+      const RowLds& rl = rows_s[r];
+      const uint32_t d = rl.stk_depth, lo = d > (uint32_t)kWalkWin ? d - kWalkWin : 0u;
+      if (rl.valid == kRowValid && lo + j < d) win_all[i] = pool[rl.stk_off + lo + j];
+    }
     // trailing flags of every DFA state under A(sigma) and after the winner's shift
     for (int i = tid; i < gr * tb.S; i += kWalkThreads) {
       const int r = i / tb.S, q = i - r * tb.S;
@@ -1119,17 +1249,26 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
         if (rows_s[r].valid == kRowValid && any_in_range(rows_s[r].alive, rg & 0xFFu, rg >> 8)) return k;
       }
     };
+    // scan summary word of (row's DFA state, spelling); without the table
+    // every lane scans its bytes
+    auto summary = [&](int k, int r, int u) -> uint32_t {
+      if (!tb.scan) return 2u << 26;
+      const uint32_t q = k < mine ? rows_s[r].q : 0u;
+      return tb.scan[(size_t)q * tb.U + (u < tb.U ? u : 0)];
+    };
     int k0 = next_live();
     int r0;
     int u = spelling(k0, r0);
     uint4 rk = recs[u < tb.U ? u : 0];
     uint4 tl = tails[u < tb.U ? u : 0];
+    uint32_t sc = summary(k0, r0, u);
     while (k0 < mine) {
       const int k1 = next_live();
       int r1;
       const int u1 = spelling(k1, r1);
       const uint4 rk1 = recs[u1 < tb.U ? u1 : 0];
       const uint4 tl1 = tails[u1 < tb.U ? u1 : 0];
+      const uint32_t sc1 = summary(k1, r1, u1);
 
       const RowLds& rl = rows_s[r0];
       const uint32_t n = u < tb.U ? (rk.w & 0xFFu) : 0u;
@@ -1139,10 +1278,11 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
       const uint32_t kind = (e >> 16) & 3u;
       if (n != 0 && kind != kFbDead) {
         uint8_t* rw = rows + (size_t)(g0 + r0) * rbytes;
-        RowCtx rc;
+        RowCtx<true> rc;
         rc.tb = &tb;
         rc.pt = pt;
-        rc.bs = BaseStack{pool + rl.stk_off, nullptr, rl.stk_depth, rl.stk_depth};
+        rc.bs = BaseStack<true>{pool + rl.stk_off, in_mem<true>((const uint16_t*)(win_all + r0 * kWalkWin)),
+                                rl.stk_depth, rl.stk_depth > (uint32_t)kWalkWin ? rl.stk_depth - kWalkWin : 0u};
         rc.sl = rl.sl;
         rc.tv = TermView{tinfo_s, I_s, rl.R, live_s, MW};
         rc.acc_off = (const uint32_t*)(lds + WL.acc_off);
@@ -1181,7 +1321,28 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
                              : 0ull;
           lx.node = lx.need && lx.len > 8 ? lex_child(tb, rl.sl, rl.lexnode, b0) : kNoLex;
         }
-        const int ok = walk_bytes<MW>(rc, ln, q1, lx, 1u, n, byte_at, step, lane_area, kFastLane);
+        // the scan summary settles lanes whose spelling ends at most one
+        // lexeme; the others scan from the first lexeme end on
+        int ok = 0;
+        bool scan = false;
+        if (!(sc & kScanReject)) {
+          if (scan_ends(sc) < 2) ok = summary_verdict<true, MW>(rc, ln, sc, lx, n, byte_at, lane_area, kFastLane);
+          else scan = true;
+        }
+        if (scan) {
+          int qs = q1;
+          uint32_t is = 1;
+          const uint32_t p = scan_p_first(sc);
+          if (p > 0) {  // bytes 1 .. p-1 only extend the pending lexeme
+            for (uint32_t i = 1; i < p; ++i) {
+              const uint32_t b = byte_at(i);
+              if (lx.need) lex_push(tb, rl.sl, lx, b);
+            }
+            qs = (int)scan_q_first(sc);
+            is = p;
+          }
+          ok = walk_bytes<true, MW>(rc, ln, qs, lx, is, n, byte_at, step, lane_area, kFastLane);
+        }
         if (ok < 0) {  // the lane's stack area is too small: hand over
           RowHeader* hdr = (RowHeader*)rw;
           const uint32_t slot = atomicAdd(&hdr->slow_count, 1u);
@@ -1200,6 +1361,7 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
       u = u1;
       rk = rk1;
       tl = tl1;
+      sc = sc1;
     }
   }
 
@@ -1240,14 +1402,14 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
       }
       I_s[tid] = iw;
     }
-    const ParseTabs pt = global_parse(tb);  // rare: tables stay in global memory
+    const ParseTabs<false> pt = global_parse(tb);  // rare: tables stay in global memory
     __syncthreads();
     if (tid < kSlowThreads) {
       const grid_config cfg = cfgs[row];
-      RowCtx rc;
+      RowCtx<false> rc;
       rc.tb = &tb;
       rc.pt = pt;
-      rc.bs = BaseStack{pool + cfg.stk_off, nullptr, cfg.stk_depth, cfg.stk_depth};
+      rc.bs = BaseStack<false>{pool + cfg.stk_off, nullptr, cfg.stk_depth, cfg.stk_depth};
       rc.sl = load_slot(tb, cfg.slot);
       rc.tv = TermView{tb.term_info, I_s, hdr->R, tb.live, 8};
       rc.acc_off = tb.acc_off;
@@ -1277,8 +1439,8 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
         for (int w = 0; w < MW; ++w) ln.acur[w] = hdr->A[w];
         const uint32_t base = tb.spell_off[su];
         auto byte_at = [&](uint32_t i) -> uint32_t { return tb.spell_bytes[base + i]; };
-        const int ok = walk_bytes<MW>(rc, ln, cfg.q, lex0, 0u, tb.spell_off[su + 1] - base, byte_at, step, ov,
-                                      kSlowLane);
+        const int ok = walk_bytes<false, MW>(rc, ln, cfg.q, lex0, 0u, tb.spell_off[su + 1] - base, byte_at, step,
+                                             ov, kSlowLane);
         if (ok > 0) {
           atomicOr((uint32_t*)(rw + RL.smask) + (su >> 5), 1u << (su & 31));
           slow_ok = 1;
@@ -1466,7 +1628,7 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
                                GRID_ART_ALIAS_OFF,   GRID_ART_ALIAS_IDS,   GRID_ART_LEX_FLAGS,
                                GRID_ART_LEX_HASH,    GRID_ART_LEX_SLOTS,   GRID_ART_PARSE_STATE,
                                GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH,   GRID_ART_LEX_PREFIX,
-                               GRID_ART_SPELL_RANGE, GRID_ART_SPELL_OF_ID};
+                               GRID_ART_SPELL_RANGE, GRID_ART_SPELL_OF_ID, GRID_ART_SCAN_SUMMARY};
   for (int w : needed)
     if (!bound(g, w)) return fail(GRID_E_UNBOUND, "grid_mask: artifact " + std::to_string(w) + " is not bound");
   Tables tb;
@@ -1476,11 +1638,10 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   tb.acc_list = (const uint8_t*)g->dev[GRID_ART_DFA_ACCEPT_LIST];
   tb.live = (const uint32_t*)g->dev[GRID_ART_DFA_LIVE];
   tb.action = (const uint16_t*)g->dev[GRID_ART_ACTION];
-  tb.prod = (const uint32_t*)g->dev[GRID_ART_PROD];
   tb.term_info = (const uint32_t*)g->dev[GRID_ART_TERM_INFO];
   tb.pstate = (const uint32_t*)g->dev[GRID_ART_PARSE_STATE];
   tb.predx = (const uint32_t*)g->dev[GRID_ART_PARSE_REDX];
-  tb.ghash = (const uint8_t*)g->dev[GRID_ART_GOTO_HASH];
+  tb.ghash = (const uint2*)g->dev[GRID_ART_GOTO_HASH];
   tb.spell_off = (const uint32_t*)g->dev[GRID_ART_SPELL_OFF];
   tb.spell_bytes = (const uint8_t*)g->dev[GRID_ART_SPELL_BYTES];
   tb.spell_rec = (const uint4*)g->dev[GRID_ART_SPELL_REC];
@@ -1493,6 +1654,7 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   tb.lex_prefix = (const uint4*)g->dev[GRID_ART_LEX_PREFIX];
   tb.sub_range = (const uint16_t*)g->dev[GRID_ART_SPELL_RANGE];
   tb.spell_of_id = (const uint32_t*)g->dev[GRID_ART_SPELL_OF_ID];
+  tb.scan = g->scan.empty() ? nullptr : (const uint32_t*)g->dev[GRID_ART_SCAN_SUMMARY];
   tb.S = g->dfa.S;
   tb.C = g->dfa.C;
   tb.T = g->parser.T;
@@ -1509,16 +1671,20 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   tb.n_predx = (int)g->parser.predx.size();
   tb.n_acc = (int)g->dfa.accept_list.size();
   tb.hbits = g->parser.goto_hbits;
-  const int mw = tb.tw <= 4 ? 4 : 8;
+  const int mw = tb.tw;
   const WalkLds WL = walk_lds(tb, mw, B);
-  if (tb.T > 255 || tb.tw > 8 || WL.total + 64 > kWalkLdsMax || parse_lds(tb, 0).total > 24 * 1024)
+  if (tb.T > 255 || (mw != 2 && mw != 4 && mw != 8) || WL.total + 64 > kWalkLdsMax ||
+      parse_lds(tb, 0).total > 24 * 1024)
     return fail(GRID_E_CAPACITY, "grid_mask: lexer DFA or LR tables too large for the LDS staging");
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace_dev;
-  const int rc = mw == 4 ? launch_mask<4>(tb, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, ws, rb,
-                                          phases, s)
-                         : launch_mask<8>(tb, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, ws, rb,
-                                          phases, s);
+  int rc;
+  if (mw == 2)
+    rc = launch_mask<2>(tb, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, ws, rb, phases, s);
+  else if (mw == 4)
+    rc = launch_mask<4>(tb, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, ws, rb, phases, s);
+  else
+    rc = launch_mask<8>(tb, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, ws, rb, phases, s);
   if (rc != GRID_OK) return rc;
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_mask launch: ") + hipGetErrorString(e));

@@ -318,14 +318,21 @@ Parser build_parser(const GrammarText& g, const std::vector<std::string>& drop) 
 // Compact tables for simulating a whole set of lookahead terminals at once:
 // per state the terminals that shift (or accept, end-of-input column), the
 // terminals reduced by the state's main production, and any further reduce
-// productions with their own terminal sets; GOTO as per-state lists.
+// productions with their own terminal sets; productions appear as
+// lhs | length << 16, so a reduce needs no further lookup; GOTO as an
+// open-addressing hash of (key, target) pairs.  Terminal sets take TW words,
+// TW a power of two (at least 2), and a state record is padded to a multiple of 16 bytes
+// so the kernels read it with 16-byte loads.
 void compact_tables(Parser& P) {
   const int T1 = P.T + 1;
-  const int TW = (T1 + 31) / 32;
+  int TW = 2;
+  while (TW * 32 < T1) TW *= 2;
+  if (TW > kTermWords) throw Error(GRID_E_CAPACITY, "more than 255 terminals");
   P.tw = TW;
-  const int stride = 2 * TW + 2;
+  const int stride = parse_record_words(TW);
   P.pstate.assign((size_t)P.n_states * stride, 0);
   P.predx.clear();
+  auto packed = [&](int p) { return P.prod[p]; };  // lhs | length << 16
   std::vector<std::pair<uint32_t, uint16_t>> gotos;
   for (int s = 0; s < P.n_states; ++s) {
     uint32_t* rec = &P.pstate[(size_t)s * stride];
@@ -342,7 +349,7 @@ void compact_tables(Parser& P) {
         g[t >> 5] |= 1u << (t & 31);
       }
     }
-    int main_prod = 0xFFFF;
+    int main_prod = -1;
     size_t best = 0;
     for (auto& g : groups) {
       size_t n = 0;
@@ -350,17 +357,20 @@ void compact_tables(Parser& P) {
       if (n > best) { best = n; main_prod = g.first; }
     }
     uint32_t n_extra = 0;
-    rec[2 * TW + 1] = (uint32_t)P.predx.size();
+    const size_t off = P.predx.size();
+    if (off >= (1u << 24)) throw Error(GRID_E_CAPACITY, "reduce groups larger than 2^24 words");
     for (auto& g : groups) {
       if (g.first == main_prod) {
         for (int w = 0; w < TW; ++w) rec[TW + w] = g.second[w];
       } else {
-        P.predx.push_back((uint32_t)g.first);
+        P.predx.push_back(packed(g.first));
         P.predx.insert(P.predx.end(), g.second.begin(), g.second.end());
         ++n_extra;
       }
     }
-    rec[2 * TW] = (uint32_t)main_prod | n_extra << 16;
+    if (n_extra > 255) throw Error(GRID_E_CAPACITY, "more than 255 reduce productions in one state");
+    rec[2 * TW] = main_prod < 0 ? 0xFFFFFFFFu : packed(main_prod);
+    rec[2 * TW + 1] = n_extra | (uint32_t)off << 8;
     for (int a = 0; a < P.N; ++a) {
       const uint16_t g = P.gto(s, a);
       if (g != kNoGoto) gotos.push_back({goto_key(s, a), g});
@@ -371,19 +381,15 @@ void compact_tables(Parser& P) {
   while ((size_t)1 << hb < gotos.size() + gotos.size() / 2) ++hb;
   if (P.n_states >= 0xFFFF || P.N > 0xFFFF) throw Error(GRID_E_CAPACITY, "more than 65534 LR states");
   const uint32_t H = 1u << hb;
-  std::vector<uint32_t> keys(H, 0);
-  std::vector<uint16_t> vals(H, kNoGoto);
+  P.goto_hbits = hb;
+  P.goto_hash.assign((size_t)H * 2, 0);
   for (auto& e : gotos)
     for (uint32_t h = goto_slot(e.first, hb);; h = (h + 1) & (H - 1))
-      if (keys[h] == 0) {
-        keys[h] = e.first;
-        vals[h] = e.second;
+      if (P.goto_hash[2 * h] == 0) {
+        P.goto_hash[2 * h] = e.first;
+        P.goto_hash[2 * h + 1] = e.second;
         break;
       }
-  P.goto_hbits = hb;
-  P.goto_hash.resize((size_t)H * 6);
-  memcpy(P.goto_hash.data(), keys.data(), (size_t)H * 4);
-  memcpy(P.goto_hash.data() + (size_t)H * 4, vals.data(), (size_t)H * 2);
 }
 
 }  // namespace grid

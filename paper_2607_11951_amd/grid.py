@@ -27,7 +27,7 @@ ART_NAMES = ["DFA_DENSE", "DFA_CLASS", "BYTE_CLASS", "DFA_ACCEPT_OFF", "DFA_ACCE
              "ACTION", "GOTO", "PROD", "TERM_INFO", "SPELL_OFF", "SPELL_BYTES", "ALIAS_OFF",
              "ALIAS_IDS", "TRIE_LEVEL_OFF", "TRIE_NODES", "LEX_FLAGS", "LEX_HASH", "LEX_SLOTS",
              "SPELL_REC", "PARSE_STATE", "PARSE_REDX", "GOTO_HASH", "SPELL_TAIL", "LEX_PREFIX",
-             "SPELL_RANGE", "SPELL_OF_ID"]
+             "SPELL_RANGE", "SPELL_OF_ID", "SCAN_SUMMARY"]
 ART = {n: i for i, n in enumerate(ART_NAMES)}
 
 CONFIG_DTYPE = np.dtype([("stk_off", "<u4"), ("stk_depth", "<u4"), ("lexnode", "<u4"), ("q", "<u2"),

@@ -289,3 +289,112 @@ def test_dfa_tables_consistent(G):
     assert (dense == nxt[:, cls]).all()
     assert (dense[0] == 0).all()           # the dead state is absorbing
     assert len(set(cls.tolist())) == C
+
+
+def _munch_summary(dense, accepting, q, sp):
+    # maximal munch over sp from DFA state q, written out byte by byte
+    cur, ends, q_first, p_first = q, 0, 0, 0
+    for i, b in enumerate(sp):
+        nq = int(dense[cur, b])
+        if nq != 0:
+            cur = nq
+            continue
+        if not accepting[cur]:
+            return 1 << 28
+        if ends == 0:
+            q_first, p_first = cur, i
+        ends += 1
+        if ends == 2:
+            return q_first << 9 | p_first << 18 | 2 << 26
+        cur = int(dense[1, b])
+        if cur == 0:
+            return 1 << 28
+    return cur | q_first << 9 | p_first << 18 | ends << 26
+
+
+def test_scan_summary_matches_maximal_munch(G):
+    rng = np.random.default_rng(11)
+    alphabet = np.frombuffer(b"selct frmwhe*,()'0123456789abcxyz_.=<>;\n\t-\"", np.uint8)
+    vocab = [bytes([b]) for b in range(256)]
+    vocab += [bytes(rng.choice(alphabet, int(n))) for n in rng.integers(2, 40, 600)]
+    vocab += [b"SELECT", b" FROM", b"'abc'", b"),", b"1;", b"x" * 200]
+    g = G.Grid(grammar_text("sql_dml"), ["insert", "update", "delete"], vocab)
+    info = g.info()
+    S, U = info["n_dfa_states"], info["n_spellings"]
+    dense = np.frombuffer(g.artifact("DFA_DENSE"), np.uint16).reshape(S, 256)
+    aoff = np.frombuffer(g.artifact("DFA_ACCEPT_OFF"), np.uint32)
+    accepting = aoff[1:] > aoff[:-1]
+    off = np.frombuffer(g.artifact("SPELL_OFF"), np.uint32)
+    data = np.frombuffer(g.artifact("SPELL_BYTES"), np.uint8)
+    scan = np.frombuffer(g.artifact("SCAN_SUMMARY"), np.uint32).reshape(S, U)
+    seen = set()
+    for u in range(U):
+        sp = data[off[u]:off[u + 1]].tolist()
+        for q in range(S):
+            got = int(scan[q, u])
+            assert got == _munch_summary(dense, accepting, q, sp), (q, bytes(sp))
+            seen.add(got >> 26)
+    assert {0, 1, 2, 4} <= seen  # lexeme-internal, one end, several ends, rejected
+
+
+def test_scan_summary_absent_for_large_dfa(G):
+    # more than 512 DFA states: no table (the kernels then scan every byte)
+    kws = [f"Q{i:03d}X{i * 7 % 1000:03d}" for i in range(100)]
+    text = "start E\n" + "".join(f'token K{i} "{k}"\n' for i, k in enumerate(kws))
+    text += "E : " + " | ".join(f"K{i}" for i in range(len(kws))) + " ;\n"
+    g = G.Grid(text, (), [bytes([b]) for b in range(256)])
+    assert g.info()["n_dfa_states"] > 512
+    assert g.artifact("SCAN_SUMMARY") == b""
+
+
+@pytest.mark.parametrize("name,drop", [("expr", []), ("sql_select", []),
+                                       ("sql_dml", ["insert", "update", "delete"])])
+def test_compact_parse_tables_match_dense(G, name, drop):
+    # the kernels' compact LR records and GOTO hash decode to the dense tables
+    g = G.Grid(grammar_text(name), drop, [b"a"])
+    info = g.info()
+    NS, T, N = info["n_lr_states"], info["n_terminals"], info["n_nonterminals"]
+    action = np.frombuffer(g.artifact("ACTION"), np.uint16).reshape(NS, T + 1)
+    go = np.frombuffer(g.artifact("GOTO"), np.uint16).reshape(NS, N)
+    prod = np.frombuffer(g.artifact("PROD"), np.uint32)
+    st = np.frombuffer(g.artifact("PARSE_STATE"), np.uint32)
+    redx = np.frombuffer(g.artifact("PARSE_REDX"), np.uint32)
+    gh = np.frombuffer(g.artifact("GOTO_HASH"), np.uint32).reshape(-1, 2)
+    tw = 2
+    while 32 * tw < T + 1:
+        tw *= 2
+    R = (2 * tw + 2 + 3) // 4 * 4
+    rec = st.reshape(NS, R)
+    for s in range(NS):
+        main, extra = int(rec[s, 2 * tw]), int(rec[s, 2 * tw + 1])
+        groups = []
+        off = extra >> 8
+        for e in range(extra & 0xFF):
+            groups.append((int(redx[off]), redx[off + 1:off + 1 + tw]))
+            off += tw + 1
+        for t in range(T + 1):
+            w, bit = t >> 5, 1 << (t & 31)
+            a = int(action[s, t])
+            if rec[s, w] & bit:
+                got = "shift"
+            elif rec[s, tw + w] & bit:
+                got = main
+            else:
+                got = next((p for p, bits in groups if bits[w] & bit), None)
+            if a == 0:
+                assert got is None, (s, t)
+            elif a & 0xC000 in (0x4000, 0xC000):
+                assert got == "shift", (s, t)
+            else:
+                assert got == int(prod[a & 0x3FFF]), (s, t)
+    H = len(gh)
+    hb = H.bit_length() - 1
+    assert H == 1 << hb and 3 * int((gh[:, 0] != 0).sum()) <= 2 * H
+    for s in range(NS):
+        for a in range(N):
+            key = ((s << 16) | a) + 1
+            h = ((key * 0x9E3779B1) & 0xFFFFFFFF) >> (32 - hb)
+            while gh[h, 0] != 0 and gh[h, 0] != key:
+                h = (h + 1) % H
+            found = int(gh[h, 1]) if gh[h, 0] == key else 0xFFFF
+            assert found == int(go[s, a]), (s, a)
