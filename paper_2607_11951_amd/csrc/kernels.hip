@@ -74,7 +74,8 @@ constexpr int kSub = 64;             // spellings per wave item (one per lane)
 constexpr int kFastLane = 16;        // per-lane stack area in LDS (overlay at the bottom,
                                      // virtual pushes above it)
 constexpr int kRowGroup = 32;        // rows resident in LDS at once (at most)
-constexpr int kWalkWin = 64;         // top stack entries of each resident row in LDS
+constexpr int kWalkWin = 64;         // top stack entries of each row in the walk's LDS
+constexpr int kMaxItems = 512;       // work items of one walk workgroup per row group (at most)
 constexpr uint32_t kWalkLdsMax = 160 * 1024;
 
 struct Tables {
@@ -106,19 +107,26 @@ struct Tables {
 };
 
 // ---------------------------------------------------------------- workspace
+// Row header, written by the prologue: everything the walk needs of a row
+// besides the tables that follow it (the walk copies header, tables and
+// stack window to LDS in one piece).
 struct RowHeader {
   uint32_t A[8];              // allowed terminals of sigma
   uint32_t Aw[8];             // allowed terminals after shifting the winner
   uint32_t R[8];              // terminals whose category the row's lexicon restricts
+  uint32_t alive[8];          // first bytes that can start a token
+  uint32_t slot[8];           // the row's lexicon slot record
   uint32_t eos_ok;
   uint32_t valid;
   int32_t winner;             // pending lexeme's winner at an emission, -1 none
+  uint32_t wkind;             // 0 no winner, 1 the winner is ignored, 2 it shifts
+  uint32_t stk_off, stk_depth, q, lexnode;
+  uint32_t rem_lo, rem_hi, rem_len;  // first 8 bytes and length of the pending lexeme
   uint32_t slow_count;
   int32_t pstat;              // status bits from the prologue
   int32_t wstat;              // status bits from the walk
   uint32_t nonempty;          // the walk allowed some token
-  uint32_t alive[8];          // first bytes whose first-byte entry is not rejected
-  uint32_t pad[25];
+  uint32_t pad[9];
 };
 static_assert(sizeof(RowHeader) == 256, "row header is 256 bytes");
 
@@ -131,20 +139,28 @@ struct Post {                 // stack after shifting one allowed terminal
 static_assert(sizeof(Post) == 32, "post entry is 32 bytes");
 
 struct RowLayout {
-  size_t post, a2, fb, smask, slow, slow_ov, total;
+  size_t cls, win, block, post, a2, smask, slow, slow_ov, total;
 };
 
-// One row's workspace.  smask is the row's mask in sorted-spelling order, one
-// 64-bit word per 64-spelling sub-tile.
-__host__ __device__ inline RowLayout row_layout(int T, int U) {
+__host__ __device__ inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u; }
+
+// One row's workspace: header; trailing-flag tables under A(sigma) and after
+// the winner's shift (one byte per DFA state each); the top kWalkWin states
+// of the stack; [block ends here]; post-shift stacks and allowed sets of the
+// allowed terminals; the row's mask in sorted-spelling order (one 64-bit word
+// per 64-spelling sub-tile); the slow path's list and stack areas.
+__host__ __device__ inline RowLayout row_layout(int T, int U, int S) {
   RowLayout L;
   size_t o = sizeof(RowHeader);
+  L.cls = o;
+  o += 2 * (size_t)pad16((uint32_t)S);
+  L.win = o;
+  o += kWalkWin * 2;
+  L.block = o;
   L.post = o;
   o += (size_t)T * sizeof(Post);
   L.a2 = o;
   o += (size_t)T * 32;
-  L.fb = o;
-  o += 256 * 4;
   L.smask = o;
   o += (size_t)((U + 63) / 64) * 8;
   L.slow = o;
@@ -155,19 +171,71 @@ __host__ __device__ inline RowLayout row_layout(int T, int U) {
   return L;
 }
 
-// first-byte table entry: q | kind << 16 | fresh << 18 | t1 << 24 (kind 0
-// rejected, 1 alive on sigma, 2 alive after shifting t1; fresh: the byte
-// starts a new lexeme)
-constexpr uint32_t kFbDead = 0, kFbMode0 = 1, kFbMode1 = 2;
 
-__host__ __device__ inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u; }
+// Several global -> LDS copies (each region 16-byte aligned) in one pass:
+// the regions' 16-byte chunks are numbered consecutively and every thread
+// issues the loads of K chunks before it stores any, so the whole staging
+// costs about one memory round trip instead of one per region.  The last,
+// partial chunk of a region is copied byte by byte.
+struct StageRegion {
+  const uint8_t* src;
+  uint8_t* dst;
+  uint32_t bytes;
+};
 
-// Copies bytes from global to LDS with 16-byte loads (both 16-byte aligned).
-__device__ inline void stage16(uint8_t* dst, const uint8_t* src, uint32_t bytes, int tid, int nt) {
-  const uint32_t n16 = bytes >> 4;
-#pragma unroll 4
-  for (uint32_t i = tid; i < n16; i += nt) reinterpret_cast<uint4*>(dst)[i] = reinterpret_cast<const uint4*>(src)[i];
-  for (uint32_t i = (n16 << 4) + tid; i < bytes; i += nt) dst[i] = src[i];
+template <int N, int K>
+__device__ inline void stage_regions(const StageRegion (&rg)[N], int tid, int nt) {
+  uint32_t total = 0;
+#pragma unroll
+  for (int j = 0; j < N; ++j) total += (rg[j].bytes + 15u) / 16u;
+  for (uint32_t base = tid; base < total; base += (uint32_t)nt * K) {
+    uint4 v[K];
+    uint8_t* dst[K];
+    uint32_t left[K];  // bytes of the region from this chunk on (0: no chunk)
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const uint32_t i = base + (uint32_t)(k * nt);
+      // the region holding chunk i, chosen without indexing rg at run time
+      const uint8_t* src = rg[0].src;
+      dst[k] = rg[0].dst;
+      uint32_t bytes = rg[0].bytes, first = 0, pre = 0;
+#pragma unroll
+      for (int t = 0; t < N; ++t) {
+        if (t > 0 && i >= pre) {
+          src = rg[t].src;
+          dst[k] = rg[t].dst;
+          bytes = rg[t].bytes;
+          first = pre;
+        }
+        pre += (rg[t].bytes + 15u) / 16u;
+      }
+      const uint32_t off = (i - first) * 16u;
+      left[k] = i < total ? bytes - off : 0u;
+      src += off;
+      dst[k] += off;
+      v[k] = make_uint4(0, 0, 0, 0);
+      if (left[k] >= 16u) {
+        v[k] = *reinterpret_cast<const uint4*>(src);
+      } else if (left[k] > 0) {
+        uint32_t w[4] = {0, 0, 0, 0};
+#pragma unroll
+        for (int b = 0; b < 16; ++b)  // independent loads, all in flight
+          if ((uint32_t)b < left[k]) w[b >> 2] |= (uint32_t)src[b] << (8 * (b & 3));
+        v[k] = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (left[k] >= 16u) {
+        *reinterpret_cast<uint4*>(dst[k]) = v[k];
+      } else if (left[k] > 0) {
+        const uint32_t w[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
+#pragma unroll
+        for (int b = 0; b < 16; ++b)
+          if ((uint32_t)b < left[k]) dst[k][b] = (uint8_t)(w[b >> 2] >> (8 * (b & 3)));
+      }
+    }
+  }
 }
 
 // Terminal set of every terminal (not the end of input), word w.
@@ -229,10 +297,14 @@ __host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base) {
   return L;
 }
 
-__device__ inline ParseTabs<true> stage_parse(const Tables& tb, uint8_t* lds, const ParseLds& L, int tid, int nt) {
-  stage16(lds + L.st, (const uint8_t*)tb.pstate, (uint32_t)tb.n_pstate * 4, tid, nt);
-  stage16(lds + L.redx, (const uint8_t*)tb.predx, (uint32_t)tb.n_predx * 4, tid, nt);
-  stage16(lds + L.ghash, (const uint8_t*)tb.ghash, 8u << tb.hbits, tid, nt);
+__device__ inline StageRegion parse_region(const Tables& tb, uint8_t* lds, const ParseLds& L, int which) {
+  if (which == 0) return {(const uint8_t*)tb.pstate, lds + L.st, (uint32_t)tb.n_pstate * 4};
+  if (which == 1) return {(const uint8_t*)tb.predx, lds + L.redx, (uint32_t)tb.n_predx * 4};
+  return {(const uint8_t*)tb.ghash, lds + L.ghash, 8u << tb.hbits};
+}
+
+// The LR tables in LDS (the caller stages them, see parse_region).
+__device__ inline ParseTabs<true> lds_parse(const Tables& tb, uint8_t* lds, const ParseLds& L) {
   return {in_mem<true>((const uint32_t*)(lds + L.st)), in_mem<true>((const uint32_t*)(lds + L.redx)),
           in_mem<true>((const u32x2*)(lds + L.ghash)), tb.action, tb.T, tb.hbits};
 }
@@ -663,11 +735,17 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   __shared__ int bad, overflow, winner, eos_ok;
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
-  const RowLayout L = row_layout(tb.T, tb.U);
+  const RowLayout L = row_layout(tb.T, tb.U, tb.S);
   Post* post = (Post*)(rw + L.post);
   uint32_t* a2 = (uint32_t*)(rw + L.a2);
   const grid_config cfg = cfgs[row];
-  const ParseTabs<true> pt = stage_parse(tb, plds, parse_lds(tb, 0), tid, kBlock);
+  const ParseLds PL = parse_lds(tb, 0);
+  {
+    const StageRegion rg[3] = {parse_region(tb, plds, PL, 0), parse_region(tb, plds, PL, 1),
+                               parse_region(tb, plds, PL, 2)};
+    stage_regions<3, 8>(rg, tid, kBlock);
+  }
+  const ParseTabs<true> pt = lds_parse(tb, plds, PL);
 
   if (tid == 0) {
     int b = 0;
@@ -785,43 +863,41 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     eos_ok = ok;
   }
   __syncthreads();
-  // phase 3: first-byte table
-  uint32_t* fb = (uint32_t*)(rw + L.fb);
+  // phase 3: which first bytes can start a token (continuing the pending
+  // lexeme, or emitting it as its winner and starting a new one), and the
+  // trailing-flag tables of every DFA state under A(sigma) and after the
+  // winner's shift
   {
     const int b = tid;  // kBlock == 256: one byte value per thread
     const uint32_t c = tb.bclass[b];
-    uint32_t kind = kFbDead, q1 = 0, t1 = 0, lex1 = kNoLex;
+    bool live = false;
     uint32_t a0[MW], aw[MW];
 #pragma unroll
     for (int k = 0; k < MW; ++k) {
       a0[k] = A[k];
       aw[k] = Aw[k];
     }
-    uint32_t fresh = 0;
     const int nq = tb.dfa[(size_t)cfg.q * tb.C + c];
     if (nq != kDead) {
-      lex1 = lex_child(tb, sl, cfg.lexnode, b);
-      if (trail_ok<MW>(tv, a0, nq, lex_flags_of(tb, sl, lex1))) {
-        kind = kFbMode0;
-        q1 = nq;
-      }
+      live = trail_ok<MW>(tv, a0, nq, lex_flags_of(tb, sl, lex_child(tb, sl, cfg.lexnode, b)));
     } else if (!rem_empty && w >= 0) {
       const int sq = tb.dfa[(size_t)kStart * tb.C + c];
       if (sq != kDead) {
-        lex1 = lex_child(tb, sl, 0u, b);
-        const uint32_t lf1 = lex_flags_of(tb, sl, lex1);
-        if (!w_shifts) {
-          if (trail_ok<MW>(tv, a0, sq, lf1)) kind = kFbMode0;
-        } else if (trail_ok<MW>(tv, aw, sq, lf1)) {
-          kind = kFbMode1;
-          t1 = (uint32_t)w;
-        }
-        q1 = sq;
-        fresh = 1;
+        const uint32_t lf1 = lex_flags_of(tb, sl, lex_child(tb, sl, 0u, b));
+        live = w_shifts ? trail_ok<MW>(tv, aw, sq, lf1) : trail_ok<MW>(tv, a0, sq, lf1);
       }
     }
-    fb[b] = q1 | kind << 16 | fresh << 18 | t1 << 24;
-    if (kind != kFbDead) atomicOr(&alive[b >> 5], 1u << (b & 31));
+    if (live) atomicOr(&alive[b >> 5], 1u << (b & 31));
+    uint8_t* clsA = rw + L.cls;
+    uint8_t* clsW = clsA + pad16((uint32_t)tb.S);
+    for (int q = tid; q < tb.S; q += kBlock) {
+      clsA[q] = (uint8_t)trail_flags<MW>(tv, a0, q);
+      clsW[q] = (uint8_t)trail_flags<MW>(tv, aw, q);
+    }
+    // the top of the stack for the walk's LDS
+    uint16_t* wwin = (uint16_t*)(rw + L.win);
+    const uint32_t wlo = depth > (uint32_t)kWalkWin ? depth - kWalkWin : 0u;
+    if ((uint32_t)tid < depth - wlo) wwin[tid] = win[wlo + tid - lo];
   }
   __syncthreads();
   if (tid < 8) {
@@ -829,11 +905,22 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     hdr->A[tid] = A[tid];
     hdr->Aw[tid] = Aw[tid];
     hdr->R[tid] = R[tid];
+    hdr->slot[tid] = tb.lex_slots[(size_t)cfg.slot * kSlotWords + tid];
   }
   if (tid == 0) {
     hdr->eos_ok = (uint32_t)eos_ok;
     if (eos_out) eos_out[row] = (uint8_t)eos_ok;
     hdr->winner = w;
+    hdr->wkind = w < 0 ? 0u : (w_shifts ? 2u : 1u);
+    hdr->stk_off = cfg.stk_off;
+    hdr->stk_depth = depth;
+    hdr->q = cfg.q;
+    hdr->lexnode = cfg.lexnode;
+    hdr->rem_lo = (uint32_t)cfg.rem_head[0] | (uint32_t)cfg.rem_head[1] << 8 | (uint32_t)cfg.rem_head[2] << 16 |
+                  (uint32_t)cfg.rem_head[3] << 24;
+    hdr->rem_hi = (uint32_t)cfg.rem_head[4] | (uint32_t)cfg.rem_head[5] << 8 | (uint32_t)cfg.rem_head[6] << 16 |
+                  (uint32_t)cfg.rem_head[7] << 24;
+    hdr->rem_len = rem_empty ? 0u : cfg.rem_len;
     hdr->slow_count = 0;
     hdr->wstat = 0;
     hdr->nonempty = 0;
@@ -846,7 +933,10 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
 // A lane's parser side.  Mode 0: the stack is sigma and acur = A(sigma).
 // Mode 1: sigma plus the shift of t1, acur = that stack's allowed set (from
 // the prologue).  Mode 2: a stack of its own (base[0,k) ++ overlay[0,m)) and
-// its allowed set, set-simulated after every shift.
+// the part of its allowed set that the current lexeme can still use: after
+// every shift only the terminals live in the DFA state reached by the next
+// lexeme's first byte are set-simulated (live sets only shrink along a
+// lexeme, so every later check of that lexeme asks about a subset of them).
 template <int MW>
 struct Lane {
   int mode;
@@ -873,16 +963,34 @@ struct RowCtx {
   const Post* post;         // row's stacks after each first shift (global)
 };
 
-// Emits the pending lexeme in DFA state q (lexicon state lx).  ov is the
-// lane's stack area of cap entries: the overlay occupies [0, m), virtual
-// pushes use [m, cap).  1 ok, 0 reject, -1 capacity.
+// Mode 2: acur = the allowed terminals of the lane's stack among those live
+// in DFA state q_next (ignored ones left out: they are always viable).  1 ok,
+// -1 capacity.
+template <bool L, int MW>
+__device__ __forceinline__ int lane_allowed(const RowCtx<L>& rc, Lane<MW>& ln, mptr<L, uint16_t> ov, int cap,
+                                            int q_next) {
+  uint32_t X[MW];
+  const uint32_t* lv = rc.tv.live + (size_t)q_next * rc.tv.lstride;
+#pragma unroll
+  for (int w = 0; w < MW; ++w) {
+    X[w] = q_next == kDead ? 0u : lv[w] & ~rc.tv.I[w];
+    ln.acur[w] = 0;
+  }
+  return sim_set<L, MW>(rc.pt, rc.bs, ln.k, ln.m, ov, ov + ln.m, cap - ln.m, X, ln.acur) < 0 ? -1 : 1;
+}
+
+// Emits the pending lexeme in DFA state q (lexicon state lx); q_next is the
+// DFA state after the next lexeme's first byte.  ov is the lane's stack area
+// of cap entries: the overlay occupies [0, m), virtual pushes use [m, cap).
+// 1 ok, 0 reject, -1 capacity.
 template <bool L, int MW>
 __device__ __forceinline__ int emit(const RowCtx<L>& rc, Lane<MW>& ln, mptr<L, uint16_t> ov, int cap, int q,
-                                    const LexState& lx) {
+                                    const LexState& lx, int q_next) {
   const int t = winner_of<MW>(rc.tv, rc.acc_off, rc.acc_list, ln.acur, q,
                               [&]() { return lex_flags_now(*rc.tb, rc.sl, lx); });
   if (t < 0) return 0;
-  if (bit_of(rc.tv.I, t)) return 1;  // ignored: the stack is unchanged
+  if (bit_of(rc.tv.I, t))  // ignored: the stack is unchanged, but in mode 2
+    return ln.mode == 2 ? lane_allowed<L, MW>(rc, ln, ov, cap, q_next) : 1;  // the next lexeme asks anew
   if (ln.mode == 0) {
     ln.mode = 1;
     ln.t1 = t;
@@ -900,7 +1008,7 @@ __device__ __forceinline__ int emit(const RowCtx<L>& rc, Lane<MW>& ln, mptr<L, u
   }
   const int r = sim1_shift<L, MW>(rc.pt, rc.bs, ln.k, ln.m, ov, cap, t);
   if (r != 1) return r < 0 ? -1 : 0;
-  return allowed_set<L, MW>(rc.pt, rc.bs, ln.k, ln.m, ov, ov + ln.m, cap - ln.m, ln.acur) < 0 ? -1 : 1;
+  return lane_allowed<L, MW>(rc, ln, ov, cap, q_next);
 }
 
 struct DfaView {  // lexer DFA by byte class (LDS copy or global)
@@ -959,7 +1067,7 @@ __device__ __forceinline__ int walk_bytes(const RowCtx<L>& rc, Lane<MW>& ln, int
     const bool em = status == 2 && pend >= 0;
     if (!__any(em)) break;
     if (em) {  // emission phase
-      const int r = emit<L, MW>(rc, ln, ov, cap, q, lx);
+      const int r = emit<L, MW>(rc, ln, ov, cap, q, lx, step.next(kStart, (uint32_t)pend));
       if (r <= 0) {
         status = r;
       } else {
@@ -996,7 +1104,7 @@ __device__ __forceinline__ int summary_verdict(const RowCtx<L>& rc, Lane<MW>& ln
       const uint32_t b = byte_at(i);
       if (lx.need) lex_push(tb, rc.sl, lx, b);
     }
-    const int r = emit<L, MW>(rc, ln, ov, cap, (int)scan_q_first(sc), lx);
+    const int r = emit<L, MW>(rc, ln, ov, cap, (int)scan_q_first(sc), lx, kDead);  // mode 0: no simulation
     if (r <= 0) return 0;
     lx = LexState{byte_at(p), 1u, kNoLex, 1u};
     i = p + 1;
@@ -1013,29 +1121,16 @@ __device__ __forceinline__ int summary_verdict(const RowCtx<L>& rc, Lane<MW>& ln
 }
 
 // -------------------------------------------------------------------- walk
-// Per-row data a walk workgroup keeps in LDS for every row of its group.
-struct RowLds {
-  uint32_t A[8], Aw[8], R[8];
-  uint32_t alive[8];  // first bytes whose first-byte entry is not rejected
-  Slot sl;
-  uint32_t valid, stk_off, stk_depth;
-  uint32_t rem_lo, rem_hi;  // first 8 bytes of the pending lexeme
-  uint32_t rem_len;
-  uint32_t lexnode;         // lexicon node of the pending lexeme
-  int32_t winner;           // its winner when a byte ends it (-1 none)
-  uint32_t q;               // DFA state of the pending lexeme (clamped below S)
-  uint32_t pad[16];
-};
-static_assert(sizeof(RowLds) == 256, "row record is 256 bytes");
-
 struct WalkLds {  // byte offsets into dynamic LDS
-  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, live, range, lanes, rows, fb, cls, win, total;
-  uint32_t cls_row;  // bytes per row of trailing-flag tables (two of S entries)
-  int group;         // rows per group
+  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, live, range, lanes, umask, upre, rows, total;
+  uint32_t block;  // bytes per resident row: header, trailing-flag tables, stack window
+  int group;       // rows per group
   ParseLds pl;
 };
 
-__host__ __device__ inline WalkLds walk_lds(const Tables& tb, int mw, int B) {
+// blocks: the walk's grid size (a group's items per workgroup stay within
+// kMaxItems)
+__host__ __device__ inline WalkLds walk_lds(const Tables& tb, int mw, int B, int blocks) {
   WalkLds w;
   uint32_t o = 0;
   w.dfa = o;
@@ -1059,22 +1154,22 @@ __host__ __device__ inline WalkLds walk_lds(const Tables& tb, int mw, int B) {
   o += pad16((uint32_t)((tb.U + 63) / 64) * 2);
   w.lanes = o;
   o += kWalkThreads * kFastLane * 2;
+  w.umask = o;  // per work item: its undecided lanes
+  o += kMaxItems * 8;
+  w.upre = o;   // prefix counts of undecided lanes over the items
+  o += (kMaxItems + 4) * 4;
   // as many rows as fit beside the static LDS (counters), at most kRowGroup
-  // and B
+  // and B, with at most kMaxItems items per workgroup
   const uint32_t fixed = o + 64;
-  w.cls_row = 2 * pad16((uint32_t)tb.S);
-  const uint32_t per_row = sizeof(RowLds) + 256 * 4 + w.cls_row + kWalkWin * 2;
+  w.block = (uint32_t)row_layout(tb.T, tb.U, tb.S).block;
+  const int nsub = (tb.U + kSub - 1) / kSub;
   int g = kRowGroup < B ? kRowGroup : B;
-  while (g > 1 && fixed + per_row * (uint32_t)g > kWalkLdsMax) --g;
+  while (g > 1 && (fixed + w.block * (uint32_t)g > kWalkLdsMax ||
+                   (long long)g * nsub > (long long)kMaxItems * blocks))
+    --g;
   w.group = g;
   w.rows = o;
-  o += sizeof(RowLds) * (uint32_t)g;
-  w.fb = o;
-  o += 256 * 4 * (uint32_t)g;
-  w.cls = o;
-  o += w.cls_row * (uint32_t)g;
-  w.win = o;
-  o += kWalkWin * 2 * (uint32_t)g;
+  o += w.block * (uint32_t)g;
   w.total = o;
   return w;
 }
@@ -1121,46 +1216,245 @@ __device__ inline int wave_grab(int* ctr) {
   return __builtin_amdgcn_readfirstlane(v);
 }
 
-// Persistent, one workgroup per compute unit.  The grammar tables are staged
-// once; then, for each group of rows that fits, the rows' first-byte tables
-// and scalars are staged.  A work item is one row against one 64-spelling
-// sub-tile.  The workgroup's share of the items -- every gridDim.x-th in
-// row-major order, so each workgroup sees every row and all of the
-// vocabulary -- is taken by its waves one item at a time from an LDS counter;
-// items whose spellings cannot start a token (the sub-tile's first-byte range
-// misses the row's table) are passed over without loading anything, and the
-// next live item's records and tail chunks are in flight while one is walked.
-// There is no barrier between items.
+// Lane verdict from the scan summary word alone, without the spelling's
+// bytes: 1 allowed, 0 rejected, 2 undecided (the lexicon must see the bytes,
+// or the spelling ends two or more lexemes).  Covers a spelling that stays in
+// the pending lexeme, one whose first byte ends the pending lexeme, and one
+// that ends it later with a winner the lexicon does not restrict; the last
+// lexeme is then judged by its trailing flags under the allowed set it sees.
 template <int MW>
-__global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const grid_config* __restrict__ cfgs,
-                                                            const uint16_t* __restrict__ pool,
+__device__ __forceinline__ int fast_verdict(const RowHeader& h, const uint8_t* clsA, const uint8_t* clsW,
+                                            const uint32_t* I_s, const uint32_t* acc_off, const uint8_t* acc_list,
+                                            const TermView& tv, const uint32_t* a2, uint32_t sc) {
+  if (sc & kScanReject) return 0;
+  const uint32_t ends = scan_ends(sc);
+  if (ends >= 2) return 2;
+  const int qf = (int)scan_q_end(sc);
+  const uint32_t p = scan_p_first(sc);
+  int sel;  // -1 A(sigma), -2 after the winner's shift, >= 0 after shifting that terminal
+  if (ends == 0) {
+    sel = -1;
+  } else if (p == 0) {  // byte 0 ends the pending lexeme: its winner, from the prologue
+    if (h.wkind == 0) return 0;
+    sel = h.wkind == 1 ? -1 : -2;
+  } else {  // bytes 0..p-1 extend the pending lexeme, byte p ends it in q_d
+    const int qd = (int)scan_q_first(sc);
+    int t = -1;
+    for (uint32_t j = acc_off[qd]; j < acc_off[qd + 1]; ++j) {
+      const int c = acc_list[j];
+      if (bit_of(I_s, c)) {
+        t = c;
+        break;
+      }
+      if (!bit_of(h.A, c)) continue;
+      if (bit_of(h.R, c)) return 2;  // the lexicon decides this candidate
+      t = c;
+      break;
+    }
+    if (t < 0) return 0;
+    sel = bit_of(I_s, t) ? -1 : (t == h.winner ? -2 : t);
+  }
+  uint32_t f;
+  if (sel == -1) {
+    f = clsA[qf];
+  } else if (sel == -2) {
+    f = clsW[qf];
+  } else {
+    uint32_t acur[MW];
+#pragma unroll
+    for (int w = 0; w < MW; ++w) acur[w] = a2[sel * 8 + w];
+    f = trail_flags<MW>(tv, acur, qf);
+  }
+  return (f & 1u) ? 1 : ((f & 2u) ? 2 : 0);
+}
+
+// The rank-th set bit of m (rank < popcount(m)).
+__device__ inline int nth_set_bit(uint64_t m, int rank) {
+  int pos = 0;
+#pragma unroll
+  for (int w = 32; w >= 1; w >>= 1) {
+    const uint64_t low = m & ((1ull << w) - 1ull);
+    const int c = __popcll(low);
+    if (rank >= c) {
+      rank -= c;
+      m >>= w;
+      pos += w;
+    } else {
+      m = low;
+    }
+  }
+  return pos;
+}
+
+// Everything the walk's lanes share about the grammar (pointers into LDS).
+template <int MW>
+struct WalkShared {
+  const Tables* tb;
+  ParseTabs<true> pt;
+  DfaView step;
+  const uint32_t* tinfo;
+  const uint32_t* I;
+  const uint32_t* live;
+  const uint32_t* acc_off;
+  const uint8_t* acc_list;
+  const uint16_t* pool;
+};
+
+// Verdict of an undecided lane (see fast_verdict): the spelling's bytes, the
+// lane's state after byte 0, then the lexicon checks of the summary path or
+// the byte-by-byte walk from the first lexeme end.  A lane whose stack area
+// is too small hands its spelling to the slow path.  1 allowed, 0 rejected
+// or handed over.
+template <int MW>
+__device__ __forceinline__ int undecided_lane(const WalkShared<MW>& sh, const RowHeader& h, const uint8_t* rowblk,
+                                              uint8_t* rw, const RowLayout& RL, int u, uint32_t sc,
+                                              mptr<true, uint16_t> lane_area) {
+  const Tables& tb = *sh.tb;
+  const uint8_t* clsA = rowblk + sizeof(RowHeader);
+  const uint8_t* clsW = clsA + pad16((uint32_t)tb.S);
+  const uint4 rk = tb.spell_rec[u];
+  const uint4 tl = tb.spell_tail[u];
+  const uint32_t n = rk.w & 0xFFu;
+  const uint64_t hb = (uint64_t)rk.x | (uint64_t)rk.y << 32;
+  const uint32_t b0 = (uint32_t)(hb & 0xFF);
+  const uint32_t c0 = sh.step.cls(b0);
+  Slot sl;
+  sl.fbase = h.slot[0];
+  sl.hbase = h.slot[1];
+  sl.hmask = h.slot[2];
+  sl.restricted = h.slot[3];
+  sl.nodes = h.slot[4];
+  sl.pbase = h.slot[5];
+  sl.pmask = h.slot[6];
+  RowCtx<true> rc;
+  rc.tb = &tb;
+  rc.pt = sh.pt;
+  rc.bs = BaseStack<true>{sh.pool + h.stk_off, in_mem<true>((const uint16_t*)(rowblk + RL.win)), h.stk_depth,
+                          h.stk_depth > (uint32_t)kWalkWin ? h.stk_depth - kWalkWin : 0u};
+  rc.sl = sl;
+  rc.tv = TermView{sh.tinfo, sh.I, h.R, sh.live, MW};
+  rc.acc_off = sh.acc_off;
+  rc.acc_list = sh.acc_list;
+  rc.a2 = (const uint32_t*)(rw + RL.a2);
+  rc.a2_stride = 8;
+  rc.post = (const Post*)(rw + RL.post);
+  rc.clsA = clsA;
+  rc.clsW = clsW;
+  rc.winner = h.wkind == 2 ? h.winner : -1;
+  Lane<MW> ln;
+  ln.k = 0;
+  ln.m = 0;
+  LexState lx;
+  int q1 = sh.step.next((int)h.q, c0);
+  const uint8_t* ct = clsA;
+  bool dead = false;
+  if (q1 != kDead) {  // byte 0 extends the pending lexeme
+    ln.mode = 0;
+    ln.t1 = -1;
+    lx.len = h.rem_len + 1;
+    lx.w = lx.len <= 8 ? (((uint64_t)h.rem_lo | (uint64_t)h.rem_hi << 32) | (uint64_t)b0 << (8 * h.rem_len)) : 0ull;
+  } else {  // byte 0 ends it: its winner, then a new lexeme
+    dead = h.wkind == 0;
+    q1 = sh.step.next(kStart, c0);
+    dead = dead || q1 == kDead;
+    ln.mode = h.wkind == 2 ? 1 : 0;
+    ln.t1 = h.wkind == 2 ? h.winner : -1;
+    ct = h.wkind == 2 ? clsW : clsA;
+    lx.len = 1;
+    lx.w = b0;
+  }
+#pragma unroll
+  for (int w = 0; w < MW; ++w) ln.acur[w] = ln.mode == 1 ? h.Aw[w] : h.A[w];
+  if (dead) return 0;
+  lx.need = sl.restricted != 0 && (ct[q1] & 2u) ? 1u : 0u;
+  lx.node = lx.need && lx.len > 8 ? lex_child(tb, sl, h.lexnode, b0) : kNoLex;
+  SpellBytes byte_at;
+  byte_at.win = hb >> 8;
+  byte_at.lo0 = (uint64_t)tl.x | (uint64_t)tl.y << 32;
+  byte_at.hi = (uint64_t)tl.z | (uint64_t)tl.w << 32;
+  byte_at.ovf = tb.spell_tail + (rk.w >> 8);
+  int ok = 0;
+  bool scan = false;
+  if (scan_ends(sc) < 2)
+    ok = summary_verdict<true, MW>(rc, ln, sc, lx, n, byte_at, lane_area, kFastLane);
+  else
+    scan = true;
+  if (scan) {
+    int qs = q1;
+    uint32_t is = 1;
+    const uint32_t p = scan_p_first(sc);
+    if (p > 0) {  // bytes 1 .. p-1 only extend the pending lexeme
+      for (uint32_t i = 1; i < p; ++i) {
+        const uint32_t b = byte_at(i);
+        if (lx.need) lex_push(tb, sl, lx, b);
+      }
+      qs = (int)scan_q_first(sc);
+      is = p;
+    }
+    ok = walk_bytes<true, MW>(rc, ln, qs, lx, is, n, byte_at, sh.step, lane_area, kFastLane);
+  }
+  if (ok < 0) {  // the lane's stack area is too small: hand over
+    RowHeader* gh = (RowHeader*)rw;
+    const uint32_t slot = atomicAdd(&gh->slow_count, 1u);
+    if (slot < (uint32_t)kSlowCap) ((uint32_t*)(rw + RL.slow))[slot] = (uint32_t)u;
+    else atomicOr(&gh->wstat, GRID_ROW_OVERFLOW);
+    ok = 0;
+  }
+  return ok;
+}
+
+// Persistent, one workgroup per compute unit.  The grammar tables are staged
+// once; then, for each group of rows that fits, the rows' blocks (header,
+// trailing-flag tables, stack window, all written by the prologue) are copied
+// in one pass.  A work item is one row against one 64-spelling sub-tile.  The
+// workgroup's share of the items -- every gridDim.x-th in row-major order, so
+// each workgroup sees every row and all of the vocabulary -- is taken by its
+// waves one item at a time from an LDS counter; items whose spellings cannot
+// start a token (the sub-tile's first-byte range misses the row's table) are
+// passed over without loading anything.  A lane first judges its spelling
+// from the scan summary word alone (the words of the next two items are in
+// flight meanwhile).  Lanes that stay undecided are only marked; once the
+// group's items are done the marked lanes are packed, 64 to a wave, and
+// each loads its spelling's bytes and runs the lexicon checks or the
+// byte-by-byte walk, so a few undecided lanes no longer hold a whole wave.
+template <int MW>
+__global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const uint16_t* __restrict__ pool,
                                                             uint8_t* __restrict__ ws, size_t rbytes, int B) {
   extern __shared__ __align__(16) uint8_t lds[];
   __shared__ int item_ctr;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const WalkLds WL = walk_lds(tb, MW, B);
-  const RowLayout RL = row_layout(tb.T, tb.U);
+  __shared__ int chunk_ctr;
+  const WalkLds WL = walk_lds(tb, MW, B, (int)gridDim.x);
+  const RowLayout RL = row_layout(tb.T, tb.U, tb.S);
   uint8_t* bcls = lds + WL.bcls;
+  uint64_t* umask_s = (uint64_t*)(lds + WL.umask);
+  uint32_t* upre_s = (uint32_t*)(lds + WL.upre);
   uint32_t* tinfo_s = (uint32_t*)(lds + WL.tinfo);
   uint32_t* I_s = (uint32_t*)(lds + WL.I);
   uint32_t* live_s = (uint32_t*)(lds + WL.live);
-  RowLds* rows_s = (RowLds*)(lds + WL.rows);
-  const uint32_t* fb_all = (const uint32_t*)(lds + WL.fb);
-  uint8_t* cls_all = lds + WL.cls;
-  uint16_t* win_all = (uint16_t*)(lds + WL.win);
+  const uint32_t* acc_off_s = (const uint32_t*)(lds + WL.acc_off);
+  const uint8_t* acc_list_s = lds + WL.acc_list;
+  uint8_t* rows_s = lds + WL.rows;
   const uint16_t* range_s = (const uint16_t*)(lds + WL.range);
   const mptr<true, uint16_t> lane_area = in_mem<true>((uint16_t*)(lds + WL.lanes) + tid * kFastLane);
   uint8_t* rows = ws + kWsHead;
   const int nsub = (tb.U + kSub - 1) / kSub;
+  const uint32_t clsW_off = pad16((uint32_t)tb.S);
 
   // grammar tables, once per workgroup
-  stage16(lds + WL.dfa, (const uint8_t*)tb.dfa, (uint32_t)(tb.S * tb.C * 2), tid, kWalkThreads);
-  stage16(bcls, tb.bclass, 256, tid, kWalkThreads);
-  stage16(lds + WL.acc_off, (const uint8_t*)tb.acc_off, (uint32_t)(tb.S + 1) * 4, tid, kWalkThreads);
-  stage16(lds + WL.acc_list, tb.acc_list, (uint32_t)tb.n_acc, tid, kWalkThreads);
-  stage16(lds + WL.range, (const uint8_t*)tb.sub_range, (uint32_t)nsub * 2, tid, kWalkThreads);
-  const ParseTabs<true> pt = stage_parse(tb, lds, WL.pl, tid, kWalkThreads);
+  {
+    const StageRegion rg[8] = {{(const uint8_t*)tb.dfa, lds + WL.dfa, (uint32_t)(tb.S * tb.C * 2)},
+                               {tb.bclass, bcls, 256u},
+                               {(const uint8_t*)tb.acc_off, lds + WL.acc_off, (uint32_t)(tb.S + 1) * 4},
+                               {tb.acc_list, lds + WL.acc_list, (uint32_t)tb.n_acc},
+                               {(const uint8_t*)tb.sub_range, lds + WL.range, (uint32_t)nsub * 2},
+                               parse_region(tb, lds, WL.pl, 0),
+                               parse_region(tb, lds, WL.pl, 1),
+                               parse_region(tb, lds, WL.pl, 2)};
+    stage_regions<8, 4>(rg, tid, kWalkThreads);
+  }
+  const ParseTabs<true> pt = lds_parse(tb, lds, WL.pl);
   for (int i = tid; i < tb.S * MW; i += kWalkThreads) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
   for (int t = tid; t < 256; t += kWalkThreads) tinfo_s[t] = t < tb.T ? tb.term_info[t] : 0u;
   __syncthreads();
@@ -1172,73 +1466,33 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
   }
 
   const DfaView step{(const uint16_t*)(lds + WL.dfa), bcls, tb.C};
-  const uint4* recs = tb.spell_rec;
-  const uint4* tails = tb.spell_tail;
+  const WalkShared<MW> sh{&tb, pt, step, tinfo_s, I_s, live_s, acc_off_s, acc_list_s, pool};
   for (int g0 = 0; g0 < B; g0 += WL.group) {
     const int gr = min(WL.group, B - g0);
-    __syncthreads();  // the previous group is done with the row tables
-    for (int r = 0; r < gr; ++r) {
-      const uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
-      stage16((uint8_t*)(fb_all + r * 256), rw + RL.fb, 256 * 4, tid, kWalkThreads);
-    }
-
-    for (int r = tid; r < gr; r += kWalkThreads) {
-      const RowHeader* hdr = (const RowHeader*)(rows + (size_t)(g0 + r) * rbytes);
-      const grid_config cfg = cfgs[g0 + r];
-      RowLds& rl = rows_s[r];
-      for (int w = 0; w < 8; ++w) {
-        rl.A[w] = hdr->A[w];
-        rl.Aw[w] = hdr->Aw[w];
-        rl.R[w] = hdr->R[w];
-        rl.alive[w] = hdr->alive[w];
+    __syncthreads();  // the previous group is done with the row blocks
+    {
+      // the rows' blocks, two 16-byte chunks per thread in flight at a time
+      const uint32_t n16 = WL.block / 16u, total = (uint32_t)gr * n16;
+      for (uint32_t i = tid; i < total; i += 2u * kWalkThreads) {
+        const uint32_t i2 = i + kWalkThreads;
+        const uint32_t r = i / n16, r2 = i2 / n16;
+        const uint4 v = reinterpret_cast<const uint4*>(rows + (size_t)(g0 + r) * rbytes)[i - r * n16];
+        uint4 v2 = make_uint4(0, 0, 0, 0);
+        if (i2 < total) v2 = reinterpret_cast<const uint4*>(rows + (size_t)(g0 + r2) * rbytes)[i2 - r2 * n16];
+        reinterpret_cast<uint4*>(rows_s)[i] = v;
+        if (i2 < total) reinterpret_cast<uint4*>(rows_s)[i2] = v2;
       }
-      rl.valid = hdr->valid;
-      rl.stk_off = cfg.stk_off;
-      rl.stk_depth = cfg.stk_depth;
-      rl.sl = load_slot(tb, rl.valid == kRowValid ? cfg.slot : 0);
-      rl.rem_lo = (uint32_t)cfg.rem_head[0] | (uint32_t)cfg.rem_head[1] << 8 | (uint32_t)cfg.rem_head[2] << 16 |
-                  (uint32_t)cfg.rem_head[3] << 24;
-      rl.rem_hi = (uint32_t)cfg.rem_head[4] | (uint32_t)cfg.rem_head[5] << 8 | (uint32_t)cfg.rem_head[6] << 16 |
-                  (uint32_t)cfg.rem_head[7] << 24;
-      rl.rem_len = cfg.flags & 1u ? 0u : cfg.rem_len;
-      rl.lexnode = cfg.lexnode;
-      rl.q = cfg.q < tb.S ? cfg.q : 0u;
-      rl.winner = hdr->winner >= 0 && !((I_s[hdr->winner >> 5] >> (hdr->winner & 31)) & 1u) ? hdr->winner : -1;
     }
-    if (tid == 0) item_ctr = 0;
-    __syncthreads();
-    // the top of every valid row's stack (the prologue checked its entries)
-    for (int i = tid; i < gr * kWalkWin; i += kWalkThreads) {
-      const int r = i / kWalkWin, j = i - r * kWalkWin;
-      const RowLds& rl = rows_s[r];
-      const uint32_t d = rl.stk_depth, lo = d > (uint32_t)kWalkWin ? d - kWalkWin : 0u;
-      if (rl.valid == kRowValid && lo + j < d) win_all[i] = pool[rl.stk_off + lo + j];
-    }
-    // trailing flags of every DFA state under A(sigma) and after the winner's shift
-    for (int i = tid; i < gr * tb.S; i += kWalkThreads) {
-      const int r = i / tb.S, q = i - r * tb.S;
-      const RowLds& rl = rows_s[r];
-      const TermView tv{tinfo_s, I_s, rl.R, live_s, MW};
-      uint32_t a[MW], aw[MW];
-#pragma unroll
-      for (int w = 0; w < MW; ++w) {
-        a[w] = rl.A[w];
-        aw[w] = rl.Aw[w];
-      }
-      uint8_t* ct = cls_all + r * WL.cls_row;
-      ct[q] = (uint8_t)trail_flags<MW>(tv, a, q);
-      ct[WL.cls_row / 2 + q] = (uint8_t)trail_flags<MW>(tv, aw, q);
-    }
-    __syncthreads();
-
     // item k: j = blockIdx.x + k * gridDim.x, row j / nsub, sub-tile j % nsub
     const int total = gr * nsub;
     const int mine = total > (int)blockIdx.x ? (total - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x : 0;
-    auto spelling = [&](int k, int& r) -> int {
-      const int j = (int)blockIdx.x + (k < mine ? k : 0) * (int)gridDim.x;
-      r = j / nsub;
-      return (j - r * nsub) * kSub + lane;
-    };
+    for (int k = tid; k < mine; k += kWalkThreads) umask_s[k] = 0ull;
+    if (tid == 0) {
+      item_ctr = 0;
+      chunk_ctr = 0;
+    }
+    __syncthreads();
+    auto row_hdr = [&](int r) -> const RowHeader& { return *(const RowHeader*)(rows_s + (size_t)r * WL.block); };
     auto next_live = [&]() -> int {
       for (;;) {
         const int k = wave_grab(&item_ctr);
@@ -1246,125 +1500,113 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const gri
         const int j = (int)blockIdx.x + k * (int)gridDim.x;
         const int r = j / nsub;
         const uint32_t rg = range_s[j - r * nsub];
-        if (rows_s[r].valid == kRowValid && any_in_range(rows_s[r].alive, rg & 0xFFu, rg >> 8)) return k;
+        const RowHeader& h = row_hdr(r);
+        if (h.valid == kRowValid && any_in_range(h.alive, rg & 0xFFu, rg >> 8)) return k;
       }
     };
-    // scan summary word of (row's DFA state, spelling); without the table
-    // every lane scans its bytes
+    // spelling of this lane in item k (row r), and its scan summary word;
+    // without the table every lane walks its bytes
+    auto spelling = [&](int k, int& r) -> int {
+      const int j = (int)blockIdx.x + (k < mine ? k : 0) * (int)gridDim.x;
+      r = j / nsub;
+      return (j - r * nsub) * kSub + lane;
+    };
     auto summary = [&](int k, int r, int u) -> uint32_t {
       if (!tb.scan) return 2u << 26;
-      const uint32_t q = k < mine ? rows_s[r].q : 0u;
-      return tb.scan[(size_t)q * tb.U + (u < tb.U ? u : 0)];
+      const uint32_t q = k < mine ? row_hdr(r).q : 0u;
+      return tb.scan[(size_t)(q < (uint32_t)tb.S ? q : 0u) * tb.U + (u < tb.U ? u : 0)];
     };
-    int k0 = next_live();
-    int r0;
-    int u = spelling(k0, r0);
-    uint4 rk = recs[u < tb.U ? u : 0];
-    uint4 tl = tails[u < tb.U ? u : 0];
-    uint32_t sc = summary(k0, r0, u);
+    int k0 = next_live(), r0;
+    int u0 = spelling(k0, r0);
+    uint32_t sc0 = summary(k0, r0, u0);
+    int k1 = next_live(), r1;
+    int u1 = spelling(k1, r1);
+    uint32_t sc1 = summary(k1, r1, u1);
     while (k0 < mine) {
-      const int k1 = next_live();
-      int r1;
-      const int u1 = spelling(k1, r1);
-      const uint4 rk1 = recs[u1 < tb.U ? u1 : 0];
-      const uint4 tl1 = tails[u1 < tb.U ? u1 : 0];
-      const uint32_t sc1 = summary(k1, r1, u1);
+      const int k2 = next_live();
+      int r2;
+      const int u2 = spelling(k2, r2);
+      const uint32_t sc2 = summary(k2, r2, u2);
 
-      const RowLds& rl = rows_s[r0];
-      const uint32_t n = u < tb.U ? (rk.w & 0xFFu) : 0u;
-      const uint64_t h = (uint64_t)rk.x | (uint64_t)rk.y << 32;
-      const uint32_t b0 = (uint32_t)(h & 0xFF);
-      const uint32_t e = fb_all[r0 * 256 + b0];
-      const uint32_t kind = (e >> 16) & 3u;
-      if (n != 0 && kind != kFbDead) {
-        uint8_t* rw = rows + (size_t)(g0 + r0) * rbytes;
-        RowCtx<true> rc;
-        rc.tb = &tb;
-        rc.pt = pt;
-        rc.bs = BaseStack<true>{pool + rl.stk_off, in_mem<true>((const uint16_t*)(win_all + r0 * kWalkWin)),
-                                rl.stk_depth, rl.stk_depth > (uint32_t)kWalkWin ? rl.stk_depth - kWalkWin : 0u};
-        rc.sl = rl.sl;
-        rc.tv = TermView{tinfo_s, I_s, rl.R, live_s, MW};
-        rc.acc_off = (const uint32_t*)(lds + WL.acc_off);
-        rc.acc_list = lds + WL.acc_list;
-        rc.a2 = (const uint32_t*)(rw + RL.a2);
-        rc.a2_stride = 8;
-        rc.post = (const Post*)(rw + RL.post);
-        rc.clsA = cls_all + r0 * WL.cls_row;
-        rc.clsW = rc.clsA + WL.cls_row / 2;
-        rc.winner = rl.winner;
-        Lane<MW> ln;
-        ln.mode = (int)kind - 1;
-        ln.t1 = (int)(e >> 24);
-        ln.k = 0;
-        ln.m = 0;
-#pragma unroll
-        for (int w = 0; w < MW; ++w) ln.acur[w] = kind == kFbMode0 ? rl.A[w] : rl.Aw[w];
-        SpellBytes byte_at;
-        byte_at.win = h >> 8;
-        byte_at.lo0 = (uint64_t)tl.x | (uint64_t)tl.y << 32;
-        byte_at.hi = (uint64_t)tl.z | (uint64_t)tl.w << 32;
-        byte_at.ovf = tails + (rk.w >> 8);
-        // the lexeme after byte 0: a new one, or the pending lexeme plus the
-        // byte; the lexicon follows it only if a restricted terminal is viable
-        const int q1 = (int)(e & 0xFFFF);
-        const uint8_t* ct = kind == kFbMode0 ? rc.clsA : rc.clsW;
-        LexState lx;
-        lx.need = rl.sl.restricted != 0 && (ct[q1] & 2u) ? 1u : 0u;
-        if ((e >> 18) & 1u) {
-          lx.w = b0;
-          lx.len = 1;
-          lx.node = kNoLex;
-        } else {
-          lx.len = rl.rem_len + 1;
-          lx.w = lx.len <= 8 ? (((uint64_t)rl.rem_lo | (uint64_t)rl.rem_hi << 32) | (uint64_t)b0 << (8 * rl.rem_len))
-                             : 0ull;
-          lx.node = lx.need && lx.len > 8 ? lex_child(tb, rl.sl, rl.lexnode, b0) : kNoLex;
-        }
-        // the scan summary settles lanes whose spelling ends at most one
-        // lexeme; the others scan from the first lexeme end on
-        int ok = 0;
-        bool scan = false;
-        if (!(sc & kScanReject)) {
-          if (scan_ends(sc) < 2) ok = summary_verdict<true, MW>(rc, ln, sc, lx, n, byte_at, lane_area, kFastLane);
-          else scan = true;
-        }
-        if (scan) {
-          int qs = q1;
-          uint32_t is = 1;
-          const uint32_t p = scan_p_first(sc);
-          if (p > 0) {  // bytes 1 .. p-1 only extend the pending lexeme
-            for (uint32_t i = 1; i < p; ++i) {
-              const uint32_t b = byte_at(i);
-              if (lx.need) lex_push(tb, rl.sl, lx, b);
-            }
-            qs = (int)scan_q_first(sc);
-            is = p;
-          }
-          ok = walk_bytes<true, MW>(rc, ln, qs, lx, is, n, byte_at, step, lane_area, kFastLane);
-        }
-        if (ok < 0) {  // the lane's stack area is too small: hand over
-          RowHeader* hdr = (RowHeader*)rw;
-          const uint32_t slot = atomicAdd(&hdr->slow_count, 1u);
-          if (slot < (uint32_t)kSlowCap) ((uint32_t*)(rw + RL.slow))[slot] = (uint32_t)u;
-          else atomicOr(&hdr->wstat, GRID_ROW_OVERFLOW);
-        }
-        // the sub-tile's word of the sorted-spelling mask: one wave owns it
-        const uint64_t allowed = __ballot(ok > 0);
-        if (allowed && lane == __ffsll((unsigned long long)__ballot(1)) - 1) {
-          ((uint64_t*)(rw + RL.smask))[u / kSub] = allowed;
-          ((RowHeader*)rw)->nonempty = 1u;
-        }
+      const RowHeader& h = row_hdr(r0);
+      const uint8_t* clsA = rows_s + (size_t)r0 * WL.block + sizeof(RowHeader);
+      const uint8_t* clsW = clsA + clsW_off;
+      uint8_t* rw = rows + (size_t)(g0 + r0) * rbytes;
+      const TermView tv{tinfo_s, I_s, h.R, live_s, MW};
+      int ok = 0;
+      if (u0 < tb.U)
+        ok = fast_verdict<MW>(h, clsA, clsW, I_s, acc_off_s, acc_list_s, tv, (const uint32_t*)(rw + RL.a2), sc0);
+      const uint64_t und = __ballot(ok == 2);
+      if (lane == 0) umask_s[k0] = und;
+      // the sub-tile's word of the sorted-spelling mask (its undecided lanes
+      // add their bits later, so both use atomic ORs)
+      const uint64_t allowed = __ballot(ok == 1);
+      if (allowed && lane == __ffsll((unsigned long long)__ballot(1)) - 1) {
+        atomicOr((unsigned long long*)(rw + RL.smask) + u0 / kSub, (unsigned long long)allowed);
+        ((RowHeader*)rw)->nonempty = 1u;
       }
       k0 = k1;
       r0 = r1;
-      u = u1;
-      rk = rk1;
-      tl = tl1;
-      sc = sc1;
+      u0 = u1;
+      sc0 = sc1;
+      k1 = k2;
+      r1 = r2;
+      u1 = u2;
+      sc1 = sc2;
+    }
+    __syncthreads();
+    // undecided lanes: prefix counts over the items (one wave), then waves
+    // take 64 of them at a time
+    if (tid < 64) {
+      const int per = (mine + 63) / 64;
+      uint32_t sum = 0;
+      for (int i = 0; i < per; ++i) {
+        const int k = lane * per + i;
+        if (k < mine) sum += (uint32_t)__popcll(umask_s[k]);
+      }
+      uint32_t incl = sum;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t t = __shfl_up(incl, d);
+        if (lane >= d) incl += t;
+      }
+      uint32_t run = incl - sum;
+      for (int i = 0; i < per; ++i) {
+        const int k = lane * per + i;
+        if (k < mine) {
+          upre_s[k] = run;
+          run += (uint32_t)__popcll(umask_s[k]);
+        }
+      }
+      if (lane == 63) upre_s[mine] = incl;
+    }
+    __syncthreads();
+    const int n_und = (int)upre_s[mine];
+    for (;;) {
+      const int c = wave_grab(&chunk_ctr);
+      if (c * 64 >= n_und) break;
+      const int pos = c * 64 + lane;
+      if (pos < n_und) {
+        // the item holding position pos: last k with upre_s[k] <= pos
+        int lo = 0, hi = mine - 1;
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if ((int)upre_s[mid] <= pos) lo = mid;
+          else hi = mid - 1;
+        }
+        const int bit = nth_set_bit(umask_s[lo], pos - (int)upre_s[lo]);
+        const int j = (int)blockIdx.x + lo * (int)gridDim.x;
+        const int r = j / nsub;
+        const int u = (j - r * nsub) * kSub + bit;
+        const uint8_t* rowblk = rows_s + (size_t)r * WL.block;
+        uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
+        if (undecided_lane<MW>(sh, *(const RowHeader*)rowblk, rowblk, rw, RL, u, summary(lo, r, u), lane_area) > 0) {
+          atomicOr((unsigned long long*)(rw + RL.smask) + u / kSub, 1ull << (u & (kSub - 1)));
+          ((RowHeader*)rw)->nonempty = 1u;
+        }
+      }
     }
   }
-
 }
 
 // ---------------------------------------------------------------- finalize
@@ -1386,7 +1628,7 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
   const int lane = tid & 63;
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
-  const RowLayout RL = row_layout(tb.T, tb.U);
+  const RowLayout RL = row_layout(tb.T, tb.U, tb.S);
   const bool valid = hdr->valid == kRowValid;
   const uint32_t count = valid ? min(hdr->slow_count, (uint32_t)kSlowCap) : 0u;
   if (count > 0 && blockIdx.y != 0) return;  // uniform
@@ -1580,13 +1822,16 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
     hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool, eos, ws,
                        rb);
   if ((phases & GRID_PHASE_WALK) && tb.U > 0) {
-    const WalkLds WL = walk_lds(tb, MW, B);
-    const int n_items = ((tb.U + kSub - 1) / kSub) * std::min(B, WL.group);
-    const int resident = walk_grid_size<MW>(WL.total);
+    const WalkLds W0 = walk_lds(tb, MW, B, 1 << 20);
+    const int nsub = (tb.U + kSub - 1) / kSub;
+    const int resident = walk_grid_size<MW>(W0.total);
     if (resident <= 0) return fail(GRID_E_HIP, "grid_mask: cannot raise the walk's LDS limit");
+    const int n_items = nsub * std::min(B, W0.group);
     const int blocks = std::min((n_items + kWalkThreads / 64 - 1) / (kWalkThreads / 64), resident);
-    hipLaunchKernelGGL(walk_kernel<MW>, dim3(blocks), dim3(kWalkThreads), WL.total, s, tb, cfg_dev, pool, ws, rb,
-                       B);
+    const WalkLds WL = walk_lds(tb, MW, B, blocks);
+    if ((long long)nsub > (long long)kMaxItems * blocks)
+      return fail(GRID_E_CAPACITY, "grid_mask: vocabulary too large for the walk's item bookkeeping");
+    hipLaunchKernelGGL(walk_kernel<MW>, dim3(blocks), dim3(kWalkThreads), WL.total, s, tb, pool, ws, rb, B);
   }
   if (phases & GRID_PHASE_FINALIZE)
     hipLaunchKernelGGL(finalize_kernel<MW>, dim3(B, kGatherGroups), dim3(kBlock), 0, s, tb, cfg_dev, pool, mask,
@@ -1602,7 +1847,7 @@ static int n_spellings(const grid_compiled* g) { return (int)g->vocab.spell_off.
 
 // head, then B rows
 static size_t workspace_size(const grid_compiled* g, int B) {
-  return kWsHead + row_layout(g->parser.T, n_spellings(g)).total * (size_t)B;
+  return kWsHead + row_layout(g->parser.T, n_spellings(g), g->dfa.S).total * (size_t)B;
 }
 
 extern "C" size_t grid_mask_workspace_bytes(const grid_compiled* g, int32_t B) {
@@ -1618,7 +1863,7 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   if (phases & ~GRID_PHASE_ALL) return fail(GRID_E_ARG, "grid_mask: unknown phase bits");
   if (!g || B <= 0 || B > 65535 || !cfg_dev || !stack_pool_dev || !mask_dev || !workspace_dev)
     return fail(GRID_E_ARG, "grid_mask: null pointer or batch size out of range");
-  const size_t rb = row_layout(g->parser.T, n_spellings(g)).total;
+  const size_t rb = row_layout(g->parser.T, n_spellings(g), g->dfa.S).total;
   if (workspace_bytes < workspace_size(g, B)) return fail(GRID_E_ARG, "grid_mask: workspace too small");
   if (((uintptr_t)workspace_dev & 255) != 0) return fail(GRID_E_ARG, "grid_mask: workspace not 256-byte aligned");
   static const int needed[] = {GRID_ART_DFA_CLASS,   GRID_ART_BYTE_CLASS,  GRID_ART_DFA_ACCEPT_OFF,
@@ -1672,7 +1917,7 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   tb.n_acc = (int)g->dfa.accept_list.size();
   tb.hbits = g->parser.goto_hbits;
   const int mw = tb.tw;
-  const WalkLds WL = walk_lds(tb, mw, B);
+  const WalkLds WL = walk_lds(tb, mw, B, 1 << 20);
   if (tb.T > 255 || (mw != 2 && mw != 4 && mw != 8) || WL.total + 64 > kWalkLdsMax ||
       parse_lds(tb, 0).total > 24 * 1024)
     return fail(GRID_E_CAPACITY, "grid_mask: lexer DFA or LR tables too large for the LDS staging");
