@@ -7,8 +7,10 @@ of bf16 logits [32, V].  Steps cycle through distinct, device-resident config
 batches; the mask cache is not used (every step is a cold walk).
 
 Prints one JSON line (rank 0): masks/s, p50/p99 microseconds per mask, the
-walk kernel's roofline numbers (HIP events on the launch stream) and the CPU
-oracle's throughput on a bounded sample of the same workload.
+walk kernel's roofline numbers (HIP events on the launch stream), the CPU
+oracle's throughput on a bounded sample of the same workload, and, beside the
+cold figure, the mask cache's miss-and-insert and hit throughputs on the same
+batches (grid_mask_cached).
 """
 
 import argparse
@@ -134,13 +136,42 @@ def main():
     tail_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
     per_mask_us = step_ms * 1000.0 / B
 
-    # algorithmic bytes of one walk launch: each row reads every distinct
-    # spelling's bytes and its 4-byte offset and writes its W mask words
-    spell_bytes = len(grid.artifact("SPELL_BYTES")) - 32
+    # algorithmic bytes of one walk launch: each row streams the scan-summary
+    # word of every distinct spelling for its DFA state and writes its W mask
+    # words (the spelling bytes read by undecided lanes are not counted)
     n_spell = info["n_spellings"]
-    bytes_per_mask = spell_bytes + 4 * (n_spell + 1) + 4 * grid.W
+    bytes_per_mask = 4 * n_spell + 4 * grid.W
     walk_s = float(walk_ms.mean()) / 1000.0
     achieved = B * bytes_per_mask / walk_s / 1e9
+
+    # mask cache beside the cold figure: every row missing and inserting (the
+    # cache cleared before each step), then every row hitting
+    n_entries = 1
+    while n_entries < 2 * B * len(batches):
+        n_entries *= 2
+    cache = grid.new_cache(n_entries, dev)
+    cache_steps = max(10, args.steps // 4)
+
+    def cached_step(i, clear):
+        c, p = batches[i % len(batches)]
+        if clear:
+            grid.clear_cache(cache, stream)
+        grid.mask(c, p, B, mask, eos, status, ws, stream, cache=cache)
+        G.apply(mask, logits, stream)
+
+    cache_out = {"entries": n_entries}
+    for label, clear in (("miss_insert", True), ("hit", False)):
+        for i in range(len(batches)):
+            cached_step(i, clear)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(cache_steps):
+            cached_step(i, clear)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        cache_out[f"{label}_masks_per_s"] = B * cache_steps / (e0.elapsed_time(e1) / 1000.0)
+    assert (status.cpu() == 0).all()
 
     if args.copy_calib:
         a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -195,6 +226,7 @@ def main():
                      "traffic": walk_traffic_bytes(), "bytes_per_mask": bytes_per_mask,
                      "walk_us_per_launch": walk_s * 1e6},
         "cpu_baseline": cpu,
+        "cache": cache_out,
     }
     print(json.dumps(out), flush=True)
 

@@ -256,6 +256,36 @@ int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_config* cfg_d
                      int32_t* status_dev, void* workspace_dev, size_t workspace_bytes,
                      uint32_t phases, void* stream);
 
+/* --------------------------------------------------------------- mask cache */
+/* A configuration-keyed mask cache (section 4.3, configuration-keyed
+ * caching; the per-token hot path's cache probe and write-back, section 6.1)
+ * in caller-owned device memory: an open-addressing table whose entry holds
+ * one whole mask row (with its EOS byte and row status), keyed by everything
+ * the row's mask depends on -- the DFA state q, the pending lexeme (length,
+ * first 8 bytes, lexicon node, empty flag), the lexicon slot (one key per
+ * schema, so an identifier position never reads another schema's entry:
+ * Proposition 6) and a 128-bit content hash of the whole LR stack -- plus a
+ * fingerprint of the compiled handle.  A hit reproduces the cold row bit for
+ * bit (cache-on equals cache-off) unless two stacks collide in the 128-bit
+ * hash.  Entries are written once and never evicted; a row whose probe
+ * window (8 slots) is full stays uncached.  Calls sharing a cache may run
+ * concurrently: a slot is claimed by an atomic compare-and-swap, written,
+ * then published, and only published entries are read. */
+#define GRID_CACHE_LOOKUP 1u   /* rows whose key is published copy the cached row */
+#define GRID_CACHE_INSERT 2u   /* rows that miss claim a slot and publish their row */
+/* Device bytes of a cache of n_entries entries (a power of two >= 1); 0 if
+ * n_entries is not one. */
+size_t grid_cache_bytes(const grid_compiled* g, int32_t n_entries);
+/* Empties a cache of cache_bytes (from grid_cache_bytes) with a fill kernel,
+ * asynchronous on stream. */
+int grid_cache_clear(const grid_compiled* g, void* cache_dev, size_t cache_bytes, void* stream);
+/* grid_mask with a cache (cache_flags: GRID_CACHE_*; a null cache or flags 0
+ * is exactly grid_mask).  Hit rows skip the walk. */
+int grid_mask_cached(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                     const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
+                     int32_t* status_dev, void* workspace_dev, size_t workspace_bytes, void* cache_dev,
+                     size_t cache_bytes, uint32_t cache_flags, void* stream);
+
 /* -------------------------------------------------------------------- apply */
 #define GRID_DTYPE_F32 0
 #define GRID_DTYPE_BF16 1

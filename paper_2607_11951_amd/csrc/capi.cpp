@@ -66,6 +66,20 @@ extern "C" int grid_compile(const grid_compile_args* a, grid_compiled** out) {
                            a->n_special, a->eos_id);
     g->scan = build_scan_summary(g->dfa, g->vocab);
     add_lexicon(g->lex, g->dfa, g->gram, g->term_cat, {});  // slot 0: no restrictions
+    // FNV-1a over the tables a cached mask row depends on
+    uint32_t fp = 2166136261u;
+    auto mix = [&fp](const void* p, size_t n) {
+      const uint8_t* b = (const uint8_t*)p;
+      for (size_t i = 0; i < n; ++i) fp = (fp ^ b[i]) * 16777619u;
+    };
+    const int32_t dims[] = {g->dfa.S, g->dfa.C, g->parser.T, g->parser.N, g->parser.n_states, g->vocab.V,
+                            (int32_t)g->vocab.spell_off.size()};
+    mix(dims, sizeof(dims));
+    mix(g->dfa.next.data(), g->dfa.next.size() * 2);
+    mix(g->parser.action.data(), g->parser.action.size() * 2);
+    mix(g->vocab.spell_bytes.data(), g->vocab.spell_bytes.size());
+    mix(g->vocab.alias_ids.data(), g->vocab.alias_ids.size() * 4);
+    g->fingerprint = fp;
     *out = g.release();
     return GRID_OK;
   } catch (const Error& e) {

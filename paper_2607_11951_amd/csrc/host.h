@@ -144,6 +144,7 @@ struct grid_compiled {
   grid::VocabArtifacts vocab;
   grid::LexiconStore lex;
   std::vector<uint32_t> scan;         // scan summary [S][U]
+  uint32_t fingerprint = 0;           // of the lexer, parser and vocabulary (mask-cache entries)
   std::vector<int> term_cat;          // category index per terminal or -1
   std::vector<uint32_t> term_info;    // device word per terminal
   std::vector<int> cat_term;          // terminal id per category index

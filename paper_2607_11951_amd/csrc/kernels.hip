@@ -104,7 +104,36 @@ struct Tables {
   const uint32_t* scan;       // scan summary [S][U], or null (scan every byte)
   int S, C, T, N, NS, P, U, V, W, n_slots, eos_id;
   int tw, n_pstate, n_predx, n_acc, hbits;
+  uint8_t* cache;             // mask cache (null: off)
+  uint32_t cache_mask;        // entries - 1
+  uint32_t cache_flags;       // GRID_CACHE_*
+  uint32_t cache_stride;      // bytes per entry
+  uint32_t fp;                // fingerprint of the compiled handle
 };
+
+// ------------------------------------------------------------- mask cache
+// Entry: a 64-byte key/state header, then the row's W mask words.  state 0
+// empty, 1 claimed (being written), 2 published.
+struct CacheEntry {
+  uint32_t state, fp, q, slot, flags, rem_len, rem_lo, rem_hi, lexnode, depth;
+  uint32_t h[4];  // 128-bit content hash of the stack
+  uint32_t eos, status;
+};
+static_assert(sizeof(CacheEntry) == 64, "cache entry header is 64 bytes");
+constexpr int kCacheProbes = 8;
+constexpr uint32_t kRowCached = 0xCAC4;  // RowHeader::valid of a row served from the cache
+
+__host__ __device__ inline uint32_t cache_stride_of(int W) { return 64u + ((uint32_t)W * 4u + 15u) / 16u * 16u; }
+
+// One stack entry's share of the stack hash: a 64-bit mix of (position,
+// state) under a salt; the hash is the sum over the stack, so every thread
+// adds its positions in any order.
+__device__ inline uint64_t stack_mix(uint32_t i, uint32_t s, uint64_t salt) {
+  uint64_t z = ((uint64_t)i << 32 | s) + salt;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
 
 // ---------------------------------------------------------------- workspace
 // Row header, written by the prologue: everything the walk needs of a row
@@ -126,7 +155,9 @@ struct RowHeader {
   int32_t pstat;              // status bits from the prologue
   int32_t wstat;              // status bits from the walk
   uint32_t nonempty;          // the walk allowed some token
-  uint32_t pad[9];
+  int32_t cache_slot;         // mask-cache entry this row publishes to, -1 none
+  int32_t fstat;              // final row status (finalize)
+  uint32_t pad[7];
 };
 static_assert(sizeof(RowHeader) == 256, "row header is 256 bytes");
 
@@ -723,6 +754,7 @@ __device__ inline int winner_of(const TermView& tv, const uint32_t* acc_off, con
 template <int MW>
 __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_config* __restrict__ cfgs,
                                                           const uint16_t* __restrict__ pool,
+                                                          uint32_t* __restrict__ mask,
                                                           uint8_t* __restrict__ eos_out,
                                                           uint8_t* __restrict__ ws, size_t rbytes) {
   extern __shared__ __align__(16) uint8_t plds[];
@@ -732,7 +764,8 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   __shared__ uint32_t A[8], I[8], R[8], Aw[8], alive[8];
   __shared__ Post posts[256];
   __shared__ uint16_t scratch[kBlock][kPostCap + kTmpCap];
-  __shared__ int bad, overflow, winner, eos_ok;
+  __shared__ int bad, overflow, winner, eos_ok, cache_hit;
+  __shared__ unsigned long long hacc[2];
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
   const RowLayout L = row_layout(tb.T, tb.U, tb.S);
@@ -758,6 +791,9 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     overflow = 0;
     winner = -1;
     eos_ok = 0;
+    cache_hit = -1;
+    hacc[0] = 0;
+    hacc[1] = 0;
   }
   {
     uint64_t* sm = (uint64_t*)(rw + L.smask);
@@ -767,10 +803,19 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   const uint32_t depth = cfg.stk_depth;
   const uint32_t lo = depth > (uint32_t)kStackWin ? depth - kStackWin : 0;
   if (!bad) {
+    uint64_t h1 = 0, h2 = 0;
     for (uint32_t i = tid; i < depth; i += kBlock) {
       const uint16_t s = pool[cfg.stk_off + i];
       if (s >= tb.NS) bad = 1;
       if (i >= lo) win[i - lo] = s;
+      if (tb.cache) {
+        h1 += stack_mix(i, s, 0x9E3779B97F4A7C15ull);
+        h2 += stack_mix(i, s, 0xD1B54A32D192ED03ull);
+      }
+    }
+    if (tb.cache) {
+      atomicAdd(&hacc[0], (unsigned long long)h1);
+      atomicAdd(&hacc[1], (unsigned long long)h2);
     }
   }
   __syncthreads();
@@ -782,7 +827,79 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
       hdr->slow_count = 0;
       hdr->wstat = 0;
       hdr->nonempty = 0;
+      hdr->cache_slot = -1;
       if (eos_out) eos_out[row] = 0;
+    }
+    return;
+  }
+  // mask cache: probe the row's key; a published entry is the row's mask, an
+  // empty slot on the way is claimed for the row when inserting
+  if (tb.cache && tid == 0) {
+    const uint64_t h1 = hacc[0], h2 = hacc[1];
+    const uint32_t key[13] = {tb.fp,
+                              cfg.q,
+                              cfg.slot,
+                              cfg.flags & 1u,
+                              cfg.rem_len,
+                              (uint32_t)cfg.rem_head[0] | (uint32_t)cfg.rem_head[1] << 8 |
+                                  (uint32_t)cfg.rem_head[2] << 16 | (uint32_t)cfg.rem_head[3] << 24,
+                              (uint32_t)cfg.rem_head[4] | (uint32_t)cfg.rem_head[5] << 8 |
+                                  (uint32_t)cfg.rem_head[6] << 16 | (uint32_t)cfg.rem_head[7] << 24,
+                              cfg.lexnode,
+                              depth,
+                              (uint32_t)h1,
+                              (uint32_t)(h1 >> 32),
+                              (uint32_t)h2,
+                              (uint32_t)(h2 >> 32)};
+    // home slot: every key word mixed in (rows on one stack but another
+    // schema or scan state start elsewhere)
+    uint64_t home = h1;
+    for (int k = 0; k < 9; ++k) home = stack_mix((uint32_t)k, key[k], home);
+    int hit = -1, claim = -1;
+    for (int pr = 0; pr < kCacheProbes; ++pr) {
+      const uint32_t idx = (uint32_t)(home + (uint64_t)pr) & tb.cache_mask;
+      CacheEntry* e = (CacheEntry*)(tb.cache + (size_t)idx * tb.cache_stride);
+      const uint32_t st = __hip_atomic_load(&e->state, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+      if (st == 2u) {
+        const uint32_t* ek = &e->fp;
+        bool same = true;
+        for (int k = 0; k < 13; ++k) same = same && ek[k] == key[k];
+        if (same && (tb.cache_flags & GRID_CACHE_LOOKUP)) {
+          hit = (int)idx;
+          break;
+        }
+        continue;
+      }
+      if (st == 0u) {
+        if (!(tb.cache_flags & GRID_CACHE_INSERT)) break;
+        if (atomicCAS(&e->state, 0u, 1u) == 0u) {
+          uint32_t* ek = &e->fp;
+          for (int k = 0; k < 13; ++k) ek[k] = key[k];
+          claim = (int)idx;
+          break;
+        }
+      }
+    }
+    cache_hit = hit;
+    hdr->cache_slot = claim;
+  } else if (tid == 0) {
+    hdr->cache_slot = -1;
+  }
+  __syncthreads();
+  if (cache_hit >= 0) {  // the cached row: mask, EOS byte, status
+    const CacheEntry* e = (const CacheEntry*)(tb.cache + (size_t)cache_hit * tb.cache_stride);
+    const uint32_t* src = (const uint32_t*)(e + 1);
+    uint32_t* dst = mask + (size_t)row * tb.W;
+    for (int i = tid; i < tb.W; i += kBlock) dst[i] = src[i];
+    if (tid == 0) {
+      hdr->valid = kRowCached;
+      hdr->pstat = (int32_t)e->status;
+      hdr->eos_ok = e->eos;
+      hdr->slow_count = 0;
+      hdr->wstat = 0;
+      hdr->nonempty = 1;
+      hdr->cache_slot = -1;
+      if (eos_out) eos_out[row] = (uint8_t)e->eos;
     }
     return;
   }
@@ -1629,6 +1746,10 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
   const RowLayout RL = row_layout(tb.T, tb.U, tb.S);
+  if (hdr->valid == kRowCached) {  // served from the mask cache by the prologue
+    if (blockIdx.y == 0 && threadIdx.x == 0 && status) status[row] = hdr->pstat;
+    return;
+  }
   const bool valid = hdr->valid == kRowValid;
   const uint32_t count = valid ? min(hdr->slow_count, (uint32_t)kSlowCap) : 0u;
   if (count > 0 && blockIdx.y != 0) return;  // uniform
@@ -1738,12 +1859,42 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
       st = hdr->pstat | GRID_ROW_BAD_CONFIG;
     }
     if (status) status[row] = st;
+    hdr->fstat = st;
+  }
+}
+
+// Mask cache write-back: each row that claimed an entry in the prologue
+// copies its finished mask row, EOS flag and status into it, then publishes
+// it (a device-scope fence orders the copy before the state word).
+__global__ __launch_bounds__(kBlock) void cache_publish_kernel(Tables tb, const uint32_t* __restrict__ mask,
+                                                               const uint8_t* __restrict__ ws, size_t rbytes) {
+  const int row = blockIdx.x;
+  const RowHeader* hdr = (const RowHeader*)(ws + kWsHead + (size_t)row * rbytes);
+  if (hdr->valid != kRowValid || hdr->cache_slot < 0) return;  // uniform
+  CacheEntry* e = (CacheEntry*)(tb.cache + (size_t)hdr->cache_slot * tb.cache_stride);
+  uint32_t* dst = (uint32_t*)(e + 1);
+  const uint32_t* src = mask + (size_t)row * tb.W;
+  for (int i = threadIdx.x; i < tb.W; i += kBlock) dst[i] = src[i];
+  if (threadIdx.x == 0) {
+    e->eos = hdr->eos_ok;
+    e->status = (uint32_t)hdr->fstat;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    __hip_atomic_store(&e->state, 2u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
 // ------------------------------------------------------------------- apply
 // Each thread covers 8 consecutive logits of one row; the mask byte for them
 // comes from one word.  Fully masked groups take one or two 16-byte stores.
+// Empties a mask cache: every entry's state word to 0.
+__global__ __launch_bounds__(kBlock) void cache_clear_kernel(uint8_t* cache, uint32_t n, uint32_t stride) {
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock)
+    ((CacheEntry*)(cache + (size_t)i * stride))->state = 0u;
+}
+
 template <typename T>
 __global__ __launch_bounds__(kBlock) void apply_kernel(const uint32_t* __restrict__ mask, T* logits, int B,
                                                        int V, int W, int64_t stride, uint32_t neg_inf_bits,
@@ -1819,7 +1970,7 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
   if (!raise_lds((const void*)prologue_kernel<MW>, parse_bytes))
     return fail(GRID_E_HIP, "grid_mask: cannot raise the LDS limit");
   if (phases & GRID_PHASE_PROLOGUE)
-    hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool, eos, ws,
+    hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool, mask, eos, ws,
                        rb);
   if ((phases & GRID_PHASE_WALK) && tb.U > 0) {
     const WalkLds W0 = walk_lds(tb, MW, B, 1 << 20);
@@ -1833,9 +1984,12 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
       return fail(GRID_E_CAPACITY, "grid_mask: vocabulary too large for the walk's item bookkeeping");
     hipLaunchKernelGGL(walk_kernel<MW>, dim3(blocks), dim3(kWalkThreads), WL.total, s, tb, pool, ws, rb, B);
   }
-  if (phases & GRID_PHASE_FINALIZE)
+  if (phases & GRID_PHASE_FINALIZE) {
     hipLaunchKernelGGL(finalize_kernel<MW>, dim3(B, kGatherGroups), dim3(kBlock), 0, s, tb, cfg_dev, pool, mask,
                        ws, rb, status);
+    if (tb.cache && (tb.cache_flags & GRID_CACHE_INSERT))
+      hipLaunchKernelGGL(cache_publish_kernel, dim3(B), dim3(kBlock), 0, s, tb, mask, ws, rb);
+  }
   return GRID_OK;
 }
 
@@ -1855,12 +2009,13 @@ extern "C" size_t grid_mask_workspace_bytes(const grid_compiled* g, int32_t B) {
   return workspace_size(g, B);
 }
 
-extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
-                                const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
-                                int32_t* status_dev, void* workspace_dev, size_t workspace_bytes,
-                                uint32_t phases, void* stream) {
+static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_dev, const uint16_t* stack_pool_dev,
+                     uint32_t* mask_dev, uint8_t* eos_dev, int32_t* status_dev, void* workspace_dev,
+                     size_t workspace_bytes, void* cache_dev, size_t cache_bytes, uint32_t cache_flags,
+                     uint32_t phases, void* stream) {
   clear_error();
   if (phases & ~GRID_PHASE_ALL) return fail(GRID_E_ARG, "grid_mask: unknown phase bits");
+  if (cache_flags & ~(GRID_CACHE_LOOKUP | GRID_CACHE_INSERT)) return fail(GRID_E_ARG, "grid_mask: unknown cache flags");
   if (!g || B <= 0 || B > 65535 || !cfg_dev || !stack_pool_dev || !mask_dev || !workspace_dev)
     return fail(GRID_E_ARG, "grid_mask: null pointer or batch size out of range");
   const size_t rb = row_layout(g->parser.T, n_spellings(g), g->dfa.S).total;
@@ -1916,6 +2071,20 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   tb.n_predx = (int)g->parser.predx.size();
   tb.n_acc = (int)g->dfa.accept_list.size();
   tb.hbits = g->parser.goto_hbits;
+  tb.cache = nullptr;
+  tb.cache_mask = 0;
+  tb.cache_flags = 0;
+  tb.cache_stride = cache_stride_of(tb.W);
+  tb.fp = g->fingerprint;
+  if (cache_dev && cache_flags) {
+    const size_t n = cache_bytes / tb.cache_stride;
+    if (n == 0 || (n & (n - 1)) != 0 || n > 0x80000000ull || n * tb.cache_stride != cache_bytes)
+      return fail(GRID_E_ARG, "grid_mask: cache size is not grid_cache_bytes of a power of two");
+    if (((uintptr_t)cache_dev & 15) != 0) return fail(GRID_E_ARG, "grid_mask: cache not 16-byte aligned");
+    tb.cache = (uint8_t*)cache_dev;
+    tb.cache_mask = (uint32_t)(n - 1);
+    tb.cache_flags = cache_flags;
+  }
   const int mw = tb.tw;
   const WalkLds WL = walk_lds(tb, mw, B, 1 << 20);
   if (tb.T > 255 || (mw != 2 && mw != 4 && mw != 8) || WL.total + 64 > kWalkLdsMax ||
@@ -1936,11 +2105,47 @@ extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_co
   return GRID_OK;
 }
 
+extern "C" int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                                const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
+                                int32_t* status_dev, void* workspace_dev, size_t workspace_bytes,
+                                uint32_t phases, void* stream) {
+  return mask_call(g, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, workspace_dev, workspace_bytes,
+                   nullptr, 0, 0, phases, stream);
+}
+
 extern "C" int grid_mask(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
                          const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
                          int32_t* status_dev, void* workspace_dev, size_t workspace_bytes, void* stream) {
-  return grid_mask_phases(g, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, workspace_dev,
-                          workspace_bytes, GRID_PHASE_ALL, stream);
+  return mask_call(g, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, workspace_dev, workspace_bytes,
+                   nullptr, 0, 0, GRID_PHASE_ALL, stream);
+}
+
+extern "C" int grid_mask_cached(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                                const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
+                                int32_t* status_dev, void* workspace_dev, size_t workspace_bytes, void* cache_dev,
+                                size_t cache_bytes, uint32_t cache_flags, void* stream) {
+  return mask_call(g, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, workspace_dev, workspace_bytes,
+                   cache_dev, cache_bytes, cache_flags, GRID_PHASE_ALL, stream);
+}
+
+extern "C" size_t grid_cache_bytes(const grid_compiled* g, int32_t n_entries) {
+  if (!g || n_entries < 1 || (n_entries & (n_entries - 1)) != 0) return 0;
+  return (size_t)n_entries * cache_stride_of((g->vocab.V + 31) / 32);
+}
+
+extern "C" int grid_cache_clear(const grid_compiled* g, void* cache_dev, size_t cache_bytes, void* stream) {
+  clear_error();
+  if (!g || !cache_dev) return fail(GRID_E_ARG, "grid_cache_clear: null argument");
+  const uint32_t stride = cache_stride_of((g->vocab.V + 31) / 32);
+  const size_t n = cache_bytes / stride;
+  if (n == 0 || (n & (n - 1)) != 0 || n > 0x80000000ull || n * stride != cache_bytes)
+    return fail(GRID_E_ARG, "grid_cache_clear: cache size is not grid_cache_bytes of a power of two");
+  const int blocks = (int)std::min<size_t>((n + kBlock - 1) / kBlock, 1024);
+  hipLaunchKernelGGL(cache_clear_kernel, dim3(blocks), dim3(kBlock), 0, (hipStream_t)stream, (uint8_t*)cache_dev,
+                     (uint32_t)n, stride);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_cache_clear launch: ") + hipGetErrorString(e));
+  return GRID_OK;
 }
 
 extern "C" int grid_apply(const uint32_t* mask_dev, void* logits_dev, int32_t dtype, int32_t B, int32_t V,

@@ -21,6 +21,7 @@ ERRORS = {
     -11: "GRID_E_CAPACITY",
 }
 ROW_OK, ROW_EMPTY, ROW_BAD_CONFIG, ROW_OVERFLOW = 0, 1, 2, 4
+CACHE_LOOKUP, CACHE_INSERT = 1, 2
 DTYPE_F32, DTYPE_BF16 = 0, 1
 
 ART_NAMES = ["DFA_DENSE", "DFA_CLASS", "BYTE_CLASS", "DFA_ACCEPT_OFF", "DFA_ACCEPT_LIST", "DFA_LIVE",
@@ -38,7 +39,8 @@ assert CONFIG_DTYPE.itemsize == 32
 # every symbol include/grid.h declares
 EXPORTS = ["grid_compile", "grid_free", "grid_last_error", "grid_info", "grid_add_lexicon",
            "grid_artifact", "grid_bind_device", "grid_config_from_prefix",
-           "grid_mask_workspace_bytes", "grid_mask", "grid_mask_phases", "grid_apply"]
+           "grid_mask_workspace_bytes", "grid_mask", "grid_mask_phases", "grid_apply",
+           "grid_cache_bytes", "grid_cache_clear", "grid_mask_cached"]
 PHASE_PROLOGUE, PHASE_WALK, PHASE_FINALIZE, PHASE_ALL = 1, 2, 4, 7
 
 
@@ -94,6 +96,10 @@ def lib():
         L.grid_mask.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, sz, vp]
         L.grid_mask_phases.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
         L.grid_apply.argtypes = [vp, vp, i32, i32, i32, ctypes.c_int64, vp]
+        L.grid_mask_cached.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, sz, vp, sz, ctypes.c_uint32, vp]
+        L.grid_cache_bytes.argtypes = [vp, i32]
+        L.grid_cache_bytes.restype = sz
+        L.grid_cache_clear.argtypes = [vp, vp, sz, vp]
         _lib = L
     return _lib
 
@@ -216,10 +222,29 @@ class Grid:
         import torch
         return torch.empty(self.workspace_bytes(B), dtype=torch.uint8, device=device or self.device)
 
+    def cache_bytes(self, n_entries):
+        """Device bytes of a mask cache of n_entries (a power of two) entries."""
+        n = lib().grid_cache_bytes(self.h, n_entries)
+        if n == 0:
+            raise ValueError("n_entries must be a power of two")
+        return n
+
+    def new_cache(self, n_entries, device=None, stream=None):
+        """A cleared mask cache (uint8 device tensor)."""
+        import torch
+        c = torch.empty(self.cache_bytes(n_entries), dtype=torch.uint8, device=device or self.device)
+        self.clear_cache(c, stream)
+        return c
+
+    def clear_cache(self, cache, stream=None):
+        _check(lib().grid_cache_clear(self.h, ctypes.c_void_p(cache.data_ptr()), cache.numel(),
+                                      _stream_handle(stream)))
+
     def mask(self, cfg_dev, pool_dev, B, out=None, eos=None, status=None, workspace=None, stream=None,
-             phases=PHASE_ALL):
+             phases=PHASE_ALL, cache=None, cache_flags=CACHE_LOOKUP | CACHE_INSERT):
         """Enqueues the mask of B rows; returns (mask int32 [B, W], eos u8 [B], status i32 [B]).
-        phases selects a subset of the launches (grid_mask_phases)."""
+        phases selects a subset of the launches (grid_mask_phases); cache (from new_cache)
+        serves and records rows through the mask cache (grid_mask_cached)."""
         import torch
         dev = cfg_dev.device
         if out is None:
@@ -234,7 +259,11 @@ class Grid:
         args = (self.h, B, ctypes.c_void_p(cfg_dev.data_ptr()), ctypes.c_void_p(pool_dev.data_ptr()),
                 ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(eos.data_ptr()),
                 ctypes.c_void_p(status.data_ptr()), ctypes.c_void_p(workspace.data_ptr()), workspace.numel())
-        if phases == PHASE_ALL:
+        if cache is not None:
+            assert phases == PHASE_ALL
+            _check(lib().grid_mask_cached(*args, ctypes.c_void_p(cache.data_ptr()), cache.numel(), cache_flags,
+                                          _stream_handle(stream)))
+        elif phases == PHASE_ALL:
             _check(lib().grid_mask(*args, _stream_handle(stream)))
         else:
             _check(lib().grid_mask_phases(*args, phases, _stream_handle(stream)))

@@ -13,6 +13,7 @@
   byte-completeness is reported.
 """
 
+import ctypes
 import itertools
 import random
 import re
@@ -398,3 +399,22 @@ def test_compact_parse_tables_match_dense(G, name, drop):
                 h = (h + 1) % H
             found = int(gh[h, 1]) if gh[h, 0] == key else 0xFFFF
             assert found == int(go[s, a]), (s, a)
+
+
+def test_cache_sizes_and_argument_errors(G):
+    g = G.Grid(grammar_text("expr"), (), [bytes([b]) for b in range(256)] + [b"ab", b"12"])
+    W = (g.V + 31) // 32
+    stride = 64 + (4 * W + 15) // 16 * 16
+    for n in (1, 2, 64, 1024):
+        assert g.cache_bytes(n) == n * stride
+    for n in (0, 3, 1000, -4):
+        assert G.lib().grid_cache_bytes(g.h, n) == 0
+    with pytest.raises(ValueError):
+        g.cache_bytes(12)
+    # a cache of the wrong size is rejected before anything is launched
+    rc = G.lib().grid_cache_clear(g.h, ctypes.c_void_p(16), ctypes.c_size_t(stride * 3), None)
+    assert rc == -1 and b"power of two" in G.lib().grid_last_error()
+    rc = G.lib().grid_mask_cached(g.h, 1, ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256),
+                                  None, None, ctypes.c_void_p(256), ctypes.c_size_t(1 << 30),
+                                  ctypes.c_void_p(256), ctypes.c_size_t(stride * 3), 3, None)
+    assert rc != 0
