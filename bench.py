@@ -63,7 +63,76 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU oracle sample budget")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration runs)")
+    ap.add_argument("--flatness", action="store_true",
+                    help="instead: per-mask cost against position n and nesting depth on the "
+                         "16,000-token workload (one JSON line)")
     return ap.parse_args()
+
+
+def flatness(args):
+    """Cost per mask at positions n = 1k / 4k / 16k tokens and nesting depths
+    1 / 8 / 32 / 128 (32 configurations per cell, one batch each), and per depth
+    the least-squares slope of the per-mask cost against n with a 95% interval
+    (t quantile for the degrees of freedom); flat when |slope| x 15,000 stays
+    under 5 % of the cost at n = 1,000."""
+    import torch
+    import paper_2607_11951_amd as G
+    from workloads import make_workload
+    from scipy import stats
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    wl = make_workload(4)
+    grid, slots = G.from_workload(wl)
+    grid.to_device(dev)
+    B = wl.batch
+    print(f"16,000-token workload ready in {time.time() - t0:.0f}s", file=sys.stderr, flush=True)
+    stream = torch.cuda.current_stream()
+    ws = grid.new_workspace(B, dev)
+    mask = torch.empty((B, grid.W), dtype=torch.int32, device=dev)
+    eos = torch.empty(B, dtype=torch.uint8, device=dev)
+    status = torch.empty(B, dtype=torch.int32, device=dev)
+    cells, samples = [], {}
+    for idx in wl.batches():
+        n_pos, depth, _ = wl.meta["cells"][idx[0]]
+        cfgs, pool = grid.configs([wl.prefixes[j] for j in idx], [slots[wl.slots[j]] for j in idx])
+        c, p = grid.configs_to_device(cfgs, pool, dev)
+        for _ in range(args.warmup):
+            grid.mask(c, p, B, mask, eos, status, ws, stream)
+        torch.cuda.synchronize()
+        assert (status.cpu() == 0).all()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for e0, e1 in evs:
+            e0.record(stream)
+            grid.mask(c, p, B, mask, eos, status, ws, stream)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        us = np.array([e0.elapsed_time(e1) * 1000.0 / B for e0, e1 in evs])
+        samples[(n_pos, depth)] = us
+        cells.append({"n": n_pos, "depth": depth, "us_per_mask_median": float(np.median(us)),
+                      "us_per_mask_p99": float(np.percentile(us, 99)),
+                      "max_stack_depth": int(cfgs["stk_depth"].max())})
+        print(f"n={n_pos:6d} depth={depth:4d}: {np.median(us):.2f} us/mask "
+              f"(stack <= {int(cfgs['stk_depth'].max())})", file=sys.stderr, flush=True)
+    slopes = []
+    for depth in sorted({d for _, d in samples}):
+        xs, ys = [], []
+        for (n_pos, d), us in samples.items():
+            if d == depth:
+                xs += [n_pos] * len(us)
+                ys += list(us)
+        fit = stats.linregress(xs, ys)
+        dof = len(xs) - 2
+        half = stats.t.ppf(0.975, dof) * fit.stderr
+        base = float(np.median(samples[(1000, depth)]))
+        slopes.append({"depth": depth, "slope_us_per_token": float(fit.slope),
+                       "ci95": [float(fit.slope - half), float(fit.slope + half)],
+                       "cost_at_1k_us": base, "change_over_15k_tokens_pct": float(100.0 * fit.slope * 15000 / base),
+                       "flat": bool(abs(fit.slope) * 15000 < 0.05 * base)})
+    print(json.dumps({"metric": "per-mask cost vs position n and nesting depth (flatness)",
+                      "unit": "us/mask", "steps_per_cell": args.steps, "batch": B, "vocab": wl.V,
+                      "workload": "read-only DML SQL, 16,000-token sentences, 32 configs per cell",
+                      "cells": cells, "slopes": slopes}), flush=True)
 
 
 def main():
@@ -80,6 +149,9 @@ def main():
     from workloads import make_workload
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.flatness:
+        flatness(args)
+        return
     dev = torch.device("cuda:0")
     t0 = time.time()
     wl = make_workload(3, n_batches=args.batches)
