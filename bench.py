@@ -183,10 +183,13 @@ def main():
         grid.mask(c, p, B, mask, eos, status, ws, stream, phases=G.grid.PHASE_WALK)
         if ev is not None:
             ev[2].record(stream)
+        grid.mask(c, p, B, mask, eos, status, ws, stream, phases=G.grid.PHASE_RESIDUE)
+        if ev is not None:
+            ev[3].record(stream)
         grid.mask(c, p, B, mask, eos, status, ws, stream, phases=G.grid.PHASE_FINALIZE)
         G.apply(mask, logits, stream)
         if ev is not None:
-            ev[3].record(stream)
+            ev[4].record(stream)
 
     for i in range(args.warmup):
         step(i)
@@ -194,7 +197,7 @@ def main():
     st = status.cpu()
     assert (st == 0).all(), f"row status {st.tolist()}"
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(args.steps):
@@ -202,17 +205,17 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
 
-    step_ms = np.array([e[0].elapsed_time(e[3]) for e in evs])
+    step_ms = np.array([e[0].elapsed_time(e[4]) for e in evs])
     pro_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
     walk_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
-    tail_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    res_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    tail_ms = np.array([e[3].elapsed_time(e[4]) for e in evs])
     per_mask_us = step_ms * 1000.0 / B
 
-    # algorithmic bytes of one walk launch: each row streams the scan-summary
-    # word of every distinct spelling for its DFA state and writes its W mask
-    # words (the spelling bytes read by undecided lanes are not counted)
-    n_spell = info["n_spellings"]
-    bytes_per_mask = 4 * n_spell + 4 * grid.W
+    # algorithmic bytes of one stream launch per row: the class of every token
+    # id for the row's lexer state (u16) and the row's W mask words; the
+    # verdict table (2 bits per class) is not counted
+    bytes_per_mask = 2 * wl.V + 4 * grid.W
     walk_s = float(walk_ms.mean()) / 1000.0
     achieved = B * bytes_per_mask / walk_s / 1e9
 
@@ -291,12 +294,12 @@ def main():
                    "global_batch": B, "vocab": wl.V, "parallelism": "none (1 GPU)"},
         "p50_us_per_mask": float(np.percentile(per_mask_us, 50)),
         "p99_us_per_mask": float(np.percentile(per_mask_us, 99)),
-        "phase_ms": {"prologue": float(pro_ms.mean()), "walk": float(walk_ms.mean()),
-                     "finalize+apply": float(tail_ms.mean())},
-        "roofline": {"bound": "hbm", "kernel": "walk_kernel", "achieved": achieved,
+        "phase_ms": {"prologue+verdicts": float(pro_ms.mean()), "stream": float(walk_ms.mean()),
+                     "residue": float(res_ms.mean()), "finalize+apply": float(tail_ms.mean())},
+        "roofline": {"bound": "hbm", "kernel": "stream_kernel", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": walk_traffic_bytes(), "bytes_per_mask": bytes_per_mask,
-                     "walk_us_per_launch": walk_s * 1e6},
+                     "stream_us_per_launch": walk_s * 1e6},
         "cpu_baseline": cpu,
         "cache": cache_out,
     }

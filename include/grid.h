@@ -152,9 +152,10 @@ enum {
   GRID_ART_LEX_FLAGS,       /* u16 per lexicon-trie node: bit c prefix-of-category-c,
                                bit 8+c word-of-category-c */
   GRID_ART_LEX_HASH,        /* u32 [2] per entry: key = node * 256 + byte + 1 (0 empty), child */
-  GRID_ART_LEX_SLOTS,       /* u32 [8] per slot: flags base, hash base, hash mask,
+  GRID_ART_LEX_SLOTS,       /* u32 [12] per slot: flags base, hash base, hash mask,
                                restricted-category mask, node count, prefix-table base,
-                               prefix-table mask, 1 reserved */
+                               prefix-table mask, stride-table base, stride-table mask,
+                               3 reserved */
   GRID_ART_SPELL_REC,       /* u32 [U][4] per spelling: its first 8 bytes (little-
                                endian, zero padded), first alias id | 1 << 31 when more ids
                                share the spelling, length | overflow chunk << 8 (bytes 24..
@@ -182,15 +183,34 @@ enum {
                                byte | highest first byte << 8 of its spellings */
   GRID_ART_SPELL_OF_ID,     /* u32 [V]: spelling index of each token id, 0xFFFFFFFF
                                for specials and empty tokens */
-  GRID_ART_SCAN_SUMMARY,    /* u32 [S][U]: for lexer DFA state q and spelling u, how
-                               maximal munch segments u when the scan resumes in q (the
-                               walk's scan state, section 4.1; lexeme-internal versus
-                               boundary-crossing tokens, section 4.2).  Bits 0-8 state
-                               after the last byte, 9-17 state in which the first lexeme
-                               ended, 18-25 index of the byte that ended it, 26-27 lexeme
-                               ends inside u (2 = two or more), bit 28 rejected by the
-                               lexer alone.  Empty (0 bytes) when S > 512; the kernels
-                               then scan every byte */
+  GRID_ART_CLASS_MAP,       /* u16 [S][V]: class of token id when the scan resumes in lexer
+                               DFA state q (the walk's scan state, section 4.1), local to
+                               q: tokens whose lexeme programs from q are equal -- the
+                               number of lexeme ends maximal munch makes inside the token,
+                               the DFA states of the first three ends and the state after
+                               the last byte -- share a class (verdict-equivalence classes,
+                               section 4.2).  Class 0: rejected by the lexer alone, special
+                               or empty; class 1: judged by walking the bytes */
+  GRID_ART_CLASS_OFF,       /* u32 [S+1]: first record of each state's classes */
+  GRID_ART_CLASS_REC,       /* u32 [classes][4] per class: ends (0..3, 4 = more) | 8 if
+                               rejected | 16 if byte 0 ends the pending lexeme | 32 for
+                               class 1; state after the last byte | state of end 0 << 16;
+                               state of end 1 | state of end 2 << 16; the byte indices
+                               that ended lexemes 0, 1, 2 (8 bits each, 0 if missing) */
+  GRID_ART_LEX_STRIDE,      /* u32 [8] per entry, per slot an open-addressing table of every
+                               lexicon-trie node of depth d > 8 keyed by its ancestor at
+                               depth 8 * floor((d - 1) / 8) and its 1..8 bytes below it:
+                               ancestor node, bytes lo, bytes hi (little-endian, zero
+                               padded), length | flags << 16 (length 0 = empty), node,
+                               3 zero words */
+  GRID_ART_LEX_TOKEN,       /* u32 [slots][V]: per lexicon slot and token id, for start
+                               offsets o = 0 (bits 0-15) and o = 1 (bits 16-31): the
+                               prefix-of-category flags of the token's bytes from o to its
+                               end (low byte) and the word-of-category flags of the first
+                               lexeme maximal munch cuts from o in the start state (high
+                               byte; 0 when that lexeme runs to the token's end) */
+  GRID_ART_ID_FIRST,        /* u8 [V]: first byte of each token id's spelling (0 for
+                               specials and empty tokens) */
   GRID_ART_COUNT
 };
 int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);
@@ -239,18 +259,21 @@ int grid_mask(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
               int32_t* status_dev, void* workspace_dev, size_t workspace_bytes, void* stream);
 
 /* The same work split into its launches, for callers that time or overlap
- * them: phases is a bit set of GRID_PHASE_* run in order on the stream.  A
- * walk needs the prologue of the same rows and workspace to have run before
- * it (earlier on the stream); finalize needs the walk; the mask is exact once
- * all three have run.  grid_mask equals grid_mask_phases with GRID_PHASE_ALL. */
-#define GRID_PHASE_PROLOGUE 1u      /* allowed sets, EOS gate, first-byte table */
-#define GRID_PHASE_WALK 2u          /* full-vocabulary walk into a mask in spelling
-                                       order (workspace) */
-#define GRID_PHASE_FINALIZE 4u      /* the spellings the walk handed to the slow path,
-                                       then mask_dev (each id takes its spelling's bit;
-                                       the EOS bit) and the row status when status_dev
-                                       is not null */
-#define GRID_PHASE_ALL 7u
+ * them: phases is a bit set of GRID_PHASE_* run in the order below on the
+ * stream.  Each phase needs the earlier ones of the same rows and workspace
+ * to have run before it (earlier on the stream); the mask is exact once all
+ * four have run.  grid_mask equals grid_mask_phases with GRID_PHASE_ALL. */
+#define GRID_PHASE_PROLOGUE 1u      /* allowed sets, EOS gate, post-shift stacks, then
+                                       the verdict of every lexeme-program class of the
+                                       row's lexer state */
+#define GRID_PHASE_WALK 2u          /* mask_dev in token-id order from the class map;
+                                       tokens whose class needs their bytes go to the
+                                       row's residue list (workspace) */
+#define GRID_PHASE_RESIDUE 4u       /* byte walk of the residue lists, OR-ing allowed
+                                       bits into mask_dev */
+#define GRID_PHASE_FINALIZE 8u      /* tokens the residue walk handed to the slow path,
+                                       then the row status when status_dev is not null */
+#define GRID_PHASE_ALL 15u
 int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
                      const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
                      int32_t* status_dev, void* workspace_dev, size_t workspace_bytes,

@@ -10,11 +10,12 @@
 // CSR form of the same trie (level by level, children in byte order, each
 // node pointing at its parent and at the spelling that ends there).
 //
-// Scan summary (section 4.1: the walk carries the scan state; section 4.2: a
-// token either stays inside the current lexeme or crosses boundaries): for
-// every DFA state q and spelling u, where maximal munch ends lexemes in u when
-// the scan resumes in q, packed as in lexhash.h.  It depends on the lexer and
-// the vocabulary only, so it is built once per compile.
+// Lexeme-program classes (section 4.1: the walk carries the scan state;
+// section 4.2: a token either stays inside the current lexeme or crosses
+// boundaries, and tokens with equal verdict inputs form classes): for every
+// DFA state q and token id, the class of its lexeme program from q, laid out
+// as in lexhash.h.  It depends on the lexer and the vocabulary only, so it is
+// built once per compile.
 //
 // Schema lexicon (section 2, L3): per slot, one byte trie over the words of
 // every category with per-node flags "prefix of a category-c word" and
@@ -26,6 +27,7 @@
 #include <map>
 #include <numeric>
 #include <thread>
+#include <unordered_map>
 
 #include "host.h"
 #include "lexhash.h"
@@ -110,8 +112,12 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
     if (s.size() == 1) single[(uint8_t)s[0]] = 1;
   va.byte_complete = std::all_of(single.begin(), single.end(), [](char c) { return c != 0; });
   va.spell_of_id.assign(V, 0xFFFFFFFFu);
+  va.id_first.assign(V, 0);
   for (size_t u = 0; u < U; ++u)
-    for (uint32_t k = va.alias_off[u]; k < va.alias_off[u + 1]; ++k) va.spell_of_id[va.alias_ids[k]] = (uint32_t)u;
+    for (uint32_t k = va.alias_off[u]; k < va.alias_off[u + 1]; ++k) {
+      va.spell_of_id[va.alias_ids[k]] = (uint32_t)u;
+      va.id_first[va.alias_ids[k]] = (uint8_t)uniq[u][0];
+    }
   // first-byte range of every 64 consecutive spellings (first bytes are
   // non-decreasing, so the first and the last spelling of the group bound it)
   for (size_t u0 = 0; u0 < uniq.size(); u0 += 64) {
@@ -148,14 +154,20 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
   return va;
 }
 
-std::vector<uint32_t> build_scan_summary(const LexerDfa& dfa, const VocabArtifacts& va) {
+ClassTables build_class_tables(const LexerDfa& dfa, const VocabArtifacts& va) {
   const size_t U = va.spell_off.size() - 1;
-  if ((uint32_t)dfa.S > kScanMaxStates || U == 0) return {};
-  std::vector<uint32_t> out((size_t)dfa.S * U);
-  auto one = [&](int q, size_t u) -> uint32_t {
+  const size_t S = (size_t)dfa.S, V = (size_t)va.V;
+  if (S * V > ((size_t)3 << 29))
+    throw Error(GRID_E_CAPACITY, "class map of " + std::to_string(S) + " lexer states x " + std::to_string(V) +
+                                     " tokens is larger than 3 GiB");
+  ClassTables ct;
+  ct.map.assign(S * V, 0);
+  std::vector<std::vector<uint32_t>> recs(S);
+  // the lexeme program of spelling u when the scan resumes in q
+  auto program = [&](uint32_t q, size_t u, uint32_t (&r)[4]) {
     const uint8_t* b = va.spell_bytes.data() + va.spell_off[u];
     const uint32_t n = va.spell_off[u + 1] - va.spell_off[u];
-    uint32_t cur = (uint32_t)q, q_first = 0, p_first = 0, ends = 0;
+    uint32_t cur = q, ends = 0, qe[kClassEnds] = {0, 0, 0}, pe[kClassEnds] = {0, 0, 0}, flags = 0;
     for (uint32_t i = 0; i < n; ++i) {
       const uint32_t nq = dfa.step((int)cur, b[i]);
       if (nq != (uint32_t)kDead) {
@@ -164,26 +176,85 @@ std::vector<uint32_t> build_scan_summary(const LexerDfa& dfa, const VocabArtifac
       }
       // byte i ends the lexeme in state cur; it must accept something, and
       // byte i must start the next lexeme
-      if (!dfa.accepting[cur]) return kScanReject;
-      if (ends == 0) {
-        q_first = cur;
-        p_first = i;
+      if (!dfa.accepting[cur]) {
+        r[0] = kClassReject, r[1] = r[2] = r[3] = 0;
+        return;
       }
-      if (++ends == 2) return scan_word(0, q_first, p_first, 2);
+      if (i == 0) flags |= kClassP0;
+      if (ends < (uint32_t)kClassEnds) {
+        qe[ends] = cur;
+        pe[ends] = i;
+      }
+      ++ends;
       cur = dfa.step(kStart, b[i]);
-      if (cur == (uint32_t)kDead) return kScanReject;
+      if (cur == (uint32_t)kDead) {
+        r[0] = kClassReject, r[1] = r[2] = r[3] = 0;
+        return;
+      }
     }
-    return scan_word(cur, q_first, p_first, ends);
+    r[0] = (ends > (uint32_t)kClassEnds ? kClassMore : ends) | flags;
+    r[1] = cur | qe[0] << 16;
+    r[2] = qe[1] | qe[2] << 16;
+    r[3] = pe[0] | pe[1] << 8 | pe[2] << 16;
+  };
+  struct Key {
+    uint32_t a, b, c, d;
+    bool operator==(const Key& o) const { return a == o.a && b == o.b && c == o.c && d == o.d; }
+  };
+  struct KeyHash {
+    size_t operator()(const Key& k) const {
+      uint64_t h = ((uint64_t)k.a << 32 | k.b) * 0x9E3779B97F4A7C15ull ^
+                   ((uint64_t)k.c << 32 | k.d) * 0xC2B2AE3D27D4EB4Full;
+      return (size_t)(h ^ (h >> 29));
+    }
   };
   const int nt = (int)std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
   std::vector<std::thread> pool;
   for (int w = 0; w < nt; ++w)
     pool.emplace_back([&, w]() {
-      for (int q = w; q < dfa.S; q += nt)
-        for (size_t u = 0; u < U; ++u) out[(size_t)q * U + u] = one(q, u);
+      std::vector<uint16_t> local(U);
+      std::unordered_map<Key, uint32_t, KeyHash> seen;
+      for (size_t q = (size_t)w; q < S; q += (size_t)nt) {
+        seen.clear();
+        std::vector<uint32_t>& rq = recs[q];
+        rq = {kClassReject, 0, 0, 0, kClassWalk, 0, 0, 0};  // local classes 0 and 1
+        for (size_t u = 0; u < U; ++u) {
+          uint32_t r[4];
+          program((uint32_t)q, u, r);
+          if (r[0] & kClassReject) {
+            local[u] = 0;
+            continue;
+          }
+          auto it = seen.find(Key{r[0], r[1], r[2], r[3]});
+          if (it != seen.end()) {
+            local[u] = (uint16_t)it->second;
+            continue;
+          }
+          const uint32_t c = (uint32_t)(rq.size() / 4);
+          if (c >= kClassMaxLocal) {  // beyond capacity: this token walks its bytes
+            local[u] = 1;
+            continue;
+          }
+          seen.emplace(Key{r[0], r[1], r[2], r[3]}, c);
+          rq.insert(rq.end(), {r[0], r[1], r[2], r[3]});
+          local[u] = (uint16_t)c;
+        }
+        uint16_t* m = ct.map.data() + q * V;
+        for (size_t id = 0; id < V; ++id) {
+          const uint32_t u = va.spell_of_id[id];
+          m[id] = u == 0xFFFFFFFFu ? (uint16_t)0 : local[u];
+        }
+      }
     });
   for (auto& th : pool) th.join();
-  return out;
+  ct.off.assign(S + 1, 0);
+  for (size_t q = 0; q < S; ++q) {
+    ct.off[q + 1] = ct.off[q] + (uint32_t)(recs[q].size() / 4);
+    ct.max_classes = std::max(ct.max_classes, ct.off[q + 1] - ct.off[q]);
+  }
+  ct.rec.reserve((size_t)ct.off[S] * 4);
+  for (size_t q = 0; q < S; ++q) ct.rec.insert(ct.rec.end(), recs[q].begin(), recs[q].end());
+  return ct;
 }
 
 uint32_t LexiconStore::child(int slot, uint32_t node, uint8_t b) const {
@@ -202,7 +273,7 @@ uint16_t LexiconStore::node_flags(int slot, uint32_t node) const {
   return flags[slots[(size_t)slot * kSlotWords] + node];
 }
 
-void add_lexicon(LexiconStore& st, const LexerDfa& dfa, const GrammarText& g,
+void add_lexicon(LexiconStore& st, const LexerDfa& dfa, const GrammarText& g, const VocabArtifacts& va,
                  const std::vector<int>& term_cat,
                  const std::vector<std::pair<std::string, std::vector<std::string>>>& cats) {
   struct Node {
@@ -304,8 +375,82 @@ void add_lexicon(LexiconStore& st, const LexerDfa& dfa, const GrammarText& g,
       }
     }
   }
+  // stride table: every node of depth > 8 keyed by its ancestor at the last
+  // multiple of 8 above it and its bytes below that ancestor
+  struct Deep {
+    uint32_t anc, lo, hi, len, node;
+  };
+  std::vector<Deep> deep;
+  {
+    struct Todo {
+      uint32_t n, depth, anc;
+      uint64_t bytes;  // bytes below anc
+    };
+    std::vector<Todo> todo{{0u, 0u, 0u, 0ull}};
+    while (!todo.empty()) {
+      const Todo t = todo.back();
+      todo.pop_back();
+      for (auto& e : nodes[t.n].kids) {
+        const uint32_t d = t.depth + 1, k = (d - 1) & 7u;  // k: index of this byte below anc
+        const uint64_t b2 = (k == 0 ? 0ull : t.bytes) | (uint64_t)e.first << (8 * k);
+        if (d > 8) deep.push_back({t.anc, (uint32_t)b2, (uint32_t)(b2 >> 32), k + 1, e.second});
+        // the children of a node at a multiple of 8 hang below it
+        todo.push_back({e.second, d, d % 8 == 0 ? e.second : t.anc, b2});
+      }
+    }
+  }
+  uint32_t ssize = 16;
+  while (ssize < 2 * deep.size()) ssize <<= 1;
+  const uint32_t stride_base = (uint32_t)(st.stride.size() / 8);
+  st.stride.resize(st.stride.size() + (size_t)ssize * 8, 0);
+  for (auto& e : deep) {
+    for (uint32_t h = lexs_hash(e.anc, e.lo, e.hi, e.len) & (ssize - 1);; h = (h + 1) & (ssize - 1)) {
+      uint32_t* slot = &st.stride[(size_t)(stride_base + h) * 8];
+      if ((slot[3] & 0xFFFF) == 0) {
+        slot[0] = e.anc;
+        slot[1] = e.lo;
+        slot[2] = e.hi;
+        slot[3] = e.len | (uint32_t)nodes[e.node].flags << 16;
+        slot[4] = e.node;
+        break;
+      }
+    }
+  }
+  // token flags: for every token id and start offset o in {0, 1}, the
+  // prefix flags of the token's bytes from o to its end and the word flags of
+  // the first lexeme maximal munch cuts from o (scanning from the start state)
+  const size_t tok_base = st.token.size();
+  st.token.resize(tok_base + (size_t)va.V, 0u);
+  if (restricted) {
+    const size_t U = va.spell_off.size() - 1;
+    for (size_t u = 0; u < U; ++u) {
+      const uint8_t* b = va.spell_bytes.data() + va.spell_off[u];
+      const uint32_t n = va.spell_off[u + 1] - va.spell_off[u];
+      uint32_t f = 0;
+      for (uint32_t o = 0; o < 2 && o < n; ++o) {
+        uint32_t e1 = n, q = kStart;  // end of the first lexeme from o
+        for (uint32_t i = o; i < n; ++i) {
+          q = dfa.step((int)q, b[i]);
+          if (q == (uint32_t)kDead) {
+            e1 = i;
+            break;
+          }
+        }
+        uint32_t node = 0, pre = 0, word = 0;
+        for (uint32_t i = o; i < n; ++i) {
+          auto it = nodes[node].kids.find(b[i]);
+          if (it == nodes[node].kids.end()) break;
+          node = it->second;
+          if (i + 1 == e1 && e1 < n) word = nodes[node].flags >> 8;
+          if (i + 1 == n) pre = nodes[node].flags & 0xFFu;
+        }
+        f |= (pre | word << 8) << (16 * o);
+      }
+      for (uint32_t k = va.alias_off[u]; k < va.alias_off[u + 1]; ++k) st.token[tok_base + va.alias_ids[k]] = f;
+    }
+  }
   uint32_t rec[kSlotWords] = {flags_base, hash_base, size - 1, restricted, (uint32_t)nodes.size(),
-                              pref_base,  psize - 1, 0};
+                              pref_base,  psize - 1, stride_base, ssize - 1, 0, 0, 0};
   st.slots.insert(st.slots.end(), rec, rec + kSlotWords);
   st.n_slots += 1;
 }

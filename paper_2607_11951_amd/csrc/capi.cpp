@@ -64,8 +64,8 @@ extern "C" int grid_compile(const grid_compile_args* a, grid_compiled** out) {
     }
     g->vocab = build_vocab(a->vocab_bytes, a->vocab_offsets, a->vocab_size, a->special_ids,
                            a->n_special, a->eos_id);
-    g->scan = build_scan_summary(g->dfa, g->vocab);
-    add_lexicon(g->lex, g->dfa, g->gram, g->term_cat, {});  // slot 0: no restrictions
+    g->classes = build_class_tables(g->dfa, g->vocab);
+    add_lexicon(g->lex, g->dfa, g->gram, g->vocab, g->term_cat, {});  // slot 0: no restrictions
     // FNV-1a over the tables a cached mask row depends on
     uint32_t fp = 2166136261u;
     auto mix = [&fp](const void* p, size_t n) {
@@ -135,10 +135,11 @@ extern "C" int grid_add_lexicon(grid_compiled* g, const grid_lexicon_args* la, i
     if (g->lex.n_slots >= 0xFFFF) return fail(GRID_E_CAPACITY, "too many lexicon slots");
     // add_lexicon validates every word before it appends anything, so a
     // failing call leaves the handle unchanged
-    add_lexicon(g->lex, g->dfa, g->gram, g->term_cat, cats);
+    add_lexicon(g->lex, g->dfa, g->gram, g->vocab, g->term_cat, cats);
     *slot = g->lex.n_slots - 1;
     // lexicon artifacts changed: device copies must be re-bound
     g->dev[GRID_ART_LEX_FLAGS] = g->dev[GRID_ART_LEX_HASH] = g->dev[GRID_ART_LEX_SLOTS] = nullptr;
+    g->dev[GRID_ART_LEX_PREFIX] = g->dev[GRID_ART_LEX_STRIDE] = g->dev[GRID_ART_LEX_TOKEN] = nullptr;
     return GRID_OK;
   } catch (const Error& e) {
     return fail(e.code, e.what());
@@ -183,7 +184,12 @@ extern "C" int grid_artifact(const grid_compiled* g, int32_t which, const void**
     case GRID_ART_LEX_PREFIX: put(g->lex.prefix, p, n); break;
     case GRID_ART_SPELL_RANGE: put(g->vocab.sub_range, p, n); break;
     case GRID_ART_SPELL_OF_ID: put(g->vocab.spell_of_id, p, n); break;
-    case GRID_ART_SCAN_SUMMARY: put(g->scan, p, n); break;
+    case GRID_ART_CLASS_MAP: put(g->classes.map, p, n); break;
+    case GRID_ART_CLASS_OFF: put(g->classes.off, p, n); break;
+    case GRID_ART_CLASS_REC: put(g->classes.rec, p, n); break;
+    case GRID_ART_LEX_STRIDE: put(g->lex.stride, p, n); break;
+    case GRID_ART_LEX_TOKEN: put(g->lex.token, p, n); break;
+    case GRID_ART_ID_FIRST: put(g->vocab.id_first, p, n); break;
     case GRID_ART_PARSE_STATE: put(g->parser.pstate, p, n); break;
     case GRID_ART_PARSE_REDX: put(g->parser.predx, p, n); break;
     case GRID_ART_GOTO_HASH: put(g->parser.goto_hash, p, n); break;

@@ -103,6 +103,7 @@ struct VocabArtifacts {
   std::vector<uint8_t> spell_tail;   // bytes 8.. per spelling, 16-byte aligned chunks
   std::vector<uint16_t> sub_range;   // per 64 spellings: lowest | highest first byte << 8
   std::vector<uint32_t> spell_of_id; // [V]: spelling index, 0xFFFFFFFF none
+  std::vector<uint8_t> id_first;     // [V]: first byte of the spelling, 0 none
   std::vector<uint32_t> alias_off;   // [U+1]
   std::vector<int32_t> alias_ids;
   std::vector<uint32_t> level_off;   // [Lmax+2]
@@ -115,14 +116,22 @@ struct VocabArtifacts {
 VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, const int32_t* specials,
                            int n_special, int eos_id);
 
-// scan summary [S][U] (lexhash.h); empty when the DFA has more than 512 states
-std::vector<uint32_t> build_scan_summary(const LexerDfa& dfa, const VocabArtifacts& va);
+// lexeme-program classes per lexer state (lexhash.h)
+struct ClassTables {
+  std::vector<uint16_t> map;   // [S][V] local class of each token id
+  std::vector<uint32_t> off;   // [S+1] first record of each state
+  std::vector<uint32_t> rec;   // [classes][4]
+  uint32_t max_classes = 0;    // largest class count of one state
+};
+ClassTables build_class_tables(const LexerDfa& dfa, const VocabArtifacts& va);
 
 // ---- lexicon slots
 struct LexiconStore {
   std::vector<uint16_t> flags;     // all slots' nodes
   std::vector<uint32_t> hash;      // all slots' entries (2 u32 each)
   std::vector<uint32_t> prefix;    // all slots' prefix-table entries (4 u32 each)
+  std::vector<uint32_t> stride;    // all slots' stride-table entries (8 u32 each)
+  std::vector<uint32_t> token;     // all slots' token flags ([V] u32 each)
   std::vector<uint32_t> slots;     // kSlotWords u32 per slot
   int n_slots = 0;
   // host-side lookup helpers
@@ -131,7 +140,7 @@ struct LexiconStore {
   uint32_t restricted(int slot) const { return slots[(size_t)slot * kSlotWords + 3]; }
 };
 
-void add_lexicon(LexiconStore& store, const LexerDfa& dfa, const GrammarText& g,
+void add_lexicon(LexiconStore& store, const LexerDfa& dfa, const GrammarText& g, const VocabArtifacts& va,
                  const std::vector<int>& term_cat,
                  const std::vector<std::pair<std::string, std::vector<std::string>>>& cats);
 
@@ -143,7 +152,7 @@ struct grid_compiled {
   grid::Parser parser;
   grid::VocabArtifacts vocab;
   grid::LexiconStore lex;
-  std::vector<uint32_t> scan;         // scan summary [S][U]
+  grid::ClassTables classes;          // lexeme-program classes
   uint32_t fingerprint = 0;           // of the lexer, parser and vocabulary (mask-cache entries)
   std::vector<int> term_cat;          // category index per terminal or -1
   std::vector<uint32_t> term_info;    // device word per terminal

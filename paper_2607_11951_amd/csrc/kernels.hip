@@ -60,22 +60,19 @@ constexpr int kStackWin = 256;       // top of the row's stack kept in LDS (prol
 constexpr int kPostCap = 14;         // overlay states recorded per first shift
 constexpr int kTmpCap = 32;          // prologue: virtual pushes of one simulation
 constexpr int kGuard = 4096;         // reduce-chain step bound
-constexpr int kSlowCap = 4096;       // spellings handed to the slow path per row
+constexpr int kSlowCap = 4096;       // tokens handed to the slow path per row
 constexpr int kSlowThreads = 64;
 constexpr int kSlowLane = 512;       // slow path per-thread stack area (workspace)
-constexpr int kGatherGroups = 128;   // finalize workgroups per row
 constexpr uint32_t kRowValid = 0x600D;
 constexpr size_t kWsHead = 256;      // workspace head (reserved)
 constexpr int kMaxRounds = 257;      // set-simulation reruns (each peels one reduce group)
 
-// walk launch shape: one 1024-thread workgroup per compute unit
+// residue walk launch shape: one 1024-thread workgroup per compute unit
 constexpr int kWalkThreads = 1024;
-constexpr int kSub = 64;             // spellings per wave item (one per lane)
 constexpr int kFastLane = 16;        // per-lane stack area in LDS (overlay at the bottom,
                                      // virtual pushes above it)
 constexpr int kRowGroup = 32;        // rows resident in LDS at once (at most)
 constexpr int kWalkWin = 64;         // top stack entries of each row in the walk's LDS
-constexpr int kMaxItems = 512;       // work items of one walk workgroup per row group (at most)
 constexpr uint32_t kWalkLdsMax = 160 * 1024;
 
 struct Tables {
@@ -100,9 +97,14 @@ struct Tables {
   const uint32_t* lex_hash;
   const uint32_t* lex_slots;
   const uint4* lex_prefix;
-  const uint16_t* sub_range;  // per 64 spellings: lowest | highest first byte << 8
-  const uint32_t* scan;       // scan summary [S][U], or null (scan every byte)
+  const uint4* lex_stride;    // [entries][2]
+  const uint32_t* lex_token;  // [slots][V] token flags at start offsets 0 and 1
+  const uint8_t* id_first;    // [V] first byte of each token
+  const uint16_t* cmap;       // class of each token per lexer state [S][V]
+  const uint32_t* coff;       // [S+1] first class record of each state
+  const uint4* crec;          // class records
   int S, C, T, N, NS, P, U, V, W, n_slots, eos_id;
+  int max_classes;            // largest class count of one lexer state
   int tw, n_pstate, n_predx, n_acc, hbits;
   uint8_t* cache;             // mask cache (null: off)
   uint32_t cache_mask;        // entries - 1
@@ -143,8 +145,8 @@ struct RowHeader {
   uint32_t A[8];              // allowed terminals of sigma
   uint32_t Aw[8];             // allowed terminals after shifting the winner
   uint32_t R[8];              // terminals whose category the row's lexicon restricts
-  uint32_t alive[8];          // first bytes that can start a token
-  uint32_t slot[8];           // the row's lexicon slot record
+  uint32_t slot[kSlotWords];  // the row's lexicon slot record
+  uint32_t cont[8];           // bytes b such that (pending lexeme) b prefixes a lexicon word
   uint32_t eos_ok;
   uint32_t valid;
   int32_t winner;             // pending lexeme's winner at an emission, -1 none
@@ -157,9 +159,13 @@ struct RowHeader {
   uint32_t nonempty;          // the walk allowed some token
   int32_t cache_slot;         // mask-cache entry this row publishes to, -1 none
   int32_t fstat;              // final row status (finalize)
-  uint32_t pad[7];
+  uint32_t res_count;         // tokens the stream kernel left to the lexicon pass
+  uint32_t walk_count;        // tokens the stream kernel left to the byte walk
+  uint32_t cls_base, n_cls;   // the row's lexer state's class records
+  uint32_t slot_id;           // the row's lexicon slot
+  uint32_t pad[14];
 };
-static_assert(sizeof(RowHeader) == 256, "row header is 256 bytes");
+static_assert(sizeof(RowHeader) == 320, "row header is 320 bytes");
 
 struct Post {                 // stack after shifting one allowed terminal
   uint16_t k;                 // shared base entries kept
@@ -170,7 +176,7 @@ struct Post {                 // stack after shifting one allowed terminal
 static_assert(sizeof(Post) == 32, "post entry is 32 bytes");
 
 struct RowLayout {
-  size_t cls, win, block, post, a2, smask, slow, slow_ov, total;
+  size_t cls, win, block, post, a2, vcode, vrule, lexl, walkl, slow, slow_ov, total;
 };
 
 __host__ __device__ inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u; }
@@ -178,9 +184,11 @@ __host__ __device__ inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u;
 // One row's workspace: header; trailing-flag tables under A(sigma) and after
 // the winner's shift (one byte per DFA state each); the top kWalkWin states
 // of the stack; [block ends here]; post-shift stacks and allowed sets of the
-// allowed terminals; the row's mask in sorted-spelling order (one 64-bit word
-// per 64-spelling sub-tile); the slow path's list and stack areas.
-__host__ __device__ inline RowLayout row_layout(int T, int U, int S) {
+// allowed terminals; the class verdicts (2 bits per class of the row's lexer
+// state) and lexicon shortcuts (a byte per class); the lexicon list ((token id, class) pairs the stream kernel left
+// to the lexicon pass) and the walk list (token ids left to the byte walk);
+// the slow path's list and stack areas.
+__host__ __device__ inline RowLayout row_layout(int T, int S, int V, int max_classes) {
   RowLayout L;
   size_t o = sizeof(RowHeader);
   L.cls = o;
@@ -192,8 +200,14 @@ __host__ __device__ inline RowLayout row_layout(int T, int U, int S) {
   o += (size_t)T * sizeof(Post);
   L.a2 = o;
   o += (size_t)T * 32;
-  L.smask = o;
-  o += (size_t)((U + 63) / 64) * 8;
+  L.vcode = o;
+  o += (size_t)pad16(((uint32_t)max_classes + 3u) / 4u);
+  L.vrule = o;
+  o += (size_t)pad16((uint32_t)max_classes);
+  L.lexl = o;
+  o += (size_t)V * 8;
+  L.walkl = o;
+  o += (size_t)V * 4;
   L.slow = o;
   o += kSlowCap * 4;
   L.slow_ov = o;
@@ -202,6 +216,7 @@ __host__ __device__ inline RowLayout row_layout(int T, int U, int S) {
   return L;
 }
 
+__host__ __device__ inline RowLayout row_layout(const Tables& tb) { return row_layout(tb.T, tb.S, tb.V, tb.max_classes); }
 
 // Several global -> LDS copies (each region 16-byte aligned) in one pass:
 // the regions' 16-byte chunks are numbered consecutively and every thread
@@ -594,13 +609,12 @@ __device__ __forceinline__ int allowed_set(const ParseTabs<L>& pt, const BaseSta
 
 // ---------------------------------------------------------- lexicon helpers
 struct Slot {
-  uint32_t fbase, hbase, hmask, restricted, nodes, pbase, pmask;
+  uint32_t fbase, hbase, hmask, restricted, nodes, pbase, pmask, sbase, smask;
 };
 
-__device__ inline Slot load_slot(const Tables& tb, int s) {
-  const uint32_t* r = tb.lex_slots + (size_t)s * kSlotWords;
-  return {r[0], r[1], r[2], r[3], r[4], r[5], r[6]};
-}
+__device__ inline Slot slot_of(const uint32_t* r) { return {r[0], r[1], r[2], r[3], r[4], r[5], r[6], r[7], r[8]}; }
+
+__device__ inline Slot load_slot(const Tables& tb, int s) { return slot_of(tb.lex_slots + (size_t)s * kSlotWords); }
 
 __device__ inline uint32_t lex_child(const Tables& tb, const Slot& sl, uint32_t node, uint32_t b) {
   if (node == kNoLex) return kNoLex;
@@ -630,6 +644,37 @@ __device__ inline uint2 lexp_find(const Tables& tb, const Slot& sl, uint64_t byt
     if (e.x == lo && e.y == hi && el == len) return make_uint2(e.z >> 16, e.w);
   }
   return make_uint2(0u, kNoLex);
+}
+
+// Flags and node of the lexicon-trie node below node anc (at a depth that is
+// a multiple of 8) reached by len (1..8) more bytes: one probe in the slot's
+// stride table.  (0, kNoLex) if no word has that prefix.
+__device__ inline uint2 lexs_find(const Tables& tb, const Slot& sl, uint32_t anc, uint64_t bytes, uint32_t len) {
+  const uint32_t lo = (uint32_t)bytes, hi = (uint32_t)(bytes >> 32);
+  uint32_t h = lexs_hash(anc, lo, hi, len) & sl.smask;
+  for (uint32_t probe = 0; probe <= sl.smask; ++probe, h = (h + 1) & sl.smask) {
+    const uint4 e = tb.lex_stride[2 * (size_t)(sl.sbase + h)];
+    const uint32_t el = e.w & 0xFFFFu;
+    if (el == 0) break;
+    if (e.x == anc && e.y == lo && e.z == hi && el == len) return make_uint2(e.w >> 16, tb.lex_stride[2 * (size_t)(sl.sbase + h) + 1].x);
+  }
+  return make_uint2(0u, kNoLex);
+}
+
+__device__ inline uint64_t low_bytes(uint64_t w, uint32_t n) { return n >= 8 ? w : w & ((1ull << (8 * n)) - 1ull); }
+
+// Lexicon flags of a lexeme of len (1..24) bytes held in b0 b1 b2
+// (little-endian, 8 bytes a word): at most three probes (prefix table, then
+// stride table).
+__device__ __forceinline__ uint32_t lex_flags_bytes(const Tables& tb, const Slot& sl, uint64_t b0, uint64_t b1,
+                                                    uint64_t b2, uint32_t len) {
+  if (len <= 8) return lexp_find(tb, sl, low_bytes(b0, len), len).x;
+  uint32_t node = lexp_find(tb, sl, b0, 8).y;
+  if (node == kNoLex) return 0u;
+  if (len <= 16) return lexs_find(tb, sl, node, low_bytes(b1, len - 8), len - 8).x;
+  node = lexs_find(tb, sl, node, b1, 8).y;
+  if (node == kNoLex) return 0u;
+  return lexs_find(tb, sl, node, low_bytes(b2, len - 16), len - 16).x;
 }
 
 // The pending lexeme as the lexicon sees it: its bytes while it has at most 8
@@ -761,14 +806,14 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   const int row = blockIdx.x;
   const int tid = threadIdx.x;
   __shared__ uint16_t win[kStackWin];
-  __shared__ uint32_t A[8], I[8], R[8], Aw[8], alive[8];
+  __shared__ uint32_t A[8], I[8], R[8], Aw[8];
   __shared__ Post posts[256];
   __shared__ uint16_t scratch[kBlock][kPostCap + kTmpCap];
   __shared__ int bad, overflow, winner, eos_ok, cache_hit;
   __shared__ unsigned long long hacc[2];
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
-  const RowLayout L = row_layout(tb.T, tb.U, tb.S);
+  const RowLayout L = row_layout(tb);
   Post* post = (Post*)(rw + L.post);
   uint32_t* a2 = (uint32_t*)(rw + L.a2);
   const grid_config cfg = cfgs[row];
@@ -794,10 +839,8 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     cache_hit = -1;
     hacc[0] = 0;
     hacc[1] = 0;
-  }
-  {
-    uint64_t* sm = (uint64_t*)(rw + L.smask);
-    for (int i = tid; i < (tb.U + 63) / 64; i += kBlock) sm[i] = 0ull;
+    hdr->res_count = 0;
+    hdr->walk_count = 0;
   }
   __syncthreads();
   const uint32_t depth = cfg.stk_depth;
@@ -909,7 +952,6 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     R[tid] = 0;
     A[tid] = 0;
     Aw[tid] = 0;
-    alive[tid] = 0;
   }
   __syncthreads();
   if (tid < tb.T) {  // ignored and restricted terminals, one per thread
@@ -980,50 +1022,39 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     eos_ok = ok;
   }
   __syncthreads();
-  // phase 3: which first bytes can start a token (continuing the pending
-  // lexeme, or emitting it as its winner and starting a new one), and the
-  // trailing-flag tables of every DFA state under A(sigma) and after the
-  // winner's shift
+  // phase 3: the trailing-flag tables of every DFA state under A(sigma) and
+  // after the winner's shift, the bytes that continue the pending lexeme in
+  // the lexicon (thread b), and the top of the stack for the residue walk
   {
-    const int b = tid;  // kBlock == 256: one byte value per thread
-    const uint32_t c = tb.bclass[b];
-    bool live = false;
+    const uint32_t b = (uint32_t)tid;  // kBlock == 256: one byte value per thread
+    const bool c = !rem_empty && lex_child(tb, sl, cfg.lexnode, b) != kNoLex;
+    const uint64_t bal = __ballot(c);
+    if ((tid & 31) == 0) hdr->cont[tid >> 5] = (uint32_t)(bal >> (tid & 32));
+  }
+  {
     uint32_t a0[MW], aw[MW];
 #pragma unroll
     for (int k = 0; k < MW; ++k) {
       a0[k] = A[k];
       aw[k] = Aw[k];
     }
-    const int nq = tb.dfa[(size_t)cfg.q * tb.C + c];
-    if (nq != kDead) {
-      live = trail_ok<MW>(tv, a0, nq, lex_flags_of(tb, sl, lex_child(tb, sl, cfg.lexnode, b)));
-    } else if (!rem_empty && w >= 0) {
-      const int sq = tb.dfa[(size_t)kStart * tb.C + c];
-      if (sq != kDead) {
-        const uint32_t lf1 = lex_flags_of(tb, sl, lex_child(tb, sl, 0u, b));
-        live = w_shifts ? trail_ok<MW>(tv, aw, sq, lf1) : trail_ok<MW>(tv, a0, sq, lf1);
-      }
-    }
-    if (live) atomicOr(&alive[b >> 5], 1u << (b & 31));
     uint8_t* clsA = rw + L.cls;
     uint8_t* clsW = clsA + pad16((uint32_t)tb.S);
     for (int q = tid; q < tb.S; q += kBlock) {
       clsA[q] = (uint8_t)trail_flags<MW>(tv, a0, q);
       clsW[q] = (uint8_t)trail_flags<MW>(tv, aw, q);
     }
-    // the top of the stack for the walk's LDS
     uint16_t* wwin = (uint16_t*)(rw + L.win);
     const uint32_t wlo = depth > (uint32_t)kWalkWin ? depth - kWalkWin : 0u;
     if ((uint32_t)tid < depth - wlo) wwin[tid] = win[wlo + tid - lo];
   }
   __syncthreads();
   if (tid < 8) {
-    hdr->alive[tid] = alive[tid];
     hdr->A[tid] = A[tid];
     hdr->Aw[tid] = Aw[tid];
     hdr->R[tid] = R[tid];
-    hdr->slot[tid] = tb.lex_slots[(size_t)cfg.slot * kSlotWords + tid];
   }
+  if (tid < kSlotWords) hdr->slot[tid] = tb.lex_slots[(size_t)cfg.slot * kSlotWords + tid];
   if (tid == 0) {
     hdr->eos_ok = (uint32_t)eos_ok;
     if (eos_out) eos_out[row] = (uint8_t)eos_ok;
@@ -1041,6 +1072,9 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     hdr->slow_count = 0;
     hdr->wstat = 0;
     hdr->nonempty = 0;
+    hdr->slot_id = cfg.slot;
+    hdr->cls_base = tb.coff[cfg.q];
+    hdr->n_cls = tb.coff[cfg.q + 1] - tb.coff[cfg.q];
     hdr->pstat = overflow ? GRID_ROW_OVERFLOW : GRID_ROW_OK;
     hdr->valid = kRowValid;
   }
@@ -1136,7 +1170,8 @@ struct DfaView {  // lexer DFA by byte class (LDS copy or global)
   __device__ int next(int q, uint32_t c) const { return next_[q * C + c]; }
 };
 
-// Walks the bytes [i, n) of one spelling from lane state (ln, q, lx).
+// Walks the bytes [i, n) of one spelling from lane state (ln, q, lx); f is
+// the trailing flags of the last byte taken before i (1 if none).
 // byte_at(i) yields byte i, called once per i in increasing order.  The lanes
 // of a wave alternate between a scan phase (every lane that can takes its
 // next byte: a DFA step and the trailing class, all in LDS) and an emission
@@ -1149,7 +1184,7 @@ struct DfaView {  // lexer DFA by byte class (LDS copy or global)
 template <bool L, int MW, class ByteAt>
 __device__ __forceinline__ int walk_bytes(const RowCtx<L>& rc, Lane<MW>& ln, int q, LexState lx, uint32_t i,
                                           uint32_t n, ByteAt byte_at, const DfaView& step, mptr<L, uint16_t> ov,
-                                          int cap) {
+                                          int cap, uint32_t f) {
   const Tables& tb = *rc.tb;
   const bool track = rc.sl.restricted != 0;
   // trailing flags of a state: from the row's table while the lane's allowed
@@ -1158,7 +1193,7 @@ __device__ __forceinline__ int walk_bytes(const RowCtx<L>& rc, Lane<MW>& ln, int
   int status = 2;         // 2 running, else the result
   int pend = -1;          // byte class waiting for an emission
   uint32_t pend_b = 0;    // that byte
-  uint32_t f = 1;         // trailing flags after the last byte taken
+  // f: trailing flags after the last byte taken (the caller's, before any)
   for (;;) {
     for (;;) {  // scan phase
       const bool run = status == 2 && pend < 0 && i < n;
@@ -1201,96 +1236,6 @@ __device__ __forceinline__ int walk_bytes(const RowCtx<L>& rc, Lane<MW>& ln, int
   return status;
 }
 
-// Verdict of a lane whose spelling ends at most one lexeme, from the scan
-// summary word sc of (row's DFA state, spelling): the DFA steps were taken at
-// compile time, what is left is the parser side -- the ended lexeme's winner
-// and its shift, from the prologue's tables -- and the trailing check of the
-// last lexeme, which reads the lexicon only where a restricted terminal alone
-// keeps the lexeme viable.  ln and lx describe the lane after byte 0;
-// byte_at yields bytes 1, 2, ... in order.  1 allowed, 0 rejected.
-template <bool L, int MW, class ByteAt>
-__device__ __forceinline__ int summary_verdict(const RowCtx<L>& rc, Lane<MW>& ln, uint32_t sc, LexState lx,
-                                               uint32_t n, ByteAt& byte_at, mptr<L, uint16_t> ov, int cap) {
-  const Tables& tb = *rc.tb;
-  uint32_t i = 1;
-  const uint32_t p = scan_p_first(sc);
-  if (scan_ends(sc) == 1 && p > 0) {
-    // bytes 1 .. p-1 extend the pending lexeme; byte p ends it and starts the
-    // last lexeme
-    for (; i < p; ++i) {
-      const uint32_t b = byte_at(i);
-      if (lx.need) lex_push(tb, rc.sl, lx, b);
-    }
-    const int r = emit<L, MW>(rc, ln, ov, cap, (int)scan_q_first(sc), lx, kDead);  // mode 0: no simulation
-    if (r <= 0) return 0;
-    lx = LexState{byte_at(p), 1u, kNoLex, 1u};
-    i = p + 1;
-  }
-  const int qf = (int)scan_q_end(sc);
-  const uint8_t* ctab = ln.mode == 0 ? rc.clsA : (ln.mode == 1 && ln.t1 == rc.winner ? rc.clsW : nullptr);
-  const uint32_t f = ctab ? (uint32_t)ctab[qf] : trail_flags<MW>(rc.tv, ln.acur, qf);
-  if (f & 1u) return 1;
-  if (!(f & 2u)) return 0;
-  // only restricted terminals remain (live sets shrink along a lexeme, so the
-  // lexicon state was tracked from the lexeme's first byte): ask the lexicon
-  for (; i < n; ++i) lex_push(tb, rc.sl, lx, byte_at(i));
-  return trail_lex<MW>(rc.tv, ln.acur, qf, lex_flags_now(tb, rc.sl, lx)) ? 1 : 0;
-}
-
-// -------------------------------------------------------------------- walk
-struct WalkLds {  // byte offsets into dynamic LDS
-  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, live, range, lanes, umask, upre, rows, total;
-  uint32_t block;  // bytes per resident row: header, trailing-flag tables, stack window
-  int group;       // rows per group
-  ParseLds pl;
-};
-
-// blocks: the walk's grid size (a group's items per workgroup stay within
-// kMaxItems)
-__host__ __device__ inline WalkLds walk_lds(const Tables& tb, int mw, int B, int blocks) {
-  WalkLds w;
-  uint32_t o = 0;
-  w.dfa = o;
-  o += pad16((uint32_t)(tb.S * tb.C * 2));
-  w.bcls = o;
-  o += 256;
-  w.tinfo = o;
-  o += 256 * 4;
-  w.I = o;
-  o += 32;
-  w.acc_off = o;
-  o += pad16((uint32_t)(tb.S + 1) * 4);
-  w.acc_list = o;
-  o += pad16((uint32_t)tb.n_acc);
-  w.parse = o;
-  w.pl = parse_lds(tb, o);
-  o += w.pl.total;
-  w.live = o;
-  o += pad16((uint32_t)(tb.S * mw * 4));
-  w.range = o;
-  o += pad16((uint32_t)((tb.U + 63) / 64) * 2);
-  w.lanes = o;
-  o += kWalkThreads * kFastLane * 2;
-  w.umask = o;  // per work item: its undecided lanes
-  o += kMaxItems * 8;
-  w.upre = o;   // prefix counts of undecided lanes over the items
-  o += (kMaxItems + 4) * 4;
-  // as many rows as fit beside the static LDS (counters), at most kRowGroup
-  // and B, with at most kMaxItems items per workgroup
-  const uint32_t fixed = o + 64;
-  w.block = (uint32_t)row_layout(tb.T, tb.U, tb.S).block;
-  const int nsub = (tb.U + kSub - 1) / kSub;
-  int g = kRowGroup < B ? kRowGroup : B;
-  while (g > 1 && (fixed + w.block * (uint32_t)g > kWalkLdsMax ||
-                   (long long)g * nsub > (long long)kMaxItems * blocks))
-    --g;
-  w.group = g;
-  w.rows = o;
-  o += w.block * (uint32_t)g;
-  w.total = o;
-  return w;
-}
-
 // Bytes 1, 2, ... of one spelling, called in that order: a 64-bit window
 // holds the next bytes, taken from the record (bytes 0..7), the tail chunk
 // fetched with it (bytes 8..23), then one 16-byte load per overflow chunk.
@@ -1316,94 +1261,416 @@ struct SpellBytes {
   }
 };
 
-// Some first byte in [lo, hi] opens a token (bit set in the 256-bit mask).
-__device__ inline bool any_in_range(const uint32_t* m, uint32_t lo, uint32_t hi) {
-  for (uint32_t w = lo >> 5; w <= (hi >> 5); ++w) {
-    uint32_t bits = m[w];
-    if (w == (lo >> 5)) bits &= 0xFFFFFFFFu << (lo & 31);
-    if (w == (hi >> 5)) bits &= 0xFFFFFFFFu >> (31 - (hi & 31));
-    if (bits) return true;
+// ----------------------------------------------------------- class verdicts
+// Codes of a class for a row (2 bits per class in the row's verdict table).
+// kVerdictLexicon: the verdict depends on the schema lexicon (a lexeme's
+// winner or the trailing lexeme's viability), so each token of the class is
+// judged again with its own lexemes' lexicon flags.
+constexpr uint32_t kVerdictReject = 0, kVerdictAllow = 1, kVerdictWalk = 2, kVerdictLexicon = 3;
+
+// Answers of a lexicon policy besides flags: the question is open (the
+// verdict kernel, which has no token bytes), or the lexeme is out of reach
+// of the lookup tables (the token takes the byte walk).
+constexpr uint32_t kLexOpen = 0xFFFFFFFFu, kLexOut = 0xFFFFFFFEu;
+
+// Verdict of one lexeme-program class for a row.  The lexemes the token
+// ends are judged in order against the allowed set the parser has at that
+// point: A(sigma) before any shift, the prologue's allowed set after the
+// first shift (a2, a2_stride words per terminal), unknown after a second
+// one.  Each ended lexeme's winner is the first accept-list entry (priority
+// order) that is ignored or allowed and, for a restricted terminal, whose
+// category has the lexeme as a word (section 2, L3); the trailing lexeme
+// (state after the last byte) must still complete to an allowed or ignored
+// terminal, a restricted one only where the lexeme prefixes a word of its
+// category (Definition 2).  An ignored unrestricted terminal live there
+// accepts it under any stack.  Lexicon flags come from lex.word(i) (lexeme
+// i) and lex.trail(); a lexeme after two shifts and a token with more
+// recorded ends than the record holds are left to the byte walk.
+template <int MW, class Lex>
+__device__ __forceinline__ uint32_t class_verdict(const RowHeader& h, const uint32_t* I, const uint32_t* live,
+                                                  const uint32_t* tinfo, const uint32_t* acc_off,
+                                                  const uint8_t* acc_list, const uint32_t* a2, int a2_stride,
+                                                  uint4 rec, Lex& lex) {
+  const uint32_t w0 = rec.x;
+  if (w0 & kClassReject) return kVerdictReject;
+  if (w0 & kClassWalk) return kVerdictWalk;
+  const uint32_t ends = w0 & kClassEndsMask;
+  const uint32_t qe[kClassEnds] = {rec.y >> 16, rec.z & 0xFFFFu, rec.z >> 16};
+  int sel = -1;  // allowed set now: -1 A(sigma), t >= 0 after shifting t, -2 unknown
+  const uint32_t nchk = ends > (uint32_t)kClassEnds ? (uint32_t)kClassEnds : ends;
+  for (uint32_t i = 0; i < nchk; ++i) {
+    int t = -1;
+    if (i == 0 && (w0 & kClassP0)) {  // byte 0 ends the pending lexeme: the prologue's winner
+      if (h.wkind == 0) return kVerdictReject;
+      if (h.wkind == 1) continue;
+      t = h.winner;
+    } else {
+      if (sel == -2) return kVerdictWalk;
+      const uint32_t q = qe[i];
+      uint32_t wf = kLexOpen;  // the lexeme's lexicon flags, asked for at most once
+      for (uint32_t j = acc_off[q]; j < acc_off[q + 1]; ++j) {
+        const int c = acc_list[j];
+        const bool ok = bit_of(I, c) || (sel == -1 ? bit_of(h.A, c) : bit_of(a2 + sel * a2_stride, c));
+        if (!ok) continue;
+        if (bit_of(h.R, c)) {
+          if (wf == kLexOpen) wf = lex.word(i);
+          if (wf == kLexOpen) return kVerdictLexicon;
+          if (wf == kLexOut) return kVerdictWalk;
+          if (!((wf >> (8 + ((tinfo[c] >> 8) & 7u))) & 1u)) continue;
+        }
+        t = c;
+        break;
+      }
+      if (t < 0) return kVerdictReject;
+      if (bit_of(I, t)) continue;
+    }
+    sel = sel == -1 ? t : -2;
   }
-  return false;
+  if (ends > (uint32_t)kClassEnds) return kVerdictWalk;
+  const uint32_t* lv = live + (size_t)(rec.y & 0xFFFFu) * MW;
+  uint32_t unres = 0, res = 0, ign = 0;
+  uint32_t rw[MW];  // restricted terminals that keep the trailing lexeme viable
+#pragma unroll
+  for (int w = 0; w < MW; ++w) {
+    const uint32_t acur = sel == -1 ? h.A[w] : (sel >= 0 ? a2[sel * a2_stride + w] : 0u);
+    const uint32_t bits = lv[w] & (acur | I[w]);
+    unres |= bits & ~h.R[w];
+    rw[w] = bits & h.R[w];
+    res |= rw[w];
+    ign |= lv[w] & I[w] & ~h.R[w];
+  }
+  if (ign || (sel != -2 && unres)) return kVerdictAllow;
+  if (sel == -2) return kVerdictWalk;
+  if (!res) return kVerdictReject;
+  const uint32_t pf = lex.trail();
+  if (pf == kLexOpen) return kVerdictLexicon;
+  if (pf == kLexOut) return kVerdictWalk;
+  uint32_t cats = 0;
+#pragma unroll
+  for (int w = 0; w < MW; ++w) {
+    uint32_t r = rw[w];
+    while (r) {
+      cats |= 1u << ((tinfo[w * 32 + __ffs(r) - 1] >> 8) & 7u);
+      r &= r - 1;
+    }
+  }
+  return (pf & cats) ? kVerdictAllow : kVerdictReject;
 }
 
+// Lexicon policy of the verdict kernel: it has no token bytes.
+struct LexOpen {
+  __device__ uint32_t word(uint32_t) { return kLexOpen; }
+  __device__ uint32_t trail() { return kLexOpen; }
+};
+
+// A lexeme of the class record that starts in the start state at byte 0 or 1
+// of the token: the token-flag table (GRID_ART_LEX_TOKEN) answers for it.
+// Its start offset, or -1.  Lexeme 0 and a trailing lexeme after no end hold
+// the pending bytes, so they qualify only when those are empty.
+__device__ __forceinline__ int covered_start(uint32_t pos, uint32_t i, bool pending_empty) {
+  if (i == 0) return pending_empty ? 0 : -1;
+  const uint32_t o = (pos >> (8 * (i - 1))) & 0xFFu;
+  return o <= 1u ? (int)o : -1;
+}
+
+// Lexicon policy that answers the class's first lexicon question with "no
+// flags" and records it (kind, start offset in the token, whether the lexeme
+// holds the pending bytes); it notes whether a second question is asked.
+struct LexNo {
+  uint32_t pos, ends;
+  bool pending_empty;
+  int kind;           // first question: -1 none yet, 0 trailing prefix, 1 word
+  int start;          // its start offset in the token, or -1
+  bool pending;       // its lexeme holds the pending bytes
+  bool second;        // a second question was asked
+  __device__ void first(uint32_t i, int k) {
+    kind = k;
+    pending = i == 0 && !pending_empty;
+    start = covered_start(pos, i, pending_empty);
+  }
+  __device__ uint32_t word(uint32_t i) {
+    if (kind >= 0) second = true;
+    else first(i, 1);
+    return 0u;
+  }
+  __device__ uint32_t trail() {
+    if (kind >= 0 || ends > (uint32_t)kClassEnds) second = true;
+    else first(ends, 0);
+    return 0u;
+  }
+};
+
+// Shortcut of a class the lexicon decides: its verdict v_no when the answer
+// to its first lexicon question is "no flags", valid when that answer leads
+// to no second question.  The stream kernel knows the answer is "no flags"
+// when the question's lexeme starts with the pending bytes and the token's
+// first byte does not continue them in the lexicon (the row's cont table), or
+// when the lexeme starts at token byte 0 or 1 in the start state and the
+// token-flag entry has no flags there.  Encoded as 3 (the class code) |
+// kind << 2 (0 pending bytes, 1 trailing prefix at o, 2 word at o) | o << 4 |
+// v_no << 5 | valid << 7.
+constexpr uint32_t kNoValid = 1u << 7;
+template <int MW>
+__device__ __forceinline__ uint32_t class_shortcut(const RowHeader& h, const uint32_t* I, const uint32_t* live,
+                                                   const uint32_t* tinfo, const uint32_t* acc_off,
+                                                   const uint8_t* acc_list, const uint32_t* a2, uint4 rec) {
+  LexNo ln{rec.w, rec.x & kClassEndsMask, h.rem_len == 0, -1, -1, false, false};
+  const uint32_t v = class_verdict<MW>(h, I, live, tinfo, acc_off, acc_list, a2, MW, rec, ln);
+  if (ln.kind < 0 || ln.second || v == kVerdictLexicon) return kVerdictLexicon;
+  if (ln.pending) return kVerdictLexicon | v << 5 | kNoValid;
+  if (ln.start < 0) return kVerdictLexicon;
+  return kVerdictLexicon | (ln.kind == 0 ? 1u : 2u) << 2 | (uint32_t)ln.start << 4 | v << 5 | kNoValid;
+}
+
+// Workgroups (row, y): the verdicts of the row's classes, four per thread
+// (one byte of the 2-bit verdict table), workgroup y taking every
+// gridDim.y-th group of kBlock of them; a class the lexicon decides also gets
+// its shortcut byte.  The row's allowed sets, the accept lists and
+// the live sets are staged in LDS first.
+template <int MW>
+__global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __restrict__ ws, size_t rbytes) {
+  extern __shared__ __align__(16) uint8_t vlds[];
+  __shared__ RowHeader h;
+  __shared__ uint32_t I_s[8];
+  const int tid = threadIdx.x;
+  uint8_t* rw = ws + kWsHead + (size_t)blockIdx.x * rbytes;
+  if (tid < (int)(sizeof(RowHeader) / 4)) ((uint32_t*)&h)[tid] = ((const uint32_t*)rw)[tid];
+  __syncthreads();
+  const uint32_t ngroups = (h.n_cls + 3u) / 4u;  // four classes per thread
+  if (h.valid != kRowValid || blockIdx.y * (uint32_t)kBlock >= ngroups) return;  // uniform
+  const RowLayout RL = row_layout(tb);
+  uint32_t* live_s = (uint32_t*)vlds;
+  uint32_t* a2_s = live_s + tb.S * MW;
+  uint32_t* tinfo_s = a2_s + tb.T * MW;
+  uint32_t* acc_off_s = tinfo_s + tb.T;
+  uint8_t* acc_list_s = (uint8_t*)(acc_off_s + tb.S + 1);
+  const uint32_t* a2g = (const uint32_t*)(rw + RL.a2);
+  for (int i = tid; i < tb.S * MW; i += kBlock) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
+  for (int i = tid; i < tb.T * MW; i += kBlock) a2_s[i] = a2g[(i / MW) * 8 + i % MW];
+  for (int i = tid; i < tb.T; i += kBlock) tinfo_s[i] = tb.term_info[i];
+  for (int i = tid; i <= tb.S; i += kBlock) acc_off_s[i] = tb.acc_off[i];
+  for (int i = tid; i < tb.n_acc; i += kBlock) acc_list_s[i] = tb.acc_list[i];
+  if (tid < 8) {
+    uint32_t iw = 0;
+    for (int j = 0; j < 32; ++j) {
+      const int t = tid * 32 + j;
+      if (t < tb.T && (tb.term_info[t] & 1u)) iw |= 1u << j;
+    }
+    I_s[tid] = iw;
+  }
+  __syncthreads();
+  uint8_t* vc = rw + RL.vcode;
+  uint8_t* vr = rw + RL.vrule;
+  const uint4* rec = tb.crec + h.cls_base;
+  for (uint32_t j = blockIdx.y * kBlock + tid; j < ngroups; j += gridDim.y * kBlock) {
+    uint4 r[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) r[k] = 4 * j + k < h.n_cls ? rec[4 * j + k] : make_uint4(kClassReject, 0, 0, 0);
+    uint32_t code = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      LexOpen lex;
+      const uint32_t v = class_verdict<MW>(h, I_s, live_s, tinfo_s, acc_off_s, acc_list_s, a2_s, MW, r[k], lex);
+      code |= v << (2 * k);
+      if (v == kVerdictLexicon)
+        vr[4 * j + k] = (uint8_t)class_shortcut<MW>(h, I_s, live_s, tinfo_s, acc_off_s, acc_list_s, a2_s, r[k]);
+    }
+    vc[j] = (uint8_t)code;
+  }
+}
+
+__host__ __device__ inline uint32_t verdict_lds(const Tables& tb, int mw) {
+  return pad16((uint32_t)(tb.S + tb.T) * (uint32_t)mw * 4u + (uint32_t)(tb.T + tb.S + 1) * 4u + (uint32_t)tb.n_acc);
+}
+
+// ------------------------------------------------------------------ stream
+// The mask in token-id order straight from the class map.  Workgroup i runs
+// on XCD i mod 8 and covers one row and kStreamChunks consecutive 64-id
+// chunks inside that XCD's eighth of the vocabulary, so each XCD's L2 holds
+// one eighth of every lexer state's class map.  A wave turns 64 ids into two
+// mask words with one ballot (class verdict "allow", or the EOS id when the
+// row may end).  A token whose class the lexicon decides takes the class's
+// shortcut verdict when the answer to the class's first lexicon question is
+// "no flags" for it (from its first byte and the row's continuation table, or
+// from its token-flag entry); otherwise it is appended to the row's lexicon
+// list with its class.  Tokens whose class needs the byte
+// walk go to the walk list (one atomic per list, workgroup and round).  Rows
+// served from the mask cache are skipped; rows with a bad configuration get
+// zero words.
+constexpr int kStreamWaves = kBlock / 64;
+constexpr int kStreamUnroll = 4;   // chunks per wave in flight
+constexpr int kStreamRounds = 4;
+constexpr int kStreamChunks = kStreamWaves * kStreamUnroll * kStreamRounds;
+
+__host__ __device__ inline int stream_slices(int V) { return ((V + 63) / 64 + 7) / 8; }
+__host__ __device__ inline int stream_groups(int V) { return (stream_slices(V) + kStreamChunks - 1) / kStreamChunks; }
+
+__global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __restrict__ mask,
+                                                        uint8_t* __restrict__ ws, size_t rbytes, int B) {
+  extern __shared__ __align__(16) uint32_t vc_s[];
+  __shared__ uint32_t wtot[2][kStreamWaves];
+  __shared__ uint32_t base_s[2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int x = (int)(blockIdx.x & 7u);
+  const int g = (int)(blockIdx.x >> 3);
+  const int row = g % B, k = g / B;
+  const int nch = (tb.V + 63) / 64, cps = stream_slices(tb.V);
+  const int c_lo = x * cps + k * kStreamChunks;
+  const int c_hi = min(min(c_lo + kStreamChunks, (x + 1) * cps), nch);
+  if (c_lo >= c_hi) return;  // uniform
+  uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
+  RowHeader* hdr = (RowHeader*)rw;
+  const uint32_t valid = hdr->valid;
+  if (valid == kRowCached) return;
+  uint32_t* mrow = mask + (size_t)row * tb.W;
+  if (valid != kRowValid) {  // bad configuration: an empty row
+    for (int c = c_lo + wave; c < c_hi; c += kStreamWaves)
+      if (lane < 2 && 2 * c + lane < tb.W) mrow[2 * c + lane] = 0u;
+    return;
+  }
+  const RowLayout RL = row_layout(tb);
+  const uint32_t q = hdr->q, n_cls = hdr->n_cls;
+  const int eos = hdr->eos_ok ? tb.eos_id : -1;
+  {
+    const uint32_t* vg = (const uint32_t*)(rw + RL.vcode);
+    const uint32_t nw = (n_cls + 15u) / 16u;
+    for (uint32_t i = tid; i < nw; i += kBlock) vc_s[i] = vg[i];
+  }
+  const uint16_t* cm = tb.cmap + (size_t)q * tb.V;
+  const uint32_t* tflags = tb.lex_token + (size_t)hdr->slot_id * tb.V;
+  const uint8_t* vrule = rw + RL.vrule;
+  uint32_t cont[8];
+#pragma unroll
+  for (int w = 0; w < 8; ++w) cont[w] = hdr->cont[w];
+  uint2* lexl = (uint2*)(rw + RL.lexl);
+  uint32_t* walkl = (uint32_t*)(rw + RL.walkl);
+  const uint64_t below = (1ull << lane) - 1ull;
+  bool any = false;
+  __syncthreads();
+  for (int rd = 0; rd < kStreamRounds; ++rd) {
+    const int c0 = c_lo + rd * kStreamWaves * kStreamUnroll + wave;
+    uint32_t cls[kStreamUnroll];
+#pragma unroll
+    for (int j = 0; j < kStreamUnroll; ++j) {
+      const int c = c0 + j * kStreamWaves;
+      const int id = c * 64 + lane;
+      cls[j] = (c < c_hi && id < tb.V) ? (uint32_t)cm[id] : 0u;
+    }
+    uint64_t lexb[kStreamUnroll], walkb[kStreamUnroll];
+    uint32_t nlex = 0, nwalk = 0;
+#pragma unroll
+    for (int j = 0; j < kStreamUnroll; ++j) {
+      const int c = c0 + j * kStreamWaves;
+      lexb[j] = walkb[j] = 0;
+      if (c >= c_hi) continue;  // uniform across the wave
+      const int id = c * 64 + lane;
+      uint32_t code = (vc_s[cls[j] >> 4] >> ((cls[j] & 15u) * 2u)) & 3u;
+      if (__ballot(code == kVerdictLexicon)) {  // uniform: lexicon shortcuts
+        if (code == kVerdictLexicon && id < tb.V) {
+          const uint32_t sc = vrule[cls[j]];
+          if (sc & kNoValid) {
+            const uint32_t kind = (sc >> 2) & 3u;
+            bool no;
+            if (kind == 0) {
+              const uint32_t b = tb.id_first[id];
+              no = !((cont[b >> 5] >> (b & 31u)) & 1u);
+            } else {
+              no = ((tflags[id] >> (16 * ((sc >> 4) & 1u) + (kind == 2 ? 8u : 0u))) & 0xFFu) == 0u;
+            }
+            if (no) code = (sc >> 5) & 3u;
+          }
+        }
+      }
+      const uint64_t al = __ballot(code == kVerdictAllow || id == eos);
+      lexb[j] = __ballot(code == kVerdictLexicon && id < tb.V);
+      walkb[j] = __ballot(code == kVerdictWalk && id < tb.V);
+      nlex += (uint32_t)__popcll(lexb[j]);
+      nwalk += (uint32_t)__popcll(walkb[j]);
+      any = any || al != 0;
+      if (lane < 2 && 2 * c + lane < tb.W) mrow[2 * c + lane] = (uint32_t)(al >> (32 * lane));
+    }
+    // this round's list entries: one atomic per list for the workgroup
+    if (lane == 0) {
+      wtot[0][wave] = nlex;
+      wtot[1][wave] = nwalk;
+    }
+    __syncthreads();
+    if (tid < 2) {
+      uint32_t tot = 0;
+      for (int w = 0; w < kStreamWaves; ++w) tot += wtot[tid][w];
+      base_s[tid] = tot ? atomicAdd(tid == 0 ? &hdr->res_count : &hdr->walk_count, tot) : 0u;
+    }
+    __syncthreads();
+    uint32_t pl = base_s[0], pw = base_s[1];
+    for (int w = 0; w < wave; ++w) {
+      pl += wtot[0][w];
+      pw += wtot[1][w];
+    }
+    __syncthreads();  // wtot and base_s are reused by the next round
+    if (nlex == 0 && nwalk == 0) continue;  // uniform across the wave
+#pragma unroll
+    for (int j = 0; j < kStreamUnroll; ++j) {
+      const uint32_t id = (uint32_t)((c0 + j * kStreamWaves) * 64 + lane);
+      if ((lexb[j] >> lane) & 1ull) lexl[pl + (uint32_t)__popcll(lexb[j] & below)] = make_uint2(id, cls[j]);
+      if ((walkb[j] >> lane) & 1ull) walkl[pw + (uint32_t)__popcll(walkb[j] & below)] = id;
+      pl += (uint32_t)__popcll(lexb[j]);
+      pw += (uint32_t)__popcll(walkb[j]);
+    }
+  }
+  if (lane == 0 && any) hdr->nonempty = 1u;
+}
+
+// ----------------------------------------------------------------- residue
+// The next value of an LDS counter for the whole wave (one atomic).
 __device__ inline int wave_grab(int* ctr) {
   int v = 0;
   if ((threadIdx.x & 63) == 0) v = atomicAdd(ctr, 1);
   return __builtin_amdgcn_readfirstlane(v);
 }
 
-// Lane verdict from the scan summary word alone, without the spelling's
-// bytes: 1 allowed, 0 rejected, 2 undecided (the lexicon must see the bytes,
-// or the spelling ends two or more lexemes).  Covers a spelling that stays in
-// the pending lexeme, one whose first byte ends the pending lexeme, and one
-// that ends it later with a winner the lexicon does not restrict; the last
-// lexeme is then judged by its trailing flags under the allowed set it sees.
-template <int MW>
-__device__ __forceinline__ int fast_verdict(const RowHeader& h, const uint8_t* clsA, const uint8_t* clsW,
-                                            const uint32_t* I_s, const uint32_t* acc_off, const uint8_t* acc_list,
-                                            const TermView& tv, const uint32_t* a2, uint32_t sc) {
-  if (sc & kScanReject) return 0;
-  const uint32_t ends = scan_ends(sc);
-  if (ends >= 2) return 2;
-  const int qf = (int)scan_q_end(sc);
-  const uint32_t p = scan_p_first(sc);
-  int sel;  // -1 A(sigma), -2 after the winner's shift, >= 0 after shifting that terminal
-  if (ends == 0) {
-    sel = -1;
-  } else if (p == 0) {  // byte 0 ends the pending lexeme: its winner, from the prologue
-    if (h.wkind == 0) return 0;
-    sel = h.wkind == 1 ? -1 : -2;
-  } else {  // bytes 0..p-1 extend the pending lexeme, byte p ends it in q_d
-    const int qd = (int)scan_q_first(sc);
-    int t = -1;
-    for (uint32_t j = acc_off[qd]; j < acc_off[qd + 1]; ++j) {
-      const int c = acc_list[j];
-      if (bit_of(I_s, c)) {
-        t = c;
-        break;
-      }
-      if (!bit_of(h.A, c)) continue;
-      if (bit_of(h.R, c)) return 2;  // the lexicon decides this candidate
-      t = c;
-      break;
-    }
-    if (t < 0) return 0;
-    sel = bit_of(I_s, t) ? -1 : (t == h.winner ? -2 : t);
-  }
-  uint32_t f;
-  if (sel == -1) {
-    f = clsA[qf];
-  } else if (sel == -2) {
-    f = clsW[qf];
-  } else {
-    uint32_t acur[MW];
-#pragma unroll
-    for (int w = 0; w < MW; ++w) acur[w] = a2[sel * 8 + w];
-    f = trail_flags<MW>(tv, acur, qf);
-  }
-  return (f & 1u) ? 1 : ((f & 2u) ? 2 : 0);
+struct ResLds {  // byte offsets into dynamic LDS
+  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, live, lanes, pre, rows, total;
+  uint32_t block;  // bytes per resident row: header, trailing-flag tables, stack window
+  int group;       // rows per group
+  ParseLds pl;
+};
+
+__host__ __device__ inline ResLds res_lds(const Tables& tb, int mw, int B) {
+  ResLds w;
+  uint32_t o = 0;
+  w.dfa = o;
+  o += pad16((uint32_t)(tb.S * tb.C * 2));
+  w.bcls = o;
+  o += 256;
+  w.tinfo = o;
+  o += 256 * 4;
+  w.I = o;
+  o += 32;
+  w.acc_off = o;
+  o += pad16((uint32_t)(tb.S + 1) * 4);
+  w.acc_list = o;
+  o += pad16((uint32_t)tb.n_acc);
+  w.parse = o;
+  w.pl = parse_lds(tb, o);
+  o += w.pl.total;
+  w.live = o;
+  o += pad16((uint32_t)(tb.S * mw * 4));
+  w.lanes = o;
+  o += kWalkThreads * kFastLane * 2;
+  w.pre = o;  // walk chunk prefix counts of the group's rows
+  o += (kRowGroup + 4) * 4;
+  const uint32_t fixed = o + 64;
+  w.block = (uint32_t)row_layout(tb).block;
+  int g = kRowGroup < B ? kRowGroup : B;
+  while (g > 1 && fixed + w.block * (uint32_t)g > kWalkLdsMax) --g;
+  w.group = g;
+  w.rows = o;
+  o += w.block * (uint32_t)g;
+  w.total = o;
+  return w;
 }
 
-// The rank-th set bit of m (rank < popcount(m)).
-__device__ inline int nth_set_bit(uint64_t m, int rank) {
-  int pos = 0;
-#pragma unroll
-  for (int w = 32; w >= 1; w >>= 1) {
-    const uint64_t low = m & ((1ull << w) - 1ull);
-    const int c = __popcll(low);
-    if (rank >= c) {
-      rank -= c;
-      m >>= w;
-      pos += w;
-    } else {
-      m = low;
-    }
-  }
-  return pos;
-}
-
-// Everything the walk's lanes share about the grammar (pointers into LDS).
+// Everything the residue lanes share about the grammar (pointers into LDS).
 template <int MW>
 struct WalkShared {
   const Tables* tb;
@@ -1417,18 +1684,19 @@ struct WalkShared {
   const uint16_t* pool;
 };
 
-// Verdict of an undecided lane (see fast_verdict): the spelling's bytes, the
-// lane's state after byte 0, then the lexicon checks of the summary path or
-// the byte-by-byte walk from the first lexeme end.  A lane whose stack area
-// is too small hands its spelling to the slow path.  1 allowed, 0 rejected
-// or handed over.
+// Verdict of one token left to the byte walk: byte 0 (continuing the pending
+// lexeme, or ending it with the prologue's winner and starting a new one),
+// then the byte-by-byte walk of the rest with emissions, overlay shifts and
+// lexicon checks.  A lane whose stack area is too small hands its token to
+// the slow path.  1 allowed, 0 rejected or handed over.
 template <int MW>
-__device__ __forceinline__ int undecided_lane(const WalkShared<MW>& sh, const RowHeader& h, const uint8_t* rowblk,
-                                              uint8_t* rw, const RowLayout& RL, int u, uint32_t sc,
-                                              mptr<true, uint16_t> lane_area) {
+__device__ __forceinline__ int residue_lane(const WalkShared<MW>& sh, const RowHeader& h, const uint8_t* rowblk,
+                                            uint8_t* rw, const RowLayout& RL, int id,
+                                            mptr<true, uint16_t> lane_area) {
   const Tables& tb = *sh.tb;
   const uint8_t* clsA = rowblk + sizeof(RowHeader);
   const uint8_t* clsW = clsA + pad16((uint32_t)tb.S);
+  const uint32_t u = tb.spell_of_id[id];
   const uint4 rk = tb.spell_rec[u];
   const uint4 tl = tb.spell_tail[u];
   const uint32_t n = rk.w & 0xFFu;
@@ -1443,6 +1711,8 @@ __device__ __forceinline__ int undecided_lane(const WalkShared<MW>& sh, const Ro
   sl.nodes = h.slot[4];
   sl.pbase = h.slot[5];
   sl.pmask = h.slot[6];
+  sl.sbase = h.slot[7];
+  sl.smask = h.slot[8];
   RowCtx<true> rc;
   rc.tb = &tb;
   rc.pt = sh.pt;
@@ -1482,243 +1752,298 @@ __device__ __forceinline__ int undecided_lane(const WalkShared<MW>& sh, const Ro
   }
 #pragma unroll
   for (int w = 0; w < MW; ++w) ln.acur[w] = ln.mode == 1 ? h.Aw[w] : h.A[w];
-  if (dead) return 0;
-  lx.need = sl.restricted != 0 && (ct[q1] & 2u) ? 1u : 0u;
+  const uint32_t f0 = dead ? 0u : (uint32_t)ct[q1];
+  if (f0 == 0) return 0;  // byte 0 leaves no allowed or ignored terminal completable
+  lx.need = sl.restricted != 0 && (f0 & 2u) ? 1u : 0u;
   lx.node = lx.need && lx.len > 8 ? lex_child(tb, sl, h.lexnode, b0) : kNoLex;
   SpellBytes byte_at;
   byte_at.win = hb >> 8;
   byte_at.lo0 = (uint64_t)tl.x | (uint64_t)tl.y << 32;
   byte_at.hi = (uint64_t)tl.z | (uint64_t)tl.w << 32;
   byte_at.ovf = tb.spell_tail + (rk.w >> 8);
-  int ok = 0;
-  bool scan = false;
-  if (scan_ends(sc) < 2)
-    ok = summary_verdict<true, MW>(rc, ln, sc, lx, n, byte_at, lane_area, kFastLane);
-  else
-    scan = true;
-  if (scan) {
-    int qs = q1;
-    uint32_t is = 1;
-    const uint32_t p = scan_p_first(sc);
-    if (p > 0) {  // bytes 1 .. p-1 only extend the pending lexeme
-      for (uint32_t i = 1; i < p; ++i) {
-        const uint32_t b = byte_at(i);
-        if (lx.need) lex_push(tb, sl, lx, b);
-      }
-      qs = (int)scan_q_first(sc);
-      is = p;
-    }
-    ok = walk_bytes<true, MW>(rc, ln, qs, lx, is, n, byte_at, sh.step, lane_area, kFastLane);
-  }
+  int ok = walk_bytes<true, MW>(rc, ln, q1, lx, 1u, n, byte_at, sh.step, lane_area, kFastLane, f0);
   if (ok < 0) {  // the lane's stack area is too small: hand over
     RowHeader* gh = (RowHeader*)rw;
     const uint32_t slot = atomicAdd(&gh->slow_count, 1u);
-    if (slot < (uint32_t)kSlowCap) ((uint32_t*)(rw + RL.slow))[slot] = (uint32_t)u;
+    if (slot < (uint32_t)kSlowCap) ((uint32_t*)(rw + RL.slow))[slot] = (uint32_t)id;
     else atomicOr(&gh->wstat, GRID_ROW_OVERFLOW);
     ok = 0;
   }
   return ok;
 }
 
+// Bytes [s, s + 8) of the 24-byte window b0 b1 b2 (zero beyond it).
+__device__ __forceinline__ uint64_t window8(uint64_t b0, uint64_t b1, uint64_t b2, uint32_t s) {
+  const uint32_t w = s >> 3, sh = (s & 7u) * 8u;
+  const uint64_t lo = w == 0 ? b0 : (w == 1 ? b1 : (w == 2 ? b2 : 0ull));
+  const uint64_t hi = w == 0 ? b1 : (w == 1 ? b2 : 0ull);
+  return sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
+}
+
+// Lexicon policy of a token judged with its own bytes: lexeme i of the
+// class record (the pending bytes and the token's bytes before end 0, or the
+// bytes between ends i-1 and i) and the trailing lexeme.  A lexeme starting
+// in the start state at byte 0 or 1 is answered by the token-flag entry tf;
+// others are looked up in the prefix and stride tables, and one that does not
+// lie in the token's first 24 bytes is out of reach.  The pending bytes are
+// known up to 8; beyond that the lexeme continues from the pending lexeme's
+// trie node.  Plain scalar members only, so the policy lives in registers.
+struct LexLane {
+  const Tables* tb;
+  Slot sl;
+  uint64_t b0, b1, b2;  // token bytes 0..23, zero padded
+  uint32_t n;           // token length
+  uint32_t ends;        // lexeme ends (kClassMore: more than recorded)
+  uint32_t pos;         // byte indices of ends 0, 1, 2 (8 bits each)
+  uint64_t rem;         // pending bytes (first 8)
+  uint32_t rem_len, lexnode;
+  uint32_t tf;          // token-flag entry
+  __device__ __forceinline__ uint32_t end_at(uint32_t i) const { return (pos >> (8 * i)) & 0xFFu; }
+  __device__ __forceinline__ uint32_t span(uint32_t o, uint32_t e, bool pending) const {
+    if (e > 24) return kLexOut;
+    if (pending && rem_len > 0) {
+      if (rem_len > 8) {  // continue from the pending lexeme's node
+        uint32_t node = lexnode;
+        for (uint32_t i = 0; i < e && node != kNoLex; ++i)
+          node = lex_child(*tb, sl, node, (uint32_t)(window8(b0, b1, b2, i) & 0xFFu));
+        return lex_flags_of(*tb, sl, node);
+      }
+      const uint32_t len = rem_len + e;
+      if (len > 24) return kLexOut;
+      const uint32_t s = 8u * rem_len;  // 8..64 bits: the token's bytes move up by rem_len
+      const uint64_t c0 = rem | (s < 64 ? b0 << s : 0ull);
+      const uint64_t c1 = (b0 >> (64 - s)) | (s < 64 ? b1 << s : 0ull);
+      const uint64_t c2 = (b1 >> (64 - s)) | (s < 64 ? b2 << s : 0ull);
+      return lex_flags_bytes(*tb, sl, c0, c1, c2, len);
+    }
+    return lex_flags_bytes(*tb, sl, window8(b0, b1, b2, o), window8(b0, b1, b2, o + 8), window8(b0, b1, b2, o + 16),
+                           e - o);
+  }
+  __device__ __forceinline__ uint32_t word(uint32_t i) const {
+    const int o = covered_start(pos, i, rem_len == 0);
+    if (o >= 0) return ((tf >> (16 * o + 8)) & 0xFFu) << 8;
+    return i == 0 ? span(0, end_at(0), true) : span(end_at(i - 1), end_at(i), false);
+  }
+  __device__ __forceinline__ uint32_t trail() const {
+    if (ends > (uint32_t)kClassEnds) return kLexOut;
+    const int o = covered_start(pos, ends, rem_len == 0);
+    if (o >= 0) return (tf >> (16 * o)) & 0xFFu;
+    return ends == 0 ? span(0, n, true) : span(end_at(ends - 1), n, false);
+  }
+};
+
+// Workgroups (x, y): row group y (kRowGroup rows) and every gridDim.x-th
+// share of the group's lexicon lists, concatenated, kLexPer (token, class)
+// entries per thread at a time -- so one long list is spread over all
+// workgroups.  Each token's class verdict is taken again with the token's
+// own lexemes' lexicon flags (token-flag table, prefix and stride tables);
+// tokens whose lexemes are out of the tables' reach are appended to the walk
+// list.  The accept lists, live sets and terminal info are staged in LDS;
+// row headers and the allowed sets after one shift are read from the
+// workspace.
+constexpr int kLexPer = 2;
+template <int MW>
+__global__ __launch_bounds__(kBlock) void lexicon_kernel(Tables tb, uint32_t* __restrict__ mask,
+                                                         uint8_t* __restrict__ ws, size_t rbytes, int B) {
+  extern __shared__ __align__(16) uint8_t xlds[];
+  __shared__ uint32_t I_s[8];
+  __shared__ uint32_t pre_s[kRowGroup + 1];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int g0 = (int)blockIdx.y * kRowGroup, gr = min(kRowGroup, B - g0);
+  uint8_t* rows = ws + kWsHead;
+  if (tid < gr) {
+    const RowHeader* h = (const RowHeader*)(rows + (size_t)(g0 + tid) * rbytes);
+    pre_s[tid + 1] = h->valid == kRowValid ? h->res_count : 0u;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    pre_s[0] = 0;
+    for (int r = 1; r <= gr; ++r) pre_s[r] += pre_s[r - 1];
+  }
+  __syncthreads();
+  const uint32_t n = pre_s[gr];
+  if (blockIdx.x * (uint32_t)(kBlock * kLexPer) >= n) return;  // uniform
+  const RowLayout RL = row_layout(tb);
+  uint32_t* live_s = (uint32_t*)xlds;
+  uint32_t* tinfo_s = live_s + tb.S * MW;
+  uint32_t* acc_off_s = tinfo_s + tb.T;
+  uint8_t* acc_list_s = (uint8_t*)(acc_off_s + tb.S + 1);
+  for (int i = tid; i < tb.S * MW; i += kBlock) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
+  for (int i = tid; i < tb.T; i += kBlock) tinfo_s[i] = tb.term_info[i];
+  for (int i = tid; i <= tb.S; i += kBlock) acc_off_s[i] = tb.acc_off[i];
+  for (int i = tid; i < tb.n_acc; i += kBlock) acc_list_s[i] = tb.acc_list[i];
+  if (tid < 8) {
+    uint32_t iw = 0;
+    for (int j = 0; j < 32; ++j) {
+      const int t = tid * 32 + j;
+      if (t < tb.T && (tb.term_info[t] & 1u)) iw |= 1u << j;
+    }
+    I_s[tid] = iw;
+  }
+  __syncthreads();
+  const uint32_t step = gridDim.x * (uint32_t)(kBlock * kLexPer);
+  for (uint32_t e0 = blockIdx.x * (uint32_t)(kBlock * kLexPer); e0 < n; e0 += step) {  // uniform
+    int row[kLexPer];
+    uint2 ent[kLexPer];
+    uint4 rec[kLexPer], rk[kLexPer], tl[kLexPer];
+    uint32_t tf[kLexPer];
+#pragma unroll
+    for (int k = 0; k < kLexPer; ++k) {
+      const uint32_t e = e0 + (uint32_t)(k * kBlock + tid);
+      int r = 0;  // the row holding entry e: last r with pre_s[r] <= e
+      while (r + 1 < gr && pre_s[r + 1] <= e) ++r;
+      row[k] = r;
+      const uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
+      ent[k] = e < n ? ((const uint2*)(rw + RL.lexl))[e - pre_s[r]] : make_uint2(0xFFFFFFFFu, 0u);
+    }
+#pragma unroll
+    for (int k = 0; k < kLexPer; ++k) {
+      const bool on = ent[k].x != 0xFFFFFFFFu;
+      const RowHeader* h = (const RowHeader*)(rows + (size_t)(g0 + row[k]) * rbytes);
+      rec[k] = on ? tb.crec[h->cls_base + ent[k].y] : make_uint4(kClassReject, 0, 0, 0);
+      const uint32_t u = on ? tb.spell_of_id[ent[k].x] : 0u;
+      tf[k] = on ? tb.lex_token[(size_t)h->slot_id * tb.V + ent[k].x] : 0u;
+      rk[k] = on ? tb.spell_rec[u] : make_uint4(0, 0, 0, 0);
+      tl[k] = on && (rk[k].w & 0xFFu) > 8 ? tb.spell_tail[u] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < kLexPer; ++k) {
+      const bool on = ent[k].x != 0xFFFFFFFFu;
+      const uint32_t id = ent[k].x;
+      uint8_t* rw = rows + (size_t)(g0 + row[k]) * rbytes;
+      RowHeader* hdr = (RowHeader*)rw;
+      uint32_t v = kVerdictReject;
+      if (on) {
+        const RowHeader& h = *hdr;
+        LexLane lx;
+        lx.tb = &tb;
+        lx.sl = slot_of(h.slot);
+        lx.n = rk[k].w & 0xFFu;
+        lx.b0 = (uint64_t)rk[k].x | (uint64_t)rk[k].y << 32;
+        lx.b1 = (uint64_t)tl[k].x | (uint64_t)tl[k].y << 32;
+        lx.b2 = (uint64_t)tl[k].z | (uint64_t)tl[k].w << 32;
+        lx.ends = rec[k].x & kClassEndsMask;
+        lx.pos = rec[k].w;
+        lx.rem = (uint64_t)h.rem_lo | (uint64_t)h.rem_hi << 32;
+        lx.rem_len = h.rem_len;
+        lx.lexnode = h.lexnode;
+        lx.tf = tf[k];
+        v = class_verdict<MW>(h, I_s, live_s, tinfo_s, acc_off_s, acc_list_s, (const uint32_t*)(rw + RL.a2), 8,
+                              rec[k], lx);
+      }
+      if (v == kVerdictAllow) {
+        atomicOr(mask + (size_t)(g0 + row[k]) * tb.W + (id >> 5), 1u << (id & 31));
+        hdr->nonempty = 1u;
+      }
+      if (v == kVerdictWalk) {  // rare: one atomic per token
+        const uint32_t slot = atomicAdd(&hdr->walk_count, 1u);
+        ((uint32_t*)(rw + RL.walkl))[slot] = id;
+      }
+    }
+  }
+}
+
+__host__ __device__ inline uint32_t lexicon_lds(const Tables& tb, int mw) {
+  return pad16((uint32_t)tb.S * (uint32_t)mw * 4u + (uint32_t)(tb.T + tb.S + 1) * 4u + (uint32_t)tb.n_acc);
+}
+
 // Persistent, one workgroup per compute unit.  The grammar tables are staged
 // once; then, for each group of rows that fits, the rows' blocks (header,
 // trailing-flag tables, stack window, all written by the prologue) are copied
-// in one pass.  A work item is one row against one 64-spelling sub-tile.  The
-// workgroup's share of the items -- every gridDim.x-th in row-major order, so
-// each workgroup sees every row and all of the vocabulary -- is taken by its
-// waves one item at a time from an LDS counter; items whose spellings cannot
-// start a token (the sub-tile's first-byte range misses the row's table) are
-// passed over without loading anything.  A lane first judges its spelling
-// from the scan summary word alone (the words of the next two items are in
-// flight meanwhile).  Lanes that stay undecided are only marked; once the
-// group's items are done the marked lanes are packed, 64 to a wave, and
-// each loads its spelling's bytes and runs the lexicon checks or the
-// byte-by-byte walk, so a few undecided lanes no longer hold a whole wave.
+// in one pass.  The group's walk lists, cut into chunks of 64 ids, are
+// dealt to the workgroups in turn and taken by each workgroup's waves from an
+// LDS counter; each lane walks one token and ORs its bit into the row's mask
+// word.
 template <int MW>
-__global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const uint16_t* __restrict__ pool,
-                                                            uint8_t* __restrict__ ws, size_t rbytes, int B) {
+__global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const uint16_t* __restrict__ pool,
+                                                               uint32_t* __restrict__ mask, uint8_t* __restrict__ ws,
+                                                               size_t rbytes, int B) {
   extern __shared__ __align__(16) uint8_t lds[];
-  __shared__ int item_ctr;
+  __shared__ int chunk_ctr;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  __shared__ int chunk_ctr;
-  const WalkLds WL = walk_lds(tb, MW, B, (int)gridDim.x);
-  const RowLayout RL = row_layout(tb.T, tb.U, tb.S);
+  const ResLds WL = res_lds(tb, MW, B);
+  const RowLayout RL = row_layout(tb);
   uint8_t* bcls = lds + WL.bcls;
-  uint64_t* umask_s = (uint64_t*)(lds + WL.umask);
-  uint32_t* upre_s = (uint32_t*)(lds + WL.upre);
   uint32_t* tinfo_s = (uint32_t*)(lds + WL.tinfo);
   uint32_t* I_s = (uint32_t*)(lds + WL.I);
   uint32_t* live_s = (uint32_t*)(lds + WL.live);
+  uint32_t* pre_s = (uint32_t*)(lds + WL.pre);
   const uint32_t* acc_off_s = (const uint32_t*)(lds + WL.acc_off);
   const uint8_t* acc_list_s = lds + WL.acc_list;
   uint8_t* rows_s = lds + WL.rows;
-  const uint16_t* range_s = (const uint16_t*)(lds + WL.range);
   const mptr<true, uint16_t> lane_area = in_mem<true>((uint16_t*)(lds + WL.lanes) + tid * kFastLane);
   uint8_t* rows = ws + kWsHead;
-  const int nsub = (tb.U + kSub - 1) / kSub;
-  const uint32_t clsW_off = pad16((uint32_t)tb.S);
 
-  // grammar tables, once per workgroup
-  {
-    const StageRegion rg[8] = {{(const uint8_t*)tb.dfa, lds + WL.dfa, (uint32_t)(tb.S * tb.C * 2)},
-                               {tb.bclass, bcls, 256u},
-                               {(const uint8_t*)tb.acc_off, lds + WL.acc_off, (uint32_t)(tb.S + 1) * 4},
-                               {tb.acc_list, lds + WL.acc_list, (uint32_t)tb.n_acc},
-                               {(const uint8_t*)tb.sub_range, lds + WL.range, (uint32_t)nsub * 2},
-                               parse_region(tb, lds, WL.pl, 0),
-                               parse_region(tb, lds, WL.pl, 1),
-                               parse_region(tb, lds, WL.pl, 2)};
-    stage_regions<8, 4>(rg, tid, kWalkThreads);
-  }
-  const ParseTabs<true> pt = lds_parse(tb, lds, WL.pl);
-  for (int i = tid; i < tb.S * MW; i += kWalkThreads) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
-  for (int t = tid; t < 256; t += kWalkThreads) tinfo_s[t] = t < tb.T ? tb.term_info[t] : 0u;
-  __syncthreads();
-  if (tid < 8) {
-    uint32_t iw = 0;
-    for (int j = 0; j < 32; ++j)
-      if (tinfo_s[tid * 32 + j] & 1u) iw |= 1u << j;
-    I_s[tid] = iw;
-  }
-
-  const DfaView step{(const uint16_t*)(lds + WL.dfa), bcls, tb.C};
-  const WalkShared<MW> sh{&tb, pt, step, tinfo_s, I_s, live_s, acc_off_s, acc_list_s, pool};
+  bool staged = false;
   for (int g0 = 0; g0 < B; g0 += WL.group) {
     const int gr = min(WL.group, B - g0);
     __syncthreads();  // the previous group is done with the row blocks
+    if (tid < gr) {  // chunks of each row of the group, then their prefix sums
+      const RowHeader* h = (const RowHeader*)(rows + (size_t)(g0 + tid) * rbytes);
+      pre_s[tid + 1] = h->valid == kRowValid ? (h->walk_count + 63u) / 64u : 0u;
+    }
+    if (tid == 0) chunk_ctr = 0;
+    __syncthreads();
+    if (tid == 0) {
+      pre_s[0] = 0;
+      for (int r = 1; r <= gr; ++r) pre_s[r] += pre_s[r - 1];
+    }
+    __syncthreads();
+    const uint32_t total = pre_s[gr];
+    if (total == 0) continue;  // uniform
+    if (!staged) {  // grammar tables, once per workgroup
+      const StageRegion rg[7] = {{(const uint8_t*)tb.dfa, lds + WL.dfa, (uint32_t)(tb.S * tb.C * 2)},
+                                 {tb.bclass, bcls, 256u},
+                                 {(const uint8_t*)tb.acc_off, lds + WL.acc_off, (uint32_t)(tb.S + 1) * 4},
+                                 {tb.acc_list, lds + WL.acc_list, (uint32_t)tb.n_acc},
+                                 parse_region(tb, lds, WL.pl, 0),
+                                 parse_region(tb, lds, WL.pl, 1),
+                                 parse_region(tb, lds, WL.pl, 2)};
+      stage_regions<7, 4>(rg, tid, kWalkThreads);
+      for (int i = tid; i < tb.S * MW; i += kWalkThreads) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
+      for (int t = tid; t < 256; t += kWalkThreads) tinfo_s[t] = t < tb.T ? tb.term_info[t] : 0u;
+      __syncthreads();
+      if (tid < 8) {
+        uint32_t iw = 0;
+        for (int j = 0; j < 32; ++j)
+          if (tinfo_s[tid * 32 + j] & 1u) iw |= 1u << j;
+        I_s[tid] = iw;
+      }
+      staged = true;
+    }
     {
       // the rows' blocks, two 16-byte chunks per thread in flight at a time
-      const uint32_t n16 = WL.block / 16u, total = (uint32_t)gr * n16;
-      for (uint32_t i = tid; i < total; i += 2u * kWalkThreads) {
+      const uint32_t n16 = WL.block / 16u, tot16 = (uint32_t)gr * n16;
+      for (uint32_t i = tid; i < tot16; i += 2u * kWalkThreads) {
         const uint32_t i2 = i + kWalkThreads;
         const uint32_t r = i / n16, r2 = i2 / n16;
         const uint4 v = reinterpret_cast<const uint4*>(rows + (size_t)(g0 + r) * rbytes)[i - r * n16];
         uint4 v2 = make_uint4(0, 0, 0, 0);
-        if (i2 < total) v2 = reinterpret_cast<const uint4*>(rows + (size_t)(g0 + r2) * rbytes)[i2 - r2 * n16];
+        if (i2 < tot16) v2 = reinterpret_cast<const uint4*>(rows + (size_t)(g0 + r2) * rbytes)[i2 - r2 * n16];
         reinterpret_cast<uint4*>(rows_s)[i] = v;
-        if (i2 < total) reinterpret_cast<uint4*>(rows_s)[i2] = v2;
+        if (i2 < tot16) reinterpret_cast<uint4*>(rows_s)[i2] = v2;
       }
-    }
-    // item k: j = blockIdx.x + k * gridDim.x, row j / nsub, sub-tile j % nsub
-    const int total = gr * nsub;
-    const int mine = total > (int)blockIdx.x ? (total - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x : 0;
-    for (int k = tid; k < mine; k += kWalkThreads) umask_s[k] = 0ull;
-    if (tid == 0) {
-      item_ctr = 0;
-      chunk_ctr = 0;
     }
     __syncthreads();
-    auto row_hdr = [&](int r) -> const RowHeader& { return *(const RowHeader*)(rows_s + (size_t)r * WL.block); };
-    auto next_live = [&]() -> int {
-      for (;;) {
-        const int k = wave_grab(&item_ctr);
-        if (k >= mine) return k;
-        const int j = (int)blockIdx.x + k * (int)gridDim.x;
-        const int r = j / nsub;
-        const uint32_t rg = range_s[j - r * nsub];
-        const RowHeader& h = row_hdr(r);
-        if (h.valid == kRowValid && any_in_range(h.alive, rg & 0xFFu, rg >> 8)) return k;
-      }
-    };
-    // spelling of this lane in item k (row r), and its scan summary word;
-    // without the table every lane walks its bytes
-    auto spelling = [&](int k, int& r) -> int {
-      const int j = (int)blockIdx.x + (k < mine ? k : 0) * (int)gridDim.x;
-      r = j / nsub;
-      return (j - r * nsub) * kSub + lane;
-    };
-    auto summary = [&](int k, int r, int u) -> uint32_t {
-      if (!tb.scan) return 2u << 26;
-      const uint32_t q = k < mine ? row_hdr(r).q : 0u;
-      return tb.scan[(size_t)(q < (uint32_t)tb.S ? q : 0u) * tb.U + (u < tb.U ? u : 0)];
-    };
-    int k0 = next_live(), r0;
-    int u0 = spelling(k0, r0);
-    uint32_t sc0 = summary(k0, r0, u0);
-    int k1 = next_live(), r1;
-    int u1 = spelling(k1, r1);
-    uint32_t sc1 = summary(k1, r1, u1);
-    while (k0 < mine) {
-      const int k2 = next_live();
-      int r2;
-      const int u2 = spelling(k2, r2);
-      const uint32_t sc2 = summary(k2, r2, u2);
-
-      const RowHeader& h = row_hdr(r0);
-      const uint8_t* clsA = rows_s + (size_t)r0 * WL.block + sizeof(RowHeader);
-      const uint8_t* clsW = clsA + clsW_off;
-      uint8_t* rw = rows + (size_t)(g0 + r0) * rbytes;
-      const TermView tv{tinfo_s, I_s, h.R, live_s, MW};
-      int ok = 0;
-      if (u0 < tb.U)
-        ok = fast_verdict<MW>(h, clsA, clsW, I_s, acc_off_s, acc_list_s, tv, (const uint32_t*)(rw + RL.a2), sc0);
-      const uint64_t und = __ballot(ok == 2);
-      if (lane == 0) umask_s[k0] = und;
-      // the sub-tile's word of the sorted-spelling mask (its undecided lanes
-      // add their bits later, so both use atomic ORs)
-      const uint64_t allowed = __ballot(ok == 1);
-      if (allowed && lane == __ffsll((unsigned long long)__ballot(1)) - 1) {
-        atomicOr((unsigned long long*)(rw + RL.smask) + u0 / kSub, (unsigned long long)allowed);
-        ((RowHeader*)rw)->nonempty = 1u;
-      }
-      k0 = k1;
-      r0 = r1;
-      u0 = u1;
-      sc0 = sc1;
-      k1 = k2;
-      r1 = r2;
-      u1 = u2;
-      sc1 = sc2;
-    }
-    __syncthreads();
-    // undecided lanes: prefix counts over the items (one wave), then waves
-    // take 64 of them at a time
-    if (tid < 64) {
-      const int per = (mine + 63) / 64;
-      uint32_t sum = 0;
-      for (int i = 0; i < per; ++i) {
-        const int k = lane * per + i;
-        if (k < mine) sum += (uint32_t)__popcll(umask_s[k]);
-      }
-      uint32_t incl = sum;
-#pragma unroll
-      for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t t = __shfl_up(incl, d);
-        if (lane >= d) incl += t;
-      }
-      uint32_t run = incl - sum;
-      for (int i = 0; i < per; ++i) {
-        const int k = lane * per + i;
-        if (k < mine) {
-          upre_s[k] = run;
-          run += (uint32_t)__popcll(umask_s[k]);
-        }
-      }
-      if (lane == 63) upre_s[mine] = incl;
-    }
-    __syncthreads();
-    const int n_und = (int)upre_s[mine];
+    const ParseTabs<true> pt = lds_parse(tb, lds, WL.pl);
+    const DfaView step{(const uint16_t*)(lds + WL.dfa), bcls, tb.C};
+    const WalkShared<MW> sh{&tb, pt, step, tinfo_s, I_s, live_s, acc_off_s, acc_list_s, pool};
+    // this workgroup's chunks are blockIdx.x + k * gridDim.x; its waves take
+    // them in turn from an LDS counter
     for (;;) {
-      const int c = wave_grab(&chunk_ctr);
-      if (c * 64 >= n_und) break;
-      const int pos = c * 64 + lane;
-      if (pos < n_und) {
-        // the item holding position pos: last k with upre_s[k] <= pos
-        int lo = 0, hi = mine - 1;
-        while (lo < hi) {
-          const int mid = (lo + hi + 1) >> 1;
-          if ((int)upre_s[mid] <= pos) lo = mid;
-          else hi = mid - 1;
-        }
-        const int bit = nth_set_bit(umask_s[lo], pos - (int)upre_s[lo]);
-        const int j = (int)blockIdx.x + lo * (int)gridDim.x;
-        const int r = j / nsub;
-        const int u = (j - r * nsub) * kSub + bit;
-        const uint8_t* rowblk = rows_s + (size_t)r * WL.block;
-        uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
-        if (undecided_lane<MW>(sh, *(const RowHeader*)rowblk, rowblk, rw, RL, u, summary(lo, r, u), lane_area) > 0) {
-          atomicOr((unsigned long long*)(rw + RL.smask) + u / kSub, 1ull << (u & (kSub - 1)));
+      const uint32_t c = blockIdx.x + (uint32_t)wave_grab(&chunk_ctr) * gridDim.x;
+      if (c >= total) break;
+      int r = 0;  // the row holding chunk c: last r with pre_s[r] <= c
+      while (r + 1 < gr && pre_s[r + 1] <= c) ++r;
+      const uint8_t* rowblk = rows_s + (size_t)r * WL.block;
+      const RowHeader& h = *(const RowHeader*)rowblk;
+      uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
+      const uint32_t e = (c - pre_s[r]) * 64u + (uint32_t)lane;
+      if (e < h.walk_count) {
+        const int id = (int)((const uint32_t*)(rw + RL.walkl))[e];
+        if (residue_lane<MW>(sh, h, rowblk, rw, RL, id, lane_area) > 0) {
+          atomicOr(mask + (size_t)(g0 + r) * tb.W + (id >> 5), 1u << (id & 31));
           ((RowHeader*)rw)->nonempty = 1u;
         }
       }
@@ -1727,14 +2052,10 @@ __global__ __launch_bounds__(kWalkThreads) void walk_kernel(Tables tb, const uin
 }
 
 // ---------------------------------------------------------------- finalize
-// Workgroups (row, y), y < kGatherGroups.  The row's mask over token ids is
-// gathered from the mask in spelling order: each wave turns 64 consecutive ids
-// into two mask words by a ballot (every alias takes its spelling's bit;
-// specials and padding are 0; the EOS bit mirrors eos_ok).  When the walk
-// handed spellings to the slow path, workgroup (row, 0) alone first re-walks
-// them from the row's configuration with a large stack area per thread in
-// the workspace, then gathers the whole row; the other workgroups of that row
-// exit.  Workgroup (row, 0) also writes the row status.
+// One workgroup per row.  Tokens the residue walk handed over (their lane
+// stack area was too small) are walked again from the row's configuration
+// with a large stack area per thread in the workspace, reading the tables
+// from global memory; then the row status is written.
 template <int MW>
 __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_config* __restrict__ cfgs,
                                                           const uint16_t* __restrict__ pool,
@@ -1742,21 +2063,19 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
                                                           size_t rbytes, int32_t* __restrict__ status) {
   const int row = blockIdx.x;
   const int tid = threadIdx.x;
-  const int lane = tid & 63;
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
-  const RowLayout RL = row_layout(tb.T, tb.U, tb.S);
+  const RowLayout RL = row_layout(tb);
   if (hdr->valid == kRowCached) {  // served from the mask cache by the prologue
-    if (blockIdx.y == 0 && threadIdx.x == 0 && status) status[row] = hdr->pstat;
+    if (threadIdx.x == 0 && status) status[row] = hdr->pstat;
     return;
   }
   const bool valid = hdr->valid == kRowValid;
   const uint32_t count = valid ? min(hdr->slow_count, (uint32_t)kSlowCap) : 0u;
-  if (count > 0 && blockIdx.y != 0) return;  // uniform
   __shared__ uint32_t I_s[8];
   __shared__ int slow_ok;
   if (tid == 0) slow_ok = 0;
-  if (count > 0) {
+  if (count > 0) {  // uniform
     if (tid < 8) {
       uint32_t iw = 0;
       for (int j = 0; j < 32; ++j) {
@@ -1792,7 +2111,8 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
       lex0.w = 0;
       for (int k = 0; k < 8; ++k) lex0.w |= (uint64_t)cfg.rem_head[k] << (8 * k);
       for (uint32_t k = tid; k < count; k += kSlowThreads) {
-        const int su = (int)((const uint32_t*)(rw + RL.slow))[k];
+        const int id = (int)((const uint32_t*)(rw + RL.slow))[k];
+        const uint32_t su = tb.spell_of_id[id];
         Lane<MW> ln;
         ln.mode = 0;
         ln.t1 = -1;
@@ -1803,53 +2123,18 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
         const uint32_t base = tb.spell_off[su];
         auto byte_at = [&](uint32_t i) -> uint32_t { return tb.spell_bytes[base + i]; };
         const int ok = walk_bytes<false, MW>(rc, ln, cfg.q, lex0, 0u, tb.spell_off[su + 1] - base, byte_at, step,
-                                             ov, kSlowLane);
+                                             ov, kSlowLane, 1u);
         if (ok > 0) {
-          atomicOr((uint32_t*)(rw + RL.smask) + (su >> 5), 1u << (su & 31));
+          atomicOr(mask + (size_t)row * tb.W + (id >> 5), 1u << (id & 31));
           slow_ok = 1;
         } else if (ok < 0) {
           atomicOr(&hdr->wstat, GRID_ROW_OVERFLOW);
         }
       }
     }
-    __syncthreads();
-    __threadfence();  // the gather below reads the bits set above
   }
-
-  const uint64_t* sm = (const uint64_t*)(rw + RL.smask);
-  uint32_t* mrow = mask + (size_t)row * tb.W;
-  const int eos = valid && hdr->eos_ok ? tb.eos_id : -1;
-  // ids [64 c, 64 c + 64) for the chunks c of this workgroup, four per wave at
-  // a time so their loads overlap
-  const int n_chunks = (tb.V + 63) / 64;
-  const int groups = count > 0 ? 1 : kGatherGroups;
-  const int per = (n_chunks + groups - 1) / groups;
-  const int c_begin = (count > 0 ? 0 : (int)blockIdx.y) * per;
-  const int c_end = min(n_chunks, c_begin + per);
-  constexpr int kWaves = kBlock / 64, kUnroll = 8;
-  for (int c0 = c_begin + (tid >> 6); c0 < c_end; c0 += kWaves * kUnroll) {
-    uint32_t su[kUnroll];
-    uint64_t word[kUnroll];
-#pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
-      const int c = c0 + k * kWaves;
-      const int id = c * 64 + lane;
-      su[k] = (c < c_end && id < tb.V && valid) ? tb.spell_of_id[id] : 0xFFFFFFFFu;
-    }
-#pragma unroll
-    for (int k = 0; k < kUnroll; ++k) word[k] = su[k] != 0xFFFFFFFFu ? sm[su[k] >> 6] : 0ull;
-#pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
-      const int c = c0 + k * kWaves;
-      if (c >= c_end) break;  // uniform across the wave
-      const int id = c * 64 + lane;
-      const bool bit = (su[k] != 0xFFFFFFFFu && ((word[k] >> (su[k] & 63)) & 1ull)) || id == eos;
-      const uint64_t bits = __ballot(bit);
-      if (lane == 0) mrow[2 * c] = (uint32_t)bits;
-      if (lane == 1 && 2 * c + 1 < tb.W) mrow[2 * c + 1] = (uint32_t)(bits >> 32);
-    }
-  }
-  if (blockIdx.y == 0 && tid == 0) {
+  __syncthreads();
+  if (tid == 0) {
     int32_t st;
     if (valid) {
       st = hdr->pstat | hdr->wstat;
@@ -1949,15 +2234,15 @@ bool raise_lds(const void* fn, uint32_t bytes) {
   return true;
 }
 
-// Resident walk workgroups on the current device (compute units x
+// Resident residue workgroups on the current device (compute units x
 // occupancy) for an LDS size; raises the kernel's LDS limit first.
 template <int MW>
-int walk_grid_size(uint32_t lds) {
-  if (!raise_lds((const void*)walk_kernel<MW>, lds)) return -1;
+int residue_grid_size(uint32_t lds) {
+  if (!raise_lds((const void*)residue_kernel<MW>, lds)) return -1;
   int dev = 0, cus = 0, per_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -1;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, walk_kernel<MW>, kWalkThreads, lds) != hipSuccess ||
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, residue_kernel<MW>, kWalkThreads, lds) != hipSuccess ||
       per_cu <= 0)
     per_cu = 1;
   return cus * per_cu;
@@ -1969,24 +2254,34 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
   const uint32_t parse_bytes = parse_lds(tb, 0).total;
   if (!raise_lds((const void*)prologue_kernel<MW>, parse_bytes))
     return fail(GRID_E_HIP, "grid_mask: cannot raise the LDS limit");
-  if (phases & GRID_PHASE_PROLOGUE)
+  if (phases & GRID_PHASE_PROLOGUE) {
     hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool, mask, eos, ws,
                        rb);
-  if ((phases & GRID_PHASE_WALK) && tb.U > 0) {
-    const WalkLds W0 = walk_lds(tb, MW, B, 1 << 20);
-    const int nsub = (tb.U + kSub - 1) / kSub;
-    const int resident = walk_grid_size<MW>(W0.total);
-    if (resident <= 0) return fail(GRID_E_HIP, "grid_mask: cannot raise the walk's LDS limit");
-    const int n_items = nsub * std::min(B, W0.group);
-    const int blocks = std::min((n_items + kWalkThreads / 64 - 1) / (kWalkThreads / 64), resident);
-    const WalkLds WL = walk_lds(tb, MW, B, blocks);
-    if ((long long)nsub > (long long)kMaxItems * blocks)
-      return fail(GRID_E_CAPACITY, "grid_mask: vocabulary too large for the walk's item bookkeeping");
-    hipLaunchKernelGGL(walk_kernel<MW>, dim3(blocks), dim3(kWalkThreads), WL.total, s, tb, pool, ws, rb, B);
+    const uint32_t vgroups = ((uint32_t)tb.max_classes + 3u) / 4u;
+    const uint32_t vy = (vgroups + kBlock - 1) / kBlock;
+    hipLaunchKernelGGL(verdict_kernel<MW>, dim3(B, vy), dim3(kBlock), verdict_lds(tb, MW), s, tb, ws, rb);
+  }
+  if (phases & GRID_PHASE_WALK) {
+    const uint32_t lds = pad16(((uint32_t)tb.max_classes + 15u) / 16u * 4u);
+    if (!raise_lds((const void*)stream_kernel, lds)) return fail(GRID_E_HIP, "grid_mask: cannot raise the LDS limit");
+    const long long blocks = 8ll * B * stream_groups(tb.V);
+    if (blocks > 0x7FFFFFFFll) return fail(GRID_E_CAPACITY, "grid_mask: batch x vocabulary too large");
+    hipLaunchKernelGGL(stream_kernel, dim3((uint32_t)blocks), dim3(kBlock), lds, s, tb, mask, ws, rb, B);
+  }
+  if ((phases & GRID_PHASE_RESIDUE) && tb.U > 0) {
+    // a few hundred workgroups per row group: idle ones still cost dispatch time
+    const uint32_t lx = (uint32_t)std::max(1, std::min(256, (tb.V * kRowGroup / 8 + kBlock * kLexPer - 1) /
+                                                                 (kBlock * kLexPer)));
+    const uint32_t ly = (uint32_t)((B + kRowGroup - 1) / kRowGroup);
+    hipLaunchKernelGGL(lexicon_kernel<MW>, dim3(lx, ly), dim3(kBlock), lexicon_lds(tb, MW), s, tb, mask, ws, rb, B);
+    const ResLds RL = res_lds(tb, MW, B);
+    const int resident = residue_grid_size<MW>(RL.total);
+    if (resident <= 0) return fail(GRID_E_HIP, "grid_mask: cannot raise the residue walk's LDS limit");
+    hipLaunchKernelGGL(residue_kernel<MW>, dim3(resident), dim3(kWalkThreads), RL.total, s, tb, pool, mask, ws, rb,
+                       B);
   }
   if (phases & GRID_PHASE_FINALIZE) {
-    hipLaunchKernelGGL(finalize_kernel<MW>, dim3(B, kGatherGroups), dim3(kBlock), 0, s, tb, cfg_dev, pool, mask,
-                       ws, rb, status);
+    hipLaunchKernelGGL(finalize_kernel<MW>, dim3(B), dim3(kBlock), 0, s, tb, cfg_dev, pool, mask, ws, rb, status);
     if (tb.cache && (tb.cache_flags & GRID_CACHE_INSERT))
       hipLaunchKernelGGL(cache_publish_kernel, dim3(B), dim3(kBlock), 0, s, tb, mask, ws, rb);
   }
@@ -1997,12 +2292,12 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
 
 int grid::overlay_capacity() { return kFastLane; }
 
-static int n_spellings(const grid_compiled* g) { return (int)g->vocab.spell_off.size() - 1; }
-
 // head, then B rows
-static size_t workspace_size(const grid_compiled* g, int B) {
-  return kWsHead + row_layout(g->parser.T, n_spellings(g), g->dfa.S).total * (size_t)B;
+static size_t row_bytes(const grid_compiled* g) {
+  return row_layout(g->parser.T, g->dfa.S, g->vocab.V, (int)g->classes.max_classes).total;
 }
+
+static size_t workspace_size(const grid_compiled* g, int B) { return kWsHead + row_bytes(g) * (size_t)B; }
 
 extern "C" size_t grid_mask_workspace_bytes(const grid_compiled* g, int32_t B) {
   if (!g || B <= 0) return 0;
@@ -2018,7 +2313,7 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
   if (cache_flags & ~(GRID_CACHE_LOOKUP | GRID_CACHE_INSERT)) return fail(GRID_E_ARG, "grid_mask: unknown cache flags");
   if (!g || B <= 0 || B > 65535 || !cfg_dev || !stack_pool_dev || !mask_dev || !workspace_dev)
     return fail(GRID_E_ARG, "grid_mask: null pointer or batch size out of range");
-  const size_t rb = row_layout(g->parser.T, n_spellings(g), g->dfa.S).total;
+  const size_t rb = row_bytes(g);
   if (workspace_bytes < workspace_size(g, B)) return fail(GRID_E_ARG, "grid_mask: workspace too small");
   if (((uintptr_t)workspace_dev & 255) != 0) return fail(GRID_E_ARG, "grid_mask: workspace not 256-byte aligned");
   static const int needed[] = {GRID_ART_DFA_CLASS,   GRID_ART_BYTE_CLASS,  GRID_ART_DFA_ACCEPT_OFF,
@@ -2028,7 +2323,9 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
                                GRID_ART_ALIAS_OFF,   GRID_ART_ALIAS_IDS,   GRID_ART_LEX_FLAGS,
                                GRID_ART_LEX_HASH,    GRID_ART_LEX_SLOTS,   GRID_ART_PARSE_STATE,
                                GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH,   GRID_ART_LEX_PREFIX,
-                               GRID_ART_SPELL_RANGE, GRID_ART_SPELL_OF_ID, GRID_ART_SCAN_SUMMARY};
+                               GRID_ART_SPELL_OF_ID, GRID_ART_CLASS_MAP, GRID_ART_CLASS_OFF,
+                               GRID_ART_CLASS_REC,   GRID_ART_LEX_STRIDE,  GRID_ART_LEX_TOKEN,
+                               GRID_ART_ID_FIRST};
   for (int w : needed)
     if (!bound(g, w)) return fail(GRID_E_UNBOUND, "grid_mask: artifact " + std::to_string(w) + " is not bound");
   Tables tb;
@@ -2052,9 +2349,14 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
   tb.lex_hash = (const uint32_t*)g->dev[GRID_ART_LEX_HASH];
   tb.lex_slots = (const uint32_t*)g->dev[GRID_ART_LEX_SLOTS];
   tb.lex_prefix = (const uint4*)g->dev[GRID_ART_LEX_PREFIX];
-  tb.sub_range = (const uint16_t*)g->dev[GRID_ART_SPELL_RANGE];
+  tb.lex_stride = (const uint4*)g->dev[GRID_ART_LEX_STRIDE];
+  tb.lex_token = (const uint32_t*)g->dev[GRID_ART_LEX_TOKEN];
+  tb.id_first = (const uint8_t*)g->dev[GRID_ART_ID_FIRST];
   tb.spell_of_id = (const uint32_t*)g->dev[GRID_ART_SPELL_OF_ID];
-  tb.scan = g->scan.empty() ? nullptr : (const uint32_t*)g->dev[GRID_ART_SCAN_SUMMARY];
+  tb.cmap = (const uint16_t*)g->dev[GRID_ART_CLASS_MAP];
+  tb.coff = (const uint32_t*)g->dev[GRID_ART_CLASS_OFF];
+  tb.crec = (const uint4*)g->dev[GRID_ART_CLASS_REC];
+  tb.max_classes = (int)g->classes.max_classes;
   tb.S = g->dfa.S;
   tb.C = g->dfa.C;
   tb.T = g->parser.T;
@@ -2086,9 +2388,9 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
     tb.cache_flags = cache_flags;
   }
   const int mw = tb.tw;
-  const WalkLds WL = walk_lds(tb, mw, B, 1 << 20);
+  const ResLds WL = res_lds(tb, mw, B);
   if (tb.T > 255 || (mw != 2 && mw != 4 && mw != 8) || WL.total + 64 > kWalkLdsMax ||
-      parse_lds(tb, 0).total > 24 * 1024)
+      parse_lds(tb, 0).total > 24 * 1024 || verdict_lds(tb, mw) > 64 * 1024)
     return fail(GRID_E_CAPACITY, "grid_mask: lexer DFA or LR tables too large for the LDS staging");
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace_dev;

@@ -44,26 +44,46 @@ GRID_HD uint32_t lexp_hash(uint32_t lo, uint32_t hi, uint32_t len) {
   return h ^ (h >> 12);
 }
 
-// Scan summary word of (lexer DFA state q, spelling u): how maximal munch
-// segments the bytes of u when the scan resumes in q.  Bits 0-8: the DFA
-// state after the last byte; 9-17: the state in which the first lexeme ended;
-// 18-25: the index of the byte that ended it; 26-27: the number of lexeme ends
-// inside u (2 = two or more); bit 28: the lexer alone rejects u (a lexeme
-// ends in a state that accepts nothing, or a byte starts no lexeme).  The
-// table exists when the DFA has at most 512 states.
-constexpr uint32_t kScanMaxStates = 512;
-constexpr uint32_t kScanReject = 1u << 28;
-GRID_HD uint32_t scan_word(uint32_t q_end, uint32_t q_first, uint32_t p_first, uint32_t ends) {
-  return q_end | q_first << 9 | p_first << 18 | ends << 26;
+// Stride table: every lexicon-trie node of depth d > 8, keyed by its
+// ancestor at depth 8 * floor((d - 1) / 8) and its bytes below that ancestor
+// (1..8, little-endian, zero padded), so a lexeme of up to 24 bytes is looked
+// up with at most three probes.  Entry, 8 u32: ancestor node, bytes lo,
+// bytes hi, length | flags << 16 (length 0 = empty), node, 0, 0, 0.
+GRID_HD uint32_t lexs_hash(uint32_t anc, uint32_t lo, uint32_t hi, uint32_t len) {
+  return lexp_hash(lo ^ anc * 0x27D4EB2Fu, hi + anc, len);
 }
-GRID_HD uint32_t scan_q_end(uint32_t w) { return w & 0x1FFu; }
-GRID_HD uint32_t scan_q_first(uint32_t w) { return (w >> 9) & 0x1FFu; }
-GRID_HD uint32_t scan_p_first(uint32_t w) { return (w >> 18) & 0xFFu; }
-GRID_HD uint32_t scan_ends(uint32_t w) { return (w >> 26) & 3u; }
 
-// Per-slot record (8 u32): flags base, hash base (entries), hash mask,
+// Lexeme-program classes (verdict-equivalence classes of section 4.2, keyed
+// by lexer state).  When the scan resumes in DFA state q, maximal munch cuts
+// the bytes of a token into lexemes independently of the parser (munch length
+// comes from the lexer alone); what the parser later decides depends only on
+// the DFA states in which those lexemes end and the state after the last
+// byte.  Tokens with equal programs from q form a class; CLASS_MAP[q][id] is
+// the token's class index local to q, and the classes of q are the records
+// CLASS_REC[CLASS_OFF[q] ...], four u32 each:
+//   w0: ends (0..kClassEnds, kClassMore = more) | reject | first-byte-ends-lexeme
+//   w1: state after the last byte | state where lexeme 0 ended << 16
+//   w2: state where lexeme 1 ended | state where lexeme 2 ended << 16
+//   w3: the byte indices that ended lexemes 0, 1, 2 (8 bits each, 0 for
+//       missing ends): lexeme 0 is the pending bytes and the token's bytes
+//       before its end, lexeme i the bytes between ends i-1 and i, and the
+//       trailing lexeme the bytes after the last end (all of the token and
+//       the pending bytes when there is none)
+// Local class 0 of every state is "rejected by the lexer alone" (also special
+// and empty tokens); local class 1 is "walk the bytes" (tokens of a state
+// whose class count exceeds 65536).
+constexpr int kClassEnds = 3;
+constexpr uint32_t kClassMore = 4;
+constexpr uint32_t kClassEndsMask = 7u;
+constexpr uint32_t kClassReject = 1u << 3;
+constexpr uint32_t kClassP0 = 1u << 4;
+constexpr uint32_t kClassWalk = 1u << 5;
+constexpr uint32_t kClassMaxLocal = 65536;
+
+// Per-slot record (12 u32): flags base, hash base (entries), hash mask,
 // restricted-category mask, node count, prefix-table base (entries),
-// prefix-table mask, 1 reserved.
-constexpr int kSlotWords = 8;
+// prefix-table mask, stride-table base (entries), stride-table mask, 3
+// reserved.
+constexpr int kSlotWords = 12;
 
 }  // namespace grid

@@ -28,7 +28,8 @@ ART_NAMES = ["DFA_DENSE", "DFA_CLASS", "BYTE_CLASS", "DFA_ACCEPT_OFF", "DFA_ACCE
              "ACTION", "GOTO", "PROD", "TERM_INFO", "SPELL_OFF", "SPELL_BYTES", "ALIAS_OFF",
              "ALIAS_IDS", "TRIE_LEVEL_OFF", "TRIE_NODES", "LEX_FLAGS", "LEX_HASH", "LEX_SLOTS",
              "SPELL_REC", "PARSE_STATE", "PARSE_REDX", "GOTO_HASH", "SPELL_TAIL", "LEX_PREFIX",
-             "SPELL_RANGE", "SPELL_OF_ID", "SCAN_SUMMARY"]
+             "SPELL_RANGE", "SPELL_OF_ID", "CLASS_MAP", "CLASS_OFF", "CLASS_REC", "LEX_STRIDE",
+             "LEX_TOKEN", "ID_FIRST"]
 ART = {n: i for i, n in enumerate(ART_NAMES)}
 
 CONFIG_DTYPE = np.dtype([("stk_off", "<u4"), ("stk_depth", "<u4"), ("lexnode", "<u4"), ("q", "<u2"),
@@ -41,7 +42,7 @@ EXPORTS = ["grid_compile", "grid_free", "grid_last_error", "grid_info", "grid_ad
            "grid_artifact", "grid_bind_device", "grid_config_from_prefix",
            "grid_mask_workspace_bytes", "grid_mask", "grid_mask_phases", "grid_apply",
            "grid_cache_bytes", "grid_cache_clear", "grid_mask_cached"]
-PHASE_PROLOGUE, PHASE_WALK, PHASE_FINALIZE, PHASE_ALL = 1, 2, 4, 7
+PHASE_PROLOGUE, PHASE_WALK, PHASE_RESIDUE, PHASE_FINALIZE, PHASE_ALL = 1, 2, 4, 8, 15
 
 
 class GridError(RuntimeError):

@@ -92,7 +92,7 @@ def test_lexicon_prefix_table(G):
     words_c = ["id", "emp_no", "employee_name_full", "e_x", "order_id"]
     g = G.Grid(grammar_text("crud"), ["insert", "update", "delete"], [b"a"])
     slot = g.add_lexicon({"TABLE_NAME": words_t, "COLUMN_NAME": words_c})
-    rec = np.frombuffer(g.artifact("LEX_SLOTS"), np.uint32).reshape(-1, 8)[slot]
+    rec = np.frombuffer(g.artifact("LEX_SLOTS"), np.uint32).reshape(-1, 12)[slot]
     flags = np.frombuffer(g.artifact("LEX_FLAGS"), np.uint16)
     edges = np.frombuffer(g.artifact("LEX_HASH"), np.uint32).reshape(-1, 2)
     pref = np.frombuffer(g.artifact("LEX_PREFIX"), np.uint32).reshape(-1, 4)
@@ -133,6 +133,41 @@ def test_lexicon_prefix_table(G):
         if p[:8] not in prefixes:
             assert lookup(p[:8]) is None, p
     assert int((pref[pbase:pbase + pmask + 1, 2] & 0xFFFF > 0).sum()) == len(prefixes)
+
+    # stride table: every node deeper than 8 is found from its ancestor at the
+    # last multiple of 8 and its bytes below it
+    stride = np.frombuffer(g.artifact("LEX_STRIDE"), np.uint32).reshape(-1, 8)
+    sbase, smask = int(rec[7]), int(rec[8])
+
+    def node_of(bs):
+        node = 0
+        for b in bs:
+            node = child(node, b) if node is not None else None
+        return node
+
+    def deep_lookup(bs):
+        anc = node_of(bs[:(len(bs) - 1) // 8 * 8])
+        tail = bs[(len(bs) - 1) // 8 * 8:]
+        lo = int.from_bytes(tail[:4].ljust(4, b"\0"), "little")
+        hi = int.from_bytes(tail[4:8].ljust(4, b"\0"), "little")
+        m = 0xFFFFFFFF
+        h = _lexp_hash(lo ^ ((anc * 0x27D4EB2F) & m), (hi + anc) & m, len(tail)) & smask
+        while True:
+            e = stride[sbase + h]
+            if e[3] & 0xFFFF == 0:
+                return None
+            if e[0] == anc and e[1] == lo and e[2] == hi and e[3] & 0xFFFF == len(tail):
+                return int(e[3] >> 16), int(e[4])
+            h = (h + 1) & smask
+
+    deep = {w[:k].encode() for w in words_t + words_c for k in range(9, len(w) + 1)}
+    assert any(len(p) > 16 for p in deep)
+    for p in deep:
+        node = node_of(p)
+        assert deep_lookup(p) == (int(flags[fbase + node]), node), p
+    for p in [b"employeesX", b"dept_history_2021", b"employee_name_fulL"]:
+        assert deep_lookup(p) is None, p
+    assert int((stride[sbase:sbase + smask + 1, 3] & 0xFFFF > 0).sum()) == len(deep)
 
 
 def test_config_pending_head_bytes(G):
@@ -292,60 +327,86 @@ def test_dfa_tables_consistent(G):
     assert len(set(cls.tolist())) == C
 
 
-def _munch_summary(dense, accepting, q, sp):
-    # maximal munch over sp from DFA state q, written out byte by byte
-    cur, ends, q_first, p_first = q, 0, 0, 0
+def _munch_program(dense, accepting, q, sp):
+    # maximal munch over sp from DFA state q, written out byte by byte: None
+    # if the lexer alone rejects it, else (ends, byte 0 ends the pending
+    # lexeme, states and byte indices of the first three ends, state after
+    # the last byte)
+    cur, ends, qe, pe, p0 = q, 0, [], [], False
     for i, b in enumerate(sp):
         nq = int(dense[cur, b])
         if nq != 0:
             cur = nq
             continue
         if not accepting[cur]:
-            return 1 << 28
-        if ends == 0:
-            q_first, p_first = cur, i
+            return None
+        if i == 0:
+            p0 = True
+        if len(qe) < 3:
+            qe.append(cur)
+            pe.append(i)
         ends += 1
-        if ends == 2:
-            return q_first << 9 | p_first << 18 | 2 << 26
         cur = int(dense[1, b])
         if cur == 0:
-            return 1 << 28
-    return cur | q_first << 9 | p_first << 18 | ends << 26
+            return None
+    return min(ends, 4), p0, tuple(qe + [0] * (3 - len(qe))), tuple(pe + [0] * (3 - len(pe))), cur
 
 
-def test_scan_summary_matches_maximal_munch(G):
+def test_class_tables_match_maximal_munch(G):
     rng = np.random.default_rng(11)
     alphabet = np.frombuffer(b"selct frmwhe*,()'0123456789abcxyz_.=<>;\n\t-\"", np.uint8)
     vocab = [bytes([b]) for b in range(256)]
     vocab += [bytes(rng.choice(alphabet, int(n))) for n in rng.integers(2, 40, 600)]
-    vocab += [b"SELECT", b" FROM", b"'abc'", b"),", b"1;", b"x" * 200]
-    g = G.Grid(grammar_text("sql_dml"), ["insert", "update", "delete"], vocab)
+    vocab += [b"SELECT", b" FROM", b"'abc'", b"),", b"1;", b"x" * 200, b"", b"a b c d e"]
+    specials = [3]
+    g = G.Grid(grammar_text("sql_dml"), ["insert", "update", "delete"], vocab, specials)
     info = g.info()
-    S, U = info["n_dfa_states"], info["n_spellings"]
+    S, V = info["n_dfa_states"], info["vocab_size"]
     dense = np.frombuffer(g.artifact("DFA_DENSE"), np.uint16).reshape(S, 256)
     aoff = np.frombuffer(g.artifact("DFA_ACCEPT_OFF"), np.uint32)
     accepting = aoff[1:] > aoff[:-1]
-    off = np.frombuffer(g.artifact("SPELL_OFF"), np.uint32)
-    data = np.frombuffer(g.artifact("SPELL_BYTES"), np.uint8)
-    scan = np.frombuffer(g.artifact("SCAN_SUMMARY"), np.uint32).reshape(S, U)
-    seen = set()
-    for u in range(U):
-        sp = data[off[u]:off[u + 1]].tolist()
-        for q in range(S):
-            got = int(scan[q, u])
-            assert got == _munch_summary(dense, accepting, q, sp), (q, bytes(sp))
-            seen.add(got >> 26)
-    assert {0, 1, 2, 4} <= seen  # lexeme-internal, one end, several ends, rejected
+    cmap = np.frombuffer(g.artifact("CLASS_MAP"), np.uint16).reshape(S, V)
+    coff = np.frombuffer(g.artifact("CLASS_OFF"), np.uint32)
+    rec = np.frombuffer(g.artifact("CLASS_REC"), np.uint32).reshape(-1, 4)
+    assert coff[0] == 0 and coff[-1] == len(rec) and (np.diff(coff) >= 2).all()
+    kinds = set()
+    for q in range(S):
+        recs = rec[coff[q]:coff[q + 1]]
+        assert recs[0].tolist() == [8, 0, 0, 0] and recs[1].tolist() == [32, 0, 0, 0]
+        decoded = [tuple(r) for r in recs[2:].tolist()]
+        assert len(set(decoded)) == len(decoded)  # one record per distinct program
+        for t, sp in enumerate(vocab):
+            c = int(cmap[q, t])
+            want = None if (t in specials or not sp) else _munch_program(dense, accepting, q, list(sp))
+            if want is None:
+                assert c == 0, (q, sp)
+                continue
+            assert c >= 2, (q, sp)
+            w0, w1, w2, w3 = recs[c].tolist()
+            ends, p0, qe, pe, last = want
+            assert w0 == ends | (16 if p0 else 0), (q, sp)
+            pos = pe[0] | pe[1] << 8 | pe[2] << 16
+            assert (w1 & 0xFFFF, w1 >> 16, w2 & 0xFFFF, w2 >> 16, w3) == (last, qe[0], qe[1], qe[2], pos), (q, sp)
+            kinds.add(ends)
+    assert {0, 1, 2, 3, 4} <= kinds  # inside one lexeme, one to three ends, more
 
 
-def test_scan_summary_absent_for_large_dfa(G):
-    # more than 512 DFA states: no table (the kernels then scan every byte)
+def test_class_tables_large_dfa(G):
+    # more than 512 DFA states: 16-bit states in the class records
     kws = [f"Q{i:03d}X{i * 7 % 1000:03d}" for i in range(100)]
     text = "start E\n" + "".join(f'token K{i} "{k}"\n' for i, k in enumerate(kws))
     text += "E : " + " | ".join(f"K{i}" for i in range(len(kws))) + " ;\n"
-    g = G.Grid(text, (), [bytes([b]) for b in range(256)])
-    assert g.info()["n_dfa_states"] > 512
-    assert g.artifact("SCAN_SUMMARY") == b""
+    vocab = [bytes([b]) for b in range(256)] + [k.encode() for k in kws[:5]]
+    g = G.Grid(text, (), vocab)
+    info = g.info()
+    S, V = info["n_dfa_states"], info["vocab_size"]
+    assert S > 512
+    cmap = np.frombuffer(g.artifact("CLASS_MAP"), np.uint16).reshape(S, V)
+    coff = np.frombuffer(g.artifact("CLASS_OFF"), np.uint32)
+    rec = np.frombuffer(g.artifact("CLASS_REC"), np.uint32).reshape(-1, 4)
+    # from the start state, each keyword stays inside one lexeme, in its own state
+    ends_in = {int(rec[coff[1] + cmap[1, 256 + i], 1] & 0xFFFF) for i in range(5)}
+    assert len(ends_in) == 5 and max(ends_in) < S
 
 
 @pytest.mark.parametrize("name,drop", [("expr", []), ("sql_select", []),
