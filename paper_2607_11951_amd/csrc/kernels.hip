@@ -73,6 +73,7 @@ constexpr int kFastLane = 16;        // per-lane stack area in LDS (overlay at t
                                      // virtual pushes above it)
 constexpr int kRowGroup = 32;        // rows resident in LDS at once (at most)
 constexpr int kWalkWin = 64;         // top stack entries of each row in the walk's LDS
+constexpr int kMaxItems = 1024;      // residue work items a workgroup scans at once
 constexpr uint32_t kWalkLdsMax = 160 * 1024;
 
 struct Tables {
@@ -159,11 +160,9 @@ struct RowHeader {
   uint32_t nonempty;          // the walk allowed some token
   int32_t cache_slot;         // mask-cache entry this row publishes to, -1 none
   int32_t fstat;              // final row status (finalize)
-  uint32_t res_count;         // tokens the stream kernel left to the lexicon pass
-  uint32_t walk_count;        // tokens the stream kernel left to the byte walk
   uint32_t cls_base, n_cls;   // the row's lexer state's class records
   uint32_t slot_id;           // the row's lexicon slot
-  uint32_t pad[14];
+  uint32_t pad[16];
 };
 static_assert(sizeof(RowHeader) == 320, "row header is 320 bytes");
 
@@ -176,7 +175,7 @@ struct Post {                 // stack after shifting one allowed terminal
 static_assert(sizeof(Post) == 32, "post entry is 32 bytes");
 
 struct RowLayout {
-  size_t cls, win, block, post, a2, vcode, vrule, lexl, walkl, slow, slow_ov, total;
+  size_t cls, win, block, post, a2, vcode, vrule, rbits, rcls, slow, slow_ov, total;
 };
 
 __host__ __device__ inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u; }
@@ -185,10 +184,12 @@ __host__ __device__ inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u;
 // the winner's shift (one byte per DFA state each); the top kWalkWin states
 // of the stack; [block ends here]; post-shift stacks and allowed sets of the
 // allowed terminals; the class verdicts (2 bits per class of the row's lexer
-// state) and lexicon shortcuts (a byte per class); the lexicon list ((token id, class) pairs the stream kernel left
-// to the lexicon pass) and the walk list (token ids left to the byte walk);
-// the slow path's list and stack areas.
-__host__ __device__ inline RowLayout row_layout(int T, int S, int V, int max_classes) {
+// state) and lexicon shortcuts (a byte per class); the residue bitmaps (one
+// bit per spelling the stream kernel left to the residue pass, in spelling
+// order: first those the lexicon decides, then those the byte walk decides)
+// and the class of each such spelling (u16); the slow path's list and stack
+// areas.
+__host__ __device__ inline RowLayout row_layout(int T, int S, int U, int max_classes) {
   RowLayout L;
   size_t o = sizeof(RowHeader);
   L.cls = o;
@@ -204,10 +205,10 @@ __host__ __device__ inline RowLayout row_layout(int T, int S, int V, int max_cla
   o += (size_t)pad16(((uint32_t)max_classes + 3u) / 4u);
   L.vrule = o;
   o += (size_t)pad16((uint32_t)max_classes);
-  L.lexl = o;
-  o += (size_t)V * 8;
-  L.walkl = o;
-  o += (size_t)V * 4;
+  L.rbits = o;
+  o += (size_t)((U + 63) / 64) * 16;
+  L.rcls = o;
+  o += (size_t)pad16((uint32_t)U * 2u);
   L.slow = o;
   o += kSlowCap * 4;
   L.slow_ov = o;
@@ -216,7 +217,7 @@ __host__ __device__ inline RowLayout row_layout(int T, int S, int V, int max_cla
   return L;
 }
 
-__host__ __device__ inline RowLayout row_layout(const Tables& tb) { return row_layout(tb.T, tb.S, tb.V, tb.max_classes); }
+__host__ __device__ inline RowLayout row_layout(const Tables& tb) { return row_layout(tb.T, tb.S, tb.U, tb.max_classes); }
 
 // Several global -> LDS copies (each region 16-byte aligned) in one pass:
 // the regions' 16-byte chunks are numbered consecutively and every thread
@@ -839,8 +840,10 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     cache_hit = -1;
     hacc[0] = 0;
     hacc[1] = 0;
-    hdr->res_count = 0;
-    hdr->walk_count = 0;
+  }
+  {
+    uint64_t* rb = (uint64_t*)(rw + L.rbits);
+    for (int i = tid; i < 2 * ((tb.U + 63) / 64); i += kBlock) rb[i] = 0ull;
   }
   __syncthreads();
   const uint32_t depth = cfg.stk_depth;
@@ -1276,7 +1279,8 @@ constexpr uint32_t kLexOpen = 0xFFFFFFFFu, kLexOut = 0xFFFFFFFEu;
 // Verdict of one lexeme-program class for a row.  The lexemes the token
 // ends are judged in order against the allowed set the parser has at that
 // point: A(sigma) before any shift, the prologue's allowed set after the
-// first shift (a2, a2_stride words per terminal), unknown after a second
+// first shift (a2, a2_stride words per terminal; the live sets have
+// live_stride words per DFA state), unknown after a second
 // one.  Each ended lexeme's winner is the first accept-list entry (priority
 // order) that is ignored or allowed and, for a restricted terminal, whose
 // category has the lexeme as a word (section 2, L3); the trailing lexeme
@@ -1285,10 +1289,12 @@ constexpr uint32_t kLexOpen = 0xFFFFFFFFu, kLexOut = 0xFFFFFFFEu;
 // category (Definition 2).  An ignored unrestricted terminal live there
 // accepts it under any stack.  Lexicon flags come from lex.word(i) (lexeme
 // i) and lex.trail(); a lexeme after two shifts and a token with more
-// recorded ends than the record holds are left to the byte walk.
-template <int MW, class Lex>
+// recorded ends than the record holds are left to the byte walk.  With Reg,
+// the row's allowed, restricted and ignored sets are first copied to
+// registers (fewer dependent LDS reads, more registers).
+template <int MW, class Lex, bool Reg = true>
 __device__ __forceinline__ uint32_t class_verdict(const RowHeader& h, const uint32_t* I, const uint32_t* live,
-                                                  const uint32_t* tinfo, const uint32_t* acc_off,
+                                                  int live_stride, const uint32_t* tinfo, const uint32_t* acc_off,
                                                   const uint8_t* acc_list, const uint32_t* a2, int a2_stride,
                                                   uint4 rec, Lex& lex) {
   const uint32_t w0 = rec.x;
@@ -1296,6 +1302,25 @@ __device__ __forceinline__ uint32_t class_verdict(const RowHeader& h, const uint
   if (w0 & kClassWalk) return kVerdictWalk;
   const uint32_t ends = w0 & kClassEndsMask;
   const uint32_t qe[kClassEnds] = {rec.y >> 16, rec.z & 0xFFFFu, rec.z >> 16};
+  // the row's sets: 0 allowed A(sigma), 1 restricted R, 2 ignored I
+  uint32_t Ar[MW], Rr[MW], Ir[MW];
+  if constexpr (Reg) {
+#pragma unroll
+    for (int w = 0; w < MW; ++w) {
+      Ar[w] = h.A[w];
+      Rr[w] = h.R[w];
+      Ir[w] = I[w];
+    }
+  }
+  auto bit = [&](int which, int c) -> bool {
+    if constexpr (!Reg) return bit_of(which == 0 ? h.A : (which == 1 ? h.R : I), c);
+    const uint32_t* set = which == 0 ? Ar : (which == 1 ? Rr : Ir);
+    uint32_t word = 0;
+#pragma unroll
+    for (int w = 0; w < MW; ++w)
+      if (w == (c >> 5)) word = set[w];
+    return (word >> (c & 31)) & 1u;
+  };
   int sel = -1;  // allowed set now: -1 A(sigma), t >= 0 after shifting t, -2 unknown
   const uint32_t nchk = ends > (uint32_t)kClassEnds ? (uint32_t)kClassEnds : ends;
   for (uint32_t i = 0; i < nchk; ++i) {
@@ -1310,9 +1335,9 @@ __device__ __forceinline__ uint32_t class_verdict(const RowHeader& h, const uint
       uint32_t wf = kLexOpen;  // the lexeme's lexicon flags, asked for at most once
       for (uint32_t j = acc_off[q]; j < acc_off[q + 1]; ++j) {
         const int c = acc_list[j];
-        const bool ok = bit_of(I, c) || (sel == -1 ? bit_of(h.A, c) : bit_of(a2 + sel * a2_stride, c));
+        const bool ok = bit(2, c) || (sel == -1 ? bit(0, c) : bit_of(a2 + sel * a2_stride, c));
         if (!ok) continue;
-        if (bit_of(h.R, c)) {
+        if (bit(1, c)) {
           if (wf == kLexOpen) wf = lex.word(i);
           if (wf == kLexOpen) return kVerdictLexicon;
           if (wf == kLexOut) return kVerdictWalk;
@@ -1322,22 +1347,23 @@ __device__ __forceinline__ uint32_t class_verdict(const RowHeader& h, const uint
         break;
       }
       if (t < 0) return kVerdictReject;
-      if (bit_of(I, t)) continue;
+      if (bit(2, t)) continue;
     }
     sel = sel == -1 ? t : -2;
   }
   if (ends > (uint32_t)kClassEnds) return kVerdictWalk;
-  const uint32_t* lv = live + (size_t)(rec.y & 0xFFFFu) * MW;
+  const uint32_t* lv = live + (size_t)(rec.y & 0xFFFFu) * live_stride;
   uint32_t unres = 0, res = 0, ign = 0;
   uint32_t rw[MW];  // restricted terminals that keep the trailing lexeme viable
 #pragma unroll
   for (int w = 0; w < MW; ++w) {
-    const uint32_t acur = sel == -1 ? h.A[w] : (sel >= 0 ? a2[sel * a2_stride + w] : 0u);
-    const uint32_t bits = lv[w] & (acur | I[w]);
-    unres |= bits & ~h.R[w];
-    rw[w] = bits & h.R[w];
+    const uint32_t Aw = Reg ? Ar[w] : h.A[w], Rw = Reg ? Rr[w] : h.R[w], Iw = Reg ? Ir[w] : I[w];
+    const uint32_t acur = sel == -1 ? Aw : (sel >= 0 ? a2[sel * a2_stride + w] : 0u);
+    const uint32_t bits = lv[w] & (acur | Iw);
+    unres |= bits & ~Rw;
+    rw[w] = bits & Rw;
     res |= rw[w];
-    ign |= lv[w] & I[w] & ~h.R[w];
+    ign |= lv[w] & Iw & ~Rw;
   }
   if (ign || (sel != -2 && unres)) return kVerdictAllow;
   if (sel == -2) return kVerdictWalk;
@@ -1415,73 +1441,114 @@ __device__ __forceinline__ uint32_t class_shortcut(const RowHeader& h, const uin
                                                    const uint32_t* tinfo, const uint32_t* acc_off,
                                                    const uint8_t* acc_list, const uint32_t* a2, uint4 rec) {
   LexNo ln{rec.w, rec.x & kClassEndsMask, h.rem_len == 0, -1, -1, false, false};
-  const uint32_t v = class_verdict<MW>(h, I, live, tinfo, acc_off, acc_list, a2, MW, rec, ln);
+  const uint32_t v = class_verdict<MW>(h, I, live, 8, tinfo, acc_off, acc_list, a2, 8, rec, ln);
   if (ln.kind < 0 || ln.second || v == kVerdictLexicon) return kVerdictLexicon;
   if (ln.pending) return kVerdictLexicon | v << 5 | kNoValid;
   if (ln.start < 0) return kVerdictLexicon;
   return kVerdictLexicon | (ln.kind == 0 ? 1u : 2u) << 2 | (uint32_t)ln.start << 4 | v << 5 | kNoValid;
 }
 
-// Workgroups (row, y): the verdicts of the row's classes, four per thread
-// (one byte of the 2-bit verdict table), workgroup y taking every
-// gridDim.y-th group of kBlock of them; a class the lexicon decides also gets
-// its shortcut byte.  The row's allowed sets, the accept lists and
-// the live sets are staged in LDS first.
+// LDS layout of the verdict kernel: live sets and the row's allowed sets
+// after one shift (8 words per DFA state / terminal), terminal info, accept
+// lists.
+struct VerdictLds {
+  uint32_t live, a2, tinfo, acc_off, acc_list, total;
+};
+
+__host__ __device__ inline VerdictLds verdict_lds(const Tables& tb) {
+  VerdictLds L;
+  uint32_t o = 0;
+  L.live = o;
+  o += (uint32_t)tb.S * 32u;
+  L.a2 = o;
+  o += (uint32_t)tb.T * 32u;
+  L.tinfo = o;
+  o += pad16((uint32_t)tb.T * 4u);
+  L.acc_off = o;
+  o += pad16((uint32_t)(tb.S + 1) * 4u);
+  L.acc_list = o;
+  o += pad16((uint32_t)tb.n_acc);
+  L.total = o;
+  return L;
+}
+
+// Two 16-bit masks interleaved bit by bit: bit i of a goes to bit 2i, bit i
+// of b to bit 2i + 1.
+__device__ inline uint32_t interleave16(uint32_t a, uint32_t b) {
+  auto spread = [](uint32_t x) {
+    x &= 0xFFFFu;
+    x = (x | (x << 8)) & 0x00FF00FFu;
+    x = (x | (x << 4)) & 0x0F0F0F0Fu;
+    x = (x | (x << 2)) & 0x33333333u;
+    x = (x | (x << 1)) & 0x55555555u;
+    return x;
+  };
+  return spread(a) | spread(b) << 1;
+}
+
+// Workgroups (row, y): the verdicts of the row's classes, one class per
+// thread, workgroup y taking every gridDim.y-th group of kBlock classes; each
+// wave packs its 64 two-bit codes with two ballots.  A class the lexicon
+// decides also gets its shortcut byte.  The row's allowed sets after one
+// shift, the accept lists, the live sets and the terminal info are staged in
+// LDS first (one batched pass).
 template <int MW>
 __global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __restrict__ ws, size_t rbytes) {
   extern __shared__ __align__(16) uint8_t vlds[];
   __shared__ RowHeader h;
   __shared__ uint32_t I_s[8];
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
   uint8_t* rw = ws + kWsHead + (size_t)blockIdx.x * rbytes;
   if (tid < (int)(sizeof(RowHeader) / 4)) ((uint32_t*)&h)[tid] = ((const uint32_t*)rw)[tid];
   __syncthreads();
-  const uint32_t ngroups = (h.n_cls + 3u) / 4u;  // four classes per thread
-  if (h.valid != kRowValid || blockIdx.y * (uint32_t)kBlock >= ngroups) return;  // uniform
+  const uint32_t n = h.n_cls;
+  if (h.valid != kRowValid || blockIdx.y * (uint32_t)kBlock >= n) return;  // uniform
   const RowLayout RL = row_layout(tb);
-  uint32_t* live_s = (uint32_t*)vlds;
-  uint32_t* a2_s = live_s + tb.S * MW;
-  uint32_t* tinfo_s = a2_s + tb.T * MW;
-  uint32_t* acc_off_s = tinfo_s + tb.T;
-  uint8_t* acc_list_s = (uint8_t*)(acc_off_s + tb.S + 1);
-  const uint32_t* a2g = (const uint32_t*)(rw + RL.a2);
-  for (int i = tid; i < tb.S * MW; i += kBlock) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
-  for (int i = tid; i < tb.T * MW; i += kBlock) a2_s[i] = a2g[(i / MW) * 8 + i % MW];
-  for (int i = tid; i < tb.T; i += kBlock) tinfo_s[i] = tb.term_info[i];
-  for (int i = tid; i <= tb.S; i += kBlock) acc_off_s[i] = tb.acc_off[i];
-  for (int i = tid; i < tb.n_acc; i += kBlock) acc_list_s[i] = tb.acc_list[i];
+  const VerdictLds VL = verdict_lds(tb);
+  uint32_t* live_s = (uint32_t*)(vlds + VL.live);
+  uint32_t* a2_s = (uint32_t*)(vlds + VL.a2);
+  uint32_t* tinfo_s = (uint32_t*)(vlds + VL.tinfo);
+  uint32_t* acc_off_s = (uint32_t*)(vlds + VL.acc_off);
+  uint8_t* acc_list_s = vlds + VL.acc_list;
+  {
+    const StageRegion rg[5] = {{(const uint8_t*)tb.live, (uint8_t*)live_s, (uint32_t)tb.S * 32u},
+                               {rw + RL.a2, (uint8_t*)a2_s, (uint32_t)tb.T * 32u},
+                               {(const uint8_t*)tb.term_info, (uint8_t*)tinfo_s, (uint32_t)tb.T * 4u},
+                               {(const uint8_t*)tb.acc_off, (uint8_t*)acc_off_s, (uint32_t)(tb.S + 1) * 4u},
+                               {tb.acc_list, acc_list_s, (uint32_t)tb.n_acc}};
+    stage_regions<5, 4>(rg, tid, kBlock);
+  }
+  __syncthreads();
   if (tid < 8) {
     uint32_t iw = 0;
     for (int j = 0; j < 32; ++j) {
       const int t = tid * 32 + j;
-      if (t < tb.T && (tb.term_info[t] & 1u)) iw |= 1u << j;
+      if (t < tb.T && (tinfo_s[t] & 1u)) iw |= 1u << j;
     }
     I_s[tid] = iw;
   }
   __syncthreads();
-  uint8_t* vc = rw + RL.vcode;
+  uint32_t* vc = (uint32_t*)(rw + RL.vcode);
   uint8_t* vr = rw + RL.vrule;
-  const uint4* rec = tb.crec + h.cls_base;
-  for (uint32_t j = blockIdx.y * kBlock + tid; j < ngroups; j += gridDim.y * kBlock) {
-    uint4 r[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) r[k] = 4 * j + k < h.n_cls ? rec[4 * j + k] : make_uint4(kClassReject, 0, 0, 0);
-    uint32_t code = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
+  for (uint32_t c0 = blockIdx.y * kBlock; c0 < n; c0 += gridDim.y * kBlock) {  // uniform
+    const uint32_t c = c0 + tid;
+    uint32_t code = kVerdictReject;
+    if (c < n) {
+      const uint4 rec = tb.crec[h.cls_base + c];
       LexOpen lex;
-      const uint32_t v = class_verdict<MW>(h, I_s, live_s, tinfo_s, acc_off_s, acc_list_s, a2_s, MW, r[k], lex);
-      code |= v << (2 * k);
-      if (v == kVerdictLexicon)
-        vr[4 * j + k] = (uint8_t)class_shortcut<MW>(h, I_s, live_s, tinfo_s, acc_off_s, acc_list_s, a2_s, r[k]);
+      code = class_verdict<MW>(h, I_s, live_s, 8, tinfo_s, acc_off_s, acc_list_s, a2_s, 8, rec, lex);
+      if (code == kVerdictLexicon)
+        vr[c] = (uint8_t)class_shortcut<MW>(h, I_s, live_s, tinfo_s, acc_off_s, acc_list_s, a2_s, rec);
     }
-    vc[j] = (uint8_t)code;
+    const uint64_t b0 = __ballot(code & 1u), b1 = __ballot(code & 2u);
+    // this wave's 64 classes are words (c0 + 64 * wave) / 16 .. + 3 of the table
+    if (lane < 4) {
+      const uint32_t first = c0 + (uint32_t)(tid & ~63) + 16u * (uint32_t)lane;
+      if (first < n) vc[first >> 4] = interleave16((uint32_t)(b0 >> (16 * lane)), (uint32_t)(b1 >> (16 * lane)));
+    }
   }
 }
 
-__host__ __device__ inline uint32_t verdict_lds(const Tables& tb, int mw) {
-  return pad16((uint32_t)(tb.S + tb.T) * (uint32_t)mw * 4u + (uint32_t)(tb.T + tb.S + 1) * 4u + (uint32_t)tb.n_acc);
-}
 
 // ------------------------------------------------------------------ stream
 // The mask in token-id order straight from the class map.  Workgroup i runs
@@ -1492,11 +1559,9 @@ __host__ __device__ inline uint32_t verdict_lds(const Tables& tb, int mw) {
 // row may end).  A token whose class the lexicon decides takes the class's
 // shortcut verdict when the answer to the class's first lexicon question is
 // "no flags" for it (from its first byte and the row's continuation table, or
-// from its token-flag entry); otherwise it is appended to the row's lexicon
-// list with its class.  Tokens whose class needs the byte
-// walk go to the walk list (one atomic per list, workgroup and round).  Rows
-// served from the mask cache are skipped; rows with a bad configuration get
-// zero words.
+// from its token-flag entry).  Every other undecided token marks its
+// spelling in the row's residue bitmap.  Rows served from the mask cache are
+// skipped; rows with a bad configuration get zero words.
 constexpr int kStreamWaves = kBlock / 64;
 constexpr int kStreamUnroll = 4;   // chunks per wave in flight
 constexpr int kStreamRounds = 4;
@@ -1508,8 +1573,6 @@ __host__ __device__ inline int stream_groups(int V) { return (stream_slices(V) +
 __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __restrict__ mask,
                                                         uint8_t* __restrict__ ws, size_t rbytes, int B) {
   extern __shared__ __align__(16) uint32_t vc_s[];
-  __shared__ uint32_t wtot[2][kStreamWaves];
-  __shared__ uint32_t base_s[2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int x = (int)(blockIdx.x & 7u);
   const int g = (int)(blockIdx.x >> 3);
@@ -1539,84 +1602,69 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
   const uint16_t* cm = tb.cmap + (size_t)q * tb.V;
   const uint32_t* tflags = tb.lex_token + (size_t)hdr->slot_id * tb.V;
   const uint8_t* vrule = rw + RL.vrule;
+  unsigned long long* rbits = (unsigned long long*)(rw + RL.rbits);
   uint32_t cont[8];
 #pragma unroll
   for (int w = 0; w < 8; ++w) cont[w] = hdr->cont[w];
-  uint2* lexl = (uint2*)(rw + RL.lexl);
-  uint32_t* walkl = (uint32_t*)(rw + RL.walkl);
-  const uint64_t below = (1ull << lane) - 1ull;
   bool any = false;
-  __syncthreads();
-  for (int rd = 0; rd < kStreamRounds; ++rd) {
-    const int c0 = c_lo + rd * kStreamWaves * kStreamUnroll + wave;
-    uint32_t cls[kStreamUnroll];
+  constexpr int kPer = kStreamRounds * kStreamUnroll;  // chunks per wave
+  // pass 1: class ids of all of this wave's chunks (loads in flight together)
+  uint32_t cls[kPer];
 #pragma unroll
-    for (int j = 0; j < kStreamUnroll; ++j) {
-      const int c = c0 + j * kStreamWaves;
-      const int id = c * 64 + lane;
-      cls[j] = (c < c_hi && id < tb.V) ? (uint32_t)cm[id] : 0u;
-    }
-    uint64_t lexb[kStreamUnroll], walkb[kStreamUnroll];
-    uint32_t nlex = 0, nwalk = 0;
-#pragma unroll
-    for (int j = 0; j < kStreamUnroll; ++j) {
-      const int c = c0 + j * kStreamWaves;
-      lexb[j] = walkb[j] = 0;
-      if (c >= c_hi) continue;  // uniform across the wave
-      const int id = c * 64 + lane;
-      uint32_t code = (vc_s[cls[j] >> 4] >> ((cls[j] & 15u) * 2u)) & 3u;
-      if (__ballot(code == kVerdictLexicon)) {  // uniform: lexicon shortcuts
-        if (code == kVerdictLexicon && id < tb.V) {
-          const uint32_t sc = vrule[cls[j]];
-          if (sc & kNoValid) {
-            const uint32_t kind = (sc >> 2) & 3u;
-            bool no;
-            if (kind == 0) {
-              const uint32_t b = tb.id_first[id];
-              no = !((cont[b >> 5] >> (b & 31u)) & 1u);
-            } else {
-              no = ((tflags[id] >> (16 * ((sc >> 4) & 1u) + (kind == 2 ? 8u : 0u))) & 0xFFu) == 0u;
-            }
-            if (no) code = (sc >> 5) & 3u;
-          }
-        }
-      }
-      const uint64_t al = __ballot(code == kVerdictAllow || id == eos);
-      lexb[j] = __ballot(code == kVerdictLexicon && id < tb.V);
-      walkb[j] = __ballot(code == kVerdictWalk && id < tb.V);
-      nlex += (uint32_t)__popcll(lexb[j]);
-      nwalk += (uint32_t)__popcll(walkb[j]);
-      any = any || al != 0;
-      if (lane < 2 && 2 * c + lane < tb.W) mrow[2 * c + lane] = (uint32_t)(al >> (32 * lane));
-    }
-    // this round's list entries: one atomic per list for the workgroup
-    if (lane == 0) {
-      wtot[0][wave] = nlex;
-      wtot[1][wave] = nwalk;
-    }
-    __syncthreads();
-    if (tid < 2) {
-      uint32_t tot = 0;
-      for (int w = 0; w < kStreamWaves; ++w) tot += wtot[tid][w];
-      base_s[tid] = tot ? atomicAdd(tid == 0 ? &hdr->res_count : &hdr->walk_count, tot) : 0u;
-    }
-    __syncthreads();
-    uint32_t pl = base_s[0], pw = base_s[1];
-    for (int w = 0; w < wave; ++w) {
-      pl += wtot[0][w];
-      pw += wtot[1][w];
-    }
-    __syncthreads();  // wtot and base_s are reused by the next round
-    if (nlex == 0 && nwalk == 0) continue;  // uniform across the wave
-#pragma unroll
-    for (int j = 0; j < kStreamUnroll; ++j) {
-      const uint32_t id = (uint32_t)((c0 + j * kStreamWaves) * 64 + lane);
-      if ((lexb[j] >> lane) & 1ull) lexl[pl + (uint32_t)__popcll(lexb[j] & below)] = make_uint2(id, cls[j]);
-      if ((walkb[j] >> lane) & 1ull) walkl[pw + (uint32_t)__popcll(walkb[j] & below)] = id;
-      pl += (uint32_t)__popcll(lexb[j]);
-      pw += (uint32_t)__popcll(walkb[j]);
-    }
+  for (int j = 0; j < kPer; ++j) {
+    const int c = c_lo + wave + j * kStreamWaves;
+    const int id = c * 64 + lane;
+    cls[j] = (c < c_hi && id < tb.V) ? (uint32_t)cm[id] : 0u;
   }
+  __syncthreads();
+  // pass 2: codes; for a class the lexicon decides, its shortcut byte and the
+  // token's first byte and token flags (again all loads in flight together)
+  uint32_t code[kPer], sc[kPer], fb[kPer], tf[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int c = c_lo + wave + j * kStreamWaves;
+    const int id = c * 64 + lane;
+    code[j] = c < c_hi ? (vc_s[cls[j] >> 4] >> ((cls[j] & 15u) * 2u)) & 3u : kVerdictReject;
+    const bool lexq = code[j] == kVerdictLexicon && id < tb.V;
+    sc[j] = lexq ? vrule[cls[j]] : 0u;
+    fb[j] = lexq ? tb.id_first[id] : 0u;
+    tf[j] = lexq ? tflags[id] : 0u;
+  }
+  // pass 3: shortcut verdicts, mask words, residue ids
+  uint32_t resu[kPer];  // this lane's residue ids (or ~0)
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int c = c_lo + wave + j * kStreamWaves;
+    const int id = c * 64 + lane;
+    resu[j] = 0xFFFFFFFFu;
+    if (c >= c_hi) continue;  // uniform across the wave
+    uint32_t cd = code[j];
+    if (cd == kVerdictLexicon && (sc[j] & kNoValid)) {
+      const uint32_t kind = (sc[j] >> 2) & 3u;
+      const bool no = kind == 0 ? !((cont[fb[j] >> 5] >> (fb[j] & 31u)) & 1u)
+                                : ((tf[j] >> (16 * ((sc[j] >> 4) & 1u) + (kind == 2 ? 8u : 0u))) & 0xFFu) == 0u;
+      if (no) cd = (sc[j] >> 5) & 3u;
+    }
+    const uint64_t al = __ballot(cd == kVerdictAllow || id == eos);
+    any = any || al != 0;
+    if (lane < 2 && 2 * c + lane < tb.W) mrow[2 * c + lane] = (uint32_t)(al >> (32 * lane));
+    if (cd >= kVerdictWalk && id < tb.V) resu[j] = (uint32_t)id;
+    code[j] = cd;
+  }
+  // mark the residue spellings in the row's bitmaps (lexicon or byte walk)
+  // and record their class, last, so no load above waits behind these
+  // atomics; the spelling lookups are issued together
+#pragma unroll
+  for (int k2 = 0; k2 < kPer; ++k2) resu[k2] = resu[k2] != 0xFFFFFFFFu ? tb.spell_of_id[resu[k2]] : 0xFFFFFFFFu;
+  const uint32_t nsub = ((uint32_t)tb.U + 63u) / 64u;
+  uint16_t* rcls = (uint16_t*)(rw + RL.rcls);
+#pragma unroll
+  for (int k2 = 0; k2 < kPer; ++k2)
+    if (resu[k2] != 0xFFFFFFFFu) {
+      const uint32_t u = resu[k2];
+      rcls[u] = (uint16_t)cls[k2];
+      atomicOr(rbits + (code[k2] == kVerdictWalk ? nsub : 0u) + (u >> 6), 1ull << (u & 63u));
+    }
   if (lane == 0 && any) hdr->nonempty = 1u;
 }
 
@@ -1629,7 +1677,7 @@ __device__ inline int wave_grab(int* ctr) {
 }
 
 struct ResLds {  // byte offsets into dynamic LDS
-  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, live, lanes, pre, rows, total;
+  uint32_t dfa, bcls, tinfo, I, acc_off, acc_list, parse, live, lanes, umask, upre, rows, total;
   uint32_t block;  // bytes per resident row: header, trailing-flag tables, stack window
   int group;       // rows per group
   ParseLds pl;
@@ -1657,8 +1705,10 @@ __host__ __device__ inline ResLds res_lds(const Tables& tb, int mw, int B) {
   o += pad16((uint32_t)(tb.S * mw * 4));
   w.lanes = o;
   o += kWalkThreads * kFastLane * 2;
-  w.pre = o;  // walk chunk prefix counts of the group's rows
-  o += (kRowGroup + 4) * 4;
+  w.umask = o;  // per work item: its residue bitmap word
+  o += kMaxItems * 8;
+  w.upre = o;   // prefix counts of residue spellings over the items
+  o += (kMaxItems + 4) * 4;
   const uint32_t fixed = o + 64;
   w.block = (uint32_t)row_layout(tb).block;
   int g = kRowGroup < B ? kRowGroup : B;
@@ -1684,21 +1734,18 @@ struct WalkShared {
   const uint16_t* pool;
 };
 
-// Verdict of one token left to the byte walk: byte 0 (continuing the pending
-// lexeme, or ending it with the prologue's winner and starting a new one),
-// then the byte-by-byte walk of the rest with emissions, overlay shifts and
-// lexicon checks.  A lane whose stack area is too small hands its token to
-// the slow path.  1 allowed, 0 rejected or handed over.
+// Verdict of one spelling left to the byte walk: byte 0 (continuing the
+// pending lexeme, or ending it with the prologue's winner and starting a new
+// one), then the byte-by-byte walk of the rest with emissions, overlay shifts
+// and lexicon checks.  A lane whose stack area is too small hands its
+// spelling to the slow path.  1 allowed, 0 rejected or handed over.
 template <int MW>
 __device__ __forceinline__ int residue_lane(const WalkShared<MW>& sh, const RowHeader& h, const uint8_t* rowblk,
-                                            uint8_t* rw, const RowLayout& RL, int id,
-                                            mptr<true, uint16_t> lane_area) {
+                                            uint8_t* rw, const RowLayout& RL, uint32_t u, const uint4& rk,
+                                            const uint4& tl, mptr<true, uint16_t> lane_area) {
   const Tables& tb = *sh.tb;
   const uint8_t* clsA = rowblk + sizeof(RowHeader);
   const uint8_t* clsW = clsA + pad16((uint32_t)tb.S);
-  const uint32_t u = tb.spell_of_id[id];
-  const uint4 rk = tb.spell_rec[u];
-  const uint4 tl = tb.spell_tail[u];
   const uint32_t n = rk.w & 0xFFu;
   const uint64_t hb = (uint64_t)rk.x | (uint64_t)rk.y << 32;
   const uint32_t b0 = (uint32_t)(hb & 0xFF);
@@ -1765,7 +1812,7 @@ __device__ __forceinline__ int residue_lane(const WalkShared<MW>& sh, const RowH
   if (ok < 0) {  // the lane's stack area is too small: hand over
     RowHeader* gh = (RowHeader*)rw;
     const uint32_t slot = atomicAdd(&gh->slow_count, 1u);
-    if (slot < (uint32_t)kSlowCap) ((uint32_t*)(rw + RL.slow))[slot] = (uint32_t)id;
+    if (slot < (uint32_t)kSlowCap) ((uint32_t*)(rw + RL.slow))[slot] = u;
     else atomicOr(&gh->wstat, GRID_ROW_OVERFLOW);
     ok = 0;
   }
@@ -1832,128 +1879,83 @@ struct LexLane {
   }
 };
 
-// Workgroups (x, y): row group y (kRowGroup rows) and every gridDim.x-th
-// share of the group's lexicon lists, concatenated, kLexPer (token, class)
-// entries per thread at a time -- so one long list is spread over all
-// workgroups.  Each token's class verdict is taken again with the token's
-// own lexemes' lexicon flags (token-flag table, prefix and stride tables);
-// tokens whose lexemes are out of the tables' reach are appended to the walk
-// list.  The accept lists, live sets and terminal info are staged in LDS;
-// row headers and the allowed sets after one shift are read from the
-// workspace.
-constexpr int kLexPer = 2;
+// Verdict of one spelling of the residue bitmaps: for a spelling of the
+// lexicon bitmap, its class cls (recorded by the stream kernel) is taken
+// again with its own lexemes' lexicon flags (token-flag table, prefix and
+// stride tables); the byte walk decides the rest.  1 allowed, 0 rejected or
+// handed over.
 template <int MW>
-__global__ __launch_bounds__(kBlock) void lexicon_kernel(Tables tb, uint32_t* __restrict__ mask,
-                                                         uint8_t* __restrict__ ws, size_t rbytes, int B) {
-  extern __shared__ __align__(16) uint8_t xlds[];
-  __shared__ uint32_t I_s[8];
-  __shared__ uint32_t pre_s[kRowGroup + 1];
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int g0 = (int)blockIdx.y * kRowGroup, gr = min(kRowGroup, B - g0);
-  uint8_t* rows = ws + kWsHead;
-  if (tid < gr) {
-    const RowHeader* h = (const RowHeader*)(rows + (size_t)(g0 + tid) * rbytes);
-    pre_s[tid + 1] = h->valid == kRowValid ? h->res_count : 0u;
+__device__ __forceinline__ int residue_token(const WalkShared<MW>& sh, const RowHeader& h, const uint8_t* rowblk,
+                                             uint8_t* rw, const RowLayout& RL, uint32_t u, const uint4& rk,
+                                             bool lexicon, uint32_t cls, mptr<true, uint16_t> lane_area) {
+  const Tables& tb = *sh.tb;
+  const uint32_t id0 = rk.z & 0x7FFFFFFFu;
+  const uint32_t n = rk.w & 0xFFu;
+  const uint4 tl = tb.spell_tail[u];
+  if (lexicon) {
+    const uint4 rec = tb.crec[h.cls_base + cls];
+    LexLane lx;
+    lx.tb = &tb;
+    lx.sl = slot_of(h.slot);
+    lx.n = n;
+    lx.b0 = (uint64_t)rk.x | (uint64_t)rk.y << 32;
+    lx.b1 = n > 8 ? (uint64_t)tl.x | (uint64_t)tl.y << 32 : 0ull;
+    lx.b2 = n > 8 ? (uint64_t)tl.z | (uint64_t)tl.w << 32 : 0ull;
+    lx.ends = rec.x & kClassEndsMask;
+    lx.pos = rec.w;
+    lx.rem = (uint64_t)h.rem_lo | (uint64_t)h.rem_hi << 32;
+    lx.rem_len = h.rem_len;
+    lx.lexnode = h.lexnode;
+    lx.tf = tb.lex_token[(size_t)h.slot_id * tb.V + id0];
+    const uint32_t v = class_verdict<MW, LexLane, false>(h, sh.I, sh.live, MW, sh.tinfo, sh.acc_off, sh.acc_list,
+                                                         (const uint32_t*)(rw + RL.a2), 8, rec, lx);
+    if (v == kVerdictAllow) return 1;
+    if (v == kVerdictReject) return 0;
   }
-  __syncthreads();
-  if (tid == 0) {
-    pre_s[0] = 0;
-    for (int r = 1; r <= gr; ++r) pre_s[r] += pre_s[r - 1];
+  return residue_lane<MW>(sh, h, rowblk, rw, RL, u, rk, tl, lane_area);
+}
+
+// Sets the mask bit of every id that spells u (its alias ids).
+__device__ inline void allow_spelling(const Tables& tb, uint32_t* mrow, uint32_t u, const uint4& rk) {
+  if (!(rk.z >> 31)) {
+    const uint32_t id = rk.z;
+    atomicOr(mrow + (id >> 5), 1u << (id & 31u));
+    return;
   }
-  __syncthreads();
-  const uint32_t n = pre_s[gr];
-  if (blockIdx.x * (uint32_t)(kBlock * kLexPer) >= n) return;  // uniform
-  const RowLayout RL = row_layout(tb);
-  uint32_t* live_s = (uint32_t*)xlds;
-  uint32_t* tinfo_s = live_s + tb.S * MW;
-  uint32_t* acc_off_s = tinfo_s + tb.T;
-  uint8_t* acc_list_s = (uint8_t*)(acc_off_s + tb.S + 1);
-  for (int i = tid; i < tb.S * MW; i += kBlock) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
-  for (int i = tid; i < tb.T; i += kBlock) tinfo_s[i] = tb.term_info[i];
-  for (int i = tid; i <= tb.S; i += kBlock) acc_off_s[i] = tb.acc_off[i];
-  for (int i = tid; i < tb.n_acc; i += kBlock) acc_list_s[i] = tb.acc_list[i];
-  if (tid < 8) {
-    uint32_t iw = 0;
-    for (int j = 0; j < 32; ++j) {
-      const int t = tid * 32 + j;
-      if (t < tb.T && (tb.term_info[t] & 1u)) iw |= 1u << j;
-    }
-    I_s[tid] = iw;
-  }
-  __syncthreads();
-  const uint32_t step = gridDim.x * (uint32_t)(kBlock * kLexPer);
-  for (uint32_t e0 = blockIdx.x * (uint32_t)(kBlock * kLexPer); e0 < n; e0 += step) {  // uniform
-    int row[kLexPer];
-    uint2 ent[kLexPer];
-    uint4 rec[kLexPer], rk[kLexPer], tl[kLexPer];
-    uint32_t tf[kLexPer];
-#pragma unroll
-    for (int k = 0; k < kLexPer; ++k) {
-      const uint32_t e = e0 + (uint32_t)(k * kBlock + tid);
-      int r = 0;  // the row holding entry e: last r with pre_s[r] <= e
-      while (r + 1 < gr && pre_s[r + 1] <= e) ++r;
-      row[k] = r;
-      const uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
-      ent[k] = e < n ? ((const uint2*)(rw + RL.lexl))[e - pre_s[r]] : make_uint2(0xFFFFFFFFu, 0u);
-    }
-#pragma unroll
-    for (int k = 0; k < kLexPer; ++k) {
-      const bool on = ent[k].x != 0xFFFFFFFFu;
-      const RowHeader* h = (const RowHeader*)(rows + (size_t)(g0 + row[k]) * rbytes);
-      rec[k] = on ? tb.crec[h->cls_base + ent[k].y] : make_uint4(kClassReject, 0, 0, 0);
-      const uint32_t u = on ? tb.spell_of_id[ent[k].x] : 0u;
-      tf[k] = on ? tb.lex_token[(size_t)h->slot_id * tb.V + ent[k].x] : 0u;
-      rk[k] = on ? tb.spell_rec[u] : make_uint4(0, 0, 0, 0);
-      tl[k] = on && (rk[k].w & 0xFFu) > 8 ? tb.spell_tail[u] : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int k = 0; k < kLexPer; ++k) {
-      const bool on = ent[k].x != 0xFFFFFFFFu;
-      const uint32_t id = ent[k].x;
-      uint8_t* rw = rows + (size_t)(g0 + row[k]) * rbytes;
-      RowHeader* hdr = (RowHeader*)rw;
-      uint32_t v = kVerdictReject;
-      if (on) {
-        const RowHeader& h = *hdr;
-        LexLane lx;
-        lx.tb = &tb;
-        lx.sl = slot_of(h.slot);
-        lx.n = rk[k].w & 0xFFu;
-        lx.b0 = (uint64_t)rk[k].x | (uint64_t)rk[k].y << 32;
-        lx.b1 = (uint64_t)tl[k].x | (uint64_t)tl[k].y << 32;
-        lx.b2 = (uint64_t)tl[k].z | (uint64_t)tl[k].w << 32;
-        lx.ends = rec[k].x & kClassEndsMask;
-        lx.pos = rec[k].w;
-        lx.rem = (uint64_t)h.rem_lo | (uint64_t)h.rem_hi << 32;
-        lx.rem_len = h.rem_len;
-        lx.lexnode = h.lexnode;
-        lx.tf = tf[k];
-        v = class_verdict<MW>(h, I_s, live_s, tinfo_s, acc_off_s, acc_list_s, (const uint32_t*)(rw + RL.a2), 8,
-                              rec[k], lx);
-      }
-      if (v == kVerdictAllow) {
-        atomicOr(mask + (size_t)(g0 + row[k]) * tb.W + (id >> 5), 1u << (id & 31));
-        hdr->nonempty = 1u;
-      }
-      if (v == kVerdictWalk) {  // rare: one atomic per token
-        const uint32_t slot = atomicAdd(&hdr->walk_count, 1u);
-        ((uint32_t*)(rw + RL.walkl))[slot] = id;
-      }
-    }
+  for (uint32_t a = tb.alias_off[u]; a < tb.alias_off[u + 1]; ++a) {
+    const uint32_t id = (uint32_t)tb.alias_ids[a];
+    atomicOr(mrow + (id >> 5), 1u << (id & 31u));
   }
 }
 
-__host__ __device__ inline uint32_t lexicon_lds(const Tables& tb, int mw) {
-  return pad16((uint32_t)tb.S * (uint32_t)mw * 4u + (uint32_t)(tb.T + tb.S + 1) * 4u + (uint32_t)tb.n_acc);
+// The rank-th set bit of m (rank < popcount(m)).
+__device__ inline int nth_set_bit(uint64_t m, int rank) {
+  int pos = 0;
+#pragma unroll
+  for (int w = 32; w >= 1; w >>= 1) {
+    const uint64_t low = m & ((1ull << w) - 1ull);
+    const int c = __popcll(low);
+    if (rank >= c) {
+      rank -= c;
+      m >>= w;
+      pos += w;
+    } else {
+      m = low;
+    }
+  }
+  return pos;
 }
 
-// Persistent, one workgroup per compute unit.  The grammar tables are staged
-// once; then, for each group of rows that fits, the rows' blocks (header,
-// trailing-flag tables, stack window, all written by the prologue) are copied
-// in one pass.  The group's walk lists, cut into chunks of 64 ids, are
-// dealt to the workgroups in turn and taken by each workgroup's waves from an
-// LDS counter; each lane walks one token and ORs its bit into the row's mask
-// word.
+// Persistent, one workgroup per compute unit.  For each group of rows that
+// fits, a work item is one row against 64 consecutive spellings (one word of
+// one of the row's residue bitmaps, byte-walk items first since they take
+// longest); workgroup b takes items b, b + gridDim.x, ...
+// and reads their words, then the set bits are packed 64 to a wave in
+// spelling order -- lexicographic neighbours walk alike, so a wave's lanes
+// diverge little.  The grammar tables and the group's row blocks (header,
+// trailing-flag tables, stack window) are staged in LDS only when the
+// workgroup has residue spellings.  Each lane judges one spelling and sets
+// the mask bits of its ids.
 template <int MW>
 __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const uint16_t* __restrict__ pool,
                                                                uint32_t* __restrict__ mask, uint8_t* __restrict__ ws,
@@ -1968,83 +1970,121 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
   uint32_t* tinfo_s = (uint32_t*)(lds + WL.tinfo);
   uint32_t* I_s = (uint32_t*)(lds + WL.I);
   uint32_t* live_s = (uint32_t*)(lds + WL.live);
-  uint32_t* pre_s = (uint32_t*)(lds + WL.pre);
+  uint64_t* umask_s = (uint64_t*)(lds + WL.umask);
+  uint32_t* upre_s = (uint32_t*)(lds + WL.upre);
   const uint32_t* acc_off_s = (const uint32_t*)(lds + WL.acc_off);
   const uint8_t* acc_list_s = lds + WL.acc_list;
   uint8_t* rows_s = lds + WL.rows;
   const mptr<true, uint16_t> lane_area = in_mem<true>((uint16_t*)(lds + WL.lanes) + tid * kFastLane);
   uint8_t* rows = ws + kWsHead;
-
+  const int nsub = (tb.U + 63) / 64;
   bool staged = false;
   for (int g0 = 0; g0 < B; g0 += WL.group) {
     const int gr = min(WL.group, B - g0);
-    __syncthreads();  // the previous group is done with the row blocks
-    if (tid < gr) {  // chunks of each row of the group, then their prefix sums
-      const RowHeader* h = (const RowHeader*)(rows + (size_t)(g0 + tid) * rbytes);
-      pre_s[tid + 1] = h->valid == kRowValid ? (h->walk_count + 63u) / 64u : 0u;
-    }
-    if (tid == 0) chunk_ctr = 0;
-    __syncthreads();
-    if (tid == 0) {
-      pre_s[0] = 0;
-      for (int r = 1; r <= gr; ++r) pre_s[r] += pre_s[r - 1];
-    }
-    __syncthreads();
-    const uint32_t total = pre_s[gr];
-    if (total == 0) continue;  // uniform
-    if (!staged) {  // grammar tables, once per workgroup
-      const StageRegion rg[7] = {{(const uint8_t*)tb.dfa, lds + WL.dfa, (uint32_t)(tb.S * tb.C * 2)},
-                                 {tb.bclass, bcls, 256u},
-                                 {(const uint8_t*)tb.acc_off, lds + WL.acc_off, (uint32_t)(tb.S + 1) * 4},
-                                 {tb.acc_list, lds + WL.acc_list, (uint32_t)tb.n_acc},
-                                 parse_region(tb, lds, WL.pl, 0),
-                                 parse_region(tb, lds, WL.pl, 1),
-                                 parse_region(tb, lds, WL.pl, 2)};
-      stage_regions<7, 4>(rg, tid, kWalkThreads);
-      for (int i = tid; i < tb.S * MW; i += kWalkThreads) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
-      for (int t = tid; t < 256; t += kWalkThreads) tinfo_s[t] = t < tb.T ? tb.term_info[t] : 0u;
+    const int items = 2 * gr * nsub;  // walk items of the group's rows first, then lexicon items
+    const int mine = items > (int)blockIdx.x ? (items - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x : 0;
+    bool blocks = false;  // the group's row blocks are in LDS
+    for (int k0 = 0; k0 < mine; k0 += kMaxItems) {
+      const int n_it = min(kMaxItems, mine - k0);
+      __syncthreads();  // the previous round is done with umask_s / upre_s
+      for (int t = tid; t < n_it; t += kWalkThreads) {
+        const int j = (int)blockIdx.x + (k0 + t) * (int)gridDim.x;
+        const int lex = j >= gr * nsub ? 1 : 0, jr = j - lex * gr * nsub;
+        const int r = jr / nsub;
+        const uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
+        const uint32_t v = ((const RowHeader*)rw)->valid;
+        umask_s[t] = v == kRowValid ? ((const uint64_t*)(rw + RL.rbits))[(lex ? 0 : nsub) + jr - r * nsub] : 0ull;
+      }
+      if (tid == 0) chunk_ctr = 0;
       __syncthreads();
-      if (tid < 8) {
-        uint32_t iw = 0;
-        for (int j = 0; j < 32; ++j)
-          if (tinfo_s[tid * 32 + j] & 1u) iw |= 1u << j;
-        I_s[tid] = iw;
+      if (tid < 64) {  // prefix counts of set bits over the items (one wave)
+        const int per = (n_it + 63) / 64;
+        uint32_t sum = 0;
+        for (int i = 0; i < per; ++i) {
+          const int t = lane * per + i;
+          if (t < n_it) sum += (uint32_t)__popcll(umask_s[t]);
+        }
+        uint32_t incl = sum;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+          const uint32_t x = __shfl_up(incl, d);
+          if (lane >= d) incl += x;
+        }
+        uint32_t run = incl - sum;
+        for (int i = 0; i < per; ++i) {
+          const int t = lane * per + i;
+          if (t < n_it) {
+            upre_s[t] = run;
+            run += (uint32_t)__popcll(umask_s[t]);
+          }
+        }
+        if (lane == 63) upre_s[n_it] = incl;
       }
-      staged = true;
-    }
-    {
-      // the rows' blocks, two 16-byte chunks per thread in flight at a time
-      const uint32_t n16 = WL.block / 16u, tot16 = (uint32_t)gr * n16;
-      for (uint32_t i = tid; i < tot16; i += 2u * kWalkThreads) {
-        const uint32_t i2 = i + kWalkThreads;
-        const uint32_t r = i / n16, r2 = i2 / n16;
-        const uint4 v = reinterpret_cast<const uint4*>(rows + (size_t)(g0 + r) * rbytes)[i - r * n16];
-        uint4 v2 = make_uint4(0, 0, 0, 0);
-        if (i2 < tot16) v2 = reinterpret_cast<const uint4*>(rows + (size_t)(g0 + r2) * rbytes)[i2 - r2 * n16];
-        reinterpret_cast<uint4*>(rows_s)[i] = v;
-        if (i2 < tot16) reinterpret_cast<uint4*>(rows_s)[i2] = v2;
+      __syncthreads();
+      const int n_und = (int)upre_s[n_it];
+      if (n_und == 0) continue;  // uniform
+      if (!staged) {  // grammar tables, once per workgroup
+        const StageRegion rg[7] = {{(const uint8_t*)tb.dfa, lds + WL.dfa, (uint32_t)(tb.S * tb.C * 2)},
+                                   {tb.bclass, bcls, 256u},
+                                   {(const uint8_t*)tb.acc_off, lds + WL.acc_off, (uint32_t)(tb.S + 1) * 4},
+                                   {tb.acc_list, lds + WL.acc_list, (uint32_t)tb.n_acc},
+                                   parse_region(tb, lds, WL.pl, 0),
+                                   parse_region(tb, lds, WL.pl, 1),
+                                   parse_region(tb, lds, WL.pl, 2)};
+        stage_regions<7, 4>(rg, tid, kWalkThreads);
+        for (int i = tid; i < tb.S * MW; i += kWalkThreads) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
+        for (int t = tid; t < 256; t += kWalkThreads) tinfo_s[t] = t < tb.T ? tb.term_info[t] : 0u;
+        __syncthreads();
+        if (tid < 8) {
+          uint32_t iw = 0;
+          for (int j = 0; j < 32; ++j)
+            if (tinfo_s[tid * 32 + j] & 1u) iw |= 1u << j;
+          I_s[tid] = iw;
+        }
+        staged = true;
       }
-    }
-    __syncthreads();
-    const ParseTabs<true> pt = lds_parse(tb, lds, WL.pl);
-    const DfaView step{(const uint16_t*)(lds + WL.dfa), bcls, tb.C};
-    const WalkShared<MW> sh{&tb, pt, step, tinfo_s, I_s, live_s, acc_off_s, acc_list_s, pool};
-    // this workgroup's chunks are blockIdx.x + k * gridDim.x; its waves take
-    // them in turn from an LDS counter
-    for (;;) {
-      const uint32_t c = blockIdx.x + (uint32_t)wave_grab(&chunk_ctr) * gridDim.x;
-      if (c >= total) break;
-      int r = 0;  // the row holding chunk c: last r with pre_s[r] <= c
-      while (r + 1 < gr && pre_s[r + 1] <= c) ++r;
-      const uint8_t* rowblk = rows_s + (size_t)r * WL.block;
-      const RowHeader& h = *(const RowHeader*)rowblk;
-      uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
-      const uint32_t e = (c - pre_s[r]) * 64u + (uint32_t)lane;
-      if (e < h.walk_count) {
-        const int id = (int)((const uint32_t*)(rw + RL.walkl))[e];
-        if (residue_lane<MW>(sh, h, rowblk, rw, RL, id, lane_area) > 0) {
-          atomicOr(mask + (size_t)(g0 + r) * tb.W + (id >> 5), 1u << (id & 31));
-          ((RowHeader*)rw)->nonempty = 1u;
+      if (!blocks) {  // the rows' blocks, two 16-byte chunks per thread in flight at a time
+        const uint32_t n16 = WL.block / 16u, tot16 = (uint32_t)gr * n16;
+        for (uint32_t i = tid; i < tot16; i += 2u * kWalkThreads) {
+          const uint32_t i2 = i + kWalkThreads;
+          const uint32_t r = i / n16, r2 = i2 / n16;
+          const uint4 v = reinterpret_cast<const uint4*>(rows + (size_t)(g0 + r) * rbytes)[i - r * n16];
+          uint4 v2 = make_uint4(0, 0, 0, 0);
+          if (i2 < tot16) v2 = reinterpret_cast<const uint4*>(rows + (size_t)(g0 + r2) * rbytes)[i2 - r2 * n16];
+          reinterpret_cast<uint4*>(rows_s)[i] = v;
+          if (i2 < tot16) reinterpret_cast<uint4*>(rows_s)[i2] = v2;
+        }
+        blocks = true;
+      }
+      __syncthreads();
+      const ParseTabs<true> pt = lds_parse(tb, lds, WL.pl);
+      const DfaView step{(const uint16_t*)(lds + WL.dfa), bcls, tb.C};
+      const WalkShared<MW> sh{&tb, pt, step, tinfo_s, I_s, live_s, acc_off_s, acc_list_s, pool};
+      for (;;) {
+        const int c = wave_grab(&chunk_ctr);
+        if (c * 64 >= n_und) break;
+        const int pos = c * 64 + lane;
+        if (pos < n_und) {
+          // the item holding position pos: last t with upre_s[t] <= pos
+          int lo = 0, hi = n_it - 1;
+          while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if ((int)upre_s[mid] <= pos) lo = mid;
+            else hi = mid - 1;
+          }
+          const int bit = nth_set_bit(umask_s[lo], pos - (int)upre_s[lo]);
+          const int j = (int)blockIdx.x + (k0 + lo) * (int)gridDim.x;
+          const int lex = j >= gr * nsub ? 1 : 0, jr = j - lex * gr * nsub;
+          const int r = jr / nsub;
+          const uint32_t u = (uint32_t)((jr - r * nsub) * 64 + bit);
+          const uint8_t* rowblk = rows_s + (size_t)r * WL.block;
+          uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
+          const uint4 rk = tb.spell_rec[u];
+          const uint32_t cls = lex ? ((const uint16_t*)(rw + RL.rcls))[u] : 0u;
+          if (residue_token<MW>(sh, *(const RowHeader*)rowblk, rowblk, rw, RL, u, rk, lex != 0, cls, lane_area) > 0) {
+            allow_spelling(tb, mask + (size_t)(g0 + r) * tb.W, u, rk);
+            ((RowHeader*)rw)->nonempty = 1u;
+          }
         }
       }
     }
@@ -2052,7 +2092,7 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
 }
 
 // ---------------------------------------------------------------- finalize
-// One workgroup per row.  Tokens the residue walk handed over (their lane
+// One workgroup per row.  Spellings the residue walk handed over (their lane
 // stack area was too small) are walked again from the row's configuration
 // with a large stack area per thread in the workspace, reading the tables
 // from global memory; then the row status is written.
@@ -2111,8 +2151,7 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
       lex0.w = 0;
       for (int k = 0; k < 8; ++k) lex0.w |= (uint64_t)cfg.rem_head[k] << (8 * k);
       for (uint32_t k = tid; k < count; k += kSlowThreads) {
-        const int id = (int)((const uint32_t*)(rw + RL.slow))[k];
-        const uint32_t su = tb.spell_of_id[id];
+        const uint32_t su = ((const uint32_t*)(rw + RL.slow))[k];
         Lane<MW> ln;
         ln.mode = 0;
         ln.t1 = -1;
@@ -2125,7 +2164,7 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
         const int ok = walk_bytes<false, MW>(rc, ln, cfg.q, lex0, 0u, tb.spell_off[su + 1] - base, byte_at, step,
                                              ov, kSlowLane, 1u);
         if (ok > 0) {
-          atomicOr(mask + (size_t)row * tb.W + (id >> 5), 1u << (id & 31));
+          allow_spelling(tb, mask + (size_t)row * tb.W, su, tb.spell_rec[su]);
           slow_ok = 1;
         } else if (ok < 0) {
           atomicOr(&hdr->wstat, GRID_ROW_OVERFLOW);
@@ -2257,9 +2296,8 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
   if (phases & GRID_PHASE_PROLOGUE) {
     hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool, mask, eos, ws,
                        rb);
-    const uint32_t vgroups = ((uint32_t)tb.max_classes + 3u) / 4u;
-    const uint32_t vy = (vgroups + kBlock - 1) / kBlock;
-    hipLaunchKernelGGL(verdict_kernel<MW>, dim3(B, vy), dim3(kBlock), verdict_lds(tb, MW), s, tb, ws, rb);
+    const uint32_t vy = ((uint32_t)tb.max_classes + kBlock - 1) / kBlock;
+    hipLaunchKernelGGL(verdict_kernel<MW>, dim3(B, vy), dim3(kBlock), verdict_lds(tb).total, s, tb, ws, rb);
   }
   if (phases & GRID_PHASE_WALK) {
     const uint32_t lds = pad16(((uint32_t)tb.max_classes + 15u) / 16u * 4u);
@@ -2269,11 +2307,6 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
     hipLaunchKernelGGL(stream_kernel, dim3((uint32_t)blocks), dim3(kBlock), lds, s, tb, mask, ws, rb, B);
   }
   if ((phases & GRID_PHASE_RESIDUE) && tb.U > 0) {
-    // a few hundred workgroups per row group: idle ones still cost dispatch time
-    const uint32_t lx = (uint32_t)std::max(1, std::min(256, (tb.V * kRowGroup / 8 + kBlock * kLexPer - 1) /
-                                                                 (kBlock * kLexPer)));
-    const uint32_t ly = (uint32_t)((B + kRowGroup - 1) / kRowGroup);
-    hipLaunchKernelGGL(lexicon_kernel<MW>, dim3(lx, ly), dim3(kBlock), lexicon_lds(tb, MW), s, tb, mask, ws, rb, B);
     const ResLds RL = res_lds(tb, MW, B);
     const int resident = residue_grid_size<MW>(RL.total);
     if (resident <= 0) return fail(GRID_E_HIP, "grid_mask: cannot raise the residue walk's LDS limit");
@@ -2294,7 +2327,7 @@ int grid::overlay_capacity() { return kFastLane; }
 
 // head, then B rows
 static size_t row_bytes(const grid_compiled* g) {
-  return row_layout(g->parser.T, g->dfa.S, g->vocab.V, (int)g->classes.max_classes).total;
+  return row_layout(g->parser.T, g->dfa.S, (int)g->vocab.spell_off.size() - 1, (int)g->classes.max_classes).total;
 }
 
 static size_t workspace_size(const grid_compiled* g, int B) { return kWsHead + row_bytes(g) * (size_t)B; }
@@ -2390,7 +2423,7 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
   const int mw = tb.tw;
   const ResLds WL = res_lds(tb, mw, B);
   if (tb.T > 255 || (mw != 2 && mw != 4 && mw != 8) || WL.total + 64 > kWalkLdsMax ||
-      parse_lds(tb, 0).total > 24 * 1024 || verdict_lds(tb, mw) > 64 * 1024)
+      parse_lds(tb, 0).total > 24 * 1024 || verdict_lds(tb).total > 64 * 1024)
     return fail(GRID_E_CAPACITY, "grid_mask: lexer DFA or LR tables too large for the LDS staging");
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace_dev;

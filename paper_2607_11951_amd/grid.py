@@ -132,6 +132,7 @@ class Grid:
                             sp.ctypes.data, len(specials), eos_id)
         h = ctypes.c_void_p()
         _check(lib().grid_compile(ctypes.byref(args), ctypes.byref(h)))
+        self._lib_ref = lib()  # kept so that the handle can be freed during interpreter shutdown
         self.h = h
         self.V = len(vocab)
         self.W = (self.V + 31) // 32
@@ -139,8 +140,9 @@ class Grid:
         self.device = None
 
     def __del__(self):
-        if getattr(self, "h", None):
-            lib().grid_free(self.h)
+        L = getattr(self, "_lib_ref", None)
+        if getattr(self, "h", None) and L is not None:
+            L.grid_free(self.h)
             self.h = None
 
     def info(self):
@@ -156,7 +158,7 @@ class Grid:
         slot = ctypes.c_int32()
         _check(lib().grid_add_lexicon(self.h, ctypes.byref(la), ctypes.byref(slot)))
         if self.device is not None:
-            self._upload(self.device, ["LEX_FLAGS", "LEX_HASH", "LEX_SLOTS", "LEX_PREFIX"])
+            self._upload(self.device, ["LEX_FLAGS", "LEX_HASH", "LEX_SLOTS", "LEX_PREFIX", "LEX_STRIDE", "LEX_TOKEN"])
         return slot.value
 
     def artifact(self, name):
