@@ -165,7 +165,8 @@ enum {
                                that shift (or accept), terminals reduced by the state's
                                main production, that production as lhs | length << 16
                                (0xFFFFFFFF none), extra groups | their offset in
-                               PARSE_REDX << 8, padding */
+                               PARSE_REDX << 8, offset of the state's run in
+                               PARSE_SHIFT, padding */
   GRID_ART_PARSE_REDX,      /* u32 per extra reduce group: production (lhs | length << 16),
                                TW words of terminals */
   GRID_ART_GOTO_HASH,       /* GOTO as an open-addressing table of H = 2^k slots (k >= 6,
@@ -211,6 +212,10 @@ enum {
                                byte; 0 when that lexeme runs to the token's end) */
   GRID_ART_ID_FIRST,        /* u8 [V]: first byte of each token id's spelling (0 for
                                specials and empty tokens) */
+  GRID_ART_PARSE_SHIFT,     /* u16 per shift entry of the ACTION table: per LR state, in
+                               terminal order, the target state of every terminal whose
+                               PARSE_STATE shift bit is set (0 for accept); terminal t's
+                               target is entry (shift bits below t) of the state's run */
   GRID_ART_COUNT
 };
 int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);

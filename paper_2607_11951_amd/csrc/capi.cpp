@@ -192,6 +192,7 @@ extern "C" int grid_artifact(const grid_compiled* g, int32_t which, const void**
     case GRID_ART_ID_FIRST: put(g->vocab.id_first, p, n); break;
     case GRID_ART_PARSE_STATE: put(g->parser.pstate, p, n); break;
     case GRID_ART_PARSE_REDX: put(g->parser.predx, p, n); break;
+    case GRID_ART_PARSE_SHIFT: put(g->parser.pshift, p, n); break;
     case GRID_ART_GOTO_HASH: put(g->parser.goto_hash, p, n); break;
     default: return fail(GRID_E_ARG, "unknown artifact " + std::to_string(which));
   }

@@ -84,6 +84,7 @@ struct Parser {
   int tw = 0;
   std::vector<uint32_t> pstate;
   std::vector<uint32_t> predx;     // extra reduce groups: [production][bits TW]
+  std::vector<uint16_t> pshift;    // shift targets per state, in terminal order (record word 2TW+2)
   // GOTO as an open-addressing hash of H (power of two) u32 pairs: key
   // (state << 16 | nonterminal) + 1 (0 empty), target
   std::vector<uint32_t> goto_hash;

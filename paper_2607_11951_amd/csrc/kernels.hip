@@ -74,6 +74,8 @@ constexpr int kFastLane = 16;        // per-lane stack area in LDS (overlay at t
 constexpr int kRowGroup = 32;        // rows resident in LDS at once (at most)
 constexpr int kWalkWin = 64;         // top stack entries of each row in the walk's LDS
 constexpr int kMaxItems = 1024;      // residue work items a workgroup scans at once
+constexpr int kWalkChunk = 16;       // byte-walk spellings a wave takes at a time
+constexpr int kLexChunk = 32;        // lexicon spellings a wave takes at a time
 constexpr uint32_t kWalkLdsMax = 160 * 1024;
 
 struct Tables {
@@ -106,7 +108,8 @@ struct Tables {
   const uint4* crec;          // class records
   int S, C, T, N, NS, P, U, V, W, n_slots, eos_id;
   int max_classes;            // largest class count of one lexer state
-  int tw, n_pstate, n_predx, n_acc, hbits;
+  const uint16_t* pshift;      // shift targets per LR state
+  int tw, n_pstate, n_predx, n_pshift, n_acc, hbits;
   uint8_t* cache;             // mask cache (null: off)
   uint32_t cache_mask;        // entries - 1
   uint32_t cache_flags;       // GRID_CACHE_*
@@ -173,6 +176,7 @@ struct Post {                 // stack after shifting one allowed terminal
   uint16_t ov[kPostCap];
 };
 static_assert(sizeof(Post) == 32, "post entry is 32 bytes");
+static_assert(kPostCap == 14, "the walk decodes a post entry as two 16-byte halves");
 
 struct RowLayout {
   size_t cls, win, block, post, a2, vcode, vrule, rbits, rcls, slow, slow_ov, total;
@@ -323,12 +327,12 @@ struct ParseTabs {
   mptr<L, const uint32_t> st;    // state records, parse_record_words(MW) words each
   mptr<L, const uint32_t> redx;  // extra reduce groups
   mptr<L, const u32x2> gh;       // GOTO (key, target) slots
-  const uint16_t* action;        // global, dense: shift targets
+  mptr<L, const uint16_t> sl;    // shift targets (runs per state)
   int T, hbits;
 };
 
 struct ParseLds {  // byte offsets of the staged tables
-  uint32_t st, redx, ghash, total;
+  uint32_t st, redx, ghash, sl, total;
 };
 
 __host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base) {
@@ -340,6 +344,8 @@ __host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base) {
   o += pad16((uint32_t)tb.n_predx * 4);
   L.ghash = o;
   o += 8u << tb.hbits;
+  L.sl = o;
+  o += pad16((uint32_t)tb.n_pshift * 2);
   L.total = o - base;
   return L;
 }
@@ -347,17 +353,20 @@ __host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base) {
 __device__ inline StageRegion parse_region(const Tables& tb, uint8_t* lds, const ParseLds& L, int which) {
   if (which == 0) return {(const uint8_t*)tb.pstate, lds + L.st, (uint32_t)tb.n_pstate * 4};
   if (which == 1) return {(const uint8_t*)tb.predx, lds + L.redx, (uint32_t)tb.n_predx * 4};
+  if (which == 3) return {(const uint8_t*)tb.pshift, lds + L.sl, (uint32_t)tb.n_pshift * 2};
   return {(const uint8_t*)tb.ghash, lds + L.ghash, 8u << tb.hbits};
 }
 
 // The LR tables in LDS (the caller stages them, see parse_region).
 __device__ inline ParseTabs<true> lds_parse(const Tables& tb, uint8_t* lds, const ParseLds& L) {
   return {in_mem<true>((const uint32_t*)(lds + L.st)), in_mem<true>((const uint32_t*)(lds + L.redx)),
-          in_mem<true>((const u32x2*)(lds + L.ghash)), tb.action, tb.T, tb.hbits};
+          in_mem<true>((const u32x2*)(lds + L.ghash)), in_mem<true>((const uint16_t*)(lds + L.sl)), tb.T,
+          tb.hbits};
 }
 
 __device__ inline ParseTabs<false> global_parse(const Tables& tb) {
-  return {in_mem<false>(tb.pstate), in_mem<false>(tb.predx), in_mem<false>((const u32x2*)tb.ghash), tb.action,
+  return {in_mem<false>(tb.pstate), in_mem<false>(tb.predx), in_mem<false>((const u32x2*)tb.ghash),
+          in_mem<false>(tb.pshift),
           tb.T, tb.hbits};
 }
 
@@ -433,6 +442,23 @@ __device__ __forceinline__ uint32_t action_of(const ParseTabs<L>& pt, uint32_t s
   return kNoProd;
 }
 
+// Target of the shift of terminal x in state s (x's shift bit is set): entry
+// (shift bits below x) of the state's run of shift targets.
+template <bool L, int MW>
+__device__ __forceinline__ uint16_t shift_target(const ParseTabs<L>& pt, uint32_t s, int x) {
+  constexpr int R = parse_record_words(MW);
+  const mptr<L, const uint32_t> rec = pt.st + (size_t)s * R;
+  const uint32_t w = (uint32_t)x >> 5;
+  uint32_t rank = 0, base = rec[2 * MW + 2];
+#pragma unroll
+  for (int k = 0; k < MW; ++k) {
+    const uint32_t bits = rec[k];
+    if ((uint32_t)k < w) rank += (uint32_t)__popc(bits);
+    if ((uint32_t)k == w) rank += (uint32_t)__popc(bits & ((1u << (x & 31)) - 1u));
+  }
+  return pt.sl[base + rank];
+}
+
 // Virtual stack base[0,k) ++ ov[0,m) ++ tmp[0,t); the state below a pop.
 template <bool L>
 __device__ __forceinline__ uint16_t stack_at_top(const BaseStack<L>& bs, uint32_t k, int m,
@@ -486,7 +512,7 @@ __device__ __forceinline__ int sim1_shift(const ParseTabs<L>& pt, const BaseStac
     if (a == kActShiftP) {
       if (x == pt.T) return 2;
       if (m >= cap) return -1;
-      ov[m++] = (uint16_t)(pt.action[(size_t)s * (pt.T + 1) + x] & 0x3FFF);
+      ov[m++] = shift_target<L, MW>(pt, s, x);
       return 1;
     }
     if (a == kNoProd) return 0;
@@ -820,9 +846,9 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   const grid_config cfg = cfgs[row];
   const ParseLds PL = parse_lds(tb, 0);
   {
-    const StageRegion rg[3] = {parse_region(tb, plds, PL, 0), parse_region(tb, plds, PL, 1),
-                               parse_region(tb, plds, PL, 2)};
-    stage_regions<3, 8>(rg, tid, kBlock);
+    const StageRegion rg[4] = {parse_region(tb, plds, PL, 0), parse_region(tb, plds, PL, 1),
+                               parse_region(tb, plds, PL, 2), parse_region(tb, plds, PL, 3)};
+    stage_regions<4, 8>(rg, tid, kBlock);
   }
   const ParseTabs<true> pt = lds_parse(tb, plds, PL);
 
@@ -1098,6 +1124,7 @@ struct Lane {
   uint32_t k;
   int m;
   uint32_t acur[MW];
+  uint4 ph;  // mode 1: first 16 bytes of the row's stack after shifting t1, loaded early
 };
 
 template <bool L>
@@ -1148,16 +1175,27 @@ __device__ __forceinline__ int emit(const RowCtx<L>& rc, Lane<MW>& ln, mptr<L, u
   if (ln.mode == 0) {
     ln.mode = 1;
     ln.t1 = t;
+    ln.ph = reinterpret_cast<const uint4*>(rc.post)[2 * t];  // needed at the next shift
 #pragma unroll
     for (int w = 0; w < MW; ++w) ln.acur[w] = rc.a2[t * rc.a2_stride + w];
     return 1;
   }
-  if (ln.mode == 1) {
-    const Post& p = rc.post[ln.t1];
-    if (!p.ok || p.k == 0 || p.k > rc.bs.depth || p.m > kPostCap || p.m > cap) return -1;
-    ln.k = p.k;
-    ln.m = p.m;
-    for (int j = 0; j < ln.m; ++j) ov[j] = p.ov[j];
+  if (ln.mode == 1) {  // the stack after t1 (Post: k u16, m u8, ok u8, overlay u16[kPostCap])
+    const uint32_t pk = ln.ph.x & 0xFFFFu, pm = (ln.ph.x >> 16) & 0xFFu, pok = ln.ph.x >> 24;
+    if (!pok || pk == 0 || pk > rc.bs.depth || pm > (uint32_t)kPostCap || (int)pm > cap) return -1;
+    ln.k = pk;
+    ln.m = (int)pm;
+    const uint32_t lo[3] = {ln.ph.y, ln.ph.z, ln.ph.w};
+#pragma unroll
+    for (int j = 0; j < 6; ++j)
+      if (j < ln.m) ov[j] = (uint16_t)(lo[j >> 1] >> (16 * (j & 1)));
+    if (ln.m > 6) {
+      const uint4 h2 = reinterpret_cast<const uint4*>(rc.post)[2 * ln.t1 + 1];
+      const uint32_t hi[4] = {h2.x, h2.y, h2.z, h2.w};
+#pragma unroll
+      for (int j = 6; j < 14; ++j)
+        if (j < ln.m) ov[j] = (uint16_t)(hi[(j - 6) >> 1] >> (16 * (j & 1)));
+    }
     ln.mode = 2;
   }
   const int r = sim1_shift<L, MW>(rc.pt, rc.bs, ln.k, ln.m, ov, cap, t);
@@ -1793,6 +1831,7 @@ __device__ __forceinline__ int residue_lane(const WalkShared<MW>& sh, const RowH
     dead = dead || q1 == kDead;
     ln.mode = h.wkind == 2 ? 1 : 0;
     ln.t1 = h.wkind == 2 ? h.winner : -1;
+    if (ln.mode == 1) ln.ph = reinterpret_cast<const uint4*>(rc.post)[2 * ln.t1];
     ct = h.wkind == 2 ? clsW : clsA;
     lx.len = 1;
     lx.w = b0;
@@ -1950,9 +1989,10 @@ __device__ inline int nth_set_bit(uint64_t m, int rank) {
 // fits, a work item is one row against 64 consecutive spellings (one word of
 // one of the row's residue bitmaps, byte-walk items first since they take
 // longest); workgroup b takes items b, b + gridDim.x, ...
-// and reads their words, then the set bits are packed 64 to a wave in
-// spelling order -- lexicographic neighbours walk alike, so a wave's lanes
-// diverge little.  The grammar tables and the group's row blocks (header,
+// and reads their words, then the set bits are packed into waves in
+// spelling order, kWalkChunk byte-walk or kLexChunk lexicon spellings to a
+// wave -- lexicographic neighbours walk alike, and a wave's time is the sum
+// over its emission rounds of its slowest lane, so fewer lanes diverge less.  The grammar tables and the group's row blocks (header,
 // trailing-flag tables, stack window) are staged in LDS only when the
 // workgroup has residue spellings.  Each lane judges one spelling and sets
 // the mask bits of its ids.
@@ -2024,14 +2064,15 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
       const int n_und = (int)upre_s[n_it];
       if (n_und == 0) continue;  // uniform
       if (!staged) {  // grammar tables, once per workgroup
-        const StageRegion rg[7] = {{(const uint8_t*)tb.dfa, lds + WL.dfa, (uint32_t)(tb.S * tb.C * 2)},
+        const StageRegion rg[8] = {{(const uint8_t*)tb.dfa, lds + WL.dfa, (uint32_t)(tb.S * tb.C * 2)},
                                    {tb.bclass, bcls, 256u},
                                    {(const uint8_t*)tb.acc_off, lds + WL.acc_off, (uint32_t)(tb.S + 1) * 4},
                                    {tb.acc_list, lds + WL.acc_list, (uint32_t)tb.n_acc},
                                    parse_region(tb, lds, WL.pl, 0),
                                    parse_region(tb, lds, WL.pl, 1),
-                                   parse_region(tb, lds, WL.pl, 2)};
-        stage_regions<7, 4>(rg, tid, kWalkThreads);
+                                   parse_region(tb, lds, WL.pl, 2),
+                                   parse_region(tb, lds, WL.pl, 3)};
+        stage_regions<8, 4>(rg, tid, kWalkThreads);
         for (int i = tid; i < tb.S * MW; i += kWalkThreads) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
         for (int t = tid; t < 256; t += kWalkThreads) tinfo_s[t] = t < tb.T ? tb.term_info[t] : 0u;
         __syncthreads();
@@ -2060,11 +2101,25 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
       const ParseTabs<true> pt = lds_parse(tb, lds, WL.pl);
       const DfaView step{(const uint16_t*)(lds + WL.dfa), bcls, tb.C};
       const WalkShared<MW> sh{&tb, pt, step, tinfo_s, I_s, live_s, acc_off_s, acc_list_s, pool};
+      // positions [0, n_wpos) belong to byte-walk items (they come first), the
+      // rest to lexicon items; a wave takes kWalkChunk walk positions or
+      // kLexChunk lexicon positions at a time (fewer lanes, less divergence)
+      const int t_lex0 = min(max((gr * nsub - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x - k0, 0), n_it);
+      const int n_wpos = (int)upre_s[t_lex0];
+      const int nwc = (n_wpos + kWalkChunk - 1) / kWalkChunk;
       for (;;) {
         const int c = wave_grab(&chunk_ctr);
-        if (c * 64 >= n_und) break;
-        const int pos = c * 64 + lane;
-        if (pos < n_und) {
+        int pos;
+        bool in;
+        if (c < nwc) {
+          pos = c * kWalkChunk + lane;
+          in = lane < kWalkChunk && pos < n_wpos;
+        } else {
+          if (n_wpos + (c - nwc) * kLexChunk >= n_und) break;
+          pos = n_wpos + (c - nwc) * kLexChunk + lane;
+          in = lane < kLexChunk && pos < n_und;
+        }
+        if (in) {
           // the item holding position pos: last t with upre_s[t] <= pos
           int lo = 0, hi = n_it - 1;
           while (lo < hi) {
@@ -2358,7 +2413,7 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
                                GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH,   GRID_ART_LEX_PREFIX,
                                GRID_ART_SPELL_OF_ID, GRID_ART_CLASS_MAP, GRID_ART_CLASS_OFF,
                                GRID_ART_CLASS_REC,   GRID_ART_LEX_STRIDE,  GRID_ART_LEX_TOKEN,
-                               GRID_ART_ID_FIRST};
+                               GRID_ART_ID_FIRST,    GRID_ART_PARSE_SHIFT};
   for (int w : needed)
     if (!bound(g, w)) return fail(GRID_E_UNBOUND, "grid_mask: artifact " + std::to_string(w) + " is not bound");
   Tables tb;
@@ -2371,6 +2426,7 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
   tb.term_info = (const uint32_t*)g->dev[GRID_ART_TERM_INFO];
   tb.pstate = (const uint32_t*)g->dev[GRID_ART_PARSE_STATE];
   tb.predx = (const uint32_t*)g->dev[GRID_ART_PARSE_REDX];
+  tb.pshift = (const uint16_t*)g->dev[GRID_ART_PARSE_SHIFT];
   tb.ghash = (const uint2*)g->dev[GRID_ART_GOTO_HASH];
   tb.spell_off = (const uint32_t*)g->dev[GRID_ART_SPELL_OFF];
   tb.spell_bytes = (const uint8_t*)g->dev[GRID_ART_SPELL_BYTES];
@@ -2404,6 +2460,7 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
   tb.tw = g->parser.tw;
   tb.n_pstate = (int)g->parser.pstate.size();
   tb.n_predx = (int)g->parser.predx.size();
+  tb.n_pshift = (int)g->parser.pshift.size();
   tb.n_acc = (int)g->dfa.accept_list.size();
   tb.hbits = g->parser.goto_hbits;
   tb.cache = nullptr;

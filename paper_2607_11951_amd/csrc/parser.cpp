@@ -322,7 +322,9 @@ Parser build_parser(const GrammarText& g, const std::vector<std::string>& drop) 
 // lhs | length << 16, so a reduce needs no further lookup; GOTO as an
 // open-addressing hash of (key, target) pairs.  Terminal sets take TW words,
 // TW a power of two (at least 2), and a state record is padded to a multiple of 16 bytes
-// so the kernels read it with 16-byte loads.
+// so the kernels read it with 16-byte loads.  The first padding word locates the
+// state's shift targets: one u16 per set shift bit, in terminal order, so the target
+// of terminal t is entry (number of shift bits below t) of the state's run.
 void compact_tables(Parser& P) {
   const int T1 = P.T + 1;
   int TW = 2;
@@ -332,6 +334,7 @@ void compact_tables(Parser& P) {
   const int stride = parse_record_words(TW);
   P.pstate.assign((size_t)P.n_states * stride, 0);
   P.predx.clear();
+  P.pshift.clear();
   auto packed = [&](int p) { return P.prod[p]; };  // lhs | length << 16
   std::vector<std::pair<uint32_t, uint16_t>> gotos;
   for (int s = 0; s < P.n_states; ++s) {
@@ -371,6 +374,12 @@ void compact_tables(Parser& P) {
     if (n_extra > 255) throw Error(GRID_E_CAPACITY, "more than 255 reduce productions in one state");
     rec[2 * TW] = main_prod < 0 ? 0xFFFFFFFFu : packed(main_prod);
     rec[2 * TW + 1] = n_extra | (uint32_t)off << 8;
+    rec[2 * TW + 2] = (uint32_t)P.pshift.size();
+    for (int t = 0; t < T1; ++t) {
+      const uint16_t a = P.act(s, t);
+      if ((a & 0xC000) == kActShift) P.pshift.push_back((uint16_t)(a & 0x3FFF));
+      else if ((a & 0xC000) == kActAccept) P.pshift.push_back(0);
+    }
     for (int a = 0; a < P.N; ++a) {
       const uint16_t g = P.gto(s, a);
       if (g != kNoGoto) gotos.push_back({goto_key(s, a), g});

@@ -422,6 +422,7 @@ def test_compact_parse_tables_match_dense(G, name, drop):
     st = np.frombuffer(g.artifact("PARSE_STATE"), np.uint32)
     redx = np.frombuffer(g.artifact("PARSE_REDX"), np.uint32)
     gh = np.frombuffer(g.artifact("GOTO_HASH"), np.uint32).reshape(-1, 2)
+    sl = np.frombuffer(g.artifact("PARSE_SHIFT"), np.uint16)
     tw = 2
     while 32 * tw < T + 1:
         tw *= 2
@@ -447,6 +448,11 @@ def test_compact_parse_tables_match_dense(G, name, drop):
                 assert got is None, (s, t)
             elif a & 0xC000 in (0x4000, 0xC000):
                 assert got == "shift", (s, t)
+                # shift target: entry (shift bits below t) of the state's run
+                rank = sum(bin(int(rec[s, k])).count("1") for k in range(w))
+                rank += bin(int(rec[s, w]) & (bit - 1)).count("1")
+                target = int(sl[int(rec[s, 2 * tw + 2]) + rank])
+                assert target == (a & 0x3FFF if a & 0xC000 == 0x4000 else 0), (s, t)
             else:
                 assert got == int(prod[a & 0x3FFF]), (s, t)
     H = len(gh)
