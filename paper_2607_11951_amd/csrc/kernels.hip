@@ -76,6 +76,9 @@ constexpr int kWalkWin = 64;         // top stack entries of each row in the wal
 constexpr int kMaxItems = 1024;      // residue work items a workgroup scans at once
 constexpr int kWalkChunk = 16;       // byte-walk spellings a wave takes at a time
 constexpr int kLexChunk = 32;        // lexicon spellings a wave takes at a time
+constexpr int kLaneSlots = 32;       // lanes of a wave with a stack area in the residue LDS
+static_assert(kWalkChunk <= kLaneSlots && kLexChunk <= kLaneSlots, "chunks fit the lane stack areas");
+static_assert((kLaneSlots & (kLaneSlots - 1)) == 0, "kLaneSlots is a power of two");
 constexpr uint32_t kWalkLdsMax = 160 * 1024;
 
 struct Tables {
@@ -109,6 +112,7 @@ struct Tables {
   int S, C, T, N, NS, P, U, V, W, n_slots, eos_id;
   int max_classes;            // largest class count of one lexer state
   const uint16_t* pshift;      // shift targets per LR state
+  const uint16_t* go;          // dense GOTO [states][N], kNoGoto none
   int tw, n_pstate, n_predx, n_pshift, n_acc, hbits;
   uint8_t* cache;             // mask cache (null: off)
   uint32_t cache_mask;        // entries - 1
@@ -328,22 +332,27 @@ struct ParseTabs {
   mptr<L, const uint32_t> redx;  // extra reduce groups
   mptr<L, const u32x2> gh;       // GOTO (key, target) slots
   mptr<L, const uint16_t> sl;    // shift targets (runs per state)
-  int T, hbits;
+  mptr<L, const uint16_t> gd;    // dense GOTO [states][N] when dense, else unused
+  int T, hbits, N, dense;
 };
 
 struct ParseLds {  // byte offsets of the staged tables
-  uint32_t st, redx, ghash, sl, total;
+  uint32_t st, redx, ghash, sl, gdense, total;
+  int dense;  // GOTO as the dense table (else as the hash)
 };
 
-__host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base) {
+__host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base, bool dense = false) {
   ParseLds L;
   uint32_t o = base;
+  L.dense = dense ? 1 : 0;
   L.st = o;
   o += pad16((uint32_t)tb.n_pstate * 4);
   L.redx = o;
   o += pad16((uint32_t)tb.n_predx * 4);
   L.ghash = o;
-  o += 8u << tb.hbits;
+  if (!dense) o += 8u << tb.hbits;
+  L.gdense = o;
+  if (dense) o += pad16((uint32_t)(tb.NS * tb.N * 2));
   L.sl = o;
   o += pad16((uint32_t)tb.n_pshift * 2);
   L.total = o - base;
@@ -354,20 +363,20 @@ __device__ inline StageRegion parse_region(const Tables& tb, uint8_t* lds, const
   if (which == 0) return {(const uint8_t*)tb.pstate, lds + L.st, (uint32_t)tb.n_pstate * 4};
   if (which == 1) return {(const uint8_t*)tb.predx, lds + L.redx, (uint32_t)tb.n_predx * 4};
   if (which == 3) return {(const uint8_t*)tb.pshift, lds + L.sl, (uint32_t)tb.n_pshift * 2};
+  if (L.dense) return {(const uint8_t*)tb.go, lds + L.gdense, (uint32_t)(tb.NS * tb.N * 2)};
   return {(const uint8_t*)tb.ghash, lds + L.ghash, 8u << tb.hbits};
 }
 
 // The LR tables in LDS (the caller stages them, see parse_region).
 __device__ inline ParseTabs<true> lds_parse(const Tables& tb, uint8_t* lds, const ParseLds& L) {
   return {in_mem<true>((const uint32_t*)(lds + L.st)), in_mem<true>((const uint32_t*)(lds + L.redx)),
-          in_mem<true>((const u32x2*)(lds + L.ghash)), in_mem<true>((const uint16_t*)(lds + L.sl)), tb.T,
-          tb.hbits};
+          in_mem<true>((const u32x2*)(lds + L.ghash)), in_mem<true>((const uint16_t*)(lds + L.sl)),
+          in_mem<true>((const uint16_t*)(lds + L.gdense)), tb.T, tb.hbits, tb.N, L.dense};
 }
 
 __device__ inline ParseTabs<false> global_parse(const Tables& tb) {
   return {in_mem<false>(tb.pstate), in_mem<false>(tb.predx), in_mem<false>((const u32x2*)tb.ghash),
-          in_mem<false>(tb.pshift),
-          tb.T, tb.hbits};
+          in_mem<false>(tb.pshift), in_mem<false>(tb.go), tb.T, tb.hbits, tb.N, 1};
 }
 
 template <bool L>
@@ -379,16 +388,18 @@ struct BaseStack {  // the shared read-only stack of one row
 };
 
 template <bool L>
-__device__ inline uint16_t goto_of(const ParseTabs<L>& pt, uint32_t s, uint32_t a) {
+__device__ __forceinline__ uint16_t goto_of(const ParseTabs<L>& pt, uint32_t s, uint32_t a) {
+  if (pt.dense) return pt.gd[s * (uint32_t)pt.N + a];
   const uint32_t key = goto_key(s, a);
   const uint32_t mask = (1u << pt.hbits) - 1u;
   uint32_t h = goto_slot(key, pt.hbits);
-  for (uint32_t i = 0; i <= mask; ++i, h = (h + 1) & mask) {
-    const u32x2 e = pt.gh[h];
-    if (e.x == key) return (uint16_t)e.y;
-    if (e.x == 0) break;
+  u32x2 e = pt.gh[h];
+  // linear probing; the load factor (at most 2/3) keeps an empty slot
+  for (uint32_t i = 0; e.x != key && e.x != 0u && i < mask; ++i) {
+    h = (h + 1) & mask;
+    e = pt.gh[h];
   }
-  return kNoGoto;
+  return e.x == key ? (uint16_t)e.y : kNoGoto;
 }
 
 // One state record: shift bits, main-reduce bits, main production (lhs |
@@ -423,23 +434,32 @@ __device__ __forceinline__ PRec<MW> rec_of(const ParseTabs<L>& pt, uint32_t s) {
   return r;
 }
 
-// Action of terminal x in state s: kActShiftP (shift, or accept for the
-// end-of-input column), kNoProd (error), else the production to reduce.
+// Action of the terminal with set word w and bit `bit` in state s:
+// kActShiftP (shift, or accept for the end-of-input column), kNoProd
+// (error), else the production to reduce.
 constexpr uint32_t kActShiftP = 0xFFFFFFFEu;
+constexpr uint32_t kNoState = 0xFFFFFFFFu;
 template <bool L, int MW>
-__device__ __forceinline__ uint32_t action_of(const ParseTabs<L>& pt, uint32_t s, int x) {
+__device__ __forceinline__ uint32_t action_of(const ParseTabs<L>& pt, uint32_t s, uint32_t w, uint32_t bit) {
   constexpr int R = parse_record_words(MW);
   const mptr<L, const uint32_t> rec = pt.st + (size_t)s * R;
-  const uint32_t w = (uint32_t)x >> 5, bit = 1u << (x & 31);
-  const uint32_t sh = rec[w], rd = rec[MW + w];
+  const uint32_t sh = rec[w], rd = rec[MW + w];  // both loads issued together
   const u32x2 me = *(mptr<L, const u32x2>)(rec + 2 * MW);
-  if (sh & bit) return kActShiftP;
-  if (rd & bit) return me.x;
-  const uint32_t nx = me.y & 0xFFu;
+  const uint32_t hit = (sh | rd) & bit;
+  uint32_t a = (sh & bit) ? kActShiftP : (hit ? me.x : kNoProd);
+  const uint32_t nx = hit ? 0u : (me.y & 0xFFu);
   mptr<L, const uint32_t> g = pt.redx + (me.y >> 8);
-  for (uint32_t e = 0; e < nx; ++e, g += MW + 1)
-    if (g[1 + w] & bit) return g[0];
-  return kNoProd;
+  for (uint32_t e = 0; e < nx; ++e, g += MW + 1)  // the state's other reduce groups
+    if (g[1 + w] & bit) {
+      a = g[0];
+      break;
+    }
+  return a;
+}
+
+template <bool L, int MW>
+__device__ __forceinline__ uint32_t action_of(const ParseTabs<L>& pt, uint32_t s, int x) {
+  return action_of<L, MW>(pt, s, (uint32_t)x >> 5, 1u << (x & 31));
 }
 
 // Target of the shift of terminal x in state s (x's shift bit is set): entry
@@ -459,14 +479,46 @@ __device__ __forceinline__ uint16_t shift_target(const ParseTabs<L>& pt, uint32_
   return pt.sl[base + rank];
 }
 
-// Virtual stack base[0,k) ++ ov[0,m) ++ tmp[0,t); the state below a pop.
+// Virtual stack base[0,k) ++ ov[0,m) ++ tmp[0,t) (k >= 1): its top state.
+// In LDS the three places are one address space, so the address is selected
+// and read once; a base entry below the LDS window is read from the pool.
 template <bool L>
 __device__ __forceinline__ uint16_t stack_at_top(const BaseStack<L>& bs, uint32_t k, int m,
                                                  mptr<L, const uint16_t> ov, int t,
                                                  mptr<L, const uint16_t> tmp) {
-  if (t > 0) return tmp[t - 1];
-  if (m > 0) return ov[m - 1];
-  return bs.at(k - 1);
+  if constexpr (L) {
+    if (t == 0 && m == 0 && k - 1u < bs.lo) return bs.pool[k - 1u];
+    const mptr<L, const uint16_t> p = t > 0 ? tmp + (t - 1) : (m > 0 ? ov + (m - 1) : bs.win + (k - 1u - bs.lo));
+    return *p;
+  } else {
+    if (t > 0) return tmp[t - 1];
+    if (m > 0) return ov[m - 1];
+    return bs.at(k - 1u);
+  }
+}
+
+// Pops len entries from base[0,k) ++ ov[0,m) ++ tmp[0,t) (tmp first); false
+// if that would empty the stack.
+__device__ __forceinline__ bool pop_len(uint32_t len, uint32_t& k, int& m, int& t) {
+  const uint32_t dt = min((uint32_t)t, len);
+  const uint32_t dm = min((uint32_t)m, len - dt);
+  const uint32_t dk = len - dt - dm;
+  if (dk >= k) return false;
+  t -= (int)dt;
+  m -= (int)dm;
+  k -= dk;
+  return true;
+}
+
+// A chain step needs the state under the popped entries.  With one entry
+// popped it is the state that was under the top (`below`, when known); with
+// none, the top itself; else it is read.
+template <bool L>
+__device__ __forceinline__ uint32_t goto_source(const BaseStack<L>& bs, uint32_t len, uint32_t s, uint32_t below,
+                                                uint32_t k, int m, mptr<L, const uint16_t> ov, int t,
+                                                mptr<L, const uint16_t> tmp) {
+  const uint32_t sb = len == 0 ? s : below;
+  return (len > 1 || sb == kNoState) ? (uint32_t)stack_at_top<L>(bs, k, m, ov, t, tmp) : sb;
 }
 
 // Reduce chain of terminal x, not changing the stack (pushes go to tmp).  1
@@ -474,31 +526,32 @@ __device__ __forceinline__ uint16_t stack_at_top(const BaseStack<L>& bs, uint32_
 template <bool L, int MW>
 __device__ __forceinline__ int sim1_test(const ParseTabs<L>& pt, const BaseStack<L>& bs, uint32_t k, int m,
                                          mptr<L, const uint16_t> ov, mptr<L, uint16_t> tmp, int tmpcap, int x) {
+  const uint32_t w = (uint32_t)x >> 5, bit = 1u << (x & 31);
   int t = 0;
-  uint32_t s = stack_at_top<L>(bs, k, m, ov, 0, tmp);
+  uint32_t s = stack_at_top<L>(bs, k, m, ov, 0, tmp), below = kNoState;
+  int res = -1;  // guard exhausted or capacity
   for (int guard = 0; guard < kGuard; ++guard) {
-    const uint32_t a = action_of<L, MW>(pt, s, x);
-    if (a == kActShiftP) return x == pt.T ? 2 : 1;
-    if (a == kNoProd) return 0;
-    uint32_t len = a >> 16;
-    if (len > 0) {
-      uint32_t d = min((uint32_t)t, len);
-      t -= (int)d;
-      len -= d;
-      d = min((uint32_t)m, len);
-      m -= (int)d;
-      len -= d;
-      if (len >= k) return 0;
-      k -= len;
-      s = stack_at_top<L>(bs, k, m, ov, t, tmp);
+    const uint32_t a = action_of<L, MW>(pt, s, w, bit);
+    if (a >= kActShiftP) {
+      res = a == kActShiftP ? (x == pt.T ? 2 : 1) : 0;
+      break;
     }
-    const uint16_t g = goto_of<L>(pt, s, a & 0xFFFFu);
-    if (g == kNoGoto) return 0;
-    if (t >= tmpcap) return -1;
+    const uint32_t len = a >> 16;
+    if (!pop_len(len, k, m, t)) {
+      res = 0;
+      break;
+    }
+    const uint32_t sb = goto_source<L>(bs, len, s, below, k, m, ov, t, tmp);
+    const uint16_t g = goto_of<L>(pt, sb, a & 0xFFFFu);
+    if (g == kNoGoto || t >= tmpcap) {
+      res = g == kNoGoto ? 0 : -1;
+      break;
+    }
     tmp[t++] = g;
+    below = sb;
     s = g;
   }
-  return -1;
+  return res;
 }
 
 // Reduce chain of terminal x applied to (k, m, ov), then its shift.  1 shifted,
@@ -506,32 +559,36 @@ __device__ __forceinline__ int sim1_test(const ParseTabs<L>& pt, const BaseStack
 template <bool L, int MW>
 __device__ __forceinline__ int sim1_shift(const ParseTabs<L>& pt, const BaseStack<L>& bs, uint32_t& k, int& m,
                                           mptr<L, uint16_t> ov, int cap, int x) {
-  uint32_t s = stack_at_top<L>(bs, k, m, ov, 0, ov);
+  const uint32_t w = (uint32_t)x >> 5, bit = 1u << (x & 31);
+  int t = 0;
+  uint32_t s = stack_at_top<L>(bs, k, m, ov, 0, ov), below = kNoState;
+  int res = -1;  // guard exhausted or capacity
   for (int guard = 0; guard < kGuard; ++guard) {
-    const uint32_t a = action_of<L, MW>(pt, s, x);
-    if (a == kActShiftP) {
-      if (x == pt.T) return 2;
-      if (m >= cap) return -1;
-      ov[m++] = shift_target<L, MW>(pt, s, x);
-      return 1;
+    const uint32_t a = action_of<L, MW>(pt, s, w, bit);
+    if (a >= kActShiftP) {
+      res = a == kActShiftP ? 1 : 0;
+      break;
     }
-    if (a == kNoProd) return 0;
-    uint32_t len = a >> 16;
-    if (len > 0) {
-      const uint32_t d = min((uint32_t)m, len);
-      m -= (int)d;
-      len -= d;
-      if (len >= k) return 0;
-      k -= len;
-      s = stack_at_top<L>(bs, k, m, ov, 0, ov);
+    const uint32_t len = a >> 16;
+    if (!pop_len(len, k, m, t)) {
+      res = 0;
+      break;
     }
-    const uint16_t g = goto_of<L>(pt, s, a & 0xFFFFu);
-    if (g == kNoGoto) return 0;
-    if (m >= cap) return -1;
+    const uint32_t sb = goto_source<L>(bs, len, s, below, k, m, ov, 0, ov);
+    const uint16_t g = goto_of<L>(pt, sb, a & 0xFFFFu);
+    if (g == kNoGoto || m >= cap) {
+      res = g == kNoGoto ? 0 : -1;
+      break;
+    }
     ov[m++] = g;
+    below = sb;
     s = g;
   }
-  return -1;
+  if (res != 1) return res;
+  if (x == pt.T) return 2;
+  if (m >= cap) return -1;
+  ov[m++] = shift_target<L, MW>(pt, s, x);
+  return 1;
 }
 
 // Set simulation: acc |= the terminals of X that can be shifted next from
@@ -560,7 +617,7 @@ __device__ __forceinline__ int sim_set(const ParseTabs<L>& pt, const BaseStack<L
       cur[w] = todo[w];
       todo[w] = 0;
     }
-    uint32_t k = k0, s = s0;
+    uint32_t k = k0, s = s0, below = kNoState;
     int m = m0, t = 0;
     for (int guard = 0; guard < kGuard; ++guard) {
       const PRec<MW> r = rec_of<L, MW>(pt, s);
@@ -574,7 +631,7 @@ __device__ __forceinline__ int sim_set(const ParseTabs<L>& pt, const BaseStack<L
       uint32_t chosen = live ? r.main : kNoProd;
       const uint32_t nx = r.extra & 0xFFu;
       mptr<L, const uint32_t> g = pt.redx + (r.extra >> 8);
-      for (uint32_t e = 0; e < nx; ++e, g += MW + 1) {
+      for (uint32_t e = 0; e < nx; ++e, g += MW + 1) {  // the state's other reduce groups
         uint32_t gl = 0, part[MW];
 #pragma unroll
         for (int w = 0; w < MW; ++w) {
@@ -594,22 +651,14 @@ __device__ __forceinline__ int sim_set(const ParseTabs<L>& pt, const BaseStack<L
       if (chosen == kNoProd) break;
 #pragma unroll
       for (int w = 0; w < MW; ++w) cur[w] = nxt[w];
-      uint32_t len = chosen >> 16;
-      if (len > 0) {
-        uint32_t d = min((uint32_t)t, len);
-        t -= (int)d;
-        len -= d;
-        d = min((uint32_t)m, len);
-        m -= (int)d;
-        len -= d;
-        if (len >= k) break;
-        k -= len;
-        s = stack_at_top<L>(bs, k, m, ov, t, tmp);
-      }
-      const uint16_t gs = goto_of<L>(pt, s, chosen & 0xFFFFu);
+      const uint32_t len = chosen >> 16;
+      if (!pop_len(len, k, m, t)) break;
+      const uint32_t sb = goto_source<L>(bs, len, s, below, k, m, ov, t, tmp);
+      const uint16_t gs = goto_of<L>(pt, sb, chosen & 0xFFFFu);
       if (gs == kNoGoto) break;
       if (t >= tmpcap) return -1;
       tmp[t++] = gs;
+      below = sb;
       s = gs;
     }
   }
@@ -818,11 +867,12 @@ __device__ inline int winner_of(const TermView& tv, const uint32_t* acc_off, con
 }
 
 // ---------------------------------------------------------------- prologue
-// One workgroup per row, three parallel phases: every terminal's reduce chain
-// and shift from sigma (thread t; A(sigma) is the set that shifted), then the
-// pending lexeme's winner and, for every allowed terminal, the allowed set of
-// the stack after its shift; then the first-byte table (thread b) while one
-// thread runs the end-of-sequence gate.
+// One workgroup per row.  Phase 1: every terminal's reduce chain and shift
+// from sigma (A(sigma) is the set that shifted) and, for an allowed terminal,
+// the allowed set of the stack after its shift, with the end-of-sequence gate
+// run speculatively after every candidate winner's shift and from sigma; then
+// the pending lexeme's winner; then the trailing-flag tables, the lexicon
+// continuation bits of the pending lexeme and the row header.
 template <int MW>
 __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_config* __restrict__ cfgs,
                                                           const uint16_t* __restrict__ pool,
@@ -834,9 +884,9 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   const int tid = threadIdx.x;
   __shared__ uint16_t win[kStackWin];
   __shared__ uint32_t A[8], I[8], R[8], Aw[8];
-  __shared__ Post posts[256];
   __shared__ uint16_t scratch[kBlock][kPostCap + kTmpCap];
-  __shared__ int bad, overflow, winner, eos_ok, cache_hit;
+  __shared__ int bad, overflow, winner, eos_ok, eos_sigma, cache_hit;
+  __shared__ uint8_t eos_after[256];  // end-of-sequence test after shifting each candidate winner
   __shared__ unsigned long long hacc[2];
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
@@ -863,6 +913,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     overflow = 0;
     winner = -1;
     eos_ok = 0;
+    eos_sigma = 0;
     cache_hit = -1;
     hacc[0] = 0;
     hacc[1] = 0;
@@ -994,27 +1045,58 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   const TermView tv{tb.term_info, I, R, tb.live, 8};
   __syncthreads();
 
-  // phase 1: terminal tid's reduce chain and shift from sigma
-  if (tid < tb.T) {
-    const int t = tid;
+  // phase 1, with no barrier inside: terminal t's reduce chain and shift from
+  // sigma (A(sigma) is the set that shifted), then the allowed set of the
+  // stack after the shift; with T < kBlock / 2 two threads take each terminal,
+  // both shift it and each simulates half of the terminal words.  Every
+  // candidate winner of the pending lexeme also runs the end-of-sequence test
+  // after its shift, and a spare thread the test from sigma itself, so the
+  // gate is ready once the winner is known.
+  const bool two = tb.T < kBlock / 2;
+  const int t = two ? (tid & (kBlock / 2 - 1)) : tid;
+  const int half = two ? (tid / (kBlock / 2)) : -1;  // -1: all words
+  const bool rem_empty = (cfg.flags & 1u) != 0;
+  uint32_t acc[MW];
+#pragma unroll
+  for (int k = 0; k < MW; ++k) acc[k] = 0;
+  bool shifted = false;
+  if (t < tb.T) {
     uint32_t k = depth;
     int m = 0;
     const int r = sim1_shift<true, MW>(pt, bs, k, m, my, kPostCap, t);
-    if (r < 0 || (r == 1 && k > 0xFFFF)) overflow = 1;
-    if (r == 1) {
-      atomicOr(&A[t >> 5], 1u << (t & 31));
-      Post p;
-      p.k = (uint16_t)k;
-      p.m = (uint8_t)m;
-      p.ok = 1;
-      for (int j = 0; j < kPostCap; ++j) p.ov[j] = j < m ? (uint16_t)my[j] : (uint16_t)0;
-      posts[t] = p;
-      post[t] = p;
+    if (half <= 0) {
+      if (r < 0 || (r == 1 && k > 0xFFFF)) overflow = 1;
+      if (r == 1) {
+        atomicOr(&A[t >> 5], 1u << (t & 31));
+        Post p;
+        p.k = (uint16_t)k;
+        p.m = (uint8_t)m;
+        p.ok = 1;
+        for (int j = 0; j < kPostCap; ++j) p.ov[j] = j < m ? (uint16_t)my[j] : (uint16_t)0;
+        post[t] = p;
+      }
     }
+    if (r == 1) {
+      shifted = true;
+      uint32_t X[MW];
+#pragma unroll
+      for (int w = 0; w < MW; ++w) X[w] = (half < 0 || w / (MW / 2) == half) ? all_word(tb.T, w) : 0u;
+      if (sim_set<true, MW>(pt, bs, k, m, my, my + m, kPostCap + kTmpCap - m, X, acc) < 0) overflow = 1;
+#pragma unroll
+      for (int w = 0; w < MW; ++w)
+        if (half < 0 || w / (MW / 2) == half) a2[t * 8 + w] = acc[w];
+      if (half <= 0 && !rem_empty) {  // a candidate winner: the gate after its shift
+        bool cand = false;
+        for (uint32_t j = tb.acc_off[cfg.q]; j < tb.acc_off[cfg.q + 1]; ++j) cand = cand || tb.acc_list[j] == t;
+        if (cand) eos_after[t] = sim1_test<true, MW>(pt, bs, k, m, my, my + m, kPostCap + kTmpCap - m, tb.T) == 2;
+      }
+    }
+  } else if (tid == kBlock - 1) {  // the gate from sigma (empty remainder, or an ignored winner)
+    eos_sigma = sim1_test<true, MW>(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, tb.T) == 2;
   }
   __syncthreads();
   // the pending lexeme's winner if a byte ends it
-  if (tid == 0 && !(cfg.flags & 1u)) {
+  if (tid == 0 && !rem_empty) {
     uint32_t a0[MW];
 #pragma unroll
     for (int w = 0; w < MW; ++w) a0[w] = A[w];
@@ -1022,34 +1104,14 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
                            [&]() { return lex_flags_of(tb, sl, cfg.lexnode); });
   }
   __syncthreads();
-  const bool rem_empty = (cfg.flags & 1u) != 0;
   const int w = winner;
   const bool w_shifts = w >= 0 && !bit_of(I, w);
-  // phase 2: allowed set after each allowed terminal's shift; the last thread
-  // runs the end-of-sequence gate (mid-lexeme aware)
-  if (tid < tb.T && bit_of(A, tid)) {
-    const Post& p = posts[tid];
-    uint32_t acc[MW];
-    if (allowed_set<true, MW>(pt, bs, p.k, p.m, in_mem<true>((const uint16_t*)p.ov), my, kPostCap + kTmpCap, acc) <
-        0)
-      overflow = 1;
+  if (t == w && shifted) {
 #pragma unroll
-    for (int k = 0; k < MW; ++k) a2[tid * 8 + k] = acc[k];
-    if (tid == w) {
-#pragma unroll
-      for (int k = 0; k < MW; ++k) Aw[k] = acc[k];
-    }
-  } else if (tid == kBlock - 1) {
-    int ok = 0;
-    if (rem_empty || (w >= 0 && !w_shifts)) {
-      ok = sim1_test<true, MW>(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, tb.T) == 2;
-    } else if (w >= 0) {
-      const Post& p = posts[w];
-      ok = sim1_test<true, MW>(pt, bs, p.k, p.m, in_mem<true>((const uint16_t*)p.ov), my, kPostCap + kTmpCap,
-                               tb.T) == 2;
-    }
-    eos_ok = ok;
+    for (int k = 0; k < MW; ++k)
+      if (half < 0 || k / (MW / 2) == half) Aw[k] = acc[k];
   }
+  if (tid == 0) eos_ok = (rem_empty || (w >= 0 && !w_shifts)) ? eos_sigma : (w >= 0 ? (int)eos_after[w] : 0);
   __syncthreads();
   // phase 3: the trailing-flag tables of every DFA state under A(sigma) and
   // after the winner's shift, the bytes that continue the pending lexeme in
@@ -1721,7 +1783,7 @@ struct ResLds {  // byte offsets into dynamic LDS
   ParseLds pl;
 };
 
-__host__ __device__ inline ResLds res_lds(const Tables& tb, int mw, int B) {
+__host__ __device__ inline ResLds res_lds_with(const Tables& tb, int mw, int B, bool dense) {
   ResLds w;
   uint32_t o = 0;
   w.dfa = o;
@@ -1737,12 +1799,12 @@ __host__ __device__ inline ResLds res_lds(const Tables& tb, int mw, int B) {
   w.acc_list = o;
   o += pad16((uint32_t)tb.n_acc);
   w.parse = o;
-  w.pl = parse_lds(tb, o);
+  w.pl = parse_lds(tb, o, dense);
   o += w.pl.total;
   w.live = o;
   o += pad16((uint32_t)(tb.S * mw * 4));
-  w.lanes = o;
-  o += kWalkThreads * kFastLane * 2;
+  w.lanes = o;  // stack areas of the first kLaneSlots lanes of each wave
+  o += (kWalkThreads / 64) * kLaneSlots * kFastLane * 2;
   w.umask = o;  // per work item: its residue bitmap word
   o += kMaxItems * 8;
   w.upre = o;   // prefix counts of residue spellings over the items
@@ -1756,6 +1818,14 @@ __host__ __device__ inline ResLds res_lds(const Tables& tb, int mw, int B) {
   o += w.block * (uint32_t)g;
   w.total = o;
   return w;
+}
+
+// The residue kernel's LDS: GOTO as the dense table when that still leaves
+// room for the whole row group, else as the hash.
+__host__ __device__ inline ResLds res_lds(const Tables& tb, int mw, int B) {
+  const ResLds d = res_lds_with(tb, mw, B, true);
+  if (d.group == (kRowGroup < B ? kRowGroup : B) && d.total + 64 <= kWalkLdsMax) return d;
+  return res_lds_with(tb, mw, B, false);
 }
 
 // Everything the residue lanes share about the grammar (pointers into LDS).
@@ -2015,7 +2085,9 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
   const uint32_t* acc_off_s = (const uint32_t*)(lds + WL.acc_off);
   const uint8_t* acc_list_s = lds + WL.acc_list;
   uint8_t* rows_s = lds + WL.rows;
-  const mptr<true, uint16_t> lane_area = in_mem<true>((uint16_t*)(lds + WL.lanes) + tid * kFastLane);
+  // lanes kLaneSlots and above of a wave never judge a spelling (chunks are smaller)
+  const mptr<true, uint16_t> lane_area =
+      in_mem<true>((uint16_t*)(lds + WL.lanes) + ((tid >> 6) * kLaneSlots + (lane & (kLaneSlots - 1))) * kFastLane);
   uint8_t* rows = ws + kWsHead;
   const int nsub = (tb.U + 63) / 64;
   bool staged = false;
@@ -2413,7 +2485,7 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
                                GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH,   GRID_ART_LEX_PREFIX,
                                GRID_ART_SPELL_OF_ID, GRID_ART_CLASS_MAP, GRID_ART_CLASS_OFF,
                                GRID_ART_CLASS_REC,   GRID_ART_LEX_STRIDE,  GRID_ART_LEX_TOKEN,
-                               GRID_ART_ID_FIRST,    GRID_ART_PARSE_SHIFT};
+                               GRID_ART_ID_FIRST,    GRID_ART_PARSE_SHIFT, GRID_ART_GOTO};
   for (int w : needed)
     if (!bound(g, w)) return fail(GRID_E_UNBOUND, "grid_mask: artifact " + std::to_string(w) + " is not bound");
   Tables tb;
@@ -2427,6 +2499,7 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
   tb.pstate = (const uint32_t*)g->dev[GRID_ART_PARSE_STATE];
   tb.predx = (const uint32_t*)g->dev[GRID_ART_PARSE_REDX];
   tb.pshift = (const uint16_t*)g->dev[GRID_ART_PARSE_SHIFT];
+  tb.go = (const uint16_t*)g->dev[GRID_ART_GOTO];
   tb.ghash = (const uint2*)g->dev[GRID_ART_GOTO_HASH];
   tb.spell_off = (const uint32_t*)g->dev[GRID_ART_SPELL_OFF];
   tb.spell_bytes = (const uint8_t*)g->dev[GRID_ART_SPELL_BYTES];
