@@ -487,9 +487,12 @@ __device__ __forceinline__ uint16_t stack_at_top(const BaseStack<L>& bs, uint32_
                                                  mptr<L, const uint16_t> ov, int t,
                                                  mptr<L, const uint16_t> tmp) {
   if constexpr (L) {
-    if (t == 0 && m == 0 && k - 1u < bs.lo) return bs.pool[k - 1u];
-    const mptr<L, const uint16_t> p = t > 0 ? tmp + (t - 1) : (m > 0 ? ov + (m - 1) : bs.win + (k - 1u - bs.lo));
-    return *p;
+    const uint32_t i = k - 1u;
+    const bool deep = t == 0 && m == 0 && i < bs.lo;
+    const mptr<L, const uint16_t> p = t > 0 ? tmp + (t - 1) : (m > 0 ? ov + (m - 1) : bs.win + (deep ? 0u : i - bs.lo));
+    uint16_t v = *p;  // a valid LDS address in every case
+    if (deep) v = bs.pool[i];
+    return v;
   } else {
     if (t > 0) return tmp[t - 1];
     if (m > 0) return ov[m - 1];
@@ -518,7 +521,8 @@ __device__ __forceinline__ uint32_t goto_source(const BaseStack<L>& bs, uint32_t
                                                 uint32_t k, int m, mptr<L, const uint16_t> ov, int t,
                                                 mptr<L, const uint16_t> tmp) {
   const uint32_t sb = len == 0 ? s : below;
-  return (len > 1 || sb == kNoState) ? (uint32_t)stack_at_top<L>(bs, k, m, ov, t, tmp) : sb;
+  const uint32_t top = stack_at_top<L>(bs, k, m, ov, t, tmp);  // read in every case: fewer branches
+  return (len > 1 || sb == kNoState) ? top : sb;
 }
 
 // Reduce chain of terminal x, not changing the stack (pushes go to tmp).  1
@@ -1232,9 +1236,12 @@ __device__ __forceinline__ int emit(const RowCtx<L>& rc, Lane<MW>& ln, mptr<L, u
   const int t = winner_of<MW>(rc.tv, rc.acc_off, rc.acc_list, ln.acur, q,
                               [&]() { return lex_flags_now(*rc.tb, rc.sl, lx); });
   if (t < 0) return 0;
-  if (bit_of(rc.tv.I, t))  // ignored: the stack is unchanged, but in mode 2
-    return ln.mode == 2 ? lane_allowed<L, MW>(rc, ln, ov, cap, q_next) : 1;  // the next lexeme asks anew
-  if (ln.mode == 0) {
+  // an ignored winner leaves the stack unchanged; in mode 2 the next lexeme
+  // still asks anew for its live terminals (the one allowed-set call below
+  // serves ignored and shifted lanes of a wave together)
+  const bool ignored = bit_of(rc.tv.I, t);
+  if (ignored && ln.mode != 2) return 1;
+  if (!ignored && ln.mode == 0) {
     ln.mode = 1;
     ln.t1 = t;
     ln.ph = reinterpret_cast<const uint4*>(rc.post)[2 * t];  // needed at the next shift
@@ -1242,7 +1249,7 @@ __device__ __forceinline__ int emit(const RowCtx<L>& rc, Lane<MW>& ln, mptr<L, u
     for (int w = 0; w < MW; ++w) ln.acur[w] = rc.a2[t * rc.a2_stride + w];
     return 1;
   }
-  if (ln.mode == 1) {  // the stack after t1 (Post: k u16, m u8, ok u8, overlay u16[kPostCap])
+  if (!ignored && ln.mode == 1) {  // the stack after t1 (Post: k u16, m u8, ok u8, overlay u16[kPostCap])
     const uint32_t pk = ln.ph.x & 0xFFFFu, pm = (ln.ph.x >> 16) & 0xFFu, pok = ln.ph.x >> 24;
     if (!pok || pk == 0 || pk > rc.bs.depth || pm > (uint32_t)kPostCap || (int)pm > cap) return -1;
     ln.k = pk;
@@ -1260,8 +1267,10 @@ __device__ __forceinline__ int emit(const RowCtx<L>& rc, Lane<MW>& ln, mptr<L, u
     }
     ln.mode = 2;
   }
-  const int r = sim1_shift<L, MW>(rc.pt, rc.bs, ln.k, ln.m, ov, cap, t);
-  if (r != 1) return r < 0 ? -1 : 0;
+  if (!ignored) {
+    const int r = sim1_shift<L, MW>(rc.pt, rc.bs, ln.k, ln.m, ov, cap, t);
+    if (r != 1) return r < 0 ? -1 : 0;
+  }
   return lane_allowed<L, MW>(rc, ln, ov, cap, q_next);
 }
 
@@ -1663,8 +1672,8 @@ __global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __r
 // spelling in the row's residue bitmap.  Rows served from the mask cache are
 // skipped; rows with a bad configuration get zero words.
 constexpr int kStreamWaves = kBlock / 64;
-constexpr int kStreamUnroll = 4;   // chunks per wave in flight
-constexpr int kStreamRounds = 4;
+constexpr int kStreamUnroll = 2;   // chunks per wave in flight
+constexpr int kStreamRounds = 1;
 constexpr int kStreamChunks = kStreamWaves * kStreamUnroll * kStreamRounds;
 
 __host__ __device__ inline int stream_slices(int V) { return ((V + 63) / 64 + 7) / 8; }
