@@ -1619,6 +1619,9 @@ __global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __r
   uint32_t* tinfo_s = (uint32_t*)(vlds + VL.tinfo);
   uint32_t* acc_off_s = (uint32_t*)(vlds + VL.acc_off);
   uint8_t* acc_list_s = vlds + VL.acc_list;
+  // the first class record is fetched while the tables are staged
+  uint4 rec0 = make_uint4(0, 0, 0, 0);
+  if (blockIdx.y * (uint32_t)kBlock + (uint32_t)tid < n) rec0 = tb.crec[h.cls_base + blockIdx.y * kBlock + tid];
   {
     const StageRegion rg[5] = {{(const uint8_t*)tb.live, (uint8_t*)live_s, (uint32_t)tb.S * 32u},
                                {rw + RL.a2, (uint8_t*)a2_s, (uint32_t)tb.T * 32u},
@@ -1643,7 +1646,7 @@ __global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __r
     const uint32_t c = c0 + tid;
     uint32_t code = kVerdictReject;
     if (c < n) {
-      const uint4 rec = tb.crec[h.cls_base + c];
+      const uint4 rec = c0 == blockIdx.y * (uint32_t)kBlock ? rec0 : tb.crec[h.cls_base + c];
       LexOpen lex;
       code = class_verdict<MW>(h, I_s, live_s, 8, tinfo_s, acc_off_s, acc_list_s, a2_s, 8, rec, lex);
       if (code == kVerdictLexicon)
