@@ -359,6 +359,14 @@ __host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base, b
   return L;
 }
 
+// The prologue's LR tables in LDS: GOTO as the dense table when it fits
+// beside the prologue's own arrays, else as the hash.
+constexpr uint32_t kPrologueParseMax = 96 * 1024;
+__host__ __device__ inline ParseLds prologue_parse_lds(const Tables& tb) {
+  const ParseLds d = parse_lds(tb, 0, true);
+  return d.total <= kPrologueParseMax ? d : parse_lds(tb, 0, false);
+}
+
 __device__ inline StageRegion parse_region(const Tables& tb, uint8_t* lds, const ParseLds& L, int which) {
   if (which == 0) return {(const uint8_t*)tb.pstate, lds + L.st, (uint32_t)tb.n_pstate * 4};
   if (which == 1) return {(const uint8_t*)tb.predx, lds + L.redx, (uint32_t)tb.n_predx * 4};
@@ -891,6 +899,9 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   __shared__ uint16_t scratch[kBlock][kPostCap + kTmpCap];
   __shared__ int bad, overflow, winner, eos_ok, eos_sigma, cache_hit;
   __shared__ uint8_t eos_after[256];  // end-of-sequence test after shifting each candidate winner
+  __shared__ Post posts[256];          // stack after shifting each allowed terminal
+  __shared__ uint32_t a2_s[256][MW];   // allowed set after shifting each allowed terminal
+  __shared__ uint8_t alist[256];       // the allowed terminals in order
   __shared__ unsigned long long hacc[2];
   uint8_t* rw = ws + kWsHead + (size_t)row * rbytes;
   RowHeader* hdr = (RowHeader*)rw;
@@ -898,7 +909,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   Post* post = (Post*)(rw + L.post);
   uint32_t* a2 = (uint32_t*)(rw + L.a2);
   const grid_config cfg = cfgs[row];
-  const ParseLds PL = parse_lds(tb, 0);
+  const ParseLds PL = prologue_parse_lds(tb);
   {
     const StageRegion rg[4] = {parse_region(tb, plds, PL, 0), parse_region(tb, plds, PL, 1),
                                parse_region(tb, plds, PL, 2), parse_region(tb, plds, PL, 3)};
@@ -1049,56 +1060,83 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   const TermView tv{tb.term_info, I, R, tb.live, 8};
   __syncthreads();
 
-  // phase 1, with no barrier inside: terminal t's reduce chain and shift from
-  // sigma (A(sigma) is the set that shifted), then the allowed set of the
-  // stack after the shift; with T < kBlock / 2 two threads take each terminal,
-  // both shift it and each simulates half of the terminal words.  Every
-  // candidate winner of the pending lexeme also runs the end-of-sequence test
-  // after its shift, and a spare thread the test from sigma itself, so the
-  // gate is ready once the winner is known.
-  const bool two = tb.T < kBlock / 2;
-  const int t = two ? (tid & (kBlock / 2 - 1)) : tid;
-  const int half = two ? (tid / (kBlock / 2)) : -1;  // -1: all words
+  // phase 1: terminal t's reduce chain and shift from sigma (thread t; A(sigma)
+  // is the set that shifted, the stacks after the shifts go to LDS and the
+  // row's workspace); a spare thread runs the end-of-sequence gate from sigma
+  // itself (empty remainder, or an ignored winner)
   const bool rem_empty = (cfg.flags & 1u) != 0;
-  uint32_t acc[MW];
-#pragma unroll
-  for (int k = 0; k < MW; ++k) acc[k] = 0;
-  bool shifted = false;
-  if (t < tb.T) {
+  if (tid < tb.T) {
+    const int t = tid;
     uint32_t k = depth;
     int m = 0;
     const int r = sim1_shift<true, MW>(pt, bs, k, m, my, kPostCap, t);
-    if (half <= 0) {
-      if (r < 0 || (r == 1 && k > 0xFFFF)) overflow = 1;
-      if (r == 1) {
-        atomicOr(&A[t >> 5], 1u << (t & 31));
-        Post p;
-        p.k = (uint16_t)k;
-        p.m = (uint8_t)m;
-        p.ok = 1;
-        for (int j = 0; j < kPostCap; ++j) p.ov[j] = j < m ? (uint16_t)my[j] : (uint16_t)0;
-        post[t] = p;
-      }
-    }
+    if (r < 0 || (r == 1 && k > 0xFFFF)) overflow = 1;
     if (r == 1) {
-      shifted = true;
-      uint32_t X[MW];
-#pragma unroll
-      for (int w = 0; w < MW; ++w) X[w] = (half < 0 || w / (MW / 2) == half) ? all_word(tb.T, w) : 0u;
-      if (sim_set<true, MW>(pt, bs, k, m, my, my + m, kPostCap + kTmpCap - m, X, acc) < 0) overflow = 1;
-#pragma unroll
-      for (int w = 0; w < MW; ++w)
-        if (half < 0 || w / (MW / 2) == half) a2[t * 8 + w] = acc[w];
-      if (half <= 0 && !rem_empty) {  // a candidate winner: the gate after its shift
-        bool cand = false;
-        for (uint32_t j = tb.acc_off[cfg.q]; j < tb.acc_off[cfg.q + 1]; ++j) cand = cand || tb.acc_list[j] == t;
-        if (cand) eos_after[t] = sim1_test<true, MW>(pt, bs, k, m, my, my + m, kPostCap + kTmpCap - m, tb.T) == 2;
-      }
+      atomicOr(&A[t >> 5], 1u << (t & 31));
+      Post p;
+      p.k = (uint16_t)k;
+      p.m = (uint8_t)m;
+      p.ok = 1;
+      for (int j = 0; j < kPostCap; ++j) p.ov[j] = j < m ? (uint16_t)my[j] : (uint16_t)0;
+      posts[t] = p;
+      post[t] = p;
     }
-  } else if (tid == kBlock - 1) {  // the gate from sigma (empty remainder, or an ignored winner)
+  } else if (tid == kBlock - 1) {
     eos_sigma = sim1_test<true, MW>(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, tb.T) == 2;
   }
+  if (tid < 256) {
+#pragma unroll
+    for (int w = 0; w < MW; ++w) a2_s[tid][w] = 0u;
+  }
   __syncthreads();
+  // phase 2: the allowed set after each allowed terminal's shift, split into
+  // P jobs per terminal (job j simulates the terminals x with x mod P == j, so
+  // the reduce groups, each of which costs the set simulation a rerun, spread
+  // over the jobs) and sized to the workgroup; then, for every candidate
+  // winner of the pending lexeme, the end-of-sequence gate after its shift
+  int nA = 0;
+#pragma unroll
+  for (int w = 0; w < MW; ++w) nA += __popc(A[w]);
+  if (tid < tb.T && bit_of(A, tid)) {
+    int rank = 0;  // allowed terminals below tid
+#pragma unroll
+    for (int w = 0; w < MW; ++w)
+      if (w < (tid >> 5)) rank += __popc(A[w]);
+      else if (w == (tid >> 5)) rank += __popc(A[w] & ((1u << (tid & 31)) - 1u));
+    alist[rank] = (uint8_t)tid;
+  }
+  __syncthreads();
+  // the set jobs take the first kSetThreads threads, the gates the last wave
+  // (a wave runs divergent branches one after the other)
+  constexpr int kSetThreads = kBlock - 64;
+  const int P = nA > 0 ? max(1, min(32, kSetThreads / nA)) : 1;
+  const int n_set = nA * P;
+  const bool set_lane = tid < kSetThreads;
+  for (int j = set_lane ? tid : n_set + (tid - kSetThreads); j < (set_lane ? n_set : n_set + nA);
+       j += set_lane ? kSetThreads : 64) {
+    const int t = alist[j < n_set ? j / P : j - n_set];
+    const Post& p = posts[t];
+    const mptr<true, const uint16_t> ov = in_mem<true>((const uint16_t*)p.ov);
+    if (j < n_set) {
+      const int part = j % P;
+      uint32_t X[MW], acc[MW];
+#pragma unroll
+      for (int w = 0; w < MW; ++w) {
+        uint32_t x = 0;
+        for (int b = (part - w * 32 % P + P) % P; b < 32; b += P) x |= 1u << b;
+        X[w] = x & all_word(tb.T, w);
+        acc[w] = 0;
+      }
+      if (sim_set<true, MW>(pt, bs, p.k, p.m, ov, my, kPostCap + kTmpCap, X, acc) < 0) overflow = 1;
+#pragma unroll
+      for (int w = 0; w < MW; ++w)
+        if (acc[w]) atomicOr(&a2_s[t][w], acc[w]);
+    } else if (!rem_empty) {
+      bool cand = false;
+      for (uint32_t q = tb.acc_off[cfg.q]; q < tb.acc_off[cfg.q + 1]; ++q) cand = cand || tb.acc_list[q] == t;
+      if (cand) eos_after[t] = sim1_test<true, MW>(pt, bs, p.k, p.m, ov, my, kPostCap + kTmpCap, tb.T) == 2;
+    }
+  }
   // the pending lexeme's winner if a byte ends it
   if (tid == 0 && !rem_empty) {
     uint32_t a0[MW];
@@ -1110,11 +1148,11 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   __syncthreads();
   const int w = winner;
   const bool w_shifts = w >= 0 && !bit_of(I, w);
-  if (t == w && shifted) {
+  if (tid < tb.T && bit_of(A, tid)) {
 #pragma unroll
-    for (int k = 0; k < MW; ++k)
-      if (half < 0 || k / (MW / 2) == half) Aw[k] = acc[k];
+    for (int k = 0; k < MW; ++k) a2[tid * 8 + k] = a2_s[tid][k];
   }
+  if (w >= 0 && tid < MW) Aw[tid] = a2_s[w][tid];
   if (tid == 0) eos_ok = (rem_empty || (w >= 0 && !w_shifts)) ? eos_sigma : (w >= 0 ? (int)eos_after[w] : 0);
   __syncthreads();
   // phase 3: the trailing-flag tables of every DFA state under A(sigma) and
@@ -2429,7 +2467,7 @@ int residue_grid_size(uint32_t lds) {
 template <int MW>
 int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint16_t* pool, uint32_t* mask,
                 uint8_t* eos, int32_t* status, uint8_t* ws, size_t rb, uint32_t phases, hipStream_t s) {
-  const uint32_t parse_bytes = parse_lds(tb, 0).total;
+  const uint32_t parse_bytes = prologue_parse_lds(tb).total;
   if (!raise_lds((const void*)prologue_kernel<MW>, parse_bytes))
     return fail(GRID_E_HIP, "grid_mask: cannot raise the LDS limit");
   if (phases & GRID_PHASE_PROLOGUE) {
@@ -2565,7 +2603,7 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
   const int mw = tb.tw;
   const ResLds WL = res_lds(tb, mw, B);
   if (tb.T > 255 || (mw != 2 && mw != 4 && mw != 8) || WL.total + 64 > kWalkLdsMax ||
-      parse_lds(tb, 0).total > 24 * 1024 || verdict_lds(tb).total > 64 * 1024)
+      prologue_parse_lds(tb).total > kPrologueParseMax || verdict_lds(tb).total > 64 * 1024)
     return fail(GRID_E_CAPACITY, "grid_mask: lexer DFA or LR tables too large for the LDS staging");
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace_dev;
