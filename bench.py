@@ -30,12 +30,12 @@ ROOT = Path(__file__).resolve().parent
 sys.path.insert(0, str(ROOT))
 
 HBM_PEAK_GBS = 8000.0
-TRAFFIC_PROFILE = ROOT / "profiles" / "walk_kernel_traffic_dml_b32.md"
+TRAFFIC_PROFILE = ROOT / "profiles" / "stream_kernel_traffic_dml_b32.md"
 KERNEL_SOURCE = ROOT / "paper_2607_11951_amd" / "csrc" / "kernels.hip"
 
 
-def walk_traffic_bytes():
-    """HBM bytes per walk launch from the committed counter summary
+def stream_traffic_bytes():
+    """HBM bytes per stream-kernel launch from the committed counter summary
     (FETCH_SIZE and WRITE_SIZE per dispatch, each scaled by its plain-copy
     calibration factor), or None when the kernels changed since it was taken."""
     import hashlib
@@ -50,8 +50,8 @@ def walk_traffic_bytes():
     try:
         if kv.get("kernels.hip sha256") != sha:
             return None
-        fetch = float(kv["FETCH_SIZE KiB per walk dispatch"]) * float(kv["FETCH_SIZE copy factor"])
-        write = float(kv["WRITE_SIZE KiB per walk dispatch"]) * float(kv["WRITE_SIZE copy factor"])
+        fetch = float(kv["FETCH_SIZE KiB per stream dispatch"]) * float(kv["FETCH_SIZE copy factor"])
+        write = float(kv["WRITE_SIZE KiB per stream dispatch"]) * float(kv["WRITE_SIZE copy factor"])
     except (KeyError, ValueError):
         return None
     return (fetch + write) * 1024.0
@@ -314,7 +314,7 @@ def main():
                      "note": "separate pass, an event between phases"},
         "roofline": {"bound": "hbm", "kernel": "stream_kernel", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": walk_traffic_bytes(), "bytes_per_mask": bytes_per_mask,
+                     "traffic": stream_traffic_bytes(), "bytes_per_mask": bytes_per_mask,
                      "stream_us_per_launch": walk_s * 1e6},
         "cpu_baseline": cpu,
         "cache": cache_out,

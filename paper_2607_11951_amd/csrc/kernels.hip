@@ -40,6 +40,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 #include <cstdint>
 #include <string>
 
@@ -2433,16 +2434,20 @@ bool bound(const grid_compiled* g, int which) { return g->dev[which] != nullptr 
 
 // Raises a kernel's dynamic-LDS limit (needed above 64 KB of LDS in total)
 // once per kernel, device and size.
+// Raises a kernel's dynamic LDS limit once per (kernel, device, size); the
+// record of what was raised is shared by all host threads.
 bool raise_lds(const void* fn, uint32_t bytes) {
   struct Entry {
     const void* fn;
     int dev;
     uint32_t bytes;
   };
+  static std::mutex mu;
   static Entry done[64];
   static int n_done = 0;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return false;
+  std::lock_guard<std::mutex> lock(mu);
   for (int i = 0; i < n_done; ++i)
     if (done[i].fn == fn && done[i].dev == dev && done[i].bytes >= bytes) return true;
   if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) != hipSuccess) return false;
