@@ -272,10 +272,11 @@ int grid_mask(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
                                        the verdict of every lexeme-program class of the
                                        row's lexer state */
 #define GRID_PHASE_WALK 2u          /* mask_dev in token-id order from the class map;
-                                       tokens whose class needs their bytes go to the
-                                       row's residue list (workspace) */
-#define GRID_PHASE_RESIDUE 4u       /* byte walk of the residue lists, OR-ing allowed
-                                       bits into mask_dev */
+                                       tokens whose class needs their own bytes are
+                                       marked in the row's residue bitmaps (workspace) */
+#define GRID_PHASE_RESIDUE 4u       /* the marked spellings: class verdict with their own
+                                       lexicon flags, else the byte walk; allowed bits
+                                       are OR-ed into mask_dev */
 #define GRID_PHASE_FINALIZE 8u      /* tokens the residue walk handed to the slow path,
                                        then the row status when status_dev is not null */
 #define GRID_PHASE_ALL 15u

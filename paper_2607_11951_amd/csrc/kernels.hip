@@ -5,37 +5,36 @@
 //     row's stack in LDS): thread t runs terminal t's reduce chain and shift
 //     from sigma, so A(sigma) (section 3.2, allowed terminals under table
 //     compression) is the set that shifted and each one's post-shift stack (an
-//     overlay above the shared read-only stack) is recorded; thread t in A then
-//     computes the allowed set of its post-shift stack by set simulation (one
-//     reduce chain for a whole terminal set), while one thread runs the
-//     end-of-sequence gate (section 3.2, EOS gating, mid-lexeme aware); finally
-//     thread b fills entry b of a 256-entry first-byte table: the scan state
-//     after byte b starts a token (continuing the pending lexeme, or emitting
-//     it as its winner and starting a new one), or "rejected".
-//  2. walk (one 1024-thread workgroup per compute unit): items are (row, 64
-//     consecutive spellings); spellings are in byte order, so a wave's lanes
-//     share prefixes and tend to stop at the same byte.  The lexer DFA,
-//     compact LR tables, live-terminal sets, accept lists and, per row, the
-//     first-byte table and trailing-flag tables sit in LDS.  Every lane carries
-//     the allowed set of its current stack: that of sigma, that recorded after
-//     the first shift, or one set-simulated on the lane's LDS overlay after
-//     each later shift (context-dependent part, Proposition 4).  A byte that
-//     kills the DFA emits the pending lexeme as the highest-priority candidate
-//     that is allowed (or ignored) and passes the schema lexicon, then is
-//     scanned again (section 4.1, trie walk); after every byte the pending
-//     lexeme must still complete to an allowed or ignored terminal (Definition
-//     2).  Rejection is monotone, so a lane stops at its first failing byte.
-//     The DFA side of this depends only on (DFA state, spelling), so the scan
-//     summary built at compile time gives each lane where its lexemes end: a
-//     spelling that ends at most one lexeme needs no DFA step at all (the
-//     winner, its shift and the trailing check of the last lexeme remain),
-//     and a longer one starts scanning at its first lexeme end.
-//     A wave writes one 64-bit word of the row's mask in spelling order; a lane
-//     whose LDS stack area is too small hands its spelling to the slow path.
-//  3. finalize: the slow path re-walks handed-over spellings with a large stack
-//     area; then every id takes its spelling's bit (alias expansion), the EOS
-//     bit is set, and the row status is written (Proposition 8: a viable
-//     configuration has a nonempty mask).
+//     overlay above the shared read-only stack) is recorded; the allowed set
+//     of every post-shift stack follows by set simulation (one reduce chain
+//     for a whole terminal set), and the end-of-sequence gate (section 3.2) is
+//     run after each candidate winner's shift and from sigma.  Then the
+//     pending lexeme's winner, the trailing-flag tables of every lexer state
+//     under A(sigma) and after the winner's shift (Definition 2), and the
+//     bytes that continue the pending lexeme in the schema lexicon.
+//  2. verdicts (one thread per lexeme-program class of the row's lexer
+//     state): tokens whose lexeme programs from that state are equal share a
+//     class (the verdict-equivalence idea of section 4.2, fixed at compile
+//     time per state); each class is judged once against A(sigma) and the
+//     prologue's allowed sets after a first shift -- reject, allow, walk (a
+//     second shift or more than three lexeme ends) or lexicon (the verdict
+//     depends on the token's own lexicon flags, section 2 L3).
+//  3. stream (XCD-aware, 64 ids per wave): the mask in token-id order
+//     straight from the class map, one ballot per 64 ids; lexicon classes are
+//     settled by a shortcut where the token's first byte or its token-flag
+//     entry answers the class's first lexicon question; the rest mark their
+//     spellings in the row's residue bitmaps.
+//  4. residue (one 1024-thread workgroup per compute unit): marked
+//     spellings in spelling order, a few per wave; lexicon spellings re-run
+//     their class verdict with their own lexicon flags; the others walk their
+//     bytes (section 4.1): DFA steps in LDS, a byte that kills the DFA emits
+//     the pending lexeme as the highest-priority candidate that is allowed (or
+//     ignored) and passes the lexicon, later shifts simulated on the lane's LDS
+//     overlay; the allowed ids are OR-ed into the mask.  A lane whose stack
+//     area is too small hands its spelling to the slow path.
+//  5. finalize: the slow path re-walks handed-over spellings with a large
+//     stack area, then the row status (Proposition 8: a viable configuration
+//     has a nonempty mask); with a mask cache, the rows' masks are published.
 // grid_apply is a streaming in-place -inf fill of the masked logits.
 #include <hip/hip_runtime.h>
 
