@@ -270,3 +270,33 @@ def test_overlay_handoff_to_slow_path(G, oracle_mod):
     assert (s.cpu().numpy() == 0).all(), s.cpu().tolist()
     bits = np.unpackbits(m[0].cpu().numpy().view(np.uint8), bitorder="little")
     assert bits[vocab.index(b"(" * 60)] == 1    # a 60-deep run is viable and came back exact
+
+
+def test_phases_one_call_each_equal_the_whole_call(G):
+    """The benchmark's phase pass: prologue, stream, residue and finalize in
+    four grid_mask_phases calls give the same masks, EOS flags and status as
+    one grid_mask call (workload 3, B = 32), and a second whole call on the
+    same workspace gives them again."""
+    wl = make_workload(3, rows=32)
+    grid, slot_map = G.from_workload(wl)
+    grid.to_device("cuda")
+    B = len(wl.prefixes)
+    cfgs, pool = grid.configs(wl.prefixes, [slot_map[s] for s in wl.slots])
+    c, p = grid.configs_to_device(cfgs, pool)
+    ws = grid.new_workspace(B, "cuda")
+    stream = torch.cuda.current_stream()
+    outs = []
+    for split in (False, True, False):
+        m = torch.empty((B, grid.W), dtype=torch.int32, device="cuda")
+        e = torch.empty(B, dtype=torch.uint8, device="cuda")
+        s = torch.empty(B, dtype=torch.int32, device="cuda")
+        if split:
+            for ph in (G.grid.PHASE_PROLOGUE, G.grid.PHASE_WALK, G.grid.PHASE_RESIDUE, G.grid.PHASE_FINALIZE):
+                grid.mask(c, p, B, m, e, s, ws, stream, phases=ph)
+        else:
+            grid.mask(c, p, B, m, e, s, ws, stream)
+        torch.cuda.synchronize()
+        outs.append((m.cpu().numpy(), e.cpu().numpy(), s.cpu().numpy()))
+    for m, e, s in outs[1:]:
+        assert np.array_equal(m, outs[0][0]) and np.array_equal(e, outs[0][1]) and np.array_equal(s, outs[0][2])
+    assert (outs[0][2] == 0).all()
