@@ -56,6 +56,9 @@ extern "C" {
 #define GRID_ROW_BAD_CONFIG 2       /* state, slot or stack out of range */
 #define GRID_ROW_OVERFLOW 4         /* a per-lane parser overlay capacity was exceeded;
                                        the row's mask is not exact */
+#define GRID_ROW_NOT_VIABLE 8       /* grid_accept: the token is not allowed at the
+                                       configuration (the prefix would leave Prefix(L)) */
+#define GRID_ROW_FINISHED 16        /* grid_accept: the end-of-sequence token was accepted */
 
 typedef struct grid_compiled grid_compiled;
 
@@ -314,6 +317,25 @@ int grid_mask_cached(const grid_compiled* g, int32_t B, const grid_config* cfg_d
                      const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
                      int32_t* status_dev, void* workspace_dev, size_t workspace_bytes, void* cache_dev,
                      size_t cache_bytes, uint32_t cache_flags, void* stream);
+
+/* ------------------------------------------------------------------- accept */
+/* Device incremental advance (section 6.1, per-token step 7): for every row b,
+ * the configuration cfg_dev[b] (stack in stack_pool_dev) followed by token
+ * token_dev[b].  The token's bytes are lexed and parsed with the same rules as
+ * the mask (maximal munch, contextual resolution by priority, lexicon word and
+ * prefix tests, Definition 2 for the new pending lexeme); the new
+ * configuration goes to cfg_out_dev[b], its stack to
+ * stack_out_dev[b * stack_cap ..] (cfg_out_dev[b].stk_off = b * stack_cap), so
+ * cfg_out_dev and stack_out_dev are the next step's inputs.  status_dev[b]
+ * (nullable): GRID_ROW_OK, GRID_ROW_NOT_VIABLE (token not allowed),
+ * GRID_ROW_FINISHED (the end-of-sequence token, accepted: the sentence is in
+ * L), GRID_ROW_BAD_CONFIG or GRID_ROW_OVERFLOW (stack_cap too small); in all
+ * but GRID_ROW_OK the row's configuration is copied unchanged.  Device
+ * buffers are caller-owned and must not overlap; stack_cap >= 2.
+ * Asynchronous on stream. */
+int grid_accept(const grid_compiled* g, int32_t B, const grid_config* cfg_dev, const uint16_t* stack_pool_dev,
+                const int32_t* token_dev, grid_config* cfg_out_dev, uint16_t* stack_out_dev, uint32_t stack_cap,
+                int32_t* status_dev, void* stream);
 
 /* -------------------------------------------------------------------- apply */
 #define GRID_DTYPE_F32 0

@@ -2429,6 +2429,190 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(const uint32_t* __restric
   }
 }
 
+// ------------------------------------------------------------------ accept
+// Reduce chain of terminal x on the stack stk[0, d), then its shift: the
+// array itself changes.  Called only for a terminal whose test succeeded.
+// 1 shifted, 2 accept (x is the end of input), 0 error, -1 capacity.
+template <int MW>
+__device__ int stack_commit(const ParseTabs<false>& pt, uint16_t* stk, uint32_t& d, uint32_t cap, int x) {
+  const uint32_t w = (uint32_t)x >> 5, bit = 1u << (x & 31);
+  for (int guard = 0; guard < kGuard; ++guard) {
+    const uint32_t s = stk[d - 1];
+    const uint32_t a = action_of<false, MW>(pt, s, w, bit);
+    if (a == kActShiftP) {
+      if (x == pt.T) return 2;
+      if (d >= cap) return -1;
+      stk[d++] = shift_target<false, MW>(pt, s, x);
+      return 1;
+    }
+    if (a == kNoProd) return 0;
+    const uint32_t len = a >> 16;
+    if (len >= d) return 0;
+    d -= len;
+    const uint16_t g = goto_of<false>(pt, stk[d - 1], a & 0xFFFFu);
+    if (g == kNoGoto) return 0;
+    if (d >= cap) return -1;
+    stk[d++] = g;
+  }
+  return -1;
+}
+
+// Device incremental advance (section 6.1, per-token step 7): row b's
+// configuration followed by token tokens[b].  One thread per row, tables in
+// global memory (a per-step call, not the mask's hot loop).  The token's
+// bytes go through the lexer with maximal munch; a byte that kills the DFA
+// emits the pending lexeme as the highest-priority candidate that is ignored
+// or shifts and passes its category's lexicon, and a shifted terminal runs
+// its reduce chain on the row's stack, copied to pool_out + b * cap first.
+// The new pending lexeme must still complete to an allowed or ignored
+// terminal (Definition 2).  The end-of-sequence token is accepted when the
+// end-of-sequence gate holds (then the row is finished).
+template <int MW>
+__global__ __launch_bounds__(64) void accept_kernel(Tables tb, const grid_config* __restrict__ cfgs,
+                                                    const uint16_t* __restrict__ pool,
+                                                    const int32_t* __restrict__ tokens, grid_config* cfg_out,
+                                                    uint16_t* pool_out, uint32_t cap, int32_t* status, int B) {
+  const int row = (int)(blockIdx.x * 64 + threadIdx.x);
+  if (row >= B) return;
+  const grid_config cfg = cfgs[row];
+  const int tok = tokens[row];
+  grid_config out = cfg;
+  int32_t st = GRID_ROW_OK;
+  auto done = [&]() {
+    cfg_out[row] = out;
+    if (status) status[row] = st;
+  };
+  if (cfg.q >= (uint32_t)tb.S || cfg.q == (uint32_t)kDead || cfg.slot >= (uint32_t)tb.n_slots ||
+      cfg.stk_depth < 1 || cfg.stk_depth > cap || tok < 0 || tok >= tb.V) {
+    st = GRID_ROW_BAD_CONFIG;
+    return done();
+  }
+  uint16_t* stk = pool_out + (size_t)row * cap;
+  uint32_t d = cfg.stk_depth;
+  for (uint32_t i = 0; i < d; ++i) stk[i] = pool[cfg.stk_off + i];
+  const Slot sl = load_slot(tb, (int)cfg.slot);
+  const ParseTabs<false> pt = global_parse(tb);
+  auto ignored = [&](int t) { return (tb.term_info[t] & 1u) != 0; };
+  auto restricted_cat = [&](int t) -> int {  // category the row's lexicon restricts, or -1
+    const uint32_t c = (tb.term_info[t] >> 8) & 0xFFu;
+    return c != 0xFFu && ((sl.restricted >> c) & 1u) ? (int)c : -1;
+  };
+  // can terminal t be shifted from the stack now (reduce chain only, pushes
+  // above the stack, which stays as it is)?
+  // 1 shift, 2 accept (the end of input), 0 error, -1 capacity
+  auto shifts = [&](int t) -> int {
+    if (d >= cap) return -1;
+    const BaseStack<false> bs{stk, nullptr, d, d};
+    return sim1_test<false, MW>(pt, bs, d, 0, stk + d, stk + d, (int)(cap - d), t);
+  };
+  uint32_t q = cfg.q, lex = cfg.lexnode, rem = (cfg.flags & 1u) ? 0u : cfg.rem_len;
+  uint8_t head[8];
+  for (int k = 0; k < 8; ++k) head[k] = rem > 0 ? cfg.rem_head[k] : 0;
+  // the pending lexeme's winner in state q (lexicon node lex): -1 none, else
+  // the terminal; capacity problems surface as -2
+  auto winner = [&]() -> int {
+    for (uint32_t j = tb.acc_off[q]; j < tb.acc_off[q + 1]; ++j) {
+      const int t = tb.acc_list[j];
+      const int c = restricted_cat(t);
+      if (c >= 0 && !((lex_flags_of(tb, sl, lex) >> (8 + c)) & 1u)) continue;
+      if (ignored(t)) return t;
+      const int r = shifts(t);
+      if (r < 0) return -2;
+      if (r == 1) return t;
+    }
+    return -1;
+  };
+  if (tok == tb.eos_id) {  // the end-of-sequence gate (section 3.2)
+    int ok = 0;
+    if (rem == 0) {
+      ok = shifts(tb.T) == 2;
+    } else {
+      const int w = winner();
+      if (w == -2) st = GRID_ROW_OVERFLOW;
+      else if (w >= 0 && ignored(w)) ok = shifts(tb.T) == 2;
+      else if (w >= 0 && stack_commit<MW>(pt, stk, d, cap, w) == 1) ok = shifts(tb.T) == 2;
+    }
+    if (st == GRID_ROW_OK) st = ok ? GRID_ROW_FINISHED : GRID_ROW_NOT_VIABLE;
+    return done();  // the configuration itself is unchanged
+  }
+  const uint32_t su = tb.spell_of_id[tok];
+  if (su == 0xFFFFFFFFu) {  // special or empty token
+    st = GRID_ROW_NOT_VIABLE;
+    return done();
+  }
+  const uint32_t b0 = tb.spell_off[su], n = tb.spell_off[su + 1] - b0;
+  for (uint32_t i = 0; i < n && st == GRID_ROW_OK; ++i) {
+    const uint32_t b = tb.spell_bytes[b0 + i];
+    const int nq = tb.dfa[q * tb.C + tb.bclass[b]];
+    if (nq != kDead) {
+      q = (uint32_t)nq;
+      lex = lex_child(tb, sl, lex, b);
+      if (rem < 8) head[rem] = (uint8_t)b;
+      ++rem;
+      continue;
+    }
+    // b kills the pending lexeme: emit it
+    if (rem == 0 || tb.acc_off[q + 1] == tb.acc_off[q]) {
+      st = GRID_ROW_NOT_VIABLE;
+      break;
+    }
+    const int w = winner();
+    if (w == -2) {
+      st = GRID_ROW_OVERFLOW;
+      break;
+    }
+    if (w < 0) {
+      st = GRID_ROW_NOT_VIABLE;
+      break;
+    }
+    if (!ignored(w)) {
+      const int r = stack_commit<MW>(pt, stk, d, cap, w);
+      if (r != 1) {
+        st = r < 0 ? GRID_ROW_OVERFLOW : GRID_ROW_NOT_VIABLE;
+        break;
+      }
+    }
+    const int q1 = tb.dfa[kStart * tb.C + tb.bclass[b]];
+    if (q1 == kDead) {
+      st = GRID_ROW_NOT_VIABLE;
+      break;
+    }
+    q = (uint32_t)q1;
+    lex = lex_child(tb, sl, 0u, b);
+    rem = 1;
+    head[0] = (uint8_t)b;
+    for (int k = 1; k < 8; ++k) head[k] = 0;
+  }
+  if (st == GRID_ROW_OK && rem > 0) {  // Definition 2 for the pending lexeme
+    bool ok = false;
+    const uint32_t* lv = tb.live + (size_t)q * 8;
+    for (int t = 0; t < tb.T && !ok; ++t) {
+      if (!((lv[t >> 5] >> (t & 31)) & 1u)) continue;
+      const int c = restricted_cat(t);
+      if (c >= 0 && !((lex_flags_of(tb, sl, lex) >> c) & 1u)) continue;
+      if (ignored(t)) {
+        ok = true;
+      } else {
+        const int r = shifts(t);
+        if (r < 0) st = GRID_ROW_OVERFLOW;
+        ok = r == 1;
+        if (r < 0) break;
+      }
+    }
+    if (!ok && st == GRID_ROW_OK) st = GRID_ROW_NOT_VIABLE;
+  }
+  if (st == GRID_ROW_OK) {
+    out.stk_off = (uint32_t)row * cap;
+    out.stk_depth = d;
+    out.lexnode = lex;
+    out.q = (uint16_t)q;
+    out.flags = rem == 0 ? 1u : 0u;
+    out.rem_len = rem;
+    for (int k = 0; k < 8; ++k) out.rem_head[k] = head[k];
+  }
+  done();
+}
+
 bool bound(const grid_compiled* g, int which) { return g->dev[which] != nullptr || g->dev_bytes[which] == 0; }
 
 // Raises a kernel's dynamic-LDS limit (needed above 64 KB of LDS in total)
@@ -2518,18 +2702,9 @@ extern "C" size_t grid_mask_workspace_bytes(const grid_compiled* g, int32_t B) {
   return workspace_size(g, B);
 }
 
-static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_dev, const uint16_t* stack_pool_dev,
-                     uint32_t* mask_dev, uint8_t* eos_dev, int32_t* status_dev, void* workspace_dev,
-                     size_t workspace_bytes, void* cache_dev, size_t cache_bytes, uint32_t cache_flags,
-                     uint32_t phases, void* stream) {
-  clear_error();
-  if (phases & ~GRID_PHASE_ALL) return fail(GRID_E_ARG, "grid_mask: unknown phase bits");
-  if (cache_flags & ~(GRID_CACHE_LOOKUP | GRID_CACHE_INSERT)) return fail(GRID_E_ARG, "grid_mask: unknown cache flags");
-  if (!g || B <= 0 || B > 65535 || !cfg_dev || !stack_pool_dev || !mask_dev || !workspace_dev)
-    return fail(GRID_E_ARG, "grid_mask: null pointer or batch size out of range");
-  const size_t rb = row_bytes(g);
-  if (workspace_bytes < workspace_size(g, B)) return fail(GRID_E_ARG, "grid_mask: workspace too small");
-  if (((uintptr_t)workspace_dev & 255) != 0) return fail(GRID_E_ARG, "grid_mask: workspace not 256-byte aligned");
+// The device tables of a compiled handle (every artifact bound, else
+// GRID_E_UNBOUND).
+static int bind_tables(const grid_compiled* g, Tables& tb) {
   static const int needed[] = {GRID_ART_DFA_CLASS,   GRID_ART_BYTE_CLASS,  GRID_ART_DFA_ACCEPT_OFF,
                                GRID_ART_DFA_ACCEPT_LIST, GRID_ART_DFA_LIVE, GRID_ART_ACTION,
                                GRID_ART_PROD,        GRID_ART_TERM_INFO,   GRID_ART_SPELL_OFF,
@@ -2541,8 +2716,7 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
                                GRID_ART_CLASS_REC,   GRID_ART_LEX_STRIDE,  GRID_ART_LEX_TOKEN,
                                GRID_ART_ID_FIRST,    GRID_ART_PARSE_SHIFT, GRID_ART_GOTO};
   for (int w : needed)
-    if (!bound(g, w)) return fail(GRID_E_UNBOUND, "grid_mask: artifact " + std::to_string(w) + " is not bound");
-  Tables tb;
+    if (!bound(g, w)) return fail(GRID_E_UNBOUND, "artifact " + std::to_string(w) + " is not bound");
   tb.dfa = (const uint16_t*)g->dev[GRID_ART_DFA_CLASS];
   tb.bclass = (const uint8_t*)g->dev[GRID_ART_BYTE_CLASS];
   tb.acc_off = (const uint32_t*)g->dev[GRID_ART_DFA_ACCEPT_OFF];
@@ -2590,6 +2764,24 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
   tb.n_pshift = (int)g->parser.pshift.size();
   tb.n_acc = (int)g->dfa.accept_list.size();
   tb.hbits = g->parser.goto_hbits;
+  return GRID_OK;
+}
+
+static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_dev, const uint16_t* stack_pool_dev,
+                     uint32_t* mask_dev, uint8_t* eos_dev, int32_t* status_dev, void* workspace_dev,
+                     size_t workspace_bytes, void* cache_dev, size_t cache_bytes, uint32_t cache_flags,
+                     uint32_t phases, void* stream) {
+  clear_error();
+  if (phases & ~GRID_PHASE_ALL) return fail(GRID_E_ARG, "grid_mask: unknown phase bits");
+  if (cache_flags & ~(GRID_CACHE_LOOKUP | GRID_CACHE_INSERT)) return fail(GRID_E_ARG, "grid_mask: unknown cache flags");
+  if (!g || B <= 0 || B > 65535 || !cfg_dev || !stack_pool_dev || !mask_dev || !workspace_dev)
+    return fail(GRID_E_ARG, "grid_mask: null pointer or batch size out of range");
+  const size_t rb = row_bytes(g);
+  if (workspace_bytes < workspace_size(g, B)) return fail(GRID_E_ARG, "grid_mask: workspace too small");
+  if (((uintptr_t)workspace_dev & 255) != 0) return fail(GRID_E_ARG, "grid_mask: workspace not 256-byte aligned");
+  Tables tb;
+  const int brc = bind_tables(g, tb);
+  if (brc != GRID_OK) return brc;
   tb.cache = nullptr;
   tb.cache_mask = 0;
   tb.cache_flags = 0;
@@ -2664,6 +2856,32 @@ extern "C" int grid_cache_clear(const grid_compiled* g, void* cache_dev, size_t 
                      (uint32_t)n, stride);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_cache_clear launch: ") + hipGetErrorString(e));
+  return GRID_OK;
+}
+
+extern "C" int grid_accept(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                           const uint16_t* stack_pool_dev, const int32_t* token_dev, grid_config* cfg_out_dev,
+                           uint16_t* stack_out_dev, uint32_t stack_cap, int32_t* status_dev, void* stream) {
+  clear_error();
+  if (!g || B <= 0 || !cfg_dev || !stack_pool_dev || !token_dev || !cfg_out_dev || !stack_out_dev || stack_cap < 2)
+    return fail(GRID_E_ARG, "grid_accept: null pointer or bad size");
+  Tables tb;
+  const int rc = bind_tables(g, tb);
+  if (rc != GRID_OK) return rc;
+  if (tb.T > 255) return fail(GRID_E_CAPACITY, "grid_accept: more than 255 terminals");
+  hipStream_t s = (hipStream_t)stream;
+  const dim3 grid((unsigned)((B + 63) / 64));
+  if (tb.tw == 2)
+    hipLaunchKernelGGL(accept_kernel<2>, grid, dim3(64), 0, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
+                       stack_out_dev, stack_cap, status_dev, B);
+  else if (tb.tw == 4)
+    hipLaunchKernelGGL(accept_kernel<4>, grid, dim3(64), 0, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
+                       stack_out_dev, stack_cap, status_dev, B);
+  else
+    hipLaunchKernelGGL(accept_kernel<8>, grid, dim3(64), 0, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
+                       stack_out_dev, stack_cap, status_dev, B);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_accept launch: ") + hipGetErrorString(e));
   return GRID_OK;
 }
 

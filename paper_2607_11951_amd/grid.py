@@ -20,7 +20,7 @@ ERRORS = {
     -7: "GRID_E_VOCAB", -8: "GRID_E_NOT_VIABLE", -9: "GRID_E_UNBOUND", -10: "GRID_E_HIP",
     -11: "GRID_E_CAPACITY",
 }
-ROW_OK, ROW_EMPTY, ROW_BAD_CONFIG, ROW_OVERFLOW = 0, 1, 2, 4
+ROW_OK, ROW_EMPTY, ROW_BAD_CONFIG, ROW_OVERFLOW, ROW_NOT_VIABLE, ROW_FINISHED = 0, 1, 2, 4, 8, 16
 CACHE_LOOKUP, CACHE_INSERT = 1, 2
 DTYPE_F32, DTYPE_BF16 = 0, 1
 
@@ -41,7 +41,7 @@ assert CONFIG_DTYPE.itemsize == 32
 EXPORTS = ["grid_compile", "grid_free", "grid_last_error", "grid_info", "grid_add_lexicon",
            "grid_artifact", "grid_bind_device", "grid_config_from_prefix",
            "grid_mask_workspace_bytes", "grid_mask", "grid_mask_phases", "grid_apply",
-           "grid_cache_bytes", "grid_cache_clear", "grid_mask_cached"]
+           "grid_cache_bytes", "grid_cache_clear", "grid_mask_cached", "grid_accept"]
 PHASE_PROLOGUE, PHASE_WALK, PHASE_RESIDUE, PHASE_FINALIZE, PHASE_ALL = 1, 2, 4, 8, 15
 
 
@@ -97,6 +97,7 @@ def lib():
         L.grid_mask.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, sz, vp]
         L.grid_mask_phases.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
         L.grid_apply.argtypes = [vp, vp, i32, i32, i32, ctypes.c_int64, vp]
+        L.grid_accept.argtypes = [vp, i32, vp, vp, vp, vp, vp, ctypes.c_uint32, vp, vp]
         L.grid_mask_cached.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, sz, vp, sz, ctypes.c_uint32, vp]
         L.grid_cache_bytes.argtypes = [vp, i32]
         L.grid_cache_bytes.restype = sz
@@ -217,6 +218,26 @@ class Grid:
         c = torch.from_numpy(cfgs.view(np.uint8).copy()).to(device)
         p = torch.from_numpy(pool.view(np.int16).copy()).to(device)
         return c, p
+
+    def accept(self, cfg_dev, pool_dev, tokens_dev, B, stack_cap, out=None, stack_out=None, status=None,
+               stream=None):
+        """Device incremental advance (grid_accept): row b's configuration followed by
+        token tokens_dev[b].  Returns (configs uint8 [B * 32], stack pool int16
+        [B * stack_cap], status int32 [B]); the first two are the next step's inputs."""
+        import torch
+        dev = cfg_dev.device
+        if out is None:
+            out = torch.empty(B * 32, dtype=torch.uint8, device=dev)
+        if stack_out is None:
+            stack_out = torch.empty(B * stack_cap, dtype=torch.int16, device=dev)
+        if status is None:
+            status = torch.empty(B, dtype=torch.int32, device=dev)
+        assert tokens_dev.dtype == torch.int32 and tokens_dev.numel() >= B
+        _check(lib().grid_accept(self.h, B, ctypes.c_void_p(cfg_dev.data_ptr()),
+                                 ctypes.c_void_p(pool_dev.data_ptr()), ctypes.c_void_p(tokens_dev.data_ptr()),
+                                 ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(stack_out.data_ptr()),
+                                 stack_cap, ctypes.c_void_p(status.data_ptr()), _stream_handle(stream)))
+        return out, stack_out, status
 
     def workspace_bytes(self, B):
         return lib().grid_mask_workspace_bytes(self.h, B)
