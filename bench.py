@@ -227,6 +227,39 @@ def main():
     res_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
     tail_ms = np.array([e[3].elapsed_time(e[4]) for e in evs])
 
+    # device incremental advance beside the mask: every row takes one token its
+    # mask allows (grid_accept), timed over the same batches
+    acc_inputs = []
+    for i in range(len(batches)):
+        c, p = batches[i]
+        grid.mask(c, p, B, mask, eos, status, ws, stream)
+        torch.cuda.synchronize()
+        bits = np.unpackbits(mask.cpu().numpy().view(np.uint8), axis=1, bitorder="little")[:, :wl.V]
+        rng = np.random.default_rng(5000 + i)
+        toks = []
+        for r in range(B):
+            allowed = np.flatnonzero(bits[r])
+            allowed = allowed[allowed != wl.eos_id]
+            toks.append(int(rng.choice(allowed)) if len(allowed) else wl.eos_id)
+        acc_inputs.append(torch.tensor(toks, dtype=torch.int32, device=dev))
+    acc_cap = 1024
+    acc_out = (torch.empty(B * 32, dtype=torch.uint8, device=dev),
+               torch.empty(B * acc_cap, dtype=torch.int16, device=dev),
+               torch.empty(B, dtype=torch.int32, device=dev))
+    for i in range(len(batches)):
+        c, p = batches[i]
+        grid.accept(c, p, acc_inputs[i], B, acc_cap, *acc_out, stream=stream)
+    torch.cuda.synchronize()
+    assert (acc_out[2].cpu() == 0).all()
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record(stream)
+    for i in range(args.steps):
+        c, p = batches[i % len(batches)]
+        grid.accept(c, p, acc_inputs[i % len(batches)], B, acc_cap, *acc_out, stream=stream)
+    a1.record(stream)
+    torch.cuda.synchronize()
+    accept_us = a0.elapsed_time(a1) * 1000.0 / args.steps
+
     # algorithmic bytes of one stream launch per row: the class of every token
     # id for the row's lexer state (u16) and the row's W mask words; the
     # verdict table (2 bits per class) is not counted
@@ -318,6 +351,8 @@ def main():
                      "stream_us_per_launch": walk_s * 1e6},
         "cpu_baseline": cpu,
         "cache": cache_out,
+        "accept": {"us_per_step": accept_us, "rows": B,
+                   "note": "grid_accept of one allowed token per row, back to back over the same batches"},
     }
     print(json.dumps(out), flush=True)
 
