@@ -2433,23 +2433,23 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(const uint32_t* __restric
 // Reduce chain of terminal x on the stack stk[0, d), then its shift: the
 // array itself changes.  Called only for a terminal whose test succeeded.
 // 1 shifted, 2 accept (x is the end of input), 0 error, -1 capacity.
-template <int MW>
-__device__ int stack_commit(const ParseTabs<false>& pt, uint16_t* stk, uint32_t& d, uint32_t cap, int x) {
+template <bool L, int MW>
+__device__ int stack_commit(const ParseTabs<L>& pt, mptr<L, uint16_t> stk, uint32_t& d, uint32_t cap, int x) {
   const uint32_t w = (uint32_t)x >> 5, bit = 1u << (x & 31);
   for (int guard = 0; guard < kGuard; ++guard) {
     const uint32_t s = stk[d - 1];
-    const uint32_t a = action_of<false, MW>(pt, s, w, bit);
+    const uint32_t a = action_of<L, MW>(pt, s, w, bit);
     if (a == kActShiftP) {
       if (x == pt.T) return 2;
       if (d >= cap) return -1;
-      stk[d++] = shift_target<false, MW>(pt, s, x);
+      stk[d++] = shift_target<L, MW>(pt, s, x);
       return 1;
     }
     if (a == kNoProd) return 0;
     const uint32_t len = a >> 16;
     if (len >= d) return 0;
     d -= len;
-    const uint16_t g = goto_of<false>(pt, stk[d - 1], a & 0xFFFFu);
+    const uint16_t g = goto_of<L>(pt, stk[d - 1], a & 0xFFFFu);
     if (g == kNoGoto) return 0;
     if (d >= cap) return -1;
     stk[d++] = g;
@@ -2457,41 +2457,31 @@ __device__ int stack_commit(const ParseTabs<false>& pt, uint16_t* stk, uint32_t&
   return -1;
 }
 
-// Device incremental advance (section 6.1, per-token step 7): row b's
-// configuration followed by token tokens[b].  One thread per row, tables in
-// global memory (a per-step call, not the mask's hot loop).  The token's
-// bytes go through the lexer with maximal munch; a byte that kills the DFA
-// emits the pending lexeme as the highest-priority candidate that is ignored
-// or shifts and passes its category's lexicon, and a shifted terminal runs
-// its reduce chain on the row's stack, copied to pool_out + b * cap first.
-// The new pending lexeme must still complete to an allowed or ignored
-// terminal (Definition 2).  The end-of-sequence token is accepted when the
-// end-of-sequence gate holds (then the row is finished).
-template <int MW>
-__global__ __launch_bounds__(64) void accept_kernel(Tables tb, const grid_config* __restrict__ cfgs,
-                                                    const uint16_t* __restrict__ pool,
-                                                    const int32_t* __restrict__ tokens, grid_config* cfg_out,
-                                                    uint16_t* pool_out, uint32_t cap, int32_t* status, int B) {
-  const int row = (int)(blockIdx.x * 64 + threadIdx.x);
-  if (row >= B) return;
-  const grid_config cfg = cfgs[row];
-  const int tok = tokens[row];
-  grid_config out = cfg;
-  int32_t st = GRID_ROW_OK;
-  auto done = [&]() {
-    cfg_out[row] = out;
-    if (status) status[row] = st;
-  };
-  if (cfg.q >= (uint32_t)tb.S || cfg.q == (uint32_t)kDead || cfg.slot >= (uint32_t)tb.n_slots ||
-      cfg.stk_depth < 1 || cfg.stk_depth > cap || tok < 0 || tok >= tb.V) {
-    st = GRID_ROW_BAD_CONFIG;
-    return done();
-  }
-  uint16_t* stk = pool_out + (size_t)row * cap;
-  uint32_t d = cfg.stk_depth;
-  for (uint32_t i = 0; i < d; ++i) stk[i] = pool[cfg.stk_off + i];
-  const Slot sl = load_slot(tb, (int)cfg.slot);
-  const ParseTabs<false> pt = global_parse(tb);
+// The whole stack stk[0, d) as a read-only base for simulations: in LDS it
+// is the window, in global memory the pool.
+template <bool L>
+__device__ inline BaseStack<L> whole_stack(mptr<L, uint16_t> stk, uint32_t d) {
+  if constexpr (L) return BaseStack<L>{nullptr, stk, d, 0u};
+  else return BaseStack<L>{stk, nullptr, d, d};
+}
+
+struct AccLex {  // a row's lexer side: DFA state, lexicon node, pending lexeme
+  uint32_t q, lex, rem;
+  uint8_t head[8];
+};
+
+// One row's advance by token tok (section 6.1, per-token step 7) on the stack
+// stk[0, d) of capacity cap, with the LR tables pt.  The token's bytes go
+// through the lexer with maximal munch; a byte that kills the DFA emits the
+// pending lexeme as the highest-priority candidate that is ignored or shifts
+// and passes its category's lexicon, and a shifted terminal runs its reduce
+// chain on the stack.  The new pending lexeme must still complete to an
+// allowed or ignored terminal (Definition 2).  The end-of-sequence token is
+// accepted when the end-of-sequence gate holds (section 3.2).  Returns the
+// row status; with GRID_ROW_OK, d and lx are the new configuration's.
+template <bool L, int MW>
+__device__ int advance_row(const Tables& tb, const ParseTabs<L>& pt, const Slot& sl, mptr<L, uint16_t> stk,
+                           uint32_t& d, uint32_t cap, int tok, AccLex& lx) {
   auto ignored = [&](int t) { return (tb.term_info[t] & 1u) != 0; };
   auto restricted_cat = [&](int t) -> int {  // category the row's lexicon restricts, or -1
     const uint32_t c = (tb.term_info[t] >> 8) & 0xFFu;
@@ -2502,19 +2492,15 @@ __global__ __launch_bounds__(64) void accept_kernel(Tables tb, const grid_config
   // 1 shift, 2 accept (the end of input), 0 error, -1 capacity
   auto shifts = [&](int t) -> int {
     if (d >= cap) return -1;
-    const BaseStack<false> bs{stk, nullptr, d, d};
-    return sim1_test<false, MW>(pt, bs, d, 0, stk + d, stk + d, (int)(cap - d), t);
+    return sim1_test<L, MW>(pt, whole_stack<L>(stk, d), d, 0, stk + d, stk + d, (int)(cap - d), t);
   };
-  uint32_t q = cfg.q, lex = cfg.lexnode, rem = (cfg.flags & 1u) ? 0u : cfg.rem_len;
-  uint8_t head[8];
-  for (int k = 0; k < 8; ++k) head[k] = rem > 0 ? cfg.rem_head[k] : 0;
   // the pending lexeme's winner in state q (lexicon node lex): -1 none, else
   // the terminal; capacity problems surface as -2
   auto winner = [&]() -> int {
-    for (uint32_t j = tb.acc_off[q]; j < tb.acc_off[q + 1]; ++j) {
+    for (uint32_t j = tb.acc_off[lx.q]; j < tb.acc_off[lx.q + 1]; ++j) {
       const int t = tb.acc_list[j];
       const int c = restricted_cat(t);
-      if (c >= 0 && !((lex_flags_of(tb, sl, lex) >> (8 + c)) & 1u)) continue;
+      if (c >= 0 && !((lex_flags_of(tb, sl, lx.lex) >> (8 + c)) & 1u)) continue;
       if (ignored(t)) return t;
       const int r = shifts(t);
       if (r < 0) return -2;
@@ -2522,95 +2508,146 @@ __global__ __launch_bounds__(64) void accept_kernel(Tables tb, const grid_config
     }
     return -1;
   };
-  if (tok == tb.eos_id) {  // the end-of-sequence gate (section 3.2)
+  if (tok == tb.eos_id) {  // the configuration itself stays as it is
     int ok = 0;
-    if (rem == 0) {
+    if (lx.rem == 0) {
       ok = shifts(tb.T) == 2;
     } else {
       const int w = winner();
-      if (w == -2) st = GRID_ROW_OVERFLOW;
-      else if (w >= 0 && ignored(w)) ok = shifts(tb.T) == 2;
-      else if (w >= 0 && stack_commit<MW>(pt, stk, d, cap, w) == 1) ok = shifts(tb.T) == 2;
+      if (w == -2) return GRID_ROW_OVERFLOW;
+      if (w >= 0 && ignored(w)) ok = shifts(tb.T) == 2;
+      else if (w >= 0 && stack_commit<L, MW>(pt, stk, d, cap, w) == 1) ok = shifts(tb.T) == 2;
     }
-    if (st == GRID_ROW_OK) st = ok ? GRID_ROW_FINISHED : GRID_ROW_NOT_VIABLE;
-    return done();  // the configuration itself is unchanged
+    return ok ? GRID_ROW_FINISHED : GRID_ROW_NOT_VIABLE;
   }
   const uint32_t su = tb.spell_of_id[tok];
-  if (su == 0xFFFFFFFFu) {  // special or empty token
-    st = GRID_ROW_NOT_VIABLE;
-    return done();
-  }
+  if (su == 0xFFFFFFFFu) return GRID_ROW_NOT_VIABLE;  // special or empty token
   const uint32_t b0 = tb.spell_off[su], n = tb.spell_off[su + 1] - b0;
-  for (uint32_t i = 0; i < n && st == GRID_ROW_OK; ++i) {
+  for (uint32_t i = 0; i < n; ++i) {
     const uint32_t b = tb.spell_bytes[b0 + i];
-    const int nq = tb.dfa[q * tb.C + tb.bclass[b]];
+    const int nq = tb.dfa[lx.q * tb.C + tb.bclass[b]];
     if (nq != kDead) {
-      q = (uint32_t)nq;
-      lex = lex_child(tb, sl, lex, b);
-      if (rem < 8) head[rem] = (uint8_t)b;
-      ++rem;
+      lx.q = (uint32_t)nq;
+      lx.lex = lex_child(tb, sl, lx.lex, b);
+      if (lx.rem < 8) lx.head[lx.rem] = (uint8_t)b;
+      ++lx.rem;
       continue;
     }
     // b kills the pending lexeme: emit it
-    if (rem == 0 || tb.acc_off[q + 1] == tb.acc_off[q]) {
-      st = GRID_ROW_NOT_VIABLE;
-      break;
-    }
+    if (lx.rem == 0 || tb.acc_off[lx.q + 1] == tb.acc_off[lx.q]) return GRID_ROW_NOT_VIABLE;
     const int w = winner();
-    if (w == -2) {
-      st = GRID_ROW_OVERFLOW;
-      break;
-    }
-    if (w < 0) {
-      st = GRID_ROW_NOT_VIABLE;
-      break;
-    }
+    if (w == -2) return GRID_ROW_OVERFLOW;
+    if (w < 0) return GRID_ROW_NOT_VIABLE;
     if (!ignored(w)) {
-      const int r = stack_commit<MW>(pt, stk, d, cap, w);
-      if (r != 1) {
-        st = r < 0 ? GRID_ROW_OVERFLOW : GRID_ROW_NOT_VIABLE;
-        break;
-      }
+      const int r = stack_commit<L, MW>(pt, stk, d, cap, w);
+      if (r != 1) return r < 0 ? GRID_ROW_OVERFLOW : GRID_ROW_NOT_VIABLE;
     }
     const int q1 = tb.dfa[kStart * tb.C + tb.bclass[b]];
-    if (q1 == kDead) {
-      st = GRID_ROW_NOT_VIABLE;
-      break;
-    }
-    q = (uint32_t)q1;
-    lex = lex_child(tb, sl, 0u, b);
-    rem = 1;
-    head[0] = (uint8_t)b;
-    for (int k = 1; k < 8; ++k) head[k] = 0;
+    if (q1 == kDead) return GRID_ROW_NOT_VIABLE;
+    lx.q = (uint32_t)q1;
+    lx.lex = lex_child(tb, sl, 0u, b);
+    lx.rem = 1;
+    lx.head[0] = (uint8_t)b;
+    for (int k = 1; k < 8; ++k) lx.head[k] = 0;
   }
-  if (st == GRID_ROW_OK && rem > 0) {  // Definition 2 for the pending lexeme
-    bool ok = false;
-    const uint32_t* lv = tb.live + (size_t)q * 8;
-    for (int t = 0; t < tb.T && !ok; ++t) {
-      if (!((lv[t >> 5] >> (t & 31)) & 1u)) continue;
-      const int c = restricted_cat(t);
-      if (c >= 0 && !((lex_flags_of(tb, sl, lex) >> c) & 1u)) continue;
-      if (ignored(t)) {
-        ok = true;
-      } else {
-        const int r = shifts(t);
-        if (r < 0) st = GRID_ROW_OVERFLOW;
-        ok = r == 1;
-        if (r < 0) break;
-      }
-    }
-    if (!ok && st == GRID_ROW_OK) st = GRID_ROW_NOT_VIABLE;
+  if (lx.rem == 0) return GRID_ROW_OK;
+  // Definition 2 for the pending lexeme
+  const uint32_t* lv = tb.live + (size_t)lx.q * 8;
+  for (int t = 0; t < tb.T; ++t) {
+    if (!((lv[t >> 5] >> (t & 31)) & 1u)) continue;
+    const int c = restricted_cat(t);
+    if (c >= 0 && !((lex_flags_of(tb, sl, lx.lex) >> c) & 1u)) continue;
+    if (ignored(t)) return GRID_ROW_OK;
+    const int r = shifts(t);
+    if (r < 0) return GRID_ROW_OVERFLOW;
+    if (r == 1) return GRID_ROW_OK;
   }
+  return GRID_ROW_NOT_VIABLE;
+}
+
+constexpr uint32_t kAccStack = 8192;  // stack entries an accept workgroup keeps in LDS
+
+__host__ __device__ inline uint32_t accept_stack_cap(uint32_t cap) { return cap < kAccStack ? cap : kAccStack; }
+
+// Device incremental advance: one workgroup per row.  The LR tables and the
+// row's stack are staged in LDS and one thread advances the row there (the
+// chain of dependent table reads is the cost, so every read is an LDS read);
+// the stack goes back to pool_out + b * cap.  A stack that outgrows the LDS
+// area while cap allows more is advanced again from the start, by the same
+// routine, on a global copy with the tables in global memory.
+template <int MW>
+__global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_config* __restrict__ cfgs,
+                                                        const uint16_t* __restrict__ pool,
+                                                        const int32_t* __restrict__ tokens, grid_config* cfg_out,
+                                                        uint16_t* pool_out, uint32_t cap, int32_t* status) {
+  extern __shared__ __align__(16) uint8_t alds[];
+  __shared__ int s_st;
+  __shared__ uint32_t s_d;
+  const int row = (int)blockIdx.x, tid = (int)threadIdx.x;
+  const grid_config cfg = cfgs[row];
+  const int tok = tokens[row];
+  if (cfg.q >= (uint32_t)tb.S || cfg.q == (uint32_t)kDead || cfg.slot >= (uint32_t)tb.n_slots ||
+      cfg.stk_depth < 1 || cfg.stk_depth > cap || tok < 0 || tok >= tb.V) {  // uniform
+    if (tid == 0) {
+      cfg_out[row] = cfg;
+      if (status) status[row] = GRID_ROW_BAD_CONFIG;
+    }
+    return;
+  }
+  const ParseLds PL = prologue_parse_lds(tb);
+  const uint32_t lcap = accept_stack_cap(cap), d0 = cfg.stk_depth;
+  const mptr<true, uint16_t> stk_l = in_mem<true>((uint16_t*)(alds + PL.total));
+  {
+    const StageRegion rg[4] = {parse_region(tb, alds, PL, 0), parse_region(tb, alds, PL, 1),
+                               parse_region(tb, alds, PL, 2), parse_region(tb, alds, PL, 3)};
+    stage_regions<4, 8>(rg, tid, kBlock);
+  }
+  const bool fits = d0 < lcap;  // uniform
+  if (fits)
+    for (uint32_t i = (uint32_t)tid; i < d0; i += kBlock) stk_l[i] = pool[cfg.stk_off + i];
+  __syncthreads();
+  AccLex lx;
+  lx.q = cfg.q;
+  lx.lex = cfg.lexnode;
+  lx.rem = (cfg.flags & 1u) ? 0u : cfg.rem_len;
+  for (int k = 0; k < 8; ++k) lx.head[k] = lx.rem > 0 ? cfg.rem_head[k] : 0;
+  const Slot sl = load_slot(tb, (int)cfg.slot);
+  int st = -1;  // -1: not advanced in LDS
+  uint32_t d = d0;
+  if (tid == 0) {
+    if (fits) {
+      st = advance_row<true, MW>(tb, lds_parse(tb, alds, PL), sl, stk_l, d, lcap, tok, lx);
+      if (st == GRID_ROW_OVERFLOW && lcap < cap) st = -1;
+    }
+    s_st = st;
+    s_d = d;
+  }
+  __syncthreads();
+  uint16_t* out_stk = pool_out + (size_t)row * cap;
+  if (s_st == GRID_ROW_OK) {
+    for (uint32_t i = (uint32_t)tid; i < s_d; i += kBlock) out_stk[i] = stk_l[i];
+  } else if (s_st == -1 && tid == 0) {  // the global route, from the start
+    lx.q = cfg.q;
+    lx.lex = cfg.lexnode;
+    lx.rem = (cfg.flags & 1u) ? 0u : cfg.rem_len;
+    for (int k = 0; k < 8; ++k) lx.head[k] = lx.rem > 0 ? cfg.rem_head[k] : 0;
+    d = d0;
+    for (uint32_t i = 0; i < d0; ++i) out_stk[i] = pool[cfg.stk_off + i];
+    st = advance_row<false, MW>(tb, global_parse(tb), sl, out_stk, d, cap, tok, lx);
+  }
+  if (tid != 0) return;
+  grid_config out = cfg;
   if (st == GRID_ROW_OK) {
     out.stk_off = (uint32_t)row * cap;
     out.stk_depth = d;
-    out.lexnode = lex;
-    out.q = (uint16_t)q;
-    out.flags = rem == 0 ? 1u : 0u;
-    out.rem_len = rem;
-    for (int k = 0; k < 8; ++k) out.rem_head[k] = head[k];
+    out.lexnode = lx.lex;
+    out.q = (uint16_t)lx.q;
+    out.flags = lx.rem == 0 ? 1u : 0u;
+    out.rem_len = lx.rem;
+    for (int k = 0; k < 8; ++k) out.rem_head[k] = lx.head[k];
   }
-  done();
+  cfg_out[row] = out;
+  if (status) status[row] = st;
 }
 
 bool bound(const grid_compiled* g, int which) { return g->dev[which] != nullptr || g->dev_bytes[which] == 0; }
@@ -2869,17 +2906,23 @@ extern "C" int grid_accept(const grid_compiled* g, int32_t B, const grid_config*
   const int rc = bind_tables(g, tb);
   if (rc != GRID_OK) return rc;
   if (tb.T > 255) return fail(GRID_E_CAPACITY, "grid_accept: more than 255 terminals");
+  const ParseLds PL = prologue_parse_lds(tb);
+  if (PL.total > kPrologueParseMax) return fail(GRID_E_CAPACITY, "grid_accept: LR tables too large for the LDS staging");
+  const uint32_t lds = PL.total + pad16(accept_stack_cap(stack_cap) * 2u);
+  const void* fn = tb.tw == 2 ? (const void*)accept_kernel<2>
+                              : (tb.tw == 4 ? (const void*)accept_kernel<4> : (const void*)accept_kernel<8>);
+  if (!raise_lds(fn, lds)) return fail(GRID_E_HIP, "grid_accept: cannot raise the LDS limit");
   hipStream_t s = (hipStream_t)stream;
-  const dim3 grid((unsigned)((B + 63) / 64));
+  const dim3 grid((unsigned)B), block(kBlock);
   if (tb.tw == 2)
-    hipLaunchKernelGGL(accept_kernel<2>, grid, dim3(64), 0, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev, B);
+    hipLaunchKernelGGL(accept_kernel<2>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
+                       stack_out_dev, stack_cap, status_dev);
   else if (tb.tw == 4)
-    hipLaunchKernelGGL(accept_kernel<4>, grid, dim3(64), 0, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev, B);
+    hipLaunchKernelGGL(accept_kernel<4>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
+                       stack_out_dev, stack_cap, status_dev);
   else
-    hipLaunchKernelGGL(accept_kernel<8>, grid, dim3(64), 0, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev, B);
+    hipLaunchKernelGGL(accept_kernel<8>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
+                       stack_out_dev, stack_cap, status_dev);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_accept launch: ") + hipGetErrorString(e));
   return GRID_OK;

@@ -34,7 +34,7 @@ def G():
     return pkg
 
 
-def _host_check(G, grid, prefixes, slots, cfg_out, pool_out, rows):
+def _host_check(G, grid, prefixes, slots, cfg_out, pool_out, rows, cap=CAP):
     cfgs = cfg_out.cpu().numpy().view(G.CONFIG_DTYPE)
     pool = pool_out.cpu().numpy().view(np.uint16)
     for r in rows:
@@ -44,7 +44,7 @@ def _host_check(G, grid, prefixes, slots, cfg_out, pool_out, rows):
             assert int(got[f]) == int(want[f]), (r, f, prefixes[r][-40:], int(got[f]), int(want[f]))
         assert bytes(got["rem_head"]) == bytes(want["rem_head"]), (r, prefixes[r][-40:])
         off, d = int(got["stk_off"]), int(got["stk_depth"])
-        assert off == r * CAP and d == len(stack), (r, d, len(stack))
+        assert off == r * cap and d == len(stack), (r, d, len(stack))
         assert np.array_equal(pool[off:off + d], stack), (r, prefixes[r][-40:])
 
 
@@ -136,3 +136,30 @@ def test_accept_edge_cases(G):
     torch.cuda.synchronize()
     assert st.cpu().numpy()[0] == G.ROW_BAD_CONFIG
     assert st2.cpu().numpy()[2] in (G.ROW_OVERFLOW, G.ROW_BAD_CONFIG)
+
+
+def test_accept_deep_stacks_leave_the_lds_area(G):
+    """Stacks deeper than the kernel keeps in LDS (8192 entries) with a larger
+    capacity: a row that starts above that depth, one that crosses it during
+    the decode loop and a shallow one, advanced by "((" three times, equal the
+    host advance at every step."""
+    wl = make_workload(3, rows=1)
+    grid, slot_map = G.from_workload(wl)
+    grid.to_device("cuda")
+    vocab = {t: i for i, t in enumerate(wl.vocab)}
+    cap = 16384
+    prefixes = [b"select " + b"(" * 8186, b"select " + b"(" * 9000, b"select ("]
+    slots = [slot_map[0]] * len(prefixes)
+    cfgs, pool = grid.configs(prefixes, slots)
+    c, p = grid.configs_to_device(cfgs, pool)
+    tok = vocab[b"(("]
+    t = torch.full((len(prefixes),), tok, dtype=torch.int32, device="cuda")
+    for step in range(3):
+        c2, p2, st = grid.accept(c, p, t, len(prefixes), cap)
+        torch.cuda.synchronize()
+        assert (st.cpu().numpy() == G.ROW_OK).all(), (step, st.cpu().numpy().tolist())
+        prefixes = [x + b"((" for x in prefixes]
+        _host_check(G, grid, prefixes, slots, c2, p2, range(len(prefixes)), cap)
+        depths = c2.cpu().numpy().view(G.CONFIG_DTYPE)["stk_depth"].tolist()
+        log(f"deep stacks step {step}: depths {depths} equal to the host advance")
+        c, p = c2, p2.view(torch.int16)
