@@ -2430,39 +2430,54 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(const uint32_t* __restric
 }
 
 // ------------------------------------------------------------------ accept
-// Reduce chain of terminal x on the stack stk[0, d), then its shift: the
-// array itself changes.  Called only for a terminal whose test succeeded.
-// 1 shifted, 2 accept (x is the end of input), 0 error, -1 capacity.
-template <bool L, int MW>
-__device__ int stack_commit(const ParseTabs<L>& pt, mptr<L, uint16_t> stk, uint32_t& d, uint32_t cap, int x) {
-  const uint32_t w = (uint32_t)x >> 5, bit = 1u << (x & 31);
-  for (int guard = 0; guard < kGuard; ++guard) {
-    const uint32_t s = stk[d - 1];
-    const uint32_t a = action_of<L, MW>(pt, s, w, bit);
-    if (a == kActShiftP) {
-      if (x == pt.T) return 2;
-      if (d >= cap) return -1;
-      stk[d++] = shift_target<L, MW>(pt, s, x);
-      return 1;
-    }
-    if (a == kNoProd) return 0;
-    const uint32_t len = a >> 16;
-    if (len >= d) return 0;
-    d -= len;
-    const uint16_t g = goto_of<L>(pt, stk[d - 1], a & 0xFFFFu);
-    if (g == kNoGoto) return 0;
-    if (d >= cap) return -1;
-    stk[d++] = g;
-  }
-  return -1;
-}
-
 // The whole stack stk[0, d) as a read-only base for simulations: in LDS it
 // is the window, in global memory the pool.
 template <bool L>
 __device__ inline BaseStack<L> whole_stack(mptr<L, uint16_t> stk, uint32_t d) {
   if constexpr (L) return BaseStack<L>{nullptr, stk, d, 0u};
   else return BaseStack<L>{stk, nullptr, d, d};
+}
+
+// Reduce chain of terminal x on the stack stk[0, d), pushes above d (the
+// stack below stays as it is).  1 shift, 2 accept (x is the end of input), 0
+// error, -1 capacity.  With commit, a shift makes the chain's result the
+// stack: the pushed states move down onto the popped entries, then x's
+// shift target goes on top (so a winner costs one chain, not two).
+template <bool L, int MW>
+__device__ int chain_shift(const ParseTabs<L>& pt, mptr<L, uint16_t> stk, uint32_t& d, uint32_t cap, int x,
+                           bool commit) {
+  if (d >= cap) return -1;
+  const BaseStack<L> bs = whole_stack<L>(stk, d);
+  const mptr<L, uint16_t> tmp = stk + d;
+  const int tmpcap = (int)(cap - d);
+  const uint32_t w = (uint32_t)x >> 5, bit = 1u << (x & 31);
+  uint32_t k = d;
+  int m = 0, t = 0;
+  uint32_t s = stack_at_top<L>(bs, k, m, tmp, 0, tmp), below = kNoState;
+  for (int guard = 0; guard < kGuard; ++guard) {
+    const uint32_t a = action_of<L, MW>(pt, s, w, bit);
+    if (a >= kActShiftP) {
+      if (a != kActShiftP) return 0;
+      if (x == pt.T) return 2;
+      if (commit) {
+        for (int i = 0; i < t; ++i) stk[k + (uint32_t)i] = tmp[i];  // k <= d: a forward move is safe
+        d = k + (uint32_t)t;
+        if (d >= cap) return -1;
+        stk[d++] = shift_target<L, MW>(pt, s, x);
+      }
+      return 1;
+    }
+    const uint32_t len = a >> 16;
+    if (!pop_len(len, k, m, t)) return 0;
+    const uint32_t sb = goto_source<L>(bs, len, s, below, k, m, tmp, t, tmp);
+    const uint16_t g = goto_of<L>(pt, sb, a & 0xFFFFu);
+    if (g == kNoGoto) return 0;
+    if (t >= tmpcap) return -1;
+    tmp[t++] = g;
+    below = sb;
+    s = g;
+  }
+  return -1;
 }
 
 struct AccLex {  // a row's lexer side: DFA state, lexicon node, pending lexeme
@@ -2490,19 +2505,17 @@ __device__ int advance_row(const Tables& tb, const ParseTabs<L>& pt, const Slot&
   // can terminal t be shifted from the stack now (reduce chain only, pushes
   // above the stack, which stays as it is)?
   // 1 shift, 2 accept (the end of input), 0 error, -1 capacity
-  auto shifts = [&](int t) -> int {
-    if (d >= cap) return -1;
-    return sim1_test<L, MW>(pt, whole_stack<L>(stk, d), d, 0, stk + d, stk + d, (int)(cap - d), t);
-  };
-  // the pending lexeme's winner in state q (lexicon node lex): -1 none, else
-  // the terminal; capacity problems surface as -2
+  auto shifts = [&](int t) -> int { return chain_shift<L, MW>(pt, stk, d, cap, t, false); };
+  // the pending lexeme's winner in state q (lexicon node lex), its reduce
+  // chain and shift applied to the stack when it is not ignored: -1 none,
+  // else the terminal; capacity problems surface as -2
   auto winner = [&]() -> int {
     for (uint32_t j = tb.acc_off[lx.q]; j < tb.acc_off[lx.q + 1]; ++j) {
       const int t = tb.acc_list[j];
       const int c = restricted_cat(t);
       if (c >= 0 && !((lex_flags_of(tb, sl, lx.lex) >> (8 + c)) & 1u)) continue;
       if (ignored(t)) return t;
-      const int r = shifts(t);
+      const int r = chain_shift<L, MW>(pt, stk, d, cap, t, true);
       if (r < 0) return -2;
       if (r == 1) return t;
     }
@@ -2515,8 +2528,7 @@ __device__ int advance_row(const Tables& tb, const ParseTabs<L>& pt, const Slot&
     } else {
       const int w = winner();
       if (w == -2) return GRID_ROW_OVERFLOW;
-      if (w >= 0 && ignored(w)) ok = shifts(tb.T) == 2;
-      else if (w >= 0 && stack_commit<L, MW>(pt, stk, d, cap, w) == 1) ok = shifts(tb.T) == 2;
+      if (w >= 0) ok = shifts(tb.T) == 2;
     }
     return ok ? GRID_ROW_FINISHED : GRID_ROW_NOT_VIABLE;
   }
@@ -2538,10 +2550,6 @@ __device__ int advance_row(const Tables& tb, const ParseTabs<L>& pt, const Slot&
     const int w = winner();
     if (w == -2) return GRID_ROW_OVERFLOW;
     if (w < 0) return GRID_ROW_NOT_VIABLE;
-    if (!ignored(w)) {
-      const int r = stack_commit<L, MW>(pt, stk, d, cap, w);
-      if (r != 1) return r < 0 ? GRID_ROW_OVERFLOW : GRID_ROW_NOT_VIABLE;
-    }
     const int q1 = tb.dfa[kStart * tb.C + tb.bclass[b]];
     if (q1 == kDead) return GRID_ROW_NOT_VIABLE;
     lx.q = (uint32_t)q1;
@@ -2574,12 +2582,14 @@ __host__ __device__ inline uint32_t accept_stack_cap(uint32_t cap) { return cap 
 // chain of dependent table reads is the cost, so every read is an LDS read);
 // the stack goes back to pool_out + b * cap.  A stack that outgrows the LDS
 // area while cap allows more is advanced again from the start, by the same
-// routine, on a global copy with the tables in global memory.
+// routine, on a global copy with the tables in global memory; so is every
+// row when the LR tables are too large to stage (use_lds = 0).
 template <int MW>
 __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_config* __restrict__ cfgs,
                                                         const uint16_t* __restrict__ pool,
                                                         const int32_t* __restrict__ tokens, grid_config* cfg_out,
-                                                        uint16_t* pool_out, uint32_t cap, int32_t* status) {
+                                                        uint16_t* pool_out, uint32_t cap, int32_t* status,
+                                                        int use_lds) {
   extern __shared__ __align__(16) uint8_t alds[];
   __shared__ int s_st;
   __shared__ uint32_t s_d;
@@ -2597,12 +2607,12 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
   const ParseLds PL = prologue_parse_lds(tb);
   const uint32_t lcap = accept_stack_cap(cap), d0 = cfg.stk_depth;
   const mptr<true, uint16_t> stk_l = in_mem<true>((uint16_t*)(alds + PL.total));
-  {
+  if (use_lds) {
     const StageRegion rg[4] = {parse_region(tb, alds, PL, 0), parse_region(tb, alds, PL, 1),
                                parse_region(tb, alds, PL, 2), parse_region(tb, alds, PL, 3)};
     stage_regions<4, 8>(rg, tid, kBlock);
   }
-  const bool fits = d0 < lcap;  // uniform
+  const bool fits = use_lds && d0 < lcap;  // uniform
   if (fits)
     for (uint32_t i = (uint32_t)tid; i < d0; i += kBlock) stk_l[i] = pool[cfg.stk_off + i];
   __syncthreads();
@@ -2907,8 +2917,8 @@ extern "C" int grid_accept(const grid_compiled* g, int32_t B, const grid_config*
   if (rc != GRID_OK) return rc;
   if (tb.T > 255) return fail(GRID_E_CAPACITY, "grid_accept: more than 255 terminals");
   const ParseLds PL = prologue_parse_lds(tb);
-  if (PL.total > kPrologueParseMax) return fail(GRID_E_CAPACITY, "grid_accept: LR tables too large for the LDS staging");
-  const uint32_t lds = PL.total + pad16(accept_stack_cap(stack_cap) * 2u);
+  const int use_lds = PL.total <= kPrologueParseMax ? 1 : 0;
+  const uint32_t lds = use_lds ? PL.total + pad16(accept_stack_cap(stack_cap) * 2u) : 0u;
   const void* fn = tb.tw == 2 ? (const void*)accept_kernel<2>
                               : (tb.tw == 4 ? (const void*)accept_kernel<4> : (const void*)accept_kernel<8>);
   if (!raise_lds(fn, lds)) return fail(GRID_E_HIP, "grid_accept: cannot raise the LDS limit");
@@ -2916,13 +2926,13 @@ extern "C" int grid_accept(const grid_compiled* g, int32_t B, const grid_config*
   const dim3 grid((unsigned)B), block(kBlock);
   if (tb.tw == 2)
     hipLaunchKernelGGL(accept_kernel<2>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev);
+                       stack_out_dev, stack_cap, status_dev, use_lds);
   else if (tb.tw == 4)
     hipLaunchKernelGGL(accept_kernel<4>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev);
+                       stack_out_dev, stack_cap, status_dev, use_lds);
   else
     hipLaunchKernelGGL(accept_kernel<8>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev);
+                       stack_out_dev, stack_cap, status_dev, use_lds);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_accept launch: ") + hipGetErrorString(e));
   return GRID_OK;
