@@ -2480,6 +2480,16 @@ __device__ int chain_shift(const ParseTabs<L>& pt, mptr<L, uint16_t> stk, uint32
   return -1;
 }
 
+// The lexer tables an advance reads (global memory, or their LDS copies).
+struct LexPtrs {
+  const uint16_t* dfa;
+  const uint8_t* bclass;
+  const uint32_t* term_info;
+  const uint32_t* acc_off;
+  const uint8_t* acc_list;
+  const uint32_t* live;
+};
+
 struct AccLex {  // a row's lexer side: DFA state, lexicon node, pending lexeme
   uint32_t q, lex, rem;
   uint8_t head[8];
@@ -2495,11 +2505,11 @@ struct AccLex {  // a row's lexer side: DFA state, lexicon node, pending lexeme
 // accepted when the end-of-sequence gate holds (section 3.2).  Returns the
 // row status; with GRID_ROW_OK, d and lx are the new configuration's.
 template <bool L, int MW>
-__device__ int advance_row(const Tables& tb, const ParseTabs<L>& pt, const Slot& sl, mptr<L, uint16_t> stk,
-                           uint32_t& d, uint32_t cap, int tok, AccLex& lx) {
-  auto ignored = [&](int t) { return (tb.term_info[t] & 1u) != 0; };
+__device__ __forceinline__ int advance_row(const Tables& tb, const LexPtrs lp, const ParseTabs<L>& pt, const Slot& sl,
+                           mptr<L, uint16_t> stk, uint32_t& d, uint32_t cap, int tok, AccLex& lx) {
+  auto ignored = [&](int t) { return (lp.term_info[t] & 1u) != 0; };
   auto restricted_cat = [&](int t) -> int {  // category the row's lexicon restricts, or -1
-    const uint32_t c = (tb.term_info[t] >> 8) & 0xFFu;
+    const uint32_t c = (lp.term_info[t] >> 8) & 0xFFu;
     return c != 0xFFu && ((sl.restricted >> c) & 1u) ? (int)c : -1;
   };
   // can terminal t be shifted from the stack now (reduce chain only, pushes
@@ -2510,8 +2520,8 @@ __device__ int advance_row(const Tables& tb, const ParseTabs<L>& pt, const Slot&
   // chain and shift applied to the stack when it is not ignored: -1 none,
   // else the terminal; capacity problems surface as -2
   auto winner = [&]() -> int {
-    for (uint32_t j = tb.acc_off[lx.q]; j < tb.acc_off[lx.q + 1]; ++j) {
-      const int t = tb.acc_list[j];
+    for (uint32_t j = lp.acc_off[lx.q]; j < lp.acc_off[lx.q + 1]; ++j) {
+      const int t = lp.acc_list[j];
       const int c = restricted_cat(t);
       if (c >= 0 && !((lex_flags_of(tb, sl, lx.lex) >> (8 + c)) & 1u)) continue;
       if (ignored(t)) return t;
@@ -2537,7 +2547,7 @@ __device__ int advance_row(const Tables& tb, const ParseTabs<L>& pt, const Slot&
   const uint32_t b0 = tb.spell_off[su], n = tb.spell_off[su + 1] - b0;
   for (uint32_t i = 0; i < n; ++i) {
     const uint32_t b = tb.spell_bytes[b0 + i];
-    const int nq = tb.dfa[lx.q * tb.C + tb.bclass[b]];
+    const int nq = lp.dfa[lx.q * tb.C + lp.bclass[b]];
     if (nq != kDead) {
       lx.q = (uint32_t)nq;
       lx.lex = lex_child(tb, sl, lx.lex, b);
@@ -2546,11 +2556,11 @@ __device__ int advance_row(const Tables& tb, const ParseTabs<L>& pt, const Slot&
       continue;
     }
     // b kills the pending lexeme: emit it
-    if (lx.rem == 0 || tb.acc_off[lx.q + 1] == tb.acc_off[lx.q]) return GRID_ROW_NOT_VIABLE;
+    if (lx.rem == 0 || lp.acc_off[lx.q + 1] == lp.acc_off[lx.q]) return GRID_ROW_NOT_VIABLE;
     const int w = winner();
     if (w == -2) return GRID_ROW_OVERFLOW;
     if (w < 0) return GRID_ROW_NOT_VIABLE;
-    const int q1 = tb.dfa[kStart * tb.C + tb.bclass[b]];
+    const int q1 = lp.dfa[kStart * tb.C + lp.bclass[b]];
     if (q1 == kDead) return GRID_ROW_NOT_VIABLE;
     lx.q = (uint32_t)q1;
     lx.lex = lex_child(tb, sl, 0u, b);
@@ -2560,18 +2570,47 @@ __device__ int advance_row(const Tables& tb, const ParseTabs<L>& pt, const Slot&
   }
   if (lx.rem == 0) return GRID_ROW_OK;
   // Definition 2 for the pending lexeme
-  const uint32_t* lv = tb.live + (size_t)lx.q * 8;
-  for (int t = 0; t < tb.T; ++t) {
-    if (!((lv[t >> 5] >> (t & 31)) & 1u)) continue;
-    const int c = restricted_cat(t);
-    if (c >= 0 && !((lex_flags_of(tb, sl, lx.lex) >> c) & 1u)) continue;
-    if (ignored(t)) return GRID_ROW_OK;
-    const int r = shifts(t);
-    if (r < 0) return GRID_ROW_OVERFLOW;
-    if (r == 1) return GRID_ROW_OK;
+  const uint32_t* lv = lp.live + (size_t)lx.q * 8;
+  for (int wd = 0; wd < 8; ++wd) {
+    for (uint32_t bits = lv[wd]; bits != 0u; bits &= bits - 1u) {  // live terminals in id order
+      const int t = wd * 32 + __builtin_ctz(bits);
+      if (t >= tb.T) break;
+      const int c = restricted_cat(t);
+      if (c >= 0 && !((lex_flags_of(tb, sl, lx.lex) >> c) & 1u)) continue;
+      if (ignored(t)) return GRID_ROW_OK;
+      const int r = shifts(t);
+      if (r < 0) return GRID_ROW_OVERFLOW;
+      if (r == 1) return GRID_ROW_OK;
+    }
   }
   return GRID_ROW_NOT_VIABLE;
 }
+
+// LDS bytes of the lexer tables an accept workgroup stages beside the LR
+// tables and the stack: DFA, byte classes, terminal info, accept lists, live
+// sets (offsets from the start of the area).
+struct AccLexLds {
+  uint32_t dfa, bclass, tinfo, acc_off, acc_list, live, total;
+};
+__host__ __device__ inline AccLexLds accept_lex_lds(const Tables& tb) {
+  AccLexLds L;
+  uint32_t o = 0;
+  L.dfa = o;
+  o += pad16((uint32_t)(tb.S * tb.C * 2));
+  L.bclass = o;
+  o += 256;
+  L.tinfo = o;
+  o += pad16((uint32_t)tb.T * 4u);
+  L.acc_off = o;
+  o += pad16((uint32_t)(tb.S + 1) * 4u);
+  L.acc_list = o;
+  o += pad16((uint32_t)tb.n_acc);
+  L.live = o;
+  o += pad16((uint32_t)tb.S * 32u);
+  L.total = o;
+  return L;
+}
+constexpr uint32_t kAcceptLdsMax = 152 * 1024;
 
 constexpr uint32_t kAccStack = 8192;  // stack entries an accept workgroup keeps in LDS
 
@@ -2589,7 +2628,7 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
                                                         const uint16_t* __restrict__ pool,
                                                         const int32_t* __restrict__ tokens, grid_config* cfg_out,
                                                         uint16_t* pool_out, uint32_t cap, int32_t* status,
-                                                        int use_lds) {
+                                                        int use_lds, int use_lex) {
   extern __shared__ __align__(16) uint8_t alds[];
   __shared__ int s_st;
   __shared__ uint32_t s_d;
@@ -2612,6 +2651,21 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
                                parse_region(tb, alds, PL, 2), parse_region(tb, alds, PL, 3)};
     stage_regions<4, 8>(rg, tid, kBlock);
   }
+  // the lexer tables too when they fit: every byte step is then an LDS read
+  const AccLexLds XL = accept_lex_lds(tb);
+  uint8_t* xl = alds + PL.total + pad16(lcap * 2u);
+  LexPtrs lp{tb.dfa, tb.bclass, tb.term_info, tb.acc_off, tb.acc_list, tb.live};
+  if (use_lds && use_lex) {
+    const StageRegion rg[6] = {{(const uint8_t*)tb.dfa, xl + XL.dfa, (uint32_t)(tb.S * tb.C * 2)},
+                               {tb.bclass, xl + XL.bclass, 256u},
+                               {(const uint8_t*)tb.term_info, xl + XL.tinfo, (uint32_t)tb.T * 4u},
+                               {(const uint8_t*)tb.acc_off, xl + XL.acc_off, (uint32_t)(tb.S + 1) * 4u},
+                               {tb.acc_list, xl + XL.acc_list, (uint32_t)tb.n_acc},
+                               {(const uint8_t*)tb.live, xl + XL.live, (uint32_t)tb.S * 32u}};
+    stage_regions<6, 4>(rg, tid, kBlock);
+    lp = LexPtrs{(const uint16_t*)(xl + XL.dfa), xl + XL.bclass, (const uint32_t*)(xl + XL.tinfo),
+                 (const uint32_t*)(xl + XL.acc_off), xl + XL.acc_list, (const uint32_t*)(xl + XL.live)};
+  }
   const bool fits = use_lds && d0 < lcap;  // uniform
   if (fits)
     for (uint32_t i = (uint32_t)tid; i < d0; i += kBlock) stk_l[i] = pool[cfg.stk_off + i];
@@ -2626,7 +2680,7 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
   uint32_t d = d0;
   if (tid == 0) {
     if (fits) {
-      st = advance_row<true, MW>(tb, lds_parse(tb, alds, PL), sl, stk_l, d, lcap, tok, lx);
+      st = advance_row<true, MW>(tb, lp, lds_parse(tb, alds, PL), sl, stk_l, d, lcap, tok, lx);
       if (st == GRID_ROW_OVERFLOW && lcap < cap) st = -1;
     }
     s_st = st;
@@ -2643,7 +2697,8 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
     for (int k = 0; k < 8; ++k) lx.head[k] = lx.rem > 0 ? cfg.rem_head[k] : 0;
     d = d0;
     for (uint32_t i = 0; i < d0; ++i) out_stk[i] = pool[cfg.stk_off + i];
-    st = advance_row<false, MW>(tb, global_parse(tb), sl, out_stk, d, cap, tok, lx);
+    const LexPtrs lg{tb.dfa, tb.bclass, tb.term_info, tb.acc_off, tb.acc_list, tb.live};
+    st = advance_row<false, MW>(tb, lg, global_parse(tb), sl, out_stk, d, cap, tok, lx);
   }
   if (tid != 0) return;
   grid_config out = cfg;
@@ -2918,7 +2973,9 @@ extern "C" int grid_accept(const grid_compiled* g, int32_t B, const grid_config*
   if (tb.T > 255) return fail(GRID_E_CAPACITY, "grid_accept: more than 255 terminals");
   const ParseLds PL = prologue_parse_lds(tb);
   const int use_lds = PL.total <= kPrologueParseMax ? 1 : 0;
-  const uint32_t lds = use_lds ? PL.total + pad16(accept_stack_cap(stack_cap) * 2u) : 0u;
+  uint32_t lds = use_lds ? PL.total + pad16(accept_stack_cap(stack_cap) * 2u) : 0u;
+  const int use_lex = use_lds && lds + accept_lex_lds(tb).total <= kAcceptLdsMax ? 1 : 0;
+  if (use_lex) lds += accept_lex_lds(tb).total;
   const void* fn = tb.tw == 2 ? (const void*)accept_kernel<2>
                               : (tb.tw == 4 ? (const void*)accept_kernel<4> : (const void*)accept_kernel<8>);
   if (!raise_lds(fn, lds)) return fail(GRID_E_HIP, "grid_accept: cannot raise the LDS limit");
@@ -2926,13 +2983,13 @@ extern "C" int grid_accept(const grid_compiled* g, int32_t B, const grid_config*
   const dim3 grid((unsigned)B), block(kBlock);
   if (tb.tw == 2)
     hipLaunchKernelGGL(accept_kernel<2>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev, use_lds);
+                       stack_out_dev, stack_cap, status_dev, use_lds, use_lex);
   else if (tb.tw == 4)
     hipLaunchKernelGGL(accept_kernel<4>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev, use_lds);
+                       stack_out_dev, stack_cap, status_dev, use_lds, use_lex);
   else
     hipLaunchKernelGGL(accept_kernel<8>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev, use_lds);
+                       stack_out_dev, stack_cap, status_dev, use_lds, use_lex);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_accept launch: ") + hipGetErrorString(e));
   return GRID_OK;
