@@ -1722,7 +1722,6 @@ __host__ __device__ inline int stream_groups(int V) { return (stream_slices(V) +
 
 __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __restrict__ mask,
                                                         uint8_t* __restrict__ ws, size_t rbytes, int B) {
-  extern __shared__ __align__(16) uint32_t vc_s[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int x = (int)(blockIdx.x & 7u);
   const int g = (int)(blockIdx.x >> 3);
@@ -1742,13 +1741,11 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
     return;
   }
   const RowLayout RL = row_layout(tb);
-  const uint32_t q = hdr->q, n_cls = hdr->n_cls;
+  const uint32_t q = hdr->q;
   const int eos = hdr->eos_ok ? tb.eos_id : -1;
-  {
-    const uint32_t* vg = (const uint32_t*)(rw + RL.vcode);
-    const uint32_t nw = (n_cls + 15u) / 16u;
-    for (uint32_t i = tid; i < nw; i += kBlock) vc_s[i] = vg[i];
-  }
+  // the row's 2-bit class codes are read where the class map points (an
+  // L2-resident gather: staging all of them in LDS per workgroup cost more)
+  const uint32_t* vg = (const uint32_t*)(rw + RL.vcode);
   const uint16_t* cm = tb.cmap + (size_t)q * tb.V;
   const uint32_t* tflags = tb.lex_token + (size_t)hdr->slot_id * tb.V;
   const uint8_t* vrule = rw + RL.vrule;
@@ -1766,7 +1763,6 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
     const int id = c * 64 + lane;
     cls[j] = (c < c_hi && id < tb.V) ? (uint32_t)cm[id] : 0u;
   }
-  __syncthreads();
   // pass 2: codes; for a class the lexicon decides, its shortcut byte and the
   // token's first byte and token flags (again all loads in flight together)
   uint32_t code[kPer], sc[kPer], fb[kPer], tf[kPer];
@@ -1774,7 +1770,7 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
   for (int j = 0; j < kPer; ++j) {
     const int c = c_lo + wave + j * kStreamWaves;
     const int id = c * 64 + lane;
-    code[j] = c < c_hi ? (vc_s[cls[j] >> 4] >> ((cls[j] & 15u) * 2u)) & 3u : kVerdictReject;
+    code[j] = c < c_hi ? (vg[cls[j] >> 4] >> ((cls[j] & 15u) * 2u)) & 3u : kVerdictReject;
     const bool lexq = code[j] == kVerdictLexicon && id < tb.V;
     sc[j] = lexq ? vrule[cls[j]] : 0u;
     fb[j] = lexq ? tb.id_first[id] : 0u;
@@ -2767,11 +2763,9 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
     hipLaunchKernelGGL(verdict_kernel<MW>, dim3(B, vy), dim3(kBlock), verdict_lds(tb).total, s, tb, ws, rb);
   }
   if (phases & GRID_PHASE_WALK) {
-    const uint32_t lds = pad16(((uint32_t)tb.max_classes + 15u) / 16u * 4u);
-    if (!raise_lds((const void*)stream_kernel, lds)) return fail(GRID_E_HIP, "grid_mask: cannot raise the LDS limit");
     const long long blocks = 8ll * B * stream_groups(tb.V);
     if (blocks > 0x7FFFFFFFll) return fail(GRID_E_CAPACITY, "grid_mask: batch x vocabulary too large");
-    hipLaunchKernelGGL(stream_kernel, dim3((uint32_t)blocks), dim3(kBlock), lds, s, tb, mask, ws, rb, B);
+    hipLaunchKernelGGL(stream_kernel, dim3((uint32_t)blocks), dim3(kBlock), 0, s, tb, mask, ws, rb, B);
   }
   if ((phases & GRID_PHASE_RESIDUE) && tb.U > 0) {
     const ResLds RL = res_lds(tb, MW, B);
