@@ -325,14 +325,17 @@ int grid_mask_cached(const grid_compiled* g, int32_t B, const grid_config* cfg_d
  * the mask (maximal munch, contextual resolution by priority, lexicon word and
  * prefix tests, Definition 2 for the new pending lexeme); the new
  * configuration goes to cfg_out_dev[b], its stack to
- * stack_out_dev[b * stack_cap ..] (cfg_out_dev[b].stk_off = b * stack_cap), so
- * cfg_out_dev and stack_out_dev are the next step's inputs.  status_dev[b]
- * (nullable): GRID_ROW_OK, GRID_ROW_NOT_VIABLE (token not allowed),
- * GRID_ROW_FINISHED (the end-of-sequence token, accepted: the sentence is in
- * L), GRID_ROW_BAD_CONFIG or GRID_ROW_OVERFLOW (stack_cap too small); in all
- * but GRID_ROW_OK the row's configuration is copied unchanged.  Device
- * buffers are caller-owned and must not overlap; stack_cap >= 2.
- * Asynchronous on stream. */
+ * stack_out_dev[b * stack_cap ..] (cfg_out_dev[b].stk_off = b * stack_cap).
+ * status_dev[b] (nullable): GRID_ROW_OK, GRID_ROW_NOT_VIABLE (token not
+ * allowed), GRID_ROW_FINISHED (the end-of-sequence token, accepted: the
+ * sentence is in L), GRID_ROW_BAD_CONFIG (state, slot, lexicon node, stack
+ * entry or token out of range) or GRID_ROW_OVERFLOW (stack_cap too small for
+ * the advanced stack).  Whatever the status, cfg_out_dev and stack_out_dev are
+ * the next step's inputs: a row that is not GRID_ROW_OK keeps its
+ * configuration, with its input stack copied to its own output area; a row
+ * whose input stack does not fit stack_cap gets stk_depth 0 (a configuration
+ * every call reports as GRID_ROW_BAD_CONFIG).  Device buffers are
+ * caller-owned and must not overlap; stack_cap >= 2.  Asynchronous on stream. */
 int grid_accept(const grid_compiled* g, int32_t B, const grid_config* cfg_dev, const uint16_t* stack_pool_dev,
                 const int32_t* token_dev, grid_config* cfg_out_dev, uint16_t* stack_out_dev, uint32_t stack_cap,
                 int32_t* status_dev, void* stream);

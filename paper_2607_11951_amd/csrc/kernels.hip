@@ -2441,7 +2441,7 @@ __device__ inline BaseStack<L> whole_stack(mptr<L, uint16_t> stk, uint32_t d) {
 // shift target goes on top (so a winner costs one chain, not two).
 template <bool L, int MW>
 __device__ int chain_shift(const ParseTabs<L>& pt, mptr<L, uint16_t> stk, uint32_t& d, uint32_t cap, int x,
-                           bool commit) {
+                           bool commit, uint32_t& lo_mod) {
   if (d >= cap) return -1;
   const BaseStack<L> bs = whole_stack<L>(stk, d);
   const mptr<L, uint16_t> tmp = stk + d;
@@ -2457,6 +2457,7 @@ __device__ int chain_shift(const ParseTabs<L>& pt, mptr<L, uint16_t> stk, uint32
       if (x == pt.T) return 2;
       if (commit) {
         for (int i = 0; i < t; ++i) stk[k + (uint32_t)i] = tmp[i];  // k <= d: a forward move is safe
+        lo_mod = min(lo_mod, k);
         d = k + (uint32_t)t;
         if (d >= cap) return -1;
         stk[d++] = shift_target<L, MW>(pt, s, x);
@@ -2492,7 +2493,8 @@ struct AccLex {  // a row's lexer side: DFA state, lexicon node, pending lexeme
 };
 
 // One row's advance by token tok (section 6.1, per-token step 7) on the stack
-// stk[0, d) of capacity cap, with the LR tables pt.  The token's bytes go
+// stk[0, d) of capacity cap, with the LR tables pt; lo_mod falls to the
+// lowest stack index the advance rewrites (entries below it are unchanged).  The token's bytes go
 // through the lexer with maximal munch; a byte that kills the DFA emits the
 // pending lexeme as the highest-priority candidate that is ignored or shifts
 // and passes its category's lexicon, and a shifted terminal runs its reduce
@@ -2502,7 +2504,8 @@ struct AccLex {  // a row's lexer side: DFA state, lexicon node, pending lexeme
 // row status; with GRID_ROW_OK, d and lx are the new configuration's.
 template <bool L, int MW>
 __device__ __forceinline__ int advance_row(const Tables& tb, const LexPtrs lp, const ParseTabs<L>& pt, const Slot& sl,
-                           mptr<L, uint16_t> stk, uint32_t& d, uint32_t cap, int tok, AccLex& lx) {
+                           mptr<L, uint16_t> stk, uint32_t& d, uint32_t cap, int tok, AccLex& lx,
+                           uint32_t& lo_mod) {
   auto ignored = [&](int t) { return (lp.term_info[t] & 1u) != 0; };
   auto restricted_cat = [&](int t) -> int {  // category the row's lexicon restricts, or -1
     const uint32_t c = (lp.term_info[t] >> 8) & 0xFFu;
@@ -2511,7 +2514,7 @@ __device__ __forceinline__ int advance_row(const Tables& tb, const LexPtrs lp, c
   // can terminal t be shifted from the stack now (reduce chain only, pushes
   // above the stack, which stays as it is)?
   // 1 shift, 2 accept (the end of input), 0 error, -1 capacity
-  auto shifts = [&](int t) -> int { return chain_shift<L, MW>(pt, stk, d, cap, t, false); };
+  auto shifts = [&](int t) -> int { return chain_shift<L, MW>(pt, stk, d, cap, t, false, lo_mod); };
   // the pending lexeme's winner in state q (lexicon node lex), its reduce
   // chain and shift applied to the stack when it is not ignored: -1 none,
   // else the terminal; capacity problems surface as -2
@@ -2521,7 +2524,7 @@ __device__ __forceinline__ int advance_row(const Tables& tb, const LexPtrs lp, c
       const int c = restricted_cat(t);
       if (c >= 0 && !((lex_flags_of(tb, sl, lx.lex) >> (8 + c)) & 1u)) continue;
       if (ignored(t)) return t;
-      const int r = chain_shift<L, MW>(pt, stk, d, cap, t, true);
+      const int r = chain_shift<L, MW>(pt, stk, d, cap, t, true, lo_mod);
       if (r < 0) return -2;
       if (r == 1) return t;
     }
@@ -2614,11 +2617,16 @@ __host__ __device__ inline uint32_t accept_stack_cap(uint32_t cap) { return cap 
 
 // Device incremental advance: one workgroup per row.  The LR tables and the
 // row's stack are staged in LDS and one thread advances the row there (the
-// chain of dependent table reads is the cost, so every read is an LDS read);
-// the stack goes back to pool_out + b * cap.  A stack that outgrows the LDS
-// area while cap allows more is advanced again from the start, by the same
-// routine, on a global copy with the tables in global memory; so is every
-// row when the LR tables are too large to stage (use_lds = 0).
+// chain of dependent table reads is the cost, so every read is an LDS read).
+// Every row's output is self-contained, whatever its status: the input stack
+// is copied to the row's own area pool_out + b * cap (checking every entry is
+// an LR state) and the configuration written to cfg_out points there; an
+// advance then rewrites only the entries from the lowest one it changed.  A
+// stack that outgrows the LDS area while cap allows more is advanced again
+// from the start, by the same routine, on that global copy with the tables in
+// global memory; so is every row when the LR tables are too large to stage
+// (use_lds = 0).  A row whose stack does not fit cap gets depth 0 (a
+// configuration every call rejects).
 template <int MW>
 __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_config* __restrict__ cfgs,
                                                         const uint16_t* __restrict__ pool,
@@ -2626,23 +2634,26 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
                                                         uint16_t* pool_out, uint32_t cap, int32_t* status,
                                                         int use_lds, int use_lex) {
   extern __shared__ __align__(16) uint8_t alds[];
-  __shared__ int s_st;
-  __shared__ uint32_t s_d;
+  __shared__ int s_st, s_bad;
+  __shared__ uint32_t s_d, s_lo;
   const int row = (int)blockIdx.x, tid = (int)threadIdx.x;
   const grid_config cfg = cfgs[row];
   const int tok = tokens[row];
-  if (cfg.q >= (uint32_t)tb.S || cfg.q == (uint32_t)kDead || cfg.slot >= (uint32_t)tb.n_slots ||
-      cfg.stk_depth < 1 || cfg.stk_depth > cap || tok < 0 || tok >= tb.V) {  // uniform
-    if (tid == 0) {
-      cfg_out[row] = cfg;
-      if (status) status[row] = GRID_ROW_BAD_CONFIG;
-    }
-    return;
+  const uint32_t d0 = cfg.stk_depth;
+  uint16_t* out_stk = pool_out + (size_t)row * cap;
+  const bool copyable = d0 >= 1 && d0 <= cap;  // uniform
+  bool bad = !copyable || cfg.q >= (uint32_t)tb.S || cfg.q == (uint32_t)kDead || cfg.slot >= (uint32_t)tb.n_slots ||
+             tok < 0 || tok >= tb.V;
+  Slot sl{};
+  if (!bad) {
+    sl = load_slot(tb, (int)cfg.slot);
+    bad = cfg.lexnode != kNoLex && cfg.lexnode >= sl.nodes;
   }
+  if (tid == 0) s_bad = 0;
   const ParseLds PL = prologue_parse_lds(tb);
-  const uint32_t lcap = accept_stack_cap(cap), d0 = cfg.stk_depth;
+  const uint32_t lcap = accept_stack_cap(cap);
   const mptr<true, uint16_t> stk_l = in_mem<true>((uint16_t*)(alds + PL.total));
-  if (use_lds) {
+  if (use_lds && !bad) {
     const StageRegion rg[4] = {parse_region(tb, alds, PL, 0), parse_region(tb, alds, PL, 1),
                                parse_region(tb, alds, PL, 2), parse_region(tb, alds, PL, 3)};
     stage_regions<4, 8>(rg, tid, kBlock);
@@ -2651,7 +2662,7 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
   const AccLexLds XL = accept_lex_lds(tb);
   uint8_t* xl = alds + PL.total + pad16(lcap * 2u);
   LexPtrs lp{tb.dfa, tb.bclass, tb.term_info, tb.acc_off, tb.acc_list, tb.live};
-  if (use_lds && use_lex) {
+  if (use_lds && use_lex && !bad) {
     const StageRegion rg[6] = {{(const uint8_t*)tb.dfa, xl + XL.dfa, (uint32_t)(tb.S * tb.C * 2)},
                                {tb.bclass, xl + XL.bclass, 256u},
                                {(const uint8_t*)tb.term_info, xl + XL.tinfo, (uint32_t)tb.T * 4u},
@@ -2662,44 +2673,61 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
     lp = LexPtrs{(const uint16_t*)(xl + XL.dfa), xl + XL.bclass, (const uint32_t*)(xl + XL.tinfo),
                  (const uint32_t*)(xl + XL.acc_off), xl + XL.acc_list, (const uint32_t*)(xl + XL.live)};
   }
-  const bool fits = use_lds && d0 < lcap;  // uniform
-  if (fits)
-    for (uint32_t i = (uint32_t)tid; i < d0; i += kBlock) stk_l[i] = pool[cfg.stk_off + i];
+  const bool fits = use_lds && !bad && d0 < lcap;  // uniform
+  __syncthreads();  // s_bad is cleared
+  if (copyable) {  // the input stack to the row's output area (and to LDS), entries checked
+    for (uint32_t i = (uint32_t)tid; i < d0; i += kBlock) {
+      const uint16_t v = pool[cfg.stk_off + i];
+      if (v >= (uint32_t)tb.NS) s_bad = 1;
+      out_stk[i] = v;
+      if (fits) stk_l[i] = v;
+    }
+  }
   __syncthreads();
+  bad = bad || s_bad != 0;  // uniform
+  grid_config out = cfg;
+  if (copyable) out.stk_off = (uint32_t)row * cap;
+  else out.stk_depth = 0;
+  if (bad) {
+    if (tid == 0) {
+      cfg_out[row] = out;
+      if (status) status[row] = GRID_ROW_BAD_CONFIG;
+    }
+    return;
+  }
   AccLex lx;
   lx.q = cfg.q;
   lx.lex = cfg.lexnode;
   lx.rem = (cfg.flags & 1u) ? 0u : cfg.rem_len;
   for (int k = 0; k < 8; ++k) lx.head[k] = lx.rem > 0 ? cfg.rem_head[k] : 0;
-  const Slot sl = load_slot(tb, (int)cfg.slot);
   int st = -1;  // -1: not advanced in LDS
-  uint32_t d = d0;
+  uint32_t d = d0, lo = d0;
   if (tid == 0) {
     if (fits) {
-      st = advance_row<true, MW>(tb, lp, lds_parse(tb, alds, PL), sl, stk_l, d, lcap, tok, lx);
+      st = advance_row<true, MW>(tb, lp, lds_parse(tb, alds, PL), sl, stk_l, d, lcap, tok, lx, lo);
       if (st == GRID_ROW_OVERFLOW && lcap < cap) st = -1;
     }
     s_st = st;
     s_d = d;
+    s_lo = lo;
   }
   __syncthreads();
-  uint16_t* out_stk = pool_out + (size_t)row * cap;
-  if (s_st == GRID_ROW_OK) {
-    for (uint32_t i = (uint32_t)tid; i < s_d; i += kBlock) out_stk[i] = stk_l[i];
-  } else if (s_st == -1 && tid == 0) {  // the global route, from the start
+  if (s_st == GRID_ROW_OK) {  // the entries the advance rewrote
+    for (uint32_t i = s_lo + (uint32_t)tid; i < s_d; i += kBlock) out_stk[i] = stk_l[i];
+  } else if (s_st == -1 && tid == 0) {  // the global route, from the start, on the output copy
     lx.q = cfg.q;
     lx.lex = cfg.lexnode;
     lx.rem = (cfg.flags & 1u) ? 0u : cfg.rem_len;
     for (int k = 0; k < 8; ++k) lx.head[k] = lx.rem > 0 ? cfg.rem_head[k] : 0;
     d = d0;
-    for (uint32_t i = 0; i < d0; ++i) out_stk[i] = pool[cfg.stk_off + i];
+    lo = d0;
     const LexPtrs lg{tb.dfa, tb.bclass, tb.term_info, tb.acc_off, tb.acc_list, tb.live};
-    st = advance_row<false, MW>(tb, lg, global_parse(tb), sl, out_stk, d, cap, tok, lx);
+    st = advance_row<false, MW>(tb, lg, global_parse(tb), sl, out_stk, d, cap, tok, lx, lo);
+    if (st != GRID_ROW_OK)  // a refused token leaves the row's input stack in its area
+      for (uint32_t i = lo; i < d0; ++i) out_stk[i] = pool[cfg.stk_off + i];
   }
   if (tid != 0) return;
-  grid_config out = cfg;
   if (st == GRID_ROW_OK) {
-    out.stk_off = (uint32_t)row * cap;
     out.stk_depth = d;
     out.lexnode = lx.lex;
     out.q = (uint16_t)lx.q;

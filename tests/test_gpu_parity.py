@@ -106,8 +106,9 @@ def test_select_subset_batch(G, oracle_mod):
 
 
 def test_dml_full_size_batch(G, oracle_mod):
-    """The benchmark's workload and launch shape: B = 32, V = 151,936."""
-    wl = make_workload(3, n_batches=2)
+    """The benchmark's workload and launch shape: B = 32, V = 151,936, all
+    eight config batches the benchmark cycles through (256 rows)."""
+    wl = make_workload(3, n_batches=8)
     rows = list(range(len(wl.prefixes)))
     log(f"workload 3: {len(rows)} rows, V={wl.V}, batch {wl.batch}")
     t = time.time()
@@ -118,18 +119,62 @@ def test_dml_full_size_batch(G, oracle_mod):
 
 
 def test_long_sentences_positions_and_depths(G, oracle_mod):
-    """16,000-token sentences: configurations at 1k / 4k / 16k tokens, nesting
-    depth 1 / 8 / 32 / 128 (stack up to several hundred states)."""
-    wl = make_workload(4, rows=8)
+    """16,000-token sentences at the shape the flatness measurement times:
+    configurations at 1k / 4k / 16k tokens, nesting depth 1 / 8 / 32 / 128,
+    all 32 configurations of every (position, depth) cell as one B = 32 call
+    (384 rows; stacks up to several hundred states)."""
+    t = time.time()
+    wl = make_workload(4)
     rows = list(range(len(wl.prefixes)))
-    log(f"workload 4: {len(rows)} rows (8 per cell), V={wl.V}")
+    assert wl.batch == 32 and len(rows) == 384
+    log(f"workload 4: {len(rows)} rows (32 per cell, B = 32), V={wl.V}, built in {time.time() - t:.1f}s")
     grid, gm, ge, gs = _gpu_masks(G, wl, rows)
+    log(f"  GPU done at {time.time() - t:.1f}s")
     om, oe = _oracle_rows(oracle_mod, wl, rows)
+    log(f"  oracle done at {time.time() - t:.1f}s")
     _compare(wl, rows, gm, ge, gs, om, oe, "long")
     sm = _gpu_masks.slot_map
-    cfgs, _ = grid.configs([wl.prefixes[j] for j in rows[-8:]], [sm[wl.slots[j]] for j in rows[-8:]])
+    cfgs, _ = grid.configs([wl.prefixes[j] for j in rows[-32:]], [sm[wl.slots[j]] for j in rows[-32:]])
     log(f"  stack depths at depth-128 cells: {sorted(cfgs['stk_depth'].tolist())}")
-    assert cfgs["stk_depth"].max() > 300
+    assert cfgs["stk_depth"].max() > 500
+
+
+def test_worked_example_section_7_1_on_gpu(G, oracle_mod):
+    """The paper's first worked example (section 7.1, the golden fixture)
+    through the HIP path: the CRUD grammar under the analyst projection, the
+    fixture's schema lexicon, and a vocabulary of the 256 single bytes, the
+    fixture's spellings and an end-of-sequence id.  Every printed verdict must
+    hold on the GPU mask, and the whole mask must equal the oracle's."""
+    import json
+    from pathlib import Path
+    from workloads import grammar_text
+    fx = json.loads((Path(__file__).resolve().parent / "golden" / "worked_example_1.json").read_text())
+    spells = sorted({s for c in fx["cases"] for k in ("allowed", "blocked") for s in c.get(k, [])})
+    vocab = [bytes([b]) for b in range(256)] + [s.encode() for s in spells if len(s.encode()) > 1] + [b""]
+    eos = len(vocab) - 1
+    g = G.Grid(grammar_text(fx["grammar"]), fx["drop"], vocab, [eos], eos)
+    slot = g.add_lexicon(fx["lexicon"])
+    g.to_device("cuda")
+    prefixes = [c["prefix"].encode() for c in fx["cases"]]
+    cfgs, pool = g.configs(prefixes, [slot] * len(prefixes))
+    cd, pd = g.configs_to_device(cfgs, pool)
+    m, e, s = g.mask(cd, pd, len(prefixes))
+    torch.cuda.synchronize()
+    o = oracle_mod.Oracle(grammar_text(fx["grammar"]), fx["drop"], fx["lexicon"], vocab, [eos], eos)
+    got = m.cpu().numpy().view(np.uint32)
+    ids = {sp: i for i, sp in enumerate(vocab)}
+    for i, c in enumerate(fx["cases"]):
+        bit = lambda sp: (int(got[i][ids[sp] >> 5]) >> (ids[sp] & 31)) & 1  # noqa: E731
+        for sp in c.get("allowed", []):
+            assert bit(sp.encode()) == 1, (c["prefix"], sp)
+        for sp in c.get("blocked", []):
+            assert bit(sp.encode()) == 0, (c["prefix"], sp)
+        if "eos" in c:
+            assert int(e[i]) == int(c["eos"]), c["prefix"]
+        want, want_eos = o.mask(prefixes[i], mode=0)
+        assert np.array_equal(got[i], want), c["prefix"]
+        assert int(e[i]) == want_eos
+    assert (s.cpu().numpy() == 0).all()
 
 
 def test_cold_schema_batch_and_bf16_apply(G, oracle_mod):

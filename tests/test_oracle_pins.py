@@ -191,6 +191,39 @@ def test_modes_agree_and_invariants_expr(oracle_mod):
         assert any(bits[:256])
 
 
+@pytest.mark.parametrize("k,n_rows,n_rand", [(2, 8, 1500), (3, 16, 1500), (4, 12, 300)])
+def test_modes_agree_on_sql_workloads(oracle_mod, k, n_rows, n_rand):
+    """From-scratch mode (every token re-lexes and re-parses the whole
+    extended prefix, the plain reading of Definition 4) equals checkpoint mode
+    (the prefix parsed once) on the SQL grammars the GPU parity tests use:
+    seeded rows of workloads 2 and 3, and one row of every (position, depth)
+    cell of the 16,000-token workload (the longest and most deeply nested
+    prefixes), each on a seeded token subset of random ids plus ids the
+    checkpoint mask allows, so both verdicts are exercised."""
+    wl = make_workload(k)
+    o = oracle_mod.from_workload(wl)
+    rng = np.random.default_rng(6100 + k)
+    if k == 4:
+        rows = [c * wl.batch + int(rng.integers(wl.batch)) for c in range(len(wl.prefixes) // wl.batch)]
+    else:
+        rows = sorted(rng.choice(len(wl.prefixes), n_rows, replace=False).tolist())
+    n_allowed = 0
+    for j in rows:
+        w = wl.prefixes[j]
+        full, e1 = o.mask(w, mode=1)
+        bits = np.unpackbits(full.view(np.uint8), bitorder="little")[:wl.V]
+        allowed = np.flatnonzero(bits)
+        pick = rng.choice(allowed, min(len(allowed), n_rand), replace=False) if len(allowed) else allowed
+        toks = np.unique(np.concatenate([rng.choice(wl.V, n_rand, replace=False), pick])).astype(np.int32)
+        b0, e0 = o.mask(w, mode=0, tokens=toks)
+        b1, e1b = o.mask(w, mode=1, tokens=toks)
+        assert np.array_equal(b0, b1), (k, j, toks[np.flatnonzero(b0 != b1)][:8].tolist())
+        assert np.array_equal(b1, bits[toks]), (k, j)
+        assert e0 == e1 == e1b, (k, j)
+        n_allowed += int(b0.sum())
+    assert n_allowed > 0
+
+
 def test_generated_sentences_are_members(oracle_mod):
     import random
     from workloads import sentences as sen

@@ -96,8 +96,15 @@ def _vocab4():
     return voc.geometric_vocab(4000, kws, idw, 128256)
 
 
-def _greedy_tokenize(vocab, text_bytes, max_tokens):
-    """Greedy longest-match tokenization; returns byte offsets of token ends."""
+_TRIES = {}
+
+
+def _vocab_trie(vocab):
+    """Byte trie of a vocabulary's spellings (built once per vocabulary list)."""
+    key = id(vocab)
+    hit = _TRIES.get(key)
+    if hit is not None and hit[0] is vocab:
+        return hit[1]
     root = {}
     for tid, sp in enumerate(vocab):
         if not sp:
@@ -106,6 +113,13 @@ def _greedy_tokenize(vocab, text_bytes, max_tokens):
         for b in sp:
             node = node.setdefault(b, {})
         node[-1] = tid
+    _TRIES[key] = (vocab, root)
+    return root
+
+
+def _greedy_tokenize(vocab, text_bytes, max_tokens):
+    """Greedy longest-match tokenization; returns byte offsets of token ends."""
+    root = _vocab_trie(vocab)
     ends = []
     i = 0
     n = len(text_bytes)
@@ -124,6 +138,32 @@ def _greedy_tokenize(vocab, text_bytes, max_tokens):
         ends.append(best)
         i = best
     return ends
+
+
+@functools.lru_cache(maxsize=None)
+def _long_rows(per_cell):
+    """Prefixes and (position, depth, tokens) cells of the 16,000-token workload."""
+    s = _schema3()
+    vocab, _, _ = _vocab4()
+    positions = [1000, 4000, 16000]
+    depths = [1, 8, 32, 128]
+    prefixes, cells = [], []
+    for d in depths:
+        r = random.Random(4001 + d)
+        g = sen.DmlQueryGen(r, s)
+        for j in range(per_cell):
+            text = g.long_sentence(d, 100_000).encode("utf-8")
+            ends = _greedy_tokenize(vocab, text, max(positions) + 8)
+            chain_end = len(text) - 2 * d - 8
+            for p in positions:
+                n_tok = p - (j % 4)
+                cut = ends[n_tok - 1]
+                assert cut < chain_end, "sentence too short for the position"
+                prefixes.append(text[:cut])
+                cells.append((p, d, n_tok))
+    # order rows so each batch of per_cell rows is one (position, depth) cell
+    order = sorted(range(len(prefixes)), key=lambda i: (cells[i][1], cells[i][0]))
+    return tuple(prefixes[i] for i in order), tuple(cells[i] for i in order)
 
 
 def make_workload(k, n_batches=1, rows=None):
@@ -162,30 +202,11 @@ def make_workload(k, n_batches=1, rows=None):
     if k == 4:
         s = _schema3()
         vocab, specials, eos = _vocab4()
-        positions = [1000, 4000, 16000]
-        depths = [1, 8, 32, 128]
         per_cell = 32 if rows is None else rows
-        prefixes, cells = [], []
-        for d in depths:
-            r = random.Random(4001 + d)
-            g = sen.DmlQueryGen(r, s)
-            for j in range(per_cell):
-                text = g.long_sentence(d, 100_000).encode("utf-8")
-                ends = _greedy_tokenize(vocab, text, max(positions) + 8)
-                chain_end = len(text) - 2 * d - 8
-                for p in positions:
-                    n_tok = p - (j % 4)
-                    cut = ends[n_tok - 1]
-                    assert cut < chain_end, "sentence too short for the position"
-                    prefixes.append(text[:cut])
-                    cells.append((p, d, n_tok))
-        # order rows so each batch of per_cell rows is one (position, depth) cell
-        order = sorted(range(len(prefixes)), key=lambda i: (cells[i][1], cells[i][0]))
-        prefixes = [prefixes[i] for i in order]
-        cells = [cells[i] for i in order]
+        prefixes, cells = _long_rows(per_cell)
         return Workload("sql_dml_long", "sql_dml", list(READ_ONLY_ROLE), vocab, specials, eos,
-                        [s.lexicon(with_alias=True)], prefixes, [0] * len(prefixes), per_cell,
-                        meta={"cells": cells, "schema": s})
+                        [s.lexicon(with_alias=True)], list(prefixes), [0] * len(prefixes), per_cell,
+                        meta={"cells": list(cells), "schema": s})
     if k == 5:
         vocab, specials, eos = _vocab3()
         banned = sch.keyword_spellings(GRAMMAR_DIR / "sql_dml.grid")
