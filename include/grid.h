@@ -288,6 +288,22 @@ int grid_mask_phases(const grid_compiled* g, int32_t B, const grid_config* cfg_d
                      int32_t* status_dev, void* workspace_dev, size_t workspace_bytes,
                      uint32_t phases, void* stream);
 
+/* For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): grid_mask without a
+ * caller workspace.  Its workspace is a static device array of the library,
+ * grid_mask_noalloc_max_bytes() bytes (32 MiB) on every GPU the library runs
+ * on, held until the process ends; its device address is looked up once per
+ * device.  The call allocates nothing; B rows need
+ * grid_mask_workspace_bytes(g, B) of it, and a larger batch fails with
+ * GRID_E_CAPACITY before anything is enqueued.  Every call on one GPU uses
+ * the same array, and nothing is expected in it from an earlier call: calls
+ * whose work overlaps on one GPU (other streams, other host threads) race
+ * and must be ordered by the caller.  Outputs and errors as grid_mask. */
+size_t grid_mask_noalloc_max_bytes(void);
+int grid_mask_noalloc(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                      const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
+                      int32_t* status_dev, void* stream);
+
 /* --------------------------------------------------------------- mask cache */
 /* A configuration-keyed mask cache (section 4.3, configuration-keyed
  * caching; the per-token hot path's cache probe and write-back, section 6.1)

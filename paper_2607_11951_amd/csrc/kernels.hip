@@ -896,7 +896,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   const int tid = threadIdx.x;
   __shared__ uint16_t win[kStackWin];
   __shared__ uint32_t A[8], I[8], R[8], Aw[8];
-  __shared__ uint16_t scratch[kBlock][kPostCap + kTmpCap];
+  __shared__ uint16_t sim_area[kBlock][kPostCap + kTmpCap];
   __shared__ int bad, overflow, winner, eos_ok, eos_sigma, cache_hit;
   __shared__ uint8_t eos_after[256];  // end-of-sequence test after shifting each candidate winner
   __shared__ Post posts[256];          // stack after shifting each allowed terminal
@@ -1056,7 +1056,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     if (c != 0xFFu && ((sl.restricted >> c) & 1u)) atomicOr(&R[tid >> 5], 1u << (tid & 31));
   }
   const BaseStack<true> bs{pool + cfg.stk_off, in_mem<true>((const uint16_t*)win), depth, lo};
-  const mptr<true, uint16_t> my = in_mem<true>(&scratch[tid][0]);
+  const mptr<true, uint16_t> my = in_mem<true>(&sim_area[tid][0]);
   const TermView tv{tb.term_info, I, R, tb.live, 8};
   __syncthreads();
 
@@ -2961,6 +2961,60 @@ extern "C" int grid_mask_cached(const grid_compiled* g, int32_t B, const grid_co
                                 size_t cache_bytes, uint32_t cache_flags, void* stream) {
   return mask_call(g, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, workspace_dev, workspace_bytes,
                    cache_dev, cache_bytes, cache_flags, GRID_PHASE_ALL, stream);
+}
+
+// ------------------------------------------------------ no-alloc mask entry
+// The workspace of grid_mask_noalloc: a device array of the code object, one
+// copy per GPU, held until the process ends.  Host code never passes the
+// array's name to a kernel (on the host it is only a stand-in for the
+// symbol); it uses the device address hipGetSymbolAddress returns, looked up
+// once per device with that device current.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array, or nullptr (the
+// error is recorded).
+void* scratch_on_current_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    fail(GRID_E_HIP, "grid_mask_noalloc: no current device");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      fail(GRID_E_HIP, std::string("grid_mask_noalloc: hipGetSymbolAddress: ") + hipGetErrorString(e));
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+}  // namespace
+
+extern "C" size_t grid_mask_noalloc_max_bytes(void) { return kScratchBytes; }
+
+extern "C" int grid_mask_noalloc(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                                 const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
+                                 int32_t* status_dev, void* stream) {
+  clear_error();
+  if (!g || B <= 0 || B > 65535) return fail(GRID_E_ARG, "grid_mask_noalloc: null handle or batch size out of range");
+  const size_t need = workspace_size(g, B);
+  if (need > kScratchBytes)
+    return fail(GRID_E_CAPACITY, "grid_mask_noalloc: " + std::to_string(B) + " rows need " + std::to_string(need) +
+                                     " workspace bytes, more than the " + std::to_string(kScratchBytes) +
+                                     " of the static scratch array");
+  void* ws = scratch_on_current_device();
+  if (!ws) return GRID_E_HIP;
+  return mask_call(g, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, ws, kScratchBytes, nullptr, 0, 0,
+                   GRID_PHASE_ALL, stream);
 }
 
 extern "C" size_t grid_cache_bytes(const grid_compiled* g, int32_t n_entries) {

@@ -41,7 +41,8 @@ assert CONFIG_DTYPE.itemsize == 32
 EXPORTS = ["grid_compile", "grid_free", "grid_last_error", "grid_info", "grid_add_lexicon",
            "grid_artifact", "grid_bind_device", "grid_config_from_prefix",
            "grid_mask_workspace_bytes", "grid_mask", "grid_mask_phases", "grid_apply",
-           "grid_cache_bytes", "grid_cache_clear", "grid_mask_cached", "grid_accept"]
+           "grid_cache_bytes", "grid_cache_clear", "grid_mask_cached", "grid_accept",
+           "grid_mask_noalloc_max_bytes", "grid_mask_noalloc"]
 PHASE_PROLOGUE, PHASE_WALK, PHASE_RESIDUE, PHASE_FINALIZE, PHASE_ALL = 1, 2, 4, 8, 15
 
 
@@ -102,6 +103,9 @@ def lib():
         L.grid_cache_bytes.argtypes = [vp, i32]
         L.grid_cache_bytes.restype = sz
         L.grid_cache_clear.argtypes = [vp, vp, sz, vp]
+        L.grid_mask_noalloc_max_bytes.argtypes = []
+        L.grid_mask_noalloc_max_bytes.restype = sz
+        L.grid_mask_noalloc.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -292,6 +296,18 @@ class Grid:
         else:
             _check(lib().grid_mask_phases(*args, phases, _stream_handle(stream)))
         return out, eos, status
+
+
+def mask_noalloc(grid, cfg_dev, pool_dev, B, out, eos, status, stream=None):
+    """grid_mask_noalloc: the mask of B rows into caller tensors, with the
+    library's static device scratch as workspace (nothing is allocated)."""
+    assert cfg_dev.numel() >= 32 * B and out.numel() >= B * grid.W and out.is_contiguous()
+    assert eos.numel() >= B and status.numel() >= B
+    _check(lib().grid_mask_noalloc(grid.h, B, ctypes.c_void_p(cfg_dev.data_ptr()),
+                                   ctypes.c_void_p(pool_dev.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                                   ctypes.c_void_p(eos.data_ptr()), ctypes.c_void_p(status.data_ptr()),
+                                   _stream_handle(stream)))
+    return out, eos, status
 
 
 def apply(mask, logits, stream=None):
