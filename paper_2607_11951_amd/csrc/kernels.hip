@@ -79,6 +79,7 @@ constexpr int kLexChunk = 32;        // lexicon spellings a wave takes at a time
 constexpr int kLaneSlots = 32;       // lanes of a wave with a stack area in the residue LDS
 static_assert(kWalkChunk <= kLaneSlots && kLexChunk <= kLaneSlots, "chunks fit the lane stack areas");
 static_assert((kLaneSlots & (kLaneSlots - 1)) == 0, "kLaneSlots is a power of two");
+static_assert(kStackWin == kBlock, "one stack-window entry per prologue thread");
 constexpr uint32_t kWalkLdsMax = 160 * 1024;
 
 struct Tables {
@@ -232,6 +233,7 @@ __host__ __device__ inline RowLayout row_layout(const Tables& tb) { return row_l
 // issues the loads of K chunks before it stores any, so the whole staging
 // costs about one memory round trip instead of one per region.  The last,
 // partial chunk of a region is copied byte by byte.
+#define GRID_LDS_VOID __attribute__((address_space(3))) void
 struct StageRegion {
   const uint8_t* src;
   uint8_t* dst;
@@ -292,6 +294,41 @@ __device__ inline void stage_regions(const StageRegion (&rg)[N], int tid, int nt
     }
   }
 }
+
+// Global -> LDS copies by direct global-to-LDS loads (global_load_lds, 16
+// bytes a lane): no registers hold the data on the way, so every load of the
+// staging is issued before any is waited for and the whole staging costs
+// about one memory round trip.  A region's full 16-byte chunks are cut into
+// blocks of 64 (one wave instruction writes 1 KB at a wave-uniform LDS
+// address, lane l at +16 l), dealt to the waves of the workgroup round-robin
+// across all regions (first = the running block number); a region's last
+// partial chunk is copied byte by byte by one thread.  Both ends of every
+// region are 16-byte aligned.  The caller runs dma_wait() and a barrier
+// before reading the copies.
+__device__ inline uint32_t dma_region(const StageRegion& rg, int tid, int nt, uint32_t first) {
+  const uint32_t lane = (uint32_t)tid & 63u, wave = (uint32_t)tid >> 6, nw = (uint32_t)nt >> 6;
+  const uint32_t full = rg.bytes / 16u, nblk = (full + 63u) / 64u;
+  for (uint32_t b = (wave + nw - first % nw) % nw; b < nblk; b += nw) {
+    const uint32_t c = b * 64u + lane;
+    if (c < full)
+      __builtin_amdgcn_global_load_lds((const void*)(rg.src + 16u * c), (GRID_LDS_VOID*)(rg.dst + 64u * 16u * b), 16, 0,
+                                       0);
+  }
+  const uint32_t tail = rg.bytes & 15u;
+  if (tail && (uint32_t)tid == (first + nblk) % (uint32_t)nt)
+    for (uint32_t i = rg.bytes - tail; i < rg.bytes; ++i) rg.dst[i] = rg.src[i];
+  return first + nblk;
+}
+
+template <int N>
+__device__ inline uint32_t dma_regions(const StageRegion (&rg)[N], int tid, int nt, uint32_t first = 0) {
+#pragma unroll
+  for (int j = 0; j < N; ++j) first = dma_region(rg[j], tid, nt, first);
+  return first;
+}
+
+// Waits for this thread's outstanding loads, direct-to-LDS ones included.
+__device__ inline void dma_wait() { __builtin_amdgcn_s_waitcnt(0); }
 
 // Terminal set of every terminal (not the end of input), word w.
 __device__ inline uint32_t all_word(int T, int w) {
@@ -910,16 +947,21 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   uint32_t* a2 = (uint32_t*)(rw + L.a2);
   const grid_config cfg = cfgs[row];
   const ParseLds PL = prologue_parse_lds(tb);
+  const uint32_t depth = cfg.stk_depth;
+  const uint32_t lo = depth > (uint32_t)kStackWin ? depth - kStackWin : 0;
+  // one round trip to memory: the LR tables go straight to LDS while every
+  // thread loads one entry of the top kStackWin stack entries
+  const bool shape_ok = cfg.q < tb.S && cfg.slot < tb.n_slots && depth >= 1;  // uniform
   {
     const StageRegion rg[4] = {parse_region(tb, plds, PL, 0), parse_region(tb, plds, PL, 1),
                                parse_region(tb, plds, PL, 2), parse_region(tb, plds, PL, 3)};
-    stage_regions<4, 8>(rg, tid, kBlock);
+    dma_regions<4>(rg, tid, kBlock);
   }
+  uint32_t s_top = 0;
+  if (shape_ok && lo + (uint32_t)tid < depth) s_top = pool[cfg.stk_off + lo + tid];
   const ParseTabs<true> pt = lds_parse(tb, plds, PL);
-
   if (tid == 0) {
-    int b = 0;
-    if (cfg.q >= tb.S || cfg.slot >= tb.n_slots || cfg.stk_depth < 1) b = 1;
+    int b = shape_ok ? 0 : 1;
     if (!b) {
       Slot sl = load_slot(tb, cfg.slot);
       if (cfg.lexnode != kNoLex && cfg.lexnode >= sl.nodes) b = 1;
@@ -933,22 +975,29 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     hacc[0] = 0;
     hacc[1] = 0;
   }
-  {
-    uint64_t* rb = (uint64_t*)(rw + L.rbits);
-    for (int i = tid; i < 2 * ((tb.U + 63) / 64); i += kBlock) rb[i] = 0ull;
+  {  // the residue bitmaps start empty (16-byte stores)
+    uint4* rb = (uint4*)(rw + L.rbits);
+    for (int i = tid; i < (tb.U + 63) / 64; i += kBlock) rb[i] = make_uint4(0, 0, 0, 0);
   }
+  dma_wait();
   __syncthreads();
-  const uint32_t depth = cfg.stk_depth;
-  const uint32_t lo = depth > (uint32_t)kStackWin ? depth - kStackWin : 0;
-  if (!bad) {
+  if (!bad) {  // every entry is an LR state; the window goes to LDS; the content hash for the cache
     uint64_t h1 = 0, h2 = 0;
-    for (uint32_t i = tid; i < depth; i += kBlock) {
-      const uint16_t s = pool[cfg.stk_off + i];
-      if (s >= tb.NS) bad = 1;
-      if (i >= lo) win[i - lo] = s;
+    if (lo + (uint32_t)tid < depth) {
+      const uint32_t i = lo + (uint32_t)tid;
+      if (s_top >= (uint32_t)tb.NS) bad = 1;
+      win[tid] = (uint16_t)s_top;
       if (tb.cache) {
-        h1 += stack_mix(i, s, 0x9E3779B97F4A7C15ull);
-        h2 += stack_mix(i, s, 0xD1B54A32D192ED03ull);
+        h1 += stack_mix(i, s_top, 0x9E3779B97F4A7C15ull);
+        h2 += stack_mix(i, s_top, 0xD1B54A32D192ED03ull);
+      }
+    }
+    for (uint32_t i = tid; i < lo; i += kBlock) {  // entries below the window
+      const uint16_t v = pool[cfg.stk_off + i];
+      if (v >= tb.NS) bad = 1;
+      if (tb.cache) {
+        h1 += stack_mix(i, v, 0x9E3779B97F4A7C15ull);
+        h2 += stack_mix(i, v, 0xD1B54A32D192ED03ull);
       }
     }
     if (tb.cache) {
@@ -1666,8 +1715,9 @@ __global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __r
                                {(const uint8_t*)tb.term_info, (uint8_t*)tinfo_s, (uint32_t)tb.T * 4u},
                                {(const uint8_t*)tb.acc_off, (uint8_t*)acc_off_s, (uint32_t)(tb.S + 1) * 4u},
                                {tb.acc_list, acc_list_s, (uint32_t)tb.n_acc}};
-    stage_regions<5, 4>(rg, tid, kBlock);
+    dma_regions<5>(rg, tid, kBlock);
   }
+  dma_wait();
   __syncthreads();
   if (tid < 8) {
     uint32_t iw = 0;
@@ -2656,7 +2706,7 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
   if (use_lds && !bad) {
     const StageRegion rg[4] = {parse_region(tb, alds, PL, 0), parse_region(tb, alds, PL, 1),
                                parse_region(tb, alds, PL, 2), parse_region(tb, alds, PL, 3)};
-    stage_regions<4, 8>(rg, tid, kBlock);
+    dma_regions<4>(rg, tid, kBlock);
   }
   // the lexer tables too when they fit: every byte step is then an LDS read
   const AccLexLds XL = accept_lex_lds(tb);
@@ -2669,12 +2719,13 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
                                {(const uint8_t*)tb.acc_off, xl + XL.acc_off, (uint32_t)(tb.S + 1) * 4u},
                                {tb.acc_list, xl + XL.acc_list, (uint32_t)tb.n_acc},
                                {(const uint8_t*)tb.live, xl + XL.live, (uint32_t)tb.S * 32u}};
-    stage_regions<6, 4>(rg, tid, kBlock);
+    dma_regions<6>(rg, tid, kBlock, 1000u);
     lp = LexPtrs{(const uint16_t*)(xl + XL.dfa), xl + XL.bclass, (const uint32_t*)(xl + XL.tinfo),
                  (const uint32_t*)(xl + XL.acc_off), xl + XL.acc_list, (const uint32_t*)(xl + XL.live)};
   }
   const bool fits = use_lds && !bad && d0 < lcap;  // uniform
-  __syncthreads();  // s_bad is cleared
+  dma_wait();
+  __syncthreads();  // s_bad is cleared, the tables are in LDS
   if (copyable) {  // the input stack to the row's output area (and to LDS), entries checked
     for (uint32_t i = (uint32_t)tid; i < d0; i += kBlock) {
       const uint16_t v = pool[cfg.stk_off + i];
