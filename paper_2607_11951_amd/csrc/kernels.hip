@@ -1880,6 +1880,7 @@ struct ResLds {  // byte offsets into dynamic LDS
 };
 
 __host__ __device__ inline ResLds res_lds_with(const Tables& tb, int mw, int B, bool dense) {
+  (void)mw;
   ResLds w;
   uint32_t o = 0;
   w.dfa = o;
@@ -1897,8 +1898,8 @@ __host__ __device__ inline ResLds res_lds_with(const Tables& tb, int mw, int B, 
   w.parse = o;
   w.pl = parse_lds(tb, o, dense);
   o += w.pl.total;
-  w.live = o;
-  o += pad16((uint32_t)(tb.S * mw * 4));
+  w.live = o;  // the live sets as in global memory, 8 words per state
+  o += pad16((uint32_t)(tb.S * 32));
   w.lanes = o;  // stack areas of the first kLaneSlots lanes of each wave
   o += (kWalkThreads / 64) * kLaneSlots * kFastLane * 2;
   w.umask = o;  // per work item: its residue bitmap word
@@ -1970,7 +1971,7 @@ __device__ __forceinline__ int residue_lane(const WalkShared<MW>& sh, const RowH
   rc.bs = BaseStack<true>{sh.pool + h.stk_off, in_mem<true>((const uint16_t*)(rowblk + RL.win)), h.stk_depth,
                           h.stk_depth > (uint32_t)kWalkWin ? h.stk_depth - kWalkWin : 0u};
   rc.sl = sl;
-  rc.tv = TermView{sh.tinfo, sh.I, h.R, sh.live, MW};
+  rc.tv = TermView{sh.tinfo, sh.I, h.R, sh.live, 8};
   rc.acc_off = sh.acc_off;
   rc.acc_list = sh.acc_list;
   rc.a2 = (const uint32_t*)(rw + RL.a2);
@@ -2112,7 +2113,7 @@ __device__ __forceinline__ int residue_token(const WalkShared<MW>& sh, const Row
     lx.rem_len = h.rem_len;
     lx.lexnode = h.lexnode;
     lx.tf = tb.lex_token[(size_t)h.slot_id * tb.V + id0];
-    const uint32_t v = class_verdict<MW, LexLane, false>(h, sh.I, sh.live, MW, sh.tinfo, sh.acc_off, sh.acc_list,
+    const uint32_t v = class_verdict<MW, LexLane, false>(h, sh.I, sh.live, 8, sh.tinfo, sh.acc_off, sh.acc_list,
                                                          (const uint32_t*)(rw + RL.a2), 8, rec, lx);
     if (v == kVerdictAllow) return 1;
     if (v == kVerdictReject) return 0;
@@ -2186,6 +2187,22 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
       in_mem<true>((uint16_t*)(lds + WL.lanes) + ((tid >> 6) * kLaneSlots + (lane & (kLaneSlots - 1))) * kFastLane);
   uint8_t* rows = ws + kWsHead;
   const int nsub = (tb.U + 63) / 64;
+  // the grammar tables go straight to LDS at once (direct global-to-LDS
+  // loads, waited for at the first barrier that follows); the live sets are
+  // staged as in global memory, 8 words per state
+  {
+    const StageRegion rg[10] = {{(const uint8_t*)tb.dfa, lds + WL.dfa, (uint32_t)(tb.S * tb.C * 2)},
+                                {tb.bclass, bcls, 256u},
+                                {(const uint8_t*)tb.acc_off, lds + WL.acc_off, (uint32_t)(tb.S + 1) * 4},
+                                {tb.acc_list, lds + WL.acc_list, (uint32_t)tb.n_acc},
+                                {(const uint8_t*)tb.live, (uint8_t*)live_s, (uint32_t)tb.S * 32u},
+                                {(const uint8_t*)tb.term_info, (uint8_t*)tinfo_s, (uint32_t)tb.T * 4u},
+                                parse_region(tb, lds, WL.pl, 0),
+                                parse_region(tb, lds, WL.pl, 1),
+                                parse_region(tb, lds, WL.pl, 2),
+                                parse_region(tb, lds, WL.pl, 3)};
+    dma_regions<10>(rg, tid, kWalkThreads);
+  }
   bool staged = false;
   for (int g0 = 0; g0 < B; g0 += WL.group) {
     const int gr = min(WL.group, B - g0);
@@ -2194,7 +2211,8 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
     bool blocks = false;  // the group's row blocks are in LDS
     for (int k0 = 0; k0 < mine; k0 += kMaxItems) {
       const int n_it = min(kMaxItems, mine - k0);
-      __syncthreads();  // the previous round is done with umask_s / upre_s
+      dma_wait();
+      __syncthreads();  // the previous round is done with umask_s / upre_s; the tables are in LDS
       for (int t = tid; t < n_it; t += kWalkThreads) {
         const int j = (int)blockIdx.x + (k0 + t) * (int)gridDim.x;
         const int lex = j >= gr * nsub ? 1 : 0, jr = j - lex * gr * nsub;
@@ -2231,23 +2249,13 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
       __syncthreads();
       const int n_und = (int)upre_s[n_it];
       if (n_und == 0) continue;  // uniform
-      if (!staged) {  // grammar tables, once per workgroup
-        const StageRegion rg[8] = {{(const uint8_t*)tb.dfa, lds + WL.dfa, (uint32_t)(tb.S * tb.C * 2)},
-                                   {tb.bclass, bcls, 256u},
-                                   {(const uint8_t*)tb.acc_off, lds + WL.acc_off, (uint32_t)(tb.S + 1) * 4},
-                                   {tb.acc_list, lds + WL.acc_list, (uint32_t)tb.n_acc},
-                                   parse_region(tb, lds, WL.pl, 0),
-                                   parse_region(tb, lds, WL.pl, 1),
-                                   parse_region(tb, lds, WL.pl, 2),
-                                   parse_region(tb, lds, WL.pl, 3)};
-        stage_regions<8, 4>(rg, tid, kWalkThreads);
-        for (int i = tid; i < tb.S * MW; i += kWalkThreads) live_s[i] = tb.live[(i / MW) * 8 + i % MW];
-        for (int t = tid; t < 256; t += kWalkThreads) tinfo_s[t] = t < tb.T ? tb.term_info[t] : 0u;
-        __syncthreads();
+      if (!staged) {  // the ignored set from the staged terminal info, once per workgroup
         if (tid < 8) {
           uint32_t iw = 0;
-          for (int j = 0; j < 32; ++j)
-            if (tinfo_s[tid * 32 + j] & 1u) iw |= 1u << j;
+          for (int j = 0; j < 32; ++j) {
+            const int t = tid * 32 + j;
+            if (t < tb.T && (tinfo_s[t] & 1u)) iw |= 1u << j;
+          }
           I_s[tid] = iw;
         }
         staged = true;
@@ -2312,6 +2320,7 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
       }
     }
   }
+  dma_wait();  // a workgroup without items still has its table copies in flight
 }
 
 // ---------------------------------------------------------------- finalize
