@@ -219,6 +219,10 @@ enum {
                                terminal order, the target state of every terminal whose
                                PARSE_STATE shift bit is set (0 for accept); terminal t's
                                target is entry (shift bits below t) of the state's run */
+  GRID_ART_STATE_SYMBOL,    /* u32 [n_lr]: the symbol on which the LR automaton enters each
+                               state (terminal id, or 0x10000 | nonterminal index;
+                               0xFFFFFFFF for the initial state) -- the "goto" of the
+                               rolling configuration hash */
   GRID_ART_COUNT
 };
 int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);
@@ -312,13 +316,16 @@ int grid_mask_noalloc(const grid_compiled* g, int32_t B, const grid_config* cfg_
  * the row's mask depends on -- the DFA state q, the pending lexeme (length,
  * first 8 bytes, lexicon node, empty flag), the lexicon slot (one key per
  * schema, so an identifier position never reads another schema's entry:
- * Proposition 6) and a 128-bit content hash of the whole LR stack -- plus a
- * fingerprint of the compiled handle.  A hit reproduces the cold row bit for
- * bit (cache-on equals cache-off) unless two stacks collide in the 128-bit
- * hash.  Entries are written once and never evicted; a row whose probe
- * window (8 slots) is full stays uncached.  Calls sharing a cache may run
- * concurrently: a slot is claimed by an atomic compare-and-swap, written,
- * then published, and only published entries are read. */
+ * Proposition 6), the stack depth and the stack -- plus a fingerprint of the
+ * compiled handle.  The stack enters the key as its rolling configuration
+ * hash H(top) when the caller keeps one (grid_stack_hash, grid_accept_inplace;
+ * read in O(1)), else as a 128-bit content hash summed over every entry.  A
+ * hit reproduces the cold row bit for bit (cache-on equals cache-off) unless
+ * two stacks collide in the hash.  Entries are written once and never
+ * evicted; a row whose probe window (8 slots) is full stays uncached.  Calls
+ * sharing a cache may run concurrently: a slot is claimed by an atomic
+ * compare-and-swap, written, then published, and only published entries are
+ * read. */
 #define GRID_CACHE_LOOKUP 1u   /* rows whose key is published copy the cached row */
 #define GRID_CACHE_INSERT 2u   /* rows that miss claim a slot and publish their row */
 /* Device bytes of a cache of n_entries entries (a power of two >= 1); 0 if
@@ -328,11 +335,29 @@ size_t grid_cache_bytes(const grid_compiled* g, int32_t n_entries);
  * asynchronous on stream. */
 int grid_cache_clear(const grid_compiled* g, void* cache_dev, size_t cache_bytes, void* stream);
 /* grid_mask with a cache (cache_flags: GRID_CACHE_*; a null cache or flags 0
- * is exactly grid_mask).  Hit rows skip the walk. */
+ * is exactly grid_mask).  stack_hash_dev: device u64 rolling hash of every
+ * stack-pool entry (grid_stack_hash), or NULL for the content hash; a cache
+ * must be used with one kind of key only.  Hit rows skip the walk. */
 int grid_mask_cached(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
-                     const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
-                     int32_t* status_dev, void* workspace_dev, size_t workspace_bytes, void* cache_dev,
-                     size_t cache_bytes, uint32_t cache_flags, void* stream);
+                     const uint16_t* stack_pool_dev, const uint64_t* stack_hash_dev, uint32_t* mask_dev,
+                     uint8_t* eos_dev, int32_t* status_dev, void* workspace_dev, size_t workspace_bytes,
+                     void* cache_dev, size_t cache_bytes, uint32_t cache_flags, void* stream);
+
+/* ------------------------------------------------- rolling configuration hash */
+/* The rolling configuration hash of an LR stack (section 6.4, the audit
+ * chain): entry 0 (the initial state, the root) hashes to 0, entry i > 0 to
+ * H_i = low64(BLAKE2b-128(H_{i-1} || u32(state_i) || u32(goto_i))) with
+ * BLAKE2b as published (RFC 7693), the u64 and u32 fields little-endian,
+ * goto_i the state's accessing symbol (GRID_ART_STATE_SYMBOL) and low64 the
+ * first 8 digest bytes read little-endian.  A push costs one hash, a pop
+ * none.  grid_stack_hash writes stack_hash_dev[stk_off + i] for every entry of
+ * every row's stack (device, asynchronous; O(depth) per row, once when a
+ * configuration enters the device); grid_stack_hash_host does the same for one
+ * stack on the host (out[0 .. depth)); GRID_E_ARG if an entry is not an LR
+ * state. */
+int grid_stack_hash(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                    const uint16_t* stack_pool_dev, uint64_t* stack_hash_dev, void* stream);
+int grid_stack_hash_host(const grid_compiled* g, const uint16_t* states, uint32_t depth, uint64_t* out);
 
 /* ------------------------------------------------------------------- accept */
 /* Device incremental advance (section 6.1, per-token step 7): for every row b,
@@ -355,6 +380,26 @@ int grid_mask_cached(const grid_compiled* g, int32_t B, const grid_config* cfg_d
 int grid_accept(const grid_compiled* g, int32_t B, const grid_config* cfg_dev, const uint16_t* stack_pool_dev,
                 const int32_t* token_dev, grid_config* cfg_out_dev, uint16_t* stack_out_dev, uint32_t stack_cap,
                 int32_t* status_dev, void* stream);
+
+/* The device incremental advance on a persistent per-row stack arena
+ * (section 6.2, the interned stack arena; section 6.4, the rolling hash):
+ * row b's stack lives in stack_pool_dev[b * stack_cap, (b + 1) * stack_cap)
+ * (cfg_dev[b].stk_off must be b * stack_cap, else GRID_ROW_BAD_CONFIG) and is
+ * advanced in place by token_dev[b] with the rules of grid_accept: entries
+ * below the lowest one the step rewrites are neither read back nor written
+ * (each entry's parent is the entry below it), the rewritten entries are
+ * written and, when stack_hash_dev (the rolling hash of every pool entry, as
+ * grid_stack_hash writes it) is not NULL, their hashes are recomputed from
+ * their parents' -- one hash per pushed entry, nothing per popped one.
+ * cfg_dev[b] becomes the advanced configuration.  status_dev as grid_accept;
+ * a row that is not GRID_ROW_OK keeps its configuration and stack untouched;
+ * a stack that needs more than 8,192 entries in one step is reported as
+ * GRID_ROW_OVERFLOW (grid_accept advances it).  The previous configuration of
+ * an advanced row is not kept (copy the row's region first to fork it).
+ * Asynchronous on stream. */
+int grid_accept_inplace(const grid_compiled* g, int32_t B, grid_config* cfg_dev, uint16_t* stack_pool_dev,
+                        uint64_t* stack_hash_dev, uint32_t stack_cap, const int32_t* token_dev,
+                        int32_t* status_dev, void* stream);
 
 /* -------------------------------------------------------------------- apply */
 #define GRID_DTYPE_F32 0

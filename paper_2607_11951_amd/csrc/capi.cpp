@@ -194,6 +194,7 @@ extern "C" int grid_artifact(const grid_compiled* g, int32_t which, const void**
     case GRID_ART_PARSE_REDX: put(g->parser.predx, p, n); break;
     case GRID_ART_PARSE_SHIFT: put(g->parser.pshift, p, n); break;
     case GRID_ART_GOTO_HASH: put(g->parser.goto_hash, p, n); break;
+    case GRID_ART_STATE_SYMBOL: put(g->parser.state_sym, p, n); break;
     default: return fail(GRID_E_ARG, "unknown artifact " + std::to_string(which));
   }
   return GRID_OK;

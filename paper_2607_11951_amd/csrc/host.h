@@ -19,6 +19,7 @@ constexpr int kMaxCategories = 8;
 constexpr uint32_t kNoLex = 0xFFFFFFFFu;
 constexpr uint16_t kActShift = 0x4000, kActReduce = 0x8000, kActAccept = 0xC000;
 constexpr uint16_t kNoGoto = 0xFFFF;
+constexpr uint32_t kSymNonterminal = 0x10000u, kNoSymbol = 0xFFFFFFFFu;
 constexpr int kDead = 0, kStart = 1;   // lexer DFA state numbering
 
 struct Error : std::runtime_error {
@@ -89,6 +90,9 @@ struct Parser {
   // (state << 16 | nonterminal) + 1 (0 empty), target
   std::vector<uint32_t> goto_hash;
   int goto_hbits = 0;
+  // accessing symbol of each LR state: terminal id, or kSymNonterminal |
+  // nonterminal index; kNoSymbol for the initial state
+  std::vector<uint32_t> state_sym;
   uint16_t act(int s, int t) const { return action[(size_t)s * (T + 1) + t]; }
   uint16_t gto(int s, int a) const { return go[(size_t)s * N + a]; }
 };

@@ -45,6 +45,7 @@
 
 #include "host.h"
 #include "lexhash.h"
+#include "rolling_hash.h"
 
 namespace grid {
 int fail(int code, const std::string& msg);
@@ -115,6 +116,8 @@ struct Tables {
   const uint16_t* pshift;      // shift targets per LR state
   const uint16_t* go;          // dense GOTO [states][N], kNoGoto none
   int tw, n_pstate, n_predx, n_pshift, n_acc, hbits;
+  const uint32_t* state_sym;  // [NS] accessing symbol of each LR state (rolling hash)
+  const uint64_t* stack_hash; // rolling hash of every stack entry, or null (mask cache key)
   uint8_t* cache;             // mask cache (null: off)
   uint32_t cache_mask;        // entries - 1
   uint32_t cache_flags;       // GRID_CACHE_*
@@ -132,6 +135,7 @@ struct CacheEntry {
 };
 static_assert(sizeof(CacheEntry) == 64, "cache entry header is 64 bytes");
 constexpr int kCacheProbes = 8;
+constexpr uint64_t kRollingKeyTag = 0x524F4C4C494E4748ull;  // key words of a rolling-hash key
 constexpr uint32_t kRowCached = 0xCAC4;  // RowHeader::valid of a row served from the cache
 
 __host__ __device__ inline uint32_t cache_stride_of(int W) { return 64u + ((uint32_t)W * 4u + 15u) / 16u * 16u; }
@@ -981,13 +985,14 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   }
   dma_wait();
   __syncthreads();
+  const bool sum_hash = tb.cache && !tb.stack_hash;  // the cache key needs the whole stack's content
   if (!bad) {  // every entry is an LR state; the window goes to LDS; the content hash for the cache
     uint64_t h1 = 0, h2 = 0;
     if (lo + (uint32_t)tid < depth) {
       const uint32_t i = lo + (uint32_t)tid;
       if (s_top >= (uint32_t)tb.NS) bad = 1;
       win[tid] = (uint16_t)s_top;
-      if (tb.cache) {
+      if (sum_hash) {
         h1 += stack_mix(i, s_top, 0x9E3779B97F4A7C15ull);
         h2 += stack_mix(i, s_top, 0xD1B54A32D192ED03ull);
       }
@@ -995,12 +1000,12 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     for (uint32_t i = tid; i < lo; i += kBlock) {  // entries below the window
       const uint16_t v = pool[cfg.stk_off + i];
       if (v >= tb.NS) bad = 1;
-      if (tb.cache) {
+      if (sum_hash) {
         h1 += stack_mix(i, v, 0x9E3779B97F4A7C15ull);
         h2 += stack_mix(i, v, 0xD1B54A32D192ED03ull);
       }
     }
-    if (tb.cache) {
+    if (sum_hash) {
       atomicAdd(&hacc[0], (unsigned long long)h1);
       atomicAdd(&hacc[1], (unsigned long long)h2);
     }
@@ -1022,7 +1027,13 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   // mask cache: probe the row's key; a published entry is the row's mask, an
   // empty slot on the way is claimed for the row when inserting
   if (tb.cache && tid == 0) {
-    const uint64_t h1 = hacc[0], h2 = hacc[1];
+    // the stack's part of the key: its rolling hash H(top) when the caller
+    // keeps one (O(1) to read), else the content sums over every entry
+    uint64_t h1 = hacc[0], h2 = hacc[1];
+    if (tb.stack_hash) {
+      h1 = tb.stack_hash[cfg.stk_off + depth - 1];
+      h2 = kRollingKeyTag;
+    }
     const uint32_t key[13] = {tb.fp,
                               cfg.q,
                               cfg.slot,
@@ -2686,12 +2697,20 @@ __host__ __device__ inline uint32_t accept_stack_cap(uint32_t cap) { return cap 
 // global memory; so is every row when the LR tables are too large to stage
 // (use_lds = 0).  A row whose stack does not fit cap gets depth 0 (a
 // configuration every call rejects).
+//
+// In place (inplace = 1; cfg_out == cfgs, pool_out == pool): row b's stack
+// lives in pool[b * cap, (b + 1) * cap) and is its persistent arena -- the
+// entries below the lowest one a step rewrites are neither copied nor
+// written, the rewritten ones are written back from LDS, and, with hash, the
+// rolling hash of every rewritten entry is recomputed from its parent's (one
+// hash per pushed node).  A row that is not advanced keeps its stack and
+// configuration untouched; a stack too deep for the LDS area is reported as
+// an overflow (the out-of-place call handles it).
 template <int MW>
-__global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_config* __restrict__ cfgs,
-                                                        const uint16_t* __restrict__ pool,
+__global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_config* cfgs, const uint16_t* pool,
                                                         const int32_t* __restrict__ tokens, grid_config* cfg_out,
-                                                        uint16_t* pool_out, uint32_t cap, int32_t* status,
-                                                        int use_lds, int use_lex) {
+                                                        uint16_t* pool_out, uint64_t* hash, uint32_t cap,
+                                                        int32_t* status, int use_lds, int use_lex, int inplace) {
   extern __shared__ __align__(16) uint8_t alds[];
   __shared__ int s_st, s_bad;
   __shared__ uint32_t s_d, s_lo;
@@ -2700,7 +2719,7 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
   const int tok = tokens[row];
   const uint32_t d0 = cfg.stk_depth;
   uint16_t* out_stk = pool_out + (size_t)row * cap;
-  const bool copyable = d0 >= 1 && d0 <= cap;  // uniform
+  const bool copyable = d0 >= 1 && d0 <= cap && (!inplace || cfg.stk_off == (uint32_t)row * cap);  // uniform
   bool bad = !copyable || cfg.q >= (uint32_t)tb.S || cfg.q == (uint32_t)kDead || cfg.slot >= (uint32_t)tb.n_slots ||
              tok < 0 || tok >= tb.V;
   Slot sl{};
@@ -2739,18 +2758,20 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
     for (uint32_t i = (uint32_t)tid; i < d0; i += kBlock) {
       const uint16_t v = pool[cfg.stk_off + i];
       if (v >= (uint32_t)tb.NS) s_bad = 1;
-      out_stk[i] = v;
+      if (!inplace) out_stk[i] = v;
       if (fits) stk_l[i] = v;
     }
   }
   __syncthreads();
   bad = bad || s_bad != 0;  // uniform
   grid_config out = cfg;
-  if (copyable) out.stk_off = (uint32_t)row * cap;
-  else out.stk_depth = 0;
+  if (!inplace) {
+    if (copyable) out.stk_off = (uint32_t)row * cap;
+    else out.stk_depth = 0;
+  }
   if (bad) {
     if (tid == 0) {
-      cfg_out[row] = out;
+      if (!inplace) cfg_out[row] = out;
       if (status) status[row] = GRID_ROW_BAD_CONFIG;
     }
     return;
@@ -2767,6 +2788,7 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
       st = advance_row<true, MW>(tb, lp, lds_parse(tb, alds, PL), sl, stk_l, d, lcap, tok, lx, lo);
       if (st == GRID_ROW_OVERFLOW && lcap < cap) st = -1;
     }
+    if (inplace && st == -1) st = GRID_ROW_OVERFLOW;  // in place, only the LDS route
     s_st = st;
     s_d = d;
     s_lo = lo;
@@ -2787,6 +2809,19 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
       for (uint32_t i = lo; i < d0; ++i) out_stk[i] = pool[cfg.stk_off + i];
   }
   if (tid != 0) return;
+  if (st == GRID_ROW_OK && hash) {  // rolling hashes of the rewritten entries, each from its parent's
+    const uint32_t off = out.stk_off;
+    uint64_t h = hash[off + lo - 1];  // lo >= 1: the bottom entry is never popped
+    for (uint32_t i = lo; i < d; ++i) {
+      const uint32_t sv = fits ? (uint32_t)stk_l[i] : (uint32_t)out_stk[i];
+      h = node_hash(h, sv, tb.state_sym[sv]);
+      hash[off + i] = h;
+    }
+  }
+  if (inplace && st != GRID_ROW_OK) {
+    if (status) status[row] = st;
+    return;
+  }
   if (st == GRID_ROW_OK) {
     out.stk_depth = d;
     out.lexnode = lx.lex;
@@ -2797,6 +2832,23 @@ __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_co
   }
   cfg_out[row] = out;
   if (status) status[row] = st;
+}
+
+// Rolling hash of every stack entry of every row (one thread per row: each
+// entry's hash needs its parent's): entry 0 is the root (hash 0), entry i > 0
+// hashes the one below it, its LR state and that state's accessing symbol.
+__global__ __launch_bounds__(64) void stack_hash_kernel(Tables tb, const grid_config* __restrict__ cfgs,
+                                                       const uint16_t* __restrict__ pool, uint64_t* __restrict__ hash,
+                                                       int B) {
+  const int row = (int)(blockIdx.x * 64u + threadIdx.x);
+  if (row >= B) return;
+  const grid_config cfg = cfgs[row];
+  uint64_t h = 0;
+  for (uint32_t i = 0; i < cfg.stk_depth; ++i) {
+    const uint32_t sv = pool[cfg.stk_off + i];
+    if (i > 0) h = node_hash(h, sv, sv < (uint32_t)tb.NS ? tb.state_sym[sv] : kNoSymbol);
+    hash[cfg.stk_off + i] = h;
+  }
 }
 
 bool bound(const grid_compiled* g, int which) { return g->dev[which] != nullptr || g->dev_bytes[which] == 0; }
@@ -2898,7 +2950,8 @@ static int bind_tables(const grid_compiled* g, Tables& tb) {
                                GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH,   GRID_ART_LEX_PREFIX,
                                GRID_ART_SPELL_OF_ID, GRID_ART_CLASS_MAP, GRID_ART_CLASS_OFF,
                                GRID_ART_CLASS_REC,   GRID_ART_LEX_STRIDE,  GRID_ART_LEX_TOKEN,
-                               GRID_ART_ID_FIRST,    GRID_ART_PARSE_SHIFT, GRID_ART_GOTO};
+                               GRID_ART_ID_FIRST,    GRID_ART_PARSE_SHIFT, GRID_ART_GOTO,
+                               GRID_ART_STATE_SYMBOL};
   for (int w : needed)
     if (!bound(g, w)) return fail(GRID_E_UNBOUND, "artifact " + std::to_string(w) + " is not bound");
   tb.dfa = (const uint16_t*)g->dev[GRID_ART_DFA_CLASS];
@@ -2927,6 +2980,8 @@ static int bind_tables(const grid_compiled* g, Tables& tb) {
   tb.lex_token = (const uint32_t*)g->dev[GRID_ART_LEX_TOKEN];
   tb.id_first = (const uint8_t*)g->dev[GRID_ART_ID_FIRST];
   tb.spell_of_id = (const uint32_t*)g->dev[GRID_ART_SPELL_OF_ID];
+  tb.state_sym = (const uint32_t*)g->dev[GRID_ART_STATE_SYMBOL];
+  tb.stack_hash = nullptr;
   tb.cmap = (const uint16_t*)g->dev[GRID_ART_CLASS_MAP];
   tb.coff = (const uint32_t*)g->dev[GRID_ART_CLASS_OFF];
   tb.crec = (const uint4*)g->dev[GRID_ART_CLASS_REC];
@@ -2954,7 +3009,7 @@ static int bind_tables(const grid_compiled* g, Tables& tb) {
 static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_dev, const uint16_t* stack_pool_dev,
                      uint32_t* mask_dev, uint8_t* eos_dev, int32_t* status_dev, void* workspace_dev,
                      size_t workspace_bytes, void* cache_dev, size_t cache_bytes, uint32_t cache_flags,
-                     uint32_t phases, void* stream) {
+                     uint32_t phases, void* stream, const uint64_t* stack_hash_dev = nullptr) {
   clear_error();
   if (phases & ~GRID_PHASE_ALL) return fail(GRID_E_ARG, "grid_mask: unknown phase bits");
   if (cache_flags & ~(GRID_CACHE_LOOKUP | GRID_CACHE_INSERT)) return fail(GRID_E_ARG, "grid_mask: unknown cache flags");
@@ -2979,6 +3034,7 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
     tb.cache = (uint8_t*)cache_dev;
     tb.cache_mask = (uint32_t)(n - 1);
     tb.cache_flags = cache_flags;
+    tb.stack_hash = stack_hash_dev;
   }
   const int mw = tb.tw;
   const ResLds WL = res_lds(tb, mw, B);
@@ -3016,11 +3072,39 @@ extern "C" int grid_mask(const grid_compiled* g, int32_t B, const grid_config* c
 }
 
 extern "C" int grid_mask_cached(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
-                                const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev,
-                                int32_t* status_dev, void* workspace_dev, size_t workspace_bytes, void* cache_dev,
-                                size_t cache_bytes, uint32_t cache_flags, void* stream) {
+                                const uint16_t* stack_pool_dev, const uint64_t* stack_hash_dev, uint32_t* mask_dev,
+                                uint8_t* eos_dev, int32_t* status_dev, void* workspace_dev, size_t workspace_bytes,
+                                void* cache_dev, size_t cache_bytes, uint32_t cache_flags, void* stream) {
   return mask_call(g, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, workspace_dev, workspace_bytes,
-                   cache_dev, cache_bytes, cache_flags, GRID_PHASE_ALL, stream);
+                   cache_dev, cache_bytes, cache_flags, GRID_PHASE_ALL, stream, stack_hash_dev);
+}
+
+extern "C" int grid_stack_hash(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                               const uint16_t* stack_pool_dev, uint64_t* stack_hash_dev, void* stream) {
+  clear_error();
+  if (!g || B <= 0 || !cfg_dev || !stack_pool_dev || !stack_hash_dev)
+    return fail(GRID_E_ARG, "grid_stack_hash: null pointer or bad batch size");
+  Tables tb;
+  const int rc = bind_tables(g, tb);
+  if (rc != GRID_OK) return rc;
+  hipLaunchKernelGGL(stack_hash_kernel, dim3((unsigned)((B + 63) / 64)), dim3(64), 0, (hipStream_t)stream, tb, cfg_dev,
+                     stack_pool_dev, stack_hash_dev, B);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_stack_hash launch: ") + hipGetErrorString(e));
+  return GRID_OK;
+}
+
+extern "C" int grid_stack_hash_host(const grid_compiled* g, const uint16_t* states, uint32_t depth, uint64_t* out) {
+  clear_error();
+  if (!g || (depth > 0 && (!states || !out))) return fail(GRID_E_ARG, "grid_stack_hash_host: null pointer");
+  uint64_t h = 0;
+  for (uint32_t i = 0; i < depth; ++i) {
+    const uint32_t sv = states[i];
+    if (sv >= (uint32_t)g->parser.n_states) return fail(GRID_E_ARG, "grid_stack_hash_host: entry is no LR state");
+    if (i > 0) h = node_hash(h, sv, g->parser.state_sym[sv]);
+    out[i] = h;
+  }
+  return GRID_OK;
 }
 
 // ------------------------------------------------------ no-alloc mask entry
@@ -3097,12 +3181,9 @@ extern "C" int grid_cache_clear(const grid_compiled* g, void* cache_dev, size_t 
   return GRID_OK;
 }
 
-extern "C" int grid_accept(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
-                           const uint16_t* stack_pool_dev, const int32_t* token_dev, grid_config* cfg_out_dev,
-                           uint16_t* stack_out_dev, uint32_t stack_cap, int32_t* status_dev, void* stream) {
-  clear_error();
-  if (!g || B <= 0 || !cfg_dev || !stack_pool_dev || !token_dev || !cfg_out_dev || !stack_out_dev || stack_cap < 2)
-    return fail(GRID_E_ARG, "grid_accept: null pointer or bad size");
+static int accept_call(const grid_compiled* g, int32_t B, const grid_config* cfg_dev, const uint16_t* stack_pool_dev,
+                       const int32_t* token_dev, grid_config* cfg_out_dev, uint16_t* stack_out_dev, uint64_t* hash_dev,
+                       uint32_t stack_cap, int32_t* status_dev, int inplace, void* stream) {
   Tables tb;
   const int rc = bind_tables(g, tb);
   if (rc != GRID_OK) return rc;
@@ -3119,16 +3200,36 @@ extern "C" int grid_accept(const grid_compiled* g, int32_t B, const grid_config*
   const dim3 grid((unsigned)B), block(kBlock);
   if (tb.tw == 2)
     hipLaunchKernelGGL(accept_kernel<2>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev, use_lds, use_lex);
+                       stack_out_dev, hash_dev, stack_cap, status_dev, use_lds, use_lex, inplace);
   else if (tb.tw == 4)
     hipLaunchKernelGGL(accept_kernel<4>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev, use_lds, use_lex);
+                       stack_out_dev, hash_dev, stack_cap, status_dev, use_lds, use_lex, inplace);
   else
     hipLaunchKernelGGL(accept_kernel<8>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, stack_cap, status_dev, use_lds, use_lex);
+                       stack_out_dev, hash_dev, stack_cap, status_dev, use_lds, use_lex, inplace);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_accept launch: ") + hipGetErrorString(e));
   return GRID_OK;
+}
+
+extern "C" int grid_accept(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                           const uint16_t* stack_pool_dev, const int32_t* token_dev, grid_config* cfg_out_dev,
+                           uint16_t* stack_out_dev, uint32_t stack_cap, int32_t* status_dev, void* stream) {
+  clear_error();
+  if (!g || B <= 0 || !cfg_dev || !stack_pool_dev || !token_dev || !cfg_out_dev || !stack_out_dev || stack_cap < 2)
+    return fail(GRID_E_ARG, "grid_accept: null pointer or bad size");
+  return accept_call(g, B, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev, stack_out_dev, nullptr, stack_cap,
+                     status_dev, 0, stream);
+}
+
+extern "C" int grid_accept_inplace(const grid_compiled* g, int32_t B, grid_config* cfg_dev, uint16_t* stack_pool_dev,
+                                   uint64_t* stack_hash_dev, uint32_t stack_cap, const int32_t* token_dev,
+                                   int32_t* status_dev, void* stream) {
+  clear_error();
+  if (!g || B <= 0 || !cfg_dev || !stack_pool_dev || !token_dev || stack_cap < 2)
+    return fail(GRID_E_ARG, "grid_accept_inplace: null pointer or bad size");
+  return accept_call(g, B, cfg_dev, stack_pool_dev, token_dev, cfg_dev, stack_pool_dev, stack_hash_dev, stack_cap,
+                     status_dev, 1, stream);
 }
 
 extern "C" int grid_apply(const uint32_t* mask_dev, void* logits_dev, int32_t dtype, int32_t B, int32_t V,

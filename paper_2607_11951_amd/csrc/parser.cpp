@@ -292,10 +292,14 @@ Parser build_parser(const GrammarText& g, const std::vector<std::string>& drop) 
     throw Error(GRID_E_LALR_CONFLICT, "LALR(1) conflict in state " + std::to_string(s) + " on " +
                                           sym_name(t) + ": " + describe(a) + " vs " + describe(b));
   };
+  out.state_sym.assign(NS, kNoSymbol);
   for (int s = 0; s < NS; ++s) {
     for (auto& e : edges[s]) {
       if (e.first < T) out.action[(size_t)s * (T + 1) + e.first] = (uint16_t)(kActShift | e.second);
       else if (e.first - T < out.N) out.go[(size_t)s * out.N + (e.first - T)] = (uint16_t)e.second;
+      // the symbol on which every transition into a state is taken (an LR(0)
+      // state has one accessing symbol): terminals by id, nonterminals tagged
+      out.state_sym[e.second] = e.first < T ? (uint32_t)e.first : kSymNonterminal | (uint32_t)(e.first - T);
     }
     std::vector<std::pair<Item, Bits>> seed(kla[s].begin(), kla[s].end());
     auto J = closure1(seed);

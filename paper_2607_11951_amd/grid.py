@@ -29,7 +29,7 @@ ART_NAMES = ["DFA_DENSE", "DFA_CLASS", "BYTE_CLASS", "DFA_ACCEPT_OFF", "DFA_ACCE
              "ALIAS_IDS", "TRIE_LEVEL_OFF", "TRIE_NODES", "LEX_FLAGS", "LEX_HASH", "LEX_SLOTS",
              "SPELL_REC", "PARSE_STATE", "PARSE_REDX", "GOTO_HASH", "SPELL_TAIL", "LEX_PREFIX",
              "SPELL_RANGE", "SPELL_OF_ID", "CLASS_MAP", "CLASS_OFF", "CLASS_REC", "LEX_STRIDE",
-             "LEX_TOKEN", "ID_FIRST", "PARSE_SHIFT"]
+             "LEX_TOKEN", "ID_FIRST", "PARSE_SHIFT", "STATE_SYMBOL"]
 ART = {n: i for i, n in enumerate(ART_NAMES)}
 
 CONFIG_DTYPE = np.dtype([("stk_off", "<u4"), ("stk_depth", "<u4"), ("lexnode", "<u4"), ("q", "<u2"),
@@ -42,7 +42,8 @@ EXPORTS = ["grid_compile", "grid_free", "grid_last_error", "grid_info", "grid_ad
            "grid_artifact", "grid_bind_device", "grid_config_from_prefix",
            "grid_mask_workspace_bytes", "grid_mask", "grid_mask_phases", "grid_apply",
            "grid_cache_bytes", "grid_cache_clear", "grid_mask_cached", "grid_accept",
-           "grid_mask_noalloc_max_bytes", "grid_mask_noalloc"]
+           "grid_mask_noalloc_max_bytes", "grid_mask_noalloc", "grid_stack_hash", "grid_stack_hash_host",
+           "grid_accept_inplace"]
 PHASE_PROLOGUE, PHASE_WALK, PHASE_RESIDUE, PHASE_FINALIZE, PHASE_ALL = 1, 2, 4, 8, 15
 
 
@@ -99,7 +100,10 @@ def lib():
         L.grid_mask_phases.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
         L.grid_apply.argtypes = [vp, vp, i32, i32, i32, ctypes.c_int64, vp]
         L.grid_accept.argtypes = [vp, i32, vp, vp, vp, vp, vp, ctypes.c_uint32, vp, vp]
-        L.grid_mask_cached.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, sz, vp, sz, ctypes.c_uint32, vp]
+        L.grid_mask_cached.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp, sz, ctypes.c_uint32, vp]
+        L.grid_stack_hash.argtypes = [vp, i32, vp, vp, vp, vp]
+        L.grid_stack_hash_host.argtypes = [vp, vp, ctypes.c_uint32, vp]
+        L.grid_accept_inplace.argtypes = [vp, i32, vp, vp, vp, ctypes.c_uint32, vp, vp, vp]
         L.grid_cache_bytes.argtypes = [vp, i32]
         L.grid_cache_bytes.restype = sz
         L.grid_cache_clear.argtypes = [vp, vp, sz, vp]
@@ -243,6 +247,43 @@ class Grid:
                                  stack_cap, ctypes.c_void_p(status.data_ptr()), _stream_handle(stream)))
         return out, stack_out, status
 
+    def accept_inplace(self, cfg_dev, pool_dev, tokens_dev, B, stack_cap, stack_hash=None, status=None,
+                       stream=None):
+        """grid_accept_inplace: row b's configuration cfg_dev[b] (stack at
+        pool_dev[b * stack_cap ..]) advanced in place by tokens_dev[b]; the
+        rolling hashes in stack_hash (uint64/int64 tensor parallel to the pool)
+        are kept up to date.  Returns the status tensor."""
+        import torch
+        if status is None:
+            status = torch.empty(B, dtype=torch.int32, device=cfg_dev.device)
+        assert tokens_dev.dtype == torch.int32 and tokens_dev.numel() >= B
+        assert pool_dev.numel() >= B * stack_cap
+        hp = ctypes.c_void_p(stack_hash.data_ptr()) if stack_hash is not None else None
+        _check(lib().grid_accept_inplace(self.h, B, ctypes.c_void_p(cfg_dev.data_ptr()),
+                                         ctypes.c_void_p(pool_dev.data_ptr()), hp, stack_cap,
+                                         ctypes.c_void_p(tokens_dev.data_ptr()), ctypes.c_void_p(status.data_ptr()),
+                                         _stream_handle(stream)))
+        return status
+
+    def stack_hash(self, cfg_dev, pool_dev, B, out=None, stream=None):
+        """grid_stack_hash: the rolling hash of every pool entry of the B rows'
+        stacks (int64 tensor parallel to the pool; entries outside the rows'
+        stacks are left as they are)."""
+        import torch
+        if out is None:
+            out = torch.zeros(pool_dev.numel(), dtype=torch.int64, device=pool_dev.device)
+        _check(lib().grid_stack_hash(self.h, B, ctypes.c_void_p(cfg_dev.data_ptr()),
+                                     ctypes.c_void_p(pool_dev.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                                     _stream_handle(stream)))
+        return out
+
+    def stack_hash_host(self, states):
+        """grid_stack_hash_host: the rolling hashes of one stack (uint64 array)."""
+        st = np.ascontiguousarray(states, dtype=np.uint16)
+        out = np.zeros(len(st), dtype=np.uint64)
+        _check(lib().grid_stack_hash_host(self.h, st.ctypes.data, len(st), out.ctypes.data))
+        return out
+
     def workspace_bytes(self, B):
         return lib().grid_mask_workspace_bytes(self.h, B)
 
@@ -269,10 +310,11 @@ class Grid:
                                       _stream_handle(stream)))
 
     def mask(self, cfg_dev, pool_dev, B, out=None, eos=None, status=None, workspace=None, stream=None,
-             phases=PHASE_ALL, cache=None, cache_flags=CACHE_LOOKUP | CACHE_INSERT):
+             phases=PHASE_ALL, cache=None, cache_flags=CACHE_LOOKUP | CACHE_INSERT, stack_hash=None):
         """Enqueues the mask of B rows; returns (mask int32 [B, W], eos u8 [B], status i32 [B]).
         phases selects a subset of the launches (grid_mask_phases); cache (from new_cache)
-        serves and records rows through the mask cache (grid_mask_cached)."""
+        serves and records rows through the mask cache (grid_mask_cached), keyed by the
+        rolling stack hashes stack_hash (from stack_hash) when given."""
         import torch
         dev = cfg_dev.device
         if out is None:
@@ -284,13 +326,15 @@ class Grid:
         if workspace is None:
             workspace = self.new_workspace(B, dev)
         assert cfg_dev.numel() >= 32 * B and out.numel() >= B * self.W and out.is_contiguous()
-        args = (self.h, B, ctypes.c_void_p(cfg_dev.data_ptr()), ctypes.c_void_p(pool_dev.data_ptr()),
-                ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(eos.data_ptr()),
+        head = (self.h, B, ctypes.c_void_p(cfg_dev.data_ptr()), ctypes.c_void_p(pool_dev.data_ptr()))
+        tail = (ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(eos.data_ptr()),
                 ctypes.c_void_p(status.data_ptr()), ctypes.c_void_p(workspace.data_ptr()), workspace.numel())
+        args = head + tail
         if cache is not None:
             assert phases == PHASE_ALL
-            _check(lib().grid_mask_cached(*args, ctypes.c_void_p(cache.data_ptr()), cache.numel(), cache_flags,
-                                          _stream_handle(stream)))
+            hp = ctypes.c_void_p(stack_hash.data_ptr()) if stack_hash is not None else None
+            _check(lib().grid_mask_cached(*head, hp, *tail, ctypes.c_void_p(cache.data_ptr()), cache.numel(),
+                                          cache_flags, _stream_handle(stream)))
         elif phases == PHASE_ALL:
             _check(lib().grid_mask(*args, _stream_handle(stream)))
         else:

@@ -485,3 +485,57 @@ def test_cache_sizes_and_argument_errors(G):
                                   None, None, ctypes.c_void_p(256), ctypes.c_size_t(1 << 30),
                                   ctypes.c_void_p(256), ctypes.c_size_t(stride * 3), 3, None)
     assert rc != 0
+
+
+def _state_symbols(grid):
+    return np.frombuffer(grid.artifact("STATE_SYMBOL"), dtype=np.uint32)
+
+
+def test_state_symbols_match_the_transitions(G):
+    """Every shift into a state is on that state's recorded symbol, and every
+    GOTO into a state on its recorded nonterminal (an LR(0) state has one
+    accessing symbol); the initial state has none."""
+    wl = make_workload(3, rows=1)
+    grid, _ = G.from_workload(wl)
+    inf = grid.info()
+    T, N, NS = inf["n_terminals"], inf["n_nonterminals"], inf["n_lr_states"]
+    sym = _state_symbols(grid)
+    act = np.frombuffer(grid.artifact("ACTION"), dtype=np.uint16).reshape(NS, T + 1)
+    go = np.frombuffer(grid.artifact("GOTO"), dtype=np.uint16).reshape(NS, N)
+    assert len(sym) == NS and sym[0] == 0xFFFFFFFF
+    seen = np.zeros(NS, bool)
+    for s in range(NS):
+        for t in range(T):
+            a = int(act[s, t])
+            if a & 0xC000 == 0x4000:
+                assert sym[a & 0x3FFF] == t
+                seen[a & 0x3FFF] = True
+        for A in range(N):
+            if go[s, A] != 0xFFFF:
+                assert sym[go[s, A]] == 0x10000 | A
+                seen[go[s, A]] = True
+    assert seen[1:].all()
+
+
+def test_rolling_hash_is_blake2b_of_parent_state_and_symbol(G):
+    """The rolling configuration hash (section 6.4) recomputed with Python's
+    own BLAKE2b (hashlib, digest size 16) over H(parent) || u32(state) ||
+    u32(goto), H(root) = 0, on the stacks of workload prefixes, a deep stack
+    and the one-entry stack; a stack entry that is no LR state is refused."""
+    import hashlib
+    import struct
+    wl = make_workload(3, rows=24)
+    grid, slots = G.from_workload(wl)
+    sym = _state_symbols(grid)
+    prefixes = list(wl.prefixes) + [b"select " + b"(" * 300 + b"1", b""]
+    for w in prefixes:
+        _, stack = grid.config(w, slots[wl.slots[0]])
+        got = grid.stack_hash_host(stack)
+        h = 0
+        for i, s in enumerate(stack.tolist()):
+            if i > 0:
+                d = hashlib.blake2b(struct.pack("<QII", h, s, int(sym[s])), digest_size=16).digest()
+                h = int.from_bytes(d[:8], "little")
+            assert int(got[i]) == h, (w[-30:], i)
+    with pytest.raises(G.GridError):
+        grid.stack_hash_host(np.array([0, 65000], dtype=np.uint16))
