@@ -481,7 +481,7 @@ def test_cache_sizes_and_argument_errors(G):
     # a cache of the wrong size is rejected before anything is launched
     rc = G.lib().grid_cache_clear(g.h, ctypes.c_void_p(16), ctypes.c_size_t(stride * 3), None)
     assert rc == -1 and b"power of two" in G.lib().grid_last_error()
-    rc = G.lib().grid_mask_cached(g.h, 1, ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256),
+    rc = G.lib().grid_mask_cached(g.h, 1, ctypes.c_void_p(256), ctypes.c_void_p(256), None, ctypes.c_void_p(256),
                                   None, None, ctypes.c_void_p(256), ctypes.c_size_t(1 << 30),
                                   ctypes.c_void_p(256), ctypes.c_size_t(stride * 3), 3, None)
     assert rc != 0
