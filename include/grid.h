@@ -158,7 +158,8 @@ enum {
   GRID_ART_LEX_SLOTS,       /* u32 [12] per slot: flags base, hash base, hash mask,
                                restricted-category mask, node count, prefix-table base,
                                prefix-table mask, stride-table base, stride-table mask,
-                               3 reserved */
+                               schema fingerprint (FNV-1a of the categories and their
+                               sorted words), 2 reserved */
   GRID_ART_SPELL_REC,       /* u32 [U][4] per spelling: its first 8 bytes (little-
                                endian, zero padded), first alias id | 1 << 31 when more ids
                                share the spelling, length | overflow chunk << 8 (bytes 24..
@@ -342,6 +343,53 @@ int grid_mask_cached(const grid_compiled* g, int32_t B, const grid_config* cfg_d
                      const uint16_t* stack_pool_dev, const uint64_t* stack_hash_dev, uint32_t* mask_dev,
                      uint8_t* eos_dev, int32_t* status_dev, void* workspace_dev, size_t workspace_bytes,
                      void* cache_dev, size_t cache_bytes, uint32_t cache_flags, void* stream);
+
+/* ------------------------------------------------------------ the warm path */
+/* The warm per-token path (section 4.2, the split into context-independent
+ * (CI) and context-dependent (CD) tokens; section 4.3, configuration-keyed
+ * caching; section 6.1 steps 4-5): a cache of every row's CI words -- the
+ * allowed bits of the tokens whose lexeme program from the row's scan state
+ * ends no lexeme, whose verdict therefore depends only on the scan state,
+ * the pending remainder, A(sigma) and the schema lexicon -- while the CD
+ * tokens are judged against the live stack on every call, never cached (the
+ * end-of-sequence bit is always live).  Keys, GRID_CI_* flags:
+ *  - T1 (default): Definition 5's key -- the handle's fingerprint, the scan
+ *    state, the lexicon slot, the pending remainder (empty flag, length,
+ *    first 8 bytes, lexicon node) and A(sigma);
+ *  - GRID_CI_FAMILY, the cross-family tier T2: the grammar family's
+ *    fingerprint (lexer and vocabulary, the same for every role projection of
+ *    one dialect) in place of the handle's, and the schema fingerprint of the
+ *    slot's lexicon (GRID_ART_LEX_SLOTS word 9) in place of the slot, which
+ *    scopes every entry of a lexicon-bearing producer (Remark 1); handles
+ *    of one family may share a cache;
+ *  - GRID_CI_GENN (with GRID_CI_FAMILY): the remainder in the genN scanner
+ *    normal form (p, q, v): with this library's gap-free lexers a remainder
+ *    that has accepted has p = q and v empty, so its bytes leave the key --
+ *    only under the lexicon-visibility guard (no terminal the row's lexicon
+ *    restricts is live or accepting in q); otherwise the raw remainder stays.
+ * A hit row takes its CI words from the entry (its CI classes are neither
+ * judged nor walked); a miss computes the cold mask and, with
+ * GRID_CI_INSERT, claims a slot in the prologue and publishes the row's CI
+ * words after finalize (rows that do not end with status OK release their
+ * claim).  Masks are bit-identical with and without the cache.  Entries are
+ * written once and never evicted; a probe window (8 slots) that is full leaves
+ * the row uncached.  Concurrent calls may share a cache (claims by atomic
+ * compare-and-swap, published entries only are read). */
+#define GRID_CI_LOOKUP 1u
+#define GRID_CI_INSERT 2u
+#define GRID_CI_FAMILY 4u
+#define GRID_CI_GENN 8u
+/* Device bytes of a CI-words cache of n_entries entries (a power of two); 0
+ * if n_entries is not one. */
+size_t grid_ci_cache_bytes(const grid_compiled* g, int32_t n_entries);
+/* Empties such a cache with a fill kernel, asynchronous on stream. */
+int grid_ci_cache_clear(const grid_compiled* g, void* cache_dev, size_t cache_bytes, void* stream);
+/* grid_mask with the CI-words cache (a null cache or no LOOKUP/INSERT flag is
+ * exactly grid_mask).  Arguments otherwise as grid_mask. */
+int grid_mask_warm(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                   const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev, int32_t* status_dev,
+                   void* workspace_dev, size_t workspace_bytes, void* ci_cache_dev, size_t ci_cache_bytes,
+                   uint32_t ci_flags, void* stream);
 
 /* ------------------------------------------------- rolling configuration hash */
 /* The rolling configuration hash of an LR stack (section 6.4, the audit

@@ -449,8 +449,35 @@ void add_lexicon(LexiconStore& st, const LexerDfa& dfa, const GrammarText& g, co
       for (uint32_t k = va.alias_off[u]; k < va.alias_off[u + 1]; ++k) st.token[tok_base + va.alias_ids[k]] = f;
     }
   }
+  // the schema fingerprint: FNV-1a over the restricted categories and their
+  // sorted word lists, so equal lexicons in any slot or handle share it
+  uint32_t schema_fp = 2166136261u;
+  auto mix = [&schema_fp](uint32_t v) {
+    for (int k = 0; k < 4; ++k) schema_fp = (schema_fp ^ ((v >> (8 * k)) & 0xFFu)) * 16777619u;
+  };
+  {
+    std::vector<std::pair<int, std::vector<std::string>>> by_cat;
+    for (auto& cw : cats) {
+      int t = -1;
+      for (size_t k = 0; k < g.terminals.size(); ++k)
+        if (g.terminals[k].name == cw.first) t = (int)k;
+      std::vector<std::string> ws(cw.second.begin(), cw.second.end());
+      ws.erase(std::remove(ws.begin(), ws.end(), std::string()), ws.end());
+      std::sort(ws.begin(), ws.end());
+      ws.erase(std::unique(ws.begin(), ws.end()), ws.end());
+      by_cat.push_back({term_cat[t], ws});
+    }
+    std::sort(by_cat.begin(), by_cat.end());
+    for (auto& cw : by_cat) {
+      mix(0xC0DE0000u | (uint32_t)cw.first);
+      for (auto& w : cw.second) {
+        mix((uint32_t)w.size());
+        for (unsigned char ch : w) mix(ch);
+      }
+    }
+  }
   uint32_t rec[kSlotWords] = {flags_base, hash_base, size - 1, restricted, (uint32_t)nodes.size(),
-                              pref_base,  psize - 1, stride_base, ssize - 1, 0, 0, 0};
+                              pref_base,  psize - 1, stride_base, ssize - 1, schema_fp, 0, 0};
   st.slots.insert(st.slots.end(), rec, rec + kSlotWords);
   st.n_slots += 1;
 }

@@ -80,6 +80,24 @@ extern "C" int grid_compile(const grid_compile_args* a, grid_compiled** out) {
     mix(g->vocab.spell_bytes.data(), g->vocab.spell_bytes.size());
     mix(g->vocab.alias_ids.data(), g->vocab.alias_ids.size() * 4);
     g->fingerprint = fp;
+    // the grammar family's fingerprint: what context-independent words depend
+    // on besides the allowed set, the remainder and the lexicon -- the lexer
+    // (terminal numbering, priorities, ignored and category flags) and the
+    // vocabulary, not the role projection
+    uint32_t ff = 2166136261u;
+    auto mixf = [&ff](const void* p, size_t n) {
+      const uint8_t* b = (const uint8_t*)p;
+      for (size_t i = 0; i < n; ++i) ff = (ff ^ b[i]) * 16777619u;
+    };
+    const int32_t fdims[] = {g->dfa.S, g->dfa.C, T, g->vocab.V, (int32_t)g->vocab.spell_off.size()};
+    mixf(fdims, sizeof(fdims));
+    mixf(g->dfa.next.data(), g->dfa.next.size() * 2);
+    mixf(g->dfa.accept_off.data(), g->dfa.accept_off.size() * 4);
+    mixf(g->dfa.accept_list.data(), g->dfa.accept_list.size());
+    mixf(g->term_info.data(), g->term_info.size() * 4);
+    mixf(g->vocab.spell_bytes.data(), g->vocab.spell_bytes.size());
+    mixf(g->vocab.alias_ids.data(), g->vocab.alias_ids.size() * 4);
+    g->family_fp = ff;
     *out = g.release();
     return GRID_OK;
   } catch (const Error& e) {

@@ -159,6 +159,7 @@ struct grid_compiled {
   grid::LexiconStore lex;
   grid::ClassTables classes;          // lexeme-program classes
   uint32_t fingerprint = 0;           // of the lexer, parser and vocabulary (mask-cache entries)
+  uint32_t family_fp = 0;             // of the lexer and vocabulary only (shared by every role)
   std::vector<int> term_cat;          // category index per terminal or -1
   std::vector<uint32_t> term_info;    // device word per terminal
   std::vector<int> cat_term;          // terminal id per category index

@@ -123,6 +123,11 @@ struct Tables {
   uint32_t cache_flags;       // GRID_CACHE_*
   uint32_t cache_stride;      // bytes per entry
   uint32_t fp;                // fingerprint of the compiled handle
+  uint8_t* ci_cache;          // context-independent-words cache (null: off)
+  uint32_t ci_mask;           // entries - 1
+  uint32_t ci_flags;          // GRID_CI_*
+  uint32_t ci_stride;         // bytes per entry
+  uint32_t family_fp;         // fingerprint of the lexer and vocabulary (the grammar family)
 };
 
 // ------------------------------------------------------------- mask cache
@@ -139,6 +144,19 @@ constexpr uint64_t kRollingKeyTag = 0x524F4C4C494E4748ull;  // key words of a ro
 constexpr uint32_t kRowCached = 0xCAC4;  // RowHeader::valid of a row served from the cache
 
 __host__ __device__ inline uint32_t cache_stride_of(int W) { return 64u + ((uint32_t)W * 4u + 15u) / 16u * 16u; }
+
+// Context-independent-words cache entry: a 96-byte header (state word: 0
+// empty, 1 claimed, 2 published; the key), then W words holding the allowed
+// bits of the row's context-independent tokens -- those whose lexeme program
+// from the scan state ends no lexeme, so that their verdict depends only on
+// the scan state, the pending remainder, A(sigma) and the lexicon (section
+// 4.2, CI / CD split; the end-of-sequence bit is never stored).
+constexpr int kCiKeyWords = 17;
+constexpr uint32_t kCiHeader = 96;
+__host__ __device__ inline uint32_t ci_stride_of(int W) { return kCiHeader + ((uint32_t)W * 4u + 15u) / 16u * 16u; }
+// A class whose tokens end no lexeme: byte 0 continues the pending lexeme and
+// no later byte ends one.
+__host__ __device__ inline bool ci_class(uint32_t w0) { return (w0 & (kClassEndsMask | kClassP0 | kClassWalk)) == 0u; }
 
 // One stack entry's share of the stack hash: a 64-bit mix of (position,
 // state) under a salt; the hash is the sum over the stack, so every thread
@@ -174,7 +192,9 @@ struct RowHeader {
   int32_t fstat;              // final row status (finalize)
   uint32_t cls_base, n_cls;   // the row's lexer state's class records
   uint32_t slot_id;           // the row's lexicon slot
-  uint32_t pad[16];
+  int32_t ci_hit;             // context-independent-words entry serving this row, -1 none
+  int32_t ci_claim;           // such an entry this row publishes to, -1 none
+  uint32_t pad[14];
 };
 static_assert(sizeof(RowHeader) == 320, "row header is 320 bytes");
 
@@ -919,6 +939,52 @@ __device__ inline int winner_of(const TermView& tv, const uint32_t* acc_off, con
   return -1;
 }
 
+// -------------------------------------------------- CI-words cache key
+// The key of a row's context-independent words (section 4.3): per handle
+// (T1, Definition 5's key) -- the handle's fingerprint, the scan state q, the
+// lexicon slot, the pending remainder (empty flag, length, first 8 bytes,
+// lexicon node) and A(sigma) -- or, with GRID_CI_FAMILY (the cross-family
+// tier T2), the grammar family's fingerprint (lexer and vocabulary: every
+// role projection of one dialect shares it, since projections never
+// renumber terminals) and the slot's schema fingerprint, which scopes every
+// entry of a lexicon-bearing producer (Remark 1).  With GRID_CI_GENN the T2
+// remainder is taken in the genN scanner normal form: under this build's
+// gap-free lexers a remainder that has accepted has its last accept at its
+// end, so (p, q, v) = (q, q, empty) and the bytes drop out of the key -- only
+// under the lexicon-visibility guard (no terminal the row's lexicon
+// restricts is live or accepting in q); otherwise, or while the remainder
+// has not accepted, the raw remainder stays in the key.
+__device__ inline void ci_key(const Tables& tb, const grid_config& cfg, const Slot& sl, const uint32_t (&a_sig)[8],
+                              const uint32_t* R, uint32_t (&key)[kCiKeyWords]) {
+  const bool family = (tb.ci_flags & GRID_CI_FAMILY) != 0;
+  const bool empty = (cfg.flags & 1u) != 0;
+  bool genn = false;
+  if (family && (tb.ci_flags & GRID_CI_GENN)) {
+    bool guard = true;
+    const uint32_t* lv = tb.live + (size_t)cfg.q * 8;
+    for (int w = 0; w < 8; ++w) guard = guard && (lv[w] & R[w]) == 0u;
+    const bool accepting = tb.acc_off[cfg.q + 1] > tb.acc_off[cfg.q];
+    for (uint32_t j = tb.acc_off[cfg.q]; j < tb.acc_off[cfg.q + 1]; ++j) guard = guard && !bit_of(R, tb.acc_list[j]);
+    genn = guard && (accepting || empty);
+  }
+  const uint32_t rem_lo = (uint32_t)cfg.rem_head[0] | (uint32_t)cfg.rem_head[1] << 8 |
+                          (uint32_t)cfg.rem_head[2] << 16 | (uint32_t)cfg.rem_head[3] << 24;
+  const uint32_t rem_hi = (uint32_t)cfg.rem_head[4] | (uint32_t)cfg.rem_head[5] << 8 |
+                          (uint32_t)cfg.rem_head[6] << 16 | (uint32_t)cfg.rem_head[7] << 24;
+  key[0] = family ? (genn ? 3u : 2u) : 1u;
+  key[1] = family ? tb.family_fp : tb.fp;
+  key[2] = cfg.q;
+  key[3] = family ? tb.lex_slots[(size_t)cfg.slot * kSlotWords + 9] : (uint32_t)cfg.slot;
+  key[4] = empty ? 1u : 0u;
+  key[5] = genn || empty ? 0u : cfg.rem_len;
+  key[6] = genn || empty ? 0u : rem_lo;
+  key[7] = genn || empty ? 0u : rem_hi;
+  key[8] = genn || empty ? 0u : cfg.lexnode;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) key[9 + k] = a_sig[k];
+  (void)sl;
+}
+
 // ---------------------------------------------------------------- prologue
 // One workgroup per row.  Phase 1: every terminal's reduce chain and shift
 // from sigma (A(sigma) is the set that shifted) and, for an allowed terminal,
@@ -1020,6 +1086,8 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
       hdr->wstat = 0;
       hdr->nonempty = 0;
       hdr->cache_slot = -1;
+      hdr->ci_hit = -1;
+      hdr->ci_claim = -1;
       if (eos_out) eos_out[row] = 0;
     }
     return;
@@ -1097,6 +1165,8 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
       hdr->wstat = 0;
       hdr->nonempty = 1;
       hdr->cache_slot = -1;
+      hdr->ci_hit = -1;
+      hdr->ci_claim = -1;
       if (eos_out) eos_out[row] = (uint8_t)e->eos;
     }
     return;
@@ -1269,6 +1339,42 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     hdr->cls_base = tb.coff[cfg.q];
     hdr->n_cls = tb.coff[cfg.q + 1] - tb.coff[cfg.q];
     hdr->pstat = overflow ? GRID_ROW_OVERFLOW : GRID_ROW_OK;
+    // context-independent words: probe the row's key; a published entry
+    // serves the row's CI tokens, an empty slot on the way is claimed
+    int ci_hit = -1, ci_claim = -1;
+    if (tb.ci_cache && !overflow) {
+      uint32_t a_sig[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) a_sig[k] = A[k];
+      uint32_t key[kCiKeyWords];
+      ci_key(tb, cfg, sl, a_sig, R, key);
+      uint64_t home = 0x8F1BBCDC2C2D6A1Bull;
+      for (int k = 0; k < kCiKeyWords; ++k) home = stack_mix((uint32_t)k, key[k], home);
+      for (int pr = 0; pr < kCacheProbes; ++pr) {
+        const uint32_t idx = (uint32_t)(home + (uint64_t)pr) & tb.ci_mask;
+        uint32_t* e = (uint32_t*)(tb.ci_cache + (size_t)idx * tb.ci_stride);
+        const uint32_t st = __hip_atomic_load(e, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+        if (st == 2u) {
+          bool same = true;
+          for (int k = 0; k < kCiKeyWords; ++k) same = same && e[1 + k] == key[k];
+          if (same && (tb.ci_flags & GRID_CI_LOOKUP)) {
+            ci_hit = (int)idx;
+            break;
+          }
+          continue;
+        }
+        if (st == 0u) {
+          if (!(tb.ci_flags & GRID_CI_INSERT)) break;
+          if (atomicCAS(e, 0u, 1u) == 0u) {
+            for (int k = 0; k < kCiKeyWords; ++k) e[1 + k] = key[k];
+            ci_claim = (int)idx;
+            break;
+          }
+        }
+      }
+    }
+    hdr->ci_hit = ci_hit;
+    hdr->ci_claim = ci_claim;
     hdr->valid = kRowValid;
   }
 }
@@ -1747,7 +1853,10 @@ __global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __r
     if (c < n) {
       const uint4 rec = c0 == blockIdx.y * (uint32_t)kBlock ? rec0 : tb.crec[h.cls_base + c];
       LexOpen lex;
-      code = class_verdict<MW>(h, I_s, live_s, 8, tinfo_s, acc_off_s, acc_list_s, a2_s, 8, rec, lex);
+      if (h.ci_hit >= 0 && ci_class(rec.x))  // served by the row's cached context-independent words
+        code = kVerdictReject;
+      else
+        code = class_verdict<MW>(h, I_s, live_s, 8, tinfo_s, acc_off_s, acc_list_s, a2_s, 8, rec, lex);
       if (code == kVerdictLexicon)
         vr[c] = (uint8_t)class_shortcut<MW>(h, I_s, live_s, tinfo_s, acc_off_s, acc_list_s, a2_s, rec);
     }
@@ -1804,6 +1913,9 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
   const RowLayout RL = row_layout(tb);
   const uint32_t q = hdr->q;
   const int eos = hdr->eos_ok ? tb.eos_id : -1;
+  // a row served by cached context-independent words ORs them into its words
+  const int ci = hdr->ci_hit;
+  const uint32_t* ciw = ci >= 0 ? (const uint32_t*)(tb.ci_cache + (size_t)ci * tb.ci_stride + kCiHeader) : nullptr;
   // the row's 2-bit class codes are read where the class map points (an
   // L2-resident gather: staging all of them in LDS per workgroup cost more)
   const uint32_t* vg = (const uint32_t*)(rw + RL.vcode);
@@ -1853,8 +1965,10 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
       if (no) cd = (sc[j] >> 5) & 3u;
     }
     const uint64_t al = __ballot(cd == kVerdictAllow || id == eos);
-    any = any || al != 0;
-    if (lane < 2 && 2 * c + lane < tb.W) mrow[2 * c + lane] = (uint32_t)(al >> (32 * lane));
+    uint64_t cw = 0;
+    if (ciw) cw = (uint64_t)ciw[2 * c] | (2 * c + 1 < tb.W ? (uint64_t)ciw[2 * c + 1] << 32 : 0ull);
+    any = any || (al | cw) != 0;
+    if (lane < 2 && 2 * c + lane < tb.W) mrow[2 * c + lane] = (uint32_t)((al | cw) >> (32 * lane));
     if (cd >= kVerdictWalk && id < tb.V) resu[j] = (uint32_t)id;
     code[j] = cd;
   }
@@ -2453,6 +2567,41 @@ __global__ __launch_bounds__(kBlock) void cache_publish_kernel(Tables tb, const 
   }
 }
 
+// Context-independent words write-back: every row that claimed an entry in
+// the prologue and ended with status OK stores the allowed bits of its
+// context-independent tokens (from its finished mask; the end-of-sequence
+// bit left out); one wave per 64 ids, grid (chunk groups, row).
+__global__ __launch_bounds__(kBlock) void ci_publish_kernel(Tables tb, const uint32_t* __restrict__ mask,
+                                                            const uint8_t* __restrict__ ws, size_t rbytes) {
+  const int row = (int)blockIdx.y, lane = (int)(threadIdx.x & 63u);
+  const RowHeader* hdr = (const RowHeader*)(ws + kWsHead + (size_t)row * rbytes);
+  if (hdr->valid != kRowValid || hdr->ci_claim < 0 || hdr->fstat != GRID_ROW_OK) return;  // uniform
+  const int c = (int)(blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6));
+  if (c * 64 >= tb.V) return;  // uniform across the wave
+  const int id = c * 64 + lane;
+  const uint32_t* mrow = mask + (size_t)row * tb.W;
+  bool keep = false;
+  if (id < tb.V && id != tb.eos_id) {
+    const uint32_t cls = tb.cmap[(size_t)hdr->q * tb.V + id];
+    keep = ci_class(tb.crec[hdr->cls_base + cls].x) && ((mrow[id >> 5] >> (id & 31)) & 1u);
+  }
+  const uint64_t b = __ballot(keep);
+  uint32_t* dst = (uint32_t*)(tb.ci_cache + (size_t)hdr->ci_claim * tb.ci_stride + kCiHeader);
+  if (lane < 2 && 2 * c + lane < tb.W) dst[2 * c + lane] = (uint32_t)(b >> (32 * lane));
+}
+
+// Publishes the entries written above (a device-scope fence orders the words
+// before the state word); a claim whose row did not end OK is released.
+__global__ __launch_bounds__(64) void ci_seal_kernel(Tables tb, const uint8_t* __restrict__ ws, size_t rbytes, int B) {
+  const int row = (int)(blockIdx.x * 64u + threadIdx.x);
+  if (row >= B) return;
+  const RowHeader* hdr = (const RowHeader*)(ws + kWsHead + (size_t)row * rbytes);
+  if (hdr->valid != kRowValid || hdr->ci_claim < 0) return;
+  uint32_t* e = (uint32_t*)(tb.ci_cache + (size_t)hdr->ci_claim * tb.ci_stride);
+  __threadfence();
+  __hip_atomic_store(e, hdr->fstat == GRID_ROW_OK ? 2u : 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ------------------------------------------------------------------- apply
 // Each thread covers 8 consecutive logits of one row; the mask byte for them
 // comes from one word.  Fully masked groups take one or two 16-byte stores.
@@ -2918,6 +3067,11 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
     hipLaunchKernelGGL(finalize_kernel<MW>, dim3(B), dim3(kBlock), 0, s, tb, cfg_dev, pool, mask, ws, rb, status);
     if (tb.cache && (tb.cache_flags & GRID_CACHE_INSERT))
       hipLaunchKernelGGL(cache_publish_kernel, dim3(B), dim3(kBlock), 0, s, tb, mask, ws, rb);
+    if (tb.ci_cache && (tb.ci_flags & GRID_CI_INSERT)) {
+      const int groups = ((tb.V + 63) / 64 + kBlock / 64 - 1) / (kBlock / 64);
+      hipLaunchKernelGGL(ci_publish_kernel, dim3((unsigned)groups, (unsigned)B), dim3(kBlock), 0, s, tb, mask, ws, rb);
+      hipLaunchKernelGGL(ci_seal_kernel, dim3((unsigned)((B + 63) / 64)), dim3(64), 0, s, tb, ws, rb, B);
+    }
   }
   return GRID_OK;
 }
@@ -3009,10 +3163,15 @@ static int bind_tables(const grid_compiled* g, Tables& tb) {
 static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_dev, const uint16_t* stack_pool_dev,
                      uint32_t* mask_dev, uint8_t* eos_dev, int32_t* status_dev, void* workspace_dev,
                      size_t workspace_bytes, void* cache_dev, size_t cache_bytes, uint32_t cache_flags,
-                     uint32_t phases, void* stream, const uint64_t* stack_hash_dev = nullptr) {
+                     uint32_t phases, void* stream, const uint64_t* stack_hash_dev = nullptr,
+                     void* ci_dev = nullptr, size_t ci_bytes = 0, uint32_t ci_flags = 0) {
   clear_error();
   if (phases & ~GRID_PHASE_ALL) return fail(GRID_E_ARG, "grid_mask: unknown phase bits");
   if (cache_flags & ~(GRID_CACHE_LOOKUP | GRID_CACHE_INSERT)) return fail(GRID_E_ARG, "grid_mask: unknown cache flags");
+  if (ci_flags & ~(GRID_CI_LOOKUP | GRID_CI_INSERT | GRID_CI_FAMILY | GRID_CI_GENN))
+    return fail(GRID_E_ARG, "grid_mask_warm: unknown flags");
+  if ((ci_flags & GRID_CI_GENN) && !(ci_flags & GRID_CI_FAMILY))
+    return fail(GRID_E_ARG, "grid_mask_warm: the genN normal form belongs to the cross-family tier");
   if (!g || B <= 0 || B > 65535 || !cfg_dev || !stack_pool_dev || !mask_dev || !workspace_dev)
     return fail(GRID_E_ARG, "grid_mask: null pointer or batch size out of range");
   const size_t rb = row_bytes(g);
@@ -3035,6 +3194,20 @@ static int mask_call(const grid_compiled* g, int32_t B, const grid_config* cfg_d
     tb.cache_mask = (uint32_t)(n - 1);
     tb.cache_flags = cache_flags;
     tb.stack_hash = stack_hash_dev;
+  }
+  tb.ci_cache = nullptr;
+  tb.ci_mask = 0;
+  tb.ci_flags = 0;
+  tb.ci_stride = ci_stride_of(tb.W);
+  tb.family_fp = g->family_fp;
+  if (ci_dev && (ci_flags & (GRID_CI_LOOKUP | GRID_CI_INSERT))) {
+    const size_t n = ci_bytes / tb.ci_stride;
+    if (n == 0 || (n & (n - 1)) != 0 || n > 0x80000000ull || n * tb.ci_stride != ci_bytes)
+      return fail(GRID_E_ARG, "grid_mask_warm: cache size is not grid_ci_cache_bytes of a power of two");
+    if (((uintptr_t)ci_dev & 15) != 0) return fail(GRID_E_ARG, "grid_mask_warm: cache not 16-byte aligned");
+    tb.ci_cache = (uint8_t*)ci_dev;
+    tb.ci_mask = (uint32_t)(n - 1);
+    tb.ci_flags = ci_flags;
   }
   const int mw = tb.tw;
   const ResLds WL = res_lds(tb, mw, B);
@@ -3210,6 +3383,34 @@ static int accept_call(const grid_compiled* g, int32_t B, const grid_config* cfg
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_accept launch: ") + hipGetErrorString(e));
   return GRID_OK;
+}
+
+extern "C" size_t grid_ci_cache_bytes(const grid_compiled* g, int32_t n_entries) {
+  if (!g || n_entries < 1 || (n_entries & (n_entries - 1)) != 0) return 0;
+  return (size_t)n_entries * ci_stride_of((g->vocab.V + 31) / 32);
+}
+
+extern "C" int grid_ci_cache_clear(const grid_compiled* g, void* cache_dev, size_t cache_bytes, void* stream) {
+  clear_error();
+  if (!g || !cache_dev) return fail(GRID_E_ARG, "grid_ci_cache_clear: null argument");
+  const uint32_t stride = ci_stride_of((g->vocab.V + 31) / 32);
+  const size_t n = cache_bytes / stride;
+  if (n == 0 || (n & (n - 1)) != 0 || n > 0x80000000ull || n * stride != cache_bytes)
+    return fail(GRID_E_ARG, "grid_ci_cache_clear: cache size is not grid_ci_cache_bytes of a power of two");
+  const int blocks = (int)std::min<size_t>((n + kBlock - 1) / kBlock, 1024);
+  hipLaunchKernelGGL(cache_clear_kernel, dim3(blocks), dim3(kBlock), 0, (hipStream_t)stream, (uint8_t*)cache_dev,
+                     (uint32_t)n, stride);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_ci_cache_clear launch: ") + hipGetErrorString(e));
+  return GRID_OK;
+}
+
+extern "C" int grid_mask_warm(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,
+                              const uint16_t* stack_pool_dev, uint32_t* mask_dev, uint8_t* eos_dev, int32_t* status_dev,
+                              void* workspace_dev, size_t workspace_bytes, void* ci_cache_dev, size_t ci_cache_bytes,
+                              uint32_t ci_flags, void* stream) {
+  return mask_call(g, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, workspace_dev, workspace_bytes,
+                   nullptr, 0, 0, GRID_PHASE_ALL, stream, nullptr, ci_cache_dev, ci_cache_bytes, ci_flags);
 }
 
 extern "C" int grid_accept(const grid_compiled* g, int32_t B, const grid_config* cfg_dev,

@@ -43,7 +43,8 @@ EXPORTS = ["grid_compile", "grid_free", "grid_last_error", "grid_info", "grid_ad
            "grid_mask_workspace_bytes", "grid_mask", "grid_mask_phases", "grid_apply",
            "grid_cache_bytes", "grid_cache_clear", "grid_mask_cached", "grid_accept",
            "grid_mask_noalloc_max_bytes", "grid_mask_noalloc", "grid_stack_hash", "grid_stack_hash_host",
-           "grid_accept_inplace"]
+           "grid_accept_inplace", "grid_ci_cache_bytes", "grid_ci_cache_clear", "grid_mask_warm"]
+CI_LOOKUP, CI_INSERT, CI_FAMILY, CI_GENN = 1, 2, 4, 8
 PHASE_PROLOGUE, PHASE_WALK, PHASE_RESIDUE, PHASE_FINALIZE, PHASE_ALL = 1, 2, 4, 8, 15
 
 
@@ -104,6 +105,10 @@ def lib():
         L.grid_stack_hash.argtypes = [vp, i32, vp, vp, vp, vp]
         L.grid_stack_hash_host.argtypes = [vp, vp, ctypes.c_uint32, vp]
         L.grid_accept_inplace.argtypes = [vp, i32, vp, vp, vp, ctypes.c_uint32, vp, vp, vp]
+        L.grid_ci_cache_bytes.argtypes = [vp, i32]
+        L.grid_ci_cache_bytes.restype = sz
+        L.grid_ci_cache_clear.argtypes = [vp, vp, sz, vp]
+        L.grid_mask_warm.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, sz, vp, sz, ctypes.c_uint32, vp]
         L.grid_cache_bytes.argtypes = [vp, i32]
         L.grid_cache_bytes.restype = sz
         L.grid_cache_clear.argtypes = [vp, vp, sz, vp]
@@ -304,6 +309,38 @@ class Grid:
         c = torch.empty(self.cache_bytes(n_entries), dtype=torch.uint8, device=device or self.device)
         self.clear_cache(c, stream)
         return c
+
+    def new_ci_cache(self, n_entries, device=None, stream=None):
+        """A cleared cache of context-independent words (uint8 device tensor)."""
+        import torch
+        n = lib().grid_ci_cache_bytes(self.h, n_entries)
+        if n == 0:
+            raise ValueError("n_entries must be a power of two")
+        c = torch.empty(n, dtype=torch.uint8, device=device or self.device)
+        _check(lib().grid_ci_cache_clear(self.h, ctypes.c_void_p(c.data_ptr()), c.numel(), _stream_handle(stream)))
+        return c
+
+    def mask_warm(self, cfg_dev, pool_dev, B, ci_cache, flags=1 | 2, out=None, eos=None, status=None,
+                  workspace=None, stream=None):
+        """grid_mask_warm: the mask of B rows with the CI-words cache (CI_* flags)."""
+        import torch
+        dev = cfg_dev.device
+        if out is None:
+            out = torch.empty((B, self.W), dtype=torch.int32, device=dev)
+        if eos is None:
+            eos = torch.empty(B, dtype=torch.uint8, device=dev)
+        if status is None:
+            status = torch.empty(B, dtype=torch.int32, device=dev)
+        if workspace is None:
+            workspace = self.new_workspace(B, dev)
+        assert cfg_dev.numel() >= 32 * B and out.numel() >= B * self.W and out.is_contiguous()
+        _check(lib().grid_mask_warm(self.h, B, ctypes.c_void_p(cfg_dev.data_ptr()),
+                                    ctypes.c_void_p(pool_dev.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                                    ctypes.c_void_p(eos.data_ptr()), ctypes.c_void_p(status.data_ptr()),
+                                    ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                    ctypes.c_void_p(ci_cache.data_ptr()), ci_cache.numel(), flags,
+                                    _stream_handle(stream)))
+        return out, eos, status
 
     def clear_cache(self, cache, stream=None):
         _check(lib().grid_cache_clear(self.h, ctypes.c_void_p(cache.data_ptr()), cache.numel(),
