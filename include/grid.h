@@ -449,6 +449,51 @@ int grid_accept_inplace(const grid_compiled* g, int32_t B, grid_config* cfg_dev,
                         uint64_t* stack_hash_dev, uint32_t stack_cap, const int32_t* token_dev,
                         int32_t* status_dev, void* stream);
 
+/* ---------------------------------------------------------------- termination */
+/* Termination machinery, mode 1 (section 5, Proposition 9; section 6.1 step 3),
+ * host: a legal completion of the viable prefix w[0..n) on lexicon slot
+ * `slot`, as vocabulary token ids in out_tokens[0 .. *out_n) -- w followed by
+ * their bytes is a sentence of L, so the end-of-sequence token may follow
+ * it, and every intermediate output is a viable prefix.  The pending lexeme
+ * is finished by the shortest extension that a winning terminal accepts and a
+ * whitespace byte ends; then a best-first search over terminal sequences on
+ * the LR stack writes, per terminal, a separator and the shortest spelling
+ * that wins contextual resolution there (literal text, shortest regex
+ * string, or shortest word of its category in the slot's lexicon); the bytes
+ * are tokenized by greedy longest match and the result is verified to be in
+ * L before it is returned.  *out_n is the prefix's token-denominated reserve:
+ * a decode loop with budget b tokens writes this completion and the
+ * end-of-sequence token once b <= *out_n + safety.  The search is best-first
+ * under a per-state estimate (the fewest terminals finishing a kernel item),
+ * so the completion is short but not proven shortest.  GRID_E_NOT_VIABLE for
+ * a prefix outside Prefix(L); GRID_E_CAPACITY when the completion needs more
+ * than max_tokens tokens (*out_n is then its length) or none is found within
+ * the search budget. */
+int grid_complete(const grid_compiled* g, int32_t slot, const uint8_t* w, size_t n, int32_t max_tokens,
+                  int32_t* out_tokens, int32_t* out_n);
+
+/* Jump-forward (section 6.1 step 6), device: the B configurations
+ * cfg_dev[b] (stacks at stack_pool_dev[b * stack_cap ..], the layout of
+ * grid_accept_inplace) are extended by their maximal forced span, at most
+ * max_len tokens long.  Step i computes the exact mask of every row; a row
+ * whose mask allows exactly one token (the end-of-sequence token included,
+ * when it is the only one) takes that token as span_dev[b * max_len + i] and
+ * is advanced in place by it (stack_hash_dev kept as grid_accept_inplace
+ * does, or NULL); any other row gets -1 there and keeps its configuration,
+ * and so do the later steps of a row that stopped (after -1 or after the
+ * end-of-sequence token).  span_len_dev[b] is the number of forced tokens.
+ * On return mask_dev / eos_dev / status_dev ([B, W] u32, [B] u8, [B] i32, as
+ * grid_mask writes them) hold the mask of the rows' final configurations:
+ * a row with span_len < max_len there allows several tokens (or is a row
+ * that grid_mask reports with a status other than GRID_ROW_OK).  workspace
+ * as grid_mask.  max_len + 1 mask calls and max_len advances are enqueued
+ * on stream, nothing is synchronized; GRID_E_ARG for null pointers, B < 1,
+ * max_len < 1 or stack_cap < 2. */
+int grid_forced_span(const grid_compiled* g, int32_t B, grid_config* cfg_dev, uint16_t* stack_pool_dev,
+                     uint64_t* stack_hash_dev, uint32_t stack_cap, int32_t max_len, int32_t* span_dev,
+                     int32_t* span_len_dev, uint32_t* mask_dev, uint8_t* eos_dev, int32_t* status_dev,
+                     void* workspace_dev, size_t workspace_bytes, void* stream);
+
 /* -------------------------------------------------------------------- apply */
 #define GRID_DTYPE_F32 0
 #define GRID_DTYPE_BF16 1

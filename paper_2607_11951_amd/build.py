@@ -8,7 +8,7 @@ PKG = Path(__file__).resolve().parent
 CSRC = PKG / "csrc"
 OUT = PKG / "libgrid.so"
 BUILD = PKG / "_build"
-HOST_SOURCES = ["grammar.cpp", "lexer.cpp", "parser.cpp", "artifacts.cpp", "advance.cpp", "capi.cpp"]
+HOST_SOURCES = ["grammar.cpp", "lexer.cpp", "parser.cpp", "artifacts.cpp", "advance.cpp", "complete.cpp", "capi.cpp"]
 HIP_SOURCES = ["kernels.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

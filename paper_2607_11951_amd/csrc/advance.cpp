@@ -15,13 +15,10 @@
 #include "lexhash.h"
 
 namespace grid {
-namespace {
-
-enum SimResult { kSimError = 0, kSimShift = 1, kSimAccept = 2 };
 
 // Reduce chain for terminal t on a copy of the stack; with commit, the real
 // stack is reduced and t shifted.
-int simulate(const Parser& P, std::vector<uint16_t>& stack, int t, bool commit) {
+int lr_simulate(const Parser& P, std::vector<uint16_t>& stack, int t, bool commit) {
   std::vector<uint16_t> scratch;
   std::vector<uint16_t>& st = commit ? stack : (scratch = stack);
   for (int guard = 0; guard < 1 << 20; ++guard) {
@@ -43,7 +40,6 @@ int simulate(const Parser& P, std::vector<uint16_t>& stack, int t, bool commit) 
   return kSimError;
 }
 
-}  // namespace
 }  // namespace grid
 
 using namespace grid;
@@ -66,7 +62,7 @@ int host_config_from_prefix(const grid_compiled* g, int slot, const uint8_t* w, 
     if (c < 0 || !(restricted >> c & 1)) return true;
     return (L.node_flags(slot, node) >> c & 1) != 0;
   };
-  auto allowed = [&](int t) { return ignored(t) || simulate(P, stack, t, false) == 1; };
+  auto allowed = [&](int t) { return ignored(t) || lr_simulate(P, stack, t, false) == 1; };
 
   stack.assign(1, 0);
   int q = kStart;
@@ -92,7 +88,7 @@ int host_config_from_prefix(const grid_compiled* g, int slot, const uint8_t* w, 
       }
     }
     if (win < 0) return GRID_E_NOT_VIABLE;
-    if (!ignored(win) && simulate(P, stack, win, true) != 1) return GRID_E_NOT_VIABLE;
+    if (!ignored(win) && lr_simulate(P, stack, win, true) != 1) return GRID_E_NOT_VIABLE;
     q = D.step(kStart, b);
     if (q == kDead) return GRID_E_NOT_VIABLE;
     lex = L.child(slot, 0, b);

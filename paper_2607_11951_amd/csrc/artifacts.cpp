@@ -479,6 +479,21 @@ void add_lexicon(LexiconStore& st, const LexerDfa& dfa, const GrammarText& g, co
   uint32_t rec[kSlotWords] = {flags_base, hash_base, size - 1, restricted, (uint32_t)nodes.size(),
                               pref_base,  psize - 1, stride_base, ssize - 1, schema_fp, 0, 0};
   st.slots.insert(st.slots.end(), rec, rec + kSlotWords);
+  st.shortest.resize((size_t)(st.n_slots + 1) * kMaxCategories);
+  for (auto& cw : cats) {
+    int t = -1;
+    for (size_t k = 0; k < g.terminals.size(); ++k)
+      if (g.terminals[k].name == cw.first) t = (int)k;
+    std::vector<std::string> ws;
+    for (const std::string& x : cw.second)
+      if (!x.empty()) ws.push_back(x);
+    std::sort(ws.begin(), ws.end(), [](const std::string& a, const std::string& b) {
+      return a.size() != b.size() ? a.size() < b.size() : a < b;
+    });
+    ws.erase(std::unique(ws.begin(), ws.end()), ws.end());
+    if (ws.size() > 6) ws.resize(6);
+    st.shortest[(size_t)st.n_slots * kMaxCategories + (size_t)term_cat[t]] = ws;
+  }
   st.n_slots += 1;
 }
 

@@ -4,6 +4,7 @@
 #include <cstdint>
 #include <map>
 #include <memory>
+#include <mutex>
 #include <stdexcept>
 #include <string>
 #include <vector>
@@ -93,11 +94,19 @@ struct Parser {
   // accessing symbol of each LR state: terminal id, or kSymNonterminal |
   // nonterminal index; kNoSymbol for the initial state
   std::vector<uint32_t> state_sym;
+  // fewest terminals that finish one kernel item of each state (completion search)
+  std::vector<uint16_t> complete_est;
   uint16_t act(int s, int t) const { return action[(size_t)s * (T + 1) + t]; }
   uint16_t gto(int s, int a) const { return go[(size_t)s * N + a]; }
 };
 
 Parser build_parser(const GrammarText& g, const std::vector<std::string>& drop);
+
+// Host LR simulation of terminal t (the end of input is t = T) on the stack:
+// its reduce chain, then the shift; with commit the stack is changed, else a
+// copy is used.  kSimShift, kSimAccept or kSimError.
+enum SimResult { kSimError = 0, kSimShift = 1, kSimAccept = 2 };
+int lr_simulate(const Parser& P, std::vector<uint16_t>& stack, int t, bool commit);
 
 // ---- vocabulary
 struct VocabArtifacts {
@@ -143,6 +152,13 @@ struct LexiconStore {
   uint32_t child(int slot, uint32_t node, uint8_t b) const;
   uint16_t node_flags(int slot, uint32_t node) const;
   uint32_t restricted(int slot) const { return slots[(size_t)slot * kSlotWords + 3]; }
+  // the shortest words of each category of each slot (completion spellings)
+  std::vector<std::vector<std::string>> shortest;  // [slot * kMaxCategories + category]
+  const std::vector<std::string>& short_words(int slot, int cat) const {
+    static const std::vector<std::string> none;
+    const size_t i = (size_t)slot * kMaxCategories + (size_t)cat;
+    return cat >= 0 && i < shortest.size() ? shortest[i] : none;
+  }
 };
 
 void add_lexicon(LexiconStore& store, const LexerDfa& dfa, const GrammarText& g, const VocabArtifacts& va,
@@ -163,6 +179,8 @@ struct grid_compiled {
   std::vector<int> term_cat;          // category index per terminal or -1
   std::vector<uint32_t> term_info;    // device word per terminal
   std::vector<int> cat_term;          // terminal id per category index
+  std::mutex aux_mu;                  // guards the tables below, built on first use
+  std::shared_ptr<void> writer;       // completion-writer tables (complete.cpp)
   void* dev[GRID_ART_COUNT] = {};
   size_t dev_bytes[GRID_ART_COUNT] = {};
 };

@@ -2859,13 +2859,14 @@ template <int MW>
 __global__ __launch_bounds__(kBlock) void accept_kernel(Tables tb, const grid_config* cfgs, const uint16_t* pool,
                                                         const int32_t* __restrict__ tokens, grid_config* cfg_out,
                                                         uint16_t* pool_out, uint64_t* hash, uint32_t cap,
-                                                        int32_t* status, int use_lds, int use_lex, int inplace) {
+                                                        int32_t* status, int use_lds, int use_lex, int inplace,
+                                                        int tok_stride) {
   extern __shared__ __align__(16) uint8_t alds[];
   __shared__ int s_st, s_bad;
   __shared__ uint32_t s_d, s_lo;
   const int row = (int)blockIdx.x, tid = (int)threadIdx.x;
   const grid_config cfg = cfgs[row];
-  const int tok = tokens[row];
+  const int tok = tokens[(size_t)row * tok_stride];
   const uint32_t d0 = cfg.stk_depth;
   uint16_t* out_stk = pool_out + (size_t)row * cap;
   const bool copyable = d0 >= 1 && d0 <= cap && (!inplace || cfg.stk_off == (uint32_t)row * cap);  // uniform
@@ -3356,7 +3357,7 @@ extern "C" int grid_cache_clear(const grid_compiled* g, void* cache_dev, size_t 
 
 static int accept_call(const grid_compiled* g, int32_t B, const grid_config* cfg_dev, const uint16_t* stack_pool_dev,
                        const int32_t* token_dev, grid_config* cfg_out_dev, uint16_t* stack_out_dev, uint64_t* hash_dev,
-                       uint32_t stack_cap, int32_t* status_dev, int inplace, void* stream) {
+                       uint32_t stack_cap, int32_t* status_dev, int inplace, void* stream, int tok_stride = 1) {
   Tables tb;
   const int rc = bind_tables(g, tb);
   if (rc != GRID_OK) return rc;
@@ -3373,13 +3374,13 @@ static int accept_call(const grid_compiled* g, int32_t B, const grid_config* cfg
   const dim3 grid((unsigned)B), block(kBlock);
   if (tb.tw == 2)
     hipLaunchKernelGGL(accept_kernel<2>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, hash_dev, stack_cap, status_dev, use_lds, use_lex, inplace);
+                       stack_out_dev, hash_dev, stack_cap, status_dev, use_lds, use_lex, inplace, tok_stride);
   else if (tb.tw == 4)
     hipLaunchKernelGGL(accept_kernel<4>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, hash_dev, stack_cap, status_dev, use_lds, use_lex, inplace);
+                       stack_out_dev, hash_dev, stack_cap, status_dev, use_lds, use_lex, inplace, tok_stride);
   else
     hipLaunchKernelGGL(accept_kernel<8>, grid, block, lds, s, tb, cfg_dev, stack_pool_dev, token_dev, cfg_out_dev,
-                       stack_out_dev, hash_dev, stack_cap, status_dev, use_lds, use_lex, inplace);
+                       stack_out_dev, hash_dev, stack_cap, status_dev, use_lds, use_lex, inplace, tok_stride);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_accept launch: ") + hipGetErrorString(e));
   return GRID_OK;
@@ -3431,6 +3432,68 @@ extern "C" int grid_accept_inplace(const grid_compiled* g, int32_t B, grid_confi
     return fail(GRID_E_ARG, "grid_accept_inplace: null pointer or bad size");
   return accept_call(g, B, cfg_dev, stack_pool_dev, token_dev, cfg_dev, stack_pool_dev, stack_hash_dev, stack_cap,
                      status_dev, 1, stream);
+}
+
+// Jump-forward step i (section 6.1 step 6): a row whose mask allows exactly
+// one token (the end-of-sequence token counts when its bit is set) takes it
+// as span[row][i]; any other row, a row whose mask call did not end OK, and a
+// row whose span already stopped (a non-forced step, or the end-of-sequence
+// token) gets -1.  span_len[row] counts the forced tokens.
+__global__ __launch_bounds__(kBlock) void singleton_kernel(const uint32_t* __restrict__ mask,
+                                                           const int32_t* __restrict__ status, int32_t* span,
+                                                           int32_t* span_len, int W, int max_len, int i, int eos_id) {
+  const int row = (int)blockIdx.x, tid = (int)threadIdx.x;
+  __shared__ int count, word;
+  if (tid == 0) {
+    count = 0;
+    word = -1;
+  }
+  __syncthreads();
+  const uint32_t* m = mask + (size_t)row * W;
+  int c = 0, wd = -1;
+  for (int w = tid; w < W; w += kBlock) {
+    const int k = __popc(m[w]);
+    c += k;
+    if (k) wd = w;
+  }
+  if (c) atomicAdd(&count, c);
+  if (wd >= 0) atomicMax(&word, wd);
+  __syncthreads();
+  if (tid != 0) return;
+  int32_t* sp = span + (size_t)row * max_len;
+  bool open = i == 0 || (sp[i - 1] >= 0 && sp[i - 1] != eos_id);
+  if (i == 0) span_len[row] = 0;
+  int tok = -1;
+  if (open && count == 1 && (!status || status[row] == GRID_ROW_OK)) tok = word * 32 + __ffs((int)m[word]) - 1;
+  sp[i] = tok;
+  if (tok >= 0) span_len[row] = i + 1;
+}
+
+extern "C" int grid_forced_span(const grid_compiled* g, int32_t B, grid_config* cfg_dev, uint16_t* stack_pool_dev,
+                                uint64_t* stack_hash_dev, uint32_t stack_cap, int32_t max_len, int32_t* span_dev,
+                                int32_t* span_len_dev, uint32_t* mask_dev, uint8_t* eos_dev, int32_t* status_dev,
+                                void* workspace_dev, size_t workspace_bytes, void* stream) {
+  clear_error();
+  if (!g || B <= 0 || !cfg_dev || !stack_pool_dev || !span_dev || !span_len_dev || !mask_dev || !status_dev ||
+      max_len < 1 || stack_cap < 2)
+    return fail(GRID_E_ARG, "grid_forced_span: null pointer or bad size");
+  const int W = (g->vocab.V + 31) / 32;
+  hipStream_t s = (hipStream_t)stream;
+  for (int i = 0; i <= max_len; ++i) {
+    int rc = mask_call(g, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, workspace_dev, workspace_bytes,
+                       nullptr, 0, 0, GRID_PHASE_ALL, stream);
+    if (rc != GRID_OK) return rc;
+    if (i == max_len) break;  // the mask of the final configurations
+    hipLaunchKernelGGL(singleton_kernel, dim3((unsigned)B), dim3(kBlock), 0, s, mask_dev, status_dev, span_dev,
+                       span_len_dev, W, max_len, i, g->vocab.eos_id);
+    // rows with -1 are left as they are (reported as bad configurations to no one)
+    rc = accept_call(g, B, cfg_dev, stack_pool_dev, span_dev + i, cfg_dev, stack_pool_dev, stack_hash_dev, stack_cap,
+                     nullptr, 1, stream, max_len);
+    if (rc != GRID_OK) return rc;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_forced_span launch: ") + hipGetErrorString(e));
+  return GRID_OK;
 }
 
 extern "C" int grid_apply(const uint32_t* mask_dev, void* logits_dev, int32_t dtype, int32_t B, int32_t V,

@@ -292,6 +292,37 @@ Parser build_parser(const GrammarText& g, const std::vector<std::string>& drop) 
     throw Error(GRID_E_LALR_CONFLICT, "LALR(1) conflict in state " + std::to_string(s) + " on " +
                                           sym_name(t) + ": " + describe(a) + " vs " + describe(b));
   };
+  // completion estimate of every state: the fewest terminals that finish one
+  // of its kernel items (the shortest terminal yield of what follows the dot;
+  // nonterminals by the least fixpoint of their shortest derivations)
+  {
+    std::vector<int> minlen(G.N, 1 << 20);
+    for (bool ch = true; ch;) {
+      ch = false;
+      for (int p = 0; p < P; ++p) {
+        long sum = 0;
+        for (int x : G.rhs[p]) sum += G.is_nt(x) ? minlen[x - T] : 1;
+        if (sum < minlen[G.lhs[p]]) {
+          minlen[G.lhs[p]] = (int)sum;
+          ch = true;
+        }
+      }
+    }
+    out.complete_est.assign(NS, 0);
+    for (int s = 0; s < NS; ++s) {
+      long best = 1 << 20;
+      for (auto& kv : kla[s]) {
+        const int p = ip(kv.first), d = id(kv.first);
+        long sum = 0;
+        for (size_t k = (size_t)d; k < G.rhs[p].size(); ++k) {
+          const int x = G.rhs[p][k];
+          sum += G.is_nt(x) ? minlen[x - T] : 1;
+        }
+        best = std::min(best, sum);
+      }
+      out.complete_est[s] = (uint16_t)std::min<long>(best, 0xFFFF);
+    }
+  }
   out.state_sym.assign(NS, kNoSymbol);
   for (int s = 0; s < NS; ++s) {
     for (auto& e : edges[s]) {

@@ -43,7 +43,8 @@ EXPORTS = ["grid_compile", "grid_free", "grid_last_error", "grid_info", "grid_ad
            "grid_mask_workspace_bytes", "grid_mask", "grid_mask_phases", "grid_apply",
            "grid_cache_bytes", "grid_cache_clear", "grid_mask_cached", "grid_accept",
            "grid_mask_noalloc_max_bytes", "grid_mask_noalloc", "grid_stack_hash", "grid_stack_hash_host",
-           "grid_accept_inplace", "grid_ci_cache_bytes", "grid_ci_cache_clear", "grid_mask_warm"]
+           "grid_accept_inplace", "grid_ci_cache_bytes", "grid_ci_cache_clear", "grid_mask_warm",
+           "grid_complete", "grid_forced_span"]
 CI_LOOKUP, CI_INSERT, CI_FAMILY, CI_GENN = 1, 2, 4, 8
 PHASE_PROLOGUE, PHASE_WALK, PHASE_RESIDUE, PHASE_FINALIZE, PHASE_ALL = 1, 2, 4, 8, 15
 
@@ -105,6 +106,8 @@ def lib():
         L.grid_stack_hash.argtypes = [vp, i32, vp, vp, vp, vp]
         L.grid_stack_hash_host.argtypes = [vp, vp, ctypes.c_uint32, vp]
         L.grid_accept_inplace.argtypes = [vp, i32, vp, vp, vp, ctypes.c_uint32, vp, vp, vp]
+        L.grid_complete.argtypes = [vp, i32, ctypes.c_char_p, sz, i32, vp, ctypes.POINTER(i32)]
+        L.grid_forced_span.argtypes = [vp, i32, vp, vp, vp, ctypes.c_uint32, i32, vp, vp, vp, vp, vp, vp, sz, vp]
         L.grid_ci_cache_bytes.argtypes = [vp, i32]
         L.grid_ci_cache_bytes.restype = sz
         L.grid_ci_cache_clear.argtypes = [vp, vp, sz, vp]
@@ -270,6 +273,31 @@ class Grid:
                                          _stream_handle(stream)))
         return status
 
+    def forced_span(self, cfg_dev, pool_dev, B, stack_cap, max_len, stack_hash=None, workspace=None,
+                    stream=None):
+        """grid_forced_span: rows advanced in place by their forced spans (at
+        most max_len tokens).  Returns (span int32 [B, max_len] with -1 after
+        each row's span, span_len int32 [B], and the mask, eos and status of
+        the final configurations)."""
+        import torch
+        dev = cfg_dev.device
+        assert pool_dev.numel() >= B * stack_cap and max_len >= 1
+        span = torch.empty((B, max_len), dtype=torch.int32, device=dev)
+        span_len = torch.empty(B, dtype=torch.int32, device=dev)
+        out = torch.empty((B, self.W), dtype=torch.int32, device=dev)
+        eos = torch.empty(B, dtype=torch.uint8, device=dev)
+        status = torch.empty(B, dtype=torch.int32, device=dev)
+        if workspace is None:
+            workspace = self.new_workspace(B, dev)
+        hp = ctypes.c_void_p(stack_hash.data_ptr()) if stack_hash is not None else None
+        _check(lib().grid_forced_span(self.h, B, ctypes.c_void_p(cfg_dev.data_ptr()),
+                                      ctypes.c_void_p(pool_dev.data_ptr()), hp, stack_cap, max_len,
+                                      ctypes.c_void_p(span.data_ptr()), ctypes.c_void_p(span_len.data_ptr()),
+                                      ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(eos.data_ptr()),
+                                      ctypes.c_void_p(status.data_ptr()), ctypes.c_void_p(workspace.data_ptr()),
+                                      workspace.numel(), _stream_handle(stream)))
+        return span, span_len, out, eos, status
+
     def stack_hash(self, cfg_dev, pool_dev, B, out=None, stream=None):
         """grid_stack_hash: the rolling hash of every pool entry of the B rows'
         stacks (int64 tensor parallel to the pool; entries outside the rows'
@@ -281,6 +309,14 @@ class Grid:
                                      ctypes.c_void_p(pool_dev.data_ptr()), ctypes.c_void_p(out.data_ptr()),
                                      _stream_handle(stream)))
         return out
+
+    def complete(self, w, slot=0, max_tokens=4096):
+        """grid_complete: token ids of a legal completion of the viable prefix w
+        (their number is w's reserve)."""
+        out = np.zeros(max(1, max_tokens), dtype=np.int32)
+        n = ctypes.c_int32()
+        _check(lib().grid_complete(self.h, slot, w, len(w), max_tokens, out.ctypes.data, ctypes.byref(n)))
+        return out[:n.value].copy()
 
     def stack_hash_host(self, states):
         """grid_stack_hash_host: the rolling hashes of one stack (uint64 array)."""
