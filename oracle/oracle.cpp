@@ -32,6 +32,7 @@
 
 #include "oracle.h"
 
+#include <memory>
 #include <algorithm>
 #include <bitset>
 #include <cctype>
@@ -812,10 +813,10 @@ extern "C" {
 
 void* oracle_grammar_new(const char* text, const char* drops, char* err, int err_len) {
   try {
-    auto* og = new OGrammar();
+    std::unique_ptr<OGrammar> og(new OGrammar());  // freed when the build throws
     build_grammar(og->G, text ? text : "", drops ? drops : "");
     og->single.init(&og->G);
-    return og;
+    return og.release();
   } catch (const std::exception& e) {
     set_err(err, err_len, e.what());
     return nullptr;

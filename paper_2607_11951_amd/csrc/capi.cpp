@@ -4,6 +4,7 @@
 
 #include "host.h"
 #include "lexhash.h"
+#include "rolling_hash.h"
 
 int host_config_from_prefix(const grid_compiled* g, int slot, const uint8_t* w, size_t n,
                             grid_config* cfg, std::vector<uint16_t>& stack);
@@ -251,4 +252,19 @@ extern "C" int grid_config_from_prefix(const grid_compiled* g, int32_t slot, con
   } catch (const std::exception& e) {
     return fail(GRID_E_ARG, e.what());
   }
+}
+
+// Rolling hash of one stack on the host, from the same definition the device
+// kernels use (section 6.4).
+extern "C" int grid_stack_hash_host(const grid_compiled* g, const uint16_t* states, uint32_t depth, uint64_t* out) {
+  clear_error();
+  if (!g || (depth > 0 && (!states || !out))) return fail(GRID_E_ARG, "grid_stack_hash_host: null pointer");
+  uint64_t h = 0;
+  for (uint32_t i = 0; i < depth; ++i) {
+    const uint32_t sv = states[i];
+    if (sv >= (uint32_t)g->parser.n_states) return fail(GRID_E_ARG, "grid_stack_hash_host: entry is no LR state");
+    if (i > 0) h = node_hash(h, sv, g->parser.state_sym[sv]);
+    out[i] = h;
+  }
+  return GRID_OK;
 }

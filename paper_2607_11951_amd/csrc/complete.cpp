@@ -315,7 +315,7 @@ extern "C" int grid_complete(const grid_compiled* g, int32_t slot, const uint8_t
     *out_n = (int32_t)toks.size();
     if ((int32_t)toks.size() > max_tokens)
       return fail(GRID_E_CAPACITY, "grid_complete: the completion needs " + std::to_string(toks.size()) + " tokens");
-    std::memcpy(out_tokens, toks.data(), toks.size() * sizeof(int32_t));
+    if (!toks.empty()) std::memcpy(out_tokens, toks.data(), toks.size() * sizeof(int32_t));
     return GRID_OK;
   } catch (const std::exception& e) {
     return fail(GRID_E_ARG, e.what());

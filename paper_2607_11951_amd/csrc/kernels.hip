@@ -3268,19 +3268,6 @@ extern "C" int grid_stack_hash(const grid_compiled* g, int32_t B, const grid_con
   return GRID_OK;
 }
 
-extern "C" int grid_stack_hash_host(const grid_compiled* g, const uint16_t* states, uint32_t depth, uint64_t* out) {
-  clear_error();
-  if (!g || (depth > 0 && (!states || !out))) return fail(GRID_E_ARG, "grid_stack_hash_host: null pointer");
-  uint64_t h = 0;
-  for (uint32_t i = 0; i < depth; ++i) {
-    const uint32_t sv = states[i];
-    if (sv >= (uint32_t)g->parser.n_states) return fail(GRID_E_ARG, "grid_stack_hash_host: entry is no LR state");
-    if (i > 0) h = node_hash(h, sv, g->parser.state_sym[sv]);
-    out[i] = h;
-  }
-  return GRID_OK;
-}
-
 // ------------------------------------------------------ no-alloc mask entry
 // The workspace of grid_mask_noalloc: a device array of the code object, one
 // copy per GPU, held until the process ends.  Host code never passes the
