@@ -272,6 +272,126 @@ def cold_schema(torch, G, dev, steps, warmup):
             "add_lexicon_ms_per_schema": lex_ms}
 
 
+def warm_decode(torch, G, grid, wl, slots, dev, n_steps):
+    """Decode loops over the headline batches: each row's stack in its own
+    region of a pool, every step the row's mask, the bf16 -inf fill and an
+    in-place advance by a token its mask allows (grid_accept_inplace, rolling
+    hashes kept).  The token trajectories are drawn once from the masks
+    (untimed), then replayed from the same starting configurations three
+    ways: cold masks (grid_mask), warm masks with an empty cache of
+    context-independent words at the start of the replay, and warm masks
+    with the cache the previous replay left (steady state).  Rows served by
+    cached words = rows - entries published."""
+    B, cap = wl.batch, 1024
+    stride = 96 + (4 * grid.W + 15) // 16 * 16
+    starts = []
+    for idx in wl.batches():
+        cfgs, pool = grid.configs([wl.prefixes[j] for j in idx], [slots[wl.slots[j]] for j in idx])
+        region = np.zeros(B * cap, dtype=np.uint16)
+        for b in range(B):
+            off, d = int(cfgs["stk_off"][b]), int(cfgs["stk_depth"][b])
+            region[b * cap:b * cap + d] = pool[off:off + d]
+            cfgs["stk_off"][b] = b * cap
+        starts.append(grid.configs_to_device(cfgs, region, dev))
+    stream = torch.cuda.current_stream()
+    c = torch.empty_like(starts[0][0])
+    p = torch.empty_like(starts[0][1])
+    h = torch.zeros(B * cap, dtype=torch.int64, device=dev)
+    mask = torch.empty((B, grid.W), dtype=torch.int32, device=dev)
+    eos = torch.empty(B, dtype=torch.uint8, device=dev)
+    status = torch.empty(B, dtype=torch.int32, device=dev)
+    acc_st = torch.empty(B, dtype=torch.int32, device=dev)
+    ws = grid.new_workspace(B, dev)
+    logits = torch.zeros((B, wl.V), dtype=torch.bfloat16, device=dev)
+    rng = np.random.default_rng(6100)
+    traj = []
+    for c0, p0 in starts:  # token trajectories from the exact masks
+        c.copy_(c0)
+        p.copy_(p0)
+        toks = []
+        for _ in range(n_steps):
+            grid.mask(c, p, B, mask, eos, status, ws, stream)
+            torch.cuda.synchronize()
+            bits = np.unpackbits(mask.cpu().numpy().view(np.uint8), axis=1, bitorder="little")[:, :wl.V]
+            t = []
+            for r in range(B):
+                allowed = np.flatnonzero(bits[r])
+                allowed = allowed[allowed != wl.eos_id]
+                t.append(int(rng.choice(allowed)) if len(allowed) else wl.eos_id)
+            tt = torch.tensor(t, dtype=torch.int32, device=dev)
+            toks.append(tt)
+            grid.accept_inplace(c, p, tt, B, cap, status=acc_st, stream=stream)
+        traj.append(toks)
+    cache = grid.new_ci_cache(8192, dev)
+    flags = G.grid.CI_LOOKUP | G.grid.CI_INSERT
+
+    def published():
+        st = cache.view(-1, stride)[:, :4].contiguous().view(torch.int32)[:, 0]
+        return int((st == 2).sum().item())
+
+    def replay(kind):
+        total = 0.0
+        for bi, (c0, p0) in enumerate(starts):
+            c.copy_(c0)
+            p.copy_(p0)
+            grid.stack_hash(c, p, B, out=h, stream=stream)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for tt in traj[bi]:
+                if kind == "cold":
+                    grid.mask(c, p, B, mask, eos, status, ws, stream)
+                else:
+                    grid.mask_warm(c, p, B, cache, flags, mask, eos, status, ws, stream)
+                G.apply(mask, logits, stream)
+                grid.accept_inplace(c, p, tt, B, cap, stack_hash=h, status=acc_st, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            assert (status.cpu() == 0).all() and (acc_st.cpu() == 0).all()
+            total += e0.elapsed_time(e1) / 1000.0
+        return total
+
+    rows = B * n_steps * len(starts)
+    replay("cold")
+    t_cold = replay("cold")
+    grid.clear_ci_cache(cache, stream)
+    n0 = published()
+    t_first = replay("warm")
+    n1 = published()
+    t_steady = replay("warm")
+    n2 = published()
+    # the in-place advance alone, same trajectories
+    t_acc = 0.0
+    for bi, (c0, p0) in enumerate(starts):
+        c.copy_(c0)
+        p.copy_(p0)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for tt in traj[bi]:
+            grid.accept_inplace(c, p, tt, B, cap, stack_hash=h, status=acc_st, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t_acc += e0.elapsed_time(e1) / 1000.0
+    return {"workload": f"read-only DML SQL, {len(starts)} batches x B={B} rows x {n_steps} decode steps, "
+                        "tokens sampled from the exact masks, replayed",
+            "cold_masks_per_s": rows / t_cold, "cold_step_us": t_cold * 1e6 / (n_steps * len(starts)),
+            "warm_first_pass_masks_per_s": rows / t_first, "warm_first_pass_rows_cached": 1.0 - (n1 - n0) / rows,
+            "warm_steady_masks_per_s": rows / t_steady, "warm_steady_rows_cached": 1.0 - (n2 - n1) / rows,
+            "warm_steady_step_us": t_steady * 1e6 / (n_steps * len(starts)),
+            "accept_inplace_step_us": t_acc * 1e6 / (n_steps * len(starts)),
+            "note": "each step = mask (+ warm cache) + bf16 -inf fill [B, V] + in-place advance with rolling "
+                    "hashes; rows cached = 1 - entries published / rows"}
+
+
+def completion_cost(G, grid, wl, slots, n_rows):
+    """Host cost of the mode-1 reserve: grid_complete on rows of the workload."""
+    lens, t = [], time.perf_counter()
+    for j in range(n_rows):
+        lens.append(len(grid.complete(wl.prefixes[j], slots[wl.slots[j]])))
+    dt = time.perf_counter() - t
+    return {"rows": n_rows, "ms_per_completion": dt * 1000.0 / n_rows,
+            "reserve_tokens_median": float(np.median(lens)), "reserve_tokens_max": int(max(lens))}
+
+
 def cpu_baselines(wl_main, seconds):
     """The oracle on the host cores: checkpoint mode with every thread (the
     reported value) and with one thread, from-scratch mode (every token
@@ -520,6 +640,8 @@ def main():
             cache_out[f"{label}_masks_per_s"] = B * cache_steps / (e0.elapsed_time(e1) / 1000.0)
         assert (status.cpu() == 0).all()
         extra["cache"] = cache_out
+        extra["decode"] = warm_decode(torch, G, grid, wl, slots, dev, 16)
+        extra["completion"] = completion_cost(G, grid, wl, slots, 64)
         extra["cold_schema"] = cold_schema(torch, G, dev, max(20, args.steps // 4), 3)
         extra["small_workloads"] = [small_workload(torch, G, 2, dev, args.steps, args.warmup),
                                     small_workload(torch, G, 1, dev, args.steps, args.warmup)]

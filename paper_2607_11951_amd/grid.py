@@ -356,6 +356,10 @@ class Grid:
         _check(lib().grid_ci_cache_clear(self.h, ctypes.c_void_p(c.data_ptr()), c.numel(), _stream_handle(stream)))
         return c
 
+    def clear_ci_cache(self, ci_cache, stream=None):
+        _check(lib().grid_ci_cache_clear(self.h, ctypes.c_void_p(ci_cache.data_ptr()), ci_cache.numel(),
+                                         _stream_handle(stream)))
+
     def mask_warm(self, cfg_dev, pool_dev, B, ci_cache, flags=1 | 2, out=None, eos=None, status=None,
                   workspace=None, stream=None):
         """grid_mask_warm: the mask of B rows with the CI-words cache (CI_* flags)."""

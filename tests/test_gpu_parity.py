@@ -281,6 +281,58 @@ def test_gpu_invariants_full_vocab(G):
             assert not (bits[:, t] & ~bits[:, parent]).any(), sp
 
 
+def test_gpu_composition_invariant(G):
+    """Composition (section 4.1): a token t = p + b whose spelling is another
+    token p followed by one byte b is allowed at a configuration exactly when
+    p is allowed there and the one-byte token b is allowed after p.  Checked
+    on the full DML vocabulary from the GPU masks alone: masks at 8 rows, then
+    at those rows advanced by up to 48 allowed parents each (one call)."""
+    wl = make_workload(3, rows=32)
+    grid, sm = G.from_workload(wl)
+    grid.to_device("cuda")
+    first = {}
+    for t, sp in enumerate(wl.vocab):
+        if sp and t not in wl.specials:
+            first.setdefault(sp, t)
+    byte_tok = {b: first[bytes([b])] for b in range(256) if bytes([b]) in first}
+    children = {}
+    for sp, t in first.items():
+        if len(sp) > 1 and sp[:-1] in first and sp[-1] in byte_tok:
+            children.setdefault(first[sp[:-1]], []).append((t, byte_tok[sp[-1]]))
+
+    def masks(prefixes, slots):
+        cfgs, pool = grid.configs(prefixes, slots)
+        c, p = grid.configs_to_device(cfgs, pool)
+        m, _, s = grid.mask(c, p, len(prefixes))
+        torch.cuda.synchronize()
+        assert (s.cpu().numpy() == 0).all()
+        return np.unpackbits(m.cpu().numpy().view(np.uint8), axis=1, bitorder="little")
+
+    rows = list(range(0, 32, 4))
+    base = masks([wl.prefixes[j] for j in rows], [sm[wl.slots[j]] for j in rows])
+    rng = np.random.default_rng(4100)
+    ext, ext_slots, pairs = [], [], []
+    for i, j in enumerate(rows):
+        parents = [pt for pt in children if base[i, pt]]
+        for pt in rng.permutation(parents)[:48].tolist():
+            pairs.append((i, pt, len(ext)))
+            ext.append(wl.prefixes[j] + wl.vocab[pt])
+            ext_slots.append(sm[wl.slots[j]])
+    assert len(pairs) >= 8 * 24
+    after = masks(ext, ext_slots)
+    checked = 0
+    for i, pt, e in pairs:
+        for t, bt in children[pt]:
+            assert base[i, t] == after[e, bt], (rows[i], wl.vocab[pt], wl.vocab[t])
+            checked += 1
+    # and a blocked parent blocks all its children (monotone rejection)
+    for i in range(len(rows)):
+        for pt, kids in children.items():
+            if not base[i, pt]:
+                assert not any(base[i, t] for t, _ in kids)
+    log(f"composition: {checked} (token, parent, byte) triples at {len(pairs)} advanced rows")
+
+
 def test_overlay_handoff_to_slow_path(G, oracle_mod):
     """Tokens that shift many terminals (runs of '(' at a boolean position,
     '(' and ')' mixes) outgrow a walk lane's LDS stack area and are finished by
