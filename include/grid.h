@@ -224,6 +224,10 @@ enum {
                                state (terminal id, or 0x10000 | nonterminal index;
                                0xFFFFFFFF for the initial state) -- the "goto" of the
                                rolling configuration hash */
+  GRID_ART_LEX_CHILD,       /* u32 [8] per lexicon-trie node (all slots, indexed like
+                               LEX_FLAGS): bit b set when the node has a child on byte b */
+  GRID_ART_ID_SECOND,       /* u16 [V]: 0x100 | second byte of each token id's spelling,
+                               0 for spellings shorter than two bytes and specials */
   GRID_ART_COUNT
 };
 int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);

@@ -113,10 +113,12 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
   va.byte_complete = std::all_of(single.begin(), single.end(), [](char c) { return c != 0; });
   va.spell_of_id.assign(V, 0xFFFFFFFFu);
   va.id_first.assign(V, 0);
+  va.id_second.assign(V, 0);
   for (size_t u = 0; u < U; ++u)
     for (uint32_t k = va.alias_off[u]; k < va.alias_off[u + 1]; ++k) {
       va.spell_of_id[va.alias_ids[k]] = (uint32_t)u;
       va.id_first[va.alias_ids[k]] = (uint8_t)uniq[u][0];
+      if (uniq[u].size() > 1) va.id_second[va.alias_ids[k]] = (uint16_t)(0x100u | (uint8_t)uniq[u][1]);
     }
   // first-byte range of every 64 consecutive spellings (first bytes are
   // non-decreasing, so the first and the last spelling of the group bound it)
@@ -329,6 +331,9 @@ void add_lexicon(LexiconStore& st, const LexerDfa& dfa, const GrammarText& g, co
   uint32_t hash_base = (uint32_t)(st.hash.size() / 2);
   st.flags.resize(st.flags.size() + nodes.size());
   for (size_t k = 0; k < nodes.size(); ++k) st.flags[flags_base + k] = nodes[k].flags;
+  st.child_bits.resize(st.flags.size() * 8, 0u);
+  for (size_t k = 0; k < nodes.size(); ++k)
+    for (auto& e : nodes[k].kids) st.child_bits[(flags_base + k) * 8 + (e.first >> 5)] |= 1u << (e.first & 31u);
   st.hash.resize(st.hash.size() + (size_t)size * 2, 0);
   for (size_t k = 0; k < nodes.size(); ++k)
     for (auto& e : nodes[k].kids) {

@@ -159,6 +159,7 @@ extern "C" int grid_add_lexicon(grid_compiled* g, const grid_lexicon_args* la, i
     // lexicon artifacts changed: device copies must be re-bound
     g->dev[GRID_ART_LEX_FLAGS] = g->dev[GRID_ART_LEX_HASH] = g->dev[GRID_ART_LEX_SLOTS] = nullptr;
     g->dev[GRID_ART_LEX_PREFIX] = g->dev[GRID_ART_LEX_STRIDE] = g->dev[GRID_ART_LEX_TOKEN] = nullptr;
+    g->dev[GRID_ART_LEX_CHILD] = nullptr;
     return GRID_OK;
   } catch (const Error& e) {
     return fail(e.code, e.what());
@@ -214,6 +215,8 @@ extern "C" int grid_artifact(const grid_compiled* g, int32_t which, const void**
     case GRID_ART_PARSE_SHIFT: put(g->parser.pshift, p, n); break;
     case GRID_ART_GOTO_HASH: put(g->parser.goto_hash, p, n); break;
     case GRID_ART_STATE_SYMBOL: put(g->parser.state_sym, p, n); break;
+    case GRID_ART_LEX_CHILD: put(g->lex.child_bits, p, n); break;
+    case GRID_ART_ID_SECOND: put(g->vocab.id_second, p, n); break;
     default: return fail(GRID_E_ARG, "unknown artifact " + std::to_string(which));
   }
   return GRID_OK;

@@ -118,6 +118,7 @@ struct VocabArtifacts {
   std::vector<uint16_t> sub_range;   // per 64 spellings: lowest | highest first byte << 8
   std::vector<uint32_t> spell_of_id; // [V]: spelling index, 0xFFFFFFFF none
   std::vector<uint8_t> id_first;     // [V]: first byte of the spelling, 0 none
+  std::vector<uint16_t> id_second;   // [V]: second byte of the spelling | 0x100, 0 none
   std::vector<uint32_t> alias_off;   // [U+1]
   std::vector<int32_t> alias_ids;
   std::vector<uint32_t> level_off;   // [Lmax+2]
@@ -142,6 +143,7 @@ ClassTables build_class_tables(const LexerDfa& dfa, const VocabArtifacts& va);
 // ---- lexicon slots
 struct LexiconStore {
   std::vector<uint16_t> flags;     // all slots' nodes
+  std::vector<uint32_t> child_bits;  // all slots' nodes: bitmap of the bytes with a child (8 u32 each)
   std::vector<uint32_t> hash;      // all slots' entries (2 u32 each)
   std::vector<uint32_t> prefix;    // all slots' prefix-table entries (4 u32 each)
   std::vector<uint32_t> stride;    // all slots' stride-table entries (8 u32 each)

@@ -108,6 +108,8 @@ struct Tables {
   const uint4* lex_stride;    // [entries][2]
   const uint32_t* lex_token;  // [slots][V] token flags at start offsets 0 and 1
   const uint8_t* id_first;    // [V] first byte of each token
+  const uint16_t* id_second;  // [V] 0x100 | second byte of each token, 0 none
+  const uint32_t* lex_child;  // [nodes][8] child bytes of every lexicon-trie node
   const uint16_t* cmap;       // class of each token per lexer state [S][V]
   const uint32_t* coff;       // [S+1] first class record of each state
   const uint4* crec;          // class records
@@ -208,7 +210,7 @@ static_assert(sizeof(Post) == 32, "post entry is 32 bytes");
 static_assert(kPostCap == 14, "the walk decodes a post entry as two 16-byte halves");
 
 struct RowLayout {
-  size_t cls, win, block, post, a2, vcode, vrule, rbits, rcls, slow, slow_ov, total;
+  size_t cls, win, block, post, a2, vcode, vrule, cont2, rbits, slow, slow_ov, total;
 };
 
 __host__ __device__ inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u; }
@@ -217,11 +219,12 @@ __host__ __device__ inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u;
 // the winner's shift (one byte per DFA state each); the top kWalkWin states
 // of the stack; [block ends here]; post-shift stacks and allowed sets of the
 // allowed terminals; the class verdicts (2 bits per class of the row's lexer
-// state) and lexicon shortcuts (a byte per class); the residue bitmaps (one
+// state) and lexicon shortcuts (a byte per class); for every byte b that
+// continues the pending lexeme in the lexicon, the bytes that continue it
+// after b (256 bits per b, rows of other b unwritten); the residue bitmaps (one
 // bit per spelling the stream kernel left to the residue pass, in spelling
-// order: first those the lexicon decides, then those the byte walk decides)
-// and the class of each such spelling (u16); the slow path's list and stack
-// areas.
+// order: first those the lexicon decides, then those the byte walk decides);
+// the slow path's list and stack areas.
 __host__ __device__ inline RowLayout row_layout(int T, int S, int U, int max_classes) {
   RowLayout L;
   size_t o = sizeof(RowHeader);
@@ -238,10 +241,10 @@ __host__ __device__ inline RowLayout row_layout(int T, int S, int U, int max_cla
   o += (size_t)pad16(((uint32_t)max_classes + 3u) / 4u);
   L.vrule = o;
   o += (size_t)pad16((uint32_t)max_classes);
+  L.cont2 = o;
+  o += 256 * 32;
   L.rbits = o;
   o += (size_t)((U + 63) / 64) * 16;
-  L.rcls = o;
-  o += (size_t)pad16((uint32_t)U * 2u);
   L.slow = o;
   o += kSlowCap * 4;
   L.slow_ov = o;
@@ -1290,9 +1293,16 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   // the lexicon (thread b), and the top of the stack for the residue walk
   {
     const uint32_t b = (uint32_t)tid;  // kBlock == 256: one byte value per thread
-    const bool c = !rem_empty && lex_child(tb, sl, cfg.lexnode, b) != kNoLex;
+    const uint32_t n1 = rem_empty ? kNoLex : lex_child(tb, sl, cfg.lexnode, b);
+    const bool c = n1 != kNoLex;
     const uint64_t bal = __ballot(c);
     if ((tid & 31) == 0) hdr->cont[tid >> 5] = (uint32_t)(bal >> (tid & 32));
+    if (c) {  // and the bytes that continue it after b: the child bytes of its trie node
+      const uint4* src = reinterpret_cast<const uint4*>(tb.lex_child + (size_t)(sl.fbase + n1) * 8u);
+      uint4* dst = reinterpret_cast<uint4*>(rw + L.cont2 + (size_t)b * 32u);
+      dst[0] = src[0];
+      dst[1] = src[1];
+    }
   }
   {
     uint32_t a0[MW], aw[MW];
@@ -1743,11 +1753,15 @@ struct LexNo {
 // to its first lexicon question is "no flags", valid when that answer leads
 // to no second question.  The stream kernel knows the answer is "no flags"
 // when the question's lexeme starts with the pending bytes and the token's
-// first byte does not continue them in the lexicon (the row's cont table), or
-// when the lexeme starts at token byte 0 or 1 in the start state and the
-// token-flag entry has no flags there.  Encoded as 3 (the class code) |
-// kind << 2 (0 pending bytes, 1 trailing prefix at o, 2 word at o) | o << 4 |
-// v_no << 5 | valid << 7.
+// first byte does not continue them in the lexicon (the row's cont table) or,
+// when the lexeme also holds the token's second byte, that byte does not
+// continue them after the first (the row's second-byte table); or when the
+// lexeme starts at token byte 0 or 1 in the start state and the token-flag
+// entry has no flags there.  Encoded as 3 (the class code) | kind << 2 (0
+// pending bytes, 1 trailing prefix at o, 2 word at o) | o << 4 | v_no << 5 |
+// valid << 7; for kind 0, bit 4 says the lexeme holds the token's second byte
+// when the token has one (a trailing lexeme, or a word ending at offset 2 or
+// later).
 constexpr uint32_t kNoValid = 1u << 7;
 template <int MW>
 __device__ __forceinline__ uint32_t class_shortcut(const RowHeader& h, const uint32_t* I, const uint32_t* live,
@@ -1756,7 +1770,10 @@ __device__ __forceinline__ uint32_t class_shortcut(const RowHeader& h, const uin
   LexNo ln{rec.w, rec.x & kClassEndsMask, h.rem_len == 0, -1, -1, false, false};
   const uint32_t v = class_verdict<MW>(h, I, live, 8, tinfo, acc_off, acc_list, a2, 8, rec, ln);
   if (ln.kind < 0 || ln.second || v == kVerdictLexicon) return kVerdictLexicon;
-  if (ln.pending) return kVerdictLexicon | v << 5 | kNoValid;
+  if (ln.pending) {
+    const bool two = ln.kind == 0 || (rec.w & 0xFFu) >= 2u;
+    return kVerdictLexicon | (two ? 1u << 4 : 0u) | v << 5 | kNoValid;
+  }
   if (ln.start < 0) return kVerdictLexicon;
   return kVerdictLexicon | (ln.kind == 0 ? 1u : 2u) << 2 | (uint32_t)ln.start << 4 | v << 5 | kNoValid;
 }
@@ -1938,7 +1955,7 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
   }
   // pass 2: codes; for a class the lexicon decides, its shortcut byte and the
   // token's first byte and token flags (again all loads in flight together)
-  uint32_t code[kPer], sc[kPer], fb[kPer], tf[kPer];
+  uint32_t code[kPer], sc[kPer], fb[kPer], tf[kPer], sb[kPer];
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
     const int c = c_lo + wave + j * kStreamWaves;
@@ -1947,7 +1964,19 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
     const bool lexq = code[j] == kVerdictLexicon && id < tb.V;
     sc[j] = lexq ? vrule[cls[j]] : 0u;
     fb[j] = lexq ? tb.id_first[id] : 0u;
+    sb[j] = lexq ? tb.id_second[id] : 0u;
     tf[j] = lexq ? tflags[id] : 0u;
+  }
+  // pass 2b: a pending-lexeme question on a lexeme that holds the token's
+  // second byte, after a first byte that continues the lexeme: the second
+  // byte's bit in the row's table (0 when it cannot stop the question here)
+  const uint32_t* cont2 = (const uint32_t*)(rw + RL.cont2);
+  uint32_t c2[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const bool ask = code[j] == kVerdictLexicon && (sc[j] & kNoValid) && ((sc[j] >> 2) & 3u) == 0u &&
+                     ((sc[j] >> 4) & 1u) && (sb[j] & 0x100u) && ((cont[fb[j] >> 5] >> (fb[j] & 31u)) & 1u);
+    c2[j] = ask ? ~(cont2[fb[j] * 8u + ((sb[j] & 0xFFu) >> 5)] >> (sb[j] & 31u)) & 1u : 0u;
   }
   // pass 3: shortcut verdicts, mask words, residue ids
   uint32_t resu[kPer];  // this lane's residue ids (or ~0)
@@ -1960,7 +1989,7 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
     uint32_t cd = code[j];
     if (cd == kVerdictLexicon && (sc[j] & kNoValid)) {
       const uint32_t kind = (sc[j] >> 2) & 3u;
-      const bool no = kind == 0 ? !((cont[fb[j] >> 5] >> (fb[j] & 31u)) & 1u)
+      const bool no = kind == 0 ? !((cont[fb[j] >> 5] >> (fb[j] & 31u)) & 1u) || c2[j] != 0u
                                 : ((tf[j] >> (16 * ((sc[j] >> 4) & 1u) + (kind == 2 ? 8u : 0u))) & 0xFFu) == 0u;
       if (no) cd = (sc[j] >> 5) & 3u;
     }
@@ -1972,18 +2001,16 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
     if (cd >= kVerdictWalk && id < tb.V) resu[j] = (uint32_t)id;
     code[j] = cd;
   }
-  // mark the residue spellings in the row's bitmaps (lexicon or byte walk)
-  // and record their class, last, so no load above waits behind these
-  // atomics; the spelling lookups are issued together
+  // mark the residue spellings in the row's bitmaps (lexicon or byte walk),
+  // last, so no load above waits behind these atomics; the spelling lookups
+  // are issued together
 #pragma unroll
   for (int k2 = 0; k2 < kPer; ++k2) resu[k2] = resu[k2] != 0xFFFFFFFFu ? tb.spell_of_id[resu[k2]] : 0xFFFFFFFFu;
   const uint32_t nsub = ((uint32_t)tb.U + 63u) / 64u;
-  uint16_t* rcls = (uint16_t*)(rw + RL.rcls);
 #pragma unroll
   for (int k2 = 0; k2 < kPer; ++k2)
     if (resu[k2] != 0xFFFFFFFFu) {
       const uint32_t u = resu[k2];
-      rcls[u] = (uint16_t)cls[k2];
       atomicOr(rbits + (code[k2] == kVerdictWalk ? nsub : 0u) + (u >> 6), 1ull << (u & 63u));
     }
   if (lane == 0 && any) hdr->nonempty = 1u;
@@ -2211,8 +2238,8 @@ struct LexLane {
 };
 
 // Verdict of one spelling of the residue bitmaps: for a spelling of the
-// lexicon bitmap, its class cls (recorded by the stream kernel) is taken
-// again with its own lexemes' lexicon flags (token-flag table, prefix and
+// lexicon bitmap, its class cls (the class map's entry at its first id) is
+// taken again with its own lexemes' lexicon flags (token-flag table, prefix and
 // stride tables); the byte walk decides the rest.  1 allowed, 0 rejected or
 // handed over.
 template <int MW>
@@ -2436,7 +2463,10 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
           const uint8_t* rowblk = rows_s + (size_t)r * WL.block;
           uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
           const uint4 rk = tb.spell_rec[u];
-          const uint32_t cls = lex ? ((const uint16_t*)(rw + RL.rcls))[u] : 0u;
+          // a lexicon spelling's class: the class map at its first id (its
+          // aliases share it)
+          const uint32_t cls =
+              lex ? (uint32_t)tb.cmap[(size_t)((const RowHeader*)rowblk)->q * tb.V + (rk.z & 0x7FFFFFFFu)] : 0u;
           if (residue_token<MW>(sh, *(const RowHeader*)rowblk, rowblk, rw, RL, u, rk, lex != 0, cls, lane_area) > 0) {
             allow_spelling(tb, mask + (size_t)(g0 + r) * tb.W, u, rk);
             ((RowHeader*)rw)->nonempty = 1u;
@@ -3106,7 +3136,7 @@ static int bind_tables(const grid_compiled* g, Tables& tb) {
                                GRID_ART_SPELL_OF_ID, GRID_ART_CLASS_MAP, GRID_ART_CLASS_OFF,
                                GRID_ART_CLASS_REC,   GRID_ART_LEX_STRIDE,  GRID_ART_LEX_TOKEN,
                                GRID_ART_ID_FIRST,    GRID_ART_PARSE_SHIFT, GRID_ART_GOTO,
-                               GRID_ART_STATE_SYMBOL};
+                               GRID_ART_STATE_SYMBOL, GRID_ART_LEX_CHILD, GRID_ART_ID_SECOND};
   for (int w : needed)
     if (!bound(g, w)) return fail(GRID_E_UNBOUND, "artifact " + std::to_string(w) + " is not bound");
   tb.dfa = (const uint16_t*)g->dev[GRID_ART_DFA_CLASS];
@@ -3134,6 +3164,8 @@ static int bind_tables(const grid_compiled* g, Tables& tb) {
   tb.lex_stride = (const uint4*)g->dev[GRID_ART_LEX_STRIDE];
   tb.lex_token = (const uint32_t*)g->dev[GRID_ART_LEX_TOKEN];
   tb.id_first = (const uint8_t*)g->dev[GRID_ART_ID_FIRST];
+  tb.id_second = (const uint16_t*)g->dev[GRID_ART_ID_SECOND];
+  tb.lex_child = (const uint32_t*)g->dev[GRID_ART_LEX_CHILD];
   tb.spell_of_id = (const uint32_t*)g->dev[GRID_ART_SPELL_OF_ID];
   tb.state_sym = (const uint32_t*)g->dev[GRID_ART_STATE_SYMBOL];
   tb.stack_hash = nullptr;

@@ -85,6 +85,46 @@ def _lexp_hash(lo, hi, ln):
     return h ^ (h >> 12)
 
 
+def test_lexicon_child_bitmaps_and_second_bytes(G):
+    """LEX_CHILD: bit b of a trie node's bitmap is set exactly when some word
+    of the slot continues the node's string with byte b (the node reached
+    through the edge hash); ID_SECOND: 0x100 | second byte, 0 when shorter."""
+    words_t = ["employees", "emp", "e", "dept_history_2020", "orders"]
+    words_c = ["id", "emp_no", "employee_name_full", "e_x", "order_id"]
+    vocab = [b"a", b"ab", b"", b"xyz", b"\x00\xff"]
+    g = G.Grid(grammar_text("crud"), ["insert", "update", "delete"], vocab, [2])
+    slot = g.add_lexicon({"TABLE_NAME": words_t, "COLUMN_NAME": words_c})
+    rec = np.frombuffer(g.artifact("LEX_SLOTS"), np.uint32).reshape(-1, 12)[slot]
+    edges = np.frombuffer(g.artifact("LEX_HASH"), np.uint32).reshape(-1, 2)
+    child_bits = np.frombuffer(g.artifact("LEX_CHILD"), np.uint32).reshape(-1, 8)
+    assert len(child_bits) == len(np.frombuffer(g.artifact("LEX_FLAGS"), np.uint16))
+    fbase, hbase, hmask = (int(x) for x in rec[:3])
+
+    def child(node, b):
+        key = node * 256 + b + 1
+        h = ((key * 0x9E3779B1) & 0xFFFFFFFF)
+        h = (h ^ (h >> 15)) & hmask
+        while True:
+            k, c = edges[hbase + h]
+            if k == key:
+                return int(c)
+            if k == 0:
+                return None
+            h = (h + 1) & hmask
+
+    words = [w.encode() for w in words_t + words_c]
+    for p in {w[:k] for w in words for k in range(len(w) + 1)}:
+        node = 0
+        for b in p:
+            node = child(node, b)
+        want = {w[len(p)] for w in words if w.startswith(p) and len(w) > len(p)}
+        bits = child_bits[fbase + node]
+        got = {b for b in range(256) if (int(bits[b >> 5]) >> (b & 31)) & 1}
+        assert got == want, p
+    sec = np.frombuffer(g.artifact("ID_SECOND"), np.uint16)
+    assert sec.tolist() == [0, 0x100 | ord("b"), 0, 0x100 | ord("y"), 0x1FF]
+
+
 def test_lexicon_prefix_table(G):
     # every trie node of depth 1..8 is found by its bytes with the node id and
     # flags the edge hash gives; strings that prefix no word are not found
