@@ -502,8 +502,11 @@ int grid_forced_span(const grid_compiled* g, int32_t B, grid_config* cfg_dev, ui
 #define GRID_DTYPE_F32 0
 #define GRID_DTYPE_BF16 1
 /* In place: logits[b * row_stride + t] = -inf for every t < V whose mask bit
- * is 0 (fp32 0xFF800000, bf16 0xFF80); other entries are not written
+ * is 0 (fp32 0xFF800000, bf16 0xFF80); other entries keep their bit patterns
  * (section 2: hard -inf masking, a soundness precondition of Proposition 7).
+ * With 16-byte aligned rows an aligned group of 8 logits that holds kept
+ * entries is read and written back whole (kept entries rewritten with their
+ * own bits), so no other writer may touch the logits during the call.
  * mask_dev: device u32 [B][ceil(V/32)]; logits_dev: device fp32 or bf16 with
  * row_stride >= V elements.  Asynchronous on stream. */
 int grid_apply(const uint32_t* mask_dev, void* logits_dev, int32_t dtype, int32_t B, int32_t V,

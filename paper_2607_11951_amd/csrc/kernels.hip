@@ -56,7 +56,8 @@ using namespace grid;
 
 namespace {
 
-constexpr int kBlock = 256;          // prologue / apply workgroup size
+constexpr int kBlock = 256;          // workgroup size of most kernels
+constexpr int kProThreads = 512;     // prologue workgroup size (more set-simulation jobs per row)
 constexpr int kStackWin = 256;       // top of the row's stack kept in LDS (prologue)
 constexpr int kPostCap = 14;         // overlay states recorded per first shift
 constexpr int kTmpCap = 32;          // prologue: virtual pushes of one simulation
@@ -425,7 +426,7 @@ __host__ __device__ inline ParseLds parse_lds(const Tables& tb, uint32_t base, b
 
 // The prologue's LR tables in LDS: GOTO as the dense table when it fits
 // beside the prologue's own arrays, else as the hash.
-constexpr uint32_t kPrologueParseMax = 96 * 1024;
+constexpr uint32_t kPrologueParseMax = 92 * 1024;
 __host__ __device__ inline ParseLds prologue_parse_lds(const Tables& tb) {
   const ParseLds d = parse_lds(tb, 0, true);
   return d.total <= kPrologueParseMax ? d : parse_lds(tb, 0, false);
@@ -996,7 +997,7 @@ __device__ inline void ci_key(const Tables& tb, const grid_config& cfg, const Sl
 // the pending lexeme's winner; then the trailing-flag tables, the lexicon
 // continuation bits of the pending lexeme and the row header.
 template <int MW>
-__global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_config* __restrict__ cfgs,
+__global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const grid_config* __restrict__ cfgs,
                                                           const uint16_t* __restrict__ pool,
                                                           uint32_t* __restrict__ mask,
                                                           uint8_t* __restrict__ eos_out,
@@ -1006,7 +1007,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   const int tid = threadIdx.x;
   __shared__ uint16_t win[kStackWin];
   __shared__ uint32_t A[8], I[8], R[8], Aw[8];
-  __shared__ uint16_t sim_area[kBlock][kPostCap + kTmpCap];
+  __shared__ uint16_t sim_area[kProThreads][kPostCap + kTmpCap];
   __shared__ int bad, overflow, winner, eos_ok, eos_sigma, cache_hit;
   __shared__ uint8_t eos_after[256];  // end-of-sequence test after shifting each candidate winner
   __shared__ Post posts[256];          // stack after shifting each allowed terminal
@@ -1028,7 +1029,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   {
     const StageRegion rg[4] = {parse_region(tb, plds, PL, 0), parse_region(tb, plds, PL, 1),
                                parse_region(tb, plds, PL, 2), parse_region(tb, plds, PL, 3)};
-    dma_regions<4>(rg, tid, kBlock);
+    dma_regions<4>(rg, tid, kProThreads);
   }
   uint32_t s_top = 0;
   if (shape_ok && lo + (uint32_t)tid < depth) s_top = pool[cfg.stk_off + lo + tid];
@@ -1050,7 +1051,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   }
   {  // the residue bitmaps start empty (16-byte stores)
     uint4* rb = (uint4*)(rw + L.rbits);
-    for (int i = tid; i < (tb.U + 63) / 64; i += kBlock) rb[i] = make_uint4(0, 0, 0, 0);
+    for (int i = tid; i < (tb.U + 63) / 64; i += kProThreads) rb[i] = make_uint4(0, 0, 0, 0);
   }
   dma_wait();
   __syncthreads();
@@ -1066,7 +1067,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
         h2 += stack_mix(i, s_top, 0xD1B54A32D192ED03ull);
       }
     }
-    for (uint32_t i = tid; i < lo; i += kBlock) {  // entries below the window
+    for (uint32_t i = tid; i < lo; i += kProThreads) {  // entries below the window
       const uint16_t v = pool[cfg.stk_off + i];
       if (v >= tb.NS) bad = 1;
       if (sum_hash) {
@@ -1159,7 +1160,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     const CacheEntry* e = (const CacheEntry*)(tb.cache + (size_t)cache_hit * tb.cache_stride);
     const uint32_t* src = (const uint32_t*)(e + 1);
     uint32_t* dst = mask + (size_t)row * tb.W;
-    for (int i = tid; i < tb.W; i += kBlock) dst[i] = src[i];
+    for (int i = tid; i < tb.W; i += kProThreads) dst[i] = src[i];
     if (tid == 0) {
       hdr->valid = kRowCached;
       hdr->pstat = (int32_t)e->status;
@@ -1214,7 +1215,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
       posts[t] = p;
       post[t] = p;
     }
-  } else if (tid == kBlock - 1) {
+  } else if (tid == kProThreads - 1) {
     eos_sigma = sim1_test<true, MW>(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, tb.T) == 2;
   }
   if (tid < 256) {
@@ -1241,8 +1242,8 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   __syncthreads();
   // the set jobs take the first kSetThreads threads, the gates the last wave
   // (a wave runs divergent branches one after the other)
-  constexpr int kSetThreads = kBlock - 64;
-  const int P = nA > 0 ? max(1, min(32, kSetThreads / nA)) : 1;
+  constexpr int kSetThreads = kProThreads - 64;
+  const int P = nA > 0 ? max(1, min(64, kSetThreads / nA)) : 1;
   const int n_set = nA * P;
   const bool set_lane = tid < kSetThreads;
   for (int j = set_lane ? tid : n_set + (tid - kSetThreads); j < (set_lane ? n_set : n_set + nA);
@@ -1291,8 +1292,8 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
   // phase 3: the trailing-flag tables of every DFA state under A(sigma) and
   // after the winner's shift, the bytes that continue the pending lexeme in
   // the lexicon (thread b), and the top of the stack for the residue walk
-  {
-    const uint32_t b = (uint32_t)tid;  // kBlock == 256: one byte value per thread
+  if (tid < 256) {  // whole waves: one byte value per thread
+    const uint32_t b = (uint32_t)tid;
     const uint32_t n1 = rem_empty ? kNoLex : lex_child(tb, sl, cfg.lexnode, b);
     const bool c = n1 != kNoLex;
     const uint64_t bal = __ballot(c);
@@ -1313,7 +1314,7 @@ __global__ __launch_bounds__(kBlock) void prologue_kernel(Tables tb, const grid_
     }
     uint8_t* clsA = rw + L.cls;
     uint8_t* clsW = clsA + pad16((uint32_t)tb.S);
-    for (int q = tid; q < tb.S; q += kBlock) {
+    for (int q = tid; q < tb.S; q += kProThreads) {
       clsA[q] = (uint8_t)trail_flags<MW>(tv, a0, q);
       clsW[q] = (uint8_t)trail_flags<MW>(tv, aw, q);
     }
@@ -1900,7 +1901,7 @@ __global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __r
 // spelling in the row's residue bitmap.  Rows served from the mask cache are
 // skipped; rows with a bad configuration get zero words.
 constexpr int kStreamWaves = kBlock / 64;
-constexpr int kStreamUnroll = 2;   // chunks per wave in flight
+constexpr int kStreamUnroll = 4;   // chunks per wave in flight
 constexpr int kStreamRounds = 1;
 constexpr int kStreamChunks = kStreamWaves * kStreamUnroll * kStreamRounds;
 
@@ -2654,14 +2655,27 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(const uint32_t* __restric
     const uint32_t bits = (mask[(size_t)row * W + (col >> 5)] >> (col & 31)) & 0xFFu;
     if (bits == 0xFFu) continue;
     T* p = logits + row * stride + col;
-    if (bits == 0 && col + 8 <= V && vec_ok) {
+    if (col + 8 <= V && vec_ok) {  // whole group: 16-byte stores, the kept logits read back unchanged
       if (sizeof(T) == 2) {
-        const uint32_t w2 = neg_inf_bits | (neg_inf_bits << 16);
-        *reinterpret_cast<uint4*>(p) = make_uint4(w2, w2, w2, w2);
+        uint4 v = bits ? *reinterpret_cast<const uint4*>(p) : make_uint4(0, 0, 0, 0);
+        uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t lo = (bits >> (2 * k)) & 1u ? w[k] & 0xFFFFu : neg_inf_bits;
+          const uint32_t hi = (bits >> (2 * k + 1)) & 1u ? w[k] & 0xFFFF0000u : neg_inf_bits << 16;
+          w[k] = lo | hi;
+        }
+        *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
       } else {
-        const uint4 v = make_uint4(neg_inf_bits, neg_inf_bits, neg_inf_bits, neg_inf_bits);
-        reinterpret_cast<uint4*>(p)[0] = v;
-        reinterpret_cast<uint4*>(p)[1] = v;
+        uint4 v0 = make_uint4(0, 0, 0, 0), v1 = v0;
+        if (bits & 0x0Fu) v0 = reinterpret_cast<const uint4*>(p)[0];
+        if (bits & 0xF0u) v1 = reinterpret_cast<const uint4*>(p)[1];
+        const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+        uint32_t o[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) o[k] = (bits >> k) & 1u ? w[k] : neg_inf_bits;
+        reinterpret_cast<uint4*>(p)[0] = make_uint4(o[0], o[1], o[2], o[3]);
+        reinterpret_cast<uint4*>(p)[1] = make_uint4(o[4], o[5], o[6], o[7]);
       }
       continue;
     }
@@ -3077,8 +3091,8 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
   if (!raise_lds((const void*)prologue_kernel<MW>, parse_bytes))
     return fail(GRID_E_HIP, "grid_mask: cannot raise the LDS limit");
   if (phases & GRID_PHASE_PROLOGUE) {
-    hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B), dim3(kBlock), parse_bytes, s, tb, cfg_dev, pool, mask, eos, ws,
-                       rb);
+    hipLaunchKernelGGL(prologue_kernel<MW>, dim3(B), dim3(kProThreads), parse_bytes, s, tb, cfg_dev, pool, mask, eos,
+                       ws, rb);
     const uint32_t vy = ((uint32_t)tb.max_classes + kBlock - 1) / kBlock;
     hipLaunchKernelGGL(verdict_kernel<MW>, dim3(B, vy), dim3(kBlock), verdict_lds(tb).total, s, tb, ws, rb);
   }
