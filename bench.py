@@ -89,23 +89,23 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def flatness(args):
+def flatness_one(args, k):
     """Cost per mask at positions n = 1k / 4k / 16k tokens and nesting depths
-    1 / 8 / 32 / 128 (32 configurations per cell, one batch each), and per depth
-    the least-squares slope of the per-mask cost against n with a 95% interval
-    (t quantile for the degrees of freedom); flat when |slope| x 15,000 stays
-    under 5 % of the cost at n = 1,000."""
+    1 / 8 / 32 / 128 (32 configurations per cell, one batch each) on workload
+    k, and per depth the least-squares slope of the per-mask cost against n
+    with a 95% interval (t quantile for the degrees of freedom); flat when
+    |slope| x 15,000 stays under 5 % of the cost at n = 1,000."""
     import torch
     import paper_2607_11951_amd as G
     from workloads import make_workload
     from scipy import stats
     dev = torch.device("cuda:0")
     t0 = time.time()
-    wl = make_workload(4)
+    wl = make_workload(k)
     grid, slots = G.from_workload(wl)
     grid.to_device(dev)
     B = wl.batch
-    log(f"16,000-token workload ready in {time.time() - t0:.0f}s")
+    log(f"workload {wl.name} ready in {time.time() - t0:.0f}s")
     stream = torch.cuda.current_stream()
     ws = grid.new_workspace(B, dev)
     mask = torch.empty((B, grid.W), dtype=torch.int32, device=dev)
@@ -129,10 +129,13 @@ def flatness(args):
         torch.cuda.synchronize()
         us = np.array([e0.elapsed_time(e1) * 1000.0 / B for e0, e1 in evs])
         samples[(n_pos, depth)] = us
+        toks = [wl.meta["cells"][j][2] for j in idx]
         cells.append({"n": n_pos, "depth": depth, "us_per_mask_median": float(np.median(us)),
                       "us_per_mask_p99": float(np.percentile(us, 99)),
+                      "tokens_min": int(min(toks)), "tokens_max": int(max(toks)),
                       "max_stack_depth": int(cfgs["stk_depth"].max())})
-        log(f"n={n_pos:6d} depth={depth:4d}: {np.median(us):.2f} us/mask (stack <= {int(cfgs['stk_depth'].max())})")
+        log(f"{wl.name} n={n_pos:6d} depth={depth:4d}: {np.median(us):.2f} us/mask "
+            f"(stack <= {int(cfgs['stk_depth'].max())})")
     slopes = []
     for depth in sorted({d for _, d in samples}):
         xs, ys = [], []
@@ -148,10 +151,19 @@ def flatness(args):
                        "ci95": [float(fit.slope - half), float(fit.slope + half)],
                        "cost_at_1k_us": base, "change_over_15k_tokens_pct": float(100.0 * fit.slope * 15000 / base),
                        "flat": bool(abs(fit.slope) * 15000 < 0.05 * base)})
-    print(json.dumps({"metric": "per-mask cost vs position n and nesting depth (flatness)",
-                      "unit": "us/mask", "steps_per_cell": args.steps, "batch": B, "vocab": wl.V,
-                      "workload": "read-only DML SQL, 16,000-token sentences, 32 configs per cell",
-                      "cells": cells, "slopes": slopes}), flush=True)
+    return {"workload": wl.name, "vocab": wl.V, "batch": B, "cells": cells, "slopes": slopes}
+
+
+def flatness(args):
+    """Flatness on the 16,000-token workload (every configuration its own
+    content) and on its position-isolated variant (the same local contexts
+    at the three positions, so a slope there is position alone); one JSON
+    line."""
+    out = {"metric": "per-mask cost vs position n and nesting depth (flatness)", "unit": "us/mask",
+           "steps_per_cell": args.steps,
+           "content_varies": flatness_one(args, 4),
+           "position_isolated": flatness_one(args, 6)}
+    print(json.dumps(out), flush=True)
 
 
 def device_batches(G, grid, wl, slots, dev):

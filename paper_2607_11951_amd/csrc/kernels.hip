@@ -2322,6 +2322,7 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
                                                                size_t rbytes, int B) {
   extern __shared__ __align__(16) uint8_t lds[];
   __shared__ int chunk_ctr;
+  __shared__ uint32_t row_allowed[kRowGroup];  // the walk allowed a spelling of the group's row
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const ResLds WL = res_lds(tb, MW, B);
@@ -2362,6 +2363,7 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
     const int items = 2 * gr * nsub;  // walk items of the group's rows first, then lexicon items
     const int mine = items > (int)blockIdx.x ? (items - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x : 0;
     bool blocks = false;  // the group's row blocks are in LDS
+    if (tid < kRowGroup) row_allowed[tid] = 0u;
     for (int k0 = 0; k0 < mine; k0 += kMaxItems) {
       const int n_it = min(kMaxItems, mine - k0);
       dma_wait();
@@ -2470,11 +2472,13 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
               lex ? (uint32_t)tb.cmap[(size_t)((const RowHeader*)rowblk)->q * tb.V + (rk.z & 0x7FFFFFFFu)] : 0u;
           if (residue_token<MW>(sh, *(const RowHeader*)rowblk, rowblk, rw, RL, u, rk, lex != 0, cls, lane_area) > 0) {
             allow_spelling(tb, mask + (size_t)(g0 + r) * tb.W, u, rk);
-            ((RowHeader*)rw)->nonempty = 1u;
+            row_allowed[r] = 1u;
           }
         }
       }
     }
+    __syncthreads();  // every wave is done with the group: one header store per row that got a token
+    if (tid < gr && row_allowed[tid]) ((RowHeader*)(rows + (size_t)(g0 + tid) * rbytes))->nonempty = 1u;
   }
   dma_wait();  // a workgroup without items still has its table copies in flight
 }

@@ -139,6 +139,26 @@ def test_long_sentences_positions_and_depths(G, oracle_mod):
     assert cfgs["stk_depth"].max() > 500
 
 
+def test_long_sentences_position_isolated(G, oracle_mod):
+    """The position-isolated 16,000-token workload the flatness measurement
+    also times: every configuration of the n = 16,000 cells (32 per depth,
+    B = 32, stacks up to several hundred states) against the oracle, and the
+    masks at n = 1,000 / 4,000 equal to those at 16,000 row for row (same
+    local context, only the position differs)."""
+    wl = make_workload(6)
+    cells = wl.meta["cells"]
+    rows = list(range(len(wl.prefixes)))
+    grid, gm, ge, gs = _gpu_masks(G, wl, rows)
+    assert (gs == 0).all()
+    far = [i for i in rows if cells[i][0] == 16000]
+    om, oe = _oracle_rows(oracle_mod, wl, far)
+    _compare(wl, far, gm[far], ge[far], gs[far], om, oe, "isolated")
+    for d in (1, 8, 32, 128):
+        by_pos = {p: [i for i in rows if cells[i][1] == d and cells[i][0] == p] for p in (1000, 4000, 16000)}
+        for a, b, c in zip(by_pos[1000], by_pos[4000], by_pos[16000]):
+            assert np.array_equal(gm[a], gm[c]) and np.array_equal(gm[b], gm[c]), (d, cells[a], cells[c])
+
+
 def test_worked_example_section_7_1_on_gpu(G, oracle_mod):
     """The paper's first worked example (section 7.1, the golden fixture)
     through the HIP path: the CRUD grammar under the analyst projection, the

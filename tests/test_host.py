@@ -85,6 +85,29 @@ def _lexp_hash(lo, hi, ln):
     return h ^ (h >> 12)
 
 
+def test_position_isolated_workload_contexts(G):
+    """The position-isolated long workload: the configurations at n = 1k, 4k
+    and 16k tokens that share an offset inside the repeated block have the
+    same scan state, pending bytes and stack; the token counts are near the
+    three positions."""
+    from workloads import make_workload
+    wl = make_workload(6)
+    grid, slots = G.from_workload(wl)
+    cells = wl.meta["cells"]
+    for d in (1, 8, 32, 128):
+        rows = {p: [i for i, c in enumerate(cells) if c[1] == d and c[0] == p] for p in (1000, 4000, 16000)}
+        assert all(len(v) == wl.batch for v in rows.values())
+        for a, b, c in list(zip(rows[1000], rows[4000], rows[16000]))[::7]:
+            got = [grid.config(wl.prefixes[i], slots[0]) for i in (a, b, c)]
+            for cfg, st in got[1:]:
+                for f in ("q", "lexnode", "flags", "rem_len"):
+                    assert int(cfg[f]) == int(got[0][0][f])
+                assert bytes(cfg["rem_head"]) == bytes(got[0][0]["rem_head"])
+                assert np.array_equal(st, got[0][1])
+            for i, p in ((a, 1000), (b, 4000), (c, 16000)):
+                assert p <= cells[i][2] < p + 200
+
+
 def test_lexicon_child_bitmaps_and_second_bytes(G):
     """LEX_CHILD: bit b of a trie node's bitmap is set exactly when some word
     of the slot continues the node's string with byte b (the node reached

@@ -166,8 +166,57 @@ def _long_rows(per_cell):
     return tuple(prefixes[i] for i in order), tuple(cells[i] for i in order)
 
 
+@functools.lru_cache(maxsize=None)
+def _long_rows_isolated(per_cell):
+    """Prefixes and (position, depth, tokens) cells of the position-isolated
+    variant of the 16,000-token workload: per nesting depth one sentence made
+    of a header (the nesting) and a fixed block of predicates repeated until
+    the text holds more than 16,000 tokens, with no random whitespace, so the
+    greedy tokenization is periodic in the repeated part.  The configurations
+    at n = 1k / 4k / 16k tokens end at the same offsets inside a block (token
+    boundaries that recur in every block), so their local context -- scan
+    state, pending bytes and the stack above the chain -- is the same at the
+    three positions and only the position differs."""
+    s = _schema3()
+    vocab, _, _ = _vocab4()
+    positions = [1000, 4000, 16000]
+    depths = [1, 8, 32, 128]
+    prefixes, cells = [], []
+    for d in depths:
+        r = random.Random(4501 + d)
+        g = sen.DmlQueryGen(r, s)
+        head, unit = g.periodic_sentence(d)
+        head_b, unit_b = head.encode("utf-8"), unit.encode("utf-8")
+        reps = 16000 // max(1, len(unit_b) // 8) + 64
+        text = head_b + unit_b * reps
+        ends = _greedy_tokenize(vocab, text, max(positions) + 4 * len(unit_b))
+        ulen, hlen = len(unit_b), len(head_b)
+
+        def unit_of(e):
+            return (e - hlen) // ulen, (e - hlen) % ulen
+
+        by_unit = {}
+        for i, e in enumerate(ends):
+            if e > hlen:
+                k, off = unit_of(e)
+                by_unit.setdefault(k, {})[off] = i + 1  # tokens up to and including this one
+        units = {}
+        for p in positions:
+            k = unit_of(ends[p - 1])[0] + 1
+            units[p] = k
+        common = sorted(set.intersection(*(set(by_unit[units[p]]) for p in positions)))
+        assert len(common) >= 4, "no recurring token boundaries"
+        offs = [common[(j * len(common)) // per_cell % len(common)] for j in range(per_cell)]
+        for p in positions:
+            k = units[p]
+            for off in offs:
+                prefixes.append(text[:hlen + k * ulen + off])
+                cells.append((p, d, by_unit[k][off]))
+    return tuple(prefixes), tuple(cells)
+
+
 def make_workload(k, n_batches=1, rows=None):
-    """Build workload k (1..5).  n_batches > 1 adds distinct batches of the same
+    """Build workload k (1..5; 6 is the position-isolated variant of 4).  n_batches > 1 adds distinct batches of the same
     shape (workloads 2, 3); rows limits the number of rows (tests)."""
     if k == 1:
         vocab = voc.config1_vocab(1000)
@@ -224,4 +273,12 @@ def make_workload(k, n_batches=1, rows=None):
         return Workload("sql_dml_cold_schema", "sql_dml", list(READ_ONLY_ROLE), vocab,
                         specials, eos, lexicons, prefixes, list(range(n)), n,
                         meta={"logits_seed": 5999, "logits_std": 2.0})
+    if k == 6:
+        s = _schema3()
+        vocab, specials, eos = _vocab4()
+        per_cell = 32 if rows is None else rows
+        prefixes, cells = _long_rows_isolated(per_cell)
+        return Workload("sql_dml_long_isolated", "sql_dml", list(READ_ONLY_ROLE), vocab, specials, eos,
+                        [s.lexicon(with_alias=True)], list(prefixes), [0] * len(prefixes), per_cell,
+                        meta={"cells": list(cells), "schema": s})
     raise ValueError(f"no workload {k}")

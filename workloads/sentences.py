@@ -667,6 +667,37 @@ class DmlQueryGen:
                 w.kw("OFFSET")
                 w.lit(str(r.randint(0, 1000)))
 
+    # -- periodic long sentences (flatness with the position isolated)
+    def periodic_sentence(self, depth, n_preds=4):
+        """(header, block): SELECT .. WHERE <depth nested parens / IN
+        subqueries>, then a block of n_preds simple predicates, each followed
+        by AND, meant to be repeated; single spaces, fixed keyword case."""
+        r = self.r
+        t = self.tname()
+        cols = lambda: r.choice(self.s.columns[t])
+        head = ["SELECT", cols(), "FROM", self.s.tables[t], "WHERE"]
+        for lvl in range(depth):
+            if lvl % 2 == 0:
+                head.append("(")
+            else:
+                head += [cols(), "IN", "("]
+                t = self.tname()
+                head += ["SELECT", cols(), "FROM", self.s.tables[t], "WHERE"]
+        block = []
+        for i in range(n_preds):
+            c = cols()
+            kind = i % 4
+            if kind == 0:
+                block += [c, "=", str(r.randint(0, 9999))]
+            elif kind == 1:
+                block += [c, "IS", "NULL"]
+            elif kind == 2:
+                block += [c, "IN", "(", str(r.randint(0, 99)), ",", str(r.randint(0, 99)), ")"]
+            else:
+                block += [c, "<>", "'" + "".join(r.choice("abcdefgh") for _ in range(4)) + "'"]
+            block.append("AND")
+        return " ".join(head) + " ", " ".join(block) + " "
+
     # -- long sentences with controlled nesting (position / depth stress)
     def long_sentence(self, depth, min_bytes):
         """SELECT .. WHERE <depth nested parens / IN-subqueries> <long AND/OR
