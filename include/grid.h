@@ -486,17 +486,23 @@ int grid_complete(const grid_compiled* g, int32_t slot, const uint8_t* w, size_t
  * does, or NULL); any other row gets -1 there and keeps its configuration,
  * and so do the later steps of a row that stopped (after -1 or after the
  * end-of-sequence token).  span_len_dev[b] is the number of forced tokens.
- * On return mask_dev / eos_dev / status_dev ([B, W] u32, [B] u8, [B] i32, as
- * grid_mask writes them) hold the mask of the rows' final configurations:
- * a row with span_len < max_len there allows several tokens (or is a row
- * that grid_mask reports with a status other than GRID_ROW_OK).  workspace
- * as grid_mask.  max_len + 1 mask calls and max_len advances are enqueued
- * on stream, nothing is synchronized; GRID_E_ARG for null pointers, B < 1,
- * max_len < 1 or stack_cap < 2. */
+ * A forced token whose advance fails (GRID_ROW_OVERFLOW: a stack beyond the
+ * in-place advance's LDS area) is taken back: the row ends its span before
+ * it, on the configuration it had.  On return mask_dev / eos_dev / status_dev
+ * ([B, W] u32, [B] u8, [B] i32, as grid_mask writes them) hold the mask of
+ * the rows' final configurations: a row with span_len < max_len there allows
+ * several tokens (or is a row that grid_mask reports with a status other
+ * than GRID_ROW_OK, or one whose advance failed).  workspace: device scratch
+ * of at least grid_forced_span_workspace_bytes(g, B) (grid_mask's plus 4
+ * bytes per row), 256-byte aligned.  max_len + 1 mask calls and max_len
+ * advances are enqueued on stream, nothing is synchronized; GRID_E_ARG for
+ * null pointers, B < 1, max_len < 1, stack_cap < 2 or a short workspace. */
 int grid_forced_span(const grid_compiled* g, int32_t B, grid_config* cfg_dev, uint16_t* stack_pool_dev,
                      uint64_t* stack_hash_dev, uint32_t stack_cap, int32_t max_len, int32_t* span_dev,
                      int32_t* span_len_dev, uint32_t* mask_dev, uint8_t* eos_dev, int32_t* status_dev,
                      void* workspace_dev, size_t workspace_bytes, void* stream);
+/* Workspace bytes grid_forced_span needs for B rows (0 for B < 1). */
+size_t grid_forced_span_workspace_bytes(const grid_compiled* g, int32_t B);
 
 /* -------------------------------------------------------------------- apply */
 #define GRID_DTYPE_F32 0

@@ -3081,10 +3081,27 @@ int residue_grid_size(uint32_t lds) {
   if (!raise_lds((const void*)residue_kernel<MW>, lds)) return -1;
   int dev = 0, cus = 0, per_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -1;
+  // the answer per (device, LDS size), looked up once: the occupancy query
+  // costs more host time than a small batch's whole mask on the device
+  struct Entry {
+    int dev;
+    uint32_t lds;
+    int blocks;
+  };
+  static std::mutex mu;
+  static Entry seen[64];
+  static int n_seen = 0;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    for (int i = 0; i < n_seen; ++i)
+      if (seen[i].dev == dev && seen[i].lds == lds) return seen[i].blocks;
+  }
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, residue_kernel<MW>, kWalkThreads, lds) != hipSuccess ||
       per_cu <= 0)
     per_cu = 1;
+  std::lock_guard<std::mutex> lock(mu);
+  if (n_seen < 64) seen[n_seen++] = {dev, lds, cus * per_cu};
   return cus * per_cu;
 }
 
@@ -3109,8 +3126,10 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
     const ResLds RL = res_lds(tb, MW, B);
     const int resident = residue_grid_size<MW>(RL.total);
     if (resident <= 0) return fail(GRID_E_HIP, "grid_mask: cannot raise the residue walk's LDS limit");
-    hipLaunchKernelGGL(residue_kernel<MW>, dim3(resident), dim3(kWalkThreads), RL.total, s, tb, pool, mask, ws, rb,
-                       B);
+    // no more workgroups than work items (a small vocabulary has few)
+    const long long items = 2ll * std::min(B, RL.group) * ((tb.U + 63) / 64);
+    const int blocks = (int)std::max(1ll, std::min((long long)resident, items));
+    hipLaunchKernelGGL(residue_kernel<MW>, dim3(blocks), dim3(kWalkThreads), RL.total, s, tb, pool, mask, ws, rb, B);
   }
   if (phases & GRID_PHASE_FINALIZE) {
     hipLaunchKernelGGL(finalize_kernel<MW>, dim3(B), dim3(kBlock), 0, s, tb, cfg_dev, pool, mask, ws, rb, status);
@@ -3475,10 +3494,15 @@ extern "C" int grid_accept_inplace(const grid_compiled* g, int32_t B, grid_confi
 // one token (the end-of-sequence token counts when its bit is set) takes it
 // as span[row][i]; any other row, a row whose mask call did not end OK, and a
 // row whose span already stopped (a non-forced step, or the end-of-sequence
-// token) gets -1.  span_len[row] counts the forced tokens.
+// token) gets -1.  Before that, a row whose advance by span[row][i - 1]
+// failed (acc_status neither OK nor FINISHED; its configuration is then
+// unchanged) has that token taken back and stops.  span_len[row] counts the
+// forced tokens.  With take == 0 only the check of the last advance runs.
 __global__ __launch_bounds__(kBlock) void singleton_kernel(const uint32_t* __restrict__ mask,
-                                                           const int32_t* __restrict__ status, int32_t* span,
-                                                           int32_t* span_len, int W, int max_len, int i, int eos_id) {
+                                                           const int32_t* __restrict__ status,
+                                                           const int32_t* __restrict__ acc_status, int32_t* span,
+                                                           int32_t* span_len, int W, int max_len, int i, int eos_id,
+                                                           int take) {
   const int row = (int)blockIdx.x, tid = (int)threadIdx.x;
   __shared__ int count, word;
   if (tid == 0) {
@@ -3488,18 +3512,26 @@ __global__ __launch_bounds__(kBlock) void singleton_kernel(const uint32_t* __res
   __syncthreads();
   const uint32_t* m = mask + (size_t)row * W;
   int c = 0, wd = -1;
-  for (int w = tid; w < W; w += kBlock) {
-    const int k = __popc(m[w]);
-    c += k;
-    if (k) wd = w;
+  if (take) {
+    for (int w = tid; w < W; w += kBlock) {
+      const int k = __popc(m[w]);
+      c += k;
+      if (k) wd = w;
+    }
   }
   if (c) atomicAdd(&count, c);
   if (wd >= 0) atomicMax(&word, wd);
   __syncthreads();
   if (tid != 0) return;
   int32_t* sp = span + (size_t)row * max_len;
-  bool open = i == 0 || (sp[i - 1] >= 0 && sp[i - 1] != eos_id);
   if (i == 0) span_len[row] = 0;
+  bool open = i == 0 || (sp[i - 1] >= 0 && sp[i - 1] != eos_id);
+  if (i > 0 && sp[i - 1] >= 0 && acc_status[row] != GRID_ROW_OK && acc_status[row] != GRID_ROW_FINISHED) {
+    sp[i - 1] = -1;  // not applied: the row keeps the configuration before it
+    span_len[row] = i - 1;
+    open = false;
+  }
+  if (!take) return;
   int tok = -1;
   if (open && count == 1 && (!status || status[row] == GRID_ROW_OK)) tok = word * 32 + __ffs((int)m[word]) - 1;
   sp[i] = tok;
@@ -3512,25 +3544,36 @@ extern "C" int grid_forced_span(const grid_compiled* g, int32_t B, grid_config* 
                                 void* workspace_dev, size_t workspace_bytes, void* stream) {
   clear_error();
   if (!g || B <= 0 || !cfg_dev || !stack_pool_dev || !span_dev || !span_len_dev || !mask_dev || !status_dev ||
-      max_len < 1 || stack_cap < 2)
+      !workspace_dev || max_len < 1 || stack_cap < 2)
     return fail(GRID_E_ARG, "grid_forced_span: null pointer or bad size");
+  const size_t mask_ws = workspace_size(g, B);
+  if (workspace_bytes < mask_ws + (size_t)B * 4u)
+    return fail(GRID_E_ARG, "grid_forced_span: workspace smaller than grid_forced_span_workspace_bytes");
+  // the advances' statuses live after the mask workspace
+  int32_t* acc_status = (int32_t*)((uint8_t*)workspace_dev + mask_ws);
   const int W = (g->vocab.V + 31) / 32;
   hipStream_t s = (hipStream_t)stream;
   for (int i = 0; i <= max_len; ++i) {
-    int rc = mask_call(g, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, workspace_dev, workspace_bytes,
-                       nullptr, 0, 0, GRID_PHASE_ALL, stream);
+    int rc = mask_call(g, B, cfg_dev, stack_pool_dev, mask_dev, eos_dev, status_dev, workspace_dev, mask_ws, nullptr,
+                       0, 0, GRID_PHASE_ALL, stream);
     if (rc != GRID_OK) return rc;
-    if (i == max_len) break;  // the mask of the final configurations
-    hipLaunchKernelGGL(singleton_kernel, dim3((unsigned)B), dim3(kBlock), 0, s, mask_dev, status_dev, span_dev,
-                       span_len_dev, W, max_len, i, g->vocab.eos_id);
-    // rows with -1 are left as they are (reported as bad configurations to no one)
+    const int take = i < max_len ? 1 : 0;  // the last round only checks the last advance
+    hipLaunchKernelGGL(singleton_kernel, dim3((unsigned)B), dim3(kBlock), 0, s, mask_dev, status_dev, acc_status,
+                       span_dev, span_len_dev, W, max_len, i, g->vocab.eos_id, take);
+    if (!take) break;
+    // rows with -1 are left as they are (their status is not needed)
     rc = accept_call(g, B, cfg_dev, stack_pool_dev, span_dev + i, cfg_dev, stack_pool_dev, stack_hash_dev, stack_cap,
-                     nullptr, 1, stream, max_len);
+                     acc_status, 1, stream, max_len);
     if (rc != GRID_OK) return rc;
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_forced_span launch: ") + hipGetErrorString(e));
   return GRID_OK;
+}
+
+extern "C" size_t grid_forced_span_workspace_bytes(const grid_compiled* g, int32_t B) {
+  if (!g || B <= 0) return 0;
+  return workspace_size(g, B) + (size_t)B * 4u;
 }
 
 extern "C" int grid_apply(const uint32_t* mask_dev, void* logits_dev, int32_t dtype, int32_t B, int32_t V,

@@ -44,7 +44,7 @@ EXPORTS = ["grid_compile", "grid_free", "grid_last_error", "grid_info", "grid_ad
            "grid_cache_bytes", "grid_cache_clear", "grid_mask_cached", "grid_accept",
            "grid_mask_noalloc_max_bytes", "grid_mask_noalloc", "grid_stack_hash", "grid_stack_hash_host",
            "grid_accept_inplace", "grid_ci_cache_bytes", "grid_ci_cache_clear", "grid_mask_warm",
-           "grid_complete", "grid_forced_span"]
+           "grid_complete", "grid_forced_span", "grid_forced_span_workspace_bytes"]
 CI_LOOKUP, CI_INSERT, CI_FAMILY, CI_GENN = 1, 2, 4, 8
 PHASE_PROLOGUE, PHASE_WALK, PHASE_RESIDUE, PHASE_FINALIZE, PHASE_ALL = 1, 2, 4, 8, 15
 
@@ -108,6 +108,8 @@ def lib():
         L.grid_accept_inplace.argtypes = [vp, i32, vp, vp, vp, ctypes.c_uint32, vp, vp, vp]
         L.grid_complete.argtypes = [vp, i32, ctypes.c_char_p, sz, i32, vp, ctypes.POINTER(i32)]
         L.grid_forced_span.argtypes = [vp, i32, vp, vp, vp, ctypes.c_uint32, i32, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.grid_forced_span_workspace_bytes.argtypes = [vp, i32]
+        L.grid_forced_span_workspace_bytes.restype = sz
         L.grid_ci_cache_bytes.argtypes = [vp, i32]
         L.grid_ci_cache_bytes.restype = sz
         L.grid_ci_cache_clear.argtypes = [vp, vp, sz, vp]
@@ -289,7 +291,7 @@ class Grid:
         eos = torch.empty(B, dtype=torch.uint8, device=dev)
         status = torch.empty(B, dtype=torch.int32, device=dev)
         if workspace is None:
-            workspace = self.new_workspace(B, dev)
+            workspace = torch.empty(lib().grid_forced_span_workspace_bytes(self.h, B), dtype=torch.uint8, device=dev)
         hp = ctypes.c_void_p(stack_hash.data_ptr()) if stack_hash is not None else None
         _check(lib().grid_forced_span(self.h, B, ctypes.c_void_p(cfg_dev.data_ptr()),
                                       ctypes.c_void_p(pool_dev.data_ptr()), hp, stack_cap, max_len,

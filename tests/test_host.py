@@ -548,6 +548,17 @@ def test_cache_sizes_and_argument_errors(G):
                                   None, None, ctypes.c_void_p(256), ctypes.c_size_t(1 << 30),
                                   ctypes.c_void_p(256), ctypes.c_size_t(stride * 3), 3, None)
     assert rc != 0
+    # the forced-span call: its workspace is grid_mask's plus one status per row;
+    # a short one or a null pointer is refused before anything is launched
+    for B in (1, 7, 32):
+        assert G.lib().grid_forced_span_workspace_bytes(g.h, B) == g.workspace_bytes(B) + 4 * B
+    assert G.lib().grid_forced_span_workspace_bytes(g.h, 0) == 0
+    p = ctypes.c_void_p(256)
+    rc = G.lib().grid_forced_span(g.h, 2, p, p, None, 64, 4, p, p, p, p, p, p,
+                                  ctypes.c_size_t(g.workspace_bytes(2)), None)
+    assert rc == -1 and b"workspace" in G.lib().grid_last_error()
+    rc = G.lib().grid_forced_span(g.h, 2, p, p, None, 64, 0, p, p, p, p, p, p, ctypes.c_size_t(1 << 30), None)
+    assert rc == -1
 
 
 def _state_symbols(grid):
