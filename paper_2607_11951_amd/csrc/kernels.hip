@@ -1595,9 +1595,10 @@ struct SpellBytes {
 // judged again with its own lexemes' lexicon flags.
 constexpr uint32_t kVerdictReject = 0, kVerdictAllow = 1, kVerdictWalk = 2, kVerdictLexicon = 3;
 
-// Answers of a lexicon policy besides flags: the question is open (the
-// verdict kernel, which has no token bytes), or the lexeme is out of reach
-// of the lookup tables (the token takes the byte walk).
+// Answers of a lexicon policy besides flags: the question is open (no
+// answer: the class is decided by the lexicon), or the lexeme is out of
+// reach of the lookup tables (the token takes the byte walk).  kLexOpen also
+// marks a lexeme whose flags were not asked for yet.
 constexpr uint32_t kLexOpen = 0xFFFFFFFFu, kLexOut = 0xFFFFFFFEu;
 
 // Verdict of one lexeme-program class for a row.  The lexemes the token
@@ -1707,12 +1708,6 @@ __device__ __forceinline__ uint32_t class_verdict(const RowHeader& h, const uint
   return (pf & cats) ? kVerdictAllow : kVerdictReject;
 }
 
-// Lexicon policy of the verdict kernel: it has no token bytes.
-struct LexOpen {
-  __device__ uint32_t word(uint32_t) { return kLexOpen; }
-  __device__ uint32_t trail() { return kLexOpen; }
-};
-
 // A lexeme of the class record that starts in the start state at byte 0 or 1
 // of the token: the token-flag table (GRID_ART_LEX_TOKEN) answers for it.
 // Its start offset, or -1.  Lexeme 0 and a trailing lexeme after no end hold
@@ -1764,19 +1759,29 @@ struct LexNo {
 // when the token has one (a trailing lexeme, or a word ending at offset 2 or
 // later).
 constexpr uint32_t kNoValid = 1u << 7;
+// The class's code and, for a class the lexicon decides, its shortcut, from
+// one verdict run: the run under "no flags" follows the run without token
+// bytes up to the first lexicon question, so a class that asks none has its
+// final verdict there, and one that asks is a lexicon class whose verdict
+// under "no flags" is the run's result.  Returns the code; *rule receives
+// the shortcut byte of a lexicon class.
 template <int MW>
-__device__ __forceinline__ uint32_t class_shortcut(const RowHeader& h, const uint32_t* I, const uint32_t* live,
-                                                   const uint32_t* tinfo, const uint32_t* acc_off,
-                                                   const uint8_t* acc_list, const uint32_t* a2, uint4 rec) {
+__device__ __forceinline__ uint32_t class_code(const RowHeader& h, const uint32_t* I, const uint32_t* live,
+                                               const uint32_t* tinfo, const uint32_t* acc_off, const uint8_t* acc_list,
+                                               const uint32_t* a2, uint4 rec, uint32_t* rule) {
   LexNo ln{rec.w, rec.x & kClassEndsMask, h.rem_len == 0, -1, -1, false, false};
   const uint32_t v = class_verdict<MW>(h, I, live, 8, tinfo, acc_off, acc_list, a2, 8, rec, ln);
-  if (ln.kind < 0 || ln.second || v == kVerdictLexicon) return kVerdictLexicon;
+  if (ln.kind < 0) return v;  // no lexicon question: the class's verdict
+  *rule = kVerdictLexicon;
+  if (ln.second) return kVerdictLexicon;
   if (ln.pending) {
     const bool two = ln.kind == 0 || (rec.w & 0xFFu) >= 2u;
-    return kVerdictLexicon | (two ? 1u << 4 : 0u) | v << 5 | kNoValid;
+    *rule = kVerdictLexicon | (two ? 1u << 4 : 0u) | v << 5 | kNoValid;
+    return kVerdictLexicon;
   }
   if (ln.start < 0) return kVerdictLexicon;
-  return kVerdictLexicon | (ln.kind == 0 ? 1u : 2u) << 2 | (uint32_t)ln.start << 4 | v << 5 | kNoValid;
+  *rule = kVerdictLexicon | (ln.kind == 0 ? 1u : 2u) << 2 | (uint32_t)ln.start << 4 | v << 5 | kNoValid;
+  return kVerdictLexicon;
 }
 
 // LDS layout of the verdict kernel: live sets and the row's allowed sets
@@ -1870,13 +1875,13 @@ __global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __r
     uint32_t code = kVerdictReject;
     if (c < n) {
       const uint4 rec = c0 == blockIdx.y * (uint32_t)kBlock ? rec0 : tb.crec[h.cls_base + c];
-      LexOpen lex;
-      if (h.ci_hit >= 0 && ci_class(rec.x))  // served by the row's cached context-independent words
+      if (h.ci_hit >= 0 && ci_class(rec.x)) {  // served by the row's cached context-independent words
         code = kVerdictReject;
-      else
-        code = class_verdict<MW>(h, I_s, live_s, 8, tinfo_s, acc_off_s, acc_list_s, a2_s, 8, rec, lex);
-      if (code == kVerdictLexicon)
-        vr[c] = (uint8_t)class_shortcut<MW>(h, I_s, live_s, tinfo_s, acc_off_s, acc_list_s, a2_s, rec);
+      } else {
+        uint32_t rule = 0;
+        code = class_code<MW>(h, I_s, live_s, tinfo_s, acc_off_s, acc_list_s, a2_s, rec, &rule);
+        if (code == kVerdictLexicon) vr[c] = (uint8_t)rule;
+      }
     }
     const uint64_t b0 = __ballot(code & 1u), b1 = __ballot(code & 2u);
     // this wave's 64 classes are words (c0 + 64 * wave) / 16 .. + 3 of the table
