@@ -373,9 +373,9 @@ int grid_mask_cached(const grid_compiled* g, int32_t B, const grid_config* cfg_d
  *    restricts is live or accepting in q); otherwise the raw remainder stays.
  * A hit row takes its CI words from the entry (its CI classes are neither
  * judged nor walked); a miss computes the cold mask and, with
- * GRID_CI_INSERT, claims a slot in the prologue and publishes the row's CI
- * words after finalize (rows that do not end with status OK release their
- * claim).  Masks are bit-identical with and without the cache.  Entries are
+ * GRID_CI_INSERT, claims a slot in the prologue, writes its CI tokens' bits
+ * into it as the mask kernels decide them, and publishes it when the row
+ * ends with status OK (other rows release their claim).  Masks are bit-identical with and without the cache.  Entries are
  * written once and never evicted; a probe window (8 slots) that is full leaves
  * the row uncached.  Concurrent calls may share a cache (claims by atomic
  * compare-and-swap, published entries only are read). */

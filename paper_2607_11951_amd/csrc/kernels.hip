@@ -1889,6 +1889,7 @@ __global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __r
       const uint32_t first = c0 + (uint32_t)(tid & ~63) + 16u * (uint32_t)lane;
       if (first < n) vc[first >> 4] = interleave16((uint32_t)(b0 >> (16 * lane)), (uint32_t)(b1 >> (16 * lane)));
     }
+
   }
 }
 
@@ -1939,6 +1940,11 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
   // a row served by cached context-independent words ORs them into its words
   const int ci = hdr->ci_hit;
   const uint32_t* ciw = ci >= 0 ? (const uint32_t*)(tb.ci_cache + (size_t)ci * tb.ci_stride + kCiHeader) : nullptr;
+  // a row that claimed an entry writes its CI tokens' bits there (the residue
+  // pass adds those it decides; finalize publishes the entry)
+  const int claim = hdr->ci_claim;
+  uint32_t* cdst = claim >= 0 ? (uint32_t*)(tb.ci_cache + (size_t)claim * tb.ci_stride + kCiHeader) : nullptr;
+  const uint4* crow = tb.crec + hdr->cls_base;
   // the row's 2-bit class codes are read where the class map points (an
   // L2-resident gather: staging all of them in LDS per workgroup cost more)
   const uint32_t* vg = (const uint32_t*)(rw + RL.vcode);
@@ -1962,6 +1968,7 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
   // pass 2: codes; for a class the lexicon decides, its shortcut byte and the
   // token's first byte and token flags (again all loads in flight together)
   uint32_t code[kPer], sc[kPer], fb[kPer], tf[kPer], sb[kPer];
+  bool cib[kPer];
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
     const int c = c_lo + wave + j * kStreamWaves;
@@ -1972,6 +1979,7 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
     fb[j] = lexq ? tb.id_first[id] : 0u;
     sb[j] = lexq ? tb.id_second[id] : 0u;
     tf[j] = lexq ? tflags[id] : 0u;
+    cib[j] = cdst && c < c_hi && id < tb.V ? ci_class(crow[cls[j]].x) : false;
   }
   // pass 2b: a pending-lexeme question on a lexeme that holds the token's
   // second byte, after a first byte that continues the lexeme: the second
@@ -2004,6 +2012,10 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
     if (ciw) cw = (uint64_t)ciw[2 * c] | (2 * c + 1 < tb.W ? (uint64_t)ciw[2 * c + 1] << 32 : 0ull);
     any = any || (al | cw) != 0;
     if (lane < 2 && 2 * c + lane < tb.W) mrow[2 * c + lane] = (uint32_t)((al | cw) >> (32 * lane));
+    if (cdst) {  // uniform: the claimed entry's words (the end-of-sequence bit is never cached)
+      const uint64_t cb = __ballot(cib[j] && cd == kVerdictAllow && id < tb.V && id != tb.eos_id);
+      if (lane < 2 && 2 * c + lane < tb.W) cdst[2 * c + lane] = (uint32_t)(cb >> (32 * lane));
+    }
     if (cd >= kVerdictWalk && id < tb.V) resu[j] = (uint32_t)id;
     code[j] = cd;
   }
@@ -2475,8 +2487,13 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
           // aliases share it)
           const uint32_t cls =
               lex ? (uint32_t)tb.cmap[(size_t)((const RowHeader*)rowblk)->q * tb.V + (rk.z & 0x7FFFFFFFu)] : 0u;
-          if (residue_token<MW>(sh, *(const RowHeader*)rowblk, rowblk, rw, RL, u, rk, lex != 0, cls, lane_area) > 0) {
+          const RowHeader& hh = *(const RowHeader*)rowblk;
+          // a lexicon spelling of a CI class also goes to the row's claimed CI-words entry
+          const bool ci_tok = lex && hh.ci_claim >= 0 && ci_class(tb.crec[hh.cls_base + cls].x);
+          if (residue_token<MW>(sh, hh, rowblk, rw, RL, u, rk, lex != 0, cls, lane_area) > 0) {
             allow_spelling(tb, mask + (size_t)(g0 + r) * tb.W, u, rk);
+            if (ci_tok)
+              allow_spelling(tb, (uint32_t*)(tb.ci_cache + (size_t)hh.ci_claim * tb.ci_stride + kCiHeader), u, rk);
             row_allowed[r] = 1u;
           }
         }
@@ -2561,7 +2578,13 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
         const int ok = walk_bytes<false, MW>(rc, ln, cfg.q, lex0, 0u, tb.spell_off[su + 1] - base, byte_at, step,
                                              ov, kSlowLane, 1u);
         if (ok > 0) {
-          allow_spelling(tb, mask + (size_t)row * tb.W, su, tb.spell_rec[su]);
+          const uint4 rk = tb.spell_rec[su];
+          allow_spelling(tb, mask + (size_t)row * tb.W, su, rk);
+          if (hdr->ci_claim >= 0) {  // a CI-class spelling also goes to the row's claimed entry
+            const uint32_t cls = tb.cmap[(size_t)cfg.q * tb.V + (rk.z & 0x7FFFFFFFu)];
+            if (ci_class(tb.crec[hdr->cls_base + cls].x))
+              allow_spelling(tb, (uint32_t*)(tb.ci_cache + (size_t)hdr->ci_claim * tb.ci_stride + kCiHeader), su, rk);
+          }
           slow_ok = 1;
         } else if (ok < 0) {
           atomicOr(&hdr->wstat, GRID_ROW_OVERFLOW);
@@ -2581,6 +2604,11 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
     }
     if (status) status[row] = st;
     hdr->fstat = st;
+    if (valid && hdr->ci_claim >= 0) {  // publish the row's CI-words entry, or give the slot back
+      uint32_t* e = (uint32_t*)(tb.ci_cache + (size_t)hdr->ci_claim * tb.ci_stride);
+      __threadfence();
+      __hip_atomic_store(e, st == GRID_ROW_OK ? 2u : 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 }
 
@@ -2607,50 +2635,17 @@ __global__ __launch_bounds__(kBlock) void cache_publish_kernel(Tables tb, const 
   }
 }
 
-// Context-independent words write-back: every row that claimed an entry in
-// the prologue and ended with status OK stores the allowed bits of its
-// context-independent tokens (from its finished mask; the end-of-sequence
-// bit left out); one wave per 64 ids, grid (chunk groups, row).
-__global__ __launch_bounds__(kBlock) void ci_publish_kernel(Tables tb, const uint32_t* __restrict__ mask,
-                                                            const uint8_t* __restrict__ ws, size_t rbytes) {
-  const int row = (int)blockIdx.y, lane = (int)(threadIdx.x & 63u);
-  const RowHeader* hdr = (const RowHeader*)(ws + kWsHead + (size_t)row * rbytes);
-  if (hdr->valid != kRowValid || hdr->ci_claim < 0 || hdr->fstat != GRID_ROW_OK) return;  // uniform
-  const int c = (int)(blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6));
-  if (c * 64 >= tb.V) return;  // uniform across the wave
-  const int id = c * 64 + lane;
-  const uint32_t* mrow = mask + (size_t)row * tb.W;
-  bool keep = false;
-  if (id < tb.V && id != tb.eos_id) {
-    const uint32_t cls = tb.cmap[(size_t)hdr->q * tb.V + id];
-    keep = ci_class(tb.crec[hdr->cls_base + cls].x) && ((mrow[id >> 5] >> (id & 31)) & 1u);
-  }
-  const uint64_t b = __ballot(keep);
-  uint32_t* dst = (uint32_t*)(tb.ci_cache + (size_t)hdr->ci_claim * tb.ci_stride + kCiHeader);
-  if (lane < 2 && 2 * c + lane < tb.W) dst[2 * c + lane] = (uint32_t)(b >> (32 * lane));
-}
-
-// Publishes the entries written above (a device-scope fence orders the words
-// before the state word); a claim whose row did not end OK is released.
-__global__ __launch_bounds__(64) void ci_seal_kernel(Tables tb, const uint8_t* __restrict__ ws, size_t rbytes, int B) {
-  const int row = (int)(blockIdx.x * 64u + threadIdx.x);
-  if (row >= B) return;
-  const RowHeader* hdr = (const RowHeader*)(ws + kWsHead + (size_t)row * rbytes);
-  if (hdr->valid != kRowValid || hdr->ci_claim < 0) return;
-  uint32_t* e = (uint32_t*)(tb.ci_cache + (size_t)hdr->ci_claim * tb.ci_stride);
-  __threadfence();
-  __hip_atomic_store(e, hdr->fstat == GRID_ROW_OK ? 2u : 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// ------------------------------------------------------------------- apply
-// Each thread covers 8 consecutive logits of one row; the mask byte for them
-// comes from one word.  Fully masked groups take one or two 16-byte stores.
 // Empties a mask cache: every entry's state word to 0.
 __global__ __launch_bounds__(kBlock) void cache_clear_kernel(uint8_t* cache, uint32_t n, uint32_t stride) {
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock)
     ((CacheEntry*)(cache + (size_t)i * stride))->state = 0u;
 }
 
+// ------------------------------------------------------------------- apply
+// Each thread covers 8 consecutive logits of one row; the mask byte for them
+// comes from one word.  An aligned group takes 16-byte stores (read first
+// when it keeps entries, whose bits are written back unchanged); a group at
+// a ragged row end or in an unaligned row is written logit by logit.
 template <typename T>
 __global__ __launch_bounds__(kBlock) void apply_kernel(const uint32_t* __restrict__ mask, T* logits, int B,
                                                        int V, int W, int64_t stride, uint32_t neg_inf_bits,
@@ -3140,11 +3135,7 @@ int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint1
     hipLaunchKernelGGL(finalize_kernel<MW>, dim3(B), dim3(kBlock), 0, s, tb, cfg_dev, pool, mask, ws, rb, status);
     if (tb.cache && (tb.cache_flags & GRID_CACHE_INSERT))
       hipLaunchKernelGGL(cache_publish_kernel, dim3(B), dim3(kBlock), 0, s, tb, mask, ws, rb);
-    if (tb.ci_cache && (tb.ci_flags & GRID_CI_INSERT)) {
-      const int groups = ((tb.V + 63) / 64 + kBlock / 64 - 1) / (kBlock / 64);
-      hipLaunchKernelGGL(ci_publish_kernel, dim3((unsigned)groups, (unsigned)B), dim3(kBlock), 0, s, tb, mask, ws, rb);
-      hipLaunchKernelGGL(ci_seal_kernel, dim3((unsigned)((B + 63) / 64)), dim3(64), 0, s, tb, ws, rb, B);
-    }
+
   }
   return GRID_OK;
 }
