@@ -1271,6 +1271,45 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
       if (cand) eos_after[t] = sim1_test<true, MW>(pt, bs, p.k, p.m, ov, my, kPostCap + kTmpCap, tb.T) == 2;
     }
   }
+  if (tid == kProThreads - 1) {
+    // context-independent words, by the gate wave's last thread while the set
+    // jobs run: probe the row's key (A(sigma) is known); a published entry
+    // serves the row's CI tokens, an empty slot on the way is claimed
+    int ci_hit = -1, ci_claim = -1;
+    if (tb.ci_cache && !overflow) {
+      uint32_t a_sig[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) a_sig[k] = A[k];
+      uint32_t key[kCiKeyWords];
+      ci_key(tb, cfg, sl, a_sig, R, key);
+      uint64_t home = 0x8F1BBCDC2C2D6A1Bull;
+      for (int k = 0; k < kCiKeyWords; ++k) home = stack_mix((uint32_t)k, key[k], home);
+      for (int pr = 0; pr < kCacheProbes; ++pr) {
+        const uint32_t idx = (uint32_t)(home + (uint64_t)pr) & tb.ci_mask;
+        uint32_t* e = (uint32_t*)(tb.ci_cache + (size_t)idx * tb.ci_stride);
+        const uint32_t st = __hip_atomic_load(e, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+        if (st == 2u) {
+          bool same = true;
+          for (int k = 0; k < kCiKeyWords; ++k) same = same && e[1 + k] == key[k];
+          if (same && (tb.ci_flags & GRID_CI_LOOKUP)) {
+            ci_hit = (int)idx;
+            break;
+          }
+          continue;
+        }
+        if (st == 0u) {
+          if (!(tb.ci_flags & GRID_CI_INSERT)) break;
+          if (atomicCAS(e, 0u, 1u) == 0u) {
+            for (int k = 0; k < kCiKeyWords; ++k) e[1 + k] = key[k];
+            ci_claim = (int)idx;
+            break;
+          }
+        }
+      }
+    }
+    hdr->ci_hit = ci_hit;
+    hdr->ci_claim = ci_claim;
+  }
   // the pending lexeme's winner if a byte ends it
   if (tid == 0 && !rem_empty) {
     uint32_t a0[MW];
@@ -1350,42 +1389,6 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
     hdr->cls_base = tb.coff[cfg.q];
     hdr->n_cls = tb.coff[cfg.q + 1] - tb.coff[cfg.q];
     hdr->pstat = overflow ? GRID_ROW_OVERFLOW : GRID_ROW_OK;
-    // context-independent words: probe the row's key; a published entry
-    // serves the row's CI tokens, an empty slot on the way is claimed
-    int ci_hit = -1, ci_claim = -1;
-    if (tb.ci_cache && !overflow) {
-      uint32_t a_sig[8];
-#pragma unroll
-      for (int k = 0; k < 8; ++k) a_sig[k] = A[k];
-      uint32_t key[kCiKeyWords];
-      ci_key(tb, cfg, sl, a_sig, R, key);
-      uint64_t home = 0x8F1BBCDC2C2D6A1Bull;
-      for (int k = 0; k < kCiKeyWords; ++k) home = stack_mix((uint32_t)k, key[k], home);
-      for (int pr = 0; pr < kCacheProbes; ++pr) {
-        const uint32_t idx = (uint32_t)(home + (uint64_t)pr) & tb.ci_mask;
-        uint32_t* e = (uint32_t*)(tb.ci_cache + (size_t)idx * tb.ci_stride);
-        const uint32_t st = __hip_atomic_load(e, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-        if (st == 2u) {
-          bool same = true;
-          for (int k = 0; k < kCiKeyWords; ++k) same = same && e[1 + k] == key[k];
-          if (same && (tb.ci_flags & GRID_CI_LOOKUP)) {
-            ci_hit = (int)idx;
-            break;
-          }
-          continue;
-        }
-        if (st == 0u) {
-          if (!(tb.ci_flags & GRID_CI_INSERT)) break;
-          if (atomicCAS(e, 0u, 1u) == 0u) {
-            for (int k = 0; k < kCiKeyWords; ++k) e[1 + k] = key[k];
-            ci_claim = (int)idx;
-            break;
-          }
-        }
-      }
-    }
-    hdr->ci_hit = ci_hit;
-    hdr->ci_claim = ci_claim;
     hdr->valid = kRowValid;
   }
 }
