@@ -472,7 +472,10 @@ int grid_accept_inplace(const grid_compiled* g, int32_t B, grid_config* cfg_dev,
  * so the completion is short but not proven shortest.  GRID_E_NOT_VIABLE for
  * a prefix outside Prefix(L); GRID_E_CAPACITY when the completion needs more
  * than max_tokens tokens (*out_n is then its length) or none is found within
- * the search budget. */
+ * the search budget (60,000 expansions, 256 MiB of search nodes).  Host
+ * only; safe to call from several threads on one handle, though not during
+ * grid_add_lexicon on it (the writer's tables are built once, under the
+ * handle's lock). */
 int grid_complete(const grid_compiled* g, int32_t slot, const uint8_t* w, size_t n, int32_t max_tokens,
                   int32_t* out_tokens, int32_t* out_n);
 

@@ -252,7 +252,11 @@ extern "C" int grid_complete(const grid_compiled* g, int32_t slot, const uint8_t
     open.push({estimate(stack), 0});
     std::unordered_set<std::string> visited;
     int goal = -1;
-    for (int expansions = 0; !open.empty() && expansions < 60000; ++expansions) {
+    // the search is bounded by expansions and by the bytes its nodes hold
+    // (every node keeps its whole stack: deep prefixes make nodes large)
+    constexpr size_t kSearchBytes = size_t(256) << 20;
+    size_t held = stack.size() * 2;
+    for (int expansions = 0; !open.empty() && expansions < 60000 && held < kSearchBytes; ++expansions) {
       const int idx = open.top().idx;
       open.pop();
       std::vector<uint16_t> st = nodes[idx].stack;
@@ -285,6 +289,7 @@ extern "C" int grid_complete(const grid_compiled* g, int32_t slot, const uint8_t
         lr_simulate(P, child, t, true);
         const std::string step = std::string(1, (char)W.seps[0]) + best;
         const int c = nodes[idx].cost + count_tokens(W, max_len, step);
+        held += child.size() * 2 + nodes[idx].text.size() + step.size() + sizeof(SNode);
         nodes.push_back({std::move(child), nodes[idx].text + step, c});
         open.push({(long)c + estimate(nodes.back().stack), (int)nodes.size() - 1});
       }
