@@ -588,14 +588,15 @@ __device__ __forceinline__ bool pop_len(uint32_t len, uint32_t& k, int& m, int& 
 
 // A chain step needs the state under the popped entries.  With one entry
 // popped it is the state that was under the top (`below`, when known); with
-// none, the top itself; else it is read.
+// none, the top itself; else it is read -- only then, so a run of unit
+// reductions waits for no stack read.
 template <bool L>
 __device__ __forceinline__ uint32_t goto_source(const BaseStack<L>& bs, uint32_t len, uint32_t s, uint32_t below,
                                                 uint32_t k, int m, mptr<L, const uint16_t> ov, int t,
                                                 mptr<L, const uint16_t> tmp) {
-  const uint32_t sb = len == 0 ? s : below;
-  const uint32_t top = stack_at_top<L>(bs, k, m, ov, t, tmp);  // read in every case: fewer branches
-  return (len > 1 || sb == kNoState) ? top : sb;
+  uint32_t sb = len == 0 ? s : below;
+  if (len > 1 || sb == kNoState) sb = stack_at_top<L>(bs, k, m, ov, t, tmp);
+  return sb;
 }
 
 // Reduce chain of terminal x, not changing the stack (pushes go to tmp).  1
