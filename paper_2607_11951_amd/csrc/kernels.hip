@@ -131,6 +131,7 @@ struct Tables {
   uint32_t ci_flags;          // GRID_CI_*
   uint32_t ci_stride;         // bytes per entry
   uint32_t family_fp;         // fingerprint of the lexer and vocabulary (the grammar family)
+  uint32_t ign[8];            // the ignored terminals (term_info bit 0), one bit each
 };
 
 // ------------------------------------------------------------- mask cache
@@ -1034,13 +1035,13 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
   }
   uint32_t s_top = 0;
   if (shape_ok && lo + (uint32_t)tid < depth) s_top = pool[cfg.stk_off + lo + tid];
+  // the row's lexicon slot and this thread's terminal info, in the same round trip
+  const Slot sl = shape_ok ? load_slot(tb, cfg.slot) : Slot{0, 0, 0, 0, 0, 0, 0, 0, 0};
+  const uint32_t ti = tid < tb.T ? tb.term_info[tid] : 0u;
   const ParseTabs<true> pt = lds_parse(tb, plds, PL);
   if (tid == 0) {
     int b = shape_ok ? 0 : 1;
-    if (!b) {
-      Slot sl = load_slot(tb, cfg.slot);
-      if (cfg.lexnode != kNoLex && cfg.lexnode >= sl.nodes) b = 1;
-    }
+    if (!b && cfg.lexnode != kNoLex && cfg.lexnode >= sl.nodes) b = 1;
     bad = b;
     overflow = 0;
     winner = -1;
@@ -1176,18 +1177,15 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
     }
     return;
   }
-  const Slot sl = load_slot(tb, cfg.slot);
   if (tid < 8) {
-    I[tid] = 0;
+    I[tid] = tb.ign[tid];
     R[tid] = 0;
     A[tid] = 0;
     Aw[tid] = 0;
   }
   __syncthreads();
-  if (tid < tb.T) {  // ignored and restricted terminals, one per thread
-    const uint32_t ti = tb.term_info[tid];
+  if (tid < tb.T) {  // restricted terminals, one per thread
     const uint32_t c = (ti >> 8) & 0xFFu;
-    if (ti & 1u) atomicOr(&I[tid >> 5], 1u << (tid & 31));
     if (c != 0xFFu && ((sl.restricted >> c) & 1u)) atomicOr(&R[tid >> 5], 1u << (tid & 31));
   }
   const BaseStack<true> bs{pool + cfg.stk_off, in_mem<true>((const uint16_t*)win), depth, lo};
@@ -1840,6 +1838,7 @@ __global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __r
   const int tid = threadIdx.x, lane = tid & 63;
   uint8_t* rw = ws + kWsHead + (size_t)blockIdx.x * rbytes;
   if (tid < (int)(sizeof(RowHeader) / 4)) ((uint32_t*)&h)[tid] = ((const uint32_t*)rw)[tid];
+  if (tid < 8) I_s[tid] = tb.ign[tid];
   __syncthreads();
   const uint32_t n = h.n_cls;
   if (h.valid != kRowValid || blockIdx.y * (uint32_t)kBlock >= n) return;  // uniform
@@ -1862,15 +1861,6 @@ __global__ __launch_bounds__(kBlock) void verdict_kernel(Tables tb, uint8_t* __r
     dma_regions<5>(rg, tid, kBlock);
   }
   dma_wait();
-  __syncthreads();
-  if (tid < 8) {
-    uint32_t iw = 0;
-    for (int j = 0; j < 32; ++j) {
-      const int t = tid * 32 + j;
-      if (t < tb.T && (tinfo_s[t] & 1u)) iw |= 1u << j;
-    }
-    I_s[tid] = iw;
-  }
   __syncthreads();
   uint32_t* vc = (uint32_t*)(rw + RL.vcode);
   uint8_t* vr = rw + RL.vrule;
@@ -2378,7 +2368,7 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
                                 parse_region(tb, lds, WL.pl, 3)};
     dma_regions<10>(rg, tid, kWalkThreads);
   }
-  bool staged = false;
+  if (tid < 8) I_s[tid] = tb.ign[tid];
   for (int g0 = 0; g0 < B; g0 += WL.group) {
     const int gr = min(WL.group, B - g0);
     const int items = 2 * gr * nsub;  // walk items of the group's rows first, then lexicon items
@@ -2387,16 +2377,21 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
     if (tid < kRowGroup) row_allowed[tid] = 0u;
     for (int k0 = 0; k0 < mine; k0 += kMaxItems) {
       const int n_it = min(kMaxItems, mine - k0);
-      dma_wait();
-      __syncthreads();  // the previous round is done with umask_s / upre_s; the tables are in LDS
-      for (int t = tid; t < n_it; t += kWalkThreads) {
-        const int j = (int)blockIdx.x + (k0 + t) * (int)gridDim.x;
+      // this thread's item word, loaded before the wait for the table copies
+      static_assert(kMaxItems == kWalkThreads, "one item word per thread");
+      uint64_t uw = 0ull;
+      if (tid < n_it) {
+        const int j = (int)blockIdx.x + (k0 + tid) * (int)gridDim.x;
         const int lex = j >= gr * nsub ? 1 : 0, jr = j - lex * gr * nsub;
         const int r = jr / nsub;
         const uint8_t* rw = rows + (size_t)(g0 + r) * rbytes;
         const uint32_t v = ((const RowHeader*)rw)->valid;
-        umask_s[t] = v == kRowValid ? ((const uint64_t*)(rw + RL.rbits))[(lex ? 0 : nsub) + jr - r * nsub] : 0ull;
+        const uint64_t word = ((const uint64_t*)(rw + RL.rbits))[(lex ? 0 : nsub) + jr - r * nsub];
+        uw = v == kRowValid ? word : 0ull;
       }
+      dma_wait();
+      __syncthreads();  // the previous round is done with umask_s / upre_s; the tables are in LDS
+      if (tid < n_it) umask_s[tid] = uw;
       if (tid == 0) chunk_ctr = 0;
       __syncthreads();
       if (tid < 64) {  // prefix counts of set bits over the items (one wave)
@@ -2425,17 +2420,6 @@ __global__ __launch_bounds__(kWalkThreads) void residue_kernel(Tables tb, const 
       __syncthreads();
       const int n_und = (int)upre_s[n_it];
       if (n_und == 0) continue;  // uniform
-      if (!staged) {  // the ignored set from the staged terminal info, once per workgroup
-        if (tid < 8) {
-          uint32_t iw = 0;
-          for (int j = 0; j < 32; ++j) {
-            const int t = tid * 32 + j;
-            if (t < tb.T && (tinfo_s[t] & 1u)) iw |= 1u << j;
-          }
-          I_s[tid] = iw;
-        }
-        staged = true;
-      }
       if (!blocks) {  // the rows' blocks, two 16-byte chunks per thread in flight at a time
         const uint32_t n16 = WL.block / 16u, tot16 = (uint32_t)gr * n16;
         for (uint32_t i = tid; i < tot16; i += 2u * kWalkThreads) {
@@ -2534,14 +2518,7 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Tables tb, const grid_
   __shared__ int slow_ok;
   if (tid == 0) slow_ok = 0;
   if (count > 0) {  // uniform
-    if (tid < 8) {
-      uint32_t iw = 0;
-      for (int j = 0; j < 32; ++j) {
-        const int t = tid * 32 + j;
-        if (t < tb.T && (tb.term_info[t] & 1u)) iw |= 1u << j;
-      }
-      I_s[tid] = iw;
-    }
+    if (tid < 8) I_s[tid] = tb.ign[tid];
     const ParseTabs<false> pt = global_parse(tb);  // rare: tables stay in global memory
     __syncthreads();
     if (tid < kSlowThreads) {
@@ -3227,6 +3204,9 @@ static int bind_tables(const grid_compiled* g, Tables& tb) {
   tb.n_pshift = (int)g->parser.pshift.size();
   tb.n_acc = (int)g->dfa.accept_list.size();
   tb.hbits = g->parser.goto_hbits;
+  for (int w = 0; w < 8; ++w) tb.ign[w] = 0;
+  for (int t = 0; t < tb.T && t < 256; ++t)
+    if (g->term_info[t] & 1u) tb.ign[t >> 5] |= 1u << (t & 31);
   return GRID_OK;
 }
 
