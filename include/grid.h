@@ -226,8 +226,12 @@ enum {
                                rolling configuration hash */
   GRID_ART_LEX_CHILD,       /* u32 [8] per lexicon-trie node (all slots, indexed like
                                LEX_FLAGS): bit b set when the node has a child on byte b */
-  GRID_ART_ID_SECOND,       /* u16 [V]: 0x100 | second byte of each token id's spelling,
-                               0 for spellings shorter than two bytes and specials */
+  GRID_ART_ID_HEAD,         /* u32 [V]: the first two bytes of each token id's spelling:
+                               first byte | second byte << 8 | 0x10000 when the spelling
+                               has a second byte (0 for specials and empty tokens) */
+  GRID_ART_LEX_TOKSUM,      /* u8 [slots][V]: which entries of LEX_TOKEN are nonzero: bit
+                               2o set when the prefix flags from offset o are, bit 2o + 1
+                               when the word flags from offset o are (o = 0, 1) */
   GRID_ART_COUNT
 };
 int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);

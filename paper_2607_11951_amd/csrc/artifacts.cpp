@@ -113,12 +113,13 @@ VocabArtifacts build_vocab(const uint8_t* bytes, const uint64_t* off, int V, con
   va.byte_complete = std::all_of(single.begin(), single.end(), [](char c) { return c != 0; });
   va.spell_of_id.assign(V, 0xFFFFFFFFu);
   va.id_first.assign(V, 0);
-  va.id_second.assign(V, 0);
+  va.id_head.assign(V, 0);
   for (size_t u = 0; u < U; ++u)
     for (uint32_t k = va.alias_off[u]; k < va.alias_off[u + 1]; ++k) {
       va.spell_of_id[va.alias_ids[k]] = (uint32_t)u;
       va.id_first[va.alias_ids[k]] = (uint8_t)uniq[u][0];
-      if (uniq[u].size() > 1) va.id_second[va.alias_ids[k]] = (uint16_t)(0x100u | (uint8_t)uniq[u][1]);
+      va.id_head[va.alias_ids[k]] =
+          (uint8_t)uniq[u][0] | (uniq[u].size() > 1 ? 0x10000u | (uint32_t)(uint8_t)uniq[u][1] << 8 : 0u);
     }
   // first-byte range of every 64 consecutive spellings (first bytes are
   // non-decreasing, so the first and the last spelling of the group bound it)
@@ -426,6 +427,7 @@ void add_lexicon(LexiconStore& st, const LexerDfa& dfa, const GrammarText& g, co
   // the first lexeme maximal munch cuts from o (scanning from the start state)
   const size_t tok_base = st.token.size();
   st.token.resize(tok_base + (size_t)va.V, 0u);
+  st.toksum.resize(tok_base + (size_t)va.V, 0u);
   if (restricted) {
     const size_t U = va.spell_off.size() - 1;
     for (size_t u = 0; u < U; ++u) {
@@ -451,7 +453,14 @@ void add_lexicon(LexiconStore& st, const LexerDfa& dfa, const GrammarText& g, co
         }
         f |= (pre | word << 8) << (16 * o);
       }
-      for (uint32_t k = va.alias_off[u]; k < va.alias_off[u + 1]; ++k) st.token[tok_base + va.alias_ids[k]] = f;
+      uint8_t sum = 0;  // bit 2o: prefix flags from o nonzero; bit 2o + 1: word flags from o nonzero
+      for (int o = 0; o < 2; ++o)
+        for (int k = 0; k < 2; ++k)
+          if ((f >> (16 * o + 8 * k)) & 0xFFu) sum |= (uint8_t)(1u << (2 * o + k));
+      for (uint32_t k = va.alias_off[u]; k < va.alias_off[u + 1]; ++k) {
+        st.token[tok_base + va.alias_ids[k]] = f;
+        st.toksum[tok_base + va.alias_ids[k]] = sum;
+      }
     }
   }
   // the schema fingerprint: FNV-1a over the restricted categories and their

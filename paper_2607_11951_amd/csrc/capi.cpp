@@ -159,7 +159,7 @@ extern "C" int grid_add_lexicon(grid_compiled* g, const grid_lexicon_args* la, i
     // lexicon artifacts changed: device copies must be re-bound
     g->dev[GRID_ART_LEX_FLAGS] = g->dev[GRID_ART_LEX_HASH] = g->dev[GRID_ART_LEX_SLOTS] = nullptr;
     g->dev[GRID_ART_LEX_PREFIX] = g->dev[GRID_ART_LEX_STRIDE] = g->dev[GRID_ART_LEX_TOKEN] = nullptr;
-    g->dev[GRID_ART_LEX_CHILD] = nullptr;
+    g->dev[GRID_ART_LEX_CHILD] = g->dev[GRID_ART_LEX_TOKSUM] = nullptr;
     return GRID_OK;
   } catch (const Error& e) {
     return fail(e.code, e.what());
@@ -216,7 +216,8 @@ extern "C" int grid_artifact(const grid_compiled* g, int32_t which, const void**
     case GRID_ART_GOTO_HASH: put(g->parser.goto_hash, p, n); break;
     case GRID_ART_STATE_SYMBOL: put(g->parser.state_sym, p, n); break;
     case GRID_ART_LEX_CHILD: put(g->lex.child_bits, p, n); break;
-    case GRID_ART_ID_SECOND: put(g->vocab.id_second, p, n); break;
+    case GRID_ART_ID_HEAD: put(g->vocab.id_head, p, n); break;
+    case GRID_ART_LEX_TOKSUM: put(g->lex.toksum, p, n); break;
     default: return fail(GRID_E_ARG, "unknown artifact " + std::to_string(which));
   }
   return GRID_OK;

@@ -118,7 +118,7 @@ struct VocabArtifacts {
   std::vector<uint16_t> sub_range;   // per 64 spellings: lowest | highest first byte << 8
   std::vector<uint32_t> spell_of_id; // [V]: spelling index, 0xFFFFFFFF none
   std::vector<uint8_t> id_first;     // [V]: first byte of the spelling, 0 none
-  std::vector<uint16_t> id_second;   // [V]: second byte of the spelling | 0x100, 0 none
+  std::vector<uint32_t> id_head;     // [V]: first byte | second byte << 8 | 0x10000 if it has one
   std::vector<uint32_t> alias_off;   // [U+1]
   std::vector<int32_t> alias_ids;
   std::vector<uint32_t> level_off;   // [Lmax+2]
@@ -148,6 +148,7 @@ struct LexiconStore {
   std::vector<uint32_t> prefix;    // all slots' prefix-table entries (4 u32 each)
   std::vector<uint32_t> stride;    // all slots' stride-table entries (8 u32 each)
   std::vector<uint32_t> token;     // all slots' token flags ([V] u32 each)
+  std::vector<uint8_t> toksum;     // all slots' token-flag summaries ([V] u8 each: nonzero bytes of token)
   std::vector<uint32_t> slots;     // kSlotWords u32 per slot
   int n_slots = 0;
   // host-side lookup helpers

@@ -108,8 +108,8 @@ struct Tables {
   const uint4* lex_prefix;
   const uint4* lex_stride;    // [entries][2]
   const uint32_t* lex_token;  // [slots][V] token flags at start offsets 0 and 1
-  const uint8_t* id_first;    // [V] first byte of each token
-  const uint16_t* id_second;  // [V] 0x100 | second byte of each token, 0 none
+  const uint32_t* id_head;    // [V] first byte | second byte << 8 | 0x10000 if it has one
+  const uint8_t* lex_toksum;  // [slots][V] nonzero bytes of each token-flag entry
   const uint32_t* lex_child;  // [nodes][8] child bytes of every lexicon-trie node
   const uint16_t* cmap;       // class of each token per lexer state [S][V]
   const uint32_t* coff;       // [S+1] first class record of each state
@@ -180,7 +180,7 @@ struct RowHeader {
   uint32_t A[8];              // allowed terminals of sigma
   uint32_t Aw[8];             // allowed terminals after shifting the winner
   uint32_t R[8];              // terminals whose category the row's lexicon restricts
-  uint32_t slot[kSlotWords];  // the row's lexicon slot record
+  uint32_t slot[kSlotWords];  // the row's lexicon slot record (the words Slot holds; the rest 0)
   uint32_t cont[8];           // bytes b such that (pending lexeme) b prefixes a lexicon word
   uint32_t eos_ok;
   uint32_t valid;
@@ -431,6 +431,30 @@ constexpr uint32_t kPrologueParseMax = 92 * 1024;
 __host__ __device__ inline ParseLds prologue_parse_lds(const Tables& tb) {
   const ParseLds d = parse_lds(tb, 0, true);
   return d.total <= kPrologueParseMax ? d : parse_lds(tb, 0, false);
+}
+
+// The prologue's dynamic LDS: the LR tables, then (when they fit beside
+// them) the lexer's accept lists and live sets and the terminal info.
+struct ProLds {
+  ParseLds pl;
+  uint32_t acc_off, acc_list, live, tinfo, total;
+  int lexer;  // the lexer tables are staged (else read from global memory)
+};
+__host__ __device__ inline ProLds prologue_lds(const Tables& tb) {
+  ProLds P;
+  P.pl = prologue_parse_lds(tb);
+  uint32_t o = P.pl.total;
+  P.acc_off = o;
+  o += pad16((uint32_t)(tb.S + 1) * 4u);
+  P.acc_list = o;
+  o += pad16((uint32_t)tb.n_acc);
+  P.live = o;
+  o += pad16((uint32_t)tb.S * 32u);
+  P.tinfo = o;
+  o += pad16((uint32_t)tb.T * 4u);
+  P.lexer = o <= kPrologueParseMax ? 1 : 0;
+  P.total = P.lexer ? o : P.pl.total;
+  return P;
 }
 
 __device__ inline StageRegion parse_region(const Tables& tb, uint8_t* lds, const ParseLds& L, int which) {
@@ -1022,21 +1046,39 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
   Post* post = (Post*)(rw + L.post);
   uint32_t* a2 = (uint32_t*)(rw + L.a2);
   const grid_config cfg = cfgs[row];
-  const ParseLds PL = prologue_parse_lds(tb);
+  const ProLds PR = prologue_lds(tb);
+  const ParseLds PL = PR.pl;
   const uint32_t depth = cfg.stk_depth;
   const uint32_t lo = depth > (uint32_t)kStackWin ? depth - kStackWin : 0;
-  // one round trip to memory: the LR tables go straight to LDS while every
-  // thread loads one entry of the top kStackWin stack entries
+  // one round trip to memory: the LR tables (and the lexer's accept lists and
+  // live sets and the terminal info) go straight to LDS while every thread
+  // loads one entry of the top kStackWin stack entries
   const bool shape_ok = cfg.q < tb.S && cfg.slot < tb.n_slots && depth >= 1;  // uniform
-  {
+  if (PR.lexer) {
+    const StageRegion rg[8] = {parse_region(tb, plds, PL, 0),
+                               parse_region(tb, plds, PL, 1),
+                               parse_region(tb, plds, PL, 2),
+                               parse_region(tb, plds, PL, 3),
+                               {(const uint8_t*)tb.acc_off, plds + PR.acc_off, (uint32_t)(tb.S + 1) * 4u},
+                               {tb.acc_list, plds + PR.acc_list, (uint32_t)tb.n_acc},
+                               {(const uint8_t*)tb.live, plds + PR.live, (uint32_t)tb.S * 32u},
+                               {(const uint8_t*)tb.term_info, plds + PR.tinfo, (uint32_t)tb.T * 4u}};
+    dma_regions<8>(rg, tid, kProThreads);
+  } else {
     const StageRegion rg[4] = {parse_region(tb, plds, PL, 0), parse_region(tb, plds, PL, 1),
                                parse_region(tb, plds, PL, 2), parse_region(tb, plds, PL, 3)};
     dma_regions<4>(rg, tid, kProThreads);
   }
+  const uint32_t* acc_off = PR.lexer ? (const uint32_t*)(plds + PR.acc_off) : tb.acc_off;
+  const uint8_t* acc_list = PR.lexer ? (const uint8_t*)(plds + PR.acc_list) : tb.acc_list;
+  const uint32_t* live = PR.lexer ? (const uint32_t*)(plds + PR.live) : tb.live;
+  const uint32_t* tinfo = PR.lexer ? (const uint32_t*)(plds + PR.tinfo) : tb.term_info;
   uint32_t s_top = 0;
   if (shape_ok && lo + (uint32_t)tid < depth) s_top = pool[cfg.stk_off + lo + tid];
-  // the row's lexicon slot and this thread's terminal info, in the same round trip
+  // the row's lexicon slot, its class range and this thread's terminal info,
+  // in the same round trip
   const Slot sl = shape_ok ? load_slot(tb, cfg.slot) : Slot{0, 0, 0, 0, 0, 0, 0, 0, 0};
+  const uint32_t cls_lo = shape_ok ? tb.coff[cfg.q] : 0u, cls_hi = shape_ok ? tb.coff[cfg.q + 1] : 0u;
   const uint32_t ti = tid < tb.T ? tb.term_info[tid] : 0u;
   const ParseTabs<true> pt = lds_parse(tb, plds, PL);
   if (tid == 0) {
@@ -1190,15 +1232,31 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
   }
   const BaseStack<true> bs{pool + cfg.stk_off, in_mem<true>((const uint16_t*)win), depth, lo};
   const mptr<true, uint16_t> my = in_mem<true>(&sim_area[tid][0]);
-  const TermView tv{tb.term_info, I, R, tb.live, 8};
+  const TermView tv{tinfo, I, R, live, 8};
   __syncthreads();
 
   // phase 1: terminal t's reduce chain and shift from sigma (thread t; A(sigma)
   // is the set that shifted, the stacks after the shifts go to LDS and the
   // row's workspace); a spare thread runs the end-of-sequence gate from sigma
-  // itself (empty remainder, or an ignored winner)
+  // itself (empty remainder, or an ignored winner); the upper waves meanwhile
+  // find the bytes that continue the pending lexeme in the lexicon (thread
+  // 256 + b for byte b) and, after each, the bytes that continue it further
+  // (the child bitmap of that trie node)
+  static_assert(kProThreads == 512, "the upper 256 threads probe one byte value each");
   const bool rem_empty = (cfg.flags & 1u) != 0;
-  if (tid < tb.T) {
+  if (tid >= 256) {  // whole waves
+    const uint32_t b = (uint32_t)tid - 256u;
+    const uint32_t n1 = rem_empty ? kNoLex : lex_child(tb, sl, cfg.lexnode, b);
+    const bool c = n1 != kNoLex;
+    const uint64_t bal = __ballot(c);
+    if ((b & 31) == 0) hdr->cont[b >> 5] = (uint32_t)(bal >> (b & 32));
+    if (c) {
+      const uint4* src = reinterpret_cast<const uint4*>(tb.lex_child + (size_t)(sl.fbase + n1) * 8u);
+      uint4* dst = reinterpret_cast<uint4*>(rw + L.cont2 + (size_t)b * 32u);
+      dst[0] = src[0];
+      dst[1] = src[1];
+    }
+  } else if (tid < tb.T) {
     const int t = tid;
     uint32_t k = depth;
     int m = 0;
@@ -1214,7 +1272,7 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
       posts[t] = p;
       post[t] = p;
     }
-  } else if (tid == kProThreads - 1) {
+  } else if (tid == 255) {  // at most 255 terminals: never a terminal's thread
     eos_sigma = sim1_test<true, MW>(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, tb.T) == 2;
   }
   if (tid < 256) {
@@ -1266,9 +1324,17 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
         if (acc[w]) atomicOr(&a2_s[t][w], acc[w]);
     } else if (!rem_empty) {
       bool cand = false;
-      for (uint32_t q = tb.acc_off[cfg.q]; q < tb.acc_off[cfg.q + 1]; ++q) cand = cand || tb.acc_list[q] == t;
+      for (uint32_t q = acc_off[cfg.q]; q < acc_off[cfg.q + 1]; ++q) cand = cand || acc_list[q] == t;
       if (cand) eos_after[t] = sim1_test<true, MW>(pt, bs, p.k, p.m, ov, my, kPostCap + kTmpCap, tb.T) == 2;
     }
+  }
+  // the pending lexeme's winner if a byte ends it (the gate wave's first
+  // thread, while the set jobs run)
+  if (tid == kSetThreads && !rem_empty) {
+    uint32_t a0[MW];
+#pragma unroll
+    for (int w = 0; w < MW; ++w) a0[w] = A[w];
+    winner = winner_of<MW>(tv, acc_off, acc_list, a0, cfg.q, [&]() { return lex_flags_of(tb, sl, cfg.lexnode); });
   }
   if (tid == kProThreads - 1) {
     // context-independent words, by the gate wave's last thread while the set
@@ -1309,14 +1375,6 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
     hdr->ci_hit = ci_hit;
     hdr->ci_claim = ci_claim;
   }
-  // the pending lexeme's winner if a byte ends it
-  if (tid == 0 && !rem_empty) {
-    uint32_t a0[MW];
-#pragma unroll
-    for (int w = 0; w < MW; ++w) a0[w] = A[w];
-    winner = winner_of<MW>(tv, tb.acc_off, tb.acc_list, a0, cfg.q,
-                           [&]() { return lex_flags_of(tb, sl, cfg.lexnode); });
-  }
   __syncthreads();
   const int w = winner;
   const bool w_shifts = w >= 0 && !bit_of(I, w);
@@ -1328,21 +1386,7 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
   if (tid == 0) eos_ok = (rem_empty || (w >= 0 && !w_shifts)) ? eos_sigma : (w >= 0 ? (int)eos_after[w] : 0);
   __syncthreads();
   // phase 3: the trailing-flag tables of every DFA state under A(sigma) and
-  // after the winner's shift, the bytes that continue the pending lexeme in
-  // the lexicon (thread b), and the top of the stack for the residue walk
-  if (tid < 256) {  // whole waves: one byte value per thread
-    const uint32_t b = (uint32_t)tid;
-    const uint32_t n1 = rem_empty ? kNoLex : lex_child(tb, sl, cfg.lexnode, b);
-    const bool c = n1 != kNoLex;
-    const uint64_t bal = __ballot(c);
-    if ((tid & 31) == 0) hdr->cont[tid >> 5] = (uint32_t)(bal >> (tid & 32));
-    if (c) {  // and the bytes that continue it after b: the child bytes of its trie node
-      const uint4* src = reinterpret_cast<const uint4*>(tb.lex_child + (size_t)(sl.fbase + n1) * 8u);
-      uint4* dst = reinterpret_cast<uint4*>(rw + L.cont2 + (size_t)b * 32u);
-      dst[0] = src[0];
-      dst[1] = src[1];
-    }
-  }
+  // after the winner's shift, and the top of the stack for the residue walk
   {
     uint32_t a0[MW], aw[MW];
 #pragma unroll
@@ -1366,7 +1410,12 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
     hdr->Aw[tid] = Aw[tid];
     hdr->R[tid] = R[tid];
   }
-  if (tid < kSlotWords) hdr->slot[tid] = tb.lex_slots[(size_t)cfg.slot * kSlotWords + tid];
+  if (tid == 0) {  // the slot's table bases and masks (its other words are not used on the device side)
+    const uint32_t sw[kSlotWords] = {sl.fbase, sl.hbase, sl.hmask, sl.restricted, sl.nodes, sl.pbase,
+                                     sl.pmask, sl.sbase, sl.smask, 0u,       0u,       0u};
+#pragma unroll
+    for (int k = 0; k < kSlotWords; ++k) hdr->slot[k] = sw[k];
+  }
   if (tid == 0) {
     hdr->eos_ok = (uint32_t)eos_ok;
     if (eos_out) eos_out[row] = (uint8_t)eos_ok;
@@ -1385,8 +1434,8 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
     hdr->wstat = 0;
     hdr->nonempty = 0;
     hdr->slot_id = cfg.slot;
-    hdr->cls_base = tb.coff[cfg.q];
-    hdr->n_cls = tb.coff[cfg.q + 1] - tb.coff[cfg.q];
+    hdr->cls_base = cls_lo;
+    hdr->n_cls = cls_hi - cls_lo;
     hdr->pstat = overflow ? GRID_ROW_OVERFLOW : GRID_ROW_OK;
     hdr->valid = kRowValid;
   }
@@ -1522,24 +1571,41 @@ __device__ __forceinline__ int walk_bytes(const RowCtx<L>& rc, Lane<MW>& ln, int
   int status = 2;         // 2 running, else the result
   int pend = -1;          // byte class waiting for an emission
   uint32_t pend_b = 0;    // that byte
+  // look-ahead, so that a byte costs one round trip to LDS: byte i and its
+  // class (b0, c0), the DFA step on it from q (nx), byte i + 1 and its class
+  // (b1, c1); each byte is fetched once, in increasing order, and only below n
+  uint32_t b0 = i < n ? byte_at(i) : 0u;
+  uint32_t b1 = i + 1 < n ? byte_at(i + 1) : 0u;
+  uint32_t c0 = step.cls(b0), c1 = step.cls(b1);
+  int nx = i < n ? step.next(q, c0) : kDead;
   // f: trailing flags after the last byte taken (the caller's, before any)
   for (;;) {
     for (;;) {  // scan phase
       const bool run = status == 2 && pend < 0 && i < n;
       if (!__any(run)) break;
       if (run) {
-        const uint32_t b = byte_at(i);
-        const uint32_t c = step.cls(b);
-        const int nq = step.next(q, c);
-        if (nq != kDead) {
-          q = nq;
-          if (lx.need) lex_push(tb, rc.sl, lx, b);
+        if (nx != kDead) {
+          q = nx;
+          if (lx.need) lex_push(tb, rc.sl, lx, b0);
+          // byte i's flags, the step on byte i + 1 and byte i + 2's class
+          // depend on q or on nothing: issued together
+          const uint32_t b2 = i + 2 < n ? byte_at(i + 2) : 0u;
+          const uint32_t c2 = step.cls(b2);
+          const int nx1 = i + 1 < n ? step.next(q, c1) : kDead;
           f = ctab ? (uint32_t)ctab[q] : trail_flags<MW>(rc.tv, ln.acur, q);
-          if (f == 0) status = 0;
-          else ++i;
+          if (f == 0) {
+            status = 0;
+          } else {
+            ++i;
+            b0 = b1;
+            c0 = c1;
+            nx = nx1;
+            b1 = b2;
+            c1 = c2;
+          }
         } else {
-          pend = (int)c;
-          pend_b = b;
+          pend = (int)c0;
+          pend_b = b0;
         }
       }
     }
@@ -1553,11 +1619,22 @@ __device__ __forceinline__ int walk_bytes(const RowCtx<L>& rc, Lane<MW>& ln, int
         status = r;
       } else {
         ctab = ln.mode == 0 ? rc.clsA : (ln.mode == 1 && ln.t1 == rc.winner ? rc.clsW : nullptr);
-        q = step.next(kStart, (uint32_t)pend);
+        q = step.next(kStart, (uint32_t)pend);  // byte i starts the next lexeme
+        const uint32_t b2 = q != kDead && i + 2 < n ? byte_at(i + 2) : 0u;
+        const uint32_t c2 = step.cls(b2);
+        const int nx1 = q != kDead && i + 1 < n ? step.next(q, c1) : kDead;
         f = q == kDead ? 0u : (ctab ? (uint32_t)ctab[q] : trail_flags<MW>(rc.tv, ln.acur, q));
         lx = LexState{pend_b, 1u, kNoLex, track && (f & 2u) ? 1u : 0u};
-        if (f == 0) status = 0;
-        else ++i;
+        if (f == 0) {
+          status = 0;
+        } else {
+          ++i;
+          b0 = b1;
+          c0 = c1;
+          nx = nx1;
+          b1 = b2;
+          c1 = c2;
+        }
         pend = -1;
       }
     }
@@ -1943,7 +2020,7 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
   // L2-resident gather: staging all of them in LDS per workgroup cost more)
   const uint32_t* vg = (const uint32_t*)(rw + RL.vcode);
   const uint16_t* cm = tb.cmap + (size_t)q * tb.V;
-  const uint32_t* tflags = tb.lex_token + (size_t)hdr->slot_id * tb.V;
+  const uint8_t* tsum = tb.lex_toksum + (size_t)hdr->slot_id * tb.V;
   const uint8_t* vrule = rw + RL.vrule;
   unsigned long long* rbits = (unsigned long long*)(rw + RL.rbits);
   uint32_t cont[8];
@@ -1959,9 +2036,11 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
     const int id = c * 64 + lane;
     cls[j] = (c < c_hi && id < tb.V) ? (uint32_t)cm[id] : 0u;
   }
-  // pass 2: codes; for a class the lexicon decides, its shortcut byte and the
-  // token's first byte and token flags (again all loads in flight together)
-  uint32_t code[kPer], sc[kPer], fb[kPer], tf[kPer], sb[kPer];
+  // pass 2: codes; for a class the lexicon decides, its shortcut byte, the
+  // token's first two bytes and its token-flag summary; for a token the class
+  // leaves undecided, its spelling (needed below if the shortcut leaves the
+  // token to the residue); again all loads in flight together
+  uint32_t code[kPer], sc[kPer], hd[kPer], tf[kPer], su[kPer];
   bool cib[kPer];
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
@@ -1970,9 +2049,9 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
     code[j] = c < c_hi ? (vg[cls[j] >> 4] >> ((cls[j] & 15u) * 2u)) & 3u : kVerdictReject;
     const bool lexq = code[j] == kVerdictLexicon && id < tb.V;
     sc[j] = lexq ? vrule[cls[j]] : 0u;
-    fb[j] = lexq ? tb.id_first[id] : 0u;
-    sb[j] = lexq ? tb.id_second[id] : 0u;
-    tf[j] = lexq ? tflags[id] : 0u;
+    hd[j] = lexq ? tb.id_head[id] : 0u;
+    tf[j] = lexq ? tsum[id] : 0u;
+    su[j] = code[j] >= kVerdictWalk && id < tb.V ? tb.spell_of_id[id] : 0xFFFFFFFFu;
     cib[j] = cdst && c < c_hi && id < tb.V ? ci_class(crow[cls[j]].x) : false;
   }
   // pass 2b: a pending-lexeme question on a lexeme that holds the token's
@@ -1982,12 +2061,13 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
   uint32_t c2[kPer];
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
+    const uint32_t fb = hd[j] & 0xFFu, sb = (hd[j] >> 8) & 0xFFu;
     const bool ask = code[j] == kVerdictLexicon && (sc[j] & kNoValid) && ((sc[j] >> 2) & 3u) == 0u &&
-                     ((sc[j] >> 4) & 1u) && (sb[j] & 0x100u) && ((cont[fb[j] >> 5] >> (fb[j] & 31u)) & 1u);
-    c2[j] = ask ? ~(cont2[fb[j] * 8u + ((sb[j] & 0xFFu) >> 5)] >> (sb[j] & 31u)) & 1u : 0u;
+                     ((sc[j] >> 4) & 1u) && (hd[j] & 0x10000u) && ((cont[fb >> 5] >> (fb & 31u)) & 1u);
+    c2[j] = ask ? ~(cont2[fb * 8u + (sb >> 5)] >> (sb & 31u)) & 1u : 0u;
   }
   // pass 3: shortcut verdicts, mask words, residue ids
-  uint32_t resu[kPer];  // this lane's residue ids (or ~0)
+  uint32_t resu[kPer];  // this lane's residue spellings (or ~0)
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
     const int c = c_lo + wave + j * kStreamWaves;
@@ -1996,9 +2076,9 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
     if (c >= c_hi) continue;  // uniform across the wave
     uint32_t cd = code[j];
     if (cd == kVerdictLexicon && (sc[j] & kNoValid)) {
-      const uint32_t kind = (sc[j] >> 2) & 3u;
-      const bool no = kind == 0 ? !((cont[fb[j] >> 5] >> (fb[j] & 31u)) & 1u) || c2[j] != 0u
-                                : ((tf[j] >> (16 * ((sc[j] >> 4) & 1u) + (kind == 2 ? 8u : 0u))) & 0xFFu) == 0u;
+      const uint32_t kind = (sc[j] >> 2) & 3u, fb = hd[j] & 0xFFu;
+      const bool no = kind == 0 ? !((cont[fb >> 5] >> (fb & 31u)) & 1u) || c2[j] != 0u
+                                : ((tf[j] >> (2 * ((sc[j] >> 4) & 1u) + (kind == 2 ? 1u : 0u))) & 1u) == 0u;
       if (no) cd = (sc[j] >> 5) & 3u;
     }
     const uint64_t al = __ballot(cd == kVerdictAllow || id == eos);
@@ -2010,14 +2090,11 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Tables tb, uint32_t* __r
       const uint64_t cb = __ballot(cib[j] && cd == kVerdictAllow && id < tb.V && id != tb.eos_id);
       if (lane < 2 && 2 * c + lane < tb.W) cdst[2 * c + lane] = (uint32_t)(cb >> (32 * lane));
     }
-    if (cd >= kVerdictWalk && id < tb.V) resu[j] = (uint32_t)id;
+    if (cd >= kVerdictWalk && id < tb.V) resu[j] = su[j];
     code[j] = cd;
   }
   // mark the residue spellings in the row's bitmaps (lexicon or byte walk),
-  // last, so no load above waits behind these atomics; the spelling lookups
-  // are issued together
-#pragma unroll
-  for (int k2 = 0; k2 < kPer; ++k2) resu[k2] = resu[k2] != 0xFFFFFFFFu ? tb.spell_of_id[resu[k2]] : 0xFFFFFFFFu;
+  // last, so no load above waits behind these atomics
   const uint32_t nsub = ((uint32_t)tb.U + 63u) / 64u;
 #pragma unroll
   for (int k2 = 0; k2 < kPer; ++k2)
@@ -3089,7 +3166,7 @@ int residue_grid_size(uint32_t lds) {
 template <int MW>
 int launch_mask(const Tables& tb, int B, const grid_config* cfg_dev, const uint16_t* pool, uint32_t* mask,
                 uint8_t* eos, int32_t* status, uint8_t* ws, size_t rb, uint32_t phases, hipStream_t s) {
-  const uint32_t parse_bytes = prologue_parse_lds(tb).total;
+  const uint32_t parse_bytes = prologue_lds(tb).total;
   if (!raise_lds((const void*)prologue_kernel<MW>, parse_bytes))
     return fail(GRID_E_HIP, "grid_mask: cannot raise the LDS limit");
   if (phases & GRID_PHASE_PROLOGUE) {
@@ -3149,8 +3226,9 @@ static int bind_tables(const grid_compiled* g, Tables& tb) {
                                GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH,   GRID_ART_LEX_PREFIX,
                                GRID_ART_SPELL_OF_ID, GRID_ART_CLASS_MAP, GRID_ART_CLASS_OFF,
                                GRID_ART_CLASS_REC,   GRID_ART_LEX_STRIDE,  GRID_ART_LEX_TOKEN,
-                               GRID_ART_ID_FIRST,    GRID_ART_PARSE_SHIFT, GRID_ART_GOTO,
-                               GRID_ART_STATE_SYMBOL, GRID_ART_LEX_CHILD, GRID_ART_ID_SECOND};
+                               GRID_ART_PARSE_SHIFT, GRID_ART_GOTO,
+                               GRID_ART_STATE_SYMBOL, GRID_ART_LEX_CHILD, GRID_ART_ID_HEAD,
+                               GRID_ART_LEX_TOKSUM};
   for (int w : needed)
     if (!bound(g, w)) return fail(GRID_E_UNBOUND, "artifact " + std::to_string(w) + " is not bound");
   tb.dfa = (const uint16_t*)g->dev[GRID_ART_DFA_CLASS];
@@ -3177,8 +3255,8 @@ static int bind_tables(const grid_compiled* g, Tables& tb) {
   tb.lex_prefix = (const uint4*)g->dev[GRID_ART_LEX_PREFIX];
   tb.lex_stride = (const uint4*)g->dev[GRID_ART_LEX_STRIDE];
   tb.lex_token = (const uint32_t*)g->dev[GRID_ART_LEX_TOKEN];
-  tb.id_first = (const uint8_t*)g->dev[GRID_ART_ID_FIRST];
-  tb.id_second = (const uint16_t*)g->dev[GRID_ART_ID_SECOND];
+  tb.id_head = (const uint32_t*)g->dev[GRID_ART_ID_HEAD];
+  tb.lex_toksum = (const uint8_t*)g->dev[GRID_ART_LEX_TOKSUM];
   tb.lex_child = (const uint32_t*)g->dev[GRID_ART_LEX_CHILD];
   tb.spell_of_id = (const uint32_t*)g->dev[GRID_ART_SPELL_OF_ID];
   tb.state_sym = (const uint32_t*)g->dev[GRID_ART_STATE_SYMBOL];

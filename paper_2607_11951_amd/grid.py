@@ -29,7 +29,8 @@ ART_NAMES = ["DFA_DENSE", "DFA_CLASS", "BYTE_CLASS", "DFA_ACCEPT_OFF", "DFA_ACCE
              "ALIAS_IDS", "TRIE_LEVEL_OFF", "TRIE_NODES", "LEX_FLAGS", "LEX_HASH", "LEX_SLOTS",
              "SPELL_REC", "PARSE_STATE", "PARSE_REDX", "GOTO_HASH", "SPELL_TAIL", "LEX_PREFIX",
              "SPELL_RANGE", "SPELL_OF_ID", "CLASS_MAP", "CLASS_OFF", "CLASS_REC", "LEX_STRIDE",
-             "LEX_TOKEN", "ID_FIRST", "PARSE_SHIFT", "STATE_SYMBOL", "LEX_CHILD", "ID_SECOND"]
+             "LEX_TOKEN", "ID_FIRST", "PARSE_SHIFT", "STATE_SYMBOL", "LEX_CHILD", "ID_HEAD",
+             "LEX_TOKSUM"]
 ART = {n: i for i, n in enumerate(ART_NAMES)}
 
 CONFIG_DTYPE = np.dtype([("stk_off", "<u4"), ("stk_depth", "<u4"), ("lexnode", "<u4"), ("q", "<u2"),
@@ -178,7 +179,7 @@ class Grid:
         _check(lib().grid_add_lexicon(self.h, ctypes.byref(la), ctypes.byref(slot)))
         if self.device is not None:
             self._upload(self.device, ["LEX_FLAGS", "LEX_HASH", "LEX_SLOTS", "LEX_PREFIX", "LEX_STRIDE", "LEX_TOKEN",
-                                       "LEX_CHILD"])
+                                       "LEX_CHILD", "LEX_TOKSUM"])
         return slot.value
 
     def artifact(self, name):

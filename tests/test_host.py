@@ -108,13 +108,14 @@ def test_position_isolated_workload_contexts(G):
                 assert p <= cells[i][2] < p + 200
 
 
-def test_lexicon_child_bitmaps_and_second_bytes(G):
+def test_lexicon_child_bitmaps_and_token_heads(G):
     """LEX_CHILD: bit b of a trie node's bitmap is set exactly when some word
     of the slot continues the node's string with byte b (the node reached
-    through the edge hash); ID_SECOND: 0x100 | second byte, 0 when shorter."""
+    through the edge hash); ID_HEAD: first byte | second byte << 8 | 0x10000
+    when there is a second byte; LEX_TOKSUM: the nonzero bytes of LEX_TOKEN."""
     words_t = ["employees", "emp", "e", "dept_history_2020", "orders"]
     words_c = ["id", "emp_no", "employee_name_full", "e_x", "order_id"]
-    vocab = [b"a", b"ab", b"", b"xyz", b"\x00\xff"]
+    vocab = [b"a", b"ab", b"", b"xyz", b"\x00\xff", b"emp", b" orders", b"order_id", b"e_x"]
     g = G.Grid(grammar_text("crud"), ["insert", "update", "delete"], vocab, [2])
     slot = g.add_lexicon({"TABLE_NAME": words_t, "COLUMN_NAME": words_c})
     rec = np.frombuffer(g.artifact("LEX_SLOTS"), np.uint32).reshape(-1, 12)[slot]
@@ -144,8 +145,18 @@ def test_lexicon_child_bitmaps_and_second_bytes(G):
         bits = child_bits[fbase + node]
         got = {b for b in range(256) if (int(bits[b >> 5]) >> (b & 31)) & 1}
         assert got == want, p
-    sec = np.frombuffer(g.artifact("ID_SECOND"), np.uint16)
-    assert sec.tolist() == [0, 0x100 | ord("b"), 0, 0x100 | ord("y"), 0x1FF]
+    head = np.frombuffer(g.artifact("ID_HEAD"), np.uint32)
+    assert head[:5].tolist() == [ord("a"), 0x10000 | ord("a") | ord("b") << 8, 0, 0x10000 | ord("x") | ord("y") << 8,
+                                 0x10000 | 0xFF << 8]
+    for i, v in enumerate(vocab):
+        if i != 2:
+            assert head[i] == v[0] | ((0x10000 | v[1] << 8) if len(v) > 1 else 0), v
+    tok = np.frombuffer(g.artifact("LEX_TOKEN"), np.uint32)
+    tsum = np.frombuffer(g.artifact("LEX_TOKSUM"), np.uint8)
+    assert len(tok) == len(tsum) == len(vocab) * (slot + 1)
+    want = sum((((tok >> (8 * k)) & 0xFF) != 0).astype(np.uint8) << k for k in range(4))
+    assert np.array_equal(tsum, want)
+    assert tsum[len(vocab) * slot + vocab.index(b"emp")] & 1  # "emp" prefixes words of the slot
 
 
 def test_lexicon_prefix_table(G):
