@@ -487,7 +487,7 @@ struct BaseStack {  // the shared read-only stack of one row
 
 template <bool L>
 __device__ __forceinline__ uint16_t goto_of(const ParseTabs<L>& pt, uint32_t s, uint32_t a) {
-  if (pt.dense) return pt.gd[s * (uint32_t)pt.N + a];
+  if (pt.dense) return pt.gd[__umul24(s, (uint32_t)pt.N) + a];  // states and N below 2^24
   const uint32_t key = goto_key(s, a);
   const uint32_t mask = (1u << pt.hbits) - 1u;
   uint32_t h = goto_slot(key, pt.hbits);
@@ -511,7 +511,7 @@ struct PRec {
 template <bool L, int MW>
 __device__ __forceinline__ PRec<MW> rec_of(const ParseTabs<L>& pt, uint32_t s) {
   constexpr int R = parse_record_words(MW);
-  const mptr<L, const u32x4> p = (mptr<L, const u32x4>)(pt.st + (size_t)s * R);
+  const mptr<L, const u32x4> p = (mptr<L, const u32x4>)(pt.st + s * (uint32_t)R);
   uint32_t w[R];
 #pragma unroll
   for (int i = 0; i < R / 4; ++i) {
@@ -540,7 +540,7 @@ constexpr uint32_t kNoState = 0xFFFFFFFFu;
 template <bool L, int MW>
 __device__ __forceinline__ uint32_t action_of(const ParseTabs<L>& pt, uint32_t s, uint32_t w, uint32_t bit) {
   constexpr int R = parse_record_words(MW);
-  const mptr<L, const uint32_t> rec = pt.st + (size_t)s * R;
+  const mptr<L, const uint32_t> rec = pt.st + s * (uint32_t)R;
   const uint32_t sh = rec[w], rd = rec[MW + w];  // both loads issued together
   const u32x2 me = *(mptr<L, const u32x2>)(rec + 2 * MW);
   const uint32_t hit = (sh | rd) & bit;
@@ -565,7 +565,7 @@ __device__ __forceinline__ uint32_t action_of(const ParseTabs<L>& pt, uint32_t s
 template <bool L, int MW>
 __device__ __forceinline__ uint16_t shift_target(const ParseTabs<L>& pt, uint32_t s, int x) {
   constexpr int R = parse_record_words(MW);
-  const mptr<L, const uint32_t> rec = pt.st + (size_t)s * R;
+  const mptr<L, const uint32_t> rec = pt.st + s * (uint32_t)R;
   const uint32_t w = (uint32_t)x >> 5;
   uint32_t rank = 0, base = rec[2 * MW + 2];
 #pragma unroll
@@ -1093,10 +1093,14 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
     hacc[0] = 0;
     hacc[1] = 0;
   }
-  {  // the residue bitmaps start empty (16-byte stores)
-    uint4* rb = (uint4*)(rw + L.rbits);
-    for (int i = tid; i < (tb.U + 63) / 64; i += kProThreads) rb[i] = make_uint4(0, 0, 0, 0);
-  }
+  // the residue bitmaps start empty (16-byte stores): cleared during phase 1
+  // by the waves below thread 256 that have no terminal, whose later work is
+  // all in LDS (so nothing waits on these stores), else here
+  const int z0 = ((tb.T + 63) / 64) * 64;
+  uint4* const rb = (uint4*)(rw + L.rbits);
+  const int n_rb = (tb.U + 63) / 64;
+  if (z0 >= 256)
+    for (int i = tid; i < n_rb; i += kProThreads) rb[i] = make_uint4(0, 0, 0, 0);
   dma_wait();
   __syncthreads();
   const bool sum_hash = tb.cache && !tb.stack_hash;  // the cache key needs the whole stack's content
@@ -1275,6 +1279,8 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Tables tb, const 
   } else if (tid == 255) {  // at most 255 terminals: never a terminal's thread
     eos_sigma = sim1_test<true, MW>(pt, bs, depth, 0, my, my, kPostCap + kTmpCap, tb.T) == 2;
   }
+  if (z0 < 256 && tid >= z0 && tid < 256)
+    for (int i = tid - z0; i < n_rb; i += 256 - z0) rb[i] = make_uint4(0, 0, 0, 0);
   if (tid < 256) {
 #pragma unroll
     for (int w = 0; w < MW; ++w) a2_s[tid][w] = 0u;
