@@ -173,7 +173,7 @@ enum {
                                PARSE_SHIFT, padding */
   GRID_ART_PARSE_REDX,      /* u32 per extra reduce group: production (lhs | length << 16),
                                TW words of terminals */
-  GRID_ART_GOTO_HASH,       /* GOTO as an open-addressing table of H = 2^k slots (k >= 6,
+  GRID_ART_GOTO_HASH,       /* GOTO_SKIP as an open-addressing table of H = 2^k slots (k >= 6,
                                load <= 2/3), u32 [H][2]: key (state << 16 | nonterminal) + 1
                                (0 empty), target; slot of a key =
                                (key * 0x9E3779B1 mod 2^32) >> (32 - k), linear probing */
@@ -232,6 +232,14 @@ enum {
   GRID_ART_LEX_TOKSUM,      /* u8 [slots][V]: which entries of LEX_TOKEN are nonzero: bit
                                2o set when the prefix flags from offset o are, bit 2o + 1
                                when the word flags from offset o are (o = 0, 1) */
+  GRID_ART_GOTO_SKIP,       /* u16 [n_lr][N]: the GOTO the kernels use.  A unit state has
+                               no shift and no GOTO, and on every lookahead either reduces
+                               by one production X -> A with a one-symbol right side or has
+                               no action; a transition into one from state b is redirected
+                               to GOTO(b, X), repeatedly (the state that reduction leads to).
+                               Unit states are never left on a stack after a shift, so the
+                               stacks after every shift are those of GOTO; a lookahead the
+                               unit state would refuse is refused later in the chain */
   GRID_ART_COUNT
 };
 int grid_artifact(const grid_compiled* g, int32_t which, const void** host_ptr, size_t* bytes);

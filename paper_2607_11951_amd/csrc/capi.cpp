@@ -218,6 +218,7 @@ extern "C" int grid_artifact(const grid_compiled* g, int32_t which, const void**
     case GRID_ART_LEX_CHILD: put(g->lex.child_bits, p, n); break;
     case GRID_ART_ID_HEAD: put(g->vocab.id_head, p, n); break;
     case GRID_ART_LEX_TOKSUM: put(g->lex.toksum, p, n); break;
+    case GRID_ART_GOTO_SKIP: put(g->parser.go_skip, p, n); break;
     default: return fail(GRID_E_ARG, "unknown artifact " + std::to_string(which));
   }
   return GRID_OK;

@@ -77,6 +77,7 @@ struct Parser {
   int n_states = 0;
   std::vector<uint16_t> action;   // [n_states*(T+1)]
   std::vector<uint16_t> go;       // [n_states*N]
+  std::vector<uint16_t> go_skip;  // [n_states*N]: GOTO with transitions into unit states redirected
   std::vector<uint32_t> prod;     // lhs | len << 16
   std::vector<uint8_t> term_used; // terminal appears in the reduced grammar
   // compact form for set simulation (TW = words per terminal set incl. end of

@@ -3232,7 +3232,7 @@ static int bind_tables(const grid_compiled* g, Tables& tb) {
                                GRID_ART_PARSE_REDX,  GRID_ART_GOTO_HASH,   GRID_ART_LEX_PREFIX,
                                GRID_ART_SPELL_OF_ID, GRID_ART_CLASS_MAP, GRID_ART_CLASS_OFF,
                                GRID_ART_CLASS_REC,   GRID_ART_LEX_STRIDE,  GRID_ART_LEX_TOKEN,
-                               GRID_ART_PARSE_SHIFT, GRID_ART_GOTO,
+                               GRID_ART_PARSE_SHIFT, GRID_ART_GOTO_SKIP,
                                GRID_ART_STATE_SYMBOL, GRID_ART_LEX_CHILD, GRID_ART_ID_HEAD,
                                GRID_ART_LEX_TOKSUM};
   for (int w : needed)
@@ -3247,7 +3247,7 @@ static int bind_tables(const grid_compiled* g, Tables& tb) {
   tb.pstate = (const uint32_t*)g->dev[GRID_ART_PARSE_STATE];
   tb.predx = (const uint32_t*)g->dev[GRID_ART_PARSE_REDX];
   tb.pshift = (const uint16_t*)g->dev[GRID_ART_PARSE_SHIFT];
-  tb.go = (const uint16_t*)g->dev[GRID_ART_GOTO];
+  tb.go = (const uint16_t*)g->dev[GRID_ART_GOTO_SKIP];
   tb.ghash = (const uint2*)g->dev[GRID_ART_GOTO_HASH];
   tb.spell_off = (const uint32_t*)g->dev[GRID_ART_SPELL_OFF];
   tb.spell_bytes = (const uint8_t*)g->dev[GRID_ART_SPELL_BYTES];

@@ -360,7 +360,47 @@ Parser build_parser(const GrammarText& g, const std::vector<std::string>& drop) 
 // so the kernels read it with 16-byte loads.  The first padding word locates the
 // state's shift targets: one u16 per set shift bit, in terminal order, so the target
 // of terminal t is entry (number of shift bits below t) of the state's run.
+// The kernels' GOTO.  A unit state (no shift, no GOTO, every action a
+// reduction by the same production X -> A with |A| = 1) is reduced the moment
+// it is entered: the reduction pops it and takes GOTO(b, X) from the state b
+// it was entered from.  So a transition b --A--> unit state is redirected to
+// GOTO(b, X), and again while that is a unit state.  A unit state never stays
+// on a stack below a shifted terminal, so every stack after a shift is the one
+// the LALR tables give; a lookahead the unit state has no action for is
+// refused further up the chain (the unit item's lookaheads include everything
+// the states reached from b through X can shift or reduce on), so the
+// terminals that can be shifted next are the same.
+void skip_unit_states(Parser& P) {
+  const int NS = P.n_states, T1 = P.T + 1, N = P.N;
+  std::vector<int> unit(NS, -1);
+  for (int s = 0; s < NS; ++s) {
+    int p = -1;
+    bool ok = true;
+    for (int t = 0; t < T1 && ok; ++t) {
+      const uint16_t a = P.act(s, t);
+      if (a == 0) continue;
+      if ((a & 0xC000) != kActReduce || (p >= 0 && (a & 0x3FFF) != p)) ok = false;
+      p = a & 0x3FFF;
+    }
+    for (int a = 0; a < N && ok; ++a)
+      if (P.gto(s, a) != kNoGoto) ok = false;
+    if (ok && p > 0 && (P.prod[p] >> 16) == 1) unit[s] = p;
+  }
+  P.go_skip = P.go;
+  for (int b = 0; b < NS; ++b)
+    for (int a = 0; a < N; ++a) {
+      uint16_t g = P.gto(b, a);
+      for (int guard = 0; g != kNoGoto && unit[g] >= 0 && guard <= NS; ++guard) {
+        const uint16_t g2 = P.gto(b, (int)(P.prod[unit[g]] & 0xFFFF));
+        if (g2 == kNoGoto) break;
+        g = g2;
+      }
+      P.go_skip[(size_t)b * N + a] = g;
+    }
+}
+
 void compact_tables(Parser& P) {
+  skip_unit_states(P);
   const int T1 = P.T + 1;
   int TW = 2;
   while (TW * 32 < T1) TW *= 2;
@@ -416,7 +456,7 @@ void compact_tables(Parser& P) {
       else if ((a & 0xC000) == kActAccept) P.pshift.push_back(0);
     }
     for (int a = 0; a < P.N; ++a) {
-      const uint16_t g = P.gto(s, a);
+      const uint16_t g = P.go_skip[(size_t)s * P.N + a];
       if (g != kNoGoto) gotos.push_back({goto_key(s, a), g});
     }
   }

@@ -30,7 +30,7 @@ ART_NAMES = ["DFA_DENSE", "DFA_CLASS", "BYTE_CLASS", "DFA_ACCEPT_OFF", "DFA_ACCE
              "SPELL_REC", "PARSE_STATE", "PARSE_REDX", "GOTO_HASH", "SPELL_TAIL", "LEX_PREFIX",
              "SPELL_RANGE", "SPELL_OF_ID", "CLASS_MAP", "CLASS_OFF", "CLASS_REC", "LEX_STRIDE",
              "LEX_TOKEN", "ID_FIRST", "PARSE_SHIFT", "STATE_SYMBOL", "LEX_CHILD", "ID_HEAD",
-             "LEX_TOKSUM"]
+             "LEX_TOKSUM", "GOTO_SKIP"]
 ART = {n: i for i, n in enumerate(ART_NAMES)}
 
 CONFIG_DTYPE = np.dtype([("stk_off", "<u4"), ("stk_depth", "<u4"), ("lexnode", "<u4"), ("q", "<u2"),

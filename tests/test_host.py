@@ -496,6 +496,7 @@ def test_compact_parse_tables_match_dense(G, name, drop):
     st = np.frombuffer(g.artifact("PARSE_STATE"), np.uint32)
     redx = np.frombuffer(g.artifact("PARSE_REDX"), np.uint32)
     gh = np.frombuffer(g.artifact("GOTO_HASH"), np.uint32).reshape(-1, 2)
+    skip = np.frombuffer(g.artifact("GOTO_SKIP"), np.uint16).reshape(NS, N)
     sl = np.frombuffer(g.artifact("PARSE_SHIFT"), np.uint16)
     tw = 2
     while 32 * tw < T + 1:
@@ -539,7 +540,52 @@ def test_compact_parse_tables_match_dense(G, name, drop):
             while gh[h, 0] != 0 and gh[h, 0] != key:
                 h = (h + 1) % H
             found = int(gh[h, 1]) if gh[h, 0] == key else 0xFFFF
-            assert found == int(go[s, a]), (s, a)
+            assert found == int(skip[s, a]), (s, a)
+
+
+def _unit_states(action, go, prod):
+    """States whose only actions are one reduction by a one-symbol production
+    and that have no GOTO: {state: production}."""
+    units = {}
+    for s in range(action.shape[0]):
+        acts = {int(a) for a in action[s] if a}
+        if len(acts) != 1 or (go[s] != 0xFFFF).any():
+            continue
+        a = acts.pop()
+        if a & 0xC000 == 0x8000 and int(prod[a & 0x3FFF]) >> 16 == 1:
+            units[s] = a & 0x3FFF
+    return units
+
+
+@pytest.mark.parametrize("name,drop", [("expr", []), ("sql_select", []),
+                                       ("sql_dml", ["insert", "update", "delete"])])
+def test_goto_skip_redirects_unit_states(G, name, drop):
+    """GOTO_SKIP: GOTO with every transition into a unit state redirected to
+    the GOTO on the unit production's left side from the same source, until
+    the target is no unit state (or that GOTO is undefined); written here from
+    the dense ACTION and GOTO tables, and checked to leave no chain of unit
+    reductions behind a redirected transition."""
+    g = G.Grid(grammar_text(name), drop, [b"a"])
+    info = g.info()
+    NS, T, N = info["n_lr_states"], info["n_terminals"], info["n_nonterminals"]
+    action = np.frombuffer(g.artifact("ACTION"), np.uint16).reshape(NS, T + 1)
+    go = np.frombuffer(g.artifact("GOTO"), np.uint16).reshape(NS, N)
+    prod = np.frombuffer(g.artifact("PROD"), np.uint32)
+    skip = np.frombuffer(g.artifact("GOTO_SKIP"), np.uint16).reshape(NS, N)
+    units = _unit_states(action, go, prod)
+    assert units, name  # the grammars' precedence ladders have unit states
+    redirected = 0
+    for b in range(NS):
+        for a in range(N):
+            t = int(go[b, a])
+            while t != 0xFFFF and t in units:
+                nxt = int(go[b, int(prod[units[t]]) & 0xFFFF])
+                if nxt == 0xFFFF:
+                    break
+                t = nxt
+            assert int(skip[b, a]) == t, (b, a)
+            redirected += t != int(go[b, a])
+    assert redirected > 0
 
 
 def test_cache_sizes_and_argument_errors(G):
