@@ -350,16 +350,6 @@ Parser build_parser(const GrammarText& g, const std::vector<std::string>& drop) 
   return out;
 }
 
-// Compact tables for simulating a whole set of lookahead terminals at once:
-// per state the terminals that shift (or accept, end-of-input column), the
-// terminals reduced by the state's main production, and any further reduce
-// productions with their own terminal sets; productions appear as
-// lhs | length << 16, so a reduce needs no further lookup; GOTO as an
-// open-addressing hash of (key, target) pairs.  Terminal sets take TW words,
-// TW a power of two (at least 2), and a state record is padded to a multiple of 16 bytes
-// so the kernels read it with 16-byte loads.  The first padding word locates the
-// state's shift targets: one u16 per set shift bit, in terminal order, so the target
-// of terminal t is entry (number of shift bits below t) of the state's run.
 // The kernels' GOTO.  A unit state (no shift, no GOTO, every action a
 // reduction by the same production X -> A with |A| = 1) is reduced the moment
 // it is entered: the reduction pops it and takes GOTO(b, X) from the state b
@@ -399,6 +389,17 @@ void skip_unit_states(Parser& P) {
     }
 }
 
+// Compact tables for simulating a whole set of lookahead terminals at once:
+// per state the terminals that shift (or accept, end-of-input column), the
+// terminals reduced by the state's main production, and any further reduce
+// productions with their own terminal sets; productions appear as
+// lhs | length << 16 (empty runs folded in, see below), so a reduce needs no
+// further lookup; GOTO (GOTO_SKIP) as an
+// open-addressing hash of (key, target) pairs.  Terminal sets take TW words,
+// TW a power of two (at least 2), and a state record is padded to a multiple of 16 bytes
+// so the kernels read it with 16-byte loads.  The first padding word locates the
+// state's shift targets: one u16 per set shift bit, in terminal order, so the target
+// of terminal t is entry (number of shift bits below t) of the state's run.
 void compact_tables(Parser& P) {
   skip_unit_states(P);
   const int T1 = P.T + 1;
@@ -410,11 +411,49 @@ void compact_tables(Parser& P) {
   P.pstate.assign((size_t)P.n_states * stride, 0);
   P.predx.clear();
   P.pshift.clear();
-  auto packed = [&](int p) { return P.prod[p]; };  // lhs | length << 16
+  // Empty runs: in a state with a reduction by an empty production, the
+  // reductions taken on lookahead t up to the first one that pops an entry
+  // below the state depend on (state, t) alone -- the empty ones push and pop
+  // nothing -- so when that run ends in a reduction X -> alpha popping all k
+  // entries it pushed, the run's net effect is one reduction: pop |alpha| - k
+  // entries, GOTO on X.  The record keeps that reduction (X | (|alpha| - k) <<
+  // 16) for t in place of the first empty one -- one step of a reduce chain
+  // instead of k + 1, with the same stack after it -- when every terminal of
+  // that empty production's group shares the run.
+  auto empty_run = [&](int s0, int t) -> uint32_t {
+    int st = s0, k = 0;
+    for (int guard = 0; guard <= P.n_states; ++guard) {
+      const uint16_t a = P.act(st, t);
+      if ((a & 0xC000) != kActReduce) return 0;
+      const uint32_t pr = P.prod[a & 0x3FFF];
+      const uint32_t len = pr >> 16, X = pr & 0xFFFF;
+      if (len == 0) {
+        const uint16_t g = P.go_skip[(size_t)st * P.N + X];
+        if (g == kNoGoto) return 0;
+        st = g;
+        ++k;
+        continue;
+      }
+      return k > 0 && len >= (uint32_t)k ? X | (len - (uint32_t)k) << 16 : 0u;
+    }
+    return 0;
+  };
   std::vector<std::pair<uint32_t, uint16_t>> gotos;
   for (int s = 0; s < P.n_states; ++s) {
     uint32_t* rec = &P.pstate[(size_t)s * stride];
-    std::map<int, std::vector<uint32_t>> groups;  // prod -> bits
+    // an empty production's terminals take their run's reduction when they
+    // all share one (so the state keeps its number of reduce groups, which is
+    // what the set simulation pays for)
+    std::map<int, uint32_t> run_of;  // empty production -> the shared run (0 none)
+    for (int t = 0; t < T1; ++t) {
+      const uint16_t a = P.act(s, t);
+      if ((a & 0xC000) != kActReduce || (P.prod[a & 0x3FFF] >> 16) != 0) continue;
+      const uint32_t r = empty_run(s, t);
+      auto it = run_of.find(a & 0x3FFF);
+      if (it == run_of.end()) run_of[a & 0x3FFF] = r;
+      else if (it->second != r) it->second = 0;
+    }
+    std::map<uint32_t, std::vector<uint32_t>> groups;  // reduction (lhs | pops << 16) -> bits
     for (int t = 0; t < T1; ++t) {
       const uint16_t a = P.act(s, t);
       const uint16_t kind = a & 0xC000;
@@ -422,32 +461,34 @@ void compact_tables(Parser& P) {
       if (kind == kActShift || kind == kActAccept) {
         rec[t >> 5] |= 1u << (t & 31);
       } else {
-        auto& g = groups[a & 0x3FFF];
+        auto it = run_of.find(a & 0x3FFF);
+        const uint32_t run = it == run_of.end() ? 0u : it->second;
+        auto& g = groups[run ? run : P.prod[a & 0x3FFF]];
         g.resize(TW, 0);
         g[t >> 5] |= 1u << (t & 31);
       }
     }
-    int main_prod = -1;
+    uint32_t main_red = 0xFFFFFFFFu;
     size_t best = 0;
     for (auto& g : groups) {
       size_t n = 0;
       for (uint32_t w : g.second) n += (size_t)__builtin_popcount(w);
-      if (n > best) { best = n; main_prod = g.first; }
+      if (n > best) { best = n; main_red = g.first; }
     }
     uint32_t n_extra = 0;
     const size_t off = P.predx.size();
     if (off >= (1u << 24)) throw Error(GRID_E_CAPACITY, "reduce groups larger than 2^24 words");
     for (auto& g : groups) {
-      if (g.first == main_prod) {
+      if (g.first == main_red) {
         for (int w = 0; w < TW; ++w) rec[TW + w] = g.second[w];
       } else {
-        P.predx.push_back(packed(g.first));
+        P.predx.push_back(g.first);
         P.predx.insert(P.predx.end(), g.second.begin(), g.second.end());
         ++n_extra;
       }
     }
     if (n_extra > 255) throw Error(GRID_E_CAPACITY, "more than 255 reduce productions in one state");
-    rec[2 * TW] = main_prod < 0 ? 0xFFFFFFFFu : packed(main_prod);
+    rec[2 * TW] = main_red;
     rec[2 * TW + 1] = n_extra | (uint32_t)off << 8;
     rec[2 * TW + 2] = (uint32_t)P.pshift.size();
     for (int t = 0; t < T1; ++t) {

@@ -529,7 +529,12 @@ def test_compact_parse_tables_match_dense(G, name, drop):
                 target = int(sl[int(rec[s, 2 * tw + 2]) + rank])
                 assert target == (a & 0x3FFF if a & 0xC000 == 0x4000 else 0), (s, t)
             else:
-                assert got == int(prod[a & 0x3FFF]), (s, t)
+                want = int(prod[a & 0x3FFF])
+                if want >> 16 == 0:  # an empty reduction: its whole run when its terminals share one
+                    runs = {_empty_run(action, skip, prod, s, u) for u in range(T + 1) if action[s, u] == a}
+                    if len(runs) == 1 and 0 not in runs:
+                        want = runs.pop()
+                assert got == want, (s, t)
     H = len(gh)
     hb = H.bit_length() - 1
     assert H == 1 << hb and 3 * int((gh[:, 0] != 0).sum()) <= 2 * H
@@ -541,6 +546,73 @@ def test_compact_parse_tables_match_dense(G, name, drop):
                 h = (h + 1) % H
             found = int(gh[h, 1]) if gh[h, 0] == key else 0xFFFF
             assert found == int(skip[s, a]), (s, a)
+
+
+def _empty_run(action, skip, prod, s, t):
+    """The reduction (lhs | pops << 16) that stands for the run of reductions
+    state s takes on lookahead t when the run starts with k >= 1 empty ones
+    (each a GOTO_SKIP on its left side from the state reached so far) and its
+    first non-empty one, X -> alpha, pops all k entries they pushed: pop
+    |alpha| - k, GOTO on X.  0 when the run is not of that shape."""
+    cur, k = s, 0
+    while True:
+        a = int(action[cur, t])
+        if a & 0xC000 != 0x8000:
+            return 0
+        length, lhs = int(prod[a & 0x3FFF]) >> 16, int(prod[a & 0x3FFF]) & 0xFFFF
+        if length == 0:
+            cur = int(skip[cur, lhs])
+            if cur == 0xFFFF:
+                return 0
+            k += 1
+            continue
+        return lhs | (length - k) << 16 if k > 0 and length >= k else 0
+
+
+def test_empty_runs_take_one_step(G):
+    """Simulating the reductions of the compact records (empty runs folded
+    in) reaches, for every lookahead, the stack the dense tables reach, on the
+    stacks of read-only DML prefixes; and some runs were folded."""
+    from workloads import make_workload
+    wl = make_workload(3, rows=24)
+    g, slots = G.from_workload(wl)
+    info = g.info()
+    NS, T, N = info["n_lr_states"], info["n_terminals"], info["n_nonterminals"]
+    action = np.frombuffer(g.artifact("ACTION"), np.uint16).reshape(NS, T + 1)
+    go = np.frombuffer(g.artifact("GOTO"), np.uint16).reshape(NS, N)
+    skip = np.frombuffer(g.artifact("GOTO_SKIP"), np.uint16).reshape(NS, N)
+    prod = np.frombuffer(g.artifact("PROD"), np.uint32)
+    folded = sum(1 for s in range(NS) for t in range(T + 1)
+                 if action[s, t] & 0xC000 == 0x8000 and _empty_run(action, skip, prod, s, t))
+    assert folded > 0
+
+    def run(stack, t, table, fold):
+        st = list(stack)
+        for _ in range(4096):
+            a = int(action[st[-1], t])
+            if a == 0:
+                return None
+            if a & 0xC000 == 0x4000:
+                return tuple(st) + (a & 0x3FFF,)
+            if a & 0xC000 == 0xC000:
+                return "accept"
+            red = int(prod[a & 0x3FFF])
+            if fold and red >> 16 == 0:  # any run of that shape may stand for its reductions
+                red = _empty_run(action, skip, prod, st[-1], t) or red
+            pops, lhs = red >> 16, red & 0xFFFF
+            if pops:
+                del st[-pops:]
+            if not st or table[st[-1], lhs] == 0xFFFF:
+                return None
+            st.append(int(table[st[-1], lhs]))
+        raise AssertionError("reduce chain did not end")
+
+    cfgs, pool = g.configs(wl.prefixes[:24], [slots[i] for i in wl.slots[:24]])
+    pool = pool.view(np.uint16)
+    for c in cfgs:
+        stack = pool[c["stk_off"]:c["stk_off"] + c["stk_depth"]].tolist()
+        for t in range(T + 1):
+            assert run(stack, t, go, False) == run(stack, t, skip, True), t
 
 
 def _unit_states(action, go, prod):
