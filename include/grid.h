@@ -170,7 +170,10 @@ enum {
                                main production, that production as lhs | length << 16
                                (0xFFFFFFFF none), extra groups | their offset in
                                PARSE_REDX << 8, offset of the state's run in
-                               PARSE_SHIFT, padding */
+                               PARSE_SHIFT, offset of its mask run (the same targets,
+                               except that a shift into a unit state -- see GOTO_SKIP --
+                               goes to GOTO_SKIP from the state on the unit production's
+                               left side), padding */
   GRID_ART_PARSE_REDX,      /* u32 per extra reduce group: production (lhs | length << 16),
                                TW words of terminals */
   GRID_ART_GOTO_HASH,       /* GOTO_SKIP as an open-addressing table of H = 2^k slots (k >= 6,

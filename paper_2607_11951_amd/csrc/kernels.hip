@@ -561,13 +561,16 @@ __device__ __forceinline__ uint32_t action_of(const ParseTabs<L>& pt, uint32_t s
 }
 
 // Target of the shift of terminal x in state s (x's shift bit is set): entry
-// (shift bits below x) of the state's run of shift targets.
+// (shift bits below x) of the state's run of shift targets -- the mask run,
+// where a shift into a unit state goes straight to where its reduction leads,
+// or with lalr the LALR targets (stacks the device advance hands back).
 template <bool L, int MW>
-__device__ __forceinline__ uint16_t shift_target(const ParseTabs<L>& pt, uint32_t s, int x) {
+__device__ __forceinline__ uint16_t shift_target(const ParseTabs<L>& pt, uint32_t s, int x, bool lalr = false) {
   constexpr int R = parse_record_words(MW);
+  static_assert(2 * MW + 3 < R, "the record holds both shift runs");
   const mptr<L, const uint32_t> rec = pt.st + s * (uint32_t)R;
   const uint32_t w = (uint32_t)x >> 5;
-  uint32_t rank = 0, base = rec[2 * MW + 2];
+  uint32_t rank = 0, base = rec[2 * MW + (lalr ? 2 : 3)];
 #pragma unroll
   for (int k = 0; k < MW; ++k) {
     const uint32_t bits = rec[k];
@@ -2791,7 +2794,7 @@ __device__ int chain_shift(const ParseTabs<L>& pt, mptr<L, uint16_t> stk, uint32
         lo_mod = min(lo_mod, k);
         d = k + (uint32_t)t;
         if (d >= cap) return -1;
-        stk[d++] = shift_target<L, MW>(pt, s, x);
+        stk[d++] = shift_target<L, MW>(pt, s, x, true);  // the LALR stack
       }
       return 1;
     }

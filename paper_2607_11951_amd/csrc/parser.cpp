@@ -360,7 +360,7 @@ Parser build_parser(const GrammarText& g, const std::vector<std::string>& drop) 
 // refused further up the chain (the unit item's lookaheads include everything
 // the states reached from b through X can shift or reduce on), so the
 // terminals that can be shifted next are the same.
-void skip_unit_states(Parser& P) {
+std::vector<int> skip_unit_states(Parser& P) {
   const int NS = P.n_states, T1 = P.T + 1, N = P.N;
   std::vector<int> unit(NS, -1);
   for (int s = 0; s < NS; ++s) {
@@ -387,6 +387,7 @@ void skip_unit_states(Parser& P) {
       }
       P.go_skip[(size_t)b * N + a] = g;
     }
+  return unit;
 }
 
 // Compact tables for simulating a whole set of lookahead terminals at once:
@@ -401,7 +402,7 @@ void skip_unit_states(Parser& P) {
 // state's shift targets: one u16 per set shift bit, in terminal order, so the target
 // of terminal t is entry (number of shift bits below t) of the state's run.
 void compact_tables(Parser& P) {
-  skip_unit_states(P);
+  const std::vector<int> unit = skip_unit_states(P);
   const int T1 = P.T + 1;
   int TW = 2;
   while (TW * 32 < T1) TW *= 2;
@@ -495,6 +496,32 @@ void compact_tables(Parser& P) {
       const uint16_t a = P.act(s, t);
       if ((a & 0xC000) == kActShift) P.pshift.push_back((uint16_t)(a & 0x3FFF));
       else if ((a & 0xC000) == kActAccept) P.pshift.push_back(0);
+    }
+    // the mask kernels' shift targets: a shift into a unit state (its one
+    // reduction pops the shifted entry) goes where that reduction leads, as a
+    // GOTO into one does; the stack differs from the LALR one only by that
+    // pending reduction, which any lookahead the unit state would accept
+    // takes anyway (the device advance keeps the targets above)
+    std::vector<uint16_t> red;
+    bool moved = false;
+    for (int t = 0; t < T1; ++t) {
+      const uint16_t a = P.act(s, t);
+      if ((a & 0xC000) == kActAccept) red.push_back(0);
+      if ((a & 0xC000) != kActShift) continue;
+      uint16_t tgt = (uint16_t)(a & 0x3FFF);
+      if (unit[tgt] >= 0) {
+        const uint16_t g = P.go_skip[(size_t)s * P.N + (P.prod[unit[tgt]] & 0xFFFF)];
+        if (g != kNoGoto) {
+          tgt = g;
+          moved = true;
+        }
+      }
+      red.push_back(tgt);
+    }
+    rec[2 * TW + 3] = rec[2 * TW + 2];
+    if (moved) {
+      rec[2 * TW + 3] = (uint32_t)P.pshift.size();
+      P.pshift.insert(P.pshift.end(), red.begin(), red.end());
     }
     for (int a = 0; a < P.N; ++a) {
       const uint16_t g = P.go_skip[(size_t)s * P.N + a];

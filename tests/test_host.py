@@ -498,6 +498,7 @@ def test_compact_parse_tables_match_dense(G, name, drop):
     gh = np.frombuffer(g.artifact("GOTO_HASH"), np.uint32).reshape(-1, 2)
     skip = np.frombuffer(g.artifact("GOTO_SKIP"), np.uint16).reshape(NS, N)
     sl = np.frombuffer(g.artifact("PARSE_SHIFT"), np.uint16)
+    units = _unit_states(action, go, prod)
     tw = 2
     while 32 * tw < T + 1:
         tw *= 2
@@ -528,6 +529,12 @@ def test_compact_parse_tables_match_dense(G, name, drop):
                 rank += bin(int(rec[s, w]) & (bit - 1)).count("1")
                 target = int(sl[int(rec[s, 2 * tw + 2]) + rank])
                 assert target == (a & 0x3FFF if a & 0xC000 == 0x4000 else 0), (s, t)
+                # the mask run: a shift into a unit state goes where its reduction leads
+                want = target
+                if a & 0xC000 == 0x4000 and target in units:
+                    nxt = int(skip[s, int(prod[units[target]]) & 0xFFFF])
+                    want = nxt if nxt != 0xFFFF else target
+                assert int(sl[int(rec[s, 2 * tw + 3]) + rank]) == want, (s, t)
             else:
                 want = int(prod[a & 0x3FFF])
                 if want >> 16 == 0:  # an empty reduction: its whole run when its terminals share one
