@@ -532,7 +532,8 @@ size_t grid_forced_span_workspace_bytes(const grid_compiled* g, int32_t B);
  * entries is read and written back whole (kept entries rewritten with their
  * own bits), so no other writer may touch the logits during the call.
  * mask_dev: device u32 [B][ceil(V/32)]; logits_dev: device fp32 or bf16 with
- * row_stride >= V elements.  Asynchronous on stream. */
+ * row_stride >= V elements; 1 <= B <= 65535 (GRID_E_ARG otherwise).
+ * Asynchronous on stream. */
 int grid_apply(const uint32_t* mask_dev, void* logits_dev, int32_t dtype, int32_t B, int32_t V,
                int64_t row_stride, void* stream);
 

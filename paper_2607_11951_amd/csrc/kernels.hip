@@ -2717,15 +2717,15 @@ template <typename T>
 __global__ __launch_bounds__(kBlock) void apply_kernel(const uint32_t* __restrict__ mask, T* logits, int B,
                                                        int V, int W, int64_t stride, uint32_t neg_inf_bits,
                                                        bool vec_ok) {
+  // row blockIdx.y; groups of 8 logits along it, grid-stride in x
   const int groups = (V + 7) >> 3;
-  const int64_t total = (int64_t)B * groups;
-  for (int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x; g < total;
-       g += (int64_t)gridDim.x * kBlock) {
-    const int row = (int)(g / groups);
-    const int col = (int)(g - (int64_t)row * groups) * 8;
+  const int row = (int)blockIdx.y;
+  (void)B;
+  for (int grp = (int)(blockIdx.x * kBlock + threadIdx.x); grp < groups; grp += (int)(gridDim.x * kBlock)) {
+    const int col = grp * 8;
     const uint32_t bits = (mask[(size_t)row * W + (col >> 5)] >> (col & 31)) & 0xFFu;
     if (bits == 0xFFu) continue;
-    T* p = logits + row * stride + col;
+    T* p = logits + (int64_t)row * stride + col;
     if (col + 8 <= V && vec_ok) {  // whole group: 16-byte stores, the kept logits read back unchanged
       if (sizeof(T) == 2) {
         uint4 v = bits ? *reinterpret_cast<const uint4*>(p) : make_uint4(0, 0, 0, 0);
@@ -3650,16 +3650,19 @@ extern "C" int grid_apply(const uint32_t* mask_dev, void* logits_dev, int32_t dt
     return fail(GRID_E_ARG, "grid_apply: null pointer or bad shape");
   if (dtype != GRID_DTYPE_F32 && dtype != GRID_DTYPE_BF16) return fail(GRID_E_ARG, "grid_apply: dtype");
   const int W = (V + 31) / 32;
-  const int64_t groups = (int64_t)B * ((V + 7) / 8);
-  const int blocks = (int)std::min<int64_t>((groups + kBlock - 1) / kBlock, 256 * 64);
+  if (B > 65535) return fail(GRID_E_ARG, "grid_apply: more than 65535 rows");
+  const int groups = (V + 7) / 8;
+  // one grid row per batch row; along it enough workgroups for every group
+  // of 8 logits, at most 512 (a grid-stride loop covers the rest)
+  const dim3 blocks((unsigned)std::min((groups + kBlock - 1) / kBlock, 512), (unsigned)B);
   hipStream_t s = (hipStream_t)stream;
   const size_t esz = dtype == GRID_DTYPE_BF16 ? 2 : 4;
   const bool vec_ok = ((uintptr_t)logits_dev % 16 == 0) && ((row_stride * (int64_t)esz) % 16 == 0);
   if (dtype == GRID_DTYPE_BF16)
-    hipLaunchKernelGGL(apply_kernel<uint16_t>, dim3(blocks), dim3(kBlock), 0, s, mask_dev,
+    hipLaunchKernelGGL(apply_kernel<uint16_t>, blocks, dim3(kBlock), 0, s, mask_dev,
                        (uint16_t*)logits_dev, B, V, W, row_stride, 0xFF80u, vec_ok);
   else
-    hipLaunchKernelGGL(apply_kernel<uint32_t>, dim3(blocks), dim3(kBlock), 0, s, mask_dev,
+    hipLaunchKernelGGL(apply_kernel<uint32_t>, blocks, dim3(kBlock), 0, s, mask_dev,
                        (uint32_t*)logits_dev, B, V, W, row_stride, 0xFF800000u, vec_ok);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(GRID_E_HIP, std::string("grid_apply launch: ") + hipGetErrorString(e));
