@@ -622,6 +622,107 @@ def test_empty_runs_take_one_step(G):
             assert run(stack, t, go, False) == run(stack, t, skip, True), t
 
 
+class _Tables:
+    """The LALR tables and the kernels' rewritten ones of a compiled grammar,
+    with a reduce-chain simulation over either: the LALR one reads ACTION and
+    GOTO; the kernels' one decodes PARSE_STATE / PARSE_REDX (empty runs
+    folded), the mask run of PARSE_SHIFT and GOTO_SKIP."""
+
+    def __init__(self, g):
+        info = g.info()
+        self.NS, self.T, self.N = info["n_lr_states"], info["n_terminals"], info["n_nonterminals"]
+        NS, T, N = self.NS, self.T, self.N
+        self.action = np.frombuffer(g.artifact("ACTION"), np.uint16).reshape(NS, T + 1)
+        self.go = np.frombuffer(g.artifact("GOTO"), np.uint16).reshape(NS, N)
+        self.skip = np.frombuffer(g.artifact("GOTO_SKIP"), np.uint16).reshape(NS, N)
+        self.prod = np.frombuffer(g.artifact("PROD"), np.uint32)
+        self.redx = np.frombuffer(g.artifact("PARSE_REDX"), np.uint32)
+        self.sl = np.frombuffer(g.artifact("PARSE_SHIFT"), np.uint16)
+        tw = 2
+        while 32 * tw < T + 1:
+            tw *= 2
+        self.tw = tw
+        self.rec = np.frombuffer(g.artifact("PARSE_STATE"), np.uint32).reshape(NS, (2 * tw + 2 + 3) // 4 * 4)
+
+    def lalr_step(self, s, x):
+        a = int(self.action[s, x])
+        if a == 0:
+            return None
+        if a & 0xC000 == 0x4000:
+            return ("shift", a & 0x3FFF)
+        if a & 0xC000 == 0xC000:
+            return ("accept",)
+        return ("reduce", int(self.prod[a & 0x3FFF]))
+
+    def kernel_step(self, s, x):
+        rec, tw, w, bit = self.rec[s], self.tw, x >> 5, 1 << (x & 31)
+        if int(rec[w]) & bit:
+            if x == self.T:
+                return ("accept",)
+            rank = sum(bin(int(rec[k])).count("1") for k in range(w)) + bin(int(rec[w]) & (bit - 1)).count("1")
+            return ("shift", int(self.sl[int(rec[2 * tw + 3]) + rank]))
+        if int(rec[tw + w]) & bit:
+            return ("reduce", int(rec[2 * tw]))
+        off = int(rec[2 * tw + 1]) >> 8
+        for _ in range(int(rec[2 * tw + 1]) & 0xFF):
+            if int(self.redx[off + 1 + w]) & bit:
+                return ("reduce", int(self.redx[off]))
+            off += tw + 1
+        return None
+
+    def run(self, stack, x, kernel):
+        step, table = (self.kernel_step, self.skip) if kernel else (self.lalr_step, self.go)
+        st = list(stack)
+        for _ in range(4096):
+            a = step(st[-1], x)
+            if a is None or a[0] == "accept":
+                return a
+            if a[0] == "shift":
+                return st + [a[1]]
+            pops, lhs = a[1] >> 16, a[1] & 0xFFFF
+            if pops:
+                del st[-pops:]
+            if not st or table[st[-1], lhs] == 0xFFFF:
+                return None
+            st.append(int(table[st[-1], lhs]))
+        raise AssertionError("reduce chain did not end")
+
+    def allowed(self, stack, kernel):
+        return {x for x in range(self.T + 1) if self.run(stack, x, kernel) is not None}
+
+
+@pytest.mark.parametrize("k,rows", [(1, 24), (2, 12), (3, 6)])
+def test_rewritten_tables_keep_allowed_sets(G, k, rows):
+    """The kernels' rewritten LR tables (GOTO_SKIP, mask shift targets, folded
+    empty runs) give the allowed set the LALR tables give, on the stacks of
+    the workload's prefixes, after every allowed first shift, and after every
+    allowed second shift (each side continuing from its own stacks)."""
+    from workloads import make_workload
+    wl = make_workload(k, rows=rows)
+    g, slots = G.from_workload(wl)
+    tb = _Tables(g)
+    cfgs, pool = g.configs(wl.prefixes[:rows], [slots[i] for i in wl.slots[:rows]])
+    pool = pool.view(np.uint16)
+    checked = 0
+    for c in cfgs:
+        stack = pool[c["stk_off"]:c["stk_off"] + c["stk_depth"]].tolist()
+        a0 = tb.allowed(stack, False)
+        assert tb.allowed(stack, True) == a0
+        for x in a0:
+            s1, k1 = tb.run(stack, x, False), tb.run(stack, x, True)
+            if not isinstance(s1, list):
+                assert s1 == k1
+                continue
+            a1 = tb.allowed(s1, False)
+            assert tb.allowed(k1, True) == a1, x
+            for y in sorted(a1)[:8]:
+                s2, k2 = tb.run(s1, y, False), tb.run(k1, y, True)
+                if isinstance(s2, list):
+                    assert tb.allowed(k2, True) == tb.allowed(s2, False), (x, y)
+                    checked += 1
+    assert checked > 0
+
+
 def _unit_states(action, go, prod):
     """States whose only actions are one reduction by a one-symbol production
     and that have no GOTO: {state: production}."""
