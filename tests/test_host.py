@@ -723,6 +723,32 @@ def test_rewritten_tables_keep_allowed_sets(G, k, rows):
     assert checked > 0
 
 
+@pytest.mark.parametrize("name,drop", [("expr", []), ("lexi", []), ("crud", []), ("sql_select", []),
+                                       ("sql_dml", ["insert", "update", "delete"]), ("sql_dml", [])])
+def test_rewritten_tables_on_random_parses(G, name, drop):
+    """Random walks through the LALR automaton (each step shifts a terminal
+    the LALR tables allow, by the LALR tables): at every stack reached, the
+    kernels' rewritten tables allow the same terminals, and after the shift
+    of each of them, starting from the kernels' own stack, again the same."""
+    g = G.Grid(grammar_text(name), drop, [b"a"])
+    tb = _Tables(g)
+    rng = np.random.default_rng(5)
+    checked = 0
+    for walk in range(12):
+        stack = [0]
+        for _ in range(int(rng.integers(1, 40))):
+            allowed = sorted(tb.allowed(stack, False) - {tb.T})
+            assert tb.allowed(stack, True) == set(allowed) | (tb.allowed(stack, False) & {tb.T})
+            for x in allowed:
+                s1, k1 = tb.run(stack, x, False), tb.run(stack, x, True)
+                assert tb.allowed(k1, True) == tb.allowed(s1, False), (walk, x)
+                checked += 1
+            if not allowed:
+                break
+            stack = tb.run(stack, int(rng.choice(allowed)), False)
+    assert checked > 0
+
+
 def _unit_states(action, go, prod):
     """States whose only actions are one reduction by a one-symbol production
     and that have no GOTO: {state: production}."""
