@@ -353,6 +353,49 @@ def test_gpu_composition_invariant(G):
     log(f"composition: {checked} (token, parent, byte) triples at {len(pairs)} advanced rows")
 
 
+def test_random_grammars_match_oracle(G, oracle_mod):
+    """48 random grammars (workloads.randgram: chains of one-symbol
+    productions, empty productions, recursion, nesting, keywords that the
+    identifier regex also matches, and in about half of them two lexicon
+    categories in its place), each with its own vocabulary of 496 tokens (the
+    lexicon words among them) and 16 sampled prefixes in one batch, or 40 for
+    every fourth grammar (two residue row groups): masks, end-of-sequence
+    flags and row status bit-exact against the oracle."""
+    from workloads.randgram import RandomGrammar, random_prefixes, random_vocab
+    n_done = seed = 0
+    while n_done < 48:
+        rg = RandomGrammar(seed)
+        seed += 1
+        assert seed < 600, "too few random grammars compile"
+        words = sorted({w for ws in (rg.lexicon or {}).values() for w in ws})
+        vocab, specials, eos_id = random_vocab(rg.seed, rg.alphabet(), words=words)
+        try:
+            grid = G.Grid(rg.text(), (), vocab, specials, eos_id)
+        except G.GridError as e:
+            assert "GRID_E_LALR_CONFLICT" in str(e), (rg.seed, str(e))
+            continue
+        slot = grid.add_lexicon(rg.lexicon) if rg.lexicon else 0
+        prefixes = random_prefixes(rg, rg.seed, 40 if n_done % 4 == 3 else 16)
+        log(f"random grammar seed {rg.seed}: T={grid.info()['n_terminals']} V={len(vocab)} B={len(prefixes)} "
+            f"lexicon={rg.lexicon is not None}")
+        grid.to_device("cuda")
+        cfgs, pool = grid.configs(prefixes, [slot] * len(prefixes))
+        c, p = grid.configs_to_device(cfgs, pool)
+        m, e, s = grid.mask(c, p, len(prefixes))
+        torch.cuda.synchronize()
+        gm, ge, gs = m.cpu().numpy().view(np.uint32), e.cpu().numpy(), s.cpu().numpy()
+        o = oracle_mod.Oracle(rg.text(), (), rg.lexicon, vocab, specials, eos_id)
+        for r, w in enumerate(prefixes):
+            ow, oe = o.mask(w, mode=1)
+            if not np.array_equal(gm[r], ow) or int(ge[r]) != int(oe):
+                diff = np.nonzero(gm[r] != ow)[0]
+                toks = [int(k) * 32 + b for k in diff[:4] for b in range(32) if ((int(gm[r][k]) ^ int(ow[k])) >> b) & 1]
+                raise AssertionError(f"seed {rg.seed} prefix {w!r}: eos gpu={ge[r]} oracle={oe}, "
+                                     f"differing tokens {[(t, vocab[t]) for t in toks[:6]]}")
+        assert (gs == 0).all(), (rg.seed, gs)
+        n_done += 1
+
+
 def test_overlay_handoff_to_slow_path(G, oracle_mod):
     """Tokens that shift many terminals (runs of '(' at a boolean position,
     '(' and ')' mixes) outgrow a walk lane's LDS stack area and are finished by

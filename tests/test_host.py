@@ -749,6 +749,87 @@ def test_rewritten_tables_on_random_parses(G, name, drop):
     assert checked > 0
 
 
+def _random_grammars(G, n, first=0):
+    """The first n seeds from first on whose random grammar is LALR(1) (the
+    others fail to compile with GRID_E_LALR_CONFLICT): (grammar, compiled
+    handle, lexicon slot)."""
+    from workloads.randgram import RandomGrammar
+    out, seed = [], first
+    while len(out) < n:
+        rg = RandomGrammar(seed)
+        try:
+            g = G.Grid(rg.text(), (), [b"x"])
+            out.append((rg, g, g.add_lexicon(rg.lexicon) if rg.lexicon else 0))
+        except G.GridError as e:
+            assert "GRID_E_LALR_CONFLICT" in str(e), (seed, str(e))
+        seed += 1
+        assert seed < first + 40 * n, "too few random grammars compile"
+    return out
+
+
+def test_rewritten_tables_on_random_grammars(G):
+    """The kernels' rewritten LR tables against the LALR ones on 40 random
+    grammars (chains of one-symbol productions, empty productions, recursion,
+    nesting): random walks through the LALR automaton as above, the same
+    allowed terminals at every stack and after every allowed shift."""
+    checked = redirected = with_empty = 0
+    for rg, g, _ in _random_grammars(G, 40):
+        tb = _Tables(g)
+        redirected += int((tb.skip != tb.go).sum())
+        with_empty += any(not alt for alts in rg.prods.values() for alt in alts)
+        rng = np.random.default_rng(rg.seed)
+        for walk in range(6):
+            stack = [0]
+            for _ in range(int(rng.integers(1, 30))):
+                full = tb.allowed(stack, False)
+                assert tb.allowed(stack, True) == full, (rg.seed, stack)
+                allowed = sorted(full - {tb.T})
+                for x in allowed:
+                    s1, k1 = tb.run(stack, x, False), tb.run(stack, x, True)
+                    assert tb.allowed(k1, True) == tb.allowed(s1, False), (rg.seed, walk, x)
+                    checked += 1
+                if not allowed:
+                    break
+                stack = tb.run(stack, int(rng.choice(allowed)), False)
+    # the random grammars exercise the rewrites
+    assert checked > 1000 and redirected > 0 and with_empty > 0, (checked, redirected, with_empty)
+
+
+def test_host_advance_matches_oracle_on_random_grammars(G, oracle_mod):
+    """grid_config_from_prefix accepts exactly the prefixes the oracle finds
+    viable, on 20 random grammars: sampled prefixes of sentences and random
+    one-byte edits of them (half the grammars with lexicon categories)."""
+    from workloads.randgram import random_prefixes
+    n_yes = n_all = 0
+    for rg, g, slot in _random_grammars(G, 20):
+        o = oracle_mod.Oracle(rg.text(), (), rg.lexicon, [b"x"])
+        r = random.Random(rg.seed)
+        strings = random_prefixes(rg, rg.seed, 12)
+        alpha = rg.alphabet()
+        for w in list(strings):
+            for _ in range(3):
+                b = bytearray(w)
+                pos = r.randint(0, len(b))
+                c = ord(r.choice(alpha))
+                if b and pos < len(b) and r.random() < 0.5:
+                    b[pos] = c
+                else:
+                    b.insert(pos, c)
+                strings.append(bytes(b))
+        for s in strings:
+            want = o.viable(s)
+            try:
+                g.config(s, slot)
+                got = True
+            except G.GridError as e:
+                assert "GRID_E_NOT_VIABLE" in str(e)
+                got = False
+            assert got == want, (rg.seed, s)
+            n_yes += got
+            n_all += 1
+    assert 0 < n_yes < n_all
+
+
 def _unit_states(action, go, prod):
     """States whose only actions are one reduction by a one-symbol production
     and that have no GOTO: {state: production}."""
