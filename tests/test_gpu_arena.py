@@ -9,6 +9,9 @@ through the C ABI.
   the host advance of the extended prefix, the kept rolling hashes equal the
   host hash of the new stack (only the rewritten entries were recomputed),
   and the mask of the advanced configuration equals the oracle's.
+* The same decode loops on random LALR(1) grammars with their own
+  vocabularies (half of them with lexicon categories), ending rows that can
+  only stop with the end-of-sequence token.
 * A refused token leaves the row's configuration, stack and hashes untouched.
 * The mask cache keyed by H(top) gives the cold masks (cache-on equals
   cache-off), and a repeated configuration is a hit.
@@ -148,6 +151,77 @@ def _published(grid, cache):
     stride = 64 + (4 * grid.W + 15) // 16 * 16
     states = cache.cpu().numpy().reshape(-1, stride)[:, :4].copy().view(np.uint32)[:, 0]
     return int((states == 2).sum()), int((states == 1).sum())
+
+
+def test_inplace_decode_loops_on_random_grammars(G, oracle_mod):
+    """Decode loops on 16 random LALR(1) grammars (workloads.randgram, half of
+    them with lexicon categories), 16 rows each, 6 steps: a token sampled from
+    each row's GPU mask is accepted in place; the configuration and stack
+    then equal the host advance of the extended prefix, the kept rolling
+    hashes the host hash of the new stack, and the new mask the oracle's.  A
+    row whose mask allows only the end of sequence takes it and reports
+    GRID_ROW_FINISHED, untouched."""
+    from workloads.randgram import RandomGrammar, random_prefixes, random_vocab
+    n_done = seed = 0
+    while n_done < 16:
+        rg = RandomGrammar(1000 + seed)
+        seed += 1
+        assert seed < 300, "too few random grammars compile"
+        words = sorted({w for ws in (rg.lexicon or {}).values() for w in ws})
+        vocab, specials, eos_id = random_vocab(rg.seed, rg.alphabet(), words=words)
+        try:
+            grid = G.Grid(rg.text(), (), vocab, specials, eos_id)
+        except G.GridError as e:
+            assert "GRID_E_LALR_CONFLICT" in str(e), (rg.seed, str(e))
+            continue
+        slot = grid.add_lexicon(rg.lexicon) if rg.lexicon else 0
+        grid.to_device("cuda")
+        o = oracle_mod.Oracle(rg.text(), (), rg.lexicon, vocab, specials, eos_id)
+        prefixes = random_prefixes(rg, rg.seed, 16)
+        B = len(prefixes)
+        print(f"random grammar seed {rg.seed}: B={B} lexicon={rg.lexicon is not None}", flush=True)
+        cfgs, region = _regions(G, grid, prefixes, [slot] * B, cap=256)
+        c, p = grid.configs_to_device(cfgs, region)
+        h = grid.stack_hash(c, p, B)
+        rng = np.random.default_rng(rg.seed)
+        for step in range(6):
+            m, e, s = grid.mask(c, p, B)
+            torch.cuda.synchronize()
+            bits = np.unpackbits(m.cpu().numpy().view(np.uint8), axis=1, bitorder="little")[:, :len(vocab)]
+            toks = np.zeros(B, np.int32)
+            for r in range(B):
+                allowed = np.flatnonzero(bits[r])
+                rest = allowed[allowed != eos_id]
+                assert len(allowed) > 0, (rg.seed, step, prefixes[r])
+                toks[r] = rng.choice(rest) if len(rest) else eos_id
+            st = grid.accept_inplace(c, p, torch.from_numpy(toks).cuda(), B, 256, stack_hash=h)
+            torch.cuda.synchronize()
+            st = st.cpu().numpy()
+            for r in range(B):
+                if toks[r] == eos_id:
+                    assert st[r] == G.ROW_FINISHED, (rg.seed, step, r, st[r])
+                else:
+                    assert st[r] == G.ROW_OK, (rg.seed, step, r, st[r])
+                    prefixes[r] = prefixes[r] + vocab[toks[r]]
+            got = c.cpu().numpy().view(G.CONFIG_DTYPE)
+            pool = p.cpu().numpy().view(np.uint16)
+            hashes = h.cpu().numpy().view(np.uint64)
+            for r in range(B):
+                want, stack = grid.config(prefixes[r], slot)
+                for f in ("q", "lexnode", "flags", "rem_len", "slot"):
+                    assert int(got[r][f]) == int(want[f]), (rg.seed, step, r, f)
+                assert bytes(got[r]["rem_head"]) == bytes(want["rem_head"])
+                off, d = int(got[r]["stk_off"]), int(got[r]["stk_depth"])
+                assert off == r * 256 and d == len(stack), (rg.seed, step, r)
+                assert np.array_equal(pool[off:off + d], stack), (rg.seed, step, r)
+                assert np.array_equal(hashes[off:off + d], grid.stack_hash_host(stack)), (rg.seed, step, r)
+            m, e, s = grid.mask(c, p, B)
+            torch.cuda.synchronize()
+            gm, ge = m.cpu().numpy().view(np.uint32), e.cpu().numpy()
+            for r in range(B):
+                want, want_eos = o.mask(prefixes[r], mode=1)
+                assert np.array_equal(gm[r], want) and int(ge[r]) == int(want_eos), (rg.seed, step, prefixes[r])
+        n_done += 1
 
 
 def test_inplace_rejects_rows_outside_their_region(G):
