@@ -4,6 +4,8 @@ the C ABI.  Every mask is compared bit for bit with the cold mask of the same
 rows (cache-on equals cache-off), and with the oracle where it says so; hits
 are confirmed by the cache's state words (a hit publishes nothing new).
 
+* T1 and T2 with genN on random LALR(1) grammars with their own
+  vocabularies: warm equals cold, inserting then hitting.
 * T1: the benchmark's DML batches, missed then hit; configurations that
   differ only below the top of the stack share an entry; decode loops with
   the device advance, warm masks against cold ones and the oracle each step.
@@ -77,6 +79,50 @@ def test_t1_dml_batches_miss_then_hit(G, oracle_mod):
             want, want_eos = o.mask(w, mode=1)
             assert np.array_equal(got[r], want), (bi, r)
             assert int(e[r]) == want_eos
+
+
+@pytest.mark.parametrize("tier", ["t1", "t2_genn"])
+def test_warm_equals_cold_on_random_grammars(G, oracle_mod, tier):
+    """16 random LALR(1) grammars (workloads.randgram, half of them with
+    lexicon categories), each with its own vocabulary and a fresh cache: two
+    batches of sampled prefixes (the second sharing keys with the first where
+    their rows agree on scan state, remainder and allowed set) run warm twice
+    each, first inserting then hitting; every warm mask equals the cold one,
+    and the first batch's masks the oracle's.  With T2 the keys also take
+    the family fingerprint and the genN normal form of the remainder."""
+    from workloads.randgram import RandomGrammar, random_prefixes, random_vocab
+    flags = G.grid.CI_LOOKUP | G.grid.CI_INSERT
+    if tier == "t2_genn":
+        flags |= G.grid.CI_FAMILY | G.grid.CI_GENN
+    n_done = seed = 0
+    while n_done < 16:
+        rg = RandomGrammar(2000 + seed)
+        seed += 1
+        assert seed < 300, "too few random grammars compile"
+        words = sorted({w for ws in (rg.lexicon or {}).values() for w in ws})
+        vocab, specials, eos_id = random_vocab(rg.seed, rg.alphabet(), words=words)
+        try:
+            grid = G.Grid(rg.text(), (), vocab, specials, eos_id)
+        except G.GridError as e:
+            assert "GRID_E_LALR_CONFLICT" in str(e), (rg.seed, str(e))
+            continue
+        slot = grid.add_lexicon(rg.lexicon) if rg.lexicon else 0
+        grid.to_device("cuda")
+        print(f"random grammar seed {rg.seed}: {tier} lexicon={rg.lexicon is not None}", flush=True)
+        cache = grid.new_ci_cache(256)
+        o = oracle_mod.Oracle(rg.text(), (), rg.lexicon, vocab, specials, eos_id)
+        for half in range(2):
+            prefixes = random_prefixes(rg, rg.seed * 2 + half, 16)
+            m, e, _ = _both(G, grid, prefixes, [slot] * len(prefixes), cache, flags)   # inserts
+            n1 = _published(grid, cache)
+            _both(G, grid, prefixes, [slot] * len(prefixes), cache, flags)            # hits
+            assert _published(grid, cache) == n1
+            if half == 0:
+                got = m.view(np.uint32)
+                for r, w in enumerate(prefixes):
+                    want, want_eos = o.mask(w, mode=1)
+                    assert np.array_equal(got[r], want) and int(e[r]) == int(want_eos), (rg.seed, w)
+        n_done += 1
 
 
 def test_t1_entry_shared_by_stacks_that_differ_below_the_top(G):
