@@ -9,7 +9,9 @@
   extension (section 4.1), alias equality (section 2, alias classes),
   special tokens and padding bits;
 * the role projection (section 2, L2): dropped verbs are outside the language;
-* checkpoint mode equals from-scratch mode.
+* checkpoint mode equals from-scratch mode;
+* on random grammars with context-free lexing, viability, membership and the
+  mask equal those of a plain CYK-style check that decides Prefix(L) exactly.
 """
 
 import itertools
@@ -348,3 +350,191 @@ def test_nullable_predicted_late(oracle_mod):
     o = oracle_mod.Oracle(g)
     for s, m in [(b"z", 1), (b"yz", 1), (b"yyz", 1), (b"yyyz", 0), (b"y", 0), (b"zz", 0)]:
         assert o.member(s) == bool(m), s
+
+
+# --------------------------------------------------------------------------
+# A third, plain check on random grammars whose lexing is context-free (no
+# keywords, no lexicon categories: every lexeme belongs to one terminal):
+# maximal munch written out for the generator's token shapes, membership by
+# a CYK-style table over the token string, viability by the same table and a
+# least fixed point for "this suffix is a prefix of what A derives".  It
+# decides Prefix(L) exactly (no completion-length bound), so the oracle's
+# viability, membership and mask (Definitions 2 and 4) are compared on every
+# string up to 4 bytes over a reduced alphabet.
+
+class _CfgBrute:
+    def __init__(self, rg):
+        self.prods = rg.prods
+        self.start = rg.nts[0]
+        self.lit = {v: k for k, v in rg.literal.items()}  # one-byte punctuators
+        self.has_num = "NUM" in rg.regex
+        self.has_id = "ID" in rg.regex
+
+    def lex(self, w):
+        """(emitted terminals, pending lexeme, pending terminal or None, ok):
+        a lexeme is emitted when the next byte cannot extend it; the last one
+        is pending.  Blank runs are the ignored terminal (pending terminal
+        'WS')."""
+        s = w.decode("latin-1")
+        out, i, n = [], 0, len(s)
+        lexemes = []
+        while i < n:
+            c = s[i]
+            if c == " ":
+                j = i
+                while j < n and s[j] == " ":
+                    j += 1
+                lexemes.append((s[i:j], "WS"))
+            elif c.isdigit():
+                j = i
+                while j < n and s[j].isdigit():
+                    j += 1
+                if not self.has_num:
+                    return None
+                lexemes.append((s[i:j], "NUM"))
+            elif "a" <= c <= "z":
+                j = i
+                while j < n and ("a" <= s[j] <= "z" or s[j].isdigit()):
+                    j += 1
+                if not self.has_id:
+                    return None
+                lexemes.append((s[i:j], "ID"))
+            elif c in self.lit:
+                j = i + 1
+                lexemes.append((c, self.lit[c]))
+            else:
+                return None
+            i = j
+        if not lexemes:
+            return out, None
+        for text, t in lexemes[:-1]:
+            if t != "WS":
+                out.append(t)
+        return out, lexemes[-1][1]
+
+    def _tables(self, toks):
+        n = len(toks)
+        D = {}  # (A, i, j) -> A derives toks[i:j]
+
+        def seq(alt, i, j):
+            cur = {i}
+            for X in alt:
+                nxt = set()
+                for p in cur:
+                    if X in self.prods:
+                        nxt.update(q for q in range(p, j + 1) if D.get((X, p, q)))
+                    elif p < j and toks[p] == X:
+                        nxt.add(p + 1)
+                cur = nxt
+                if not cur:
+                    return False
+            return j in cur
+
+        for L in range(n + 1):
+            for i in range(n - L + 1):
+                j = i + L
+                changed = True
+                while changed:
+                    changed = False
+                    for A, alts in self.prods.items():
+                        if not D.get((A, i, j)) and any(seq(alt, i, j) for alt in alts):
+                            D[(A, i, j)] = True
+                            changed = True
+        # P[(A, i)]: toks[i:n] is a prefix of something A derives
+        P = {(A, n): True for A in self.prods}
+        changed = True
+        while changed:
+            changed = False
+            for i in range(n - 1, -1, -1):
+                for A, alts in self.prods.items():
+                    if P.get((A, i)):
+                        continue
+                    ok = False
+                    for alt in alts:
+                        cur = {i}
+                        for X in alt:
+                            for p in cur:  # X takes the rest, or part of it
+                                if X in self.prods:
+                                    if p < n and P.get((X, p)):
+                                        ok = True
+                                elif p == n - 1 and toks[p] == X:
+                                    ok = True
+                            if ok:
+                                break
+                            nxt = set()
+                            for p in cur:
+                                if X in self.prods:
+                                    nxt.update(q for q in range(p, n + 1) if D.get((X, p, q)))
+                                elif p < n and toks[p] == X:
+                                    nxt.add(p + 1)
+                            cur = nxt
+                            if n in cur:
+                                ok = True
+                            if ok or not cur:
+                                break
+                        if ok:
+                            break
+                    if ok:
+                        P[(A, i)] = True
+                        changed = True
+        return D, P
+
+    def _prefix(self, toks):
+        return bool(self._tables(toks)[1].get((self.start, 0)))
+
+    def _member(self, toks):
+        return bool(self._tables(toks)[0].get((self.start, 0, len(toks))))
+
+    def viable(self, w):
+        lx = self.lex(w)
+        if lx is None:
+            return False
+        toks, pend = lx
+        if pend is None or pend == "WS":
+            return self._prefix(toks)
+        return self._prefix(toks + [pend])
+
+    def member(self, w):
+        lx = self.lex(w)
+        if lx is None:
+            return False
+        toks, pend = lx
+        if pend is not None and pend != "WS":
+            toks = toks + [pend]
+        return self._member(toks)
+
+
+def test_oracle_matches_cfg_brute_force_on_random_grammars(oracle_mod):
+    """Twelve random grammars with context-free lexing (any grammar: Earley
+    needs no LALR(1), so ambiguous ones count too): on every string of up to
+    4 bytes over a blank, a letter, a digit and the grammar's punctuators the
+    oracle's viability equals the CYK check's, and membership (the
+    end-of-sequence bit) too; on those up to 3 bytes the whole mask over a
+    small vocabulary equals {t : w.t viable}."""
+    from workloads.randgram import RandomGrammar
+    n_viable = n_checked = 0
+    for seed in range(12):
+        rg = RandomGrammar(500 + seed, lexicon=False, keywords=False)
+        bf = _CfgBrute(rg)
+        alpha = [" ", "a", "1"] + list(rg.literal.values())
+        vocab = [c.encode() for c in alpha] + [b"a1", b"12", b"1a", b"  ", b"a " + alpha[3].encode(),
+                                               (alpha[3] + alpha[-1]).encode(), b""]
+        eos = len(vocab) - 1
+        o = oracle_mod.Oracle(rg.text(), (), None, vocab, [eos], eos)
+        for L in range(5):
+            for combo in itertools.product(alpha, repeat=L):
+                w = "".join(combo).encode()
+                want = bf.viable(w)
+                assert o.viable(w) == want, (rg.seed, w, want)
+                n_checked += 1
+                if not want:
+                    continue
+                n_viable += 1
+                assert o.member(w) == bf.member(w), (rg.seed, w)
+                if L <= 3:
+                    words, e = o.mask(w, mode=0)
+                    bits = np.unpackbits(np.asarray(words, np.uint32).view(np.uint8), bitorder="little")
+                    for t, tok in enumerate(vocab[:-1]):
+                        assert bool(bits[t]) == bf.viable(w + tok), (rg.seed, w, tok)
+                    assert bool(bits[eos]) == bool(e) == bf.member(w), (rg.seed, w)
+    assert 0 < n_viable < n_checked

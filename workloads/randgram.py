@@ -24,14 +24,17 @@ class RandomGrammar:
     terminal string, and N0 reaches every other one.  With lexicon=True (or
     at random when it is None) ID gives way to two lexicon categories CA and
     CB that share its regex, with word lists over a few letters (many words
-    prefixes of others) in self.lexicon."""
+    prefixes of others) in self.lexicon.  keywords=False and lexicon=False
+    give a grammar whose lexemes each belong to one terminal only."""
 
-    def __init__(self, seed, n_nt=None, lexicon=None):
+    def __init__(self, seed, n_nt=None, lexicon=None, keywords=True):
         r = random.Random(seed)
         self.seed = seed
         n = n_nt if n_nt is not None else r.randint(3, 7)
         punct = r.sample(PUNCT, r.randint(3, 7))
         kws = r.sample(KEYWORDS, r.randint(0, 2))
+        if not keywords:
+            kws = []
         self.literal = {}  # terminal name -> its text
         for i, p in enumerate(punct):
             self.literal[f"P{i}"] = p
