@@ -9,7 +9,8 @@
   extension (section 4.1), alias equality (section 2, alias classes),
   special tokens and padding bits;
 * the role projection (section 2, L2): dropped verbs are outside the language;
-* checkpoint mode equals from-scratch mode;
+* checkpoint mode equals from-scratch mode (on the workloads and on random
+  grammars with keywords and lexicon categories);
 * on random grammars with context-free lexing, viability, membership and the
   mask equal those of a plain CYK-style check that decides Prefix(L) exactly.
 """
@@ -538,3 +539,24 @@ def test_oracle_matches_cfg_brute_force_on_random_grammars(oracle_mod):
                         assert bool(bits[t]) == bf.viable(w + tok), (rg.seed, w, tok)
                     assert bool(bits[eos]) == bool(e) == bf.member(w), (rg.seed, w)
     assert 0 < n_viable < n_checked
+
+
+def test_modes_agree_on_random_grammars(oracle_mod):
+    """Checkpoint mode (what the GPU parity tests compare against) equals
+    from-scratch mode on 16 random grammars with keywords and, in about half
+    of them, two lexicon categories sharing the identifier regex: 12 sampled
+    prefixes each, the whole mask over the grammar's own 496-token vocabulary."""
+    from workloads.randgram import RandomGrammar, random_prefixes, random_vocab
+    n_rows = 0
+    for seed in range(16):
+        rg = RandomGrammar(3000 + seed)
+        words = sorted({w for ws in (rg.lexicon or {}).values() for w in ws})
+        vocab, specials, eos_id = random_vocab(rg.seed, rg.alphabet(), words=words)
+        o = oracle_mod.Oracle(rg.text(), (), rg.lexicon, vocab, specials, eos_id)
+        for w in random_prefixes(rg, rg.seed, 12):
+            m0, e0 = o.mask(w, mode=0)
+            m1, e1 = o.mask(w, mode=1)
+            assert np.array_equal(m0, m1) and e0 == e1, (rg.seed, w)
+            assert np.asarray(m1).any() or e1, (rg.seed, w)  # a viable prefix has a continuation
+            n_rows += 1
+    assert n_rows == 16 * 12
