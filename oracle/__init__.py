@@ -69,12 +69,13 @@ class Grammar:
         if not h:
             raise OracleError(err.value.decode())
         self.h = h
+        self._free = lib().oracle_grammar_free  # kept: module globals may be gone at exit
         self.T = lib().oracle_num_terminals(h)
         self.terminals = [lib().oracle_terminal_name(h, i).decode() for i in range(self.T)]
 
     def __del__(self):
         if getattr(self, "h", None):
-            lib().oracle_grammar_free(self.h)
+            self._free(self.h)
             self.h = None
 
 
@@ -89,10 +90,11 @@ class Lexicon:
         if not h:
             raise OracleError(err.value.decode())
         self.h = h
+        self._free = lib().oracle_lexicon_free
 
     def __del__(self):
         if getattr(self, "h", None):
-            lib().oracle_lexicon_free(self.h)
+            self._free(self.h)
             self.h = None
 
 
@@ -105,10 +107,11 @@ class Vocab:
         sp = np.asarray(list(specials) or [0], dtype=np.int32)
         self.h = lib().oracle_vocab_new(data.ctypes.data, offs.ctypes.data, self.V,
                                         sp.ctypes.data, len(specials), eos_id)
+        self._free = lib().oracle_vocab_free
 
     def __del__(self):
         if getattr(self, "h", None):
-            lib().oracle_vocab_free(self.h)
+            self._free(self.h)
             self.h = None
 
 
