@@ -1,5 +1,6 @@
 """Random-grammar campaign on the GPU: N random LALR(1) grammars (seeds from
-START on; one in three with 8..14 nonterminals), each with its own vocabulary
+START on; one in three with 8..14 nonterminals, one in four under a role
+projection that drops one or two labelled alternatives), each with its own vocabulary
 of 2,500 tokens of up to 12 bytes (half of them strings of several lexemes,
 so byte walks emit several terminals) and 8, 32 or 48 sampled prefixes in one
 batch; every mask, end-of-sequence byte and row status is compared with the
@@ -61,6 +62,7 @@ def compare(vocab, rg, gm, ge, gs, o, prefixes, B, what):
             print(rg.text(), rg.lexicon, flush=True)
             return False
     return True
+
 
 
 def decode(G, grid, slot, vocab, eos, rg, o, prefixes, rng, steps=8, cap=512):
@@ -125,10 +127,11 @@ def main(start, n_want, with_decode=False):
         tried += 1
         r = random.Random(seed * 7)
         vocab, eos = vocabulary(rg, r)
+        drop = rg.random_drop(r, r.randint(1, 2)) if seed % 4 == 0 else []
         try:
-            grid = G.Grid(rg.text(), (), vocab, [eos], eos)
+            grid = G.Grid(rg.text(), drop, vocab, [eos], eos)
         except G.GridError as e:
-            assert "GRID_E_LALR_CONFLICT" in str(e), str(e)
+            assert "GRID_E_LALR_CONFLICT" in str(e) or "GRID_E_EMPTY_LANGUAGE" in str(e), str(e)
             continue
         slot = grid.add_lexicon(rg.lexicon) if rg.lexicon else 0
         grid.to_device("cuda")
@@ -136,14 +139,14 @@ def main(start, n_want, with_decode=False):
         rr = random.Random(seed)
         prefixes = []
         while len(prefixes) < B:
-            s = rg.sentence(rr, max_depth=10, max_len=120)
+            s = rg.sentence(rr, max_depth=10, max_len=120, drop=drop)
             prefixes.append(s[:rr.randint(0, len(s))] if rr.random() < 0.9 else s)
         cfgs, pool = grid.configs(prefixes, [slot] * B)
         c, p = grid.configs_to_device(cfgs, pool)
         m, e, st = grid.mask(c, p, B)
         torch.cuda.synchronize()
         gm, ge, gs = m.cpu().numpy().view(np.uint32), e.cpu().numpy(), st.cpu().numpy()
-        o = oracle.Oracle(rg.text(), (), rg.lexicon, vocab, [eos], eos)
+        o = oracle.Oracle(rg.text(), drop, rg.lexicon, vocab, [eos], eos)
         if not compare(vocab, rg, gm, ge, gs, o, prefixes, B, "mask"):
             return 1
         if with_decode and not decode(G, grid, slot, vocab, eos, rg, o, prefixes, np.random.default_rng(seed)):

@@ -357,10 +357,12 @@ def test_random_grammars_match_oracle(G, oracle_mod):
     """48 random grammars (workloads.randgram: chains of one-symbol
     productions, empty productions, recursion, nesting, keywords that the
     identifier regex also matches, and in about half of them two lexicon
-    categories in its place), each with its own vocabulary of 496 tokens (the
-    lexicon words among them) and 16 sampled prefixes in one batch, or 40 for
-    every fourth grammar (two residue row groups): masks, end-of-sequence
-    flags and row status bit-exact against the oracle."""
+    categories in its place, every third under a role projection that drops
+    one or two labelled alternatives), each with its own vocabulary of 496
+    tokens (the lexicon words among them) and 16 sampled prefixes in one
+    batch, or 40 for every fourth grammar (two residue row groups): masks,
+    end-of-sequence flags and row status bit-exact against the oracle."""
+    import random
     from workloads.randgram import RandomGrammar, random_prefixes, random_vocab
     n_done = seed = 0
     while n_done < 48:
@@ -369,22 +371,23 @@ def test_random_grammars_match_oracle(G, oracle_mod):
         assert seed < 600, "too few random grammars compile"
         words = sorted({w for ws in (rg.lexicon or {}).values() for w in ws})
         vocab, specials, eos_id = random_vocab(rg.seed, rg.alphabet(), words=words)
+        drop = rg.random_drop(random.Random(rg.seed), 1 + rg.seed % 2) if n_done % 3 == 2 else []
         try:
-            grid = G.Grid(rg.text(), (), vocab, specials, eos_id)
+            grid = G.Grid(rg.text(), drop, vocab, specials, eos_id)
         except G.GridError as e:
-            assert "GRID_E_LALR_CONFLICT" in str(e), (rg.seed, str(e))
+            assert "GRID_E_LALR_CONFLICT" in str(e) or "GRID_E_EMPTY_LANGUAGE" in str(e), (rg.seed, str(e))
             continue
         slot = grid.add_lexicon(rg.lexicon) if rg.lexicon else 0
-        prefixes = random_prefixes(rg, rg.seed, 40 if n_done % 4 == 3 else 16)
+        prefixes = random_prefixes(rg, rg.seed, 40 if n_done % 4 == 3 else 16, drop=drop)
         log(f"random grammar seed {rg.seed}: T={grid.info()['n_terminals']} V={len(vocab)} B={len(prefixes)} "
-            f"lexicon={rg.lexicon is not None}")
+            f"lexicon={rg.lexicon is not None} drop={drop}")
         grid.to_device("cuda")
         cfgs, pool = grid.configs(prefixes, [slot] * len(prefixes))
         c, p = grid.configs_to_device(cfgs, pool)
         m, e, s = grid.mask(c, p, len(prefixes))
         torch.cuda.synchronize()
         gm, ge, gs = m.cpu().numpy().view(np.uint32), e.cpu().numpy(), s.cpu().numpy()
-        o = oracle_mod.Oracle(rg.text(), (), rg.lexicon, vocab, specials, eos_id)
+        o = oracle_mod.Oracle(rg.text(), drop, rg.lexicon, vocab, specials, eos_id)
         for r, w in enumerate(prefixes):
             ow, oe = o.mask(w, mode=1)
             if not np.array_equal(gm[r], ow) or int(ge[r]) != int(oe):

@@ -830,6 +830,48 @@ def test_host_advance_matches_oracle_on_random_grammars(G, oracle_mod):
     assert 0 < n_yes < n_all
 
 
+def test_host_advance_matches_oracle_on_projected_random_grammars(G, oracle_mod):
+    """Role projections of random grammars (one or two labelled alternatives
+    dropped; the product drops them, reduces the grammar and builds LALR(1)
+    tables, the oracle runs Earley over its own reduction): the host advance
+    accepts exactly the prefixes the oracle finds viable, on sampled prefixes
+    of the projected language and one-byte edits of them."""
+    from workloads.randgram import RandomGrammar, random_prefixes
+    n_grammars = n_yes = n_all = 0
+    seed = 0
+    while n_grammars < 20:
+        rg = RandomGrammar(seed)
+        drop = rg.random_drop(random.Random(seed), 1 + seed % 2)
+        seed += 1
+        try:
+            g = G.Grid(rg.text(), drop, [b"x"])
+        except G.GridError as e:
+            assert "GRID_E_LALR_CONFLICT" in str(e) or "GRID_E_EMPTY_LANGUAGE" in str(e), (rg.seed, str(e))
+            continue
+        slot = g.add_lexicon(rg.lexicon) if rg.lexicon else 0
+        o = oracle_mod.Oracle(rg.text(), drop, rg.lexicon, [b"x"])
+        r = random.Random(rg.seed)
+        strings = random_prefixes(rg, rg.seed, 10, drop=drop)
+        alpha = rg.alphabet()
+        for w in list(strings):
+            b = bytearray(w)
+            b.insert(r.randint(0, len(b)), ord(r.choice(alpha)))
+            strings.append(bytes(b))
+        for s in strings:
+            want = o.viable(s)
+            try:
+                g.config(s, slot)
+                got = True
+            except G.GridError as e:
+                assert "GRID_E_NOT_VIABLE" in str(e)
+                got = False
+            assert got == want, (rg.seed, drop, s)
+            n_yes += got
+            n_all += 1
+        n_grammars += 1
+    assert 0 < n_yes < n_all
+
+
 def _unit_states(action, go, prod):
     """States whose only actions are one reduction by a one-symbol production
     and that have no GOTO: {state: production}."""

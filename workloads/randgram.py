@@ -108,16 +108,31 @@ class RandomGrammar:
                 host = self.nts[r.randrange(i)]
                 self.prods[host].append([r.choice(terms), a])
                 used.add(a)
-        self._height = self._heights()
+        self._heights_of = {}
 
-    def _heights(self):
-        """Least derivation depth of each nonterminal (all finite by construction)."""
+    def label(self, a, k):
+        """The label of nonterminal a's k-th alternative (role projections
+        drop alternatives by label)."""
+        return f"{a}_{k}"
+
+    def labels(self):
+        return [self.label(a, k) for a in self.nts for k in range(len(self.prods[a]))]
+
+    def _alts(self, a, drop):
+        return [alt for k, alt in enumerate(self.prods[a]) if self.label(a, k) not in drop]
+
+    def _heights(self, drop=()):
+        """Least derivation depth of each nonterminal once the alternatives
+        labelled in drop are gone (None: it derives no terminal string)."""
+        key = tuple(sorted(drop))
+        if key in self._heights_of:
+            return self._heights_of[key]
         h = {a: None for a in self.nts}
         changed = True
         while changed:
             changed = False
             for a in self.nts:
-                for alt in self.prods[a]:
+                for alt in self._alts(a, drop):
                     sub = [h[s] for s in alt if s in h]
                     if any(x is None for x in sub):
                         continue
@@ -125,8 +140,12 @@ class RandomGrammar:
                     if h[a] is None or v < h[a]:
                         h[a] = v
                         changed = True
-        assert all(v is not None for v in h.values())
+        self._heights_of[key] = h
         return h
+
+    def random_drop(self, r, n):
+        """n labels to drop, at random."""
+        return r.sample(self.labels(), min(n, len(self.labels())))
 
     def text(self):
         out = [f"# random grammar, seed {self.seed}", "start N0", ""]
@@ -137,7 +156,8 @@ class RandomGrammar:
         out.append("token WS /[ ]+/ ignore")
         out.append("")
         for a in self.nts:
-            alts = [" ".join(alt) if alt else "%empty" for alt in self.prods[a]]
+            alts = [(" ".join(alt) if alt else "%empty") + f" @{self.label(a, k)}"
+                    for k, alt in enumerate(self.prods[a])]
             out.append(f"{a} : {' | '.join(alts)} ;")
         return "\n".join(out) + "\n"
 
@@ -153,17 +173,24 @@ class RandomGrammar:
             if w not in self.literal.values():
                 return w
 
-    def sentence(self, r, max_depth=7, max_len=60):
-        """A random member of the language: a derivation that takes the
+    def sentence(self, r, max_depth=7, max_len=60, drop=()):
+        """A random member of the language (of its projection without the
+        alternatives labelled in drop): a derivation that takes the
         shallowest alternative below the depth limit, lexemes joined by one
         blank (so maximal munch splits them where they were joined)."""
         out = []
+        h = self._heights(drop)
+        assert h[self.nts[0]] is not None, "the projection leaves an empty language"
+
+        def height(alt):
+            sub = [h[s] for s in alt if s in h]
+            return None if any(x is None for x in sub) else 1 + max(sub, default=0)
 
         def expand(a, d):
-            alts = self.prods[a]
+            alts = [alt for alt in self._alts(a, drop) if height(alt) is not None]
             if d >= max_depth or len(out) > max_len:
-                best = min(self._alt_height(alt) for alt in alts)
-                alts = [alt for alt in alts if self._alt_height(alt) == best]
+                best = min(height(alt) for alt in alts)
+                alts = [alt for alt in alts if height(alt) == best]
             for s in r.choice(alts):
                 if s in self.prods:
                     expand(s, d + 1)
@@ -172,9 +199,6 @@ class RandomGrammar:
 
         expand(self.nts[0], 0)
         return " ".join(out).encode()
-
-    def _alt_height(self, alt):
-        return 1 + max((self._height[s] for s in alt if s in self._height), default=0)
 
     def alphabet(self):
         """The bytes the grammar's lexemes and blanks use."""
@@ -214,13 +238,13 @@ def random_vocab(seed, alphabet, n_multi=400, eos=True, words=()):
     return vocab, specials, eos_id
 
 
-def random_prefixes(g, seed, n):
+def random_prefixes(g, seed, n, drop=()):
     """n viable prefixes: random sentences cut at random byte offsets, with
     the empty prefix and whole sentences among them."""
     r = random.Random(seed)
     out = [b""]
     while len(out) < n:
-        s = g.sentence(r)
+        s = g.sentence(r, drop=drop)
         cut = len(s) if r.random() < 0.15 else r.randint(0, len(s))
         out.append(s[:cut])
     return out
